@@ -1,0 +1,201 @@
+"""CPU oracle for DFP INT16 convolution -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, ``__graft_entry__.smoke()`` and ``bench.py``'s CPU-baseline leg
+may import this package.  The product library (``paper_1802_00930_amd``) never
+imports, links or calls it, and it shares no code with the HIP path.
+
+Thin ctypes wrapper around ``dfp_oracle.c`` (plain C, float64/int64 exact
+arithmetic, one output at a time).  Each function below states the passage of
+Das et al. (ICLR 2018) it follows; the C file lists the readings taken where the
+paper is silent.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "dfp_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+ROUND_NEAREST, ROUND_STOCHASTIC, ROUND_BIASED, ROUND_DOWN = 0, 1, 2, 3
+ROUNDING = {"nearest": 0, "stochastic": 1, "biased": 2, "down": 3}
+ROLE_X, ROLE_W, ROLE_DY, ROLE_Y, ROLE_DX = 0, 1, 2, 3, 4
+FWD, BWD_DATA, BWD_WT = 0, 1, 2
+
+FLAG_NONFINITE = 1
+FLAG_EXP_CLAMPED = 2
+FLAG_SATURATED = 4
+FLAG_ZERO_TENSOR = 8
+FLAG_OUTPUT_INF = 16
+
+
+def build(force: bool = False) -> str:
+    """Compile dfp_oracle.c into liboracle.so (gcc -O2 -fopenmp, no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+                               "-fno-fast-math", "-ffp-contract=off", "-Wall", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class Geom(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32) for name in
+                ("n", "c", "h", "w", "k", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w")]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        L = ctypes.CDLL(build())
+        P = ctypes.c_void_p
+        L.orc_philox4x32_10.argtypes = [P, P, P]
+        L.orc_philox4x32_10.restype = None
+        L.orc_rng_word.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint64]
+        L.orc_rng_word.restype = ctypes.c_uint32
+        L.orc_quantize.argtypes = [P, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_uint64,
+                                   ctypes.c_uint32, P, P]
+        L.orc_quantize.restype = ctypes.c_uint32
+        L.orc_downconvert_i32.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int, ctypes.c_int,
+                                          ctypes.c_uint64, ctypes.c_uint32, P, P]
+        L.orc_downconvert_i32.restype = ctypes.c_uint32
+        L.orc_conv.argtypes = [ctypes.POINTER(Geom), ctypes.c_int, P, P, ctypes.c_int32, ctypes.c_int32,
+                               ctypes.c_int32, P, P]
+        L.orc_conv.restype = ctypes.c_int64
+        L.orc_conv_at.argtypes = [ctypes.POINTER(Geom), ctypes.c_int, P, P, ctypes.c_int32, ctypes.c_int32,
+                                  ctypes.c_int32, P, ctypes.c_int64, P, P]
+        L.orc_conv_at.restype = ctypes.c_int64
+        L.orc_num_chunks.argtypes = [ctypes.POINTER(Geom), ctypes.c_int, ctypes.c_int32]
+        L.orc_num_chunks.restype = ctypes.c_int64
+        L.orc_output_len.argtypes = [ctypes.POINTER(Geom), ctypes.c_int]
+        L.orc_output_len.restype = ctypes.c_int64
+        L.orc_default_seg_chunks.argtypes = [ctypes.c_int32]
+        L.orc_default_seg_chunks.restype = ctypes.c_int32
+        L.orc_output_flags.argtypes = [P, ctypes.c_int64]
+        L.orc_output_flags.restype = ctypes.c_uint32
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def geom(n, c, h, w, k, r, s, stride=1, pad=0, stride_w=None, pad_w=None) -> Geom:
+    return Geom(n, c, h, w, k, r, s, stride, stride if stride_w is None else stride_w,
+                pad, pad if pad_w is None else pad_w)
+
+
+def out_hw(g: Geom):
+    return ((g.h + 2 * g.pad_h - g.r) // g.stride_h + 1, (g.w + 2 * g.pad_w - g.s) // g.stride_w + 1)
+
+
+# --------------------------------------------------------------------------
+# Philox4x32-10 (Salmon et al., SC'11): the counter-based generator that draws
+# the uniforms for stochastic rounding (the paper names the rounding mode,
+# Sec. 1, but no generator).
+# --------------------------------------------------------------------------
+def philox4x32_10(ctr, key):
+    c = np.asarray(ctr, dtype=np.uint32).copy()
+    k = np.asarray(key, dtype=np.uint32).copy()
+    out = np.zeros(4, dtype=np.uint32)
+    lib().orc_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def rng_word(seed: int, role: int, idx: int) -> int:
+    return int(lib().orc_rng_word(seed, role, idx))
+
+
+# --------------------------------------------------------------------------
+# Quantisation FP32 -> DFP-P: shared exponent from the max magnitude (Eq. 1-2),
+# integers such that f ~ i * 2^Es (Eq. 3), rounded with the requested mode
+# (Sec. 1).  Also used for the down-conversion of a conv output (Sec. 4.1).
+# --------------------------------------------------------------------------
+def quantize(f: np.ndarray, bits: int = 15, rounding: int = ROUND_NEAREST, seed: int = 0,
+             role: int = ROLE_X):
+    f = np.ascontiguousarray(f, dtype=np.float32)
+    out = np.empty(f.shape, dtype=np.int16)
+    es = np.zeros(1, dtype=np.int32)
+    flags = lib().orc_quantize(_ptr(f), f.size, bits, rounding, seed, role, _ptr(out), _ptr(es))
+    return out, int(es[0]), int(flags)
+
+
+def downconvert_i32(i32: np.ndarray, e_in: int, bits: int = 15, rounding: int = ROUND_NEAREST,
+                    seed: int = 0, role: int = ROLE_Y):
+    """Eq. 6 (integer DFP-32 -> DFP-P), with the shift count placing the max at
+    bit P-2 as Eq. 2 does."""
+    src = np.ascontiguousarray(i32, dtype=np.int32)
+    out = np.empty(src.shape, dtype=np.int16)
+    es = np.zeros(1, dtype=np.int32)
+    flags = lib().orc_downconvert_i32(_ptr(src), src.size, e_in, bits, rounding, seed, role,
+                                      _ptr(out), _ptr(es))
+    return out, int(es[0]), int(flags)
+
+
+# --------------------------------------------------------------------------
+# Convolutions (Alg. 2 and Sec. 4.3): INT32 partials over chunks of L products,
+# FP32 sum in chunk order, one scale 2^(Ea+Eb) (Eq. 4).
+# --------------------------------------------------------------------------
+def num_chunks(g: Geom, direction: int, L: int) -> int:
+    return int(lib().orc_num_chunks(ctypes.byref(g), direction, L))
+
+
+def default_seg_chunks(L: int) -> int:
+    return int(lib().orc_default_seg_chunks(L))
+
+
+def _out_shape(g: Geom, direction: int):
+    P, Q = out_hw(g)
+    if direction == FWD:
+        return (g.n, g.k, P, Q)
+    if direction == BWD_DATA:
+        return (g.n, g.c, g.h, g.w)
+    return (g.k, g.c, g.r, g.s)
+
+
+def conv(g: Geom, direction: int, a: np.ndarray, b: np.ndarray, e: int, L: int, G: int = 0,
+         want_partials: bool = False):
+    """Returns (out float32, partials int32 [J, outputs] or None, wrapped-partial count).
+
+    fwd: a = x, b = w; bwd-data: a = dy, b = w; bwd-wt: a = x, b = dy; e = Ea + Eb."""
+    a = np.ascontiguousarray(a, dtype=np.int16)
+    b = np.ascontiguousarray(b, dtype=np.int16)
+    shape = _out_shape(g, direction)
+    out = np.empty(shape, dtype=np.float32)
+    parts = None
+    if want_partials:
+        J = num_chunks(g, direction, L)
+        parts = np.empty((J, out.size), dtype=np.int32)
+    ov = lib().orc_conv(ctypes.byref(g), direction, _ptr(a), _ptr(b), e, L, G, _ptr(out),
+                        _ptr(parts) if parts is not None else None)
+    return out, parts, int(ov)
+
+
+def conv_at(g: Geom, direction: int, a: np.ndarray, b: np.ndarray, e: int, L: int, idx, G: int = 0,
+            want_partials: bool = False):
+    """The same as :func:`conv` at the flat output indices ``idx`` only.
+    Returns (values float32 [len], partials int32 [len, J] or None, wrapped count)."""
+    a = np.ascontiguousarray(a, dtype=np.int16)
+    b = np.ascontiguousarray(b, dtype=np.int16)
+    idx = np.ascontiguousarray(idx, dtype=np.int64)
+    out = np.empty(idx.size, dtype=np.float32)
+    parts = None
+    if want_partials:
+        J = num_chunks(g, direction, L)
+        parts = np.empty((idx.size, J), dtype=np.int32)
+    ov = lib().orc_conv_at(ctypes.byref(g), direction, _ptr(a), _ptr(b), e, L, G, _ptr(idx), idx.size,
+                           _ptr(out), _ptr(parts) if parts is not None else None)
+    return out, parts, int(ov)
+
+
+def output_flags(y: np.ndarray) -> int:
+    y = np.ascontiguousarray(y, dtype=np.float32)
+    return int(lib().orc_output_flags(_ptr(y), y.size))
