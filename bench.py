@@ -1,0 +1,230 @@
+#!/usr/bin/env python3
+"""Benchmark of the DFP INT16 convolution hot path on one MI355X.
+
+One step = the whole path over one batch of the ResNet-50 conv2_x 3x3 layer
+(N=32, C=K=64, 56x56, 3x3, stride 1, pad 1; ReLU(N(0,1)) activations,
+He-normal weights, output gradients N(0,1)*1e-3; stochastic rounding, seed 1;
+DFP15; chunk length 64):
+
+    Q(x), Q(w), Q(dy)             quantise FP32 -> DFP16      (Eq. 1-3)
+    fwd, DC(y)                    forward conv, down-convert  (Alg. 2, Sec. 4.3)
+    bwd-data, DC(dx)              backward-data, down-convert
+    bwd-wt                        backward-weights (FP32 dW)
+
+value = algorithmic INT16 operations of the three convolutions
+(3 x 2 x N*K*C*R*S*P*Q) per second of whole-step time, inputs resident in HBM.
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "DFP INT16 conv TOPS (fwd/bwd-data/bwd-wt) and % of integer-path roofline"
+WORKLOAD = "resnet50_conv2x_3x3"
+# MI355X published peaks used for the roofline fraction.
+PEAK_INT8_MFMA_TOPS = 5030.0          # dense int8 MFMA, 256 CU x 2.4 GHz x 8192 ops/clk
+PEAK_INT16_BYTESPLIT_TOPS = PEAK_INT8_MFMA_TOPS / 4  # 4 int8 products per INT16 product
+PEAK_VALU_DOT2_TOPS = 157.3           # 256 CU x 4 SIMD x 16 lanes x 2.4 GHz x 4 ops (dot2)
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--chunk", type=int, default=64)
+    ap.add_argument("--path", type=int, default=0, help="0 auto, 1 MFMA, 2 VALU")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+class Step:
+    """Device buffers and the ABI calls of one step."""
+
+    def __init__(self, layer, x, w, dy, L, rounding, seed, path, dev):
+        import torch
+        from paper_1802_00930_amd import dfp
+        self.dfp = dfp
+        self.torch = torch
+        self.layer = layer
+        self.d = dfp.make_desc(layer.n, layer.c, layer.h, layer.w, layer.k, layer.r, layer.s, layer.stride,
+                               layer.pad, chunk_len=L, rounding=rounding, seed=seed, path=path)
+        self.fx, self.fw, self.fdy = (torch.from_numpy(a).to(dev) for a in (x, w, dy))
+        self.qx = torch.empty_like(self.fx, dtype=torch.int16)
+        self.qw = torch.empty_like(self.fw, dtype=torch.int16)
+        self.qdy = torch.empty_like(self.fdy, dtype=torch.int16)
+        self.y = torch.empty(layer.n, layer.k, layer.p, layer.q, dtype=torch.float32, device=dev)
+        self.dx = torch.empty_like(self.fx)
+        self.dw = torch.empty_like(self.fw)
+        self.qy = torch.empty_like(self.y, dtype=torch.int16)
+        self.qdx = torch.empty_like(self.dx, dtype=torch.int16)
+        self.sx, self.sw, self.sdy, self.sy, self.sdx = (dfp.new_scale(dev) for _ in range(5))
+        self.ws = [dfp.alloc_workspace(self.d, k, dev) for k in range(3)]
+
+    def run(self):
+        dfp, d = self.dfp, self.d
+        dfp.dfp_quantize(d, dfp.ROLE_X, self.fx, self.qx, self.sx)
+        dfp.dfp_quantize(d, dfp.ROLE_W, self.fw, self.qw, self.sw)
+        dfp.dfp_quantize(d, dfp.ROLE_DY, self.fdy, self.qdy, self.sdy)
+        dfp.dfp_conv_fwd(d, self.qx, self.sx, self.qw, self.sw, self.y, self.sy, self.ws[0])
+        dfp.dfp_downconvert(d, dfp.ROLE_Y, self.y, self.qy, self.sy, amax_ready=True)
+        dfp.dfp_conv_bwd_data(d, self.qdy, self.sdy, self.qw, self.sw, self.dx, self.sdx, self.ws[1])
+        dfp.dfp_downconvert(d, dfp.ROLE_DX, self.dx, self.qdx, self.sdx, amax_ready=True)
+        dfp.dfp_conv_bwd_weights(d, self.qx, self.sx, self.qdy, self.sdy, self.dw, self.ws[2])
+
+
+def timed(step, steps, warmup, profile=False):
+    torch = step.torch
+    for _ in range(warmup):
+        step.run()
+    torch.cuda.synchronize()
+    if profile:
+        step.dfp.profile_start(64 * steps + 64)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step.run()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    recs = step.dfp.profile_stop(64 * steps + 64) if profile else []
+    return (t1 - t0) / steps, recs
+
+
+def cpu_baseline(layer, x, w, dy, L, rounding, seed, budget_s):
+    """The CPU oracle on a bounded sample of the same layer: every quantisation
+    in full, then the three convolutions at sampled output elements."""
+    import oracle
+    rnd = oracle.ROUNDING[rounding]
+    t0 = time.perf_counter()
+    ox, ex, _ = oracle.quantize(x, 15, rnd, seed, oracle.ROLE_X)
+    ow, ew, _ = oracle.quantize(w, 15, rnd, seed, oracle.ROLE_W)
+    ody, edy, _ = oracle.quantize(dy, 15, rnd, seed, oracle.ROLE_DY)
+    tq = time.perf_counter() - t0
+    g = oracle.geom(layer.n, layer.c, layer.h, layer.w, layer.k, layer.r, layer.s, layer.stride, layer.pad)
+    rng = np.random.default_rng(0)
+    T = {0: layer.c * layer.r * layer.s, 1: layer.k * layer.r * layer.s, 2: layer.n * layer.p * layer.q}
+    O = {0: layer.n * layer.k * layer.p * layer.q, 1: layer.n * layer.c * layer.h * layer.w,
+         2: layer.k * layer.c * layer.r * layer.s}
+    args = {0: (ox, ow, ex + ew), 1: (ody, ow, edy + ew), 2: (ox, ody, ex + edy)}
+    # calibrate on a small sample, then size each direction to ~budget/3 seconds
+    macs = 0
+    secs = 0.0
+    samples = {}
+    for dirn in (0, 1, 2):
+        m = max(16, 2_000_000 // T[dirn])
+        idx = rng.choice(O[dirn], size=min(m, O[dirn]), replace=False)
+        t0 = time.perf_counter()
+        oracle.conv_at(g, dirn, args[dirn][0], args[dirn][1], args[dirn][2], L, idx)
+        dt = time.perf_counter() - t0
+        per = dt / idx.size
+        m2 = int(min(O[dirn], max(idx.size, (budget_s / 3.0) / max(per, 1e-9))))
+        idx = rng.choice(O[dirn], size=m2, replace=False)
+        t0 = time.perf_counter()
+        oracle.conv_at(g, dirn, args[dirn][0], args[dirn][1], args[dirn][2], L, idx)
+        secs += time.perf_counter() - t0
+        macs += idx.size * T[dirn]
+        samples[dirn] = int(idx.size)
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {
+        "value": round(2.0 * macs / secs / 1e12, 6),
+        "unit": "TOPS",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": "oracle conv at %d fwd / %d bwd-data / %d bwd-wt sampled outputs (%.3g MAC, %.1f s) of the same "
+                  "layer and chunk length; quantisation of x, w, dy in full took %.2f s (not in value)"
+                  % (samples[0], samples[1], samples[2], macs, secs, tq),
+    }
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print("bench.py: this build runs on one GPU only (the path is per-GPU); --gpus %d is not supported"
+              % a.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_1802_00930_amd.workloads import WORKLOADS, layer_inputs
+    from paper_1802_00930_amd import dfp
+    dfp.lib()  # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    wl = WORKLOADS[WORKLOAD]
+    layer, x, w, dy = layer_inputs(wl, 0)
+    rounding, seed = wl.roundings[0], wl.seed
+    ops_per_dir = 2.0 * layer.macs
+
+    step = Step(layer, x, w, dy, a.chunk, rounding, seed, a.path, dev)
+    sec, recs = timed(step, a.steps, a.warmup, profile=True)
+    per_kernel = {}
+    for name, ms in recs:
+        per_kernel.setdefault(name, []).append(ms)
+    kstats = {k: {"launches_per_step": len(v) / a.steps, "avg_ms": float(np.mean(v)),
+                  "total_ms_per_step": float(np.sum(v)) / a.steps} for k, v in per_kernel.items()}
+    conv_kernels = {k: v for k, v in kstats.items() if k.startswith("conv_")}
+    dominant = max(conv_kernels, key=lambda k: conv_kernels[k]["total_ms_per_step"])
+    dk = kstats[dominant]
+    mfma = "mfma" in dominant
+    peak = PEAK_INT16_BYTESPLIT_TOPS if mfma else PEAK_VALU_DOT2_TOPS
+    achieved = ops_per_dir / (dk["avg_ms"] * 1e-3) / 1e12
+    per_dir = {}
+    for k, v in conv_kernels.items():
+        per_dir[k] = {"avg_ms": round(v["avg_ms"], 5),
+                      "tops": round(ops_per_dir / (v["avg_ms"] * 1e-3) / 1e12, 3)}
+
+    sweep = {}
+    if not a.no_sweep:
+        for L in (8, 16, 32, 64):
+            s2 = Step(layer, x, w, dy, L, rounding, seed, a.path, dev)
+            t2, _ = timed(s2, max(3, a.steps // 2), 2)
+            sweep[str(L)] = {"ms_per_step": round(t2 * 1e3, 4), "tops": round(3 * ops_per_dir / t2 / 1e12, 3)}
+            del s2
+
+    out = {
+        "metric": METRIC,
+        "value": round(3 * ops_per_dir / sec / 1e12, 4),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(sec * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int16",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: N=%d C=%d K=%d %dx%d 3x3 s1 p1, DFP15, chunk_len=%d, %s rounding seed %d; step = "
+                        "Q(x)+Q(w)+Q(dy)+fwd+DC(y)+bwd-data+DC(dx)+bwd-wt"
+                        % (WORKLOAD, layer.n, layer.c, layer.k, layer.h, layer.w, a.chunk, rounding, seed),
+            "chunk_len": a.chunk, "bits": 15, "rounding": rounding, "path": a.path,
+        },
+        "roofline": {
+            "bound": "mfma" if mfma else "alu",
+            "kernel": dominant,
+            "achieved": round(achieved, 3),
+            "peak": peak,
+            "unit": "TOP/s (INT16-equivalent ops)" if mfma else "TOP/s (INT16 ops)",
+            "frac": round(achieved / peak, 4),
+            "traffic": None,
+        },
+        "per_direction": per_dir,
+        "kernels": {k: {kk: round(vv, 5) for kk, vv in v.items()} for k, v in kstats.items()},
+        "chunk_sweep": sweep,
+    }
+    if not a.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(layer, x, w, dy, a.chunk, rounding, seed, a.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,208 @@
+/*
+ * dfp.h -- C ABI of libdfp: Dynamic Fixed Point (DFP) INT16 convolution for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: Das et al., "Mixed Precision Training of Convolutional Neural
+ * Networks using Integer Operations", ICLR 2018.
+ *   - A DFP tensor is an integer tensor I with one shared exponent Es; element
+ *     n stands for i_n * 2^Es (Sec. 3, Eq. 3).
+ *   - Es comes from the tensor-wide max magnitude: Es = E(max|f|) - (P - 2)
+ *     with P the integer width (Sec. 3.1, Eq. 1-2); stored as an 8-bit signed
+ *     value (Sec. 3).
+ *   - FP (forward), BP (backward-data) and WU (backward-weights) convolutions
+ *     take two DFP16 tensors and produce FP32 (Sec. 4.1).  Products are
+ *     INT16 x INT16 summed into INT32 over short chains; each chain's INT32
+ *     partial is converted to FP32 and accumulated with the scale 2^(Ea+Eb)
+ *     (Sec. 4.2 Algorithm 2, Sec. 4.3, Eq. 4).
+ *   - FP32 outputs are down-converted to DFP16 using the max of the current
+ *     output and nearest, stochastic or biased rounding (Sec. 1, Sec. 4.1).
+ *
+ * Conventions shared by every entry point
+ *   - Tensor pointers are DEVICE pointers owned by the caller.  Activations and
+ *     gradients are NCHW, filters KCRS, all densely packed.  The library
+ *     allocates no device memory: scratch space is the caller's `workspace`.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Every call only
+ *     enqueues work on that stream and returns; nothing synchronises.
+ *   - Return codes report argument errors detected on the host before any
+ *     HIP call (nothing is enqueued then), or a failed launch (DFP_ERR_HIP).
+ *     Conditions that depend on the data are reported in the device-side
+ *     dfp_scale.flags word, readable after the stream has finished.
+ *   - Outputs are overwritten, never accumulated into.
+ *   - Not re-entrant on one dfp_scale: two calls in flight that write the
+ *     same dfp_scale race.  Otherwise stateless and thread-safe (the optional
+ *     profiler below is process-global).
+ *
+ * Numerics (identical in the CPU oracle used by the tests)
+ *   - E(.) = floor(log2 |.|) (subnormals included).  Es = E(max|f|) - (P-2),
+ *     clamped below at -128 (flag EXP_CLAMPED).  All-zero tensor: Es = 0,
+ *     flag ZERO_TENSOR.  Any NaN/Inf: all integers 0, Es = 0, flag NONFINITE.
+ *   - P = bits in {15, 16}.  15 is the paper's experimental setting (inputs
+ *     shifted by one bit, "DFP15", Sec. 4.3): integers in [-2^14, 2^14], never
+ *     saturating.  P = 16 clamps to [-32767, 32767] (flag SATURATED).
+ *   - Rounding of x = f * 2^-Es: NEAREST = ties to even; BIASED = ties toward
+ *     +inf, floor(x + 1/2); STOCHASTIC = floor(x) + (U < F) with
+ *     F = floor(frac(x) * 2^32) and U a Philox4x32-10 word (Salmon et al.,
+ *     SC'11): key = seed, counter = (q mod 2^32, q div 2^32, role, 0),
+ *     q = idx / 4, U = word idx % 4 of the block, idx = the element's flat
+ *     index; DOWN = floor(x) (the plain right shift of Eq. 6).
+ *   - Reduction order and chunks: chunk j holds the L consecutive reduction
+ *     indices t in [jL, min(T, (j+1)L)) of
+ *        forward         t = (r*S + s)*C + c      (T = C*R*S)
+ *        backward-data   t = (r*S + s)*K + k      (T = K*R*S)
+ *        backward-weight t = (n*P + p)*Q + q      (T = N*P*Q)
+ *     Padding taps and stride holes contribute 0 and keep their slot.
+ *     P_j = sum of the chunk's products modulo 2^32 (two's-complement wrap).
+ *   - FP32: F_j = (float)P_j (round to nearest even).  Forward and
+ *     backward-data add F_0, F_1, ... strictly in order.  Backward-weights
+ *     adds chunks in order inside segments of G = seg_chunks chunks, then adds
+ *     the segment sums in order.  The result is scaled once by 2^(Ea+Eb)
+ *     (single rounding, gradual underflow; +-inf on overflow, flag OUTPUT_INF).
+ */
+#ifndef DFP_H_
+#define DFP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum dfp_status {
+  DFP_OK = 0,
+  DFP_ERR_NULL = 1,      /* a required pointer is NULL                        */
+  DFP_ERR_SHAPE = 2,     /* a dimension < 1, pad < 0, stride < 1, output < 1, or
+                            an element count beyond 2^40                       */
+  DFP_ERR_PARAM = 3,     /* bits, rounding, role, chunk_len, seg_chunks or path */
+  DFP_ERR_ALIGN = 4,     /* FP32 src not 16-byte aligned or INT16 dst not 8-byte */
+  DFP_ERR_WORKSPACE = 5, /* workspace NULL or smaller than dfp_workspace_bytes() */
+  DFP_ERR_HIP = 6        /* a HIP launch or runtime call failed                 */
+} dfp_status;
+
+typedef enum dfp_rounding {
+  DFP_ROUND_NEAREST = 0,
+  DFP_ROUND_STOCHASTIC = 1,
+  DFP_ROUND_BIASED = 2,
+  DFP_ROUND_DOWN = 3
+} dfp_rounding;
+
+/* Role of a tensor: selects its logical shape from the descriptor
+ * (X, DX: N,C,H,W;  W: K,C,R,S;  DY, Y: N,K,P,Q) and is word 2 of the Philox
+ * counter, so the five tensors of a layer draw independent streams. */
+typedef enum dfp_role {
+  DFP_ROLE_X = 0,
+  DFP_ROLE_W = 1,
+  DFP_ROLE_DY = 2,
+  DFP_ROLE_Y = 3,
+  DFP_ROLE_DX = 4
+} dfp_role;
+
+typedef enum dfp_direction { DFP_FWD = 0, DFP_BWD_DATA = 1, DFP_BWD_WT = 2 } dfp_direction;
+
+/* Integer-product path (the measured choice is the default). */
+typedef enum dfp_path {
+  DFP_PATH_AUTO = 0, /* byte-split int8 MFMA                                   */
+  DFP_PATH_MFMA = 1, /* exact INT16 products from int8 MFMA on byte digits      */
+  DFP_PATH_VALU = 2  /* one lane per output, VALU integer multiply-add          */
+} dfp_path;
+
+#define DFP_FLAG_NONFINITE 1u    /* input held NaN or Inf                     */
+#define DFP_FLAG_EXP_CLAMPED 2u  /* Es fell below -128 and was clamped        */
+#define DFP_FLAG_SATURATED 4u    /* P = 16 only: an integer clamped to +-32767 */
+#define DFP_FLAG_ZERO_TENSOR 8u  /* every element was zero                    */
+#define DFP_FLAG_OUTPUT_INF 16u  /* a convolution output overflowed FP32      */
+
+/* Host-side layer descriptor, read only during the call. */
+typedef struct dfp_desc {
+  int32_t n, c, h, w;       /* activations NCHW                                */
+  int32_t k, r, s;          /* filters KCRS                                     */
+  int32_t stride_h, stride_w;
+  int32_t pad_h, pad_w;     /* output P = (H + 2 pad_h - R)/stride_h + 1, same Q */
+  int32_t chunk_len;        /* L >= 1: products per INT32 partial               */
+  int32_t seg_chunks;       /* backward-weights segment size G in chunks;
+                               0 -> max(1, 4096 / L)                            */
+  int32_t bits;             /* P in {15, 16}                                    */
+  int32_t rounding;         /* dfp_rounding, for quantise / down-convert        */
+  int32_t path;             /* dfp_path                                         */
+  uint64_t seed;            /* Philox key for stochastic rounding               */
+} dfp_desc;
+
+/* Device-resident scale of one DFP tensor (16 bytes, caller-allocated). */
+typedef struct dfp_scale {
+  uint32_t amax_bits; /* max over elements of (bit pattern & 0x7fffffff)      */
+  int32_t exp;        /* shared exponent Es (int8 range)                      */
+  uint32_t flags;     /* DFP_FLAG_* bits                                      */
+  uint32_t reserved;
+} dfp_scale;
+
+/* Quantise an FP32 tensor to DFP (Sec. 3.1 Eq. 1-3; the quantisers Q_a, Q_w,
+ * Q_e of Sec. 4.1).  src: FP32 [numel(role)], 16-byte aligned; dst: INT16
+ * [numel(role)], 8-byte aligned; s: receives amax_bits, exp and flags.
+ * Enqueues a max-magnitude reduction followed by the rounding pass. */
+dfp_status dfp_quantize(const dfp_desc* d, int32_t role, const float* src, int16_t* dst,
+                        dfp_scale* s, void* stream);
+
+/* Forward convolution FP (Algorithm 2, Sec. 4.3).  x: INT16 [N,C,H,W] with
+ * scale sx; w: INT16 [K,C,R,S] with scale sw; y: FP32 [N,K,P,Q].
+ * sy (nullable): receives max|y| in amax_bits and OUTPUT_INF, ready for
+ * dfp_downconvert(..., amax_ready = 1).  partials (nullable, for tests):
+ * INT32 [J][N*K*P*Q], every chunk partial P_j.  workspace: device scratch of
+ * at least dfp_workspace_bytes(d, DFP_FWD) bytes, 256-byte aligned. */
+dfp_status dfp_conv_fwd(const dfp_desc* d, const int16_t* x, const dfp_scale* sx, const int16_t* w,
+                        const dfp_scale* sw, float* y, dfp_scale* sy, void* workspace,
+                        size_t ws_bytes, int32_t* partials, void* stream);
+
+/* Backward-data convolution BP (Sec. 4.1, the adjoint of FP):
+ * dx[n,c,h,w] = sum over (r,s,k) of dy[n,k,p,q] * w[k,c,r,s] with
+ * p = (h + pad_h - r)/stride_h, q = (w + pad_w - s)/stride_w when both are
+ * integers in range.  dy: INT16 [N,K,P,Q]; w: INT16 [K,C,R,S];
+ * dx: FP32 [N,C,H,W]; sdx, partials, workspace as for the forward call. */
+dfp_status dfp_conv_bwd_data(const dfp_desc* d, const int16_t* dy, const dfp_scale* sdy,
+                             const int16_t* w, const dfp_scale* sw, float* dx, dfp_scale* sdx,
+                             void* workspace, size_t ws_bytes, int32_t* partials, void* stream);
+
+/* Backward-weights convolution WU (Sec. 4.1; chains longer than a million
+ * products, Sec. 4.3): dw[k,c,r,s] = sum over (n,p,q) of dy[n,k,p,q] *
+ * x[n,c,p*stride_h-pad_h+r, q*stride_w-pad_w+s].  x: INT16 [N,C,H,W];
+ * dy: INT16 [N,K,P,Q]; dw: FP32 [K,C,R,S] (not quantised, Fig. 2 caption).
+ * workspace: at least dfp_workspace_bytes(d, DFP_BWD_WT) bytes. */
+dfp_status dfp_conv_bwd_weights(const dfp_desc* d, const int16_t* x, const dfp_scale* sx,
+                                const int16_t* dy, const dfp_scale* sdy, float* dw, void* workspace,
+                                size_t ws_bytes, int32_t* partials, void* stream);
+
+/* Down-convert an FP32 convolution output to DFP (Sec. 1: scale from the max
+ * of the current output; Sec. 4.1: Q_a after FP, Q_e after BP).  role is
+ * DFP_ROLE_Y or DFP_ROLE_DX (sets the shape and the Philox stream).
+ * amax_ready = 1: s->amax_bits (and flags) were produced by the convolution
+ * that wrote src (its sy / sdx), so the max pass is skipped; 0: recompute. */
+dfp_status dfp_downconvert(const dfp_desc* d, int32_t role, const float* src, int16_t* dst,
+                           dfp_scale* s, int32_t amax_ready, void* stream);
+
+/* Device workspace needed by a convolution direction (bytes, 0 if none);
+ * 0 also for an invalid descriptor. */
+size_t dfp_workspace_bytes(const dfp_desc* d, int32_t direction);
+
+/* Number of chunks J = ceil(T / L) of a direction; -1 for an invalid descriptor. */
+int64_t dfp_num_chunks(const dfp_desc* d, int32_t direction);
+
+/* Output height and width of the forward convolution; DFP_ERR_SHAPE if < 1. */
+dfp_status dfp_output_dims(const dfp_desc* d, int32_t* p, int32_t* q);
+
+/* Static text for a status code. */
+const char* dfp_status_str(int32_t status);
+
+/* ---- optional launch profiler (process-global, for benchmarks) ----------
+ * dfp_profile_start(cap): from now on every kernel the library launches is
+ * bracketed by a pair of HIP events on its stream, up to cap launches.
+ * dfp_profile_stop(ids, ms, cap): waits for the recorded events, writes the
+ * kernel id and duration (ms) of each launch, returns how many were written
+ * and stops recording.  dfp_kernel_name(id): static name of a kernel id. */
+dfp_status dfp_profile_start(int32_t capacity);
+int32_t dfp_profile_stop(int32_t* kernel_ids, float* ms, int32_t capacity);
+const char* dfp_kernel_name(int32_t kernel_id);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DFP_H_ */

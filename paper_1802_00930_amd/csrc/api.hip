@@ -1,0 +1,273 @@
+// C ABI of libdfp: host-side validation and dispatch.  Every argument check
+// runs before the first HIP call, so an invalid call enqueues nothing.
+#include <mutex>
+#include <vector>
+
+#include "dfp_internal.h"
+
+namespace dfp {
+
+// ----------------------------------------------------------------- profiler
+namespace {
+struct ProfRec {
+  int32_t id;
+  hipEvent_t start, stop;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+int32_t g_prof_cap = 0;
+std::vector<ProfRec> g_prof;
+std::vector<hipEvent_t> g_event_pool;
+
+hipEvent_t pooled_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+}  // namespace
+
+int prof_begin(int32_t id, hipStream_t st) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof_on || (int32_t)g_prof.size() >= g_prof_cap) return -1;
+  ProfRec rec{id, pooled_event(), pooled_event()};
+  if (!rec.start || !rec.stop) return -1;
+  hipEventRecord(rec.start, st);
+  g_prof.push_back(rec);
+  return (int)g_prof.size() - 1;
+}
+
+void prof_end(int slot, hipStream_t st) {
+  if (slot < 0) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  hipEventRecord(g_prof[slot].stop, st);
+}
+
+// ------------------------------------------------------------- validation
+namespace {
+
+bool geom_from_desc(const dfp_desc* d, Geom* g) {
+  if (d->n < 1 || d->c < 1 || d->h < 1 || d->w < 1 || d->k < 1 || d->r < 1 || d->s < 1) return false;
+  if (d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0) return false;
+  const int64_t hp = (int64_t)d->h + 2 * (int64_t)d->pad_h - d->r;
+  const int64_t wp = (int64_t)d->w + 2 * (int64_t)d->pad_w - d->s;
+  if (hp < 0 || wp < 0) return false;
+  const int64_t p = hp / d->stride_h + 1, q = wp / d->stride_w + 1;
+  if (p < 1 || q < 1 || p > (1 << 30) || q > (1 << 30)) return false;
+  const int64_t lim = (int64_t)1 << 40;
+  const int64_t xs = (int64_t)d->n * d->c * d->h * d->w;
+  const int64_t ys = (int64_t)d->n * d->k * p * q;
+  const int64_t ws = (int64_t)d->k * d->c * d->r * d->s;
+  if (xs > lim || ys > lim || ws > lim) return false;
+  g->n = d->n; g->c = d->c; g->h = d->h; g->w = d->w;
+  g->k = d->k; g->r = d->r; g->s = d->s;
+  g->sh = d->stride_h; g->sw = d->stride_w; g->ph = d->pad_h; g->pw = d->pad_w;
+  g->p = (int32_t)p; g->q = (int32_t)q;
+  g->L = d->chunk_len;
+  g->G = d->seg_chunks > 0 ? d->seg_chunks : ((4096 / (d->chunk_len > 0 ? d->chunk_len : 1)) > 1 ? 4096 / d->chunk_len : 1);
+  return true;
+}
+
+bool params_ok(const dfp_desc* d) {
+  if (d->bits != 15 && d->bits != 16) return false;
+  if (d->rounding < 0 || d->rounding > 3) return false;
+  if (d->chunk_len < 1 || d->seg_chunks < 0) return false;
+  if (d->path < DFP_PATH_AUTO || d->path > DFP_PATH_VALU) return false;
+  return true;
+}
+
+int64_t role_numel(const Geom& g, int32_t role) {
+  switch (role) {
+    case DFP_ROLE_X:
+    case DFP_ROLE_DX: return (int64_t)g.n * g.c * g.h * g.w;
+    case DFP_ROLE_W: return (int64_t)g.k * g.c * g.r * g.s;
+    case DFP_ROLE_DY:
+    case DFP_ROLE_Y: return (int64_t)g.n * g.k * g.p * g.q;
+    default: return -1;
+  }
+}
+
+int64_t reduction_len(const Geom& g, int32_t dir) {
+  if (dir == DFP_FWD) return (int64_t)g.c * g.r * g.s;
+  if (dir == DFP_BWD_DATA) return (int64_t)g.k * g.r * g.s;
+  return (int64_t)g.n * g.p * g.q;
+}
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Common checks for the three convolutions.
+dfp_status conv_checks(const dfp_desc* d, Geom* g, const void* a, const void* sa, const void* b,
+                       const void* sb, const void* out) {
+  if (!d || !a || !sa || !b || !sb || !out) return DFP_ERR_NULL;
+  if (!params_ok(d)) return DFP_ERR_PARAM;
+  if (!geom_from_desc(d, g)) return DFP_ERR_SHAPE;
+  return DFP_OK;
+}
+
+size_t workspace_bytes(const Geom& g, int32_t dir) {
+  (void)g;
+  (void)dir;
+  return 0;
+}
+
+dfp_status ws_check(const Geom& g, int32_t dir, const void* ws, size_t ws_bytes) {
+  const size_t need = workspace_bytes(g, dir);
+  if (need == 0) return DFP_OK;
+  if (!ws || ws_bytes < need || !aligned(ws, 256)) return DFP_ERR_WORKSPACE;
+  return DFP_OK;
+}
+
+}  // namespace
+}  // namespace dfp
+
+using namespace dfp;
+
+extern "C" {
+
+const char* dfp_status_str(int32_t status) {
+  switch (status) {
+    case DFP_OK: return "ok";
+    case DFP_ERR_NULL: return "null pointer";
+    case DFP_ERR_SHAPE: return "invalid shape";
+    case DFP_ERR_PARAM: return "invalid parameter";
+    case DFP_ERR_ALIGN: return "misaligned pointer";
+    case DFP_ERR_WORKSPACE: return "workspace missing or too small";
+    case DFP_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+dfp_status dfp_output_dims(const dfp_desc* d, int32_t* p, int32_t* q) {
+  if (!d || !p || !q) return DFP_ERR_NULL;
+  Geom g;
+  if (!geom_from_desc(d, &g)) return DFP_ERR_SHAPE;
+  *p = g.p;
+  *q = g.q;
+  return DFP_OK;
+}
+
+int64_t dfp_num_chunks(const dfp_desc* d, int32_t direction) {
+  Geom g;
+  if (!d || d->chunk_len < 1 || direction < 0 || direction > 2 || !geom_from_desc(d, &g)) return -1;
+  const int64_t T = reduction_len(g, direction);
+  return (T + d->chunk_len - 1) / d->chunk_len;
+}
+
+size_t dfp_workspace_bytes(const dfp_desc* d, int32_t direction) {
+  Geom g;
+  if (!d || !params_ok(d) || direction < 0 || direction > 2 || !geom_from_desc(d, &g)) return 0;
+  return workspace_bytes(g, direction);
+}
+
+dfp_status dfp_quantize(const dfp_desc* d, int32_t role, const float* src, int16_t* dst, dfp_scale* s,
+                        void* stream) {
+  if (!d || !src || !dst || !s) return DFP_ERR_NULL;
+  if (!params_ok(d) || role < DFP_ROLE_X || role > DFP_ROLE_DX) return DFP_ERR_PARAM;
+  Geom g;
+  if (!geom_from_desc(d, &g)) return DFP_ERR_SHAPE;
+  if (!aligned(src, 16) || !aligned(dst, 8) || !aligned(s, 16)) return DFP_ERR_ALIGN;
+  const int64_t n = role_numel(g, role);
+  hipStream_t st = (hipStream_t)stream;
+  dfp_status rc;
+  if ((rc = launch_scale_reset(s, st)) != DFP_OK) return rc;
+  if ((rc = launch_amax(src, n, s, st)) != DFP_OK) return rc;
+  return launch_quant_convert(src, dst, n, s, d->bits, d->rounding, d->seed, (uint32_t)role, st);
+}
+
+dfp_status dfp_downconvert(const dfp_desc* d, int32_t role, const float* src, int16_t* dst, dfp_scale* s,
+                           int32_t amax_ready, void* stream) {
+  if (!d || !src || !dst || !s) return DFP_ERR_NULL;
+  if (!params_ok(d) || (role != DFP_ROLE_Y && role != DFP_ROLE_DX) || (amax_ready != 0 && amax_ready != 1))
+    return DFP_ERR_PARAM;
+  Geom g;
+  if (!geom_from_desc(d, &g)) return DFP_ERR_SHAPE;
+  if (!aligned(src, 16) || !aligned(dst, 8) || !aligned(s, 16)) return DFP_ERR_ALIGN;
+  const int64_t n = role_numel(g, role);
+  hipStream_t st = (hipStream_t)stream;
+  dfp_status rc;
+  if (!amax_ready) {
+    if ((rc = launch_scale_reset(s, st)) != DFP_OK) return rc;
+    if ((rc = launch_amax(src, n, s, st)) != DFP_OK) return rc;
+  }
+  return launch_quant_convert(src, dst, n, s, d->bits, d->rounding, d->seed, (uint32_t)role, st);
+}
+
+static dfp_status conv_common(int32_t dir, const dfp_desc* d, const int16_t* a, const dfp_scale* sa,
+                              const int16_t* b, const dfp_scale* sb, float* out, dfp_scale* so, void* ws,
+                              size_t ws_bytes, int32_t* partials, void* stream) {
+  Geom g;
+  dfp_status rc = conv_checks(d, &g, a, sa, b, sb, out);
+  if (rc != DFP_OK) return rc;
+  if ((rc = ws_check(g, dir, ws, ws_bytes)) != DFP_OK) return rc;
+  if (so && !aligned(so, 16)) return DFP_ERR_ALIGN;
+  hipStream_t st = (hipStream_t)stream;
+  if (so && (rc = launch_scale_reset(so, st)) != DFP_OK) return rc;
+  return launch_conv_valu(dir, g, a, sa, b, sb, out, so, partials, st);
+}
+
+dfp_status dfp_conv_fwd(const dfp_desc* d, const int16_t* x, const dfp_scale* sx, const int16_t* w,
+                        const dfp_scale* sw, float* y, dfp_scale* sy, void* workspace, size_t ws_bytes,
+                        int32_t* partials, void* stream) {
+  return conv_common(DFP_FWD, d, x, sx, w, sw, y, sy, workspace, ws_bytes, partials, stream);
+}
+
+dfp_status dfp_conv_bwd_data(const dfp_desc* d, const int16_t* dy, const dfp_scale* sdy, const int16_t* w,
+                             const dfp_scale* sw, float* dx, dfp_scale* sdx, void* workspace, size_t ws_bytes,
+                             int32_t* partials, void* stream) {
+  return conv_common(DFP_BWD_DATA, d, dy, sdy, w, sw, dx, sdx, workspace, ws_bytes, partials, stream);
+}
+
+dfp_status dfp_conv_bwd_weights(const dfp_desc* d, const int16_t* x, const dfp_scale* sx, const int16_t* dy,
+                                const dfp_scale* sdy, float* dw, void* workspace, size_t ws_bytes,
+                                int32_t* partials, void* stream) {
+  return conv_common(DFP_BWD_WT, d, x, sx, dy, sdy, dw, nullptr, workspace, ws_bytes, partials, stream);
+}
+
+dfp_status dfp_profile_start(int32_t capacity) {
+  if (capacity < 0) return DFP_ERR_PARAM;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto& r : g_prof) {
+    g_event_pool.push_back(r.start);
+    g_event_pool.push_back(r.stop);
+  }
+  g_prof.clear();
+  g_prof.reserve(capacity);
+  g_prof_cap = capacity;
+  g_prof_on = true;
+  return DFP_OK;
+}
+
+int32_t dfp_profile_stop(int32_t* kernel_ids, float* ms, int32_t capacity) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_on = false;
+  int32_t n = 0;
+  for (auto& r : g_prof) {
+    if (n < capacity && kernel_ids && ms) {
+      float t = -1.f;
+      if (hipEventSynchronize(r.stop) == hipSuccess && hipEventElapsedTime(&t, r.start, r.stop) == hipSuccess) {
+        kernel_ids[n] = r.id;
+        ms[n] = t;
+        ++n;
+      }
+    }
+    g_event_pool.push_back(r.start);
+    g_event_pool.push_back(r.stop);
+  }
+  g_prof.clear();
+  return n;
+}
+
+const char* dfp_kernel_name(int32_t id) {
+  static const char* names[K_NUM_KERNELS] = {
+      "scale_reset", "amax", "quant_convert", "conv_fwd_valu", "conv_bwd_data_valu", "conv_bwd_wt_valu",
+      "weight_prep", "conv_fwd_mfma", "conv_bwd_data_mfma", "conv_bwd_wt_mfma", "bwd_wt_segment_reduce",
+      "act_prep"};
+  if (id < 0 || id >= K_NUM_KERNELS) return "unknown";
+  return names[id];
+}
+
+}  // extern "C"

@@ -1,0 +1,64 @@
+// Internal declarations shared by the libdfp translation units (host + device).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/dfp.h"
+
+namespace dfp {
+
+// Kernel ids reported by the launch profiler (dfp_profile_*).
+enum KernelId : int32_t {
+  K_SCALE_RESET = 0,
+  K_AMAX = 1,
+  K_QUANT = 2,
+  K_FWD_VALU = 3,
+  K_BWDD_VALU = 4,
+  K_BWDW_VALU = 5,
+  K_WPREP = 6,
+  K_FWD_MFMA = 7,
+  K_BWDD_MFMA = 8,
+  K_BWDW_MFMA = 9,
+  K_BWDW_REDUCE = 10,
+  K_XPREP = 11,
+  K_NUM_KERNELS = 12
+};
+
+// Convolution geometry handed to kernels by value.
+struct Geom {
+  int32_t n, c, h, w;   // activations NCHW
+  int32_t k, r, s;      // filters KCRS
+  int32_t sh, sw, ph, pw;
+  int32_t p, q;         // forward output height / width
+  int32_t L;            // chunk length (products per INT32 partial)
+  int32_t G;            // backward-weights segment size in chunks
+};
+
+// Profiler hooks (api.hip). prof_begin returns a record slot or -1.
+int prof_begin(int32_t id, hipStream_t st);
+void prof_end(int slot, hipStream_t st);
+
+// Launch with profiling and error capture; used inside functions returning dfp_status.
+#define DFP_LAUNCH(ID, KERNEL, GRID, BLOCK, SHMEM, STREAM, ...)                 \
+  do {                                                                          \
+    int _slot = ::dfp::prof_begin((ID), (STREAM));                              \
+    hipLaunchKernelGGL(KERNEL, (GRID), (BLOCK), (SHMEM), (STREAM), __VA_ARGS__); \
+    hipError_t _err = hipGetLastError();                                        \
+    ::dfp::prof_end(_slot, (STREAM));                                           \
+    if (_err != hipSuccess) return DFP_ERR_HIP;                                 \
+  } while (0)
+
+// ---- launchers (one per translation unit) ----
+// quantize.hip
+dfp_status launch_scale_reset(dfp_scale* s, hipStream_t st);
+dfp_status launch_amax(const float* src, int64_t n, dfp_scale* s, hipStream_t st);
+dfp_status launch_quant_convert(const float* src, int16_t* dst, int64_t n, dfp_scale* s, int32_t bits,
+                                int32_t rounding, uint64_t seed, uint32_t role, hipStream_t st);
+
+// conv_valu.hip: one lane per output, VALU integer multiply-add.
+dfp_status launch_conv_valu(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa,
+                            const int16_t* b, const dfp_scale* sb, float* out, dfp_scale* so,
+                            int32_t* partials, hipStream_t st);
+
+}  // namespace dfp

@@ -1,0 +1,100 @@
+"""Shared plumbing for the GPU parity tests: run the HIP path through the C ABI
+and the CPU oracle on identical inputs, and compare element by element."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+from paper_1802_00930_amd import dfp
+
+DEV = torch.device("cuda:0") if torch.cuda.is_available() else None
+
+# FP32 outputs: |gpu - oracle| <= REL_TOL * |oracle| per element (oracle 0 -> gpu 0).
+# Both sides add the same FP32 values in the same order, so 0 ulp is expected;
+# the bound is the stated acceptance threshold.
+REL_TOL = 1e-6
+
+
+def note(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def assert_fp32_close(got: np.ndarray, ref: np.ndarray, what: str):
+    got = got.reshape(-1).astype(np.float64)
+    ref = ref.reshape(-1).astype(np.float64)
+    assert got.shape == ref.shape, what
+    same_inf = np.isinf(ref) & (got == ref)
+    err = np.where(same_inf, 0.0, np.abs(got - ref))
+    lim = REL_TOL * np.abs(ref)
+    bad = np.nonzero(err > lim)[0]
+    assert bad.size == 0, "%s: %d elements off, first %s gpu=%r ref=%r" % (
+        what, bad.size, bad[:5], got[bad[:5]], ref[bad[:5]])
+
+
+def ulp_diff(got: np.ndarray, ref: np.ndarray) -> int:
+    a = got.reshape(-1).astype(np.float32).view(np.int32).astype(np.int64)
+    b = ref.reshape(-1).astype(np.float32).view(np.int32).astype(np.int64)
+    return int(np.abs(a - b).max()) if a.size else 0
+
+
+class GpuLayer:
+    """The DFP path of one conv layer on the GPU, all calls through libdfp."""
+
+    def __init__(self, n, c, h, w, k, r, s, stride=1, pad=0, L=64, bits=15, rounding="nearest", seed=0,
+                 path=dfp.PATH_AUTO, G=0):
+        self.d = dfp.make_desc(n, c, h, w, k, r, s, stride, pad, chunk_len=L, seg_chunks=G, bits=bits,
+                               rounding=rounding, path=path, seed=seed)
+        self.p, self.q = dfp.output_dims(self.d)
+        self.shape_x = (n, c, h, w)
+        self.shape_w = (k, c, r, s)
+        self.shape_y = (n, k, self.p, self.q)
+
+    def quantize(self, f: np.ndarray, role: int):
+        t = to_dev(f.astype(np.float32))
+        out = torch.empty(t.shape, dtype=torch.int16, device=DEV)
+        sc = dfp.new_scale(DEV)
+        dfp.dfp_quantize(self.d, role, t, out, sc)
+        return out, sc
+
+    def conv(self, direction, a, sa, b, sb, want_scale=True, want_partials=False):
+        if direction == dfp.FWD:
+            shape = self.shape_y
+        elif direction == dfp.BWD_DATA:
+            shape = self.shape_x
+        else:
+            shape = self.shape_w
+        out = torch.empty(shape, dtype=torch.float32, device=DEV)
+        so = dfp.new_scale(DEV) if (want_scale and direction != dfp.BWD_WT) else None
+        ws = dfp.alloc_workspace(self.d, direction, DEV)
+        parts = None
+        if want_partials:
+            J = dfp.num_chunks(self.d, direction)
+            parts = torch.full((J, out.numel()), 0x5a5a5a5a, dtype=torch.int32, device=DEV)
+        if direction == dfp.FWD:
+            dfp.dfp_conv_fwd(self.d, a, sa, b, sb, out, so, ws, parts)
+        elif direction == dfp.BWD_DATA:
+            dfp.dfp_conv_bwd_data(self.d, a, sa, b, sb, out, so, ws, parts)
+        else:
+            dfp.dfp_conv_bwd_weights(self.d, a, sa, b, sb, out, ws, parts)
+        return out, so, parts
+
+    def downconvert(self, y, role, sc=None):
+        out = torch.empty(y.shape, dtype=torch.int16, device=DEV)
+        ready = sc is not None
+        if sc is None:
+            sc = dfp.new_scale(DEV)
+        dfp.dfp_downconvert(self.d, role, y, out, sc, amax_ready=ready)
+        return out, sc
+
+
+def oracle_geom(layer_like):
+    d = layer_like.d
+    return oracle.geom(d.n, d.c, d.h, d.w, d.k, d.r, d.s, d.stride_h, d.pad_h, d.stride_w, d.pad_w)

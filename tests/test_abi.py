@@ -1,0 +1,168 @@
+"""The C ABI contract, checked on the CPU: libdfp.so loads, exports every entry
+point include/dfp.h declares, and rejects invalid arguments on the host before
+any HIP call (no call here reaches a kernel launch)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dfp.h")
+
+
+@pytest.fixture(scope="module")
+def dl():
+    from paper_1802_00930_amd import dfp
+    if not os.path.exists(dfp.LIB_PATH):
+        pytest.skip("libdfp.so not built")
+    return dfp
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dfp_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_five_calls():
+    names = declared_functions()
+    for n in ("dfp_quantize", "dfp_conv_fwd", "dfp_conv_bwd_data", "dfp_conv_bwd_weights", "dfp_downconvert"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(dl):
+    lib = ctypes.CDLL(dl.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_binding_exposes_same_names(dl):
+    import paper_1802_00930_amd.dfp as b
+    for n in ("dfp_quantize", "dfp_conv_fwd", "dfp_conv_bwd_data", "dfp_conv_bwd_weights", "dfp_downconvert"):
+        assert callable(getattr(b, n))
+
+
+def test_desc_layout_matches_header(dl):
+    # 16 int32 fields then a uint64 seed: 72 bytes with natural alignment
+    assert ctypes.sizeof(dl.Desc) == 72
+    assert dl.Desc.seed.offset == 64
+
+
+FAKE = 1 << 20  # never dereferenced: host validation rejects these calls first
+
+
+def _p(v):
+    return ctypes.c_void_p(v)
+
+
+def good_desc(dl, **kw):
+    args = dict(n=2, c=16, h=14, w=14, k=32, r=3, s=3, stride=1, pad=1, chunk_len=16)
+    args.update(kw)
+    return dl.make_desc(**args)
+
+
+def quant(dl, d, role=0, src=FAKE, dst=FAKE, sc=FAKE):
+    return dl.lib().dfp_quantize(ctypes.byref(d) if d is not None else None, role, _p(src), _p(dst), _p(sc), None)
+
+
+def fwd(dl, d, ws=None, wsn=0, x=FAKE):
+    return dl.lib().dfp_conv_fwd(ctypes.byref(d), _p(x), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None,
+                                 _p(ws) if ws else None, wsn, None, None)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("bits", 14, 3), ("bits", 17, 3), ("rounding", 4, 3), ("rounding", -1, 3), ("chunk_len", 0, 3),
+    ("seg_chunks", -1, 3), ("path", 3, 3),
+    ("n", 0, 2), ("c", -1, 2), ("r", 0, 2), ("stride_h", 0, 2), ("pad_w", -1, 2), ("r", 17, 2),
+])
+def test_quantize_rejects(dl, field, value, code):
+    d = good_desc(dl)
+    setattr(d, field, value)
+    assert quant(dl, d) == code
+
+
+def test_quantize_null_and_role(dl):
+    d = good_desc(dl)
+    assert quant(dl, None) == dl.ERR_NULL
+    assert quant(dl, d, src=0) == dl.ERR_NULL
+    assert quant(dl, d, dst=0) == dl.ERR_NULL
+    assert quant(dl, d, sc=0) == dl.ERR_NULL
+    assert quant(dl, d, role=5) == dl.ERR_PARAM
+    assert quant(dl, d, role=-1) == dl.ERR_PARAM
+
+
+def test_quantize_alignment(dl):
+    d = good_desc(dl)
+    assert quant(dl, d, src=FAKE + 4) == dl.ERR_ALIGN
+    assert quant(dl, d, dst=FAKE + 2) == dl.ERR_ALIGN
+    assert quant(dl, d, sc=FAKE + 8) == dl.ERR_ALIGN
+
+
+def test_downconvert_rejects(dl):
+    d = good_desc(dl)
+    f = dl.lib().dfp_downconvert
+    assert f(ctypes.byref(d), dl.ROLE_X, _p(FAKE), _p(FAKE), _p(FAKE), 1, None) == dl.ERR_PARAM
+    assert f(ctypes.byref(d), dl.ROLE_Y, _p(FAKE), _p(FAKE), _p(FAKE), 2, None) == dl.ERR_PARAM
+    assert f(ctypes.byref(d), dl.ROLE_Y, None, _p(FAKE), _p(FAKE), 1, None) == dl.ERR_NULL
+    assert f(ctypes.byref(d), dl.ROLE_DX, _p(FAKE + 4), _p(FAKE), _p(FAKE), 1, None) == dl.ERR_ALIGN
+
+
+def test_conv_rejects(dl):
+    d = good_desc(dl)
+    assert fwd(dl, d, x=0) == dl.ERR_NULL
+    bad = good_desc(dl, chunk_len=0)
+    assert fwd(dl, bad) == dl.ERR_PARAM
+    bad = good_desc(dl, h=2, pad=0)
+    assert fwd(dl, bad) == dl.ERR_SHAPE
+    lib = dl.lib()
+    # backward-weights with NULL dw
+    assert lib.dfp_conv_bwd_weights(ctypes.byref(d), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None, None, 0,
+                                    None, None) == dl.ERR_NULL
+    assert lib.dfp_conv_bwd_data(ctypes.byref(bad), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None,
+                                 None, 0, None, None) == dl.ERR_SHAPE
+
+
+def test_conv_workspace_checked(dl):
+    for direction in (dl.FWD, dl.BWD_DATA, dl.BWD_WT):
+        d = good_desc(dl, path=dl.PATH_MFMA, chunk_len=64)
+        need = dl.workspace_bytes(d, direction)
+        if need == 0:
+            continue
+        lib = dl.lib()
+        args_small = (_p(FAKE), need - 1)
+        if direction == dl.FWD:
+            rc = lib.dfp_conv_fwd(ctypes.byref(d), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None,
+                                  *args_small, None, None)
+        elif direction == dl.BWD_DATA:
+            rc = lib.dfp_conv_bwd_data(ctypes.byref(d), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None,
+                                       *args_small, None, None)
+        else:
+            rc = lib.dfp_conv_bwd_weights(ctypes.byref(d), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE),
+                                          *args_small, None, None)
+        assert rc == dl.ERR_WORKSPACE
+
+
+def test_host_queries(dl):
+    d = good_desc(dl, chunk_len=16)
+    assert dl.output_dims(d) == (14, 14)
+    assert dl.num_chunks(d, dl.FWD) == 9      # 16*9 = 144 products / 16
+    assert dl.num_chunks(d, dl.BWD_DATA) == 18  # 32*9 = 288 / 16
+    assert dl.num_chunks(d, dl.BWD_WT) == 25  # 2*14*14 = 392 / 16 -> 24.5
+    s = good_desc(dl, h=9, w=8, stride=2, pad=1)
+    assert dl.output_dims(s) == (5, 4)
+    assert dl.num_chunks(good_desc(dl, chunk_len=0), dl.FWD) == -1
+    for code in range(8):
+        assert isinstance(dl.status_str(code), str)
+    assert dl.lib().dfp_kernel_name(0) == b"scale_reset"
+
+
+def test_oracle_not_reachable_from_product():
+    """The product package never imports the oracle."""
+    pkg = os.path.join(ROOT, "paper_1802_00930_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, fn)).read()
+                assert "import oracle" not in text and "from oracle" not in text, fn
+                assert "liboracle" not in text and "dfp_oracle" not in text, fn

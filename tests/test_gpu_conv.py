@@ -1,0 +1,207 @@
+"""GPU parity of the three DFP convolutions and the down-convert against the
+CPU oracle on identical seeded inputs: INT32 chunk partials and INT16 tensors
+bit-exact, exponents equal, FP32 outputs within 1e-6 relative (expected 0 ulp).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import DEV, GpuLayer, assert_fp32_close, note, oracle_geom, to_dev, ulp_diff
+from paper_1802_00930_amd import dfp
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [
+    # n, c, h, w, k, r, s, stride, pad
+    (2, 16, 14, 14, 32, 3, 3, 1, 1),
+    (2, 3, 9, 8, 4, 3, 3, 1, 1),
+    (1, 5, 7, 7, 3, 1, 1, 1, 0),
+    (2, 4, 10, 9, 5, 3, 3, 2, 1),
+    (1, 3, 23, 23, 8, 7, 7, 2, 3),
+    (2, 8, 6, 6, 6, 1, 1, 2, 0),
+    (1, 2, 5, 6, 3, 3, 2, 1, 0),
+    (1, 6, 4, 4, 2, 3, 3, 3, 2),
+    (3, 64, 9, 11, 40, 3, 3, 1, 1),
+    (2, 96, 7, 7, 130, 1, 1, 1, 0),
+    (1, 70, 12, 12, 33, 3, 3, 2, 1),
+]
+
+
+def run_all(shape, L, path=dfp.PATH_AUTO, rounding="nearest", seed=0, G=0, scale=1.0, partials=True, bits=15):
+    n, c, h, w, k, r, s, st, pd = shape
+    gl = GpuLayer(n, c, h, w, k, r, s, st, pd, L=L, bits=bits, rounding=rounding, seed=seed, path=path, G=G)
+    rng = np.random.default_rng(abs(hash((shape, L, seed))) % 2 ** 32)
+    x = (rng.standard_normal(gl.shape_x) * scale).astype(np.float32)
+    wt = (rng.standard_normal(gl.shape_w) * scale).astype(np.float32)
+    dy = (rng.standard_normal(gl.shape_y) * scale).astype(np.float32)
+    rnd = dfp.ROUNDING[rounding]
+    qx, sx = gl.quantize(x, dfp.ROLE_X)
+    qw, sw = gl.quantize(wt, dfp.ROLE_W)
+    qdy, sdy = gl.quantize(dy, dfp.ROLE_DY)
+    ox, ex, _ = oracle.quantize(x, bits, rnd, seed, oracle.ROLE_X)
+    ow, ew, _ = oracle.quantize(wt, bits, rnd, seed, oracle.ROLE_W)
+    ody, edy, _ = oracle.quantize(dy, bits, rnd, seed, oracle.ROLE_DY)
+    torch.cuda.synchronize()
+    assert np.array_equal(qx.cpu().numpy(), ox) and np.array_equal(qw.cpu().numpy(), ow)
+    assert np.array_equal(qdy.cpu().numpy(), ody)
+    g = oracle_geom(gl)
+    Gd = G if G > 0 else oracle.default_seg_chunks(L)
+    res = {}
+    for direction, a, sa, b, sb, oa, ob, e in (
+            (dfp.FWD, qx, sx, qw, sw, ox, ow, ex + ew),
+            (dfp.BWD_DATA, qdy, sdy, qw, sw, ody, ow, edy + ew),
+            (dfp.BWD_WT, qx, sx, qdy, sdy, ox, ody, ex + edy)):
+        note("conv shape=%s L=%d dir=%d path=%d" % (shape, L, direction, path))
+        out, so, parts = gl.conv(direction, a, sa, b, sb, want_partials=partials)
+        ref, rparts, ov = oracle.conv(g, direction, oa, ob, e, L, Gd, want_partials=partials)
+        torch.cuda.synchronize()
+        if partials:
+            gp = parts.cpu().numpy()
+            bad = np.argwhere(gp != rparts)
+            assert bad.size == 0, "partials differ dir=%d at %s" % (direction, bad[:5])
+        got = out.cpu().numpy()
+        assert_fp32_close(got, ref, "dir %d" % direction)
+        assert ulp_diff(got, ref) == 0
+        res[direction] = (gl, out, so, ref)
+    return res
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("L", [1, 5, 8, 16, 64, 10 ** 7])
+def test_small_shapes(shape, L):
+    run_all(shape, L)
+
+
+@pytest.mark.parametrize("path", [dfp.PATH_MFMA, dfp.PATH_VALU])
+@pytest.mark.parametrize("L", [8, 16, 32, 64, 96, 128])
+def test_paths_agree(path, L):
+    for shape in ((2, 64, 10, 10, 64, 3, 3, 1, 1), (2, 128, 7, 7, 96, 1, 1, 1, 0), (1, 32, 9, 9, 64, 3, 3, 2, 1)):
+        run_all(shape, L, path=path)
+
+
+@pytest.mark.parametrize("G", [1, 2, 3, 50])
+def test_bwd_wt_segments(G):
+    run_all((4, 16, 12, 12, 8, 3, 3, 1, 1), 16, G=G)
+
+
+def test_stochastic_chain_and_downconvert():
+    """quantise -> conv -> down-convert, stochastic rounding, both amax routes."""
+    res = run_all((2, 16, 14, 14, 32, 3, 3, 1, 1), 16, rounding="stochastic", seed=9)
+    for direction, role in ((dfp.FWD, dfp.ROLE_Y), (dfp.BWD_DATA, dfp.ROLE_DX)):
+        gl, out, so, ref = res[direction]
+        oq, oe, ofl = oracle.quantize(ref, 15, oracle.ROUND_STOCHASTIC, 9, role)
+        for sc in (so, None):  # epilogue max, then a fresh max pass
+            q, s2 = gl.downconvert(out, role, sc)
+            torch.cuda.synchronize()
+            assert np.array_equal(q.cpu().numpy(), oq)
+            info = dfp.read_scale(s2)
+            assert info["exp"] == oe and info["flags"] == ofl
+            assert info["amax_bits"] == int((ref.view(np.uint32) & 0x7fffffff).max())
+
+
+def test_overflow_wraps_like_oracle():
+    """All operands at +2^14 (DFP15 max): 8 products reach 2^31 and wrap to -2^31."""
+    for L in (7, 8, 9, 64):
+        gl = GpuLayer(1, 64, 4, 4, 8, 3, 3, 1, 1, L=L)
+        v = np.float32(16383.75 / 8192)  # x = 16383.75 rounds to 2^14 (Es = -13)
+        fx = np.full(gl.shape_x, v, np.float32)
+        fw = np.full(gl.shape_w, v, np.float32)
+        qx, sx = gl.quantize(fx, dfp.ROLE_X)
+        qw, sw = gl.quantize(fw, dfp.ROLE_W)
+        ox, ex, _ = oracle.quantize(fx, 15)
+        ow, ew, _ = oracle.quantize(fw, 15)
+        assert int(ox.max()) == 2 ** 14
+        g = oracle_geom(gl)
+        out, _, parts = gl.conv(dfp.FWD, qx, sx, qw, sw, want_partials=True)
+        ref, rparts, ov = oracle.conv(g, oracle.FWD, ox, ow, ex + ew, L, want_partials=True)
+        torch.cuda.synchronize()
+        assert np.array_equal(parts.cpu().numpy(), rparts)
+        assert np.array_equal(out.cpu().numpy(), ref)
+        if L >= 8:
+            assert ov > 0
+
+
+def test_p16_three_products_overflow():
+    gl = GpuLayer(1, 3, 1, 1, 1, 1, 1, L=3, bits=16)
+    v = np.full(gl.shape_x, np.float32(32767.0 / 16384.0))
+    qx, sx = gl.quantize(v, dfp.ROLE_X)
+    qw, sw = gl.quantize(v.reshape(gl.shape_w), dfp.ROLE_W)
+    out, _, parts = gl.conv(dfp.FWD, qx, sx, qw, sw, want_partials=True)
+    torch.cuda.synchronize()
+    assert int(qx.cpu().numpy().reshape(-1)[0]) == 32767
+    assert int(parts.cpu().numpy()[0, 0]) == -1073938429
+
+
+def test_scale_extremes():
+    """Ea + Eb far outside FP32: outputs overflow to inf (OUTPUT_INF) or land in
+    the subnormal range with a single rounding."""
+    for sc_x, sc_w in ((3e38, 3e38), (1e-30, 1e-30), (2e-20, 1e-19)):
+        gl = GpuLayer(1, 8, 5, 5, 4, 3, 3, 1, 1, L=16)
+        rng = np.random.default_rng(3)
+        x = (rng.standard_normal(gl.shape_x) * sc_x).astype(np.float32)
+        w = (rng.standard_normal(gl.shape_w) * sc_w).astype(np.float32)
+        x = np.clip(x, -3e38, 3e38)
+        w = np.clip(w, -3e38, 3e38)
+        qx, sx = gl.quantize(x, dfp.ROLE_X)
+        qw, sw = gl.quantize(w, dfp.ROLE_W)
+        ox, ex, _ = oracle.quantize(x, 15)
+        ow, ew, _ = oracle.quantize(w, 15)
+        out, so, _ = gl.conv(dfp.FWD, qx, sx, qw, sw)
+        ref, _, _ = oracle.conv(oracle_geom(gl), oracle.FWD, ox, ow, ex + ew, 16)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+        flags = dfp.read_scale(so)["flags"]
+        assert bool(flags & dfp.FLAG_OUTPUT_INF) == bool(np.isinf(ref).any())
+
+
+def test_layer16x32_full_chain():
+    """The 2x16x14x14, 16->32 3x3 layer of the workload list (seed 0, nearest,
+    L = 16): every stage bit-exact, both down-converts."""
+    from paper_1802_00930_amd.workloads import WORKLOADS, layer_inputs
+    wl = WORKLOADS["layer16x32"]
+    layer, x, w, dy = layer_inputs(wl, 0)
+    gl = GpuLayer(layer.n, layer.c, layer.h, layer.w, layer.k, layer.r, layer.s, layer.stride, layer.pad, L=16)
+    qx, sx = gl.quantize(x, dfp.ROLE_X)
+    qw, sw = gl.quantize(w, dfp.ROLE_W)
+    qdy, sdy = gl.quantize(dy, dfp.ROLE_DY)
+    ox, ex, _ = oracle.quantize(x, 15, 0, 0, 0)
+    ow, ew, _ = oracle.quantize(w, 15, 0, 0, 1)
+    ody, edy, _ = oracle.quantize(dy, 15, 0, 0, 2)
+    g = oracle_geom(gl)
+    y, sy, py = gl.conv(dfp.FWD, qx, sx, qw, sw, want_partials=True)
+    dx, sdx, pdx = gl.conv(dfp.BWD_DATA, qdy, sdy, qw, sw, want_partials=True)
+    dw, _, pdw = gl.conv(dfp.BWD_WT, qx, sx, qdy, sdy, want_partials=True)
+    qy, sqy = gl.downconvert(y, dfp.ROLE_Y, sy)
+    qdx, sqdx = gl.downconvert(dx, dfp.ROLE_DX, sdx)
+    oy, opy, _ = oracle.conv(g, oracle.FWD, ox, ow, ex + ew, 16, want_partials=True)
+    odx, opdx, _ = oracle.conv(g, oracle.BWD_DATA, ody, ow, edy + ew, 16, want_partials=True)
+    odw, opdw, _ = oracle.conv(g, oracle.BWD_WT, ox, ody, ex + edy, 16, want_partials=True)
+    oqy, eqy, _ = oracle.quantize(oy, 15, 0, 0, 3)
+    oqdx, eqdx, _ = oracle.quantize(odx, 15, 0, 0, 4)
+    torch.cuda.synchronize()
+    assert np.array_equal(qx.cpu().numpy(), ox) and dfp.read_scale(sx)["exp"] == ex
+    assert np.array_equal(qw.cpu().numpy(), ow) and dfp.read_scale(sw)["exp"] == ew
+    assert np.array_equal(qdy.cpu().numpy(), ody) and dfp.read_scale(sdy)["exp"] == edy
+    for got, ref in ((py, opy), (pdx, opdx), (pdw, opdw)):
+        assert np.array_equal(got.cpu().numpy(), ref)
+    for got, ref in ((y, oy), (dx, odx), (dw, odw)):
+        assert np.array_equal(got.cpu().numpy(), ref)
+    assert np.array_equal(qy.cpu().numpy(), oqy) and dfp.read_scale(sqy)["exp"] == eqy
+    assert np.array_equal(qdx.cpu().numpy(), oqdx) and dfp.read_scale(sqdx)["exp"] == eqdx
+
+
+def test_deterministic():
+    shape = (2, 64, 10, 10, 64, 3, 3, 1, 1)
+    gl = GpuLayer(*shape, L=64)
+    rng = np.random.default_rng(1)
+    qx, sx = gl.quantize(rng.standard_normal(gl.shape_x).astype(np.float32), dfp.ROLE_X)
+    qdy, sdy = gl.quantize(rng.standard_normal(gl.shape_y).astype(np.float32), dfp.ROLE_DY)
+    qw, sw = gl.quantize(rng.standard_normal(gl.shape_w).astype(np.float32), dfp.ROLE_W)
+    for direction, a, sa, b, sb in ((dfp.FWD, qx, sx, qw, sw), (dfp.BWD_DATA, qdy, sdy, qw, sw),
+                                    (dfp.BWD_WT, qx, sx, qdy, sdy)):
+        o1, _, _ = gl.conv(direction, a, sa, b, sb)
+        o2, _, _ = gl.conv(direction, a, sa, b, sb)
+        torch.cuda.synchronize()
+        assert torch.equal(o1.view(torch.int32), o2.view(torch.int32))
