@@ -4,6 +4,7 @@
 #include <vector>
 
 #include "dfp_internal.h"
+#include "conv_mfma.h"
 
 namespace dfp {
 
@@ -108,14 +109,21 @@ dfp_status conv_checks(const dfp_desc* d, Geom* g, const void* a, const void* sa
   return DFP_OK;
 }
 
-size_t workspace_bytes(const Geom& g, int32_t dir) {
-  (void)g;
+// The byte-digit split is exact for integers in [-32768, 32639], which holds
+// for every DFP15 tensor; 16-bit tensors (up to +-32767) take the VALU path.
+bool use_mfma(int32_t path, int32_t bits, int32_t dir) {
   (void)dir;
+  return path != DFP_PATH_VALU && bits == 15;
+}
+
+size_t workspace_bytes(const Geom& g, int32_t dir, int32_t path, int32_t bits) {
+  if (!use_mfma(path, bits, dir)) return 0;
+  if (dir == DFP_FWD || dir == DFP_BWD_DATA) return (size_t)plan_conv_mfma(g, dir).bytes;
   return 0;
 }
 
-dfp_status ws_check(const Geom& g, int32_t dir, const void* ws, size_t ws_bytes) {
-  const size_t need = workspace_bytes(g, dir);
+dfp_status ws_check(const Geom& g, int32_t dir, int32_t path, int32_t bits, const void* ws, size_t ws_bytes) {
+  const size_t need = workspace_bytes(g, dir, path, bits);
   if (need == 0) return DFP_OK;
   if (!ws || ws_bytes < need || !aligned(ws, 256)) return DFP_ERR_WORKSPACE;
   return DFP_OK;
@@ -160,7 +168,7 @@ int64_t dfp_num_chunks(const dfp_desc* d, int32_t direction) {
 size_t dfp_workspace_bytes(const dfp_desc* d, int32_t direction) {
   Geom g;
   if (!d || !params_ok(d) || direction < 0 || direction > 2 || !geom_from_desc(d, &g)) return 0;
-  return workspace_bytes(g, direction);
+  return workspace_bytes(g, direction, d->path, d->bits);
 }
 
 dfp_status dfp_quantize(const dfp_desc* d, int32_t role, const float* src, int16_t* dst, dfp_scale* s,
@@ -202,10 +210,12 @@ static dfp_status conv_common(int32_t dir, const dfp_desc* d, const int16_t* a, 
   Geom g;
   dfp_status rc = conv_checks(d, &g, a, sa, b, sb, out);
   if (rc != DFP_OK) return rc;
-  if ((rc = ws_check(g, dir, ws, ws_bytes)) != DFP_OK) return rc;
+  if ((rc = ws_check(g, dir, d->path, d->bits, ws, ws_bytes)) != DFP_OK) return rc;
   if (so && !aligned(so, 16)) return DFP_ERR_ALIGN;
   hipStream_t st = (hipStream_t)stream;
   if (so && (rc = launch_scale_reset(so, st)) != DFP_OK) return rc;
+  if (use_mfma(d->path, d->bits, dir) && dir != DFP_BWD_WT)
+    return launch_conv_mfma(dir, g, a, sa, b, sb, out, so, partials, ws, st);
   return launch_conv_valu(dir, g, a, sa, b, sb, out, so, partials, st);
 }
 

@@ -1,0 +1,34 @@
+// Internal interface of the MFMA convolution kernels.
+#pragma once
+
+#include "dfp_internal.h"
+
+namespace dfp {
+
+// Workspace plan of the forward / backward-data MFMA path.
+struct ConvMfmaPlan {
+  int32_t M, Mp, Cin, T, KB, CG;   // output channels (padded), reduction channels, T, 32-blocks, 16-groups
+  int32_t Hp, Wp, top, left, dil_h, dil_w;  // channels-last digit tensor geometry
+  int32_t Po, Qo;                  // output spatial size
+  int64_t ws_a_bytes, ws_b_bytes, bytes;
+};
+
+struct ConvMfmaArgs {
+  const uint8_t* xs;    // B digits [n][Hp][Wp][CG][32]
+  const uint8_t* wsa;   // A digits [KB][Mp][2][32]
+  const dfp_scale* ea;  // exponent of the B-source tensor
+  const dfp_scale* eb;  // exponent of the filter
+  float* out;
+  dfp_scale* so;
+  int32_t* partials;
+  int64_t NP, O;
+  int32_t M, Mp, Cin, S, T, KB, L, CG, Hp, Wp, Po, Qo;
+  int32_t ustride_h, ustride_w, rsign, roff_h, roff_w;
+};
+
+ConvMfmaPlan plan_conv_mfma(const Geom& g, int32_t dir);
+dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,
+                            const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, void* ws,
+                            hipStream_t st);
+
+}  // namespace dfp

@@ -1,0 +1,460 @@
+// MFMA product path for the forward and backward-data convolutions.
+//
+// Exact INT16 x INT16 products from int8 matrix cores: every INT16 operand a
+// is split into two signed byte digits, lo = a mod 256 read as int8 and
+// hi = (a + 128) >> 8, so a = 256*hi + lo (exact for a in [-32768, 32639];
+// DFP15 integers are within [-2^14, 2^14]).  Then
+//   a*b = 65536*(hi_a*hi_b) + 256*(hi_a*lo_b + lo_a*hi_b) + lo_a*lo_b,
+// and one chunk's INT32 partial is
+//   P_j = (HH << 16) + (X << 8) + LL   (mod 2^32)
+// with HH, X, LL three int32 MFMA accumulators over the chunk's products.
+// Integer MFMA accumulation wraps modulo 2^32, so P_j equals the wrapped
+// INT32 chunk sum bit for bit (Sec. 4.3 overflow semantics).
+//
+// Implicit GEMM: D[m][g] = sum_t A[m][t] * B[t][g], m = output channel,
+// g = output pixel (n, p, q), t = canonical reduction index.
+//   forward        A[k][t] = w[k,c,r,s]          t = (r*S + s)*C + c
+//                  B[t][g] = x[n, c, p*sh - ph + r, q*sw - pw + s]
+//   backward-data  A[c][t] = w[k,c,r,s]          t = (r*S + s)*K + k
+//                  B[t][g] = dy[n, k, (h+ph-r)/sh, (w+pw-s)/sw]
+// Two prep kernels rewrite the operands once per call into the workspace:
+//   - A as digit planes blocked by 32 reduction indices, [kb][m][half][32 B]
+//     (16 hi digits then 16 lo digits), zero-padded past T and past M;
+//   - B as a zero-padded (and, for strided backward-data, zero-dilated)
+//     channels-last digit tensor [n][row][col][cgroup][32 B], so every
+//     (pixel, tap, 16 channels) operand is one aligned 32-byte load and
+//     padding needs no bounds checks.
+// Main kernel: 256 threads = 4 waves; workgroup tile 64 output channels x 128
+// pixels; wave tile 64 x 32 = two v_mfma_i32_32x32x32_i8 tiles.  Per block of
+// 32 reduction indices each lane loads its B column (32 B) and its two A rows
+// (2 x 32 B) and issues HH, LL and the two cross products per tile.  At each
+// chunk end the three accumulators are recombined, converted to FP32 and added
+// to the running FP32 sum in chunk order; chunk lengths that are not a
+// multiple of 32 run the block once per chunk it overlaps, with the bytes of
+// the other chunks masked to zero.
+#include "dfp_internal.h"
+#include "conv_mfma.h"
+
+namespace dfp {
+
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr int kThreads = 256;
+constexpr int kMT = 64;   // output channels per workgroup
+constexpr int kNT = 128;  // output pixels per workgroup
+
+// Byte digits of an INT16 value.
+__device__ __forceinline__ uint32_t hi_digit(int32_t a) { return (uint32_t)((a + 128) >> 8) & 0xffu; }
+__device__ __forceinline__ uint32_t lo_digit(int32_t a) { return (uint32_t)a & 0xffu; }
+
+// ---------------------------------------------------------------- A prep
+// A[m][t] for t = (r*S + s)*Cin + ci.  fwd: m = k, ci = c, value w[m][ci][r][s].
+// bwd-data: m = c, ci = k, value w[ci][m][r][s].
+__global__ __launch_bounds__(256) void k_prep_a(const int16_t* __restrict__ w, uint8_t* __restrict__ ws,
+                                               int32_t M, int32_t Mp, int32_t Cin, int32_t R, int32_t S,
+                                               int32_t T, int32_t KB, int32_t transposed, int32_t Cw) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (kb, m, half)
+  const int64_t total = (int64_t)KB * Mp * 2;
+  if (idx >= total) return;
+  const int32_t half = (int32_t)(idx & 1);
+  const int32_t m = (int32_t)((idx >> 1) % Mp);
+  const int32_t kb = (int32_t)((idx >> 1) / Mp);
+  uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+  if (m < M) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int32_t t = kb * 32 + half * 16 + i;
+      int32_t v = 0;
+      if (t < T) {
+        const int32_t ci = t % Cin, tap = t / Cin;
+        const int32_t r = tap / S, s = tap % S;
+        // forward: w[m][ci][r][s] (Cw = C); backward-data: w[ci][m][r][s] (Cw = C)
+        const int64_t off = transposed ? (((int64_t)ci * Cw + m) * R + r) * S + s
+                                       : (((int64_t)m * Cw + ci) * R + r) * S + s;
+        v = w[off];
+      }
+      hi[i >> 2] |= hi_digit(v) << (8 * (i & 3));
+      lo[i >> 2] |= lo_digit(v) << (8 * (i & 3));
+    }
+  }
+  uint4* dst = reinterpret_cast<uint4*>(ws + idx * 32);
+  dst[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+  dst[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+}
+
+// ---------------------------------------------------------------- B prep
+// Xs[n][u][v][cg][32 B] = digits of src[n][cg*16 + i][(u-top)/dil][(v-left)/dil]
+// when (u-top), (v-left) are non-negative multiples of dil inside the source,
+// else 0.  One thread per (n, u, v, cg); v runs fastest for coalesced reads.
+__global__ __launch_bounds__(256) void k_prep_b(const int16_t* __restrict__ src, uint8_t* __restrict__ xs,
+                                               int32_t N, int32_t Cs, int32_t Hs, int32_t Wsrc, int32_t Hp,
+                                               int32_t Wp, int32_t CG, int32_t top, int32_t left, int32_t dil_h,
+                                               int32_t dil_w) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (int64_t)N * CG * Hp * Wp;
+  if (idx >= total) return;
+  const int32_t v = (int32_t)(idx % Wp);
+  const int32_t u = (int32_t)((idx / Wp) % Hp);
+  const int32_t cg = (int32_t)((idx / ((int64_t)Wp * Hp)) % CG);
+  const int64_t n = idx / ((int64_t)Wp * Hp * CG);
+  const int32_t zu = u - top, zv = v - left;
+  const bool inside =
+      zu >= 0 && zv >= 0 && (zu % dil_h) == 0 && (zv % dil_w) == 0 && zu / dil_h < Hs && zv / dil_w < Wsrc;
+  uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+  if (inside) {
+    const int64_t plane = (int64_t)Hs * Wsrc;
+    const int16_t* p = src + (n * Cs + (int64_t)cg * 16) * plane + (int64_t)(zu / dil_h) * Wsrc + zv / dil_w;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int32_t a = (cg * 16 + i < Cs) ? (int32_t)p[i * plane] : 0;
+      hi[i >> 2] |= hi_digit(a) << (8 * (i & 3));
+      lo[i >> 2] |= lo_digit(a) << (8 * (i & 3));
+    }
+  }
+  uint4* dst = reinterpret_cast<uint4*>(xs + ((((n * Hp + u) * Wp + v) * CG) + cg) * 32);
+  dst[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+  dst[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+}
+
+// Byte mask keeping bytes [lo, hi) of a 16-byte operand (0 <= lo <= hi <= 16).
+__device__ __forceinline__ v4i byte_mask16(int32_t lo, int32_t hi) {
+  const uint32_t bits = ((hi >= 16 ? 0xffffu : ((1u << hi) - 1u)) & ~((1u << lo) - 1u)) & 0xffffu;
+  v4i m;
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const uint32_t b = (bits >> (4 * d)) & 0xfu;
+    m[d] = (int)((((b * 0x00204081u) & 0x01010101u)) * 0xffu);
+  }
+  return m;
+}
+
+struct Acc3 {
+  v16i hh, xx, ll;
+};
+
+// HH, LL and the two cross products of one 32x32 tile.  fresh: the block opens
+// a chunk, so the accumulators start from zero.
+__device__ __forceinline__ void mfma_tile(Acc3& acc, const v4i& ahi, const v4i& alo, const v4i& bhi,
+                                          const v4i& blo, bool fresh) {
+  if (fresh) {
+    const v16i z = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    acc.hh = __builtin_amdgcn_mfma_i32_32x32x32_i8(ahi, bhi, z, 0, 0, 0);
+    acc.ll = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, blo, z, 0, 0, 0);
+    acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(ahi, blo, z, 0, 0, 0);
+  } else {
+    acc.hh = __builtin_amdgcn_mfma_i32_32x32x32_i8(ahi, bhi, acc.hh, 0, 0, 0);
+    acc.ll = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, blo, acc.ll, 0, 0, 0);
+    acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(ahi, blo, acc.xx, 0, 0, 0);
+  }
+  acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, bhi, acc.xx, 0, 0, 0);
+}
+
+// (a << 8) + b as one v_lshl_add_u32 (the compiler otherwise re-associates the
+// recombination into three instructions).
+__device__ __forceinline__ uint32_t shl8_add(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_lshl_add_u32 %0, %1, 8, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// Chunk end: P_j = ((HH << 8) + X) << 8) + LL modulo 2^32, converted to FP32
+// (round to nearest even) and added to the running sum in chunk order.
+template <bool PARTIALS>
+__device__ __forceinline__ void flush_tile(const Acc3& acc, float (&sum)[16], int64_t j, int32_t* partials,
+                                           int64_t O, int64_t obase, int64_t PQ, int32_t mrow0, int32_t M,
+                                           bool gvalid) {
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const uint32_t p = shl8_add(shl8_add((uint32_t)acc.hh[v], (uint32_t)acc.xx[v]), (uint32_t)acc.ll[v]);
+    sum[v] += (float)(int32_t)p;
+    if (PARTIALS) {
+      const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
+      if (gvalid && m < M) partials[j * O + obase + (int64_t)m * PQ] = (int32_t)p;
+    }
+  }
+}
+
+// Operands of one block of 32 reduction indices for one lane.
+struct Operands {
+  v4i bhi, blo;
+  v4i ahi[2], alo[2];
+};
+
+// Forward / backward-data main kernel.  Output pixels g in [0, NP) map to
+// (img, po, qo) of an [Nimg][M][Po][Qo] FP32 output.
+template <bool MASKED, bool PARTIALS, bool CHAN16>
+__global__ __launch_bounds__(kThreads, 2) void k_conv_mfma(ConvMfmaArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int half = lane >> 5;
+  const int col = lane & 31;
+  const int32_t m0 = blockIdx.y * kMT;
+  const int64_t g = (int64_t)blockIdx.x * kNT + wave * 32 + col;
+  const bool gvalid = g < a.NP;
+  const int64_t gg = gvalid ? g : 0;
+  const int32_t qo = (int32_t)(gg % a.Qo);
+  const int32_t po = (int32_t)((gg / a.Qo) % a.Po);
+  const int64_t img = gg / ((int64_t)a.Qo * a.Po);
+  // B byte address of this pixel at tap (0, 0), channel group 0
+  const uint8_t* __restrict__ bpix =
+      a.xs +
+      (((img * a.Hp + (int64_t)po * a.ustride_h + a.roff_h) * a.Wp + (int64_t)qo * a.ustride_w + a.roff_w) * a.CG) *
+          32;
+  const int32_t tap_row_bytes = a.rsign * a.Wp * a.CG * 32;  // one filter row
+  const int32_t tap_col_bytes = a.rsign * a.CG * 32;         // one filter column
+  // A address of this lane's row in tile 0 at block 0; tile 1 is 32 rows (2048 B) further
+  const uint8_t* __restrict__ apix = a.wsa + ((int64_t)(m0 + col) * 2 + half) * 32;
+  const int64_t a_block_bytes = (int64_t)a.Mp * 64;
+  const int64_t PQ = (int64_t)a.Po * a.Qo;
+  const int64_t obase = img * a.M * PQ + (int64_t)po * a.Qo + qo;
+  const int32_t T = a.T, L = a.L, Cin = a.Cin;
+
+  Acc3 acc[2];
+  float sum[2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      acc[i].hh[v] = 0; acc[i].xx[v] = 0; acc[i].ll[v] = 0;
+      sum[i][v] = 0.f;
+    }
+  }
+
+  // Reduction position (uniform) of the first 16 indices of the next block to load.
+  int32_t ld_c = 0, ld_r = 0, ld_s = 0;
+  auto load = [&](int32_t kb, Operands& op) {
+    const int32_t t0 = kb * 32 + half * 16;
+    op.bhi = (v4i){0, 0, 0, 0};
+    op.blo = (v4i){0, 0, 0, 0};
+    if (CHAN16) {
+      // half 0 reads channels [ld_c, ld_c+16) of tap (ld_r, ld_s); half 1 the next 16 indices
+      const int32_t off0 = ld_r * tap_row_bytes + ld_s * tap_col_bytes + (ld_c >> 4) * 32;
+      int32_t off1;
+      if (ld_c + 16 < Cin) {
+        off1 = off0 + 32;
+      } else {
+        const int32_t s1 = (ld_s + 1 == a.S) ? 0 : ld_s + 1;
+        const int32_t r1 = (ld_s + 1 == a.S) ? ld_r + 1 : ld_r;
+        off1 = r1 * tap_row_bytes + s1 * tap_col_bytes;
+      }
+      if (t0 < T) {
+        const uint4* src = reinterpret_cast<const uint4*>(bpix + (half ? off1 : off0));
+        const uint4 h4 = src[0], l4 = src[1];
+        op.bhi = (v4i){(int)h4.x, (int)h4.y, (int)h4.z, (int)h4.w};
+        op.blo = (v4i){(int)l4.x, (int)l4.y, (int)l4.z, (int)l4.w};
+      }
+      ld_c += 32;
+      while (ld_c >= Cin) {
+        ld_c -= Cin;
+        if (++ld_s == a.S) { ld_s = 0; ++ld_r; }
+      }
+    } else {
+      uint32_t hw[4] = {0u, 0u, 0u, 0u}, lw[4] = {0u, 0u, 0u, 0u};
+      for (int i = 0; i < 16; ++i) {
+        const int32_t t = t0 + i;
+        if (t < T) {
+          const int32_t ci = t % Cin, tap = t / Cin;
+          const int32_t r = tap / a.S, s = tap % a.S;
+          const uint8_t* p = bpix + r * tap_row_bytes + s * tap_col_bytes + (ci >> 4) * 32 + (ci & 15);
+          hw[i >> 2] |= (uint32_t)p[0] << (8 * (i & 3));
+          lw[i >> 2] |= (uint32_t)p[16] << (8 * (i & 3));
+        }
+      }
+      op.bhi = (v4i){(int)hw[0], (int)hw[1], (int)hw[2], (int)hw[3]};
+      op.blo = (v4i){(int)lw[0], (int)lw[1], (int)lw[2], (int)lw[3]};
+    }
+    const uint8_t* ap = apix + kb * a_block_bytes;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const uint4* src = reinterpret_cast<const uint4*>(ap + i * 2048);
+      const uint4 h4 = src[0], l4 = src[1];
+      op.ahi[i] = (v4i){(int)h4.x, (int)h4.y, (int)h4.z, (int)h4.w};
+      op.alo[i] = (v4i){(int)l4.x, (int)l4.y, (int)l4.z, (int)l4.w};
+    }
+  };
+
+  int64_t j = 0;           // current chunk
+  int32_t blk_in_chunk = 0;  // unmasked path: blocks of the current chunk seen so far
+  const int32_t chunk_blocks = L / 32;
+  auto compute = [&](int32_t kb, const Operands& op) {
+    if (!MASKED) {
+      const bool fresh = blk_in_chunk == 0;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) mfma_tile(acc[i], op.ahi[i], op.alo[i], op.bhi, op.blo, fresh);
+      ++blk_in_chunk;
+      if (blk_in_chunk == chunk_blocks || kb == a.KB - 1) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          flush_tile<PARTIALS>(acc[i], sum[i], j, a.partials, a.O, obase, PQ, m0 + 32 * i + 4 * half, a.M, gvalid);
+        ++j;
+        blk_in_chunk = 0;
+      }
+    } else {
+      const int32_t t0 = kb * 32 + half * 16;
+      const int32_t t_lo = kb * 32, t_hi = min(kb * 32 + 32, T);
+      while (true) {
+        const int64_t cs = j * (int64_t)L;
+        const int64_t ce = min(cs + L, (int64_t)T);
+        const int32_t seg_lo = (int32_t)max((int64_t)t_lo, cs), seg_hi = (int32_t)min((int64_t)t_hi, ce);
+        const v4i mk = byte_mask16(min(max(seg_lo - t0, 0), 16), min(max(seg_hi - t0, 0), 16));
+        const v4i mhi = op.bhi & mk, mlo = op.blo & mk;
+        const bool fresh = seg_lo == cs;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) mfma_tile(acc[i], op.ahi[i], op.alo[i], mhi, mlo, fresh);
+        if (ce <= t_hi) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            flush_tile<PARTIALS>(acc[i], sum[i], j, a.partials, a.O, obase, PQ, m0 + 32 * i + 4 * half, a.M,
+                                 gvalid);
+          ++j;
+        }
+        if (ce >= t_hi) break;
+      }
+    }
+  };
+
+  // software pipeline: the next block's loads are in flight while this one computes
+  Operands op0, op1;
+  load(0, op0);
+  int32_t kb = 0;
+  for (; kb + 2 <= a.KB; kb += 2) {
+    load(kb + 1, op1);
+    compute(kb, op0);
+    if (kb + 2 < a.KB) load(kb + 2, op0);
+    compute(kb + 1, op1);
+  }
+  if (kb < a.KB) compute(kb, op0);
+
+  // ---- epilogue: scale once, store, max |y|
+  const int32_t e = a.ea->exp + a.eb->exp;
+  uint32_t amax = 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
+      const float y = ldexpf(sum[i][v], e);
+      if (gvalid && m < a.M) {
+        a.out[obase + (int64_t)m * PQ] = y;
+        amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
+      }
+    }
+  }
+  if (a.so) {
+    __shared__ uint32_t red[kThreads / 64];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
+    if (lane == 0) red[wave] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t b = red[0];
+      for (int i = 1; i < kThreads / 64; ++i) b = max(b, red[i]);
+      atomicMax(&a.so->amax_bits, b);
+      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+    }
+  }
+}
+
+inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
+
+}  // namespace
+
+// Workspace layout of the forward / backward-data MFMA path.
+ConvMfmaPlan plan_conv_mfma(const Geom& g, int32_t dir) {
+  ConvMfmaPlan p{};
+  const bool fwd = dir == DFP_FWD;
+  p.M = fwd ? g.k : g.c;
+  p.Cin = fwd ? g.c : g.k;
+  p.T = p.Cin * g.r * g.s;
+  p.KB = (p.T + 31) / 32;
+  p.Mp = (p.M + kMT - 1) / kMT * kMT;
+  p.CG = (p.Cin + 15) / 16;
+  if (fwd) {
+    p.Hp = g.h + 2 * g.ph;
+    p.Wp = g.w + 2 * g.pw;
+    p.top = g.ph; p.left = g.pw; p.dil_h = 1; p.dil_w = 1;
+    p.Po = g.p; p.Qo = g.q;
+  } else {
+    p.Hp = g.h + g.r - 1;
+    p.Wp = g.w + g.s - 1;
+    p.top = g.r - 1 - g.ph;
+    p.left = g.s - 1 - g.pw;
+    p.dil_h = g.sh;
+    p.dil_w = g.sw;
+    p.Po = g.h; p.Qo = g.w;
+  }
+  p.ws_a_bytes = align256((int64_t)p.KB * p.Mp * 2 * 32);
+  p.ws_b_bytes = align256((int64_t)g.n * p.Hp * p.Wp * p.CG * 32);
+  p.bytes = p.ws_a_bytes + p.ws_b_bytes;
+  return p;
+}
+
+dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,
+                            const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, void* ws,
+                            hipStream_t st) {
+  // fwd: a = x (B source), b = w.  bwd-data: a = dy (B source), b = w.
+  const ConvMfmaPlan p = plan_conv_mfma(g, dir);
+  const bool fwd = dir == DFP_FWD;
+  uint8_t* wsa = reinterpret_cast<uint8_t*>(ws);
+  uint8_t* xs = wsa + p.ws_a_bytes;
+  {
+    const int64_t total = (int64_t)p.KB * p.Mp * 2;
+    DFP_LAUNCH(K_WPREP, k_prep_a, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, b, wsa, p.M, p.Mp,
+               p.Cin, g.r, g.s, p.T, p.KB, fwd ? 0 : 1, g.c);
+  }
+  {
+    const int32_t Cs = fwd ? g.c : g.k, Hs = fwd ? g.h : g.p, Wsrc = fwd ? g.w : g.q;
+    const int64_t total = (int64_t)g.n * p.CG * p.Hp * p.Wp;
+    DFP_LAUNCH(K_XPREP, k_prep_b, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, a, xs, g.n, Cs, Hs,
+               Wsrc, p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w);
+  }
+  ConvMfmaArgs args{};
+  args.xs = xs;
+  args.wsa = wsa;
+  args.ea = sa;
+  args.eb = sb;
+  args.out = out;
+  args.so = so;
+  args.partials = partials;
+  args.M = p.M; args.Mp = p.Mp; args.Cin = p.Cin; args.S = g.s; args.T = p.T; args.KB = p.KB; args.L = g.L;
+  args.CG = p.CG; args.Hp = p.Hp; args.Wp = p.Wp; args.Po = p.Po; args.Qo = p.Qo;
+  args.NP = (int64_t)g.n * p.Po * p.Qo;
+  args.O = args.NP * p.M;
+  if (fwd) {
+    args.ustride_h = g.sh;
+    args.ustride_w = g.sw;
+    args.rsign = 1;
+    args.roff_h = 0;
+    args.roff_w = 0;
+  } else {
+    args.ustride_h = 1;
+    args.ustride_w = 1;
+    args.rsign = -1;
+    args.roff_h = g.r - 1;
+    args.roff_w = g.s - 1;
+  }
+  const dim3 grid((unsigned)((args.NP + kNT - 1) / kNT), (unsigned)(p.Mp / kMT));
+  const bool masked = (g.L % 32) != 0;
+  const bool chan16 = (p.Cin % 16) == 0;
+  const int kid = fwd ? K_FWD_MFMA : K_BWDD_MFMA;
+#define DFP_CONV_MFMA_CASE(MK, PT, CH)                                                      \
+  if (masked == MK && (partials != nullptr) == PT && chan16 == CH) {                       \
+    DFP_LAUNCH(kid, (k_conv_mfma<MK, PT, CH>), grid, dim3(kThreads), 0, st, args);          \
+    return DFP_OK;                                                                          \
+  }
+  DFP_CONV_MFMA_CASE(false, false, true)
+  DFP_CONV_MFMA_CASE(false, false, false)
+  DFP_CONV_MFMA_CASE(false, true, true)
+  DFP_CONV_MFMA_CASE(false, true, false)
+  DFP_CONV_MFMA_CASE(true, false, true)
+  DFP_CONV_MFMA_CASE(true, false, false)
+  DFP_CONV_MFMA_CASE(true, true, true)
+  DFP_CONV_MFMA_CASE(true, true, false)
+#undef DFP_CONV_MFMA_CASE
+  return DFP_ERR_PARAM;
+}
+
+}  // namespace dfp
