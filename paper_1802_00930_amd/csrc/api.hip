@@ -5,6 +5,7 @@
 
 #include "dfp_internal.h"
 #include "conv_mfma.h"
+#include "conv_bwdw_mfma.h"
 
 namespace dfp {
 
@@ -111,15 +112,16 @@ dfp_status conv_checks(const dfp_desc* d, Geom* g, const void* a, const void* sa
 
 // The byte-digit split is exact for integers in [-32768, 32639], which holds
 // for every DFP15 tensor; 16-bit tensors (up to +-32767) take the VALU path.
-bool use_mfma(int32_t path, int32_t bits, int32_t dir) {
-  (void)dir;
-  return path != DFP_PATH_VALU && bits == 15;
+bool use_mfma(const Geom& g, int32_t path, int32_t bits, int32_t dir) {
+  if (path == DFP_PATH_VALU || bits != 15) return false;
+  if (dir == DFP_BWD_WT) return bwdw_mfma_supported(g);
+  return true;
 }
 
 size_t workspace_bytes(const Geom& g, int32_t dir, int32_t path, int32_t bits) {
-  if (!use_mfma(path, bits, dir)) return 0;
+  if (!use_mfma(g, path, bits, dir)) return 0;
   if (dir == DFP_FWD || dir == DFP_BWD_DATA) return (size_t)plan_conv_mfma(g, dir).bytes;
-  return 0;
+  return (size_t)plan_bwdw_mfma(g).bytes;
 }
 
 dfp_status ws_check(const Geom& g, int32_t dir, int32_t path, int32_t bits, const void* ws, size_t ws_bytes) {
@@ -214,8 +216,10 @@ static dfp_status conv_common(int32_t dir, const dfp_desc* d, const int16_t* a, 
   if (so && !aligned(so, 16)) return DFP_ERR_ALIGN;
   hipStream_t st = (hipStream_t)stream;
   if (so && (rc = launch_scale_reset(so, st)) != DFP_OK) return rc;
-  if (use_mfma(d->path, d->bits, dir) && dir != DFP_BWD_WT)
+  if (use_mfma(g, d->path, d->bits, dir)) {
+    if (dir == DFP_BWD_WT) return launch_bwdw_mfma(g, a, sa, b, sb, out, partials, ws, st);
     return launch_conv_mfma(dir, g, a, sa, b, sb, out, so, partials, ws, st);
+  }
   return launch_conv_valu(dir, g, a, sa, b, sb, out, so, partials, st);
 }
 

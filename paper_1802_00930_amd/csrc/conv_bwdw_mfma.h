@@ -1,0 +1,35 @@
+// Internal interface of the backward-weights MFMA kernels.
+#pragma once
+
+#include <algorithm>
+
+#include "dfp_internal.h"
+
+namespace dfp {
+
+struct BwdwPlan {
+  int64_t T, KBT;                       // reduction length, blocks of 32
+  int32_t Mp, Hpad, Wpad, nseg;         // padded rows of dy digits, padded x rows / row width, segments
+  int32_t nch_max, rows_max, band_ch_stride;
+  int64_t band_bytes, smem_bytes;       // LDS band (all channels of a column tile) + offset table
+  int64_t ad_bytes, xp_bytes, u_bytes, bytes;
+};
+
+struct BwdwArgs {
+  const uint8_t* ad;      // dy digits [KBT][Mp][2][32]
+  const uint16_t* xp;     // x digit pairs [C][N*Hpad][Wpad]
+  const dfp_scale* ea;    // x scale
+  const dfp_scale* eb;    // dy scale
+  float* out;             // dW [K][C][R][S]
+  float* useg;            // segment sums [nseg][K*C*R*S]
+  int32_t* partials;
+  int64_t T, O;
+  int32_t K, Mp, C, R, S, P, Q, sh, sw, Hpad, Wpad, NH, L, G, nseg, band_bytes, band_ch_stride;
+};
+
+BwdwPlan plan_bwdw_mfma(const Geom& g);
+bool bwdw_mfma_supported(const Geom& g);
+dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx, const int16_t* dy,
+                            const dfp_scale* sdy, float* dw, int32_t* partials, void* ws, hipStream_t st);
+
+}  // namespace dfp

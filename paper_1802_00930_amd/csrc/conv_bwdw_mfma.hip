@@ -1,0 +1,421 @@
+// MFMA product path for the backward-weights convolution (WU, Sec. 4.1):
+//   dW[k][(c,r,s)] = sum over t = (n*P + p)*Q + q of
+//                    dy[n,k,p,q] * x[n, c, p*sh - ph + r, q*sw - pw + s].
+// The reduction runs over every output position of the batch (chains beyond a
+// million products, Sec. 4.3), so it is split into segments of G chunks that
+// run in parallel; each workgroup adds its segment's chunk partials in chunk
+// order (FP32) and a second kernel adds the segment sums in segment order, so
+// the result does not depend on scheduling.
+//
+// Operands (same byte-digit split as the forward path, see conv_mfma.hip):
+//   A = dy digits blocked by 32 reduction indices, [kb][k][half][32 B],
+//       written by a prep kernel in canonical t order;
+//   B = x digits as (lo | hi << 8) 16-bit pairs in a zero-padded,
+//       channel-major layout XP[c][n*Hpad + row][col] (Hpad = H + 2 ph,
+//       row width padded to 8 pairs), also written by a prep kernel.
+// For every block of 128 reduction indices a workgroup copies, for each input
+// channel its 128 columns touch, the contiguous band of padded rows those
+// indices read into LDS, plus a table of each index's row/column offset in
+// that band.  A lane owning column (c, r, s) then gathers its 16 operand pairs
+// as band[c][offset(t) + r*Wpad + s], which covers padding, strides and image
+// boundaries with no branches.
+#include "conv_bwdw_mfma.h"
+
+namespace dfp {
+
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr int kThreads = 256;
+constexpr int kMT = 64;    // output rows (k) per workgroup
+constexpr int kNT = 128;   // output columns (c, r, s) per workgroup
+constexpr int kSBT = 128;  // reduction indices staged per LDS band
+
+__device__ __forceinline__ uint32_t hi_digit(int32_t a) { return (uint32_t)((a + 128) >> 8) & 0xffu; }
+__device__ __forceinline__ uint32_t lo_digit(int32_t a) { return (uint32_t)a & 0xffu; }
+
+// A digits from dy in canonical order: Ad[kb][m][half][16 hi | 16 lo].
+// One thread per (m, kb, half), kb fastest so consecutive threads read
+// consecutive reduction indices of one dy plane.
+__global__ __launch_bounds__(256) void k_prep_dy(const int16_t* __restrict__ dy, uint8_t* __restrict__ ad, int32_t K,
+                                                int32_t Mp, int64_t PQ, int64_t T, int64_t KBT) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = KBT * Mp * 2;
+  if (idx >= total) return;
+  const int32_t half = (int32_t)(idx & 1);
+  const int64_t kb = (idx >> 1) % KBT;
+  const int32_t m = (int32_t)((idx >> 1) / KBT);
+  uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+  if (m < K) {
+    int64_t t = kb * 32 + half * 16;
+    int64_t n = t / PQ, pq = t % PQ;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      int32_t v = 0;
+      if (t < T) v = dy[(n * K + m) * PQ + pq];
+      hi[i >> 2] |= hi_digit(v) << (8 * (i & 3));
+      lo[i >> 2] |= lo_digit(v) << (8 * (i & 3));
+      ++t;
+      if (++pq == PQ) { pq = 0; ++n; }
+    }
+  }
+  uint4* dst = reinterpret_cast<uint4*>(ad + ((kb * Mp + m) * 2 + half) * 32);
+  dst[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+  dst[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+}
+
+// XP[c][n*Hpad + u][v] = (lo | hi << 8) of x[n][c][u - ph][v - pw], zero outside.
+__global__ __launch_bounds__(256) void k_prep_xp(const int16_t* __restrict__ x, uint16_t* __restrict__ xp, int32_t N,
+                                                int32_t C, int32_t H, int32_t W, int32_t Hpad, int32_t Wpad,
+                                                int32_t ph, int32_t pw) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (int64_t)C * N * Hpad * Wpad;
+  if (idx >= total) return;
+  const int32_t v = (int32_t)(idx % Wpad);
+  const int64_t z = (idx / Wpad) % ((int64_t)N * Hpad);
+  const int32_t c = (int32_t)(idx / ((int64_t)Wpad * N * Hpad));
+  const int32_t n = (int32_t)(z / Hpad), u = (int32_t)(z % Hpad);
+  const int32_t ih = u - ph, iw = v - pw;
+  uint32_t pair = 0;
+  if (ih >= 0 && ih < H && iw >= 0 && iw < W) {
+    const int32_t a = x[(((int64_t)n * C + c) * H + ih) * W + iw];
+    pair = lo_digit(a) | (hi_digit(a) << 8);
+  }
+  xp[idx] = (uint16_t)pair;
+}
+
+// Byte mask keeping bytes [lo, hi) of a 16-byte operand.
+__device__ __forceinline__ v4i byte_mask16(int32_t lo, int32_t hi) {
+  const uint32_t bits = ((hi >= 16 ? 0xffffu : ((1u << hi) - 1u)) & ~((1u << lo) - 1u)) & 0xffffu;
+  v4i m;
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const uint32_t b = (bits >> (4 * d)) & 0xfu;
+    m[d] = (int)((((b * 0x00204081u) & 0x01010101u)) * 0xffu);
+  }
+  return m;
+}
+
+struct Acc3 {
+  v16i hh, xx, ll;
+};
+
+__device__ __forceinline__ void mfma_tile(Acc3& acc, const v4i& ahi, const v4i& alo, const v4i& bhi,
+                                          const v4i& blo, bool fresh) {
+  if (fresh) {
+    const v16i z = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    acc.hh = __builtin_amdgcn_mfma_i32_32x32x32_i8(ahi, bhi, z, 0, 0, 0);
+    acc.ll = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, blo, z, 0, 0, 0);
+    acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(ahi, blo, z, 0, 0, 0);
+  } else {
+    acc.hh = __builtin_amdgcn_mfma_i32_32x32x32_i8(ahi, bhi, acc.hh, 0, 0, 0);
+    acc.ll = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, blo, acc.ll, 0, 0, 0);
+    acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(ahi, blo, acc.xx, 0, 0, 0);
+  }
+  acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, bhi, acc.xx, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t shl8_add(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_lshl_add_u32 %0, %1, 8, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// Chunk end: P_j recombined, converted (round to nearest even), added in order.
+template <bool PARTIALS>
+__device__ __forceinline__ void flush_tile(const Acc3& acc, float (&sum)[16], int64_t j, int32_t* partials,
+                                           int64_t O, int64_t col, int64_t CRS, int32_t mrow0, int32_t M,
+                                           bool cvalid) {
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const uint32_t p = shl8_add(shl8_add((uint32_t)acc.hh[v], (uint32_t)acc.xx[v]), (uint32_t)acc.ll[v]);
+    sum[v] += (float)(int32_t)p;
+    if (PARTIALS) {
+      const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
+      if (cvalid && m < M) partials[j * O + (int64_t)m * CRS + col] = (int32_t)p;
+    }
+  }
+}
+
+template <bool MASKED, bool PARTIALS>
+__global__ __launch_bounds__(kThreads, 2) void k_bwdw_mfma(BwdwArgs a) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  uint16_t* band = reinterpret_cast<uint16_t*>(smem);                        // [nch][rows][Wpad]
+  int32_t* toff = reinterpret_cast<int32_t*>(smem + a.band_bytes);           // [kSBT]
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int half = lane >> 5;
+  const int lc = lane & 31;
+  const int32_t RS = a.R * a.S;
+  const int64_t CRS = (int64_t)a.C * RS;
+  const int64_t col0 = (int64_t)blockIdx.x * kNT;
+  const int64_t col = col0 + wave * 32 + lc;
+  const bool cvalid = col < CRS;
+  const int64_t colc = cvalid ? col : col0;
+  const int32_t c = (int32_t)(colc / RS), rr = (int32_t)((colc % RS) / a.S), ss = (int32_t)(colc % a.S);
+  const int32_t c_lo = (int32_t)(col0 / RS);
+  const int32_t c_hi = (int32_t)(min(col0 + kNT - 1, CRS - 1) / RS);
+  const int32_t nch = c_hi - c_lo + 1;
+  const int32_t m0 = blockIdx.y * kMT;
+
+  // reduction range of this segment
+  const int64_t g = blockIdx.z;
+  const int64_t t_seg0 = g * (int64_t)a.G * a.L;
+  const int64_t t_seg1 = min(t_seg0 + (int64_t)a.G * a.L, a.T);
+  int64_t j = g * (int64_t)a.G;  // first chunk of the segment
+
+  Acc3 acc[2];
+  float sum[2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      acc[i].hh[v] = 0; acc[i].xx[v] = 0; acc[i].ll[v] = 0;
+      sum[i][v] = 0.f;
+    }
+
+  const uint8_t* apix = a.ad + ((int64_t)(m0 + lc) * 2 + half) * 32;
+  const int64_t a_block_bytes = (int64_t)a.Mp * 64;
+  const int32_t Wpad = a.Wpad;
+  const int32_t PQ = a.P * a.Q;
+  int32_t blk_in_chunk = 0;
+  const int32_t chunk_blocks = a.L / 32;
+
+  // first K-block touching the segment, and the block after its last index
+  const int64_t kb_begin = t_seg0 / 32;
+  const int64_t kb_end = (t_seg1 + 31) / 32;
+  for (int64_t sb = kb_begin; sb < kb_end; sb += kSBT / 32) {
+    const int64_t sb_end = min(sb + kSBT / 32, kb_end);
+    const int64_t t_a = max(sb * 32, t_seg0);
+    const int64_t t_b = min(sb_end * 32, t_seg1) - 1;  // last index of the band
+    // padded-row span of the band
+    const int64_t na = t_a / PQ, pa = (t_a % PQ) / a.Q;
+    const int64_t nb = t_b / PQ, pb = (t_b % PQ) / a.Q;
+    const int64_t z_a = na * a.Hpad + pa * a.sh;
+    const int64_t z_b = nb * a.Hpad + pb * a.sh + a.R - 1;
+    const int32_t rows = (int32_t)(z_b - z_a + 1);
+    __syncthreads();  // previous band fully consumed
+    // offset table: t -> (z(t) - z_a) * Wpad + q * sw, for the band's 128 indices
+    if (threadIdx.x < kSBT) {
+      const int64_t t = sb * 32 + threadIdx.x;
+      int32_t off = 0;
+      if (t >= t_a && t <= t_b) {
+        const int64_t n = t / PQ, pq = t % PQ;
+        const int64_t p = pq / a.Q, q = pq % a.Q;
+        off = (int32_t)((n * a.Hpad + p * a.sh - z_a) * Wpad + q * a.sw);
+      }
+      toff[threadIdx.x] = off;
+    }
+    // band copy: for each channel, rows [z_a, z_a + rows) of XP are contiguous
+    {
+      const int32_t vec_per_row = Wpad / 8;  // 16-byte vectors
+      const int32_t vec_per_ch = rows * vec_per_row;
+      const int32_t total = nch * vec_per_ch;
+      for (int32_t i = threadIdx.x; i < total; i += kThreads) {
+        const int32_t cc = i / vec_per_ch, rem = i % vec_per_ch;
+        const uint4* src = reinterpret_cast<const uint4*>(
+            a.xp + (((int64_t)(c_lo + cc) * a.NH + z_a) * Wpad)) + rem;
+        reinterpret_cast<uint4*>(band + (int64_t)cc * a.band_ch_stride)[rem] = *src;
+      }
+    }
+    __syncthreads();
+    const int32_t lane_base = (c - c_lo) * a.band_ch_stride + rr * Wpad + ss;
+    for (int64_t kb = sb; kb < sb_end; ++kb) {
+      // ---- B: 16 (lo, hi) pairs of column (c, r, s)
+      const int32_t tb = (int32_t)(kb - sb) * 32 + half * 16;
+      uint32_t pr[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t p0 = band[lane_base + toff[tb + 2 * i]];
+        const uint32_t p1 = band[lane_base + toff[tb + 2 * i + 1]];
+        pr[i] = p0 | (p1 << 16);
+      }
+      v4i bhi, blo;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        blo[d] = (int)__builtin_amdgcn_perm(pr[2 * d + 1], pr[2 * d], 0x06040200u);
+        bhi[d] = (int)__builtin_amdgcn_perm(pr[2 * d + 1], pr[2 * d], 0x07050301u);
+      }
+      // indices of this block outside the segment (or past T) contribute 0
+      const int64_t t0 = kb * 32 + half * 16;
+      {
+        const int32_t lo_i = (int32_t)min(max(t_seg0 - t0, (int64_t)0), (int64_t)16);
+        const int32_t hi_i = (int32_t)min(max(t_seg1 - t0, (int64_t)0), (int64_t)16);
+        if (lo_i != 0 || hi_i != 16) {
+          const v4i mk = byte_mask16(lo_i, hi_i);
+          bhi &= mk;
+          blo &= mk;
+        }
+      }
+      // ---- A: two 32-row tiles of dy digits
+      v4i ahi[2], alo[2];
+      const uint8_t* ap = apix + kb * a_block_bytes;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const uint4* src = reinterpret_cast<const uint4*>(ap + i * 2048);
+        const uint4 h4 = src[0], l4 = src[1];
+        ahi[i] = (v4i){(int)h4.x, (int)h4.y, (int)h4.z, (int)h4.w};
+        alo[i] = (v4i){(int)l4.x, (int)l4.y, (int)l4.z, (int)l4.w};
+      }
+      if (!MASKED) {
+        const bool fresh = blk_in_chunk == 0;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) mfma_tile(acc[i], ahi[i], alo[i], bhi, blo, fresh);
+        ++blk_in_chunk;
+        if (blk_in_chunk == chunk_blocks || kb == kb_end - 1) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            flush_tile<PARTIALS>(acc[i], sum[i], j, a.partials, a.O, colc, CRS, m0 + 32 * i + 4 * half, a.K,
+                                 cvalid);
+          ++j;
+          blk_in_chunk = 0;
+        }
+      } else {
+        const int64_t t_lo = max(kb * 32, t_seg0), t_hi = min(kb * 32 + 32, t_seg1);
+        while (true) {
+          const int64_t cs = j * (int64_t)a.L;
+          const int64_t ce = min(cs + a.L, a.T);
+          const int64_t seg_lo = max(t_lo, cs), seg_hi = min(t_hi, ce);
+          const v4i mk = byte_mask16((int32_t)min(max(seg_lo - t0, (int64_t)0), (int64_t)16),
+                                     (int32_t)min(max(seg_hi - t0, (int64_t)0), (int64_t)16));
+          const v4i mhi = bhi & mk, mlo = blo & mk;
+          const bool fresh = seg_lo == cs;
+#pragma unroll
+          for (int i = 0; i < 2; ++i) mfma_tile(acc[i], ahi[i], alo[i], mhi, mlo, fresh);
+          if (ce <= t_hi) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+              flush_tile<PARTIALS>(acc[i], sum[i], j, a.partials, a.O, colc, CRS, m0 + 32 * i + 4 * half, a.K,
+                                   cvalid);
+            ++j;
+          }
+          if (ce >= t_hi) break;
+        }
+      }
+    }
+  }
+
+  // ---- segment sum: scaled result (single segment) or U_g for the ordered reduction
+  const int32_t e = a.ea->exp + a.eb->exp;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
+      if (cvalid && m < a.K) {
+        const int64_t o = (int64_t)m * CRS + col;
+        if (a.nseg == 1) a.out[o] = ldexpf(sum[i][v], e);
+        else a.useg[g * a.O + o] = sum[i][v];
+      }
+    }
+  }
+}
+
+// dW = 2^e * (((U_0 + U_1) + U_2) + ...), segment order.
+__global__ __launch_bounds__(256) void k_seg_reduce(const float* __restrict__ useg, float* __restrict__ out, int64_t O,
+                                                   int32_t nseg, const dfp_scale* ea, const dfp_scale* eb) {
+  const int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (o >= O) return;
+  float s = 0.f;
+  for (int32_t g = 0; g < nseg; ++g) s += useg[(int64_t)g * O + o];
+  out[o] = ldexpf(s, ea->exp + eb->exp);
+}
+
+inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
+
+}  // namespace
+
+BwdwPlan plan_bwdw_mfma(const Geom& g) {
+  BwdwPlan p{};
+  p.T = (int64_t)g.n * g.p * g.q;
+  p.KBT = (p.T + 31) / 32;
+  p.Mp = (g.k + kMT - 1) / kMT * kMT;
+  p.Hpad = g.h + 2 * g.ph;
+  p.Wpad = (g.w + 2 * g.pw + 7) / 8 * 8;
+  const int64_t J = (p.T + g.L - 1) / g.L;
+  p.nseg = (int32_t)((J + g.G - 1) / g.G);
+  // largest band (padded rows touched by kSBT consecutive indices of a segment)
+  const int64_t PQ = (int64_t)g.p * g.q;
+  int64_t rows_max = 0;
+  const int64_t seg_len = (int64_t)g.G * g.L;
+  for (int64_t s = 0; s < p.nseg; ++s) {
+    const int64_t t0 = s * seg_len, t1 = std::min(t0 + seg_len, p.T);
+    for (int64_t sb = t0 / 32; sb < (t1 + 31) / 32; sb += kSBT / 32) {
+      const int64_t ta = std::max(sb * 32, t0), tb = std::min((sb + kSBT / 32) * 32, t1) - 1;
+      const int64_t za = (ta / PQ) * p.Hpad + ((ta % PQ) / g.q) * g.sh;
+      const int64_t zb = (tb / PQ) * p.Hpad + ((tb % PQ) / g.q) * g.sh + g.r - 1;
+      rows_max = std::max(rows_max, zb - za + 1);
+    }
+  }
+  const int64_t RS = (int64_t)g.r * g.s;
+  p.nch_max = (int32_t)std::min<int64_t>(g.c, (kNT - 1) / RS + 2);
+  p.rows_max = (int32_t)rows_max;
+  p.band_ch_stride = (int32_t)(rows_max * p.Wpad);
+  p.band_bytes = align256((int64_t)p.nch_max * p.band_ch_stride * 2);
+  p.smem_bytes = p.band_bytes + kSBT * 4;
+  p.ad_bytes = align256(p.KBT * p.Mp * 64);
+  p.xp_bytes = align256((int64_t)g.c * g.n * p.Hpad * p.Wpad * 2);
+  p.u_bytes = p.nseg > 1 ? align256((int64_t)p.nseg * g.k * g.c * RS * 4) : 0;
+  p.bytes = p.ad_bytes + p.xp_bytes + p.u_bytes;
+  return p;
+}
+
+bool bwdw_mfma_supported(const Geom& g) {
+  const BwdwPlan p = plan_bwdw_mfma(g);
+  return p.smem_bytes <= 64 * 1024;
+}
+
+dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx, const int16_t* dy,
+                            const dfp_scale* sdy, float* dw, int32_t* partials, void* ws, hipStream_t st) {
+  const BwdwPlan p = plan_bwdw_mfma(g);
+  uint8_t* base = reinterpret_cast<uint8_t*>(ws);
+  uint8_t* ad = base;
+  uint16_t* xp = reinterpret_cast<uint16_t*>(base + p.ad_bytes);
+  float* useg = reinterpret_cast<float*>(base + p.ad_bytes + p.xp_bytes);
+  {
+    const int64_t total = p.KBT * p.Mp * 2;
+    DFP_LAUNCH(K_WPREP, k_prep_dy, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, dy, ad, g.k, p.Mp,
+               (int64_t)g.p * g.q, p.T, p.KBT);
+  }
+  {
+    const int64_t total = (int64_t)g.c * g.n * p.Hpad * p.Wpad;
+    DFP_LAUNCH(K_XPREP, k_prep_xp, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, xp, g.n, g.c, g.h,
+               g.w, p.Hpad, p.Wpad, g.ph, g.pw);
+  }
+  BwdwArgs args{};
+  args.ad = ad;
+  args.xp = xp;
+  args.ea = sx;
+  args.eb = sdy;
+  args.out = dw;
+  args.useg = useg;
+  args.partials = partials;
+  args.T = p.T;
+  args.O = (int64_t)g.k * g.c * g.r * g.s;
+  args.K = g.k; args.Mp = p.Mp; args.C = g.c; args.R = g.r; args.S = g.s;
+  args.P = g.p; args.Q = g.q; args.sh = g.sh; args.sw = g.sw;
+  args.Hpad = p.Hpad; args.Wpad = p.Wpad; args.NH = g.n * p.Hpad;
+  args.L = g.L; args.G = g.G; args.nseg = p.nseg;
+  args.band_bytes = (int32_t)p.band_bytes;
+  args.band_ch_stride = p.band_ch_stride;
+  const dim3 grid((unsigned)((args.O / g.k + kNT - 1) / kNT), (unsigned)(p.Mp / kMT), (unsigned)p.nseg);
+  const bool masked = (g.L % 32) != 0;
+  const size_t smem = (size_t)p.smem_bytes;
+  if (masked) {
+    if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_mfma<true, true>), grid, dim3(kThreads), smem, st, args);
+    else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_mfma<true, false>), grid, dim3(kThreads), smem, st, args);
+  } else {
+    if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_mfma<false, true>), grid, dim3(kThreads), smem, st, args);
+    else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_mfma<false, false>), grid, dim3(kThreads), smem, st, args);
+  }
+  if (p.nseg > 1) {
+    DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 255) / 256)), dim3(256), 0, st, useg, dw,
+               args.O, p.nseg, sx, sdy);
+  }
+  return DFP_OK;
+}
+
+}  // namespace dfp
