@@ -37,16 +37,16 @@ __device__ __forceinline__ uint32_t hi_digit(int32_t a) { return (uint32_t)((a +
 __device__ __forceinline__ uint32_t lo_digit(int32_t a) { return (uint32_t)a & 0xffu; }
 
 // A digits from dy in canonical order: Ad[kb][m][half][16 hi | 16 lo].
-// One thread per (m, kb, half), kb fastest so consecutive threads read
-// consecutive reduction indices of one dy plane.
+// One thread per (kb, m, half), written in that order so a wave's stores are
+// contiguous; each thread reads 16 consecutive reduction indices of one plane.
 __global__ __launch_bounds__(256) void k_prep_dy(const int16_t* __restrict__ dy, uint8_t* __restrict__ ad, int32_t K,
                                                 int32_t Mp, int64_t PQ, int64_t T, int64_t KBT) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t total = KBT * Mp * 2;
   if (idx >= total) return;
   const int32_t half = (int32_t)(idx & 1);
-  const int64_t kb = (idx >> 1) % KBT;
-  const int32_t m = (int32_t)((idx >> 1) / KBT);
+  const int32_t m = (int32_t)((idx >> 1) % Mp);
+  const int64_t kb = (idx >> 1) / Mp;
   uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
   if (m < K) {
     int64_t t = kb * 32 + half * 16;
@@ -67,23 +67,33 @@ __global__ __launch_bounds__(256) void k_prep_dy(const int16_t* __restrict__ dy,
 }
 
 // XP[c][n*Hpad + u][v] = (lo | hi << 8) of x[n][c][u - ph][v - pw], zero outside.
+// One thread per 8 consecutive pairs of a row (Wpad is a multiple of 8): one
+// 16-byte store.
 __global__ __launch_bounds__(256) void k_prep_xp(const int16_t* __restrict__ x, uint16_t* __restrict__ xp, int32_t N,
                                                 int32_t C, int32_t H, int32_t W, int32_t Hpad, int32_t Wpad,
                                                 int32_t ph, int32_t pw) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t total = (int64_t)C * N * Hpad * Wpad;
+  const int32_t W8 = Wpad / 8;
+  const int64_t total = (int64_t)C * N * Hpad * W8;
   if (idx >= total) return;
-  const int32_t v = (int32_t)(idx % Wpad);
-  const int64_t z = (idx / Wpad) % ((int64_t)N * Hpad);
-  const int32_t c = (int32_t)(idx / ((int64_t)Wpad * N * Hpad));
+  const int32_t v0 = (int32_t)(idx % W8) * 8;
+  const int64_t z = (idx / W8) % ((int64_t)N * Hpad);
+  const int32_t c = (int32_t)(idx / ((int64_t)W8 * N * Hpad));
   const int32_t n = (int32_t)(z / Hpad), u = (int32_t)(z % Hpad);
-  const int32_t ih = u - ph, iw = v - pw;
-  uint32_t pair = 0;
-  if (ih >= 0 && ih < H && iw >= 0 && iw < W) {
-    const int32_t a = x[(((int64_t)n * C + c) * H + ih) * W + iw];
-    pair = lo_digit(a) | (hi_digit(a) << 8);
+  const int32_t ih = u - ph;
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+  if (ih >= 0 && ih < H) {
+    const int16_t* row = x + (((int64_t)n * C + c) * H + ih) * W;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int32_t iw = v0 + i - pw;
+      if (iw >= 0 && iw < W) {
+        const int32_t a = row[iw];
+        w[i >> 1] |= (lo_digit(a) | (hi_digit(a) << 8)) << (16 * (i & 1));
+      }
+    }
   }
-  xp[idx] = (uint16_t)pair;
+  reinterpret_cast<uint4*>(xp)[idx] = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 // Byte mask keeping bytes [lo, hi) of a 16-byte operand.
@@ -315,12 +325,20 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_mfma(BwdwArgs a) {
 }
 
 // dW = 2^e * (((U_0 + U_1) + U_2) + ...), segment order.
-__global__ __launch_bounds__(256) void k_seg_reduce(const float* __restrict__ useg, float* __restrict__ out, int64_t O,
-                                                   int32_t nseg, const dfp_scale* ea, const dfp_scale* eb) {
-  const int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x;
+__global__ __launch_bounds__(64) void k_seg_reduce(const float* __restrict__ useg, float* __restrict__ out, int64_t O,
+                                                  int32_t nseg, const dfp_scale* ea, const dfp_scale* eb) {
+  const int64_t o = (int64_t)blockIdx.x * 64 + threadIdx.x;
   if (o >= O) return;
   float s = 0.f;
-  for (int32_t g = 0; g < nseg; ++g) s += useg[(int64_t)g * O + o];
+  int32_t g = 0;
+  for (; g + 8 <= nseg; g += 8) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = useg[(int64_t)(g + i) * O + o];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += v[i];
+  }
+  for (; g < nseg; ++g) s += useg[(int64_t)g * O + o];
   out[o] = ldexpf(s, ea->exp + eb->exp);
 }
 
@@ -381,7 +399,7 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
                (int64_t)g.p * g.q, p.T, p.KBT);
   }
   {
-    const int64_t total = (int64_t)g.c * g.n * p.Hpad * p.Wpad;
+    const int64_t total = (int64_t)g.c * g.n * p.Hpad * (p.Wpad / 8);
     DFP_LAUNCH(K_XPREP, k_prep_xp, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, xp, g.n, g.c, g.h,
                g.w, p.Hpad, p.Wpad, g.ph, g.pw);
   }
@@ -412,7 +430,7 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_mfma<false, false>), grid, dim3(kThreads), smem, st, args);
   }
   if (p.nseg > 1) {
-    DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 255) / 256)), dim3(256), 0, st, useg, dw,
+    DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 63) / 64)), dim3(64), 0, st, useg, dw,
                args.O, p.nseg, sx, sdy);
   }
   return DFP_OK;

@@ -32,6 +32,8 @@
 // to the running FP32 sum in chunk order; chunk lengths that are not a
 // multiple of 32 run the block once per chunk it overlaps, with the bytes of
 // the other chunks masked to zero.
+#include <type_traits>
+
 #include "dfp_internal.h"
 #include "conv_mfma.h"
 
@@ -86,37 +88,44 @@ __global__ __launch_bounds__(256) void k_prep_a(const int16_t* __restrict__ w, u
 }
 
 // ---------------------------------------------------------------- B prep
-// Xs[n][u][v][cg][32 B] = digits of src[n][cg*16 + i][(u-top)/dil][(v-left)/dil]
-// when (u-top), (v-left) are non-negative multiples of dil inside the source,
-// else 0.  One thread per (n, u, v, cg); v runs fastest for coalesced reads.
+// Xs[n][u][v][cg][32 B] = digits of src[n][cg*16 + i][(u-top)/dil_h][(v-left)/dil_w]
+// when (u-top), (v-left) are non-negative multiples of the dilation inside the
+// source, else 0.  One thread per (n, u, v, block of up to 4 channel groups)
+// writes 4*32 contiguous bytes; consecutive threads take consecutive v, so the
+// reads of one channel row are contiguous across the wave.
 __global__ __launch_bounds__(256) void k_prep_b(const int16_t* __restrict__ src, uint8_t* __restrict__ xs,
                                                int32_t N, int32_t Cs, int32_t Hs, int32_t Wsrc, int32_t Hp,
                                                int32_t Wp, int32_t CG, int32_t top, int32_t left, int32_t dil_h,
                                                int32_t dil_w) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t total = (int64_t)N * CG * Hp * Wp;
+  const int32_t CB = (CG + 3) / 4;
+  const int64_t total = (int64_t)N * Hp * Wp * CB;
   if (idx >= total) return;
   const int32_t v = (int32_t)(idx % Wp);
-  const int32_t u = (int32_t)((idx / Wp) % Hp);
-  const int32_t cg = (int32_t)((idx / ((int64_t)Wp * Hp)) % CG);
-  const int64_t n = idx / ((int64_t)Wp * Hp * CG);
+  const int32_t cb = (int32_t)((idx / Wp) % CB);
+  const int32_t u = (int32_t)((idx / ((int64_t)Wp * CB)) % Hp);
+  const int64_t n = idx / ((int64_t)Wp * CB * Hp);
   const int32_t zu = u - top, zv = v - left;
   const bool inside =
       zu >= 0 && zv >= 0 && (zu % dil_h) == 0 && (zv % dil_w) == 0 && zu / dil_h < Hs && zv / dil_w < Wsrc;
-  uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
-  if (inside) {
-    const int64_t plane = (int64_t)Hs * Wsrc;
-    const int16_t* p = src + (n * Cs + (int64_t)cg * 16) * plane + (int64_t)(zu / dil_h) * Wsrc + zv / dil_w;
+  const int64_t plane = (int64_t)Hs * Wsrc;
+  const int16_t* p = src + n * Cs * plane + (inside ? (int64_t)(zu / dil_h) * Wsrc + zv / dil_w : 0);
+  uint4* dst = reinterpret_cast<uint4*>(xs + ((n * Hp + u) * Wp + v) * CG * 32);
+  const int32_t cg_end = min(CG, cb * 4 + 4);
+  for (int32_t cg = cb * 4; cg < cg_end; ++cg) {
+    uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+    if (inside) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int32_t a = (cg * 16 + i < Cs) ? (int32_t)p[i * plane] : 0;
-      hi[i >> 2] |= hi_digit(a) << (8 * (i & 3));
-      lo[i >> 2] |= lo_digit(a) << (8 * (i & 3));
+      for (int i = 0; i < 16; ++i) {
+        const int32_t c = cg * 16 + i;
+        const int32_t a = (c < Cs) ? (int32_t)p[c * plane] : 0;
+        hi[i >> 2] |= hi_digit(a) << (8 * (i & 3));
+        lo[i >> 2] |= lo_digit(a) << (8 * (i & 3));
+      }
     }
+    dst[2 * cg] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+    dst[2 * cg + 1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
   }
-  uint4* dst = reinterpret_cast<uint4*>(xs + ((((n * Hp + u) * Wp + v) * CG) + cg) * 32);
-  dst[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-  dst[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
 }
 
 // Byte mask keeping bytes [lo, hi) of a 16-byte operand (0 <= lo <= hi <= 16).
@@ -352,7 +361,251 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv_mfma(ConvMfmaArgs a) {
     if (threadIdx.x == 0) {
       uint32_t b = red[0];
       for (int i = 1; i < kThreads / 64; ++i) b = max(b, red[i]);
-      atomicMax(&a.so->amax_bits, b);
+      if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
+      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pipelined variant for reduction channel counts that are multiples of 16:
+// every operand block (A: 64 rows x 32 indices, B: 128 pixels x 32 indices,
+// both as hi/lo digit bytes) is fetched with direct-to-LDS 16-byte loads
+// (global_load_lds_dwordx4) into a ring of kStages stages, kStages-1 blocks
+// ahead of the MFMAs, with one workgroup barrier per block.  Each 16-byte
+// piece (row or pixel, half, digit) sits at slot row*4 + ((2*half + digit) ^
+// ((row >> 2) & 3)) of its region, which keeps the ds_read_b128 operand reads
+// of 16 consecutive rows (or pixels) on distinct banks.
+constexpr int kStages = 4;
+constexpr int kStageA = 4096;   // 64 rows x 2 halves x 32 B
+constexpr int kStageB = 8192;   // 128 pixels x 2 halves x 32 B
+constexpr int kStageBytes = kStageA + kStageB;
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+__device__ __forceinline__ int swz(int row, int piece) { return row * 4 + (piece ^ ((row >> 2) & 3)); }
+
+// s_waitcnt vmcnt(N): this lane's direct-to-LDS loads older than the newest N
+// have landed.  Issued as inline assembly together with the raw barrier below,
+// because the compiler's own wait insertion treats every LDS read as aliasing
+// every in-flight LDS load and would drain the whole pipeline.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// The six operand reads of one stage (B hi/lo, A hi/lo of two tiles), then a
+// wait for all of them.  Stage offset STAGE_OFF is an immediate.
+template <int STAGE_OFF>
+__device__ __forceinline__ void read_stage(uint32_t b0, uint32_t b1, uint32_t a00, uint32_t a01, uint32_t a10,
+                                           uint32_t a11, v4i& bhi, v4i& blo, v4i (&ahi)[2], v4i (&alo)[2]) {
+  asm volatile(
+      "ds_read_b128 %0, %6 offset:%12\n\t"
+      "ds_read_b128 %1, %7 offset:%12\n\t"
+      "ds_read_b128 %2, %8 offset:%12\n\t"
+      "ds_read_b128 %3, %9 offset:%12\n\t"
+      "ds_read_b128 %4, %10 offset:%12\n\t"
+      "ds_read_b128 %5, %11 offset:%12\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(bhi), "=&v"(blo), "=&v"(ahi[0]), "=&v"(alo[0]), "=&v"(ahi[1]), "=&v"(alo[1])
+      : "v"(b0), "v"(b1), "v"(a00), "v"(a01), "v"(a10), "v"(a11), "n"(STAGE_OFF)
+      : "memory");
+}
+
+template <bool MASKED, bool PARTIALS>
+__global__ __launch_bounds__(kThreads, 2) void k_conv_mfma_lds(ConvMfmaArgs a) {
+  __shared__ __align__(16) uint8_t smem[kStages * kStageBytes];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int half = lane >> 5;
+  const int col = lane & 31;
+  const int32_t m0 = blockIdx.y * kMT;
+  const int64_t NP = a.NP;
+  const int64_t PQ = (int64_t)a.Po * a.Qo;
+
+  // ---- output pixel of this lane (MFMA column)
+  const int64_t g = (int64_t)blockIdx.x * kNT + wave * 32 + col;
+  const bool gvalid = g < NP;
+  int64_t img, obase;
+  {
+    const int64_t gg = gvalid ? g : 0;
+    const int32_t qo = (int32_t)(gg % a.Qo), po = (int32_t)((gg / a.Qo) % a.Po);
+    img = gg / PQ;
+    obase = img * a.M * PQ + (int64_t)po * a.Qo + qo;
+  }
+
+  // ---- load assignments: A slot wave*64 + lane; B slots wave*128 + i*64 + lane
+  const int a_slot = wave * 64 + lane;
+  const int a_row = a_slot >> 2, a_piece = (a_slot & 3) ^ ((a_row >> 2) & 3);
+  const uint8_t* a_src = a.wsa + ((int64_t)(m0 + a_row) * 2 + (a_piece >> 1)) * 32 + (a_piece & 1) * 16;
+  const int64_t a_block_bytes = (int64_t)a.Mp * 64;
+  const uint8_t* b_src[2];
+  int b_half[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int slot = wave * 128 + i * 64 + lane;
+    const int px = slot >> 2, piece = (slot & 3) ^ ((px >> 2) & 3);
+    b_half[i] = piece >> 1;
+    int64_t gp = (int64_t)blockIdx.x * kNT + px;
+    if (gp >= NP) gp = 0;
+    const int32_t qo = (int32_t)(gp % a.Qo), po = (int32_t)((gp / a.Qo) % a.Po);
+    const int64_t im = gp / PQ;
+    b_src[i] = a.xs +
+               (((im * a.Hp + (int64_t)po * a.ustride_h + a.roff_h) * a.Wp + (int64_t)qo * a.ustride_w + a.roff_w) *
+                a.CG) * 32 +
+               (piece & 1) * 16;
+  }
+  const int32_t tap_row_bytes = a.rsign * a.Wp * a.CG * 32;
+  const int32_t tap_col_bytes = a.rsign * a.CG * 32;
+  const int32_t T = a.T, L = a.L, Cin = a.Cin, KB = a.KB;
+
+  // uniform reduction position of the next block to load
+  int32_t ld_c = 0, ld_r = 0, ld_s = 0;
+  auto issue = [&](int32_t kb) {
+    uint8_t* st = smem + (kb % kStages) * kStageBytes;
+    __builtin_amdgcn_global_load_lds((const void*)(a_src + kb * a_block_bytes), (lds_ptr_t)(st + wave * 1024), 16, 0,
+                                     0);
+    const int32_t off0 = ld_r * tap_row_bytes + ld_s * tap_col_bytes + (ld_c >> 4) * 32;
+    int32_t off1;
+    if (ld_c + 16 < Cin) {
+      off1 = off0 + 32;
+    } else {
+      const int32_t s1 = (ld_s + 1 == a.S) ? 0 : ld_s + 1;
+      const int32_t r1 = (ld_s + 1 == a.S) ? ld_r + 1 : ld_r;
+      off1 = r1 * tap_row_bytes + s1 * tap_col_bytes;
+    }
+    // indices at or past T read a valid dummy location (their A digits are zero)
+    const int32_t o0 = (kb * 32 < T) ? off0 : 0;
+    const int32_t o1 = (kb * 32 + 16 < T) ? off1 : 0;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(b_src[i] + (b_half[i] ? o1 : o0)),
+                                       (lds_ptr_t)(st + kStageA + wave * 2048 + i * 1024), 16, 0, 0);
+    ld_c += 32;
+    while (ld_c >= Cin) {
+      ld_c -= Cin;
+      if (++ld_s == a.S) { ld_s = 0; ++ld_r; }
+    }
+  };
+
+  Acc3 acc[2];
+  float sum[2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      acc[i].hh[v] = 0; acc[i].xx[v] = 0; acc[i].ll[v] = 0;
+      sum[i][v] = 0.f;
+    }
+
+  // LDS read offsets of this lane's operands inside a stage
+  const int b_rd0 = kStageA + swz(wave * 32 + col, 2 * half) * 16;
+  const int b_rd1 = kStageA + swz(wave * 32 + col, 2 * half + 1) * 16;
+  int a_rd[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int d = 0; d < 2; ++d) a_rd[i][d] = swz(32 * i + col, 2 * half + d) * 16;
+
+  int64_t j = 0;
+  int32_t blk_in_chunk = 0;
+  const int32_t chunk_blocks = L / 32;
+
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)smem;
+  const uint32_t rb0 = lds_base + b_rd0, rb1 = lds_base + b_rd1;
+  const uint32_t ra00 = lds_base + a_rd[0][0], ra01 = lds_base + a_rd[0][1];
+  const uint32_t ra10 = lds_base + a_rd[1][0], ra11 = lds_base + a_rd[1][1];
+
+  auto consume = [&](int32_t kb, const v4i& bhi, const v4i& blo, const v4i (&ahi)[2], const v4i (&alo)[2]) {
+    if (!MASKED) {
+      const bool fresh = blk_in_chunk == 0;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) mfma_tile(acc[i], ahi[i], alo[i], bhi, blo, fresh);
+      ++blk_in_chunk;
+      if (blk_in_chunk == chunk_blocks || kb == KB - 1) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          flush_tile<PARTIALS>(acc[i], sum[i], j, a.partials, a.O, obase, PQ, m0 + 32 * i + 4 * half, a.M, gvalid);
+        ++j;
+        blk_in_chunk = 0;
+      }
+    } else {
+      const int32_t t0 = kb * 32 + half * 16;
+      const int32_t t_lo = kb * 32, t_hi = min(kb * 32 + 32, T);
+      while (true) {
+        const int64_t cs = j * (int64_t)L;
+        const int64_t ce = min(cs + L, (int64_t)T);
+        const int32_t seg_lo = (int32_t)max((int64_t)t_lo, cs), seg_hi = (int32_t)min((int64_t)t_hi, ce);
+        const v4i mk = byte_mask16(min(max(seg_lo - t0, 0), 16), min(max(seg_hi - t0, 0), 16));
+        const v4i mhi = bhi & mk, mlo = blo & mk;
+        const bool fresh = seg_lo == cs;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) mfma_tile(acc[i], ahi[i], alo[i], mhi, mlo, fresh);
+        if (ce <= t_hi) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            flush_tile<PARTIALS>(acc[i], sum[i], j, a.partials, a.O, obase, PQ, m0 + 32 * i + 4 * half, a.M,
+                                 gvalid);
+          ++j;
+        }
+        if (ce >= t_hi) break;
+      }
+    }
+  };
+
+  // One block: wait for its loads (the kStages-2 newer blocks may stay in
+  // flight, 3 loads each), barrier, refill the slot freed by the previous
+  // block, read and consume.
+  auto step = [&](int32_t kb, auto stage_tag) {
+    constexpr int STAGE = decltype(stage_tag)::value;
+    const int32_t ahead = min(kStages - 2, KB - 1 - kb);
+    if (ahead >= 2) wait_vmcnt<6>();
+    else if (ahead == 1) wait_vmcnt<3>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kb + kStages - 1 < KB) issue(kb + kStages - 1);
+    v4i bhi, blo, ahi[2], alo[2];
+    read_stage<STAGE * kStageBytes>(rb0, rb1, ra00, ra01, ra10, ra11, bhi, blo, ahi, alo);
+    consume(kb, bhi, blo, ahi, alo);
+  };
+
+  for (int32_t s = 0; s < kStages - 1 && s < KB; ++s) issue(s);
+  int32_t kb = 0;
+  for (; kb + kStages <= KB; kb += kStages) {
+    step(kb + 0, std::integral_constant<int, 0>{});
+    step(kb + 1, std::integral_constant<int, 1>{});
+    step(kb + 2, std::integral_constant<int, 2>{});
+    step(kb + 3, std::integral_constant<int, 3>{});
+  }
+  if (kb < KB) step(kb++, std::integral_constant<int, 0>{});
+  if (kb < KB) step(kb++, std::integral_constant<int, 1>{});
+  if (kb < KB) step(kb++, std::integral_constant<int, 2>{});
+
+  // ---- epilogue: scale once, store, max |y|
+  const int32_t e = a.ea->exp + a.eb->exp;
+  uint32_t amax = 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
+      const float y = ldexpf(sum[i][v], e);
+      if (gvalid && m < a.M) {
+        a.out[obase + (int64_t)m * PQ] = y;
+        amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
+      }
+    }
+  }
+  if (a.so) {
+    __shared__ uint32_t red[kThreads / 64];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
+    if (lane == 0) red[wave] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t b = red[0];
+      for (int i = 1; i < kThreads / 64; ++i) b = max(b, red[i]);
+      if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
       if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
     }
   }
@@ -407,7 +660,7 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   }
   {
     const int32_t Cs = fwd ? g.c : g.k, Hs = fwd ? g.h : g.p, Wsrc = fwd ? g.w : g.q;
-    const int64_t total = (int64_t)g.n * p.CG * p.Hp * p.Wp;
+    const int64_t total = (int64_t)g.n * p.Hp * p.Wp * ((p.CG + 3) / 4);
     DFP_LAUNCH(K_XPREP, k_prep_b, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, a, xs, g.n, Cs, Hs,
                Wsrc, p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w);
   }
@@ -445,13 +698,16 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
     DFP_LAUNCH(kid, (k_conv_mfma<MK, PT, CH>), grid, dim3(kThreads), 0, st, args);          \
     return DFP_OK;                                                                          \
   }
-  DFP_CONV_MFMA_CASE(false, false, true)
+  if (chan16) {
+    if (!masked && !partials) DFP_LAUNCH(kid, (k_conv_mfma_lds<false, false>), grid, dim3(kThreads), 0, st, args);
+    else if (!masked) DFP_LAUNCH(kid, (k_conv_mfma_lds<false, true>), grid, dim3(kThreads), 0, st, args);
+    else if (!partials) DFP_LAUNCH(kid, (k_conv_mfma_lds<true, false>), grid, dim3(kThreads), 0, st, args);
+    else DFP_LAUNCH(kid, (k_conv_mfma_lds<true, true>), grid, dim3(kThreads), 0, st, args);
+    return DFP_OK;
+  }
   DFP_CONV_MFMA_CASE(false, false, false)
-  DFP_CONV_MFMA_CASE(false, true, true)
   DFP_CONV_MFMA_CASE(false, true, false)
-  DFP_CONV_MFMA_CASE(true, false, true)
   DFP_CONV_MFMA_CASE(true, false, false)
-  DFP_CONV_MFMA_CASE(true, true, true)
   DFP_CONV_MFMA_CASE(true, true, false)
 #undef DFP_CONV_MFMA_CASE
   return DFP_ERR_PARAM;

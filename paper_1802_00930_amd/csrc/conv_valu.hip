@@ -69,7 +69,7 @@ __device__ __forceinline__ void epilogue_amax(float y, bool active, dfp_scale* s
   if (threadIdx.x == 0) {
     uint32_t b = red[0];
     for (int i = 1; i < kBlock / 64; ++i) b = max(b, red[i]);
-    atomicMax(&so->amax_bits, b);
+    if (b > __atomic_load_n(&so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&so->amax_bits, b);
     if (b == 0x7f800000u) atomicOr(&so->flags, DFP_FLAG_OUTPUT_INF);
   }
 }

@@ -56,7 +56,8 @@ __global__ __launch_bounds__(kBlock) void k_amax(const float* __restrict__ src, 
     for (int64_t i = 4 * n4 + threadIdx.x; i < n; i += kBlock) m = max(m, s1[i] & 0x7fffffffu);
   }
   m = block_max(m);
-  if (threadIdx.x == 0) atomicMax(&s->amax_bits, m);
+  // most blocks cannot raise the running max: skip their atomic after a plain read
+  if (threadIdx.x == 0 && m > __atomic_load_n(&s->amax_bits, __ATOMIC_RELAXED)) atomicMax(&s->amax_bits, m);
 }
 
 // Philox4x32-10 (Salmon et al., SC'11).
@@ -200,7 +201,10 @@ dfp_status launch_scale_reset(dfp_scale* s, hipStream_t st) {
 }
 
 dfp_status launch_amax(const float* src, int64_t n, dfp_scale* s, hipStream_t st) {
-  DFP_LAUNCH(K_AMAX, k_amax, dim3(grid_for(n / 4)), dim3(kBlock), 0, st, src, n, s);
+  // at most 1024 blocks: each ends with one (usually skipped) atomic on the same word
+  int64_t blocks = (n / 4 + kBlock - 1) / kBlock;
+  blocks = blocks < 1 ? 1 : (blocks > 1024 ? 1024 : blocks);
+  DFP_LAUNCH(K_AMAX, k_amax, dim3((unsigned)blocks), dim3(kBlock), 0, st, src, n, s);
   return DFP_OK;
 }
 
