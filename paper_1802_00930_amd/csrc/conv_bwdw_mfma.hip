@@ -127,10 +127,13 @@ __device__ __forceinline__ void mfma_tile(Acc3& acc, const v4i& ahi, const v4i& 
   acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, bhi, acc.xx, 0, 0, 0);
 }
 
-__device__ __forceinline__ uint32_t shl8_add(uint32_t a, uint32_t b) {
-  uint32_t r;
-  asm("v_lshl_add_u32 %0, %1, 8, %2" : "=v"(r) : "v"(a), "v"(b));
-  return r;
+// ((a << 8) + b) << 8) + c as two v_lshl_add_u32.  The shift-adds are plain
+// C so the compiler's hazard checks see every read of an MFMA result; the
+// empty asm only stops the re-association into shift, shift, add3.
+__device__ __forceinline__ uint32_t recombine(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t t = (a << 8) + b;
+  asm("" : "+v"(t));
+  return (t << 8) + c;
 }
 
 // Chunk end: P_j recombined, converted (round to nearest even), added in order.
@@ -140,7 +143,7 @@ __device__ __forceinline__ void flush_tile(const Acc3& acc, float (&sum)[16], in
                                            bool cvalid) {
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
-    const uint32_t p = shl8_add(shl8_add((uint32_t)acc.hh[v], (uint32_t)acc.xx[v]), (uint32_t)acc.ll[v]);
+    const uint32_t p = recombine((uint32_t)acc.hh[v], (uint32_t)acc.xx[v], (uint32_t)acc.ll[v]);
     sum[v] += (float)(int32_t)p;
     if (PARTIALS) {
       const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);

@@ -161,12 +161,13 @@ __device__ __forceinline__ void mfma_tile(Acc3& acc, const v4i& ahi, const v4i& 
   acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, bhi, acc.xx, 0, 0, 0);
 }
 
-// (a << 8) + b as one v_lshl_add_u32 (the compiler otherwise re-associates the
-// recombination into three instructions).
-__device__ __forceinline__ uint32_t shl8_add(uint32_t a, uint32_t b) {
-  uint32_t r;
-  asm("v_lshl_add_u32 %0, %1, 8, %2" : "=v"(r) : "v"(a), "v"(b));
-  return r;
+// ((a << 8) + b) << 8) + c as two v_lshl_add_u32.  The shift-adds are plain
+// C so the compiler's hazard checks see every read of an MFMA result; the
+// empty asm only stops the re-association into shift, shift, add3.
+__device__ __forceinline__ uint32_t recombine(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t t = (a << 8) + b;
+  asm("" : "+v"(t));
+  return (t << 8) + c;
 }
 
 // Chunk end: P_j = ((HH << 8) + X) << 8) + LL modulo 2^32, converted to FP32
@@ -177,7 +178,7 @@ __device__ __forceinline__ void flush_tile(const Acc3& acc, float (&sum)[16], in
                                            bool gvalid) {
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
-    const uint32_t p = shl8_add(shl8_add((uint32_t)acc.hh[v], (uint32_t)acc.xx[v]), (uint32_t)acc.ll[v]);
+    const uint32_t p = recombine((uint32_t)acc.hh[v], (uint32_t)acc.xx[v], (uint32_t)acc.ll[v]);
     sum[v] += (float)(int32_t)p;
     if (PARTIALS) {
       const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
@@ -611,6 +612,232 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv_mfma_lds(ConvMfmaArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Skewed variant for chunks of exactly two blocks (L = 64) when every chunk is
+// full (T a multiple of 64).  At L = 64 a chunk's conversion costs as many VALU
+// cycles as its MFMAs, so the two 32-row tiles of a wave run one block out of
+// phase: tile 1 consumes block kb-1 while tile 0 consumes block kb.  The chunk
+// end of one tile then always falls in a block where only the other tile issues
+// MFMAs, and the conversion (two shift-adds, a convert and an add per output)
+// is interleaved with those MFMAs instruction by instruction.
+//   even kb: flush tile 0 (chunk kb/2-1) || tile 1 block kb-1; tile 0 block kb opens a chunk
+//   odd  kb: flush tile 1 (chunk (kb-1)/2-1) || tile 0 block kb; tile 1 block kb-1 opens a chunk
+// Operand reads of the next stage are issued before the MFMAs of this one.
+
+// Issue the six operand reads of a stage (no wait).
+template <int STAGE_OFF>
+__device__ __forceinline__ void read_stage_issue(uint32_t b0, uint32_t b1, uint32_t a00, uint32_t a01, uint32_t a10,
+                                                 uint32_t a11, v4i& bhi, v4i& blo, v4i& ahi0, v4i& alo0, v4i& ahi1,
+                                                 v4i& alo1) {
+  asm volatile(
+      "ds_read_b128 %0, %6 offset:%12\n\t"
+      "ds_read_b128 %1, %7 offset:%12\n\t"
+      "ds_read_b128 %2, %8 offset:%12\n\t"
+      "ds_read_b128 %3, %9 offset:%12\n\t"
+      "ds_read_b128 %4, %10 offset:%12\n\t"
+      "ds_read_b128 %5, %11 offset:%12"
+      : "=&v"(bhi), "=&v"(blo), "=&v"(ahi0), "=&v"(alo0), "=&v"(ahi1), "=&v"(alo1)
+      : "v"(b0), "v"(b1), "v"(a00), "v"(a01), "v"(a10), "v"(a11), "n"(STAGE_OFF)
+      : "memory");
+}
+
+// Wait for outstanding LDS reads; the operands pass through so that no use
+// can be scheduled before the wait.
+__device__ __forceinline__ void read_stage_wait(v4i& bhi, v4i& blo, v4i& ahi0, v4i& alo0, v4i& ahi1, v4i& alo1) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(bhi), "+v"(blo), "+v"(ahi0), "+v"(alo0), "+v"(ahi1), "+v"(alo1)
+               :
+               : "memory");
+}
+
+// 4 MFMAs of one tile interleaved with a 64-instruction conversion block.
+__device__ __forceinline__ void interleave_4x16() {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+  }
+}
+
+template <bool PARTIALS>
+__global__ __launch_bounds__(kThreads, 2) void k_conv_mfma_skew(ConvMfmaArgs a) {
+  __shared__ __align__(16) uint8_t smem[kStages * kStageBytes];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int half = lane >> 5;
+  const int col = lane & 31;
+  const int32_t m0 = blockIdx.y * kMT;
+  const int64_t NP = a.NP;
+  const int64_t PQ = (int64_t)a.Po * a.Qo;
+
+  const int64_t g = (int64_t)blockIdx.x * kNT + wave * 32 + col;
+  const bool gvalid = g < NP;
+  int64_t obase;
+  {
+    const int64_t gg = gvalid ? g : 0;
+    const int32_t qo = (int32_t)(gg % a.Qo), po = (int32_t)((gg / a.Qo) % a.Po);
+    const int64_t img = gg / PQ;
+    obase = img * a.M * PQ + (int64_t)po * a.Qo + qo;
+  }
+
+  const int a_slot = wave * 64 + lane;
+  const int a_row = a_slot >> 2, a_piece = (a_slot & 3) ^ ((a_row >> 2) & 3);
+  const uint8_t* a_src = a.wsa + ((int64_t)(m0 + a_row) * 2 + (a_piece >> 1)) * 32 + (a_piece & 1) * 16;
+  const int64_t a_block_bytes = (int64_t)a.Mp * 64;
+  const uint8_t* b_src[2];
+  int b_half[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int slot = wave * 128 + i * 64 + lane;
+    const int px = slot >> 2, piece = (slot & 3) ^ ((px >> 2) & 3);
+    b_half[i] = piece >> 1;
+    int64_t gp = (int64_t)blockIdx.x * kNT + px;
+    if (gp >= NP) gp = 0;
+    const int32_t qo = (int32_t)(gp % a.Qo), po = (int32_t)((gp / a.Qo) % a.Po);
+    const int64_t im = gp / PQ;
+    b_src[i] = a.xs +
+               (((im * a.Hp + (int64_t)po * a.ustride_h + a.roff_h) * a.Wp + (int64_t)qo * a.ustride_w + a.roff_w) *
+                a.CG) * 32 +
+               (piece & 1) * 16;
+  }
+  const int32_t tap_row_bytes = a.rsign * a.Wp * a.CG * 32;
+  const int32_t tap_col_bytes = a.rsign * a.CG * 32;
+  const int32_t Cin = a.Cin, KB = a.KB;
+
+  int32_t ld_c = 0, ld_r = 0, ld_s = 0;
+  auto issue = [&](int32_t kb) {
+    uint8_t* st = smem + (kb % kStages) * kStageBytes;
+    __builtin_amdgcn_global_load_lds((const void*)(a_src + kb * a_block_bytes), (lds_ptr_t)(st + wave * 1024), 16, 0,
+                                     0);
+    const int32_t off0 = ld_r * tap_row_bytes + ld_s * tap_col_bytes + (ld_c >> 4) * 32;
+    int32_t off1;
+    if (ld_c + 16 < Cin) {
+      off1 = off0 + 32;
+    } else {
+      const int32_t s1 = (ld_s + 1 == a.S) ? 0 : ld_s + 1;
+      const int32_t r1 = (ld_s + 1 == a.S) ? ld_r + 1 : ld_r;
+      off1 = r1 * tap_row_bytes + s1 * tap_col_bytes;
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(b_src[i] + (b_half[i] ? off1 : off0)),
+                                       (lds_ptr_t)(st + kStageA + wave * 2048 + i * 1024), 16, 0, 0);
+    ld_c += 32;
+    while (ld_c >= Cin) {
+      ld_c -= Cin;
+      if (++ld_s == a.S) { ld_s = 0; ++ld_r; }
+    }
+  };
+  // wait until block kb has landed for every lane of the workgroup, then refill
+  auto sync_block = [&](int32_t kb) {
+    const int32_t ahead = min(kStages - 2, KB - 1 - kb);
+    if (ahead >= 2) wait_vmcnt<6>();
+    else if (ahead == 1) wait_vmcnt<3>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kb + kStages - 1 < KB) issue(kb + kStages - 1);
+  };
+
+  Acc3 acc0, acc1;
+  float sum0[16], sum1[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    acc0.hh[v] = 0; acc0.xx[v] = 0; acc0.ll[v] = 0;
+    acc1.hh[v] = 0; acc1.xx[v] = 0; acc1.ll[v] = 0;
+    sum0[v] = 0.f; sum1[v] = 0.f;
+  }
+
+  const int b_rd0 = kStageA + swz(wave * 32 + col, 2 * half) * 16;
+  const int b_rd1 = kStageA + swz(wave * 32 + col, 2 * half + 1) * 16;
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)smem;
+  const uint32_t rb0 = lds_base + b_rd0, rb1 = lds_base + b_rd1;
+  const uint32_t ra00 = lds_base + swz(col, 2 * half) * 16, ra01 = lds_base + swz(col, 2 * half + 1) * 16;
+  const uint32_t ra10 = lds_base + swz(32 + col, 2 * half) * 16, ra11 = lds_base + swz(32 + col, 2 * half + 1) * 16;
+  const int32_t mrow0 = m0 + 4 * half, mrow1 = m0 + 32 + 4 * half;
+
+  // current block operands (c*) and tile 1's lagging block operands (p*)
+  v4i cbh, cbl, ca0h, ca0l, ca1h, ca1l;
+  v4i pbh, pbl, pa1h, pa1l;
+  auto read_issue = [&](int32_t kb) {
+    switch (kb % kStages) {
+      case 0: read_stage_issue<0 * kStageBytes>(rb0, rb1, ra00, ra01, ra10, ra11, cbh, cbl, ca0h, ca0l, ca1h, ca1l); break;
+      case 1: read_stage_issue<1 * kStageBytes>(rb0, rb1, ra00, ra01, ra10, ra11, cbh, cbl, ca0h, ca0l, ca1h, ca1l); break;
+      case 2: read_stage_issue<2 * kStageBytes>(rb0, rb1, ra00, ra01, ra10, ra11, cbh, cbl, ca0h, ca0l, ca1h, ca1l); break;
+      default: read_stage_issue<3 * kStageBytes>(rb0, rb1, ra00, ra01, ra10, ra11, cbh, cbl, ca0h, ca0l, ca1h, ca1l); break;
+    }
+  };
+
+  for (int32_t s = 0; s < kStages - 1 && s < KB; ++s) issue(s);
+  // block 0: tile 0 opens chunk 0
+  sync_block(0);
+  read_issue(0);
+  read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+  mfma_tile(acc0, ca0h, ca0l, cbh, cbl, true);
+  pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+  // block 1: tile 0 continues chunk 0, tile 1 opens chunk 0 on block 0
+  sync_block(1);
+  read_issue(1);
+  read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+  mfma_tile(acc0, ca0h, ca0l, cbh, cbl, false);
+  mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
+  pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+
+  for (int32_t kb = 2; kb < KB; kb += 2) {
+    // ---- even block kb: tile 0 chunk kb/2-1 ends; tile 1 finishes its chunk on block kb-1
+    sync_block(kb);
+    read_issue(kb);
+    flush_tile<PARTIALS>(acc0, sum0, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+    mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+    interleave_4x16();
+    read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+    mfma_tile(acc0, ca0h, ca0l, cbh, cbl, true);
+    pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+    // ---- odd block kb+1: tile 1 chunk kb/2-1 ends; tile 0 continues
+    sync_block(kb + 1);
+    read_issue(kb + 1);
+    read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+    flush_tile<PARTIALS>(acc1, sum1, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
+    mfma_tile(acc0, ca0h, ca0l, cbh, cbl, false);
+    interleave_4x16();
+    mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
+    pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+  }
+  // tail: tile 0's last chunk ends with block KB-1; tile 1 still owes block KB-1
+  flush_tile<PARTIALS>(acc0, sum0, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+  mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+  interleave_4x16();
+  flush_tile<PARTIALS>(acc1, sum1, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
+
+  // ---- epilogue: scale once, store, max |y|
+  const int32_t e = a.ea->exp + a.eb->exp;
+  uint32_t amax = 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
+      const float y = ldexpf(i == 0 ? sum0[v] : sum1[v], e);
+      if (gvalid && m < a.M) {
+        a.out[obase + (int64_t)m * PQ] = y;
+        amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
+      }
+    }
+  }
+  if (a.so) {
+    __shared__ uint32_t red[kThreads / 64];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
+    if (lane == 0) red[wave] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t b = red[0];
+      for (int i = 1; i < kThreads / 64; ++i) b = max(b, red[i]);
+      if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
+      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+    }
+  }
+}
+
 inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
 
 }  // namespace
@@ -697,6 +924,11 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   if (masked == MK && (partials != nullptr) == PT && chan16 == CH) {                       \
     DFP_LAUNCH(kid, (k_conv_mfma<MK, PT, CH>), grid, dim3(kThreads), 0, st, args);          \
     return DFP_OK;                                                                          \
+  }
+  if (chan16 && g.L == 64 && (p.T % 64) == 0 && p.KB >= 4) {
+    if (partials) DFP_LAUNCH(kid, (k_conv_mfma_skew<true>), grid, dim3(kThreads), 0, st, args);
+    else DFP_LAUNCH(kid, (k_conv_mfma_skew<false>), grid, dim3(kThreads), 0, st, args);
+    return DFP_OK;
   }
   if (chan16) {
     if (!masked && !partials) DFP_LAUNCH(kid, (k_conv_mfma_lds<false, false>), grid, dim3(kThreads), 0, st, args);

@@ -4,7 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "../../include/dfp.h"
+#include "dfp.h"
 
 namespace dfp {
 
