@@ -32,6 +32,7 @@
 // to the running FP32 sum in chunk order; chunk lengths that are not a
 // multiple of 32 run the block once per chunk it overlaps, with the bytes of
 // the other chunks masked to zero.
+#include <algorithm>
 #include <type_traits>
 
 #include "dfp_internal.h"
@@ -838,6 +839,419 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv_mfma_skew(ConvMfmaArgs a) 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Barrier-free variant (L = 64, every chunk full, all filter digits resident).
+// Workgroup = 8 waves, tile 64 output channels x 256 pixels, one workgroup per
+// CU.  The filter digits of the whole reduction (KB blocks x 4 KiB) are copied
+// into LDS once; each wave then streams only its own 32 pixels through a
+// private 4-stage LDS ring with direct-to-LDS loads, so the K loop waits only
+// on the wave's own loads and waves drift freely against each other, which
+// lets one wave's conversions overlap another wave's MFMAs.  Within a wave the
+// two tiles run one block out of phase as in the skewed kernel.
+constexpr int kWaves3 = 8;
+constexpr int kThreads3 = kWaves3 * 64;
+constexpr int kNT3 = kWaves3 * 32;           // pixels per workgroup
+constexpr int kRing3 = 4;                    // B stages per wave
+constexpr int kBStage3 = 2048;               // 32 pixels x 2 halves x 32 B
+constexpr int kARes3Max = 20;                // resident filter blocks (80 KiB)
+constexpr int kLds3 = kARes3Max * kStageA + kWaves3 * kRing3 * kBStage3;
+
+template <int STAGE_OFF>
+__device__ __forceinline__ void read_b_issue(uint32_t b0, uint32_t b1, v4i& bhi, v4i& blo) {
+  asm volatile(
+      "ds_read_b128 %0, %2 offset:%4\n\t"
+      "ds_read_b128 %1, %3 offset:%4"
+      : "=&v"(bhi), "=&v"(blo)
+      : "v"(b0), "v"(b1), "n"(STAGE_OFF)
+      : "memory");
+}
+
+__device__ __forceinline__ void read_a_issue(uint32_t a00, uint32_t a01, uint32_t a10, uint32_t a11, v4i& ahi0,
+                                             v4i& alo0, v4i& ahi1, v4i& alo1) {
+  asm volatile(
+      "ds_read_b128 %0, %4\n\t"
+      "ds_read_b128 %1, %5\n\t"
+      "ds_read_b128 %2, %6\n\t"
+      "ds_read_b128 %3, %7"
+      : "=&v"(ahi0), "=&v"(alo0), "=&v"(ahi1), "=&v"(alo1)
+      : "v"(a00), "v"(a01), "v"(a10), "v"(a11)
+      : "memory");
+}
+
+template <bool PARTIALS>
+__global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_free(ConvMfmaArgs a) {
+  __shared__ __align__(16) uint8_t smem[kLds3];
+  uint8_t* const sA = smem;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int half = lane >> 5;
+  const int col = lane & 31;
+  const int32_t m0 = blockIdx.y * kMT;
+  const int64_t NP = a.NP;
+  const int64_t PQ = (int64_t)a.Po * a.Qo;
+  const int32_t Cin = a.Cin, KB = a.KB;
+  uint8_t* const sB = smem + kARes3Max * kStageA + wave * (kRing3 * kBStage3);
+
+  // ---- all filter blocks of this 64-row tile into LDS (every thread a share)
+  {
+    const int64_t a_block_bytes = (int64_t)a.Mp * 64;
+    const int32_t pieces = KB * 256;  // 16-byte pieces
+    for (int32_t i = threadIdx.x; i < pieces; i += kThreads3) {
+      const int32_t kb = i >> 8, slot = i & 255;
+      const int row = slot >> 2, piece = (slot & 3) ^ ((row >> 2) & 3);
+      const uint4 v = *reinterpret_cast<const uint4*>(a.wsa + kb * a_block_bytes +
+                                                      ((int64_t)(m0 + row) * 2 + (piece >> 1)) * 32 + (piece & 1) * 16);
+      *reinterpret_cast<uint4*>(sA + kb * kStageA + slot * 16) = v;
+    }
+  }
+
+  // ---- this lane's output pixel and its two B load slots
+  const int64_t g = (int64_t)blockIdx.x * kNT3 + wave * 32 + col;
+  const bool gvalid = g < NP;
+  int64_t obase;
+  {
+    const int64_t gg = gvalid ? g : 0;
+    const int32_t qo = (int32_t)(gg % a.Qo), po = (int32_t)((gg / a.Qo) % a.Po);
+    obase = (gg / PQ) * a.M * PQ + (int64_t)po * a.Qo + qo;
+  }
+  const uint8_t* b_src[2];
+  int b_half[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int slot = i * 64 + lane;
+    const int px = slot >> 2, piece = (slot & 3) ^ ((px >> 2) & 3);
+    b_half[i] = piece >> 1;
+    int64_t gp = (int64_t)blockIdx.x * kNT3 + wave * 32 + px;
+    if (gp >= NP) gp = 0;
+    const int32_t qo = (int32_t)(gp % a.Qo), po = (int32_t)((gp / a.Qo) % a.Po);
+    const int64_t im = gp / PQ;
+    b_src[i] = a.xs +
+               (((im * a.Hp + (int64_t)po * a.ustride_h + a.roff_h) * a.Wp + (int64_t)qo * a.ustride_w + a.roff_w) *
+                a.CG) * 32 +
+               (piece & 1) * 16;
+  }
+  const int32_t tap_row_bytes = a.rsign * a.Wp * a.CG * 32;
+  const int32_t tap_col_bytes = a.rsign * a.CG * 32;
+
+  int32_t ld_c = 0, ld_r = 0, ld_s = 0;
+  auto issue = [&](int32_t kb) {
+    uint8_t* st = sB + (kb % kRing3) * kBStage3;
+    const int32_t off0 = ld_r * tap_row_bytes + ld_s * tap_col_bytes + (ld_c >> 4) * 32;
+    int32_t off1;
+    if (ld_c + 16 < Cin) {
+      off1 = off0 + 32;
+    } else {
+      const int32_t s1 = (ld_s + 1 == a.S) ? 0 : ld_s + 1;
+      const int32_t r1 = (ld_s + 1 == a.S) ? ld_r + 1 : ld_r;
+      off1 = r1 * tap_row_bytes + s1 * tap_col_bytes;
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(b_src[i] + (b_half[i] ? off1 : off0)),
+                                       (lds_ptr_t)(st + i * 1024), 16, 0, 0);
+    ld_c += 32;
+    while (ld_c >= Cin) {
+      ld_c -= Cin;
+      if (++ld_s == a.S) { ld_s = 0; ++ld_r; }
+    }
+  };
+  // this wave's block kb has landed (the newer kRing3-2 blocks may be in flight)
+  auto wait_block = [&](int32_t kb) {
+    const int32_t ahead = min(kRing3 - 2, KB - 1 - kb);
+    if (ahead >= 2) wait_vmcnt<4>();
+    else if (ahead == 1) wait_vmcnt<2>();
+    else wait_vmcnt<0>();
+    if (kb + kRing3 - 1 < KB) issue(kb + kRing3 - 1);
+  };
+
+  Acc3 acc0, acc1;
+  float sum0[16], sum1[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    acc0.hh[v] = 0; acc0.xx[v] = 0; acc0.ll[v] = 0;
+    acc1.hh[v] = 0; acc1.xx[v] = 0; acc1.ll[v] = 0;
+    sum0[v] = 0.f; sum1[v] = 0.f;
+  }
+  const uint32_t sA_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sA;
+  const uint32_t sB_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sB;
+  const uint32_t rb0 = sB_base + swz(col, 2 * half) * 16, rb1 = sB_base + swz(col, 2 * half + 1) * 16;
+  const uint32_t ra00 = sA_base + swz(col, 2 * half) * 16, ra01 = sA_base + swz(col, 2 * half + 1) * 16;
+  const uint32_t ra10 = sA_base + swz(32 + col, 2 * half) * 16, ra11 = sA_base + swz(32 + col, 2 * half + 1) * 16;
+  const int32_t mrow0 = m0 + 4 * half, mrow1 = m0 + 32 + 4 * half;
+
+  v4i cbh, cbl, ca0h, ca0l, ca1h, ca1l;  // block kb
+  v4i pbh, pbl, pa1h, pa1l;              // tile 1's lagging block kb-1
+  auto read_block = [&](int32_t kb) {
+    switch (kb % kRing3) {
+      case 0: read_b_issue<0 * kBStage3>(rb0, rb1, cbh, cbl); break;
+      case 1: read_b_issue<1 * kBStage3>(rb0, rb1, cbh, cbl); break;
+      case 2: read_b_issue<2 * kBStage3>(rb0, rb1, cbh, cbl); break;
+      default: read_b_issue<3 * kBStage3>(rb0, rb1, cbh, cbl); break;
+    }
+    const uint32_t ao = (uint32_t)kb * kStageA;
+    read_a_issue(ra00 + ao, ra01 + ao, ra10 + ao, ra11 + ao, ca0h, ca0l, ca1h, ca1l);
+  };
+
+  for (int32_t s = 0; s < kRing3 - 1 && s < KB; ++s) issue(s);
+  __syncthreads();  // filter digits resident
+  // block 0: tile 0 opens chunk 0
+  wait_block(0);
+  read_block(0);
+  read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+  mfma_tile(acc0, ca0h, ca0l, cbh, cbl, true);
+  pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+  // block 1
+  wait_block(1);
+  read_block(1);
+  read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+  mfma_tile(acc0, ca0h, ca0l, cbh, cbl, false);
+  mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
+  pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+
+  for (int32_t kb = 2; kb < KB; kb += 2) {
+    wait_block(kb);
+    read_block(kb);
+    flush_tile<PARTIALS>(acc0, sum0, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+    mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+    interleave_4x16();
+    read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+    mfma_tile(acc0, ca0h, ca0l, cbh, cbl, true);
+    pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+
+    wait_block(kb + 1);
+    read_block(kb + 1);
+    read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+    flush_tile<PARTIALS>(acc1, sum1, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
+    mfma_tile(acc0, ca0h, ca0l, cbh, cbl, false);
+    interleave_4x16();
+    mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
+    pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+  }
+  flush_tile<PARTIALS>(acc0, sum0, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+  mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+  interleave_4x16();
+  flush_tile<PARTIALS>(acc1, sum1, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
+
+  const int32_t e = a.ea->exp + a.eb->exp;
+  uint32_t amax = 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
+      const float y = ldexpf(i == 0 ? sum0[v] : sum1[v], e);
+      if (gvalid && m < a.M) {
+        a.out[obase + (int64_t)m * PQ] = y;
+        amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
+      }
+    }
+  }
+  if (a.so) {
+    __shared__ uint32_t red[kWaves3];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
+    if (lane == 0) red[wave] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t b = red[0];
+      for (int i = 1; i < kWaves3; ++i) b = max(b, red[i]);
+      if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
+      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Persistent barrier-free variant (L = 64, full chunks, filter digits
+// resident).  One workgroup of 8 waves per CU and per 64-row tile; the filter
+// digits of the tile are copied into LDS once with direct-to-LDS loads.  Each
+// wave then walks its own sequence of 32-pixel tiles (wave w of workgroup b
+// takes tiles b*8 + w, b*8 + w + 8*grid, ...).  Its B loads form one stream
+// over (tile, block), so the next tile's first blocks are in flight while the
+// current tile finishes and its outputs are stored.
+template <bool PARTIALS>
+__global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs a) {
+  __shared__ __align__(16) uint8_t smem[kLds3];
+  uint8_t* const sA = smem;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int half = lane >> 5;
+  const int col = lane & 31;
+  const int32_t m0 = blockIdx.y * kMT;
+  const int32_t Cin = a.Cin, KB = a.KB;
+  const int32_t NP = (int32_t)a.NP, Qo = a.Qo;
+  const int32_t PQ = a.Po * a.Qo;
+  uint8_t* const sB = smem + kARes3Max * kStageA + wave * (kRing3 * kBStage3);
+
+  // ---- filter digits of this 64-row tile: KB blocks x 256 pieces of 16 B, direct to LDS
+  {
+    const int64_t a_block_bytes = (int64_t)a.Mp * 64;
+    const int32_t insts = (KB * 256) / 64;  // one instruction fills 64 consecutive slots
+    for (int32_t j = wave; j < insts; j += kWaves3) {
+      const int32_t slot0 = j * 64;
+      const int32_t sl = slot0 + lane;
+      const int32_t kb = sl >> 8, sw = sl & 255;
+      const int row = sw >> 2, piece = (sw & 3) ^ ((row >> 2) & 3);
+      const uint8_t* src = a.wsa + kb * a_block_bytes + ((int64_t)(m0 + row) * 2 + (piece >> 1)) * 32 + (piece & 1) * 16;
+      __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(sA + slot0 * 16), 16, 0, 0);
+    }
+  }
+
+  const int32_t tiles = (NP + 31) / 32;
+  const int32_t tile_stride = gridDim.x * kWaves3;
+  const int32_t first_tile = blockIdx.x * kWaves3 + wave;
+  const int32_t my_tiles = first_tile < tiles ? (tiles - first_tile + tile_stride - 1) / tile_stride : 0;
+  const int32_t total_blocks = my_tiles * KB;
+
+  const int32_t tap_row_bytes = a.rsign * a.Wp * a.CG * 32;
+  const int32_t tap_col_bytes = a.rsign * a.CG * 32;
+  // B load stream state
+  int32_t ld_blk = 0, ld_kb = 0, ld_c = 0, ld_r = 0, ld_s = 0;
+  int32_t b_off[2] = {0, 0};  // byte offsets into xs (< 2^31, checked by the launcher)
+  int b_half[2];
+  int b_px[2], b_piece[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int slot = i * 64 + lane;
+    b_px[i] = slot >> 2;
+    b_piece[i] = (slot & 3) ^ ((b_px[i] >> 2) & 3);
+    b_half[i] = b_piece[i] >> 1;
+  }
+  auto set_b_tile = [&](int32_t tile) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      int32_t gp = tile * 32 + b_px[i];
+      if (gp >= NP) gp = 0;
+      const int32_t qo = gp % Qo, po = (gp / Qo) % a.Po, im = gp / PQ;
+      b_off[i] = (((im * a.Hp + po * a.ustride_h + a.roff_h) * a.Wp + qo * a.ustride_w + a.roff_w) * a.CG) * 32 +
+                 (b_piece[i] & 1) * 16;
+    }
+  };
+  auto issue = [&]() {  // loads block ld_blk of the stream
+    if (ld_kb == 0) {
+      set_b_tile(first_tile + (ld_blk / KB) * tile_stride);
+      ld_c = 0; ld_r = 0; ld_s = 0;
+    }
+    uint8_t* st = sB + (ld_blk % kRing3) * kBStage3;
+    const int32_t off0 = ld_r * tap_row_bytes + ld_s * tap_col_bytes + (ld_c >> 4) * 32;
+    int32_t off1;
+    if (ld_c + 16 < Cin) {
+      off1 = off0 + 32;
+    } else {
+      const int32_t s1 = (ld_s + 1 == a.S) ? 0 : ld_s + 1;
+      const int32_t r1 = (ld_s + 1 == a.S) ? ld_r + 1 : ld_r;
+      off1 = r1 * tap_row_bytes + s1 * tap_col_bytes;
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(a.xs + (uint32_t)(b_off[i] + (b_half[i] ? off1 : off0))),
+                                       (lds_ptr_t)(st + i * 1024), 16, 0, 0);
+    ld_c += 32;
+    while (ld_c >= Cin) {
+      ld_c -= Cin;
+      if (++ld_s == a.S) { ld_s = 0; ++ld_r; }
+    }
+    ++ld_blk;
+    if (++ld_kb == KB) ld_kb = 0;
+  };
+  // stream block gb has landed for this wave (newer blocks may stay in flight)
+  auto wait_block = [&](int32_t gb) {
+    const int32_t ahead = min(kRing3 - 2, total_blocks - 1 - gb);
+    if (ahead >= 2) wait_vmcnt<4>();
+    else if (ahead == 1) wait_vmcnt<2>();
+    else wait_vmcnt<0>();
+    if (ld_blk < total_blocks) issue();
+  };
+
+  const uint32_t sA_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sA;
+  const uint32_t sB_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sB;
+  const uint32_t rb0 = sB_base + swz(col, 2 * half) * 16, rb1 = sB_base + swz(col, 2 * half + 1) * 16;
+  const uint32_t ra00 = sA_base + swz(col, 2 * half) * 16, ra01 = sA_base + swz(col, 2 * half + 1) * 16;
+  const uint32_t ra10 = sA_base + swz(32 + col, 2 * half) * 16, ra11 = sA_base + swz(32 + col, 2 * half + 1) * 16;
+  const int32_t mrow0 = m0 + 4 * half, mrow1 = m0 + 32 + 4 * half;
+  const int32_t e = a.ea->exp + a.eb->exp;
+  uint32_t amax = 0;
+
+  // operand registers of two consecutive blocks (the next block's LDS reads
+  // are in flight while the current block's MFMAs issue)
+  v4i bh[1], bl[1], a0h[1], a0l[1], a1h[1], a1l[1];
+  auto read_block = [&](int32_t gb, int32_t kb, int r) {
+    switch (gb % kRing3) {
+      case 0: read_b_issue<0 * kBStage3>(rb0, rb1, bh[r], bl[r]); break;
+      case 1: read_b_issue<1 * kBStage3>(rb0, rb1, bh[r], bl[r]); break;
+      case 2: read_b_issue<2 * kBStage3>(rb0, rb1, bh[r], bl[r]); break;
+      default: read_b_issue<3 * kBStage3>(rb0, rb1, bh[r], bl[r]); break;
+    }
+    const uint32_t ao = (uint32_t)kb * kStageA;
+    read_a_issue(ra00 + ao, ra01 + ao, ra10 + ao, ra11 + ao, a0h[r], a0l[r], a1h[r], a1l[r]);
+  };
+  auto read_wait = [&](int r) { read_stage_wait(bh[r], bl[r], a0h[r], a0l[r], a1h[r], a1l[r]); };
+
+  while (ld_blk < min(kRing3 - 1, total_blocks)) issue();
+  wait_vmcnt<0>();  // filter digits (and the first B blocks) landed for this lane
+  __syncthreads();  // ... and for every lane
+
+  for (int32_t it = 0; it < my_tiles; ++it) {
+    const int32_t gb0 = it * KB;
+    const int32_t g = (first_tile + it * tile_stride) * 32 + col;
+    const bool gvalid = g < NP;
+    int32_t obase;  // < 2^31 output elements (checked by the launcher)
+    {
+      const int32_t gg = gvalid ? g : 0;
+      obase = (gg / PQ) * a.M * PQ + (gg % PQ);
+    }
+    Acc3 acc0, acc1;
+    float sum0[16], sum1[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) { sum0[v] = 0.f; sum1[v] = 0.f; }
+
+    for (int32_t kb = 0; kb < KB; kb += 2) {
+      // block kb opens chunk kb/2; block kb+1 closes it
+      wait_block(gb0 + kb);
+      read_block(gb0 + kb, kb, 0);
+      read_wait(0);
+      mfma_tile(acc0, a0h[0], a0l[0], bh[0], bl[0], true);
+      mfma_tile(acc1, a1h[0], a1l[0], bh[0], bl[0], true);
+      wait_block(gb0 + kb + 1);
+      read_block(gb0 + kb + 1, kb + 1, 0);
+      read_wait(0);
+      mfma_tile(acc0, a0h[0], a0l[0], bh[0], bl[0], false);
+      mfma_tile(acc1, a1h[0], a1l[0], bh[0], bl[0], false);
+      flush_tile<PARTIALS>(acc0, sum0, kb / 2, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+      flush_tile<PARTIALS>(acc1, sum1, kb / 2, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
+    }
+
+    // ---- outputs of this tile (the stores drain while the next tile computes)
+    float* outp = a.out + obase;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
+        const float y = ldexpf(i == 0 ? sum0[v] : sum1[v], e);
+        if (gvalid && m < a.M) {
+          outp[(uint32_t)(m * PQ)] = y;
+          amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
+        }
+      }
+    }
+  }
+
+  if (a.so) {
+    __shared__ uint32_t red[kWaves3];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
+    if (lane == 0) red[wave] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t b = red[0];
+      for (int i = 1; i < kWaves3; ++i) b = max(b, red[i]);
+      if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
+      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+    }
+  }
+}
+
 inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
 
 }  // namespace
@@ -924,6 +1338,20 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   if (masked == MK && (partials != nullptr) == PT && chan16 == CH) {                       \
     DFP_LAUNCH(kid, (k_conv_mfma<MK, PT, CH>), grid, dim3(kThreads), 0, st, args);          \
     return DFP_OK;                                                                          \
+  }
+  if (chan16 && g.L == 64 && (p.T % 64) == 0 && p.KB >= 4 && p.KB <= kARes3Max && args.O < (1ll << 31) &&
+      p.ws_b_bytes < (1ll << 31)) {
+    // one workgroup per CU for each 64-row tile of the output channels
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    const int64_t wave_tiles = (args.NP + 31) / 32;
+    const int64_t mtiles = p.Mp / kMT;
+    int64_t gx = std::max<int64_t>(1, cus / mtiles);
+    gx = std::min<int64_t>(gx, (wave_tiles + kWaves3 - 1) / kWaves3);
+    const dim3 grid3((unsigned)gx, (unsigned)mtiles);
+    if (partials) DFP_LAUNCH(kid, (k_conv_mfma_persist<true>), grid3, dim3(kThreads3), 0, st, args);
+    else DFP_LAUNCH(kid, (k_conv_mfma_persist<false>), grid3, dim3(kThreads3), 0, st, args);
+    return DFP_OK;
   }
   if (chan16 && g.L == 64 && (p.T % 64) == 0 && p.KB >= 4) {
     if (partials) DFP_LAUNCH(kid, (k_conv_mfma_skew<true>), grid, dim3(kThreads), 0, st, args);
