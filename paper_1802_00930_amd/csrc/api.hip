@@ -215,11 +215,12 @@ static dfp_status conv_common(int32_t dir, const dfp_desc* d, const int16_t* a, 
   if ((rc = ws_check(g, dir, d->path, d->bits, ws, ws_bytes)) != DFP_OK) return rc;
   if (so && !aligned(so, 16)) return DFP_ERR_ALIGN;
   hipStream_t st = (hipStream_t)stream;
-  if (so && (rc = launch_scale_reset(so, st)) != DFP_OK) return rc;
   if (use_mfma(g, d->path, d->bits, dir)) {
     if (dir == DFP_BWD_WT) return launch_bwdw_mfma(g, a, sa, b, sb, out, partials, ws, st);
+    // the filter prep kernel clears so before the main kernel raises it
     return launch_conv_mfma(dir, g, a, sa, b, sb, out, so, partials, ws, st);
   }
+  if (so && (rc = launch_scale_reset(so, st)) != DFP_OK) return rc;
   return launch_conv_valu(dir, g, a, sa, b, sb, out, so, partials, st);
 }
 

@@ -10,12 +10,13 @@ struct ConvMfmaPlan {
   int32_t M, Mp, Cin, T, KB, CG;   // output channels (padded), reduction channels, T, 32-blocks, 16-groups
   int32_t Hp, Wp, top, left, dil_h, dil_w;  // channels-last digit tensor geometry
   int32_t Po, Qo;                  // output spatial size
-  int64_t ws_a_bytes, ws_b_bytes, bytes;
+  int64_t ws_a_bytes, ws_b_bytes, ws_t_bytes, bytes;
 };
 
 struct ConvMfmaArgs {
   const uint8_t* xs;    // B digits [n][Hp][Wp][CG][32]
   const uint8_t* wsa;   // A digits [KB][Mp][2][32]
+  const int2* boff;     // per block: byte offsets into xs of its two 16-channel halves (tap and group)
   const dfp_scale* ea;  // exponent of the B-source tensor
   const dfp_scale* eb;  // exponent of the filter
   float* out;

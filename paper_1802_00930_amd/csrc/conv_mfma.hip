@@ -58,8 +58,26 @@ __device__ __forceinline__ uint32_t lo_digit(int32_t a) { return (uint32_t)a & 0
 // bwd-data: m = c, ci = k, value w[ci][m][r][s].
 __global__ __launch_bounds__(256) void k_prep_a(const int16_t* __restrict__ w, uint8_t* __restrict__ ws,
                                                int32_t M, int32_t Mp, int32_t Cin, int32_t R, int32_t S,
-                                               int32_t T, int32_t KB, int32_t transposed, int32_t Cw) {
+                                               int32_t T, int32_t KB, int32_t transposed, int32_t Cw,
+                                               dfp_scale* so, int2* boff, int32_t tap_row_bytes,
+                                               int32_t tap_col_bytes) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (kb, m, half)
+  if (so && idx == 0) {  // the output scale starts empty; the conv epilogue raises its max
+    so->amax_bits = 0u;
+    so->flags = 0u;
+  }
+  if (idx < KB) {
+    // block idx covers t0 .. t0+31; each 16-index half is one channel group of one tap
+    // (Cin is a multiple of 16 wherever the table is read); indices past T read offset 0
+    int32_t o[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int32_t t = (int32_t)idx * 32 + 16 * h;
+      const int32_t tap = t / Cin, ci = t % Cin;
+      o[h] = t < T ? (tap / S) * tap_row_bytes + (tap % S) * tap_col_bytes + (ci >> 4) * 32 : 0;
+    }
+    boff[idx] = make_int2(o[0], o[1]);
+  }
   const int64_t total = (int64_t)KB * Mp * 2;
   if (idx >= total) return;
   const int32_t half = (int32_t)(idx & 1);
@@ -614,6 +632,186 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv_mfma_lds(ConvMfmaArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Four-waves-per-SIMD variant for chunk lengths that are multiples of 32 (no
+// masking).  Workgroup = 8 waves, tile 64 output channels x 128 pixels, two
+// workgroups per CU.  Each wave owns one 32 x 32 output tile: three
+// accumulators, 16 running sums and one block of operands stay under 128
+// VGPRs, so every SIMD holds four waves and one wave's chunk conversion
+// (VALU) runs while the other waves issue MFMAs and LDS reads.  Operands pass
+// through the same 4-stage LDS ring as above (waves 0-3 load the filter
+// digits, every lane one B piece), one barrier per block.
+constexpr int kWavesQ = 8;
+constexpr int kThreadsQ = kWavesQ * 64;
+
+// The four operand reads of one block for a single 32 x 32 tile, then a wait.
+template <int STAGE_OFF>
+__device__ __forceinline__ void read_stage_q(uint32_t b0, uint32_t b1, uint32_t a0, uint32_t a1, v4i& bhi,
+                                             v4i& blo, v4i& ahi, v4i& alo) {
+  asm volatile(
+      "ds_read_b128 %0, %4 offset:%8\n\t"
+      "ds_read_b128 %1, %5 offset:%8\n\t"
+      "ds_read_b128 %2, %6 offset:%8\n\t"
+      "ds_read_b128 %3, %7 offset:%8\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(bhi), "=&v"(blo), "=&v"(ahi), "=&v"(alo)
+      : "v"(b0), "v"(b1), "v"(a0), "v"(a1), "n"(STAGE_OFF)
+      : "memory");
+}
+
+// Workgroup ids are dispatched to the 8 XCDs in turn (id mod 8), each XCD
+// with its own L2.  Map the ids of one XCD to a contiguous range of tiles,
+// with the row tiles (blockIdx.y) of one pixel tile adjacent, so each L2 holds
+// its own share of the input rows and the filter digits.
+__device__ __forceinline__ void xcd_tile(int32_t& tx, int32_t& ty) {
+  const int32_t nbx = gridDim.x, nby = gridDim.y, total = nbx * nby;
+  const int32_t lin = blockIdx.y * nbx + blockIdx.x;
+  const int32_t x = lin & 7, q = total >> 3, r = total & 7;
+  const int32_t t = x * q + min(x, r) + (lin >> 3);
+  ty = t % nby;
+  tx = t / nby;
+}
+
+template <bool PARTIALS>
+__global__ __launch_bounds__(kThreadsQ, 4) void k_conv_mfma_q(ConvMfmaArgs a) {
+  __shared__ __align__(16) uint8_t smem[kStages * kStageBytes];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int half = lane >> 5;
+  const int col = lane & 31;
+  const int wm = wave & 1, wp = wave >> 1;  // 32-row and 32-pixel sub-tile of this wave
+  int32_t tx, ty;
+  xcd_tile(tx, ty);
+  const int32_t m0 = ty * kMT;
+  // the launcher guarantees outputs and the B workspace index below 2^31
+  const int32_t NP = (int32_t)a.NP;
+  const int32_t PQ = a.Po * a.Qo;
+
+  // ---- output pixel of this lane (MFMA column)
+  const int32_t g = tx * kNT + wp * 32 + col;
+  const bool gvalid = g < NP;
+  int32_t obase;
+  {
+    const int32_t gg = gvalid ? g : 0;
+    obase = (gg / PQ) * a.M * PQ + (gg % PQ);
+  }
+
+  // ---- load assignments: A slot tid (waves 0-3 only), B slot tid
+  const bool loads_a = wave_u < 4;
+  const int a_slot = threadIdx.x & 255;
+  const int a_row = a_slot >> 2, a_piece = (a_slot & 3) ^ ((a_row >> 2) & 3);
+  const uint32_t a_voff = (uint32_t)(((m0 + a_row) * 2 + (a_piece >> 1)) * 32 + (a_piece & 1) * 16);
+  const int64_t a_block_bytes = (int64_t)a.Mp * 64;
+  int32_t b_voff;
+  bool b_upper;
+  {
+    const int slot = threadIdx.x;
+    const int px = slot >> 2, piece = (slot & 3) ^ ((px >> 2) & 3);
+    b_upper = (piece >> 1) != 0;
+    int32_t gp = tx * kNT + px;
+    if (gp >= NP) gp = 0;
+    const int32_t qo = gp % a.Qo, po = (gp / a.Qo) % a.Po, im = gp / PQ;
+    b_voff = ((im * a.Hp + po * a.ustride_h + a.roff_h) * a.Wp + qo * a.ustride_w + a.roff_w) * a.CG * 32 +
+             (piece & 1) * 16;
+  }
+  const int32_t KB = a.KB;
+
+  auto issue = [&](int32_t kb) {
+    uint8_t* st = smem + (kb % kStages) * kStageBytes;
+    if (loads_a)
+      __builtin_amdgcn_global_load_lds((const void*)(a.wsa + kb * a_block_bytes + a_voff),
+                                       (lds_ptr_t)(st + wave_u * 1024), 16, 0, 0);
+    const int2 o = a.boff[kb];
+    __builtin_amdgcn_global_load_lds((const void*)(a.xs + (uint32_t)(b_voff + (b_upper ? o.y : o.x))),
+                                     (lds_ptr_t)(st + kStageA + wave_u * 1024), 16, 0, 0);
+  };
+
+  Acc3 acc;
+  float sum[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    acc.hh[v] = 0; acc.xx[v] = 0; acc.ll[v] = 0;
+    sum[v] = 0.f;
+  }
+
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)smem;
+  const uint32_t rb0 = lds_base + kStageA + swz(wp * 32 + col, 2 * half) * 16;
+  const uint32_t rb1 = lds_base + kStageA + swz(wp * 32 + col, 2 * half + 1) * 16;
+  const uint32_t ra0 = lds_base + swz(wm * 32 + col, 2 * half) * 16;
+  const uint32_t ra1 = lds_base + swz(wm * 32 + col, 2 * half + 1) * 16;
+  const int32_t mrow0 = m0 + wm * 32 + 4 * half;
+
+  int64_t j = 0;
+  int32_t blk_in_chunk = 0;
+  const int32_t chunk_blocks = a.L / 32;
+
+  // One block: wait for its loads (the two newer blocks may stay in flight:
+  // two loads each in waves 0-3, one in waves 4-7), barrier, refill the slot
+  // freed by the previous block, read and consume.
+  auto step = [&](int32_t kb, auto stage_tag) {
+    constexpr int STAGE = decltype(stage_tag)::value;
+    const int32_t ahead = min(kStages - 2, KB - 1 - kb);
+    if (loads_a) {
+      if (ahead >= 2) wait_vmcnt<4>();
+      else if (ahead == 1) wait_vmcnt<2>();
+      else wait_vmcnt<0>();
+    } else {
+      if (ahead >= 2) wait_vmcnt<2>();
+      else if (ahead == 1) wait_vmcnt<1>();
+      else wait_vmcnt<0>();
+    }
+    __builtin_amdgcn_s_barrier();
+    if (kb + kStages - 1 < KB) issue(kb + kStages - 1);
+    v4i bhi, blo, ahi, alo;
+    read_stage_q<STAGE * kStageBytes>(rb0, rb1, ra0, ra1, bhi, blo, ahi, alo);
+    mfma_tile(acc, ahi, alo, bhi, blo, blk_in_chunk == 0);
+    if (++blk_in_chunk == chunk_blocks || kb == KB - 1) {
+      flush_tile<PARTIALS>(acc, sum, j, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+      ++j;
+      blk_in_chunk = 0;
+    }
+  };
+
+  for (int32_t s = 0; s < kStages - 1 && s < KB; ++s) issue(s);
+  int32_t kb = 0;
+  for (; kb + kStages <= KB; kb += kStages) {
+    step(kb + 0, std::integral_constant<int, 0>{});
+    step(kb + 1, std::integral_constant<int, 1>{});
+    step(kb + 2, std::integral_constant<int, 2>{});
+    step(kb + 3, std::integral_constant<int, 3>{});
+  }
+  if (kb < KB) step(kb++, std::integral_constant<int, 0>{});
+  if (kb < KB) step(kb++, std::integral_constant<int, 1>{});
+  if (kb < KB) step(kb++, std::integral_constant<int, 2>{});
+
+  // ---- epilogue: scale once, store, max |y|
+  const int32_t e = a.ea->exp + a.eb->exp;
+  uint32_t amax = 0;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
+    const float y = ldexpf(sum[v], e);
+    if (gvalid && m < a.M) {
+      a.out[(uint32_t)(obase + m * PQ)] = y;
+      amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
+    }
+  }
+  if (a.so) {
+    __shared__ uint32_t red[kWavesQ];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
+    if (lane == 0) red[wave] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t b = red[0];
+      for (int i = 1; i < kWavesQ; ++i) b = max(b, red[i]);
+      if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
+      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Skewed variant for chunks of exactly two blocks (L = 64) when every chunk is
 // full (T a multiple of 64).  At L = 64 a chunk's conversion costs as many VALU
 // cycles as its MFMAs, so the two 32-row tiles of a wave run one block out of
@@ -839,15 +1037,6 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv_mfma_skew(ConvMfmaArgs a) 
   }
 }
 
-// ---------------------------------------------------------------------------
-// Barrier-free variant (L = 64, every chunk full, all filter digits resident).
-// Workgroup = 8 waves, tile 64 output channels x 256 pixels, one workgroup per
-// CU.  The filter digits of the whole reduction (KB blocks x 4 KiB) are copied
-// into LDS once; each wave then streams only its own 32 pixels through a
-// private 4-stage LDS ring with direct-to-LDS loads, so the K loop waits only
-// on the wave's own loads and waves drift freely against each other, which
-// lets one wave's conversions overlap another wave's MFMAs.  Within a wave the
-// two tiles run one block out of phase as in the skewed kernel.
 constexpr int kWaves3 = 8;
 constexpr int kThreads3 = kWaves3 * 64;
 constexpr int kNT3 = kWaves3 * 32;           // pixels per workgroup
@@ -878,216 +1067,40 @@ __device__ __forceinline__ void read_a_issue(uint32_t a00, uint32_t a01, uint32_
       : "memory");
 }
 
-template <bool PARTIALS>
-__global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_free(ConvMfmaArgs a) {
-  __shared__ __align__(16) uint8_t smem[kLds3];
-  uint8_t* const sA = smem;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int half = lane >> 5;
-  const int col = lane & 31;
-  const int32_t m0 = blockIdx.y * kMT;
-  const int64_t NP = a.NP;
-  const int64_t PQ = (int64_t)a.Po * a.Qo;
-  const int32_t Cin = a.Cin, KB = a.KB;
-  uint8_t* const sB = smem + kARes3Max * kStageA + wave * (kRing3 * kBStage3);
-
-  // ---- all filter blocks of this 64-row tile into LDS (every thread a share)
-  {
-    const int64_t a_block_bytes = (int64_t)a.Mp * 64;
-    const int32_t pieces = KB * 256;  // 16-byte pieces
-    for (int32_t i = threadIdx.x; i < pieces; i += kThreads3) {
-      const int32_t kb = i >> 8, slot = i & 255;
-      const int row = slot >> 2, piece = (slot & 3) ^ ((row >> 2) & 3);
-      const uint4 v = *reinterpret_cast<const uint4*>(a.wsa + kb * a_block_bytes +
-                                                      ((int64_t)(m0 + row) * 2 + (piece >> 1)) * 32 + (piece & 1) * 16);
-      *reinterpret_cast<uint4*>(sA + kb * kStageA + slot * 16) = v;
-    }
-  }
-
-  // ---- this lane's output pixel and its two B load slots
-  const int64_t g = (int64_t)blockIdx.x * kNT3 + wave * 32 + col;
-  const bool gvalid = g < NP;
-  int64_t obase;
-  {
-    const int64_t gg = gvalid ? g : 0;
-    const int32_t qo = (int32_t)(gg % a.Qo), po = (int32_t)((gg / a.Qo) % a.Po);
-    obase = (gg / PQ) * a.M * PQ + (int64_t)po * a.Qo + qo;
-  }
-  const uint8_t* b_src[2];
-  int b_half[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int slot = i * 64 + lane;
-    const int px = slot >> 2, piece = (slot & 3) ^ ((px >> 2) & 3);
-    b_half[i] = piece >> 1;
-    int64_t gp = (int64_t)blockIdx.x * kNT3 + wave * 32 + px;
-    if (gp >= NP) gp = 0;
-    const int32_t qo = (int32_t)(gp % a.Qo), po = (int32_t)((gp / a.Qo) % a.Po);
-    const int64_t im = gp / PQ;
-    b_src[i] = a.xs +
-               (((im * a.Hp + (int64_t)po * a.ustride_h + a.roff_h) * a.Wp + (int64_t)qo * a.ustride_w + a.roff_w) *
-                a.CG) * 32 +
-               (piece & 1) * 16;
-  }
-  const int32_t tap_row_bytes = a.rsign * a.Wp * a.CG * 32;
-  const int32_t tap_col_bytes = a.rsign * a.CG * 32;
-
-  int32_t ld_c = 0, ld_r = 0, ld_s = 0;
-  auto issue = [&](int32_t kb) {
-    uint8_t* st = sB + (kb % kRing3) * kBStage3;
-    const int32_t off0 = ld_r * tap_row_bytes + ld_s * tap_col_bytes + (ld_c >> 4) * 32;
-    int32_t off1;
-    if (ld_c + 16 < Cin) {
-      off1 = off0 + 32;
-    } else {
-      const int32_t s1 = (ld_s + 1 == a.S) ? 0 : ld_s + 1;
-      const int32_t r1 = (ld_s + 1 == a.S) ? ld_r + 1 : ld_r;
-      off1 = r1 * tap_row_bytes + s1 * tap_col_bytes;
-    }
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(b_src[i] + (b_half[i] ? off1 : off0)),
-                                       (lds_ptr_t)(st + i * 1024), 16, 0, 0);
-    ld_c += 32;
-    while (ld_c >= Cin) {
-      ld_c -= Cin;
-      if (++ld_s == a.S) { ld_s = 0; ++ld_r; }
-    }
-  };
-  // this wave's block kb has landed (the newer kRing3-2 blocks may be in flight)
-  auto wait_block = [&](int32_t kb) {
-    const int32_t ahead = min(kRing3 - 2, KB - 1 - kb);
-    if (ahead >= 2) wait_vmcnt<4>();
-    else if (ahead == 1) wait_vmcnt<2>();
-    else wait_vmcnt<0>();
-    if (kb + kRing3 - 1 < KB) issue(kb + kRing3 - 1);
-  };
-
-  Acc3 acc0, acc1;
-  float sum0[16], sum1[16];
-#pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    acc0.hh[v] = 0; acc0.xx[v] = 0; acc0.ll[v] = 0;
-    acc1.hh[v] = 0; acc1.xx[v] = 0; acc1.ll[v] = 0;
-    sum0[v] = 0.f; sum1[v] = 0.f;
-  }
-  const uint32_t sA_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sA;
-  const uint32_t sB_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sB;
-  const uint32_t rb0 = sB_base + swz(col, 2 * half) * 16, rb1 = sB_base + swz(col, 2 * half + 1) * 16;
-  const uint32_t ra00 = sA_base + swz(col, 2 * half) * 16, ra01 = sA_base + swz(col, 2 * half + 1) * 16;
-  const uint32_t ra10 = sA_base + swz(32 + col, 2 * half) * 16, ra11 = sA_base + swz(32 + col, 2 * half + 1) * 16;
-  const int32_t mrow0 = m0 + 4 * half, mrow1 = m0 + 32 + 4 * half;
-
-  v4i cbh, cbl, ca0h, ca0l, ca1h, ca1l;  // block kb
-  v4i pbh, pbl, pa1h, pa1l;              // tile 1's lagging block kb-1
-  auto read_block = [&](int32_t kb) {
-    switch (kb % kRing3) {
-      case 0: read_b_issue<0 * kBStage3>(rb0, rb1, cbh, cbl); break;
-      case 1: read_b_issue<1 * kBStage3>(rb0, rb1, cbh, cbl); break;
-      case 2: read_b_issue<2 * kBStage3>(rb0, rb1, cbh, cbl); break;
-      default: read_b_issue<3 * kBStage3>(rb0, rb1, cbh, cbl); break;
-    }
-    const uint32_t ao = (uint32_t)kb * kStageA;
-    read_a_issue(ra00 + ao, ra01 + ao, ra10 + ao, ra11 + ao, ca0h, ca0l, ca1h, ca1l);
-  };
-
-  for (int32_t s = 0; s < kRing3 - 1 && s < KB; ++s) issue(s);
-  __syncthreads();  // filter digits resident
-  // block 0: tile 0 opens chunk 0
-  wait_block(0);
-  read_block(0);
-  read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
-  mfma_tile(acc0, ca0h, ca0l, cbh, cbl, true);
-  pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
-  // block 1
-  wait_block(1);
-  read_block(1);
-  read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
-  mfma_tile(acc0, ca0h, ca0l, cbh, cbl, false);
-  mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
-  pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
-
-  for (int32_t kb = 2; kb < KB; kb += 2) {
-    wait_block(kb);
-    read_block(kb);
-    flush_tile<PARTIALS>(acc0, sum0, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
-    mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
-    interleave_4x16();
-    read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
-    mfma_tile(acc0, ca0h, ca0l, cbh, cbl, true);
-    pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
-
-    wait_block(kb + 1);
-    read_block(kb + 1);
-    read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
-    flush_tile<PARTIALS>(acc1, sum1, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
-    mfma_tile(acc0, ca0h, ca0l, cbh, cbl, false);
-    interleave_4x16();
-    mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
-    pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
-  }
-  flush_tile<PARTIALS>(acc0, sum0, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
-  mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
-  interleave_4x16();
-  flush_tile<PARTIALS>(acc1, sum1, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
-
-  const int32_t e = a.ea->exp + a.eb->exp;
-  uint32_t amax = 0;
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
-      const float y = ldexpf(i == 0 ? sum0[v] : sum1[v], e);
-      if (gvalid && m < a.M) {
-        a.out[obase + (int64_t)m * PQ] = y;
-        amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
-      }
-    }
-  }
-  if (a.so) {
-    __shared__ uint32_t red[kWaves3];
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
-    if (lane == 0) red[wave] = amax;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      uint32_t b = red[0];
-      for (int i = 1; i < kWaves3; ++i) b = max(b, red[i]);
-      if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
-      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
-    }
-  }
-}
-
 // ---------------------------------------------------------------------------
 // Persistent barrier-free variant (L = 64, full chunks, filter digits
 // resident).  One workgroup of 8 waves per CU and per 64-row tile; the filter
 // digits of the tile are copied into LDS once with direct-to-LDS loads.  Each
 // wave then walks its own sequence of 32-pixel tiles (wave w of workgroup b
 // takes tiles b*8 + w, b*8 + w + 8*grid, ...).  Its B loads form one stream
-// over (tile, block), so the next tile's first blocks are in flight while the
-// current tile finishes and its outputs are stored.
+// over (tile, block) through a private 4-slot LDS ring, two blocks ahead, so
+// the next tile's first blocks are in flight while the current tile finishes
+// and stores its outputs.  Within a tile the two 32-row sub-tiles run one
+// block out of phase (tile 1 consumes block kb-1 while tile 0 consumes block
+// kb), so each chunk conversion of one sub-tile is interleaved with the other
+// sub-tile's MFMAs; the operand reads of a block are in flight during the
+// other sub-tile's MFMAs on the lagging block.
 template <bool PARTIALS>
 __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs a) {
   __shared__ __align__(16) uint8_t smem[kLds3];
   uint8_t* const sA = smem;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int half = lane >> 5;
   const int col = lane & 31;
   const int32_t m0 = blockIdx.y * kMT;
   const int32_t Cin = a.Cin, KB = a.KB;
+  // the launcher guarantees outputs and the B workspace index below 2^31
   const int32_t NP = (int32_t)a.NP, Qo = a.Qo;
   const int32_t PQ = a.Po * a.Qo;
-  uint8_t* const sB = smem + kARes3Max * kStageA + wave * (kRing3 * kBStage3);
+  uint8_t* const sB = smem + kARes3Max * kStageA + wave_u * (kRing3 * kBStage3);
 
   // ---- filter digits of this 64-row tile: KB blocks x 256 pieces of 16 B, direct to LDS
   {
     const int64_t a_block_bytes = (int64_t)a.Mp * 64;
     const int32_t insts = (KB * 256) / 64;  // one instruction fills 64 consecutive slots
-    for (int32_t j = wave; j < insts; j += kWaves3) {
+    for (int32_t j = wave_u; j < insts; j += kWaves3) {
       const int32_t slot0 = j * 64;
       const int32_t sl = slot0 + lane;
       const int32_t kb = sl >> 8, sw = sl & 255;
@@ -1099,37 +1112,32 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
 
   const int32_t tiles = (NP + 31) / 32;
   const int32_t tile_stride = gridDim.x * kWaves3;
-  const int32_t first_tile = blockIdx.x * kWaves3 + wave;
+  const int32_t first_tile = blockIdx.x * kWaves3 + wave_u;
   const int32_t my_tiles = first_tile < tiles ? (tiles - first_tile + tile_stride - 1) / tile_stride : 0;
   const int32_t total_blocks = my_tiles * KB;
 
   const int32_t tap_row_bytes = a.rsign * a.Wp * a.CG * 32;
   const int32_t tap_col_bytes = a.rsign * a.CG * 32;
-  // B load stream state
+  // B load stream (uniform) and this lane's two pixel offsets into xs
   int32_t ld_blk = 0, ld_kb = 0, ld_c = 0, ld_r = 0, ld_s = 0;
-  int32_t b_off[2] = {0, 0};  // byte offsets into xs (< 2^31, checked by the launcher)
-  int b_half[2];
-  int b_px[2], b_piece[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  int32_t b_off0 = 0, b_off1 = 0;
+  auto pixel_off = [&](int32_t tile, int i) {
     const int slot = i * 64 + lane;
-    b_px[i] = slot >> 2;
-    b_piece[i] = (slot & 3) ^ ((b_px[i] >> 2) & 3);
-    b_half[i] = b_piece[i] >> 1;
-  }
-  auto set_b_tile = [&](int32_t tile) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      int32_t gp = tile * 32 + b_px[i];
-      if (gp >= NP) gp = 0;
-      const int32_t qo = gp % Qo, po = (gp / Qo) % a.Po, im = gp / PQ;
-      b_off[i] = (((im * a.Hp + po * a.ustride_h + a.roff_h) * a.Wp + qo * a.ustride_w + a.roff_w) * a.CG) * 32 +
-                 (b_piece[i] & 1) * 16;
-    }
+    const int px = slot >> 2, piece = (slot & 3) ^ ((px >> 2) & 3);
+    int32_t gp = tile * 32 + px;
+    if (gp >= NP) gp = 0;
+    const int32_t qo = gp % Qo, po = (gp / Qo) % a.Po, im = gp / PQ;
+    return ((im * a.Hp + po * a.ustride_h + a.roff_h) * a.Wp + qo * a.ustride_w + a.roff_w) * a.CG * 32 +
+           (piece & 1) * 16;
   };
+  // slot i*64 + lane holds channel half ((slot & 3) ^ ((px >> 2) & 3)) >> 1 of pixel slot >> 2
+  const bool up0 = (((lane & 3) ^ ((lane >> 4) & 3)) >> 1) != 0;
+  const bool up1 = (((lane & 3) ^ (((64 + lane) >> 4) & 3)) >> 1) != 0;
   auto issue = [&]() {  // loads block ld_blk of the stream
     if (ld_kb == 0) {
-      set_b_tile(first_tile + (ld_blk / KB) * tile_stride);
+      const int32_t tile = first_tile + (ld_blk / KB) * tile_stride;
+      b_off0 = pixel_off(tile, 0);
+      b_off1 = pixel_off(tile, 1);
       ld_c = 0; ld_r = 0; ld_s = 0;
     }
     uint8_t* st = sB + (ld_blk % kRing3) * kBStage3;
@@ -1142,10 +1150,10 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
       const int32_t r1 = (ld_s + 1 == a.S) ? ld_r + 1 : ld_r;
       off1 = r1 * tap_row_bytes + s1 * tap_col_bytes;
     }
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(a.xs + (uint32_t)(b_off[i] + (b_half[i] ? off1 : off0))),
-                                       (lds_ptr_t)(st + i * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(a.xs + (uint32_t)(b_off0 + (up0 ? off1 : off0))), (lds_ptr_t)(st),
+                                     16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(a.xs + (uint32_t)(b_off1 + (up1 ? off1 : off0))),
+                                     (lds_ptr_t)(st + 1024), 16, 0, 0);
     ld_c += 32;
     while (ld_c >= Cin) {
       ld_c -= Cin;
@@ -1154,7 +1162,7 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
     ++ld_blk;
     if (++ld_kb == KB) ld_kb = 0;
   };
-  // stream block gb has landed for this wave (newer blocks may stay in flight)
+  // stream block gb has landed for this wave (the newer ones may stay in flight); refill
   auto wait_block = [&](int32_t gb) {
     const int32_t ahead = min(kRing3 - 2, total_blocks - 1 - gb);
     if (ahead >= 2) wait_vmcnt<4>();
@@ -1166,26 +1174,23 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
   const uint32_t sA_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sA;
   const uint32_t sB_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sB;
   const uint32_t rb0 = sB_base + swz(col, 2 * half) * 16, rb1 = sB_base + swz(col, 2 * half + 1) * 16;
+  // rows 32..63 sit 2048 bytes after rows 0..31 at the same swizzle position
   const uint32_t ra00 = sA_base + swz(col, 2 * half) * 16, ra01 = sA_base + swz(col, 2 * half + 1) * 16;
-  const uint32_t ra10 = sA_base + swz(32 + col, 2 * half) * 16, ra11 = sA_base + swz(32 + col, 2 * half + 1) * 16;
-  const int32_t mrow0 = m0 + 4 * half, mrow1 = m0 + 32 + 4 * half;
   const int32_t e = a.ea->exp + a.eb->exp;
   uint32_t amax = 0;
 
-  // operand registers of two consecutive blocks (the next block's LDS reads
-  // are in flight while the current block's MFMAs issue)
-  v4i bh[1], bl[1], a0h[1], a0l[1], a1h[1], a1l[1];
-  auto read_block = [&](int32_t gb, int32_t kb, int r) {
+  v4i cbh, cbl, ca0h, ca0l, ca1h, ca1l;  // block kb
+  v4i pbh, pbl, pa1h, pa1l;              // tile 1's lagging block kb-1
+  auto read_block = [&](int32_t gb, int32_t kb) {
     switch (gb % kRing3) {
-      case 0: read_b_issue<0 * kBStage3>(rb0, rb1, bh[r], bl[r]); break;
-      case 1: read_b_issue<1 * kBStage3>(rb0, rb1, bh[r], bl[r]); break;
-      case 2: read_b_issue<2 * kBStage3>(rb0, rb1, bh[r], bl[r]); break;
-      default: read_b_issue<3 * kBStage3>(rb0, rb1, bh[r], bl[r]); break;
+      case 0: read_b_issue<0 * kBStage3>(rb0, rb1, cbh, cbl); break;
+      case 1: read_b_issue<1 * kBStage3>(rb0, rb1, cbh, cbl); break;
+      case 2: read_b_issue<2 * kBStage3>(rb0, rb1, cbh, cbl); break;
+      default: read_b_issue<3 * kBStage3>(rb0, rb1, cbh, cbl); break;
     }
     const uint32_t ao = (uint32_t)kb * kStageA;
-    read_a_issue(ra00 + ao, ra01 + ao, ra10 + ao, ra11 + ao, a0h[r], a0l[r], a1h[r], a1l[r]);
+    read_a_issue(ra00 + ao, ra01 + ao, ra00 + ao + 2048, ra01 + ao + 2048, ca0h, ca0l, ca1h, ca1l);
   };
-  auto read_wait = [&](int r) { read_stage_wait(bh[r], bl[r], a0h[r], a0l[r], a1h[r], a1l[r]); };
 
   while (ld_blk < min(kRing3 - 1, total_blocks)) issue();
   wait_vmcnt<0>();  // filter digits (and the first B blocks) landed for this lane
@@ -1195,34 +1200,57 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
     const int32_t gb0 = it * KB;
     const int32_t g = (first_tile + it * tile_stride) * 32 + col;
     const bool gvalid = g < NP;
-    int32_t obase;  // < 2^31 output elements (checked by the launcher)
+    int32_t obase;
     {
       const int32_t gg = gvalid ? g : 0;
       obase = (gg / PQ) * a.M * PQ + (gg % PQ);
     }
+    const int32_t mrow0 = m0 + 4 * half, mrow1 = m0 + 32 + 4 * half;
     Acc3 acc0, acc1;
     float sum0[16], sum1[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) { sum0[v] = 0.f; sum1[v] = 0.f; }
 
-    for (int32_t kb = 0; kb < KB; kb += 2) {
-      // block kb opens chunk kb/2; block kb+1 closes it
+    // block 0: tile 0 opens chunk 0
+    wait_block(gb0);
+    read_block(gb0, 0);
+    read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+    mfma_tile(acc0, ca0h, ca0l, cbh, cbl, true);
+    pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+    // block 1: tile 0 continues, tile 1 opens chunk 0 on block 0
+    wait_block(gb0 + 1);
+    read_block(gb0 + 1, 1);
+    read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+    mfma_tile(acc0, ca0h, ca0l, cbh, cbl, false);
+    mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
+    pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+
+    for (int32_t kb = 2; kb < KB; kb += 2) {
+      // even: tile 0's chunk ended at kb-1; tile 1 finishes its chunk on block kb-1
       wait_block(gb0 + kb);
-      read_block(gb0 + kb, kb, 0);
-      read_wait(0);
-      mfma_tile(acc0, a0h[0], a0l[0], bh[0], bl[0], true);
-      mfma_tile(acc1, a1h[0], a1l[0], bh[0], bl[0], true);
+      read_block(gb0 + kb, kb);
+      flush_tile<PARTIALS>(acc0, sum0, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+      mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+      interleave_4x16();
+      read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+      mfma_tile(acc0, ca0h, ca0l, cbh, cbl, true);
+      pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
+      // odd: tile 1's chunk ended; tile 0 continues; tile 1 opens the next chunk on block kb
       wait_block(gb0 + kb + 1);
-      read_block(gb0 + kb + 1, kb + 1, 0);
-      read_wait(0);
-      mfma_tile(acc0, a0h[0], a0l[0], bh[0], bl[0], false);
-      mfma_tile(acc1, a1h[0], a1l[0], bh[0], bl[0], false);
-      flush_tile<PARTIALS>(acc0, sum0, kb / 2, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
-      flush_tile<PARTIALS>(acc1, sum1, kb / 2, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
+      read_block(gb0 + kb + 1, kb + 1);
+      read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
+      flush_tile<PARTIALS>(acc1, sum1, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
+      mfma_tile(acc0, ca0h, ca0l, cbh, cbl, false);
+      interleave_4x16();
+      mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
+      pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
     }
+    flush_tile<PARTIALS>(acc0, sum0, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+    mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+    interleave_4x16();
+    flush_tile<PARTIALS>(acc1, sum1, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
 
     // ---- outputs of this tile (the stores drain while the next tile computes)
-    float* outp = a.out + obase;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
 #pragma unroll
@@ -1230,7 +1258,7 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
         const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
         const float y = ldexpf(i == 0 ? sum0[v] : sum1[v], e);
         if (gvalid && m < a.M) {
-          outp[(uint32_t)(m * PQ)] = y;
+          a.out[(uint32_t)(obase + m * PQ)] = y;
           amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
         }
       }
@@ -1282,7 +1310,8 @@ ConvMfmaPlan plan_conv_mfma(const Geom& g, int32_t dir) {
   }
   p.ws_a_bytes = align256((int64_t)p.KB * p.Mp * 2 * 32);
   p.ws_b_bytes = align256((int64_t)g.n * p.Hp * p.Wp * p.CG * 32);
-  p.bytes = p.ws_a_bytes + p.ws_b_bytes;
+  p.ws_t_bytes = align256((int64_t)p.KB * 8);
+  p.bytes = p.ws_a_bytes + p.ws_b_bytes + p.ws_t_bytes;
   return p;
 }
 
@@ -1294,10 +1323,13 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   const bool fwd = dir == DFP_FWD;
   uint8_t* wsa = reinterpret_cast<uint8_t*>(ws);
   uint8_t* xs = wsa + p.ws_a_bytes;
+  int2* boff = reinterpret_cast<int2*>(xs + p.ws_b_bytes);
+  const int32_t rsign = fwd ? 1 : -1;
+  const int32_t tap_row_bytes = rsign * p.Wp * p.CG * 32, tap_col_bytes = rsign * p.CG * 32;
   {
     const int64_t total = (int64_t)p.KB * p.Mp * 2;
     DFP_LAUNCH(K_WPREP, k_prep_a, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, b, wsa, p.M, p.Mp,
-               p.Cin, g.r, g.s, p.T, p.KB, fwd ? 0 : 1, g.c);
+               p.Cin, g.r, g.s, p.T, p.KB, fwd ? 0 : 1, g.c, so, boff, tap_row_bytes, tap_col_bytes);
   }
   {
     const int32_t Cs = fwd ? g.c : g.k, Hs = fwd ? g.h : g.p, Wsrc = fwd ? g.w : g.q;
@@ -1308,6 +1340,7 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   ConvMfmaArgs args{};
   args.xs = xs;
   args.wsa = wsa;
+  args.boff = boff;
   args.ea = sa;
   args.eb = sb;
   args.out = out;
@@ -1351,6 +1384,11 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
     const dim3 grid3((unsigned)gx, (unsigned)mtiles);
     if (partials) DFP_LAUNCH(kid, (k_conv_mfma_persist<true>), grid3, dim3(kThreads3), 0, st, args);
     else DFP_LAUNCH(kid, (k_conv_mfma_persist<false>), grid3, dim3(kThreads3), 0, st, args);
+    return DFP_OK;
+  }
+  if (chan16 && !masked && args.O < (1ll << 31) && p.ws_b_bytes < (1ll << 31)) {
+    if (partials) DFP_LAUNCH(kid, (k_conv_mfma_q<true>), grid, dim3(kThreadsQ), 0, st, args);
+    else DFP_LAUNCH(kid, (k_conv_mfma_q<false>), grid, dim3(kThreadsQ), 0, st, args);
     return DFP_OK;
   }
   if (chan16 && g.L == 64 && (p.T % 64) == 0 && p.KB >= 4) {

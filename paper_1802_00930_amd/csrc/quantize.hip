@@ -2,11 +2,15 @@
 //
 // Two HBM-bound passes: a max-magnitude reduction (integer max over the FP32
 // bit patterns with the sign cleared, one atomic per block), then the rounding
-// pass, which derives the shared exponent on the device from that max and
-// rounds every element with integer arithmetic on its sign / exponent /
-// mantissa fields (no floating-point rounding, so denormal modes cannot
-// matter).  Each lane owns 4 consecutive elements: one 16-byte load, one
-// Philox4x32-10 block (stochastic mode), one 8-byte store.
+// pass, which derives the shared exponent on the device from that max.
+// Stochastic rounding and round-down split every element into floor and
+// 32-bit fraction with integer arithmetic on its sign / exponent / significand
+// fields; nearest-even and biased rounding scale by 2^-Es with ldexp, which is
+// exact for every normal result (FP32 denormals are preserved in these
+// kernels, so denormal inputs scale exactly too), and the smaller results
+// round the same whatever ldexp does with them.  Each lane owns 4 consecutive
+// elements: one 16-byte load, one Philox4x32-10 block (stochastic mode), one
+// 8-byte store.
 #include "dfp_internal.h"
 
 namespace dfp {
@@ -41,19 +45,30 @@ __global__ void k_scale_reset(dfp_scale* s) {
   }
 }
 
+// Max of |src| bit patterns.  Each lane keeps four independent 16-byte loads
+// in flight per iteration; one (usually skipped) atomic per block.
 __global__ __launch_bounds__(kBlock) void k_amax(const float* __restrict__ src, int64_t n,
                                                  dfp_scale* __restrict__ s) {
   const uint4* src4 = reinterpret_cast<const uint4*>(src);
   const int64_t n4 = n >> 2;
-  uint32_t m = 0;
+  uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
   const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n4; i += stride) {
-    uint4 v = src4[i];
-    m = max(m, max(max(v.x & 0x7fffffffu, v.y & 0x7fffffffu), max(v.z & 0x7fffffffu, v.w & 0x7fffffffu)));
+  int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  for (; i + 3 * stride < n4; i += 4 * stride) {
+    const uint4 a = src4[i], b = src4[i + stride], c = src4[i + 2 * stride], d = src4[i + 3 * stride];
+    m0 = max(m0, max(max(a.x & 0x7fffffffu, a.y & 0x7fffffffu), max(a.z & 0x7fffffffu, a.w & 0x7fffffffu)));
+    m1 = max(m1, max(max(b.x & 0x7fffffffu, b.y & 0x7fffffffu), max(b.z & 0x7fffffffu, b.w & 0x7fffffffu)));
+    m2 = max(m2, max(max(c.x & 0x7fffffffu, c.y & 0x7fffffffu), max(c.z & 0x7fffffffu, c.w & 0x7fffffffu)));
+    m3 = max(m3, max(max(d.x & 0x7fffffffu, d.y & 0x7fffffffu), max(d.z & 0x7fffffffu, d.w & 0x7fffffffu)));
   }
+  for (; i < n4; i += stride) {
+    const uint4 a = src4[i];
+    m0 = max(m0, max(max(a.x & 0x7fffffffu, a.y & 0x7fffffffu), max(a.z & 0x7fffffffu, a.w & 0x7fffffffu)));
+  }
+  uint32_t m = max(max(m0, m1), max(m2, m3));
   if (blockIdx.x == 0) {
     const uint32_t* s1 = reinterpret_cast<const uint32_t*>(src);
-    for (int64_t i = 4 * n4 + threadIdx.x; i < n; i += kBlock) m = max(m, s1[i] & 0x7fffffffu);
+    for (int64_t t = 4 * n4 + threadIdx.x; t < n; t += kBlock) m = max(m, s1[t] & 0x7fffffffu);
   }
   m = block_max(m);
   // most blocks cannot raise the running max: skip their atomic after a plain read
@@ -80,50 +95,55 @@ __device__ __forceinline__ int32_t floor_log2_bits(uint32_t mb) {
   return (31 - __clz((int)(mb & 0x7fffffu))) - 149;
 }
 
-// Round one FP32 value (bit pattern fb) scaled by 2^-es to an integer.
-//   value = M * 2^e exactly (M the 24-bit significand); A = |x| * 2^32 = M * 2^sh.
-//   X = floor(x * 2^32) as a signed 64-bit integer; fl = X >> 32; F = low word.
-template <bool STOCH>
-__device__ __forceinline__ int32_t round_one(uint32_t fb, int32_t es, int32_t rounding, uint32_t u) {
-  const uint32_t eb = (fb >> 23) & 0xffu;
-  const uint32_t man = fb & 0x7fffffu;
-  const uint64_t M = eb ? (uint64_t)(man | 0x800000u) : (uint64_t)man;
-  const int32_t e = (eb ? (int32_t)eb : 1) - 150;
-  const int32_t sh = e - es + 32;
-  uint64_t A;
-  bool inexact;
-  if (sh >= 0) {
-    A = M << sh;  // |x| < 2^15 keeps A below 2^47
-    inexact = false;
-  } else if (sh > -40) {
-    A = M >> (-sh);
-    inexact = (M & ((1ull << (-sh)) - 1ull)) != 0ull;
-  } else {
-    A = 0;
-    inexact = M != 0;
-  }
-  const int64_t X = (fb >> 31) ? -(int64_t)A - (inexact ? 1 : 0) : (int64_t)A;
-  const int32_t fl = (int32_t)(X >> 32);
-  const uint32_t F = (uint32_t)X;
-  bool up;
-  if (STOCH) {
-    up = u < F;
-  } else if (rounding == DFP_ROUND_NEAREST) {
-    up = (F > 0x80000000u) || (F == 0x80000000u && (fl & 1));
-  } else if (rounding == DFP_ROUND_BIASED) {
-    up = F >= 0x80000000u;
-  } else {
-    up = false;
-  }
-  return fl + (up ? 1 : 0);
+// x = f * 2^-es split as X = floor(x * 2^32) = fl * 2^32 + F, in integer
+// arithmetic on the sign / exponent / significand fields.  f = M * 2^(e1 - 150)
+// with M the 24-bit significand, so |x| * 2^32 = M * 2^(32 - sh) with
+// sh = es + 150 - e1.  Every element of the tensor has |x| < 2^(bits-1) <= 2^15,
+// which bounds sh below by 9; shifts past 63 leave nothing but the inexact bit.
+struct Split {
+  int32_t fl;   // floor(x)
+  uint32_t F;   // floor(frac(x) * 2^32)
+};
+__device__ __forceinline__ Split split_scaled(uint32_t fb, int32_t es150) {
+  const uint32_t ax = fb & 0x7fffffffu;
+  const uint32_t eb = ax >> 23;
+  const uint32_t M = (ax & 0x7fffffu) | ((eb != 0u ? 1u : 0u) << 23);
+  const uint32_t sh = min((uint32_t)(es150 - (int32_t)max(eb, 1u)), 63u);
+  const uint64_t A = ((uint64_t)M << 32) >> sh;  // floor(|x| * 2^32)
+  const bool inexact = sh > 32u && (M << (64u - sh)) != 0u;
+  // negative x: floor(-|x| 2^32) = -(A + inexact) = ~A + (1 - inexact)
+  const uint64_t sm = (uint64_t)(int64_t)((int32_t)fb >> 31);
+  const uint64_t X = (A ^ sm) + ((sm != 0u && !inexact) ? 1u : 0u);
+  return {(int32_t)(X >> 32), (uint32_t)X};
 }
 
-template <bool STOCH>
+// Round f * 2^-es to an integer (Sec. 1 rounding modes).
+//   NEAREST   ties to even: x is exact in FP32 whenever it is a normal number,
+//             and every smaller |x| rounds to 0 however ldexp rounds it.
+//   BIASED    floor(x + 1/2) as floor(x) + (frac(x) >= 1/2); frac is exact for
+//             normal x and the decision is unchanged for smaller |x|.
+//   STOCHASTIC floor(x) + (u < F), u the element's Philox word.
+//   DOWN      floor(x).
+template <int MODE>
+__device__ __forceinline__ int32_t round_one(uint32_t fb, int32_t es, uint32_t u) {
+  if (MODE == DFP_ROUND_NEAREST) {
+    return (int32_t)rintf(ldexpf(__uint_as_float(fb), -es));
+  } else if (MODE == DFP_ROUND_BIASED) {
+    const float x = ldexpf(__uint_as_float(fb), -es);
+    const float fl = floorf(x);
+    return (int32_t)fl + ((x - fl) >= 0.5f ? 1 : 0);
+  } else {
+    const Split sp = split_scaled(fb, es + 150);
+    if (MODE == DFP_ROUND_STOCHASTIC) return sp.fl + (u < sp.F ? 1 : 0);
+    return sp.fl;
+  }
+}
+
+template <int MODE, bool SAT>
 __global__ __launch_bounds__(kBlock) void k_quant_convert(const float* __restrict__ src,
                                                           int16_t* __restrict__ dst, int64_t n,
                                                           dfp_scale* __restrict__ s, int32_t bits,
-                                                          int32_t rounding, uint32_t key0,
-                                                          uint32_t key1, uint32_t role) {
+                                                          uint32_t key0, uint32_t key1, uint32_t role) {
   const uint32_t mb = s->amax_bits;
   const bool nonfinite = mb >= 0x7f800000u;
   const bool zero = mb == 0u;
@@ -143,7 +163,6 @@ __global__ __launch_bounds__(kBlock) void k_quant_convert(const float* __restric
     if (f) atomicOr(&s->flags, f);
   }
   const bool all_zero = nonfinite || zero;
-  const int32_t lim = (bits == 16) ? 32767 : 0x7fffffff;
   const int64_t groups = (n + 3) >> 2;
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   bool saturated = false;
@@ -160,16 +179,20 @@ __global__ __launch_bounds__(kBlock) void k_quant_convert(const float* __restric
       for (int i = 0; i < 4; ++i) fb[i] = (base + i < n) ? s1[base + i] : 0u;
     }
     uint32_t u[4] = {0u, 0u, 0u, 0u};
-    if (STOCH) {
+    if (MODE == DFP_ROUND_STOCHASTIC) {
       const uint4 r = philox4x32_10(make_uint4((uint32_t)g, (uint32_t)((uint64_t)g >> 32), role, 0u), key0, key1);
       u[0] = r.x; u[1] = r.y; u[2] = r.z; u[3] = r.w;
     }
     int32_t iv[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      int32_t v = all_zero ? 0 : round_one<STOCH>(fb[i], es, rounding, u[i]);
-      if (v > lim) { v = lim; saturated = true; }
-      if (v < -lim) { v = -lim; saturated = true; }
+      int32_t v = round_one<MODE>(fb[i], es, u[i]);
+      v = all_zero ? 0 : v;
+      if (SAT) {  // P = 16: |x| < 2^15 rounds to at most 2^15
+        const int32_t c = min(max(v, -32767), 32767);
+        saturated |= c != v;
+        v = c;
+      }
       iv[i] = v;
     }
     if (full) {
@@ -183,7 +206,7 @@ __global__ __launch_bounds__(kBlock) void k_quant_convert(const float* __restric
         if (base + i < n) dst[base + i] = (int16_t)iv[i];
     }
   }
-  if (saturated) atomicOr(&s->flags, DFP_FLAG_SATURATED);
+  if (SAT && saturated) atomicOr(&s->flags, DFP_FLAG_SATURATED);
 }
 
 int grid_for(int64_t work_items) {
@@ -201,22 +224,33 @@ dfp_status launch_scale_reset(dfp_scale* s, hipStream_t st) {
 }
 
 dfp_status launch_amax(const float* src, int64_t n, dfp_scale* s, hipStream_t st) {
-  // at most 1024 blocks: each ends with one (usually skipped) atomic on the same word
+  // at most 2048 blocks (8 per CU): each ends with one (usually skipped) atomic on the same word
   int64_t blocks = (n / 4 + kBlock - 1) / kBlock;
-  blocks = blocks < 1 ? 1 : (blocks > 1024 ? 1024 : blocks);
+  blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
   DFP_LAUNCH(K_AMAX, k_amax, dim3((unsigned)blocks), dim3(kBlock), 0, st, src, n, s);
+  return DFP_OK;
+}
+
+template <int MODE>
+static dfp_status launch_qc_mode(const float* src, int16_t* dst, int64_t n, dfp_scale* s, int32_t bits,
+                                 uint32_t k0, uint32_t k1, uint32_t role, hipStream_t st) {
+  const dim3 grid(grid_for((n + 3) / 4));
+  if (bits == 16)
+    DFP_LAUNCH(K_QUANT, (k_quant_convert<MODE, true>), grid, dim3(kBlock), 0, st, src, dst, n, s, bits, k0, k1, role);
+  else
+    DFP_LAUNCH(K_QUANT, (k_quant_convert<MODE, false>), grid, dim3(kBlock), 0, st, src, dst, n, s, bits, k0, k1, role);
   return DFP_OK;
 }
 
 dfp_status launch_quant_convert(const float* src, int16_t* dst, int64_t n, dfp_scale* s, int32_t bits,
                                 int32_t rounding, uint64_t seed, uint32_t role, hipStream_t st) {
-  const dim3 grid(grid_for((n + 3) / 4));
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-  if (rounding == DFP_ROUND_STOCHASTIC)
-    DFP_LAUNCH(K_QUANT, k_quant_convert<true>, grid, dim3(kBlock), 0, st, src, dst, n, s, bits, rounding, k0, k1, role);
-  else
-    DFP_LAUNCH(K_QUANT, k_quant_convert<false>, grid, dim3(kBlock), 0, st, src, dst, n, s, bits, rounding, k0, k1, role);
-  return DFP_OK;
+  switch (rounding) {
+    case DFP_ROUND_NEAREST: return launch_qc_mode<DFP_ROUND_NEAREST>(src, dst, n, s, bits, k0, k1, role, st);
+    case DFP_ROUND_STOCHASTIC: return launch_qc_mode<DFP_ROUND_STOCHASTIC>(src, dst, n, s, bits, k0, k1, role, st);
+    case DFP_ROUND_BIASED: return launch_qc_mode<DFP_ROUND_BIASED>(src, dst, n, s, bits, k0, k1, role, st);
+    default: return launch_qc_mode<DFP_ROUND_DOWN>(src, dst, n, s, bits, k0, k1, role, st);
+  }
 }
 
 }  // namespace dfp
