@@ -138,7 +138,9 @@ typedef struct dfp_scale {
 /* Quantise an FP32 tensor to DFP (Sec. 3.1 Eq. 1-3; the quantisers Q_a, Q_w,
  * Q_e of Sec. 4.1).  src: FP32 [numel(role)], 16-byte aligned; dst: INT16
  * [numel(role)], 8-byte aligned; s: receives amax_bits, exp and flags.
- * Enqueues a max-magnitude reduction followed by the rounding pass. */
+ * Enqueues a max-magnitude reduction followed by the rounding pass; the
+ * reduction keeps its per-workgroup maxima in dst until the rounding pass
+ * overwrites it, so dst must not alias src. */
 dfp_status dfp_quantize(const dfp_desc* d, int32_t role, const float* src, int16_t* dst,
                         dfp_scale* s, void* stream);
 
@@ -174,7 +176,8 @@ dfp_status dfp_conv_bwd_weights(const dfp_desc* d, const int16_t* x, const dfp_s
  * of the current output; Sec. 4.1: Q_a after FP, Q_e after BP).  role is
  * DFP_ROLE_Y or DFP_ROLE_DX (sets the shape and the Philox stream).
  * amax_ready = 1: s->amax_bits (and flags) were produced by the convolution
- * that wrote src (its sy / sdx), so the max pass is skipped; 0: recompute. */
+ * that wrote src (its sy / sdx), so the max pass is skipped; 0: recompute
+ * (dst is scratch for the max pass, as in dfp_quantize). */
 dfp_status dfp_downconvert(const dfp_desc* d, int32_t role, const float* src, int16_t* dst,
                            dfp_scale* s, int32_t amax_ready, void* stream);
 

@@ -115,7 +115,7 @@ dfp_status conv_checks(const dfp_desc* d, Geom* g, const void* a, const void* sa
 bool use_mfma(const Geom& g, int32_t path, int32_t bits, int32_t dir) {
   if (path == DFP_PATH_VALU || bits != 15) return false;
   if (dir == DFP_BWD_WT) return bwdw_mfma_supported(g);
-  return true;
+  return conv_mfma_supported(g, dir);
 }
 
 size_t workspace_bytes(const Geom& g, int32_t dir, int32_t path, int32_t bits) {
@@ -183,8 +183,7 @@ dfp_status dfp_quantize(const dfp_desc* d, int32_t role, const float* src, int16
   const int64_t n = role_numel(g, role);
   hipStream_t st = (hipStream_t)stream;
   dfp_status rc;
-  if ((rc = launch_scale_reset(s, st)) != DFP_OK) return rc;
-  if ((rc = launch_amax(src, n, s, st)) != DFP_OK) return rc;
+  if ((rc = launch_amax(src, n, dst, s, st)) != DFP_OK) return rc;
   return launch_quant_convert(src, dst, n, s, d->bits, d->rounding, d->seed, (uint32_t)role, st);
 }
 
@@ -199,10 +198,7 @@ dfp_status dfp_downconvert(const dfp_desc* d, int32_t role, const float* src, in
   const int64_t n = role_numel(g, role);
   hipStream_t st = (hipStream_t)stream;
   dfp_status rc;
-  if (!amax_ready) {
-    if ((rc = launch_scale_reset(s, st)) != DFP_OK) return rc;
-    if ((rc = launch_amax(src, n, s, st)) != DFP_OK) return rc;
-  }
+  if (!amax_ready && (rc = launch_amax(src, n, dst, s, st)) != DFP_OK) return rc;
   return launch_quant_convert(src, dst, n, s, d->bits, d->rounding, d->seed, (uint32_t)role, st);
 }
 

@@ -38,62 +38,112 @@ __device__ __forceinline__ uint32_t lo_digit(int32_t a) { return (uint32_t)a & 0
 
 // A digits from dy in canonical order: Ad[kb][m][half][16 hi | 16 lo].
 // One thread per (kb, m, half), written in that order so a wave's stores are
-// contiguous; each thread reads 16 consecutive reduction indices of one plane.
+// contiguous; each thread reads 16 consecutive reduction indices of one plane,
+// as two 16-byte loads when they lie in one image and are aligned.  Every
+// index fits 32 bits (dy has fewer than 2^31 elements).
 __global__ __launch_bounds__(256) void k_prep_dy(const int16_t* __restrict__ dy, uint8_t* __restrict__ ad, int32_t K,
-                                                int32_t Mp, int64_t PQ, int64_t T, int64_t KBT) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t total = KBT * Mp * 2;
-  if (idx >= total) return;
-  const int32_t half = (int32_t)(idx & 1);
-  const int32_t m = (int32_t)((idx >> 1) % Mp);
-  const int64_t kb = (idx >> 1) / Mp;
+                                                int32_t Mp, int32_t PQ, int32_t T, int32_t KBT) {
+  const int32_t idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= KBT * Mp * 2) return;
+  const int32_t half = idx & 1;
+  const int32_t m = (idx >> 1) % Mp;
+  const int32_t kb = (idx >> 1) / Mp;
   uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
   if (m < K) {
-    int64_t t = kb * 32 + half * 16;
-    int64_t n = t / PQ, pq = t % PQ;
+    const int32_t t0 = kb * 32 + half * 16;
+    int32_t n = t0 / PQ, pq = t0 - n * PQ;
+    const int32_t off = (n * K + m) * PQ + pq;
+    if (t0 + 16 <= T && pq + 16 <= PQ && (reinterpret_cast<uintptr_t>(dy + off) & 15) == 0) {
+      const uint4* src = reinterpret_cast<const uint4*>(dy + off);
+      const uint4 v0 = src[0], v1 = src[1];
+      const uint32_t wv[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      int32_t v = 0;
-      if (t < T) v = dy[(n * K + m) * PQ + pq];
-      hi[i >> 2] |= hi_digit(v) << (8 * (i & 3));
-      lo[i >> 2] |= lo_digit(v) << (8 * (i & 3));
-      ++t;
-      if (++pq == PQ) { pq = 0; ++n; }
+      for (int i = 0; i < 16; ++i) {
+        const int32_t v = (int32_t)(int16_t)(wv[i >> 1] >> (16 * (i & 1)));
+        hi[i >> 2] |= hi_digit(v) << (8 * (i & 3));
+        lo[i >> 2] |= lo_digit(v) << (8 * (i & 3));
+      }
+    } else {
+      int32_t t = t0;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        int32_t v = 0;
+        if (t < T) v = dy[(n * K + m) * PQ + pq];
+        hi[i >> 2] |= hi_digit(v) << (8 * (i & 3));
+        lo[i >> 2] |= lo_digit(v) << (8 * (i & 3));
+        ++t;
+        if (++pq == PQ) { pq = 0; ++n; }
+      }
     }
   }
-  uint4* dst = reinterpret_cast<uint4*>(ad + ((kb * Mp + m) * 2 + half) * 32);
+  uint4* dst = reinterpret_cast<uint4*>(ad + (int64_t)idx * 32);
   dst[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
   dst[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
 }
 
 // XP[c][n*Hpad + u][v] = (lo | hi << 8) of x[n][c][u - ph][v - pw], zero outside.
-// One thread per 8 consecutive pairs of a row (Wpad is a multiple of 8): one
-// 16-byte store.
+// Grid (rows of channel c, c): one thread per 8 consecutive pairs of a row
+// (Wpad is a multiple of 8), one 16-byte store; consecutive threads read
+// consecutive pieces of a source row.
 __global__ __launch_bounds__(256) void k_prep_xp(const int16_t* __restrict__ x, uint16_t* __restrict__ xp, int32_t N,
                                                 int32_t C, int32_t H, int32_t W, int32_t Hpad, int32_t Wpad,
                                                 int32_t ph, int32_t pw) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int32_t W8 = Wpad / 8;
-  const int64_t total = (int64_t)C * N * Hpad * W8;
-  if (idx >= total) return;
-  const int32_t v0 = (int32_t)(idx % W8) * 8;
-  const int64_t z = (idx / W8) % ((int64_t)N * Hpad);
-  const int32_t c = (int32_t)(idx / ((int64_t)W8 * N * Hpad));
-  const int32_t n = (int32_t)(z / Hpad), u = (int32_t)(z % Hpad);
+  const int32_t c = blockIdx.y;
+  const int32_t i = blockIdx.x * 256 + threadIdx.x;  // (n * Hpad + u) * W8 + v8
+  const int32_t W8 = Wpad >> 3;
+  if (i >= N * Hpad * W8) return;
+  const int32_t r = i / W8, v0 = (i - r * W8) * 8;
+  const int32_t n = r / Hpad, u = r - n * Hpad;
   const int32_t ih = u - ph;
   uint32_t w[4] = {0u, 0u, 0u, 0u};
   if (ih >= 0 && ih < H) {
-    const int16_t* row = x + (((int64_t)n * C + c) * H + ih) * W;
+    const int16_t* row = x + ((int64_t)(n * C + c) * H + ih) * W;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int32_t iw = v0 + i - pw;
+    for (int k = 0; k < 8; ++k) {
+      const int32_t iw = v0 + k - pw;
       if (iw >= 0 && iw < W) {
         const int32_t a = row[iw];
-        w[i >> 1] |= (lo_digit(a) | (hi_digit(a) << 8)) << (16 * (i & 1));
+        w[k >> 1] |= (lo_digit(a) | (hi_digit(a) << 8)) << (16 * (k & 1));
       }
     }
   }
-  reinterpret_cast<uint4*>(xp)[idx] = make_uint4(w[0], w[1], w[2], w[3]);
+  reinterpret_cast<uint4*>(xp + ((int64_t)c * N * Hpad * Wpad))[i] = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// Same layout for rows of a multiple of 8 elements, 16-byte aligned, and a
+// column pad PW below 4: each lane loads the two aligned 8-element groups
+// around its window (zero outside the row) and takes elements 8-PW .. 15-PW.
+template <int PW>
+__global__ __launch_bounds__(256) void k_prep_xp_vec(const int16_t* __restrict__ x, uint16_t* __restrict__ xp,
+                                                    int32_t N, int32_t C, int32_t H, int32_t W, int32_t Hpad,
+                                                    int32_t Wpad, int32_t ph) {
+  const int32_t c = blockIdx.y;
+  const int32_t i = blockIdx.x * 256 + threadIdx.x;  // (n * Hpad + u) * W8 + v8
+  const int32_t W8 = Wpad >> 3;
+  if (i >= N * Hpad * W8) return;
+  const int32_t r = i / W8, v0 = (i - r * W8) * 8;
+  const int32_t n = r / Hpad, u = r - n * Hpad;
+  const int32_t ih = u - ph;
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+  if (ih >= 0 && ih < H) {
+    const int16_t* row = x + ((int64_t)(n * C + c) * H + ih) * W;
+    uint32_t g[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};  // elements v0-8 .. v0+7
+    if (PW > 0 && v0 >= 8 && v0 - 8 < W) {
+      const uint4 q = *reinterpret_cast<const uint4*>(row + v0 - 8);
+      g[0] = q.x; g[1] = q.y; g[2] = q.z; g[3] = q.w;
+    }
+    if (v0 < W) {
+      const uint4 q = *reinterpret_cast<const uint4*>(row + v0);
+      g[4] = q.x; g[5] = q.y; g[6] = q.z; g[7] = q.w;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int e = 8 - PW + k;
+      const int32_t a = (int32_t)(int16_t)(g[e >> 1] >> (16 * (e & 1)));
+      w[k >> 1] |= (lo_digit(a) | (hi_digit(a) << 8)) << (16 * (k & 1));
+    }
+  }
+  reinterpret_cast<uint4*>(xp + ((int64_t)c * N * Hpad * Wpad))[i] = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 // Byte mask keeping bytes [lo, hi) of a 16-byte operand.
@@ -399,12 +449,22 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   {
     const int64_t total = p.KBT * p.Mp * 2;
     DFP_LAUNCH(K_WPREP, k_prep_dy, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, dy, ad, g.k, p.Mp,
-               (int64_t)g.p * g.q, p.T, p.KBT);
+               g.p * g.q, (int32_t)p.T, (int32_t)p.KBT);
   }
   {
-    const int64_t total = (int64_t)g.c * g.n * p.Hpad * (p.Wpad / 8);
-    DFP_LAUNCH(K_XPREP, k_prep_xp, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, xp, g.n, g.c, g.h,
-               g.w, p.Hpad, p.Wpad, g.ph, g.pw);
+    const int64_t per_c = (int64_t)g.n * p.Hpad * (p.Wpad / 8);
+    const dim3 grid_xp((unsigned)((per_c + 255) / 256), (unsigned)g.c);
+    const bool vec = (g.w % 8) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 && g.pw < 4;
+    if (vec && g.pw == 0)
+      DFP_LAUNCH(K_XPREP, k_prep_xp_vec<0>, grid_xp, dim3(256), 0, st, x, xp, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+    else if (vec && g.pw == 1)
+      DFP_LAUNCH(K_XPREP, k_prep_xp_vec<1>, grid_xp, dim3(256), 0, st, x, xp, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+    else if (vec && g.pw == 2)
+      DFP_LAUNCH(K_XPREP, k_prep_xp_vec<2>, grid_xp, dim3(256), 0, st, x, xp, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+    else if (vec)
+      DFP_LAUNCH(K_XPREP, k_prep_xp_vec<3>, grid_xp, dim3(256), 0, st, x, xp, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+    else
+      DFP_LAUNCH(K_XPREP, k_prep_xp, grid_xp, dim3(256), 0, st, x, xp, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph, g.pw);
   }
   BwdwArgs args{};
   args.ad = ad;

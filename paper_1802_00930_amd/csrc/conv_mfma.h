@@ -28,6 +28,8 @@ struct ConvMfmaArgs {
 };
 
 ConvMfmaPlan plan_conv_mfma(const Geom& g, int32_t dir);
+// The B prep kernel stages one source row of at least 16 channels in LDS.
+bool conv_mfma_supported(const Geom& g, int32_t dir);
 dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,
                             const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, void* ws,
                             hipStream_t st);

@@ -55,13 +55,16 @@ __device__ __forceinline__ uint32_t lo_digit(int32_t a) { return (uint32_t)a & 0
 
 // ---------------------------------------------------------------- A prep
 // A[m][t] for t = (r*S + s)*Cin + ci.  fwd: m = k, ci = c, value w[m][ci][r][s].
-// bwd-data: m = c, ci = k, value w[ci][m][r][s].
+// bwd-data: m = c, ci = k, value w[ci][m][r][s].  One thread per 4 digits of
+// one (kb, m, half) piece: the hi and lo words it packs land 16 bytes apart.
+// The same launch clears the output scale and writes the per-block B offset
+// table of the main kernels.
 __global__ __launch_bounds__(256) void k_prep_a(const int16_t* __restrict__ w, uint8_t* __restrict__ ws,
                                                int32_t M, int32_t Mp, int32_t Cin, int32_t R, int32_t S,
                                                int32_t T, int32_t KB, int32_t transposed, int32_t Cw,
                                                dfp_scale* so, int2* boff, int32_t tap_row_bytes,
                                                int32_t tap_col_bytes) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (kb, m, half)
+  const int32_t idx = blockIdx.x * 256 + threadIdx.x;  // ((kb, m, half), quarter)
   if (so && idx == 0) {  // the output scale starts empty; the conv epilogue raises its max
     so->amax_bits = 0u;
     so->flags = 0u;
@@ -72,78 +75,113 @@ __global__ __launch_bounds__(256) void k_prep_a(const int16_t* __restrict__ w, u
     int32_t o[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int32_t t = (int32_t)idx * 32 + 16 * h;
+      const int32_t t = idx * 32 + 16 * h;
       const int32_t tap = t / Cin, ci = t % Cin;
       o[h] = t < T ? (tap / S) * tap_row_bytes + (tap % S) * tap_col_bytes + (ci >> 4) * 32 : 0;
     }
     boff[idx] = make_int2(o[0], o[1]);
   }
-  const int64_t total = (int64_t)KB * Mp * 2;
+  const int32_t total = KB * Mp * 8;
   if (idx >= total) return;
-  const int32_t half = (int32_t)(idx & 1);
-  const int32_t m = (int32_t)((idx >> 1) % Mp);
-  const int32_t kb = (int32_t)((idx >> 1) / Mp);
-  uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+  const int32_t quarter = idx & 3;
+  const int32_t piece = idx >> 2;  // (kb * Mp + m) * 2 + half
+  const int32_t half = piece & 1;
+  const int32_t m = (piece >> 1) % Mp;
+  const int32_t kb = (piece >> 1) / Mp;
+  uint32_t hi = 0u, lo = 0u;
   if (m < M) {
+    const int32_t t0 = kb * 32 + half * 16 + quarter * 4;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int32_t t = kb * 32 + half * 16 + i;
+    for (int i = 0; i < 4; ++i) {
+      const int32_t t = t0 + i;
       int32_t v = 0;
       if (t < T) {
         const int32_t ci = t % Cin, tap = t / Cin;
         const int32_t r = tap / S, s = tap % S;
-        // forward: w[m][ci][r][s] (Cw = C); backward-data: w[ci][m][r][s] (Cw = C)
-        const int64_t off = transposed ? (((int64_t)ci * Cw + m) * R + r) * S + s
-                                       : (((int64_t)m * Cw + ci) * R + r) * S + s;
+        // forward: w[m][ci][r][s]; backward-data: w[ci][m][r][s] (Cw = C)
+        const int32_t off = transposed ? ((ci * Cw + m) * R + r) * S + s : ((m * Cw + ci) * R + r) * S + s;
         v = w[off];
       }
-      hi[i >> 2] |= hi_digit(v) << (8 * (i & 3));
-      lo[i >> 2] |= lo_digit(v) << (8 * (i & 3));
+      hi |= hi_digit(v) << (8 * i);
+      lo |= lo_digit(v) << (8 * i);
     }
   }
-  uint4* dst = reinterpret_cast<uint4*>(ws + idx * 32);
-  dst[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-  dst[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+  uint32_t* dst = reinterpret_cast<uint32_t*>(ws + (int64_t)piece * 32) + quarter;
+  dst[0] = hi;
+  dst[4] = lo;
 }
 
 // ---------------------------------------------------------------- B prep
 // Xs[n][u][v][cg][32 B] = digits of src[n][cg*16 + i][(u-top)/dil_h][(v-left)/dil_w]
 // when (u-top), (v-left) are non-negative multiples of the dilation inside the
-// source, else 0.  One thread per (n, u, v, block of up to 4 channel groups)
-// writes 4*32 contiguous bytes; consecutive threads take consecutive v, so the
-// reads of one channel row are contiguous across the wave.
+// source, else 0.  One workgroup per output row (n, u): the source row of up to
+// kPrepBElems / Wsrc channels is transposed into LDS as [w][channel] (16-byte
+// loads along w when rows are 8-element aligned), then every lane writes the
+// 32 bytes of one (v, channel group) unit from one contiguous LDS run, so the
+// output row is stored contiguously.
+constexpr int kPrepBElems = 16384;  // int16 elements staged per pass (32 KiB)
+
+template <bool VEC>
 __global__ __launch_bounds__(256) void k_prep_b(const int16_t* __restrict__ src, uint8_t* __restrict__ xs,
                                                int32_t N, int32_t Cs, int32_t Hs, int32_t Wsrc, int32_t Hp,
                                                int32_t Wp, int32_t CG, int32_t top, int32_t left, int32_t dil_h,
                                                int32_t dil_w) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int32_t CB = (CG + 3) / 4;
-  const int64_t total = (int64_t)N * Hp * Wp * CB;
-  if (idx >= total) return;
-  const int32_t v = (int32_t)(idx % Wp);
-  const int32_t cb = (int32_t)((idx / Wp) % CB);
-  const int32_t u = (int32_t)((idx / ((int64_t)Wp * CB)) % Hp);
-  const int64_t n = idx / ((int64_t)Wp * CB * Hp);
-  const int32_t zu = u - top, zv = v - left;
-  const bool inside =
-      zu >= 0 && zv >= 0 && (zu % dil_h) == 0 && (zv % dil_w) == 0 && zu / dil_h < Hs && zv / dil_w < Wsrc;
+  extern __shared__ __align__(16) int16_t tile[];  // cgc * 16 * Wsrc elements (launcher sizes it)
+  const int32_t row = blockIdx.x;  // n * Hp + u
+  const int32_t n = row / Hp, u = row - n * Hp;
+  const int32_t zu = u - top;
+  const bool row_in = zu >= 0 && (zu % dil_h) == 0 && zu / dil_h < Hs;
+  const int32_t h = row_in ? zu / dil_h : 0;
+  uint4* dst = reinterpret_cast<uint4*>(xs + (int64_t)row * Wp * CG * 32);
+  const int32_t cgc = max(1, min(CG, kPrepBElems / (16 * Wsrc)));  // channel groups per pass
   const int64_t plane = (int64_t)Hs * Wsrc;
-  const int16_t* p = src + n * Cs * plane + (inside ? (int64_t)(zu / dil_h) * Wsrc + zv / dil_w : 0);
-  uint4* dst = reinterpret_cast<uint4*>(xs + ((n * Hp + u) * Wp + v) * CG * 32);
-  const int32_t cg_end = min(CG, cb * 4 + 4);
-  for (int32_t cg = cb * 4; cg < cg_end; ++cg) {
-    uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
-    if (inside) {
+  const int16_t* srow = src + (int64_t)n * Cs * plane + (int64_t)h * Wsrc;
+  for (int32_t cg0 = 0; cg0 < CG; cg0 += cgc) {
+    const int32_t ncg = min(cgc, CG - cg0);
+    const int32_t cs = ncg * 16;  // LDS row stride in elements
+    if (row_in) {
+      __syncthreads();  // the previous pass has been consumed
+      if (VEC) {
+        const int32_t W8 = Wsrc >> 3;
+        for (int32_t j = threadIdx.x; j < cs * W8; j += 256) {
+          const int32_t cl = j / W8, w0 = (j - cl * W8) * 8;
+          const int32_t c = cg0 * 16 + cl;
+          uint4 v = make_uint4(0u, 0u, 0u, 0u);
+          if (c < Cs) v = *reinterpret_cast<const uint4*>(srow + (int64_t)c * plane + w0);
+          const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int32_t c = cg * 16 + i;
-        const int32_t a = (c < Cs) ? (int32_t)p[c * plane] : 0;
-        hi[i >> 2] |= hi_digit(a) << (8 * (i & 3));
-        lo[i >> 2] |= lo_digit(a) << (8 * (i & 3));
+          for (int k = 0; k < 8; ++k) tile[(w0 + k) * cs + cl] = (int16_t)(wv[k >> 1] >> (16 * (k & 1)));
+        }
+      } else {
+        for (int32_t e = threadIdx.x; e < cs * Wsrc; e += 256) {
+          const int32_t cl = e / Wsrc, w = e - cl * Wsrc;
+          const int32_t c = cg0 * 16 + cl;
+          tile[w * cs + cl] = c < Cs ? srow[(int64_t)c * plane + w] : (int16_t)0;
+        }
       }
+      __syncthreads();
     }
-    dst[2 * cg] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-    dst[2 * cg + 1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+    const int32_t units = Wp * ncg;
+    for (int32_t j = threadIdx.x; j < units; j += 256) {
+      const int32_t v = j / ncg, cgl = j - v * ncg;
+      const int32_t zv = v - left;
+      const bool in = row_in && zv >= 0 && (zv % dil_w) == 0 && zv / dil_w < Wsrc;
+      uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+      if (in) {
+        const uint4* tp = reinterpret_cast<const uint4*>(tile + (zv / dil_w) * cs + cgl * 16);
+        const uint4 p0 = tp[0], p1 = tp[1];
+        const uint32_t wv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int32_t a = (int32_t)(int16_t)(wv[i >> 1] >> (16 * (i & 1)));
+          hi[i >> 2] |= hi_digit(a) << (8 * (i & 3));
+          lo[i >> 2] |= lo_digit(a) << (8 * (i & 3));
+        }
+      }
+      uint4* d = dst + (v * CG + cg0 + cgl) * 2;
+      d[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+      d[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+    }
   }
 }
 
@@ -1284,6 +1322,11 @@ inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
 
 }  // namespace
 
+bool conv_mfma_supported(const Geom& g, int32_t dir) {
+  const int32_t wsrc = dir == DFP_FWD ? g.w : g.q;
+  return 16 * wsrc <= kPrepBElems;
+}
+
 // Workspace layout of the forward / backward-data MFMA path.
 ConvMfmaPlan plan_conv_mfma(const Geom& g, int32_t dir) {
   ConvMfmaPlan p{};
@@ -1327,15 +1370,21 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   const int32_t rsign = fwd ? 1 : -1;
   const int32_t tap_row_bytes = rsign * p.Wp * p.CG * 32, tap_col_bytes = rsign * p.CG * 32;
   {
-    const int64_t total = (int64_t)p.KB * p.Mp * 2;
+    const int64_t total = (int64_t)p.KB * p.Mp * 8;
     DFP_LAUNCH(K_WPREP, k_prep_a, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, b, wsa, p.M, p.Mp,
                p.Cin, g.r, g.s, p.T, p.KB, fwd ? 0 : 1, g.c, so, boff, tap_row_bytes, tap_col_bytes);
   }
   {
     const int32_t Cs = fwd ? g.c : g.k, Hs = fwd ? g.h : g.p, Wsrc = fwd ? g.w : g.q;
-    const int64_t total = (int64_t)g.n * p.Hp * p.Wp * ((p.CG + 3) / 4);
-    DFP_LAUNCH(K_XPREP, k_prep_b, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, a, xs, g.n, Cs, Hs,
-               Wsrc, p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w);
+    const bool vec = (Wsrc % 8) == 0 && (reinterpret_cast<uintptr_t>(a) & 15) == 0;
+    const int32_t cgc = std::max(1, std::min(p.CG, kPrepBElems / (16 * Wsrc)));  // as in the kernel
+    const size_t lds = (size_t)cgc * 16 * Wsrc * 2;
+    if (vec)
+      DFP_LAUNCH(K_XPREP, k_prep_b<true>, dim3((unsigned)(g.n * p.Hp)), dim3(256), lds, st, a, xs, g.n, Cs, Hs,
+                 Wsrc, p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w);
+    else
+      DFP_LAUNCH(K_XPREP, k_prep_b<false>, dim3((unsigned)(g.n * p.Hp)), dim3(256), lds, st, a, xs, g.n, Cs, Hs,
+                 Wsrc, p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w);
   }
   ConvMfmaArgs args{};
   args.xs = xs;

@@ -52,7 +52,9 @@ void prof_end(int slot, hipStream_t st);
 // ---- launchers (one per translation unit) ----
 // quantize.hip
 dfp_status launch_scale_reset(dfp_scale* s, hipStream_t st);
-dfp_status launch_amax(const float* src, int64_t n, dfp_scale* s, hipStream_t st);
+// Writes amax_bits and clears flags; scratch (the destination INT16 buffer of
+// n elements) holds partial maxima until the rounding pass overwrites it.
+dfp_status launch_amax(const float* src, int64_t n, int16_t* scratch, dfp_scale* s, hipStream_t st);
 dfp_status launch_quant_convert(const float* src, int16_t* dst, int64_t n, dfp_scale* s, int32_t bits,
                                 int32_t rounding, uint64_t seed, uint32_t role, hipStream_t st);
 

@@ -11,6 +11,8 @@
 // round the same whatever ldexp does with them.  Each lane owns 4 consecutive
 // elements: one 16-byte load, one Philox4x32-10 block (stochastic mode), one
 // 8-byte store.
+#include <algorithm>
+
 #include "dfp_internal.h"
 
 namespace dfp {
@@ -45,34 +47,62 @@ __global__ void k_scale_reset(dfp_scale* s) {
   }
 }
 
-// Max of |src| bit patterns.  Each lane keeps four independent 16-byte loads
-// in flight per iteration; one (usually skipped) atomic per block.
+// Max of |src| bit patterns in two stages with no atomics.  Stage 1:
+// workgroup b reduces the 16 KiB chunks b, b + grid, ... (each lane keeps four
+// independent 16-byte loads in flight) and stores its max in part[b].  part
+// is the destination INT16 buffer, which the rounding pass overwrites only
+// after stage 2 has read it.  Stage 2: one workgroup reduces the partial
+// maxima into the scale and clears its flags.  A tensor of at most one chunk
+// goes straight to the scale in stage 1.
+constexpr int kAmaxUnroll = 4;
+constexpr int kAmaxChunk = kBlock * kAmaxUnroll;  // 16-byte vectors per chunk
+constexpr int kAmaxMaxParts = 1024;
+
+__device__ __forceinline__ uint32_t abs_max4(uint4 v) {
+  return max(max(v.x & 0x7fffffffu, v.y & 0x7fffffffu), max(v.z & 0x7fffffffu, v.w & 0x7fffffffu));
+}
+
 __global__ __launch_bounds__(kBlock) void k_amax(const float* __restrict__ src, int64_t n,
-                                                 dfp_scale* __restrict__ s) {
+                                                 uint32_t* __restrict__ part, dfp_scale* __restrict__ s) {
   const uint4* src4 = reinterpret_cast<const uint4*>(src);
   const int64_t n4 = n >> 2;
-  uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
-  const int64_t stride = (int64_t)gridDim.x * kBlock;
-  int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  for (; i + 3 * stride < n4; i += 4 * stride) {
-    const uint4 a = src4[i], b = src4[i + stride], c = src4[i + 2 * stride], d = src4[i + 3 * stride];
-    m0 = max(m0, max(max(a.x & 0x7fffffffu, a.y & 0x7fffffffu), max(a.z & 0x7fffffffu, a.w & 0x7fffffffu)));
-    m1 = max(m1, max(max(b.x & 0x7fffffffu, b.y & 0x7fffffffu), max(b.z & 0x7fffffffu, b.w & 0x7fffffffu)));
-    m2 = max(m2, max(max(c.x & 0x7fffffffu, c.y & 0x7fffffffu), max(c.z & 0x7fffffffu, c.w & 0x7fffffffu)));
-    m3 = max(m3, max(max(d.x & 0x7fffffffu, d.y & 0x7fffffffu), max(d.z & 0x7fffffffu, d.w & 0x7fffffffu)));
+  uint32_t m[kAmaxUnroll] = {0u, 0u, 0u, 0u};
+  for (int64_t base = (int64_t)blockIdx.x * kAmaxChunk; base < n4; base += (int64_t)gridDim.x * kAmaxChunk) {
+    if (base + kAmaxChunk <= n4) {
+      uint4 v[kAmaxUnroll];
+#pragma unroll
+      for (int k = 0; k < kAmaxUnroll; ++k) v[k] = src4[base + threadIdx.x + k * kBlock];
+#pragma unroll
+      for (int k = 0; k < kAmaxUnroll; ++k) m[k] = max(m[k], abs_max4(v[k]));
+    } else {
+      for (int64_t i = base + threadIdx.x; i < n4; i += kBlock) m[0] = max(m[0], abs_max4(src4[i]));
+    }
   }
-  for (; i < n4; i += stride) {
-    const uint4 a = src4[i];
-    m0 = max(m0, max(max(a.x & 0x7fffffffu, a.y & 0x7fffffffu), max(a.z & 0x7fffffffu, a.w & 0x7fffffffu)));
-  }
-  uint32_t m = max(max(m0, m1), max(m2, m3));
+  uint32_t mm = max(max(m[0], m[1]), max(m[2], m[3]));
   if (blockIdx.x == 0) {
     const uint32_t* s1 = reinterpret_cast<const uint32_t*>(src);
-    for (int64_t t = 4 * n4 + threadIdx.x; t < n; t += kBlock) m = max(m, s1[t] & 0x7fffffffu);
+    for (int64_t t = 4 * n4 + threadIdx.x; t < n; t += kBlock) mm = max(mm, s1[t] & 0x7fffffffu);
   }
+  mm = block_max(mm);
+  if (threadIdx.x == 0) {
+    if (part) {
+      part[blockIdx.x] = mm;
+    } else {
+      s->amax_bits = mm;
+      s->flags = 0u;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_amax_final(const uint32_t* __restrict__ part, int32_t nparts,
+                                                       dfp_scale* __restrict__ s) {
+  uint32_t m = 0u;
+  for (int32_t i = threadIdx.x; i < nparts; i += kBlock) m = max(m, part[i]);
   m = block_max(m);
-  // most blocks cannot raise the running max: skip their atomic after a plain read
-  if (threadIdx.x == 0 && m > __atomic_load_n(&s->amax_bits, __ATOMIC_RELAXED)) atomicMax(&s->amax_bits, m);
+  if (threadIdx.x == 0) {
+    s->amax_bits = m;
+    s->flags = 0u;
+  }
 }
 
 // Philox4x32-10 (Salmon et al., SC'11).
@@ -223,11 +253,18 @@ dfp_status launch_scale_reset(dfp_scale* s, hipStream_t st) {
   return DFP_OK;
 }
 
-dfp_status launch_amax(const float* src, int64_t n, dfp_scale* s, hipStream_t st) {
-  // at most 2048 blocks (8 per CU): each ends with one (usually skipped) atomic on the same word
-  int64_t blocks = (n / 4 + kBlock - 1) / kBlock;
-  blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
-  DFP_LAUNCH(K_AMAX, k_amax, dim3((unsigned)blocks), dim3(kBlock), 0, st, src, n, s);
+dfp_status launch_amax(const float* src, int64_t n, int16_t* scratch, dfp_scale* s, hipStream_t st) {
+  // one workgroup per 16 KiB chunk up to kAmaxMaxParts (grid-stride beyond); the
+  // partial maxima need 4 bytes each of the 2n-byte destination
+  int64_t parts = (n / 4 + kAmaxChunk - 1) / kAmaxChunk;
+  parts = std::min<int64_t>(std::min<int64_t>(parts, kAmaxMaxParts), n / 2);
+  if (parts <= 1) {
+    DFP_LAUNCH(K_AMAX, k_amax, dim3(1), dim3(kBlock), 0, st, src, n, (uint32_t*)nullptr, s);
+    return DFP_OK;
+  }
+  uint32_t* part = reinterpret_cast<uint32_t*>(scratch);
+  DFP_LAUNCH(K_AMAX, k_amax, dim3((unsigned)parts), dim3(kBlock), 0, st, src, n, part, s);
+  DFP_LAUNCH(K_AMAX, k_amax_final, dim3(1), dim3(kBlock), 0, st, part, (int32_t)parts, s);
   return DFP_OK;
 }
 
