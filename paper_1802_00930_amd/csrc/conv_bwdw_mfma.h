@@ -18,6 +18,7 @@ struct BwdwPlan {
 struct BwdwArgs {
   const uint8_t* ad;      // dy digits [KBT][Mp][2][32]
   const uint16_t* xp;     // x digit pairs [C][N*Hpad][Wpad]
+  const uint8_t* xb;      // x digit planes [C][N*Hpad][2][Wpad] (band kernel)
   const dfp_scale* ea;    // x scale
   const dfp_scale* eb;    // dy scale
   float* out;             // dW [K][C][R][S]
@@ -25,6 +26,7 @@ struct BwdwArgs {
   int32_t* partials;
   int64_t T, O;
   int32_t K, Mp, C, R, S, P, Q, sh, sw, Hpad, Wpad, NH, L, G, nseg, band_bytes, band_ch_stride;
+  int32_t rows_max, nch_max, buf_bytes;  // band kernel: rows and channels per band, bytes per buffer
 };
 
 BwdwPlan plan_bwdw_mfma(const Geom& g);

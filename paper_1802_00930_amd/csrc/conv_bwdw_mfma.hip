@@ -377,6 +377,250 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_mfma(BwdwArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Band kernel: unit strides, output rows of a multiple of 8, filter width at
+// most 4, chunks of whole 32-index blocks.  Reduction indices then come in
+// runs of 8 that lie in one output row (t = t0 .. t0+7 are q = q0 .. q0+7 of
+// one (n, p)), and for a column (c, r, s) the run's operands are the 8
+// consecutive bytes at column q0 + s of padded input row n*Hpad + p + r.  x is
+// prepared as separate lo / hi byte planes per padded row, XB[c][z][2][Wpad],
+// so a lane reads each run as one 16-byte window at the 8-aligned column q0
+// (ds_read2_b64) and extracts its 8 bytes with two byte-aligns by s.
+// Per band of 128 indices (4 blocks, 16 runs) the workgroup copies, with
+// direct-to-LDS loads into the other half of a double buffer while the
+// current band is consumed, the band's dy digits (A, swizzled as in the
+// forward kernels) and the padded input rows its runs touch for the
+// workgroup's channels; one barrier per band.
+constexpr int kBandBlocks = kSBT / 32;               // 4
+constexpr int kBandABytes = kBandBlocks * kMT * 64;  // 16 KiB
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint8_t*)p;
+}
+__device__ __forceinline__ int swz(int row, int piece) { return row * 4 + (piece ^ ((row >> 2) & 3)); }
+
+// XB[c][n*Hpad + u][d][Wpad]: d = 0 lo digits, d = 1 hi digits of
+// x[n][c][u - ph][v - pw], zero outside.  Rows of a multiple of 8 elements,
+// 16-byte aligned, column pad PW below 4 (same windowing as k_prep_xp_vec).
+template <int PW>
+__global__ __launch_bounds__(256) void k_prep_xb(const int16_t* __restrict__ x, uint8_t* __restrict__ xb, int32_t N,
+                                                int32_t C, int32_t H, int32_t W, int32_t Hpad, int32_t Wpad,
+                                                int32_t ph) {
+  const int32_t c = blockIdx.y;
+  const int32_t i = blockIdx.x * 256 + threadIdx.x;  // (n * Hpad + u) * W8 + v8
+  const int32_t W8 = Wpad >> 3;
+  if (i >= N * Hpad * W8) return;
+  const int32_t r = i / W8, v0 = (i - r * W8) * 8;
+  const int32_t n = r / Hpad, u = r - n * Hpad;
+  const int32_t ih = u - ph;
+  uint32_t lo[2] = {0u, 0u}, hi[2] = {0u, 0u};
+  if (ih >= 0 && ih < H) {
+    const int16_t* row = x + ((int64_t)(n * C + c) * H + ih) * W;
+    uint32_t g[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};  // elements v0-8 .. v0+7
+    if (PW > 0 && v0 >= 8 && v0 - 8 < W) {
+      const uint4 q = *reinterpret_cast<const uint4*>(row + v0 - 8);
+      g[0] = q.x; g[1] = q.y; g[2] = q.z; g[3] = q.w;
+    }
+    if (v0 < W) {
+      const uint4 q = *reinterpret_cast<const uint4*>(row + v0);
+      g[4] = q.x; g[5] = q.y; g[6] = q.z; g[7] = q.w;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int e = 8 - PW + k;
+      const int32_t a = (int32_t)(int16_t)(g[e >> 1] >> (16 * (e & 1)));
+      lo[k >> 2] |= lo_digit(a) << (8 * (k & 3));
+      hi[k >> 2] |= hi_digit(a) << (8 * (k & 3));
+    }
+  }
+  uint8_t* rowp = xb + ((int64_t)c * N * Hpad + r) * 2 * Wpad + v0;
+  *reinterpret_cast<uint2*>(rowp) = make_uint2(lo[0], lo[1]);
+  *reinterpret_cast<uint2*>(rowp + Wpad) = make_uint2(hi[0], hi[1]);
+}
+
+__device__ __forceinline__ void lds_rd128(v4i& d, uint32_t addr) {
+  asm volatile("ds_read_b128 %0, %1" : "=v"(d) : "v"(addr) : "memory");
+}
+__device__ __forceinline__ void lds_rd2x64(v4i& d, uint32_t addr) {
+  asm volatile("ds_read2_b64 %0, %1 offset1:1" : "=v"(d) : "v"(addr) : "memory");
+}
+__device__ __forceinline__ void lds_rd64(uint2& d, uint32_t addr) {
+  asm volatile("ds_read_b64 %0, %1" : "=v"(d) : "v"(addr) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Bytes s .. s+7 of a 16-byte window (s in 0..3), as two dwords.
+__device__ __forceinline__ int window8_lo(const v4i& w, uint32_t s) {
+  return (int)__builtin_amdgcn_alignbyte((uint32_t)w[1], (uint32_t)w[0], s);
+}
+__device__ __forceinline__ int window8_hi(const v4i& w, uint32_t s) {
+  return (int)__builtin_amdgcn_alignbyte((uint32_t)w[2], (uint32_t)w[1], s);
+}
+
+template <bool PARTIALS>
+__global__ __launch_bounds__(kThreads, 2) void k_bwdw_band(BwdwArgs a) {
+  // two buffers, each [B band: nch_max channels x rows_max padded rows x 2 planes x Wpad][A: 16 KiB];
+  // a B window read past the last row stays inside the A part that follows it
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int half = lane >> 5;
+  const int lc = lane & 31;
+  const int32_t RS = a.R * a.S;
+  const int32_t CRS = a.C * RS;
+  const int32_t col0 = blockIdx.x * kNT;
+  const int32_t col = col0 + wave * 32 + lc;
+  const bool cvalid = col < CRS;
+  const int32_t colc = cvalid ? col : col0;
+  const int32_t c = colc / RS, rr = (colc % RS) / a.S;
+  const uint32_t ss = (uint32_t)(colc % a.S);
+  const int32_t c_lo = col0 / RS;
+  const int32_t m0 = blockIdx.y * kMT;
+  const int32_t g = blockIdx.z;
+  const int32_t seg_len = a.G * a.L;
+  const int32_t Ti = (int32_t)a.T;
+  const int32_t t_seg0 = g * seg_len;
+  const int32_t t_seg1 = min(t_seg0 + seg_len, Ti);
+  const int32_t nbands = (t_seg1 - t_seg0 + kSBT - 1) / kSBT;
+  const int32_t PQ = a.P * a.Q;
+  const int32_t row_bytes = 2 * a.Wpad;
+  const int32_t b_region = a.buf_bytes - kBandABytes;
+  const int32_t last_kb = t_seg1 / 32 - 1;
+
+  // first padded row read by the band starting at t_b0 (rows_max rows from there fit the tensor)
+  auto band_row0 = [&](int32_t t_b0) {
+    const int32_t z_first = (t_b0 / PQ) * a.Hpad + (t_b0 % PQ) / a.Q;
+    return min(z_first, a.NH - a.rows_max);
+  };
+  auto issue_band = [&](int32_t b) {
+    const int32_t t_b0 = t_seg0 + b * kSBT;
+    uint8_t* dstB = smem + (b & 1) * a.buf_bytes;
+    uint8_t* dstA = dstB + b_region;
+    // A: 4 blocks x 64 rows x 4 pieces of 16 B; slot S holds piece (S & 3) ^ ((row >> 2) & 3) of row S >> 2
+    const int32_t kb0 = t_b0 / 32;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int32_t slot = j * 256 + threadIdx.x;
+      const int32_t row = slot >> 2;
+      const int32_t piece = (slot & 3) ^ ((row >> 2) & 3);
+      const int32_t kb = min(kb0 + (row >> 6), last_kb);  // blocks past the segment reload a valid one (unused)
+      const uint8_t* src = a.ad + ((int64_t)kb * a.Mp + m0 + (row & 63)) * 64 + piece * 16;
+      __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstA + (j * 256 + wave_u * 64) * 16), 16, 0, 0);
+    }
+    // B: padded rows [za, za + rows_max) of channels c_lo .. c_lo + nch_max - 1 (clamped to C - 1)
+    const int32_t za = band_row0(t_b0);
+    const int32_t ppc = a.band_ch_stride / 16;  // = rows_max * row_bytes / 16
+    const int32_t total = a.nch_max * ppc;
+    for (int32_t base = wave_u * 64; base < total; base += 256) {
+      const int32_t pidx = base + lane;
+      if (pidx < total) {
+        const int32_t cc = pidx / ppc, k = pidx - cc * ppc;
+        const int32_t ch = min(c_lo + cc, a.C - 1);
+        const uint8_t* src = a.xb + ((int64_t)ch * a.NH + za) * row_bytes + k * 16;
+        __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstB + base * 16), 16, 0, 0);
+      }
+    }
+  };
+
+  Acc3 acc[2];
+  float sum[2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      acc[i].hh[v] = 0; acc[i].xx[v] = 0; acc[i].ll[v] = 0;
+      sum[i][v] = 0.f;
+    }
+  int32_t j = g * a.G;  // first chunk of the segment
+  int32_t blk_in_chunk = 0;
+  const int32_t chunk_blocks = a.L / 32;
+  const uint32_t smem_base = lds_addr(smem);
+  const uint32_t lane_b = (uint32_t)((c - c_lo) * a.band_ch_stride + rr * row_bytes);
+  const uint32_t rd_a0 = (uint32_t)(swz(lc, 2 * half) * 16), rd_a1 = (uint32_t)(swz(lc, 2 * half + 1) * 16);
+
+  issue_band(0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int32_t b = 0; b < nbands; ++b) {
+    if (b + 1 < nbands) issue_band(b + 1);
+    const int32_t t_b0 = t_seg0 + b * kSBT;
+    const uint32_t bufB = smem_base + (uint32_t)((b & 1) * a.buf_bytes) + lane_b;
+    const uint32_t bufA = smem_base + (uint32_t)((b & 1) * a.buf_bytes + b_region);
+    const int32_t nblk = min(kBandBlocks, (t_seg1 - t_b0) / 32);
+    // run position (uniform): image n, output row p, column q0 of run t_b0 / 8
+    const int32_t za = band_row0(t_b0);
+    int32_t rn = t_b0 / PQ, rp = (t_b0 % PQ) / a.Q, rq = t_b0 % a.Q;
+    for (int32_t kbl = 0; kbl < nblk; ++kbl) {
+      // offsets of the block's four runs; lanes of half h take runs 2h and 2h+1
+      int32_t ro[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        ro[u] = (rn * a.Hpad + rp - za) * row_bytes + rq;
+        rq += 8;
+        if (rq == a.Q) {
+          rq = 0;
+          if (++rp == a.P) { rp = 0; ++rn; }
+        }
+      }
+      const uint32_t to0 = (uint32_t)(half ? ro[2] : ro[0]), to1 = (uint32_t)(half ? ro[3] : ro[1]);
+      v4i ahi[2], alo[2], wl0, wh0, wl1, wh1;
+      const uint32_t ab = bufA + (uint32_t)(kbl * 64 * 64);
+      lds_rd128(ahi[0], ab + rd_a0);
+      lds_rd128(alo[0], ab + rd_a1);
+      lds_rd128(ahi[1], ab + rd_a0 + 2048);  // rows 32..63 sit 2048 bytes on at the same swizzle
+      lds_rd128(alo[1], ab + rd_a1 + 2048);
+      lds_rd2x64(wl0, bufB + to0);
+      lds_rd2x64(wh0, bufB + to0 + a.Wpad);
+      lds_rd2x64(wl1, bufB + to1);
+      lds_rd2x64(wh1, bufB + to1 + a.Wpad);
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(wl0), "+v"(wh0), "+v"(wl1), "+v"(wh1), "+v"(ahi[0]), "+v"(alo[0]), "+v"(ahi[1]),
+                     "+v"(alo[1])
+                   :
+                   : "memory");
+      const v4i blo = {window8_lo(wl0, ss), window8_hi(wl0, ss), window8_lo(wl1, ss), window8_hi(wl1, ss)};
+      const v4i bhi = {window8_lo(wh0, ss), window8_hi(wh0, ss), window8_lo(wh1, ss), window8_hi(wh1, ss)};
+      const bool fresh = blk_in_chunk == 0;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) mfma_tile(acc[i], ahi[i], alo[i], bhi, blo, fresh);
+      if (++blk_in_chunk == chunk_blocks) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          flush_tile<PARTIALS>(acc[i], sum[i], j, a.partials, a.O, colc, CRS, m0 + 32 * i + 4 * half, a.K, cvalid);
+        ++j;
+        blk_in_chunk = 0;
+      }
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+  if (blk_in_chunk != 0) {  // a segment ending inside a chunk (the last one, at T)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      flush_tile<PARTIALS>(acc[i], sum[i], j, a.partials, a.O, colc, CRS, m0 + 32 * i + 4 * half, a.K, cvalid);
+  }
+
+  const int32_t e = a.ea->exp + a.eb->exp;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
+      if (cvalid && m < a.K) {
+        const int32_t o = m * CRS + col;
+        if (a.nseg == 1) a.out[o] = ldexpf(sum[i][v], e);
+        else a.useg[(int64_t)g * a.O + o] = sum[i][v];
+      }
+    }
+  }
+}
+
 // dW = 2^e * (((U_0 + U_1) + U_2) + ...), segment order.
 __global__ __launch_bounds__(64) void k_seg_reduce(const float* __restrict__ useg, float* __restrict__ out, int64_t O,
                                                   int32_t nseg, const dfp_scale* ea, const dfp_scale* eb) {
@@ -434,6 +678,17 @@ BwdwPlan plan_bwdw_mfma(const Geom& g) {
   return p;
 }
 
+// The band kernel's conditions (see k_bwdw_band); returns its LDS bytes or 0.
+static int64_t band_smem(const Geom& g, const BwdwPlan& p) {
+  if (g.sh != 1 || g.sw != 1 || (g.q % 8) != 0 || g.s > 4 || g.pw >= 4 || (g.w % 8) != 0 || (g.L % 32) != 0 ||
+      (p.T % 32) != 0 || p.T >= (1ll << 31))
+    return 0;
+  const int64_t ch_stride = (int64_t)p.rows_max * 2 * p.Wpad;
+  const int64_t buf = kBandABytes + ((p.nch_max * ch_stride + 15) / 16) * 16;
+  const int64_t smem = 2 * buf;
+  return smem <= 64 * 1024 ? smem : 0;
+}
+
 bool bwdw_mfma_supported(const Geom& g) {
   const BwdwPlan p = plan_bwdw_mfma(g);
   return p.smem_bytes <= 64 * 1024;
@@ -450,6 +705,46 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     const int64_t total = p.KBT * p.Mp * 2;
     DFP_LAUNCH(K_WPREP, k_prep_dy, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, dy, ad, g.k, p.Mp,
                g.p * g.q, (int32_t)p.T, (int32_t)p.KBT);
+  }
+  const int64_t bsmem = band_smem(g, p);
+  if (bsmem > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) {
+    uint8_t* xb = reinterpret_cast<uint8_t*>(xp);  // same bytes as the pair layout
+    const int64_t per_c = (int64_t)g.n * p.Hpad * (p.Wpad / 8);
+    const dim3 grid_xb((unsigned)((per_c + 255) / 256), (unsigned)g.c);
+    if (g.pw == 0)
+      DFP_LAUNCH(K_XPREP, k_prep_xb<0>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+    else if (g.pw == 1)
+      DFP_LAUNCH(K_XPREP, k_prep_xb<1>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+    else if (g.pw == 2)
+      DFP_LAUNCH(K_XPREP, k_prep_xb<2>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+    else
+      DFP_LAUNCH(K_XPREP, k_prep_xb<3>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+    BwdwArgs args{};
+    args.ad = ad;
+    args.xb = xb;
+    args.ea = sx;
+    args.eb = sdy;
+    args.out = dw;
+    args.useg = useg;
+    args.partials = partials;
+    args.T = p.T;
+    args.O = (int64_t)g.k * g.c * g.r * g.s;
+    args.K = g.k; args.Mp = p.Mp; args.C = g.c; args.R = g.r; args.S = g.s;
+    args.P = g.p; args.Q = g.q; args.sh = 1; args.sw = 1;
+    args.Hpad = p.Hpad; args.Wpad = p.Wpad; args.NH = g.n * p.Hpad;
+    args.L = g.L; args.G = g.G; args.nseg = p.nseg;
+    args.rows_max = p.rows_max;
+    args.nch_max = p.nch_max;
+    args.band_ch_stride = p.rows_max * 2 * p.Wpad;
+    args.buf_bytes = (int32_t)(bsmem / 2);
+    const dim3 grid((unsigned)((args.O / g.k + kNT - 1) / kNT), (unsigned)(p.Mp / kMT), (unsigned)p.nseg);
+    if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<true>), grid, dim3(kThreads), (size_t)bsmem, st, args);
+    else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<false>), grid, dim3(kThreads), (size_t)bsmem, st, args);
+    if (p.nseg > 1) {
+      DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 63) / 64)), dim3(64), 0, st, useg, dw,
+                 args.O, p.nseg, sx, sdy);
+    }
+    return DFP_OK;
   }
   {
     const int64_t per_c = (int64_t)g.n * p.Hpad * (p.Wpad / 8);

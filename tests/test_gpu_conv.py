@@ -80,6 +80,24 @@ def test_paths_agree(path, L):
         run_all(shape, L, path=path)
 
 
+# Unit-stride layers whose output rows are a multiple of 8 wide and whose
+# reduction length is a multiple of 32: the backward-weights band kernel
+# (runs of 8 indices per output row) takes these, the other shapes above do not.
+BAND_SHAPES = [
+    (2, 16, 8, 8, 32, 3, 3, 1, 1),
+    (1, 24, 16, 16, 40, 3, 3, 1, 1),
+    (2, 8, 12, 24, 16, 1, 1, 1, 0),
+    (4, 32, 7, 8, 20, 3, 3, 1, 1),
+    (2, 64, 24, 16, 64, 3, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", BAND_SHAPES)
+@pytest.mark.parametrize("L,G", [(32, 0), (64, 0), (64, 3), (128, 1), (64, 5)])
+def test_bwd_wt_band_shapes(shape, L, G):
+    run_all(shape, L, G=G)
+
+
 @pytest.mark.parametrize("G", [1, 2, 3, 50])
 def test_bwd_wt_segments(G):
     run_all((4, 16, 12, 12, 8, 3, 3, 1, 1), 16, G=G)
