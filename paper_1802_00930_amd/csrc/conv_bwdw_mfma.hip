@@ -621,6 +621,187 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band(BwdwArgs a) {
   }
 }
 
+// Two-block chunks (L = 64) with every segment a whole number of chunks:
+// the two 32-row tiles run one block out of phase (tile 1 consumes block kb-1
+// while tile 0 consumes block kb, from operands kept in registers), so each
+// chunk conversion of one tile is interleaved with the other tile's MFMAs,
+// and the operand reads of a block are in flight during the lagging tile's
+// work on the previous one.
+__device__ __forceinline__ void interleave_4x16() {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+  }
+}
+
+template <bool PARTIALS>
+__global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int half = lane >> 5;
+  const int lc = lane & 31;
+  const int32_t RS = a.R * a.S;
+  const int32_t CRS = a.C * RS;
+  const int32_t col0 = blockIdx.x * kNT;
+  const int32_t col = col0 + wave * 32 + lc;
+  const bool cvalid = col < CRS;
+  const int32_t colc = cvalid ? col : col0;
+  const int32_t c = colc / RS, rr = (colc % RS) / a.S;
+  const uint32_t ss = (uint32_t)(colc % a.S);
+  const int32_t c_lo = col0 / RS;
+  const int32_t m0 = blockIdx.y * kMT;
+  const int32_t g = blockIdx.z;
+  const int32_t seg_len = a.G * a.L;
+  const int32_t Ti = (int32_t)a.T;
+  const int32_t t_seg0 = g * seg_len;
+  const int32_t t_seg1 = min(t_seg0 + seg_len, Ti);
+  const int32_t nbands = (t_seg1 - t_seg0 + kSBT - 1) / kSBT;
+  const int32_t PQ = a.P * a.Q;
+  const int32_t row_bytes = 2 * a.Wpad;
+  const int32_t b_region = a.buf_bytes - kBandABytes;
+  const int32_t last_kb = t_seg1 / 32 - 1;
+
+  auto band_row0 = [&](int32_t t_b0) {
+    const int32_t z_first = (t_b0 / PQ) * a.Hpad + (t_b0 % PQ) / a.Q;
+    return min(z_first, a.NH - a.rows_max);
+  };
+  auto issue_band = [&](int32_t b) {
+    const int32_t t_b0 = t_seg0 + b * kSBT;
+    uint8_t* dstB = smem + (b & 1) * a.buf_bytes;
+    uint8_t* dstA = dstB + b_region;
+    const int32_t kb0 = t_b0 / 32;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int32_t slot = j * 256 + threadIdx.x;
+      const int32_t row = slot >> 2;
+      const int32_t piece = (slot & 3) ^ ((row >> 2) & 3);
+      const int32_t kb = min(kb0 + (row >> 6), last_kb);
+      const uint8_t* src = a.ad + ((int64_t)kb * a.Mp + m0 + (row & 63)) * 64 + piece * 16;
+      __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstA + (j * 256 + wave_u * 64) * 16), 16, 0, 0);
+    }
+    const int32_t za = band_row0(t_b0);
+    const int32_t ppc = a.band_ch_stride / 16;
+    const int32_t total = a.nch_max * ppc;
+    for (int32_t base = wave_u * 64; base < total; base += 256) {
+      const int32_t pidx = base + lane;
+      if (pidx < total) {
+        const int32_t cc = pidx / ppc, k = pidx - cc * ppc;
+        const int32_t ch = min(c_lo + cc, a.C - 1);
+        const uint8_t* src = a.xb + ((int64_t)ch * a.NH + za) * row_bytes + k * 16;
+        __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstB + base * 16), 16, 0, 0);
+      }
+    }
+  };
+
+  Acc3 acc0, acc1;
+  float sum0[16], sum1[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) { sum0[v] = 0.f; sum1[v] = 0.f; }
+  const int32_t j0 = g * a.G;  // first chunk of the segment
+  const uint32_t smem_base = lds_addr(smem);
+  const uint32_t lane_b = (uint32_t)((c - c_lo) * a.band_ch_stride + rr * row_bytes);
+  const uint32_t rd_a0 = (uint32_t)(swz(lc, 2 * half) * 16), rd_a1 = (uint32_t)(swz(lc, 2 * half + 1) * 16);
+  const int32_t mrow0 = m0 + 4 * half, mrow1 = m0 + 32 + 4 * half;
+
+  v4i ca0h, ca0l, ca1h, ca1l, wl0, wh0, wl1, wh1;  // block being read
+  v4i pa1h, pa1l, pbh, pbl;                        // tile 1's lagging block
+  int32_t rn = 0, rp = 0, rq = 0, za = 0;          // run position (uniform)
+  auto read_block = [&](uint32_t bufA, uint32_t bufB, int32_t kbl) {
+    int32_t ro[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      ro[u] = (rn * a.Hpad + rp - za) * row_bytes + rq;
+      rq += 8;
+      if (rq == a.Q) {
+        rq = 0;
+        if (++rp == a.P) { rp = 0; ++rn; }
+      }
+    }
+    const uint32_t to0 = (uint32_t)(half ? ro[2] : ro[0]), to1 = (uint32_t)(half ? ro[3] : ro[1]);
+    const uint32_t ab = bufA + (uint32_t)(kbl * 64 * 64);
+    lds_rd128(ca0h, ab + rd_a0);
+    lds_rd128(ca0l, ab + rd_a1);
+    lds_rd128(ca1h, ab + rd_a0 + 2048);
+    lds_rd128(ca1l, ab + rd_a1 + 2048);
+    lds_rd2x64(wl0, bufB + to0);
+    lds_rd2x64(wh0, bufB + to0 + a.Wpad);
+    lds_rd2x64(wl1, bufB + to1);
+    lds_rd2x64(wh1, bufB + to1 + a.Wpad);
+  };
+  auto wait_block = [&]() {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(wl0), "+v"(wh0), "+v"(wl1), "+v"(wh1), "+v"(ca0h), "+v"(ca0l), "+v"(ca1h), "+v"(ca1l)
+                 :
+                 : "memory");
+  };
+  auto b_ops = [&](v4i& bhi, v4i& blo) {
+    blo = (v4i){window8_lo(wl0, ss), window8_hi(wl0, ss), window8_lo(wl1, ss), window8_hi(wl1, ss)};
+    bhi = (v4i){window8_lo(wh0, ss), window8_hi(wh0, ss), window8_lo(wh1, ss), window8_hi(wh1, ss)};
+  };
+
+  issue_band(0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  int32_t kbs = 0;  // block index inside the segment
+  for (int32_t b = 0; b < nbands; ++b) {
+    if (b + 1 < nbands) issue_band(b + 1);
+    const int32_t t_b0 = t_seg0 + b * kSBT;
+    const uint32_t bufB = smem_base + (uint32_t)((b & 1) * a.buf_bytes) + lane_b;
+    const uint32_t bufA = smem_base + (uint32_t)((b & 1) * a.buf_bytes + b_region);
+    const int32_t nblk = min(kBandBlocks, (t_seg1 - t_b0) / 32);  // even: segments are whole chunks
+    za = band_row0(t_b0);
+    rn = t_b0 / PQ; rp = (t_b0 % PQ) / a.Q; rq = t_b0 % a.Q;
+    for (int32_t kbl = 0; kbl < nblk; kbl += 2, kbs += 2) {
+      // even block kbs: tile 0 opens chunk kbs/2; tile 1 finishes chunk kbs/2 - 1 on block kbs - 1
+      read_block(bufA, bufB, kbl);
+      if (kbs > 0) {
+        flush_tile<PARTIALS>(acc0, sum0, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow0, a.K, cvalid);
+        mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+        interleave_4x16();
+      }
+      wait_block();
+      v4i bhi, blo;
+      b_ops(bhi, blo);
+      mfma_tile(acc0, ca0h, ca0l, bhi, blo, true);
+      pa1h = ca1h; pa1l = ca1l; pbh = bhi; pbl = blo;
+      // odd block kbs + 1: tile 0 continues; tile 1 opens chunk kbs/2 on block kbs
+      read_block(bufA, bufB, kbl + 1);
+      wait_block();
+      b_ops(bhi, blo);
+      if (kbs > 0) flush_tile<PARTIALS>(acc1, sum1, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow1, a.K, cvalid);
+      mfma_tile(acc0, ca0h, ca0l, bhi, blo, false);
+      if (kbs > 0) interleave_4x16();
+      mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
+      pa1h = ca1h; pa1l = ca1l; pbh = bhi; pbl = blo;
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+  // last chunk: tile 0 is complete; tile 1 still owes its final block
+  flush_tile<PARTIALS>(acc0, sum0, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow0, a.K, cvalid);
+  mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+  interleave_4x16();
+  flush_tile<PARTIALS>(acc1, sum1, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow1, a.K, cvalid);
+
+  const int32_t e = a.ea->exp + a.eb->exp;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
+      if (cvalid && m < a.K) {
+        const int32_t o = m * CRS + col;
+        const float sv = i == 0 ? sum0[v] : sum1[v];
+        if (a.nseg == 1) a.out[o] = ldexpf(sv, e);
+        else a.useg[(int64_t)g * a.O + o] = sv;
+      }
+    }
+  }
+}
+
 // dW = 2^e * (((U_0 + U_1) + U_2) + ...), segment order.
 __global__ __launch_bounds__(64) void k_seg_reduce(const float* __restrict__ useg, float* __restrict__ out, int64_t O,
                                                   int32_t nseg, const dfp_scale* ea, const dfp_scale* eb) {
@@ -738,8 +919,13 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.band_ch_stride = p.rows_max * 2 * p.Wpad;
     args.buf_bytes = (int32_t)(bsmem / 2);
     const dim3 grid((unsigned)((args.O / g.k + kNT - 1) / kNT), (unsigned)(p.Mp / kMT), (unsigned)p.nseg);
-    if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<true>), grid, dim3(kThreads), (size_t)bsmem, st, args);
-    else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<false>), grid, dim3(kThreads), (size_t)bsmem, st, args);
+    if (g.L == 64 && (p.T % 64) == 0) {  // every segment a whole number of two-block chunks
+      if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<true>), grid, dim3(kThreads), (size_t)bsmem, st, args);
+      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<false>), grid, dim3(kThreads), (size_t)bsmem, st, args);
+    } else {
+      if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<true>), grid, dim3(kThreads), (size_t)bsmem, st, args);
+      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<false>), grid, dim3(kThreads), (size_t)bsmem, st, args);
+    }
     if (p.nseg > 1) {
       DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 63) / 64)), dim3(64), 0, st, useg, dw,
                  args.O, p.nseg, sx, sdy);
