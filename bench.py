@@ -49,7 +49,21 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES five times (counter calibration)")
     return ap.parse_args()
+
+
+def copy_probe(nbytes):
+    """A plain copy kernel of known size: its FETCH_SIZE / WRITE_SIZE counters
+    calibrate the byte counts of the DFP kernels (rocprofv3 --pmc)."""
+    import torch
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes, "launches": 5}), flush=True)
 
 
 class Step:
@@ -154,6 +168,9 @@ def cpu_baseline(layer, x, w, dy, L, G, rounding, seed, budget_s):
 
 def main():
     a = parse()
+    if a.copy_probe:
+        copy_probe(a.copy_probe)
+        return
     if a.gpus != 1:
         print("bench.py: this build runs on one GPU only (the path is per-GPU); --gpus %d is not supported"
               % a.gpus, file=sys.stderr)

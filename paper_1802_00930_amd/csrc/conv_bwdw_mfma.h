@@ -26,7 +26,7 @@ struct BwdwArgs {
   int32_t* partials;
   int64_t T, O;
   int32_t K, Mp, C, R, S, P, Q, sh, sw, Hpad, Wpad, NH, L, G, nseg, band_bytes, band_ch_stride;
-  int32_t rows_max, nch_max, buf_bytes;  // band kernel: rows and channels per band, bytes per buffer
+  int32_t rows_max, nch_max, buf_bytes, row_bytes;  // band kernel: rows / channels per band, buffer and row bytes
 };
 
 BwdwPlan plan_bwdw_mfma(const Geom& g);

@@ -393,6 +393,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_mfma(BwdwArgs a) {
 // workgroup's channels; one barrier per band.
 constexpr int kBandBlocks = kSBT / 32;               // 4
 constexpr int kBandABytes = kBandBlocks * kMT * 64;  // 16 KiB
+constexpr int kBandLdsBytes = 76 * 1024;             // two buffers; two workgroups per CU
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -402,12 +403,13 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 __device__ __forceinline__ int swz(int row, int piece) { return row * 4 + (piece ^ ((row >> 2) & 3)); }
 
 // XB[c][n*Hpad + u][d][Wpad]: d = 0 lo digits, d = 1 hi digits of
-// x[n][c][u - ph][v - pw], zero outside.  Rows of a multiple of 8 elements,
+// x[n][c][u - ph][v - pw], zero outside; rows are row_bytes = 2*Wpad + 16 apart
+// (the 16 spare bytes shift successive rows across LDS banks).  Rows of a multiple of 8 elements,
 // 16-byte aligned, column pad PW below 4 (same windowing as k_prep_xp_vec).
 template <int PW>
 __global__ __launch_bounds__(256) void k_prep_xb(const int16_t* __restrict__ x, uint8_t* __restrict__ xb, int32_t N,
                                                 int32_t C, int32_t H, int32_t W, int32_t Hpad, int32_t Wpad,
-                                                int32_t ph) {
+                                                int32_t ph, int32_t row_bytes) {
   const int32_t c = blockIdx.y;
   const int32_t i = blockIdx.x * 256 + threadIdx.x;  // (n * Hpad + u) * W8 + v8
   const int32_t W8 = Wpad >> 3;
@@ -435,7 +437,7 @@ __global__ __launch_bounds__(256) void k_prep_xb(const int16_t* __restrict__ x, 
       hi[k >> 2] |= hi_digit(a) << (8 * (k & 3));
     }
   }
-  uint8_t* rowp = xb + ((int64_t)c * N * Hpad + r) * 2 * Wpad + v0;
+  uint8_t* rowp = xb + ((int64_t)c * N * Hpad + r) * row_bytes + v0;
   *reinterpret_cast<uint2*>(rowp) = make_uint2(lo[0], lo[1]);
   *reinterpret_cast<uint2*>(rowp + Wpad) = make_uint2(hi[0], hi[1]);
 }
@@ -466,7 +468,7 @@ template <bool PARTIALS>
 __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band(BwdwArgs a) {
   // two buffers, each [B band: nch_max channels x rows_max padded rows x 2 planes x Wpad][A: 16 KiB];
   // a B window read past the last row stays inside the A part that follows it
-  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ __align__(16) uint8_t smem[kBandLdsBytes];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
@@ -489,7 +491,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band(BwdwArgs a) {
   const int32_t t_seg1 = min(t_seg0 + seg_len, Ti);
   const int32_t nbands = (t_seg1 - t_seg0 + kSBT - 1) / kSBT;
   const int32_t PQ = a.P * a.Q;
-  const int32_t row_bytes = 2 * a.Wpad;
+  const int32_t row_bytes = a.row_bytes;
   const int32_t b_region = a.buf_bytes - kBandABytes;
   const int32_t last_kb = t_seg1 / 32 - 1;
 
@@ -513,17 +515,18 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band(BwdwArgs a) {
       const uint8_t* src = a.ad + ((int64_t)kb * a.Mp + m0 + (row & 63)) * 64 + piece * 16;
       __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstA + (j * 256 + wave_u * 64) * 16), 16, 0, 0);
     }
-    // B: padded rows [za, za + rows_max) of channels c_lo .. c_lo + nch_max - 1 (clamped to C - 1)
+    // B: rows [za, za + rows_max) of each channel, one group of up to 64 pieces per instruction
     const int32_t za = band_row0(t_b0);
-    const int32_t ppc = a.band_ch_stride / 16;  // = rows_max * row_bytes / 16
-    const int32_t total = a.nch_max * ppc;
-    for (int32_t base = wave_u * 64; base < total; base += 256) {
-      const int32_t pidx = base + lane;
-      if (pidx < total) {
-        const int32_t cc = pidx / ppc, k = pidx - cc * ppc;
+    const int32_t ppc = a.rows_max * row_bytes / 16;
+    const int32_t nk = (ppc + 63) / 64;
+    for (int32_t ii = wave_u; ii < a.nch_max * nk; ii += kThreads / 64) {
+      const int32_t cc = ii / nk, k0 = (ii - cc * nk) * 64;
+      const int32_t k = k0 + lane;
+      if (k < ppc) {
         const int32_t ch = min(c_lo + cc, a.C - 1);
         const uint8_t* src = a.xb + ((int64_t)ch * a.NH + za) * row_bytes + k * 16;
-        __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstB + base * 16), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstB + cc * a.band_ch_stride + k0 * 16), 16,
+                                         0, 0);
       }
     }
   };
@@ -637,7 +640,7 @@ __device__ __forceinline__ void interleave_4x16() {
 
 template <bool PARTIALS>
 __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
-  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ __align__(16) uint8_t smem[kBandLdsBytes];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
@@ -660,7 +663,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
   const int32_t t_seg1 = min(t_seg0 + seg_len, Ti);
   const int32_t nbands = (t_seg1 - t_seg0 + kSBT - 1) / kSBT;
   const int32_t PQ = a.P * a.Q;
-  const int32_t row_bytes = 2 * a.Wpad;
+  const int32_t row_b = a.row_bytes;
   const int32_t b_region = a.buf_bytes - kBandABytes;
   const int32_t last_kb = t_seg1 / 32 - 1;
 
@@ -682,16 +685,18 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
       const uint8_t* src = a.ad + ((int64_t)kb * a.Mp + m0 + (row & 63)) * 64 + piece * 16;
       __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstA + (j * 256 + wave_u * 64) * 16), 16, 0, 0);
     }
+    // B: rows [za, za + rows_max) of each channel, one group of up to 64 pieces per instruction
     const int32_t za = band_row0(t_b0);
-    const int32_t ppc = a.band_ch_stride / 16;
-    const int32_t total = a.nch_max * ppc;
-    for (int32_t base = wave_u * 64; base < total; base += 256) {
-      const int32_t pidx = base + lane;
-      if (pidx < total) {
-        const int32_t cc = pidx / ppc, k = pidx - cc * ppc;
+    const int32_t ppc = a.rows_max * row_b / 16;
+    const int32_t nk = (ppc + 63) / 64;
+    for (int32_t ii = wave_u; ii < a.nch_max * nk; ii += kThreads / 64) {
+      const int32_t cc = ii / nk, k0 = (ii - cc * nk) * 64;
+      const int32_t k = k0 + lane;
+      if (k < ppc) {
         const int32_t ch = min(c_lo + cc, a.C - 1);
-        const uint8_t* src = a.xb + ((int64_t)ch * a.NH + za) * row_bytes + k * 16;
-        __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstB + base * 16), 16, 0, 0);
+        const uint8_t* src = a.xb + ((int64_t)ch * a.NH + za) * row_b + k * 16;
+        __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstB + cc * a.band_ch_stride + k0 * 16), 16,
+                                         0, 0);
       }
     }
   };
@@ -702,18 +707,21 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
   for (int v = 0; v < 16; ++v) { sum0[v] = 0.f; sum1[v] = 0.f; }
   const int32_t j0 = g * a.G;  // first chunk of the segment
   const uint32_t smem_base = lds_addr(smem);
-  const uint32_t lane_b = (uint32_t)((c - c_lo) * a.band_ch_stride + rr * row_bytes);
+  const uint32_t lane_b = (uint32_t)((c - c_lo) * a.band_ch_stride + rr * row_b);
   const uint32_t rd_a0 = (uint32_t)(swz(lc, 2 * half) * 16), rd_a1 = (uint32_t)(swz(lc, 2 * half + 1) * 16);
   const int32_t mrow0 = m0 + 4 * half, mrow1 = m0 + 32 + 4 * half;
 
-  v4i ca0h, ca0l, ca1h, ca1l, wl0, wh0, wl1, wh1;  // block being read
-  v4i pa1h, pa1l, pbh, pbl;                        // tile 1's lagging block
-  int32_t rn = 0, rp = 0, rq = 0, za = 0;          // run position (uniform)
-  auto read_block = [&](uint32_t bufA, uint32_t bufB, int32_t kbl) {
+  // Operand sets X (even blocks) and Y (odd blocks): tile 1 lags on the other set, so no copies.
+  struct Ops {
+    v4i a0h, a0l, a1h, a1l, bh, bl;
+  };
+  Ops X, Y;
+  int32_t rn = 0, rp = 0, rq = 0, za = 0;  // run position (uniform)
+  auto read_block = [&](Ops& o, uint32_t bufA, uint32_t bufB, int32_t kbl) {
     int32_t ro[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      ro[u] = (rn * a.Hpad + rp - za) * row_bytes + rq;
+      ro[u] = (rn * a.Hpad + rp - za) * row_b + rq;
       rq += 8;
       if (rq == a.Q) {
         rq = 0;
@@ -722,24 +730,21 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
     }
     const uint32_t to0 = (uint32_t)(half ? ro[2] : ro[0]), to1 = (uint32_t)(half ? ro[3] : ro[1]);
     const uint32_t ab = bufA + (uint32_t)(kbl * 64 * 64);
-    lds_rd128(ca0h, ab + rd_a0);
-    lds_rd128(ca0l, ab + rd_a1);
-    lds_rd128(ca1h, ab + rd_a0 + 2048);
-    lds_rd128(ca1l, ab + rd_a1 + 2048);
+    v4i wl0, wh0, wl1, wh1;
+    lds_rd128(o.a0h, ab + rd_a0);
+    lds_rd128(o.a0l, ab + rd_a1);
+    lds_rd128(o.a1h, ab + rd_a0 + 2048);
+    lds_rd128(o.a1l, ab + rd_a1 + 2048);
     lds_rd2x64(wl0, bufB + to0);
     lds_rd2x64(wh0, bufB + to0 + a.Wpad);
     lds_rd2x64(wl1, bufB + to1);
     lds_rd2x64(wh1, bufB + to1 + a.Wpad);
-  };
-  auto wait_block = [&]() {
     asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(wl0), "+v"(wh0), "+v"(wl1), "+v"(wh1), "+v"(ca0h), "+v"(ca0l), "+v"(ca1h), "+v"(ca1l)
+                 : "+v"(wl0), "+v"(wh0), "+v"(wl1), "+v"(wh1), "+v"(o.a0h), "+v"(o.a0l), "+v"(o.a1h), "+v"(o.a1l)
                  :
                  : "memory");
-  };
-  auto b_ops = [&](v4i& bhi, v4i& blo) {
-    blo = (v4i){window8_lo(wl0, ss), window8_hi(wl0, ss), window8_lo(wl1, ss), window8_hi(wl1, ss)};
-    bhi = (v4i){window8_lo(wh0, ss), window8_hi(wh0, ss), window8_lo(wh1, ss), window8_hi(wh1, ss)};
+    o.bl = (v4i){window8_lo(wl0, ss), window8_hi(wl0, ss), window8_lo(wl1, ss), window8_hi(wl1, ss)};
+    o.bh = (v4i){window8_lo(wh0, ss), window8_hi(wh0, ss), window8_lo(wh1, ss), window8_hi(wh1, ss)};
   };
 
   issue_band(0);
@@ -755,34 +760,27 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
     za = band_row0(t_b0);
     rn = t_b0 / PQ; rp = (t_b0 % PQ) / a.Q; rq = t_b0 % a.Q;
     for (int32_t kbl = 0; kbl < nblk; kbl += 2, kbs += 2) {
-      // even block kbs: tile 0 opens chunk kbs/2; tile 1 finishes chunk kbs/2 - 1 on block kbs - 1
-      read_block(bufA, bufB, kbl);
+      // even block kbs (set X): tile 0 opens chunk kbs/2; tile 1 finishes chunk kbs/2 - 1 on block kbs - 1 (Y)
       if (kbs > 0) {
         flush_tile<PARTIALS>(acc0, sum0, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow0, a.K, cvalid);
-        mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+        mfma_tile(acc1, Y.a1h, Y.a1l, Y.bh, Y.bl, false);
         interleave_4x16();
       }
-      wait_block();
-      v4i bhi, blo;
-      b_ops(bhi, blo);
-      mfma_tile(acc0, ca0h, ca0l, bhi, blo, true);
-      pa1h = ca1h; pa1l = ca1l; pbh = bhi; pbl = blo;
-      // odd block kbs + 1: tile 0 continues; tile 1 opens chunk kbs/2 on block kbs
-      read_block(bufA, bufB, kbl + 1);
-      wait_block();
-      b_ops(bhi, blo);
+      read_block(X, bufA, bufB, kbl);
+      mfma_tile(acc0, X.a0h, X.a0l, X.bh, X.bl, true);
+      // odd block kbs + 1 (set Y): tile 0 continues; tile 1 opens chunk kbs/2 on block kbs (X)
+      read_block(Y, bufA, bufB, kbl + 1);
       if (kbs > 0) flush_tile<PARTIALS>(acc1, sum1, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow1, a.K, cvalid);
-      mfma_tile(acc0, ca0h, ca0l, bhi, blo, false);
+      mfma_tile(acc0, Y.a0h, Y.a0l, Y.bh, Y.bl, false);
       if (kbs > 0) interleave_4x16();
-      mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
-      pa1h = ca1h; pa1l = ca1l; pbh = bhi; pbl = blo;
+      mfma_tile(acc1, X.a1h, X.a1l, X.bh, X.bl, true);
     }
     wait_vmcnt<0>();
     __syncthreads();
   }
-  // last chunk: tile 0 is complete; tile 1 still owes its final block
+  // last chunk: tile 0 is complete; tile 1 still owes its final block (Y)
   flush_tile<PARTIALS>(acc0, sum0, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow0, a.K, cvalid);
-  mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+  mfma_tile(acc1, Y.a1h, Y.a1l, Y.bh, Y.bl, false);
   interleave_4x16();
   flush_tile<PARTIALS>(acc1, sum1, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow1, a.K, cvalid);
 
@@ -853,21 +851,33 @@ BwdwPlan plan_bwdw_mfma(const Geom& g) {
   p.band_bytes = align256((int64_t)p.nch_max * p.band_ch_stride * 2);
   p.smem_bytes = p.band_bytes + kSBT * 4;
   p.ad_bytes = align256(p.KBT * p.Mp * 64);
-  p.xp_bytes = align256((int64_t)g.c * g.n * p.Hpad * p.Wpad * 2);
+  // pair layout [C][N*Hpad][Wpad] u16, or the band kernel's byte planes with 16 spare bytes per row
+  p.xp_bytes = align256((int64_t)g.c * g.n * p.Hpad * (2 * p.Wpad + 16));
   p.u_bytes = p.nseg > 1 ? align256((int64_t)p.nseg * g.k * g.c * RS * 4) : 0;
   p.bytes = p.ad_bytes + p.xp_bytes + p.u_bytes;
   return p;
 }
 
-// The band kernel's conditions (see k_bwdw_band); returns its LDS bytes or 0.
-static int64_t band_smem(const Geom& g, const BwdwPlan& p) {
+// Band kernel geometry: row stride, channel stride (bytes) and bytes per
+// buffer; buf_bytes = 0 when the layer does not meet the kernel's conditions.
+struct BandLayout {
+  int32_t row_bytes, ch_stride, buf_bytes;
+};
+static BandLayout band_layout(const Geom& g, const BwdwPlan& p) {
+  BandLayout bl{0, 0, 0};
   if (g.sh != 1 || g.sw != 1 || (g.q % 8) != 0 || g.s > 4 || g.pw >= 4 || (g.w % 8) != 0 || (g.L % 32) != 0 ||
       (p.T % 32) != 0 || p.T >= (1ll << 31))
-    return 0;
-  const int64_t ch_stride = (int64_t)p.rows_max * 2 * p.Wpad;
-  const int64_t buf = kBandABytes + ((p.nch_max * ch_stride + 15) / 16) * 16;
-  const int64_t smem = 2 * buf;
-  return smem <= 64 * 1024 ? smem : 0;
+    return bl;
+  bl.row_bytes = 2 * p.Wpad + 16;
+  // channel stride congruent to 64 mod 256: with the odd row stride above, the
+  // (channel, filter row) pairs of a wave fall on distinct LDS bank groups
+  int64_t chs = (int64_t)p.rows_max * bl.row_bytes;
+  chs += (64 - chs % 256 + 256) % 256;
+  const int64_t buf = kBandABytes + p.nch_max * chs;
+  if (2 * buf > kBandLdsBytes) return bl;
+  bl.ch_stride = (int32_t)chs;
+  bl.buf_bytes = (int32_t)buf;
+  return bl;
 }
 
 bool bwdw_mfma_supported(const Geom& g) {
@@ -887,19 +897,23 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     DFP_LAUNCH(K_WPREP, k_prep_dy, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, dy, ad, g.k, p.Mp,
                g.p * g.q, (int32_t)p.T, (int32_t)p.KBT);
   }
-  const int64_t bsmem = band_smem(g, p);
-  if (bsmem > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) {
-    uint8_t* xb = reinterpret_cast<uint8_t*>(xp);  // same bytes as the pair layout
+  const BandLayout bl = band_layout(g, p);
+  if (bl.buf_bytes > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) {
+    uint8_t* xb = reinterpret_cast<uint8_t*>(xp);  // same workspace region as the pair layout
     const int64_t per_c = (int64_t)g.n * p.Hpad * (p.Wpad / 8);
     const dim3 grid_xb((unsigned)((per_c + 255) / 256), (unsigned)g.c);
     if (g.pw == 0)
-      DFP_LAUNCH(K_XPREP, k_prep_xb<0>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+      DFP_LAUNCH(K_XPREP, k_prep_xb<0>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
+                 bl.row_bytes);
     else if (g.pw == 1)
-      DFP_LAUNCH(K_XPREP, k_prep_xb<1>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+      DFP_LAUNCH(K_XPREP, k_prep_xb<1>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
+                 bl.row_bytes);
     else if (g.pw == 2)
-      DFP_LAUNCH(K_XPREP, k_prep_xb<2>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+      DFP_LAUNCH(K_XPREP, k_prep_xb<2>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
+                 bl.row_bytes);
     else
-      DFP_LAUNCH(K_XPREP, k_prep_xb<3>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph);
+      DFP_LAUNCH(K_XPREP, k_prep_xb<3>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
+                 bl.row_bytes);
     BwdwArgs args{};
     args.ad = ad;
     args.xb = xb;
@@ -916,15 +930,16 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.L = g.L; args.G = g.G; args.nseg = p.nseg;
     args.rows_max = p.rows_max;
     args.nch_max = p.nch_max;
-    args.band_ch_stride = p.rows_max * 2 * p.Wpad;
-    args.buf_bytes = (int32_t)(bsmem / 2);
+    args.band_ch_stride = bl.ch_stride;
+    args.buf_bytes = bl.buf_bytes;
+    args.row_bytes = bl.row_bytes;
     const dim3 grid((unsigned)((args.O / g.k + kNT - 1) / kNT), (unsigned)(p.Mp / kMT), (unsigned)p.nseg);
     if (g.L == 64 && (p.T % 64) == 0) {  // every segment a whole number of two-block chunks
-      if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<true>), grid, dim3(kThreads), (size_t)bsmem, st, args);
-      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<false>), grid, dim3(kThreads), (size_t)bsmem, st, args);
+      if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<true>), grid, dim3(kThreads), 0, st, args);
+      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<false>), grid, dim3(kThreads), 0, st, args);
     } else {
-      if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<true>), grid, dim3(kThreads), (size_t)bsmem, st, args);
-      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<false>), grid, dim3(kThreads), (size_t)bsmem, st, args);
+      if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<true>), grid, dim3(kThreads), 0, st, args);
+      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<false>), grid, dim3(kThreads), 0, st, args);
     }
     if (p.nseg > 1) {
       DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 63) / 64)), dim3(64), 0, st, useg, dw,
