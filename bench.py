@@ -54,6 +54,23 @@ def parse():
     return ap.parse_args()
 
 
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE passes (calibrated on a plain copy), or None when they were taken
+    on another kernel or on a source that has changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_conv2x_3x3.json")
+    try:
+        rec = json.load(open(path))
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, ValueError, KeyError):
+        return None
+    if rec.get("kernel") != kernel or hashlib.sha256(src).hexdigest() != rec.get("source_sha256"):
+        return None
+    return {"bytes": int(rec["fetch_bytes"] + rec["write_bytes"]), "fetch_bytes": int(rec["fetch_bytes"]),
+            "write_bytes": int(rec["write_bytes"]), "source": rec.get("summary")}
+
+
 def copy_probe(nbytes):
     """A plain copy kernel of known size: its FETCH_SIZE / WRITE_SIZE counters
     calibrate the byte counts of the DFP kernels (rocprofv3 --pmc)."""
@@ -199,6 +216,7 @@ def main():
     mfma = "mfma" in dominant
     peak = PEAK_INT16_BYTESPLIT_TOPS if mfma else PEAK_VALU_DOT2_TOPS
     achieved = ops_per_dir / (dk["avg_ms"] * 1e-3) / 1e12
+    traffic = measured_traffic(dominant)
     per_dir = {}
     for k, v in conv_kernels.items():
         per_dir[k] = {"avg_ms": round(v["avg_ms"], 5),
@@ -238,7 +256,8 @@ def main():
             "peak": peak,
             "unit": "TOP/s (INT16-equivalent ops)" if mfma else "TOP/s (INT16 ops)",
             "frac": round(achieved / peak, 4),
-            "traffic": None,
+            "traffic": (traffic or {}).get("bytes"),
+            "traffic_detail": traffic,
         },
         "per_direction": per_dir,
         "kernels": {k: {kk: round(vv, 5) for kk, vv in v.items()} for k, v in kstats.items()},
