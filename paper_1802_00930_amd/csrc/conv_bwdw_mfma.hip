@@ -667,10 +667,12 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
   const int32_t b_region = a.buf_bytes - kBandABytes;
   const int32_t last_kb = t_seg1 / 32 - 1;
 
-  auto band_row0 = [&](int32_t t_b0) {
-    const int32_t z_first = (t_b0 / PQ) * a.Hpad + (t_b0 % PQ) / a.Q;
-    return min(z_first, a.NH - a.rows_max);
-  };
+  // Band cursor: output position (n, p, q) of the first index of the next band
+  // to be copied, advanced without divisions; the copy records each band's
+  // position and first padded row for the reads that follow (two bands live).
+  int32_t cn = t_seg0 / PQ, cp = (t_seg0 % PQ) / a.Q, cq = t_seg0 % a.Q;
+  int32_t pn0 = 0, pp0 = 0, pq0 = 0, pza0 = 0, pn1 = 0, pp1 = 0, pq1 = 0, pza1 = 0;
+  const int32_t ppc = a.rows_max * row_b / 16;  // 16-byte pieces per channel
   auto issue_band = [&](int32_t b) {
     const int32_t t_b0 = t_seg0 + b * kSBT;
     uint8_t* dstB = smem + (b & 1) * a.buf_bytes;
@@ -685,19 +687,27 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
       const uint8_t* src = a.ad + ((int64_t)kb * a.Mp + m0 + (row & 63)) * 64 + piece * 16;
       __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstA + (j * 256 + wave_u * 64) * 16), 16, 0, 0);
     }
-    // B: rows [za, za + rows_max) of each channel, one group of up to 64 pieces per instruction
-    const int32_t za = band_row0(t_b0);
-    const int32_t ppc = a.rows_max * row_b / 16;
-    const int32_t nk = (ppc + 63) / 64;
-    for (int32_t ii = wave_u; ii < a.nch_max * nk; ii += kThreads / 64) {
-      const int32_t cc = ii / nk, k0 = (ii - cc * nk) * 64;
-      const int32_t k = k0 + lane;
-      if (k < ppc) {
-        const int32_t ch = min(c_lo + cc, a.C - 1);
-        const uint8_t* src = a.xb + ((int64_t)ch * a.NH + za) * row_b + k * 16;
-        __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstB + cc * a.band_ch_stride + k0 * 16), 16,
-                                         0, 0);
+    // B: rows [za, za + rows_max) of each channel (wave w copies channels w, w + 4, ...)
+    const int32_t za = min(cn * a.Hpad + cp, a.NH - a.rows_max);
+    for (int32_t cc = wave_u; cc < a.nch_max; cc += kThreads / 64) {
+      const int32_t ch = min(c_lo + cc, a.C - 1);
+      const uint8_t* srcc = a.xb + ((int64_t)ch * a.NH + za) * row_b;
+      uint8_t* dstc = dstB + cc * a.band_ch_stride;
+      for (int32_t k0 = 0; k0 < ppc; k0 += 64) {
+        const int32_t k = k0 + lane;
+        if (k < ppc)
+          __builtin_amdgcn_global_load_lds((const void*)(srcc + k * 16), (lds_ptr_t)(dstc + k0 * 16), 16, 0, 0);
       }
+    }
+    if (b & 1) {
+      pn1 = cn; pp1 = cp; pq1 = cq; pza1 = za;
+    } else {
+      pn0 = cn; pp0 = cp; pq0 = cq; pza0 = za;
+    }
+    cq += kSBT;
+    while (cq >= a.Q) {
+      cq -= a.Q;
+      if (++cp == a.P) { cp = 0; ++cn; }
     }
   };
 
@@ -711,13 +721,26 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
   const uint32_t rd_a0 = (uint32_t)(swz(lc, 2 * half) * 16), rd_a1 = (uint32_t)(swz(lc, 2 * half + 1) * 16);
   const int32_t mrow0 = m0 + 4 * half, mrow1 = m0 + 32 + 4 * half;
 
-  // Operand sets X (even blocks) and Y (odd blocks): tile 1 lags on the other set, so no copies.
-  struct Ops {
-    v4i a0h, a0l, a1h, a1l, bh, bl;
+  // Raw operand reads of one block (A rows of both tiles, four B windows), in
+  // flight from one block to the next: the reads of block kbs+1 are issued
+  // before the conversions and MFMAs of block kbs.
+  struct Raw {
+    v4i a0h, a0l, a1h, a1l, wl0, wh0, wl1, wh1;
   };
-  Ops X, Y;
-  int32_t rn = 0, rp = 0, rq = 0, za = 0;  // run position (uniform)
-  auto read_block = [&](Ops& o, uint32_t bufA, uint32_t bufB, int32_t kbl) {
+  Raw R0, R1;
+  int32_t rn = 0, rp = 0, rq = 0, za = 0, rkbl = 0;  // read position (uniform)
+  uint32_t rbufA = 0, rbufB = 0;
+  auto start_read_band = [&](int32_t bn) {
+    const int slot = bn & 1;
+    rn = slot ? pn1 : pn0;
+    rp = slot ? pp1 : pp0;
+    rq = slot ? pq1 : pq0;
+    za = slot ? pza1 : pza0;
+    rbufB = smem_base + (uint32_t)(slot * a.buf_bytes) + lane_b;
+    rbufA = smem_base + (uint32_t)(slot * a.buf_bytes + b_region);
+    rkbl = 0;
+  };
+  auto issue_reads = [&](Raw& r) {
     int32_t ro[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -729,60 +752,76 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
       }
     }
     const uint32_t to0 = (uint32_t)(half ? ro[2] : ro[0]), to1 = (uint32_t)(half ? ro[3] : ro[1]);
-    const uint32_t ab = bufA + (uint32_t)(kbl * 64 * 64);
-    v4i wl0, wh0, wl1, wh1;
-    lds_rd128(o.a0h, ab + rd_a0);
-    lds_rd128(o.a0l, ab + rd_a1);
-    lds_rd128(o.a1h, ab + rd_a0 + 2048);
-    lds_rd128(o.a1l, ab + rd_a1 + 2048);
-    lds_rd2x64(wl0, bufB + to0);
-    lds_rd2x64(wh0, bufB + to0 + a.Wpad);
-    lds_rd2x64(wl1, bufB + to1);
-    lds_rd2x64(wh1, bufB + to1 + a.Wpad);
+    const uint32_t ab = rbufA + (uint32_t)(rkbl * 64 * 64);
+    lds_rd128(r.a0h, ab + rd_a0);
+    lds_rd128(r.a0l, ab + rd_a1);
+    lds_rd128(r.a1h, ab + rd_a0 + 2048);
+    lds_rd128(r.a1l, ab + rd_a1 + 2048);
+    lds_rd2x64(r.wl0, rbufB + to0);
+    lds_rd2x64(r.wh0, rbufB + to0 + a.Wpad);
+    lds_rd2x64(r.wl1, rbufB + to1);
+    lds_rd2x64(r.wh1, rbufB + to1 + a.Wpad);
+    ++rkbl;
+  };
+  auto wait_raw = [&](Raw& r) {
     asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(wl0), "+v"(wh0), "+v"(wl1), "+v"(wh1), "+v"(o.a0h), "+v"(o.a0l), "+v"(o.a1h), "+v"(o.a1l)
+                 : "+v"(r.wl0), "+v"(r.wh0), "+v"(r.wl1), "+v"(r.wh1), "+v"(r.a0h), "+v"(r.a0l), "+v"(r.a1h),
+                   "+v"(r.a1l)
                  :
                  : "memory");
-    o.bl = (v4i){window8_lo(wl0, ss), window8_hi(wl0, ss), window8_lo(wl1, ss), window8_hi(wl1, ss)};
-    o.bh = (v4i){window8_lo(wh0, ss), window8_hi(wh0, ss), window8_lo(wh1, ss), window8_hi(wh1, ss)};
   };
 
+  const int32_t NB = (t_seg1 - t_seg0) / 32;  // blocks of the segment (even: whole chunks)
   issue_band(0);
   wait_vmcnt<0>();
   __syncthreads();
-  int32_t kbs = 0;  // block index inside the segment
-  for (int32_t b = 0; b < nbands; ++b) {
-    if (b + 1 < nbands) issue_band(b + 1);
-    const int32_t t_b0 = t_seg0 + b * kSBT;
-    const uint32_t bufB = smem_base + (uint32_t)((b & 1) * a.buf_bytes) + lane_b;
-    const uint32_t bufA = smem_base + (uint32_t)((b & 1) * a.buf_bytes + b_region);
-    const int32_t nblk = min(kBandBlocks, (t_seg1 - t_b0) / 32);  // even: segments are whole chunks
-    za = band_row0(t_b0);
-    rn = t_b0 / PQ; rp = (t_b0 % PQ) / a.Q; rq = t_b0 % a.Q;
-    for (int32_t kbl = 0; kbl < nblk; kbl += 2, kbs += 2) {
-      // even block kbs (set X): tile 0 opens chunk kbs/2; tile 1 finishes chunk kbs/2 - 1 on block kbs - 1 (Y)
+  if (nbands > 1) issue_band(1);
+  start_read_band(0);
+  issue_reads(R0);
+  v4i ea1h, ea1l, ebh, ebl;  // tile 1's operands of the last even block
+  v4i oa1h, oa1l, obh, obl;  // tile 1's operands of the last odd block
+  for (int32_t kbs = 0; kbs < NB; kbs += 2) {
+    // even block kbs: tile 0 opens chunk kbs/2; tile 1 finishes chunk kbs/2 - 1 on block kbs - 1
+    wait_raw(R0);
+    issue_reads(R1);  // block kbs + 1, same band (bands hold 4 blocks)
+    {
+      const v4i bl = {window8_lo(R0.wl0, ss), window8_hi(R0.wl0, ss), window8_lo(R0.wl1, ss), window8_hi(R0.wl1, ss)};
+      const v4i bh = {window8_lo(R0.wh0, ss), window8_hi(R0.wh0, ss), window8_lo(R0.wh1, ss), window8_hi(R0.wh1, ss)};
       if (kbs > 0) {
         flush_tile<PARTIALS>(acc0, sum0, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow0, a.K, cvalid);
-        mfma_tile(acc1, Y.a1h, Y.a1l, Y.bh, Y.bl, false);
+        mfma_tile(acc1, oa1h, oa1l, obh, obl, false);
         interleave_4x16();
       }
-      read_block(X, bufA, bufB, kbl);
-      mfma_tile(acc0, X.a0h, X.a0l, X.bh, X.bl, true);
-      // odd block kbs + 1 (set Y): tile 0 continues; tile 1 opens chunk kbs/2 on block kbs (X)
-      read_block(Y, bufA, bufB, kbl + 1);
-      if (kbs > 0) flush_tile<PARTIALS>(acc1, sum1, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow1, a.K, cvalid);
-      mfma_tile(acc0, Y.a0h, Y.a0l, Y.bh, Y.bl, false);
-      if (kbs > 0) interleave_4x16();
-      mfma_tile(acc1, X.a1h, X.a1l, X.bh, X.bl, true);
+      mfma_tile(acc0, R0.a0h, R0.a0l, bh, bl, true);
+      ea1h = R0.a1h; ea1l = R0.a1l; ebh = bh; ebl = bl;
     }
-    wait_vmcnt<0>();
-    __syncthreads();
+    // odd block kbs + 1: tile 0 continues; tile 1 opens chunk kbs/2 on block kbs
+    wait_raw(R1);
+    if (((kbs + 2) & 3) == 0 && kbs + 2 < NB) {
+      // block kbs + 2 opens band nb: every wave has read its last block of band nb - 1,
+      // and band nb has landed; then band nb + 1 may overwrite band nb - 1's buffer
+      wait_vmcnt<0>();
+      __syncthreads();
+      const int32_t nb = (kbs + 2) >> 2;
+      if (nb + 1 < nbands) issue_band(nb + 1);
+      start_read_band(nb);
+    }
+    if (kbs + 2 < NB) issue_reads(R0);
+    {
+      const v4i bl = {window8_lo(R1.wl0, ss), window8_hi(R1.wl0, ss), window8_lo(R1.wl1, ss), window8_hi(R1.wl1, ss)};
+      const v4i bh = {window8_lo(R1.wh0, ss), window8_hi(R1.wh0, ss), window8_lo(R1.wh1, ss), window8_hi(R1.wh1, ss)};
+      if (kbs > 0) flush_tile<PARTIALS>(acc1, sum1, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow1, a.K, cvalid);
+      mfma_tile(acc0, R1.a0h, R1.a0l, bh, bl, false);
+      if (kbs > 0) interleave_4x16();
+      mfma_tile(acc1, ea1h, ea1l, ebh, ebl, true);
+      oa1h = R1.a1h; oa1l = R1.a1l; obh = bh; obl = bl;
+    }
   }
-  // last chunk: tile 0 is complete; tile 1 still owes its final block (Y)
-  flush_tile<PARTIALS>(acc0, sum0, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow0, a.K, cvalid);
-  mfma_tile(acc1, Y.a1h, Y.a1l, Y.bh, Y.bl, false);
+  // last chunk: tile 0 is complete; tile 1 still owes the segment's last block
+  flush_tile<PARTIALS>(acc0, sum0, j0 + NB / 2 - 1, a.partials, a.O, colc, CRS, mrow0, a.K, cvalid);
+  mfma_tile(acc1, oa1h, oa1l, obh, obl, false);
   interleave_4x16();
-  flush_tile<PARTIALS>(acc1, sum1, j0 + kbs / 2 - 1, a.partials, a.O, colc, CRS, mrow1, a.K, cvalid);
+  flush_tile<PARTIALS>(acc1, sum1, j0 + NB / 2 - 1, a.partials, a.O, colc, CRS, mrow1, a.K, cvalid);
 
   const int32_t e = a.ea->exp + a.eb->exp;
 #pragma unroll
