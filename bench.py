@@ -118,6 +118,34 @@ class Step:
         dfp.dfp_conv_bwd_weights(d, self.qx, self.sx, self.qdy, self.sdy, self.dw, self.ws[2])
 
 
+class StepDfp32(Step):
+    """The same step with forward and backward-data emitting single-chunk
+    DFP-32 outputs (chunk = the whole reduction, INT32 with exponent Ea + Eb)
+    and the integer down-convert of Eq. 6 taking the epilogue's max."""
+
+    def __init__(self, layer, x, w, dy, L, rounding, seed, path, dev, G=0):
+        super().__init__(layer, x, w, dy, L, rounding, seed, path, dev, G)
+        dfp, torch = self.dfp, self.torch
+        T = max(layer.c, layer.k) * layer.r * layer.s
+        self.d32 = dfp.make_desc(layer.n, layer.c, layer.h, layer.w, layer.k, layer.r, layer.s, layer.stride,
+                                 layer.pad, chunk_len=T, rounding=rounding, seed=seed, path=path)
+        self.y = self.y.view(torch.int32)
+        self.dx = self.dx.view(torch.int32)
+        self.ws32 = [dfp.alloc_workspace(self.d32, k, dev) for k in range(2)]
+        self.sqy, self.sqdx = dfp.new_scale(dev), dfp.new_scale(dev)
+
+    def run(self):
+        dfp, d, d32 = self.dfp, self.d, self.d32
+        dfp.dfp_quantize(d, dfp.ROLE_X, self.fx, self.qx, self.sx)
+        dfp.dfp_quantize(d, dfp.ROLE_W, self.fw, self.qw, self.sw)
+        dfp.dfp_quantize(d, dfp.ROLE_DY, self.fdy, self.qdy, self.sdy)
+        dfp.dfp_conv_fwd_i32(d32, self.qx, self.sx, self.qw, self.sw, self.y, self.sy, self.ws32[0])
+        dfp.dfp_downconvert_i32(d32, dfp.ROLE_Y, self.y, self.sy, self.qy, self.sqy, amax_ready=True)
+        dfp.dfp_conv_bwd_data_i32(d32, self.qdy, self.sdy, self.qw, self.sw, self.dx, self.sdx, self.ws32[1])
+        dfp.dfp_downconvert_i32(d32, dfp.ROLE_DX, self.dx, self.sdx, self.qdx, self.sqdx, amax_ready=True)
+        dfp.dfp_conv_bwd_weights(d, self.qx, self.sx, self.qdy, self.sdy, self.dw, self.ws[2])
+
+
 def timed(step, steps, warmup, profile=False):
     """Seconds per step over `steps` steps after `warmup` untimed ones.  With
     profile=True every library launch is bracketed by HIP events on its stream
@@ -230,6 +258,19 @@ def main():
             sweep[str(L)] = {"ms_per_step": round(t2 * 1e3, 4), "tops": round(3 * ops_per_dir / t2 / 1e12, 3)}
             del s2
 
+    # the DFP-32-output variant of the same step (reported beside the headline)
+    s32 = StepDfp32(layer, x, w, dy, a.chunk, rounding, seed, a.path, dev, a.seg_chunks)
+    t32, _ = timed(s32, a.steps, a.warmup)
+    _, recs32 = timed(s32, a.steps, 1, profile=True)
+    k32 = {}
+    for name, ms in recs32:
+        k32.setdefault(name, []).append(ms)
+    dfp32 = {"ms_per_step": round(t32 * 1e3, 4), "tops": round(3 * ops_per_dir / t32 / 1e12, 3),
+             "chunk_len_fwd_bwd_data": s32.d32.chunk_len,
+             "kernels": {k: {"launches_per_step": len(v) / a.steps, "avg_ms": round(float(np.mean(v)), 5)}
+                         for k, v in k32.items()}}
+    del s32
+
     out = {
         "metric": METRIC,
         "value": round(3 * ops_per_dir / sec / 1e12, 4),
@@ -262,6 +303,7 @@ def main():
         "per_direction": per_dir,
         "kernels": {k: {kk: round(vv, 5) for kk, vv in v.items()} for k, v in kstats.items()},
         "chunk_sweep": sweep,
+        "dfp32_outputs": dfp32,
     }
     if not a.no_cpu:
         out["cpu_baseline"] = cpu_baseline(layer, x, w, dy, a.chunk, a.seg_chunks, rounding, seed, a.cpu_seconds)

@@ -39,6 +39,10 @@
  *   - P = bits in {15, 16}.  15 is the paper's experimental setting (inputs
  *     shifted by one bit, "DFP15", Sec. 4.3): integers in [-2^14, 2^14], never
  *     saturating.  P = 16 clamps to [-32767, 32767] (flag SATURATED).
+ *     Convolution operands are integers of the descriptor's P: at P = 15
+ *     |i| <= 2^14 (what dfp_quantize writes), which the matrix-core path
+ *     relies on (its byte digits hold |i| < 32640); larger magnitudes at P = 15
+ *     give unspecified outputs.  P = 16 takes the full INT16 range.
  *   - Rounding of x = f * 2^-Es: NEAREST = ties to even; BIASED = ties toward
  *     +inf, floor(x + 1/2); STOCHASTIC = floor(x) + (U < F) with
  *     F = floor(frac(x) * 2^32) and U a Philox4x32-10 word (Salmon et al.,
@@ -180,6 +184,37 @@ dfp_status dfp_conv_bwd_weights(const dfp_desc* d, const int16_t* x, const dfp_s
  * (dst is scratch for the max pass, as in dfp_quantize). */
 dfp_status dfp_downconvert(const dfp_desc* d, int32_t role, const float* src, int16_t* dst,
                            dfp_scale* s, int32_t amax_ready, void* stream);
+
+/* Single-chunk DFP-32 outputs (Alg. 2 with one chunk over the whole reduction,
+ * Sec. 4.3: the INT32 accumulator itself, with exponent Ex + Ew).  The
+ * descriptor's chunk_len must be at least the reduction length (C*R*S
+ * forward, K*R*S backward-data), else DFP_ERR_PARAM.  y / dx: INT32 in the
+ * layout of dfp_conv_fwd's y / dfp_conv_bwd_data's dx, each element the
+ * wrapped (mod 2^32) sum of its products.  sy / sdx (required, 16-byte
+ * aligned): receives exp = Ex + Ew (or Edy + Ew) and amax_bits = max |i| as an
+ * unsigned integer (2^31 for -2^31), ready for dfp_downconvert_i32(...,
+ * amax_ready = 1).  workspace: as for the FP32-output call of the same
+ * direction. */
+dfp_status dfp_conv_fwd_i32(const dfp_desc* d, const int16_t* x, const dfp_scale* sx, const int16_t* w,
+                            const dfp_scale* sw, int32_t* y, dfp_scale* sy, void* workspace,
+                            size_t ws_bytes, void* stream);
+dfp_status dfp_conv_bwd_data_i32(const dfp_desc* d, const int16_t* dy, const dfp_scale* sdy,
+                                 const int16_t* w, const dfp_scale* sw, int32_t* dx, dfp_scale* sdx,
+                                 void* workspace, size_t ws_bytes, void* stream);
+
+/* Integer down-conversion of a DFP-32 tensor <I, E_in> to DFP (Eq. 6, with the
+ * shift count read so that the max lands at bit P-2 as Eq. 2 places it):
+ * Rs = floor(log2 max|I|) - (P - 2) (negative Rs is an exact left shift), new
+ * exponent E_in + Rs (clamped at -128 by raising Rs, flag EXP_CLAMPED), each
+ * integer rounded from I * 2^-Rs in the descriptor's mode (the stochastic
+ * stream of `role`, DFP_ROLE_Y or DFP_ROLE_DX); P = 16 saturates at +-32767.
+ * src: INT32 [numel(role)], 16-byte aligned.  sin: exp = E_in; with
+ * amax_ready = 1 also amax_bits = max |I| (the sy / sdx of the _i32
+ * convolutions); amax_ready = 0 recomputes the max, using dst as scratch.
+ * dst: INT16, 8-byte aligned.  sout (not sin): receives amax_bits, exp and
+ * flags (ZERO_TENSOR for an all-zero tensor, exponent 0). */
+dfp_status dfp_downconvert_i32(const dfp_desc* d, int32_t role, const int32_t* src, const dfp_scale* sin,
+                               int16_t* dst, dfp_scale* sout, int32_t amax_ready, void* stream);
 
 /* Device workspace needed by a convolution direction (bytes, 0 if none);
  * 0 also for an invalid descriptor. */

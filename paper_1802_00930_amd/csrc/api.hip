@@ -220,6 +220,52 @@ static dfp_status conv_common(int32_t dir, const dfp_desc* d, const int16_t* a, 
   return launch_conv_valu(dir, g, a, sa, b, sb, out, so, partials, st);
 }
 
+// Single-chunk DFP-32 output (forward or backward-data): chunk_len must cover
+// the whole reduction, so the one INT32 partial is the output.
+static dfp_status conv_i32_common(int32_t dir, const dfp_desc* d, const int16_t* a, const dfp_scale* sa,
+                                  const int16_t* b, const dfp_scale* sb, int32_t* out, dfp_scale* so, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  Geom g;
+  dfp_status rc = conv_checks(d, &g, a, sa, b, sb, out);
+  if (rc != DFP_OK) return rc;
+  if (!so) return DFP_ERR_NULL;
+  if (d->chunk_len < reduction_len(g, dir)) return DFP_ERR_PARAM;
+  if ((rc = ws_check(g, dir, d->path, d->bits, ws, ws_bytes)) != DFP_OK) return rc;
+  if (!aligned(so, 16)) return DFP_ERR_ALIGN;
+  hipStream_t st = (hipStream_t)stream;
+  float* outf = reinterpret_cast<float*>(out);
+  if (use_mfma(g, d->path, d->bits, dir))  // the filter prep kernel clears so
+    return launch_conv_mfma(dir, g, a, sa, b, sb, outf, so, nullptr, ws, st, true);
+  if ((rc = launch_scale_reset(so, st)) != DFP_OK) return rc;
+  return launch_conv_valu(dir, g, a, sa, b, sb, outf, so, nullptr, st, true);
+}
+
+dfp_status dfp_conv_fwd_i32(const dfp_desc* d, const int16_t* x, const dfp_scale* sx, const int16_t* w,
+                            const dfp_scale* sw, int32_t* y, dfp_scale* sy, void* workspace, size_t ws_bytes,
+                            void* stream) {
+  return conv_i32_common(DFP_FWD, d, x, sx, w, sw, y, sy, workspace, ws_bytes, stream);
+}
+
+dfp_status dfp_conv_bwd_data_i32(const dfp_desc* d, const int16_t* dy, const dfp_scale* sdy, const int16_t* w,
+                                 const dfp_scale* sw, int32_t* dx, dfp_scale* sdx, void* workspace, size_t ws_bytes,
+                                 void* stream) {
+  return conv_i32_common(DFP_BWD_DATA, d, dy, sdy, w, sw, dx, sdx, workspace, ws_bytes, stream);
+}
+
+dfp_status dfp_downconvert_i32(const dfp_desc* d, int32_t role, const int32_t* src, const dfp_scale* sin,
+                               int16_t* dst, dfp_scale* sout, int32_t amax_ready, void* stream) {
+  if (!d || !src || !sin || !dst || !sout) return DFP_ERR_NULL;
+  if (!params_ok(d) || (role != DFP_ROLE_Y && role != DFP_ROLE_DX) || (amax_ready != 0 && amax_ready != 1) ||
+      sin == sout)
+    return DFP_ERR_PARAM;
+  Geom g;
+  if (!geom_from_desc(d, &g)) return DFP_ERR_SHAPE;
+  if (!aligned(src, 16) || !aligned(dst, 8) || !aligned(sin, 16) || !aligned(sout, 16)) return DFP_ERR_ALIGN;
+  const int64_t n = role_numel(g, role);
+  return launch_downconvert_i32(src, n, sin, dst, sout, amax_ready != 0, d->bits, d->rounding, d->seed,
+                                (uint32_t)role, (hipStream_t)stream);
+}
+
 dfp_status dfp_conv_fwd(const dfp_desc* d, const int16_t* x, const dfp_scale* sx, const int16_t* w,
                         const dfp_scale* sw, float* y, dfp_scale* sy, void* workspace, size_t ws_bytes,
                         int32_t* partials, void* stream) {
@@ -276,7 +322,7 @@ const char* dfp_kernel_name(int32_t id) {
   static const char* names[K_NUM_KERNELS] = {
       "scale_reset", "amax", "quant_convert", "conv_fwd_valu", "conv_bwd_data_valu", "conv_bwd_wt_valu",
       "weight_prep", "conv_fwd_mfma", "conv_bwd_data_mfma", "conv_bwd_wt_mfma", "bwd_wt_segment_reduce",
-      "act_prep"};
+      "act_prep", "conv_fwd_i32", "conv_bwd_data_i32", "downconvert_i32"};
   if (id < 0 || id >= K_NUM_KERNELS) return "unknown";
   return names[id];
 }

@@ -32,6 +32,6 @@ ConvMfmaPlan plan_conv_mfma(const Geom& g, int32_t dir);
 bool conv_mfma_supported(const Geom& g, int32_t dir);
 dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,
                             const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, void* ws,
-                            hipStream_t st);
+                            hipStream_t st, bool i32 = false);
 
 }  // namespace dfp

@@ -244,6 +244,29 @@ __device__ __forceinline__ void flush_tile(const Acc3& acc, float (&sum)[16], in
   }
 }
 
+// Single-chunk DFP-32 output: the chunk's wrapped INT32 sum itself, kept as
+// raw bits in the FP32 sum registers until the epilogue stores it.
+__device__ __forceinline__ void keep_tile_i32(const Acc3& acc, float (&sum)[16]) {
+#pragma unroll
+  for (int v = 0; v < 16; ++v)
+    sum[v] = __int_as_float((int32_t)recombine((uint32_t)acc.hh[v], (uint32_t)acc.xx[v], (uint32_t)acc.ll[v]));
+}
+
+// Epilogue of one output element: FP32 path stores 2^e * sum and its |.|
+// bits; the DFP-32 path stores the INT32 and |.| as an unsigned integer.
+template <bool I32>
+__device__ __forceinline__ uint32_t store_out(float* out, int64_t o, float sum, int32_t e) {
+  if (I32) {
+    const int32_t v = __float_as_int(sum);
+    reinterpret_cast<int32_t*>(out)[o] = v;
+    return v < 0 ? (uint32_t)0 - (uint32_t)v : (uint32_t)v;
+  } else {
+    const float y = ldexpf(sum, e);
+    out[o] = y;
+    return __float_as_uint(y) & 0x7fffffffu;
+  }
+}
+
 // Operands of one block of 32 reduction indices for one lane.
 struct Operands {
   v4i bhi, blo;
@@ -252,7 +275,7 @@ struct Operands {
 
 // Forward / backward-data main kernel.  Output pixels g in [0, NP) map to
 // (img, po, qo) of an [Nimg][M][Po][Qo] FP32 output.
-template <bool MASKED, bool PARTIALS, bool CHAN16>
+template <bool MASKED, bool PARTIALS, bool CHAN16, bool I32 = false>
 __global__ __launch_bounds__(kThreads, 2) void k_conv_mfma(ConvMfmaArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -354,8 +377,10 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv_mfma(ConvMfmaArgs a) {
       ++blk_in_chunk;
       if (blk_in_chunk == chunk_blocks || kb == a.KB - 1) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
-          flush_tile<PARTIALS>(acc[i], sum[i], j, a.partials, a.O, obase, PQ, m0 + 32 * i + 4 * half, a.M, gvalid);
+        for (int i = 0; i < 2; ++i) {
+          if (I32) keep_tile_i32(acc[i], sum[i]);
+          else flush_tile<PARTIALS>(acc[i], sum[i], j, a.partials, a.O, obase, PQ, m0 + 32 * i + 4 * half, a.M, gvalid);
+        }
         ++j;
         blk_in_chunk = 0;
       }
@@ -403,11 +428,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv_mfma(ConvMfmaArgs a) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
-      const float y = ldexpf(sum[i][v], e);
-      if (gvalid && m < a.M) {
-        a.out[obase + (int64_t)m * PQ] = y;
-        amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
-      }
+      if (gvalid && m < a.M) amax = max(amax, store_out<I32>(a.out, obase + (int64_t)m * PQ, sum[i][v], e));
     }
   }
   if (a.so) {
@@ -420,7 +441,11 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv_mfma(ConvMfmaArgs a) {
       uint32_t b = red[0];
       for (int i = 1; i < kThreads / 64; ++i) b = max(b, red[i]);
       if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
-      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+      if (I32) {
+        if (blockIdx.x == 0 && blockIdx.y == 0) a.so->exp = e;
+      } else if (b == 0x7f800000u) {
+        atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+      }
     }
   }
 }
@@ -709,7 +734,7 @@ __device__ __forceinline__ void xcd_tile(int32_t& tx, int32_t& ty) {
   tx = t / nby;
 }
 
-template <bool PARTIALS>
+template <bool PARTIALS, bool I32 = false>
 __global__ __launch_bounds__(kThreadsQ, 4) void k_conv_mfma_q(ConvMfmaArgs a) {
   __shared__ __align__(16) uint8_t smem[kStages * kStageBytes];
   const int lane = threadIdx.x & 63;
@@ -804,7 +829,8 @@ __global__ __launch_bounds__(kThreadsQ, 4) void k_conv_mfma_q(ConvMfmaArgs a) {
     read_stage_q<STAGE * kStageBytes>(rb0, rb1, ra0, ra1, bhi, blo, ahi, alo);
     mfma_tile(acc, ahi, alo, bhi, blo, blk_in_chunk == 0);
     if (++blk_in_chunk == chunk_blocks || kb == KB - 1) {
-      flush_tile<PARTIALS>(acc, sum, j, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+      if (I32) keep_tile_i32(acc, sum);
+      else flush_tile<PARTIALS>(acc, sum, j, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
       ++j;
       blk_in_chunk = 0;
     }
@@ -828,11 +854,7 @@ __global__ __launch_bounds__(kThreadsQ, 4) void k_conv_mfma_q(ConvMfmaArgs a) {
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
-    const float y = ldexpf(sum[v], e);
-    if (gvalid && m < a.M) {
-      a.out[(uint32_t)(obase + m * PQ)] = y;
-      amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
-    }
+    if (gvalid && m < a.M) amax = max(amax, store_out<I32>(a.out, (uint32_t)(obase + m * PQ), sum[v], e));
   }
   if (a.so) {
     __shared__ uint32_t red[kWavesQ];
@@ -844,7 +866,11 @@ __global__ __launch_bounds__(kThreadsQ, 4) void k_conv_mfma_q(ConvMfmaArgs a) {
       uint32_t b = red[0];
       for (int i = 1; i < kWavesQ; ++i) b = max(b, red[i]);
       if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
-      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+      if (I32) {
+        if (blockIdx.x == 0 && blockIdx.y == 0) a.so->exp = e;
+      } else if (b == 0x7f800000u) {
+        atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+      }
     }
   }
 }
@@ -1117,8 +1143,9 @@ __device__ __forceinline__ void read_a_issue(uint32_t a00, uint32_t a01, uint32_
 // block out of phase (tile 1 consumes block kb-1 while tile 0 consumes block
 // kb), so each chunk conversion of one sub-tile is interleaved with the other
 // sub-tile's MFMAs; the operand reads of a block are in flight during the
-// other sub-tile's MFMAs on the lagging block.
-template <bool PARTIALS>
+// other sub-tile's MFMAs on the lagging block.  I32: one chunk over the whole
+// reduction (no conversion until the end), INT32 outputs.
+template <bool PARTIALS, bool I32 = false>
 __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs a) {
   __shared__ __align__(16) uint8_t smem[kLds3];
   uint8_t* const sA = smem;
@@ -1267,26 +1294,32 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
       // even: tile 0's chunk ended at kb-1; tile 1 finishes its chunk on block kb-1
       wait_block(gb0 + kb);
       read_block(gb0 + kb, kb);
-      flush_tile<PARTIALS>(acc0, sum0, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+      if (!I32) flush_tile<PARTIALS>(acc0, sum0, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
       mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
-      interleave_4x16();
+      if (!I32) interleave_4x16();
       read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
-      mfma_tile(acc0, ca0h, ca0l, cbh, cbl, true);
+      mfma_tile(acc0, ca0h, ca0l, cbh, cbl, !I32);
       pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
       // odd: tile 1's chunk ended; tile 0 continues; tile 1 opens the next chunk on block kb
       wait_block(gb0 + kb + 1);
       read_block(gb0 + kb + 1, kb + 1);
       read_stage_wait(cbh, cbl, ca0h, ca0l, ca1h, ca1l);
-      flush_tile<PARTIALS>(acc1, sum1, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
+      if (!I32) flush_tile<PARTIALS>(acc1, sum1, kb / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
       mfma_tile(acc0, ca0h, ca0l, cbh, cbl, false);
-      interleave_4x16();
-      mfma_tile(acc1, pa1h, pa1l, pbh, pbl, true);
+      if (!I32) interleave_4x16();
+      mfma_tile(acc1, pa1h, pa1l, pbh, pbl, !I32);
       pbh = cbh; pbl = cbl; pa1h = ca1h; pa1l = ca1l;
     }
-    flush_tile<PARTIALS>(acc0, sum0, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
-    mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
-    interleave_4x16();
-    flush_tile<PARTIALS>(acc1, sum1, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
+    if (I32) {
+      keep_tile_i32(acc0, sum0);
+      mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+      keep_tile_i32(acc1, sum1);
+    } else {
+      flush_tile<PARTIALS>(acc0, sum0, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+      mfma_tile(acc1, pa1h, pa1l, pbh, pbl, false);
+      interleave_4x16();
+      flush_tile<PARTIALS>(acc1, sum1, KB / 2 - 1, a.partials, a.O, obase, PQ, mrow1, a.M, gvalid);
+    }
 
     // ---- outputs of this tile (the stores drain while the next tile computes)
 #pragma unroll
@@ -1294,11 +1327,8 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int32_t m = m0 + 32 * i + 8 * (v >> 2) + 4 * half + (v & 3);
-        const float y = ldexpf(i == 0 ? sum0[v] : sum1[v], e);
-        if (gvalid && m < a.M) {
-          a.out[(uint32_t)(obase + m * PQ)] = y;
-          amax = max(amax, __float_as_uint(y) & 0x7fffffffu);
-        }
+        if (gvalid && m < a.M)
+          amax = max(amax, store_out<I32>(a.out, (uint32_t)(obase + m * PQ), i == 0 ? sum0[v] : sum1[v], e));
       }
     }
   }
@@ -1313,7 +1343,11 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
       uint32_t b = red[0];
       for (int i = 1; i < kWaves3; ++i) b = max(b, red[i]);
       if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
-      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+      if (I32) {
+        if (blockIdx.x == 0 && blockIdx.y == 0) a.so->exp = e;
+      } else if (b == 0x7f800000u) {
+        atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+      }
     }
   }
 }
@@ -1360,7 +1394,7 @@ ConvMfmaPlan plan_conv_mfma(const Geom& g, int32_t dir) {
 
 dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,
                             const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, void* ws,
-                            hipStream_t st) {
+                            hipStream_t st, bool i32) {
   // fwd: a = x (B source), b = w.  bwd-data: a = dy (B source), b = w.
   const ConvMfmaPlan p = plan_conv_mfma(g, dir);
   const bool fwd = dir == DFP_FWD;
@@ -1416,21 +1450,39 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   const bool masked = (g.L % 32) != 0;
   const bool chan16 = (p.Cin % 16) == 0;
   const int kid = fwd ? K_FWD_MFMA : K_BWDD_MFMA;
-#define DFP_CONV_MFMA_CASE(MK, PT, CH)                                                      \
-  if (masked == MK && (partials != nullptr) == PT && chan16 == CH) {                       \
-    DFP_LAUNCH(kid, (k_conv_mfma<MK, PT, CH>), grid, dim3(kThreads), 0, st, args);          \
-    return DFP_OK;                                                                          \
-  }
-  if (chan16 && g.L == 64 && (p.T % 64) == 0 && p.KB >= 4 && p.KB <= kARes3Max && args.O < (1ll << 31) &&
-      p.ws_b_bytes < (1ll << 31)) {
-    // one workgroup per CU for each 64-row tile of the output channels
+  // persistent grid: one workgroup per CU for each 64-row tile of the output channels
+  auto persist_grid = [&]() {
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     const int64_t wave_tiles = (args.NP + 31) / 32;
     const int64_t mtiles = p.Mp / kMT;
     int64_t gx = std::max<int64_t>(1, cus / mtiles);
     gx = std::min<int64_t>(gx, (wave_tiles + kWaves3 - 1) / kWaves3);
-    const dim3 grid3((unsigned)gx, (unsigned)mtiles);
+    return dim3((unsigned)gx, (unsigned)mtiles);
+  };
+  const bool persist_ok = chan16 && (p.T % 64) == 0 && p.KB >= 4 && p.KB <= kARes3Max && args.O < (1ll << 31) &&
+                          p.ws_b_bytes < (1ll << 31);
+  if (i32) {
+    // DFP-32 output: one chunk over the whole reduction (the caller checked L >= T)
+    args.L = p.KB * 32;
+    const int kid32 = fwd ? K_FWD_I32 : K_BWDD_I32;
+    if (persist_ok)
+      DFP_LAUNCH(kid32, (k_conv_mfma_persist<false, true>), persist_grid(), dim3(kThreads3), 0, st, args);
+    else if (chan16 && args.O < (1ll << 31) && p.ws_b_bytes < (1ll << 31))
+      DFP_LAUNCH(kid32, (k_conv_mfma_q<false, true>), grid, dim3(kThreadsQ), 0, st, args);
+    else if (chan16)
+      DFP_LAUNCH(kid32, (k_conv_mfma<false, false, true, true>), grid, dim3(kThreads), 0, st, args);
+    else
+      DFP_LAUNCH(kid32, (k_conv_mfma<false, false, false, true>), grid, dim3(kThreads), 0, st, args);
+    return DFP_OK;
+  }
+#define DFP_CONV_MFMA_CASE(MK, PT, CH)                                                      \
+  if (masked == MK && (partials != nullptr) == PT && chan16 == CH) {                       \
+    DFP_LAUNCH(kid, (k_conv_mfma<MK, PT, CH>), grid, dim3(kThreads), 0, st, args);          \
+    return DFP_OK;                                                                          \
+  }
+  if (persist_ok && g.L == 64) {
+    const dim3 grid3 = persist_grid();
     if (partials) DFP_LAUNCH(kid, (k_conv_mfma_persist<true>), grid3, dim3(kThreads3), 0, st, args);
     else DFP_LAUNCH(kid, (k_conv_mfma_persist<false>), grid3, dim3(kThreads3), 0, st, args);
     return DFP_OK;

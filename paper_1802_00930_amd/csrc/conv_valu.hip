@@ -74,7 +74,20 @@ __device__ __forceinline__ void epilogue_amax(float y, bool active, dfp_scale* s
   }
 }
 
-template <bool PARTIALS>
+// Single-chunk DFP-32 output: the wrapped INT32 sum, its |.| into so->amax_bits
+// (one relaxed-read-guarded atomic per lane; this path is the reference one)
+// and the output exponent.
+__device__ __forceinline__ void store_i32(float* out, int64_t o, uint32_t acc, dfp_scale* so, int32_t e) {
+  const int32_t v = (int32_t)acc;
+  reinterpret_cast<int32_t*>(out)[o] = v;
+  if (so) {
+    const uint32_t m = v < 0 ? 0u - (uint32_t)v : (uint32_t)v;
+    if (m > __atomic_load_n(&so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&so->amax_bits, m);
+    if (o == 0) so->exp = e;
+  }
+}
+
+template <bool PARTIALS, bool I32 = false>
 __global__ __launch_bounds__(kBlock) void k_fwd_valu(Geom g, const int16_t* __restrict__ x,
                                                     const dfp_scale* __restrict__ sx,
                                                     const int16_t* __restrict__ w,
@@ -99,18 +112,23 @@ __global__ __launch_bounds__(kBlock) void k_fwd_valu(Geom g, const int16_t* __re
         const int16_t* wp = w + ((int64_t)k * g.c) * rs + r * g.s + s;
         for (int32_t c = 0; c < g.c; ++c) {
           const int32_t prod = valid ? (int32_t)xp[c * hw] * (int32_t)wp[c * rs] : 0;
-          push<PARTIALS, false>(st, prod, g.L, g.G, partials, O, o);
+          if (I32) st.acc += (uint32_t)prod;
+          else push<PARTIALS, false>(st, prod, g.L, g.G, partials, O, o);
         }
       }
+    }
+    if (I32) {
+      store_i32(y, o, st.acc, so, sx->exp + sw->exp);
+      return;
     }
     if (st.fill) flush<PARTIALS, false>(st, g.G, partials, O, o);
     yv = ldexpf(st.sum, sx->exp + sw->exp);
     y[o] = yv;
   }
-  if (so) epilogue_amax(yv, active, so);
+  if (so && !I32) epilogue_amax(yv, active, so);
 }
 
-template <bool PARTIALS>
+template <bool PARTIALS, bool I32 = false>
 __global__ __launch_bounds__(kBlock) void k_bwdd_valu(Geom g, const int16_t* __restrict__ dy,
                                                      const dfp_scale* __restrict__ sdy,
                                                      const int16_t* __restrict__ w,
@@ -136,15 +154,20 @@ __global__ __launch_bounds__(kBlock) void k_bwdd_valu(Geom g, const int16_t* __r
         const int16_t* wp = w + ((int64_t)c * g.r + r) * g.s + s;
         for (int32_t k = 0; k < g.k; ++k) {
           const int32_t prod = valid ? (int32_t)dp[k * pq] * (int32_t)wp[k * crs] : 0;
-          push<PARTIALS, false>(st, prod, g.L, g.G, partials, O, o);
+          if (I32) st.acc += (uint32_t)prod;
+          else push<PARTIALS, false>(st, prod, g.L, g.G, partials, O, o);
         }
       }
+    }
+    if (I32) {
+      store_i32(dx, o, st.acc, so, sdy->exp + sw->exp);
+      return;
     }
     if (st.fill) flush<PARTIALS, false>(st, g.G, partials, O, o);
     yv = ldexpf(st.sum, sdy->exp + sw->exp);
     dx[o] = yv;
   }
-  if (so) epilogue_amax(yv, active, so);
+  if (so && !I32) epilogue_amax(yv, active, so);
 }
 
 template <bool PARTIALS>
@@ -183,12 +206,18 @@ __global__ __launch_bounds__(kBlock) void k_bwdw_valu(Geom g, const int16_t* __r
 }  // namespace
 
 dfp_status launch_conv_valu(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,
-                            const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, hipStream_t st) {
+                            const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, hipStream_t st,
+                            bool i32) {
   int64_t O;
   if (dir == DFP_FWD) O = (int64_t)g.n * g.k * g.p * g.q;
   else if (dir == DFP_BWD_DATA) O = (int64_t)g.n * g.c * g.h * g.w;
   else O = (int64_t)g.k * g.c * g.r * g.s;
   const dim3 grid((unsigned)((O + kBlock - 1) / kBlock)), block(kBlock);
+  if (i32) {  // forward or backward-data, one chunk
+    if (dir == DFP_FWD) DFP_LAUNCH(K_FWD_I32, (k_fwd_valu<false, true>), grid, block, 0, st, g, a, sa, b, sb, out, so, partials);
+    else DFP_LAUNCH(K_BWDD_I32, (k_bwdd_valu<false, true>), grid, block, 0, st, g, a, sa, b, sb, out, so, partials);
+    return DFP_OK;
+  }
   if (dir == DFP_FWD) {
     if (partials) DFP_LAUNCH(K_FWD_VALU, k_fwd_valu<true>, grid, block, 0, st, g, a, sa, b, sb, out, so, partials);
     else DFP_LAUNCH(K_FWD_VALU, k_fwd_valu<false>, grid, block, 0, st, g, a, sa, b, sb, out, so, partials);

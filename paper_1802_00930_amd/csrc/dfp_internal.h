@@ -22,7 +22,10 @@ enum KernelId : int32_t {
   K_BWDW_MFMA = 9,
   K_BWDW_REDUCE = 10,
   K_XPREP = 11,
-  K_NUM_KERNELS = 12
+  K_FWD_I32 = 12,
+  K_BWDD_I32 = 13,
+  K_DC_I32 = 14,
+  K_NUM_KERNELS = 15
 };
 
 // Convolution geometry handed to kernels by value.
@@ -58,9 +61,17 @@ dfp_status launch_amax(const float* src, int64_t n, int16_t* scratch, dfp_scale*
 dfp_status launch_quant_convert(const float* src, int16_t* dst, int64_t n, dfp_scale* s, int32_t bits,
                                 int32_t rounding, uint64_t seed, uint32_t role, hipStream_t st);
 
+// DFP-32 -> DFP (Eq. 6): sin carries E_in (and the max |src| when amax_ready);
+// sout receives amax_bits, the new exponent and flags; dst is also the max
+// pass's scratch.
+dfp_status launch_downconvert_i32(const int32_t* src, int64_t n, const dfp_scale* sin, int16_t* dst, dfp_scale* sout,
+                                  bool amax_ready, int32_t bits, int32_t rounding, uint64_t seed, uint32_t role,
+                                  hipStream_t st);
+
 // conv_valu.hip: one lane per output, VALU integer multiply-add.
+// i32: single-chunk DFP-32 output (forward / backward-data), out holds INT32.
 dfp_status launch_conv_valu(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa,
                             const int16_t* b, const dfp_scale* sb, float* out, dfp_scale* so,
-                            int32_t* partials, hipStream_t st);
+                            int32_t* partials, hipStream_t st, bool i32 = false);
 
 }  // namespace dfp

@@ -239,6 +239,135 @@ __global__ __launch_bounds__(kBlock) void k_quant_convert(const float* __restric
   if (SAT && saturated) atomicOr(&s->flags, DFP_FLAG_SATURATED);
 }
 
+// ---------------------------------------------------------------- DFP-32 -> DFP
+// Integer down-conversion (Eq. 6 with the shift count read as in Eq. 2):
+// Rs = floor(log2 max|i|) - (P - 2), E_out = E_in + Rs (clamped at -128 by
+// raising Rs), and every integer rounded from i * 2^-Rs with the descriptor's
+// mode.  i * 2^-Rs is split exactly as X = floor(i * 2^(32-Rs)) in 64 bits.
+__device__ __forceinline__ uint32_t abs_u32(int32_t v) { return v < 0 ? 0u - (uint32_t)v : (uint32_t)v; }
+
+__global__ __launch_bounds__(kBlock) void k_amax_i32(const int32_t* __restrict__ src, int64_t n,
+                                                     uint32_t* __restrict__ part, dfp_scale* __restrict__ s) {
+  const int4* src4 = reinterpret_cast<const int4*>(src);
+  const int64_t n4 = n >> 2;
+  uint32_t m = 0u;
+  for (int64_t base = (int64_t)blockIdx.x * kAmaxChunk; base < n4; base += (int64_t)gridDim.x * kAmaxChunk) {
+    if (base + kAmaxChunk <= n4) {
+      int4 v[kAmaxUnroll];
+#pragma unroll
+      for (int k = 0; k < kAmaxUnroll; ++k) v[k] = src4[base + threadIdx.x + k * kBlock];
+#pragma unroll
+      for (int k = 0; k < kAmaxUnroll; ++k)
+        m = max(m, max(max(abs_u32(v[k].x), abs_u32(v[k].y)), max(abs_u32(v[k].z), abs_u32(v[k].w))));
+    } else {
+      for (int64_t i = base + threadIdx.x; i < n4; i += kBlock) {
+        const int4 v = src4[i];
+        m = max(m, max(max(abs_u32(v.x), abs_u32(v.y)), max(abs_u32(v.z), abs_u32(v.w))));
+      }
+    }
+  }
+  if (blockIdx.x == 0)
+    for (int64_t t = 4 * n4 + threadIdx.x; t < n; t += kBlock) m = max(m, abs_u32(src[t]));
+  m = block_max(m);
+  if (threadIdx.x == 0) {
+    if (part) {
+      part[blockIdx.x] = m;
+    } else {
+      s->amax_bits = m;
+      s->flags = 0u;
+    }
+  }
+}
+
+template <int MODE>
+__device__ __forceinline__ int32_t round_i32(int32_t v, int32_t rs, uint32_t u) {
+  int64_t X;
+  // v * 2^(32 - Rs): exact for Rs <= 32 (Rs < 0 only when max|i| < 2^(P-2), so
+  // no overflow); beyond, the dropped bits lie below the 2^-32 fraction bit
+  if (rs <= 32) X = (int64_t)((uint64_t)(int64_t)v << (32 - rs));
+  else X = (int64_t)v >> min(rs - 32, 63);
+  const int32_t fl = (int32_t)(X >> 32);
+  const uint32_t F = (uint32_t)X;
+  bool up;
+  if (MODE == DFP_ROUND_NEAREST) up = (F > 0x80000000u) || (F == 0x80000000u && (fl & 1));
+  else if (MODE == DFP_ROUND_BIASED) up = F >= 0x80000000u;
+  else if (MODE == DFP_ROUND_STOCHASTIC) up = u < F;
+  else up = false;
+  return fl + (up ? 1 : 0);
+}
+
+template <int MODE, bool SAT>
+__global__ __launch_bounds__(kBlock) void k_i32_convert(const int32_t* __restrict__ src, int16_t* __restrict__ dst,
+                                                        int64_t n, const dfp_scale* __restrict__ amax_from,
+                                                        const dfp_scale* __restrict__ sin, dfp_scale* sout,
+                                                        int32_t bits, uint32_t key0, uint32_t key1, uint32_t role) {
+  const uint32_t mx = amax_from->amax_bits;
+  const int32_t e_in = sin->exp;
+  const bool zero = mx == 0u;
+  int32_t rs = 0, e_out = 0;
+  bool clamped = false;
+  if (!zero) {
+    rs = (31 - __clz((int)mx)) - (bits - 2);
+    e_out = e_in + rs;
+    if (e_out < -128) {
+      rs += -128 - e_out;
+      e_out = -128;
+      clamped = true;
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    sout->amax_bits = mx;
+    sout->exp = e_out;
+    const uint32_t f = (zero ? DFP_FLAG_ZERO_TENSOR : 0u) | (clamped ? DFP_FLAG_EXP_CLAMPED : 0u);
+    // without saturation no other workgroup writes the flags: store them whole;
+    // with it the launcher has cleared them and workgroups OR in SATURATED
+    if (!SAT) sout->flags = f;
+    else if (f) atomicOr(&sout->flags, f);
+  }
+  const int64_t groups = (n + 3) >> 2;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  bool saturated = false;
+  for (int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x; g < groups; g += stride) {
+    const int64_t base = g << 2;
+    int32_t v[4];
+    const bool full = base + 4 <= n;
+    if (full) {
+      const int4 q = reinterpret_cast<const int4*>(src)[g];
+      v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = (base + i < n) ? src[base + i] : 0;
+    }
+    uint32_t u[4] = {0u, 0u, 0u, 0u};
+    if (MODE == DFP_ROUND_STOCHASTIC) {
+      const uint4 r = philox4x32_10(make_uint4((uint32_t)g, (uint32_t)((uint64_t)g >> 32), role, 0u), key0, key1);
+      u[0] = r.x; u[1] = r.y; u[2] = r.z; u[3] = r.w;
+    }
+    int32_t iv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int32_t r = zero ? 0 : round_i32<MODE>(v[i], rs, u[i]);
+      if (SAT) {
+        const int32_t c = min(max(r, -32767), 32767);
+        saturated |= c != r;
+        r = c;
+      }
+      iv[i] = r;
+    }
+    if (full) {
+      uint2 packed;
+      packed.x = ((uint32_t)iv[0] & 0xffffu) | ((uint32_t)iv[1] << 16);
+      packed.y = ((uint32_t)iv[2] & 0xffffu) | ((uint32_t)iv[3] << 16);
+      reinterpret_cast<uint2*>(dst)[g] = packed;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (base + i < n) dst[base + i] = (int16_t)iv[i];
+    }
+  }
+  if (SAT && saturated) atomicOr(&sout->flags, DFP_FLAG_SATURATED);
+}
+
 int grid_for(int64_t work_items) {
   int64_t blocks = (work_items + kBlock - 1) / kBlock;
   if (blocks < 1) blocks = 1;
@@ -287,6 +416,52 @@ dfp_status launch_quant_convert(const float* src, int16_t* dst, int64_t n, dfp_s
     case DFP_ROUND_STOCHASTIC: return launch_qc_mode<DFP_ROUND_STOCHASTIC>(src, dst, n, s, bits, k0, k1, role, st);
     case DFP_ROUND_BIASED: return launch_qc_mode<DFP_ROUND_BIASED>(src, dst, n, s, bits, k0, k1, role, st);
     default: return launch_qc_mode<DFP_ROUND_DOWN>(src, dst, n, s, bits, k0, k1, role, st);
+  }
+}
+
+template <int MODE>
+static dfp_status launch_i32_mode(const int32_t* src, int16_t* dst, int64_t n, const dfp_scale* amax_from,
+                                  const dfp_scale* sin, dfp_scale* sout, int32_t bits, uint32_t k0, uint32_t k1,
+                                  uint32_t role, hipStream_t st) {
+  const dim3 grid(grid_for((n + 3) / 4));
+  if (bits == 16)
+    DFP_LAUNCH(K_DC_I32, (k_i32_convert<MODE, true>), grid, dim3(kBlock), 0, st, src, dst, n, amax_from, sin, sout,
+               bits, k0, k1, role);
+  else
+    DFP_LAUNCH(K_DC_I32, (k_i32_convert<MODE, false>), grid, dim3(kBlock), 0, st, src, dst, n, amax_from, sin, sout,
+               bits, k0, k1, role);
+  return DFP_OK;
+}
+
+dfp_status launch_downconvert_i32(const int32_t* src, int64_t n, const dfp_scale* sin, int16_t* dst, dfp_scale* sout,
+                                  bool amax_ready, int32_t bits, int32_t rounding, uint64_t seed, uint32_t role,
+                                  hipStream_t st) {
+  const dfp_scale* amax_from = sin;
+  if (amax_ready) {
+    // P = 16 saturation flags are ORed in by every workgroup: start from zero
+    if (bits == 16 && launch_scale_reset(sout, st) != DFP_OK) return DFP_ERR_HIP;
+  } else {
+    int64_t parts = (n / 4 + kAmaxChunk - 1) / kAmaxChunk;
+    parts = std::min<int64_t>(std::min<int64_t>(parts, kAmaxMaxParts), n / 2);
+    if (parts <= 1) {
+      DFP_LAUNCH(K_AMAX, k_amax_i32, dim3(1), dim3(kBlock), 0, st, src, n, (uint32_t*)nullptr, sout);
+    } else {
+      uint32_t* part = reinterpret_cast<uint32_t*>(dst);
+      DFP_LAUNCH(K_AMAX, k_amax_i32, dim3((unsigned)parts), dim3(kBlock), 0, st, src, n, part, sout);
+      DFP_LAUNCH(K_AMAX, k_amax_final, dim3(1), dim3(kBlock), 0, st, part, (int32_t)parts, sout);
+    }
+    amax_from = sout;
+  }
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  switch (rounding) {
+    case DFP_ROUND_NEAREST:
+      return launch_i32_mode<DFP_ROUND_NEAREST>(src, dst, n, amax_from, sin, sout, bits, k0, k1, role, st);
+    case DFP_ROUND_STOCHASTIC:
+      return launch_i32_mode<DFP_ROUND_STOCHASTIC>(src, dst, n, amax_from, sin, sout, bits, k0, k1, role, st);
+    case DFP_ROUND_BIASED:
+      return launch_i32_mode<DFP_ROUND_BIASED>(src, dst, n, amax_from, sin, sout, bits, k0, k1, role, st);
+    default:
+      return launch_i32_mode<DFP_ROUND_DOWN>(src, dst, n, amax_from, sin, sout, bits, k0, k1, role, st);
   }
 }
 

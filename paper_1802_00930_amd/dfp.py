@@ -56,6 +56,9 @@ def lib():
             "dfp_conv_bwd_data": ([DP, P, P, P, P, P, P, P, SZ, P, P], I32),
             "dfp_conv_bwd_weights": ([DP, P, P, P, P, P, P, SZ, P, P], I32),
             "dfp_downconvert": ([DP, I32, P, P, P, I32, P], I32),
+            "dfp_conv_fwd_i32": ([DP, P, P, P, P, P, P, P, SZ, P], I32),
+            "dfp_conv_bwd_data_i32": ([DP, P, P, P, P, P, P, P, SZ, P], I32),
+            "dfp_downconvert_i32": ([DP, I32, P, P, P, P, I32, P], I32),
             "dfp_workspace_bytes": ([DP, I32], SZ),
             "dfp_num_chunks": ([DP, I32], I64),
             "dfp_output_dims": ([DP, ctypes.POINTER(I32), ctypes.POINTER(I32)], I32),
@@ -176,6 +179,33 @@ def dfp_conv_bwd_weights(d: Desc, x, sx, dy, sdy, dw, workspace=None, partials=N
     _check("dfp_conv_bwd_weights", lib().dfp_conv_bwd_weights(ctypes.byref(d), _ptr(x), _ptr(sx), _ptr(dy),
                                                               _ptr(sdy), _ptr(dw), wp, wn, _ptr(partials),
                                                               _stream(stream)))
+
+
+def dfp_conv_fwd_i32(d: Desc, x, sx, w, sw, y, sy, workspace=None, stream=None):
+    for t, dt, nm in ((x, torch.int16, "x"), (w, torch.int16, "w"), (y, torch.int32, "y"),
+                      (sx, torch.int32, "sx"), (sw, torch.int32, "sw"), (sy, torch.int32, "sy")):
+        _need(t, dt, nm)
+    wp, wn = _ws(workspace)
+    _check("dfp_conv_fwd_i32", lib().dfp_conv_fwd_i32(ctypes.byref(d), _ptr(x), _ptr(sx), _ptr(w), _ptr(sw),
+                                                      _ptr(y), _ptr(sy), wp, wn, _stream(stream)))
+
+
+def dfp_conv_bwd_data_i32(d: Desc, dy, sdy, w, sw, dx, sdx, workspace=None, stream=None):
+    for t, dt, nm in ((dy, torch.int16, "dy"), (w, torch.int16, "w"), (dx, torch.int32, "dx"),
+                      (sdy, torch.int32, "sdy"), (sw, torch.int32, "sw"), (sdx, torch.int32, "sdx")):
+        _need(t, dt, nm)
+    wp, wn = _ws(workspace)
+    _check("dfp_conv_bwd_data_i32", lib().dfp_conv_bwd_data_i32(ctypes.byref(d), _ptr(dy), _ptr(sdy), _ptr(w),
+                                                                _ptr(sw), _ptr(dx), _ptr(sdx), wp, wn,
+                                                                _stream(stream)))
+
+
+def dfp_downconvert_i32(d: Desc, role: int, src, sin, dst, sout, amax_ready: bool = False, stream=None):
+    for t, dt, nm in ((src, torch.int32, "src"), (dst, torch.int16, "dst"), (sin, torch.int32, "sin"),
+                      (sout, torch.int32, "sout")):
+        _need(t, dt, nm)
+    _check("dfp_downconvert_i32", lib().dfp_downconvert_i32(ctypes.byref(d), role, _ptr(src), _ptr(sin), _ptr(dst),
+                                                            _ptr(sout), int(bool(amax_ready)), _stream(stream)))
 
 
 def alloc_workspace(d: Desc, direction: int, device="cuda"):

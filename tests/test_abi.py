@@ -39,7 +39,8 @@ def test_every_declared_symbol_is_exported(dl):
 
 def test_binding_exposes_same_names(dl):
     import paper_1802_00930_amd.dfp as b
-    for n in ("dfp_quantize", "dfp_conv_fwd", "dfp_conv_bwd_data", "dfp_conv_bwd_weights", "dfp_downconvert"):
+    for n in ("dfp_quantize", "dfp_conv_fwd", "dfp_conv_bwd_data", "dfp_conv_bwd_weights", "dfp_downconvert",
+              "dfp_conv_fwd_i32", "dfp_conv_bwd_data_i32", "dfp_downconvert_i32"):
         assert callable(getattr(b, n))
 
 
@@ -141,6 +142,44 @@ def test_conv_workspace_checked(dl):
             rc = lib.dfp_conv_bwd_weights(ctypes.byref(d), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE),
                                           *args_small, None, None)
         assert rc == dl.ERR_WORKSPACE
+
+
+def _conv_i32(dl, direction, d, so=FAKE, ws=None, wsn=0):
+    f = dl.lib().dfp_conv_fwd_i32 if direction == dl.FWD else dl.lib().dfp_conv_bwd_data_i32
+    return f(ctypes.byref(d), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), _p(so) if so else None,
+             _p(ws) if ws else None, wsn, None)
+
+
+def test_conv_i32_rejects(dl):
+    # the single chunk must cover the reduction: C*R*S = 144 forward, K*R*S = 288 backward-data
+    for direction, t in ((dl.FWD, 144), (dl.BWD_DATA, 288)):
+        short = good_desc(dl, chunk_len=t - 1, path=dl.PATH_VALU)
+        assert _conv_i32(dl, direction, short) == dl.ERR_PARAM
+        ok = good_desc(dl, chunk_len=t, path=dl.PATH_VALU)
+        assert _conv_i32(dl, direction, ok, so=0) == dl.ERR_NULL
+        assert _conv_i32(dl, direction, ok, so=FAKE + 8) == dl.ERR_ALIGN
+        mf = good_desc(dl, chunk_len=t, path=dl.PATH_MFMA)
+        need = dl.workspace_bytes(mf, direction)
+        assert need > 0
+        assert _conv_i32(dl, direction, mf, ws=FAKE, wsn=need - 1) == dl.ERR_WORKSPACE
+    assert _conv_i32(dl, dl.FWD, good_desc(dl, chunk_len=144, h=2, pad=0)) == dl.ERR_SHAPE
+
+
+def test_downconvert_i32_rejects(dl):
+    d = good_desc(dl)
+    f = dl.lib().dfp_downconvert_i32
+
+    def call(role=dl.ROLE_Y, src=FAKE, sin=FAKE, dst=FAKE + 4096, sout=FAKE + 8192, ready=1):
+        return f(ctypes.byref(d), role, _p(src), _p(sin), _p(dst), _p(sout), ready, None)
+    assert call(role=dl.ROLE_X) == dl.ERR_PARAM
+    assert call(role=dl.ROLE_W) == dl.ERR_PARAM
+    assert call(ready=2) == dl.ERR_PARAM
+    assert call(sout=FAKE) == dl.ERR_PARAM  # sin and sout must differ
+    assert call(src=0) == dl.ERR_NULL
+    assert call(sin=0) == dl.ERR_NULL
+    assert call(src=FAKE + 8) == dl.ERR_ALIGN
+    assert call(dst=FAKE + 4096 + 4) == dl.ERR_ALIGN
+    assert call(sin=FAKE + 4) == dl.ERR_ALIGN
 
 
 def test_host_queries(dl):

@@ -135,3 +135,38 @@ def test_resnet50_all_53_layers():
         layer, x, w, dy = layer_inputs(wl, i)
         check_layer(layer, x, w, dy, 64, "nearest", wl.seed, nsample=1500, partial_samples=8)
         torch.cuda.empty_cache()
+
+
+def test_resnet50_conv2x_3x3_dfp32_full():
+    """The same layer through the single-chunk DFP-32 outputs (forward and
+    backward-data at L = C*R*S = K*R*S = 576) and the integer down-convert
+    with the epilogue's max, every element against the oracle."""
+    wl = WORKLOADS["resnet50_conv2x_3x3"]
+    layer, x, w, dy = layer_inputs(wl, 0)
+    L = layer.c * layer.r * layer.s
+    gl = GpuLayer(layer.n, layer.c, layer.h, layer.w, layer.k, layer.r, layer.s, layer.stride, layer.pad, L=L,
+                  rounding="stochastic", seed=wl.seed)
+    g = oracle_geom(gl)
+    rnd = oracle.ROUNDING["stochastic"]
+    qx, sx, ox, ex = _quantize_both(gl, x, dfp.ROLE_X, 15, "stochastic", wl.seed)
+    qw, sw, ow, ew = _quantize_both(gl, w, dfp.ROLE_W, 15, "stochastic", wl.seed)
+    qdy, sdy, ody, edy = _quantize_both(gl, dy, dfp.ROLE_DY, 15, "stochastic", wl.seed)
+    for direction, a, sa, oa, ea, role, shape in ((dfp.FWD, qx, sx, ox, ex, dfp.ROLE_Y, gl.shape_y),
+                                                  (dfp.BWD_DATA, qdy, sdy, ody, edy, dfp.ROLE_DX, gl.shape_x)):
+        note("dfp32 layer %s dir %d" % (layer.name, direction))
+        out = torch.empty(shape, dtype=torch.int32, device=DEV)
+        so = dfp.new_scale(DEV)
+        ws = dfp.alloc_workspace(gl.d, direction, DEV)
+        f = dfp.dfp_conv_fwd_i32 if direction == dfp.FWD else dfp.dfp_conv_bwd_data_i32
+        f(gl.d, a, sa, qw, sw, out, so, ws)
+        q = torch.empty(shape, dtype=torch.int16, device=DEV)
+        sq = dfp.new_scale(DEV)
+        dfp.dfp_downconvert_i32(gl.d, role, out, so, q, sq, amax_ready=True)
+        _, rparts, _ = oracle.conv(g, direction, oa, ow, ea + ew, L, 1, want_partials=True)
+        rq, re, rf = oracle.downconvert_i32(rparts[0], ea + ew, 15, rnd, wl.seed, role)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy().reshape(-1), rparts[0])
+        assert np.array_equal(q.cpu().numpy().reshape(-1), rq)
+        s = dfp.read_scale(sq)
+        assert (s["exp"], s["flags"]) == (re, rf)
+        del out, q, ws
