@@ -48,6 +48,7 @@ def parse():
                     help="backward-weights segment size G in chunks (part of the numerics: the oracle uses the same)")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-dfp32", action="store_true", help="skip the DFP-32-output variant of the step")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES five times (counter calibration)")
@@ -259,17 +260,19 @@ def main():
             del s2
 
     # the DFP-32-output variant of the same step (reported beside the headline)
-    s32 = StepDfp32(layer, x, w, dy, a.chunk, rounding, seed, a.path, dev, a.seg_chunks)
-    t32, _ = timed(s32, a.steps, a.warmup)
-    _, recs32 = timed(s32, a.steps, 1, profile=True)
-    k32 = {}
-    for name, ms in recs32:
-        k32.setdefault(name, []).append(ms)
-    dfp32 = {"ms_per_step": round(t32 * 1e3, 4), "tops": round(3 * ops_per_dir / t32 / 1e12, 3),
-             "chunk_len_fwd_bwd_data": s32.d32.chunk_len,
-             "kernels": {k: {"launches_per_step": len(v) / a.steps, "avg_ms": round(float(np.mean(v)), 5)}
-                         for k, v in k32.items()}}
-    del s32
+    dfp32 = None
+    if not a.no_dfp32:
+        s32 = StepDfp32(layer, x, w, dy, a.chunk, rounding, seed, a.path, dev, a.seg_chunks)
+        t32, _ = timed(s32, a.steps, a.warmup)
+        _, recs32 = timed(s32, a.steps, 1, profile=True)
+        k32 = {}
+        for name, ms in recs32:
+            k32.setdefault(name, []).append(ms)
+        dfp32 = {"ms_per_step": round(t32 * 1e3, 4), "tops": round(3 * ops_per_dir / t32 / 1e12, 3),
+                 "chunk_len_fwd_bwd_data": s32.d32.chunk_len,
+                 "kernels": {k: {"launches_per_step": len(v) / a.steps, "avg_ms": round(float(np.mean(v)), 5)}
+                             for k, v in k32.items()}}
+        del s32
 
     out = {
         "metric": METRIC,
