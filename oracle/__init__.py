@@ -80,6 +80,9 @@ def lib():
         L.orc_default_seg_chunks.restype = ctypes.c_int32
         L.orc_output_flags.argtypes = [P, ctypes.c_int64]
         L.orc_output_flags.restype = ctypes.c_uint32
+        L.orc_gemm.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_int, P, P,
+                               ctypes.c_int32, ctypes.c_int32, P, P]
+        L.orc_gemm.restype = ctypes.c_int64
         _lib = L
     return _lib
 
@@ -199,3 +202,25 @@ def conv_at(g: Geom, direction: int, a: np.ndarray, b: np.ndarray, e: int, L: in
 def output_flags(y: np.ndarray) -> int:
     y = np.ascontiguousarray(y, dtype=np.float32)
     return int(lib().orc_output_flags(_ptr(y), y.size))
+
+
+# --------------------------------------------------------------------------
+# GEMM with the forward convolution's chunked contract (Alg. 2, Sec. 4.3; the
+# paper's kernels serve "convolutions and GEMM", Sec. 4).
+# --------------------------------------------------------------------------
+def gemm(a: np.ndarray, b: np.ndarray, e: int, L: int, trans_a: bool = False, trans_b: bool = False,
+         want_partials: bool = False):
+    """D = opA @ opB with INT32 partials over chunks of L reduction indices,
+    FP32 sum in chunk order, scale 2^e.  a is stored [m, k] (or [k, m] with
+    trans_a), b [k, n] (or [n, k] with trans_b).  Returns (D float32 [m, n],
+    partials int32 [J, m*n] or None, wrapped-partial count)."""
+    a = np.ascontiguousarray(a, dtype=np.int16)
+    b = np.ascontiguousarray(b, dtype=np.int16)
+    m, k = (a.shape[1], a.shape[0]) if trans_a else a.shape
+    kb, n = (b.shape[1], b.shape[0]) if trans_b else b.shape
+    assert k == kb, (a.shape, b.shape, trans_a, trans_b)
+    out = np.empty((m, n), dtype=np.float32)
+    parts = np.empty(((k + L - 1) // L, m * n), dtype=np.int32) if want_partials else None
+    ov = lib().orc_gemm(m, n, k, int(trans_a), int(trans_b), _ptr(a), _ptr(b), e, L, _ptr(out),
+                        _ptr(parts) if parts is not None else None)
+    return out, parts, int(ov)

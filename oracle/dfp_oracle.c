@@ -413,3 +413,40 @@ uint32_t orc_output_flags(const float *y, int64_t n) {
     if (isinf(y[i])) return ORC_FLAG_OUTPUT_INF;
   return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* GEMM (the paper applies the same INT16 kernels to "convolutions and GEMM",
+ * Sec. 4): D[i][j] = sum over t of opA[i][t] * opB[t][j], t in [0, k), with
+ * the forward convolution's contract (Alg. 2, Sec. 4.3): INT32 partials over
+ * chunks of L consecutive t (mod 2^32), converted to FP32 and added in chunk
+ * order, scaled once by 2^e.  opA[i][t] = a[i*k + t] (trans_a = 0) or
+ * a[t*m + i] (trans_a = 1); opB[t][j] = b[t*n + j] (trans_b = 0) or
+ * b[j*k + t] (trans_b = 1).  D is row-major [m][n]; partials (nullable) is
+ * [J][m*n].  Returns the number of wrapped partials. */
+/* ------------------------------------------------------------------------ */
+int64_t orc_gemm(int64_t m, int64_t n, int64_t k, int trans_a, int trans_b, const int16_t *a,
+                 const int16_t *b, int32_t e, int32_t L, float *out, int32_t *partials) {
+  int64_t J = (k + L - 1) / L;
+  int64_t overflow = 0;
+#pragma omp parallel for schedule(dynamic, 16) reduction(+ : overflow)
+  for (int64_t o = 0; o < m * n; ++o) {
+    int64_t i = o / n, j = o % n;
+    float total = 0.0f;
+    for (int64_t c = 0; c < J; ++c) {
+      int64_t exact = 0;
+      int64_t t_end = (c + 1) * (int64_t)L < k ? (c + 1) * (int64_t)L : k;
+      for (int64_t t = c * (int64_t)L; t < t_end; ++t) {
+        int64_t av = trans_a ? a[t * m + i] : a[i * k + t];
+        int64_t bv = trans_b ? b[j * k + t] : b[t * n + j];
+        exact += av * bv;
+      }
+      int64_t pc = wrap32(exact);
+      if (pc != exact) ++overflow;
+      if (partials) partials[c * m * n + o] = (int32_t)pc;
+      float fc = (float)pc;
+      total = (c == 0) ? fc : total + fc;
+    }
+    out[o] = scale_out(total, e);
+  }
+  return overflow;
+}
