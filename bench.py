@@ -49,6 +49,7 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dfp32", action="store_true", help="skip the DFP-32-output variant of the step")
+    ap.add_argument("--no-gemm", action="store_true", help="skip the GEMM measurements")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES five times (counter calibration)")
@@ -145,6 +146,72 @@ class StepDfp32(Step):
         dfp.dfp_conv_bwd_data_i32(d32, self.qdy, self.sdy, self.qw, self.sw, self.dx, self.sdx, self.ws32[1])
         dfp.dfp_downconvert_i32(d32, dfp.ROLE_DX, self.dx, self.sdx, self.qdx, self.sqdx, amax_ready=True)
         dfp.dfp_conv_bwd_weights(d, self.qx, self.sx, self.qdy, self.sdy, self.dw, self.ws[2])
+
+
+class FcStep:
+    """One DFP step of a fully connected layer through the GEMM entry point:
+    Q(x), Q(W), Q(dy), y = x W^T, DC(y), dx = dy W, DC(dx), dW = dy^T x."""
+
+    def __init__(self, batch, fin, fout, L, rounding, seed, dev):
+        import torch
+        from paper_1802_00930_amd import dfp
+        self.dfp, self.torch = dfp, torch
+        self.rounding, self.seed = rounding, seed
+        g = torch.Generator(device="cpu").manual_seed(seed)
+        self.fx = torch.relu(torch.randn(batch, fin, generator=g)).to(dev)
+        self.fw = (torch.randn(fout, fin, generator=g) * (1.0 / fin) ** 0.5).to(dev)
+        self.fdy = (torch.randn(batch, fout, generator=g) * 1e-3).to(dev)
+        self.q = {k: torch.empty_like(v, dtype=torch.int16) for k, v in
+                  (("x", self.fx), ("w", self.fw), ("dy", self.fdy))}
+        self.s = {k: dfp.new_scale(dev) for k in ("x", "w", "dy", "y", "dx")}
+        self.y = torch.empty(batch, fout, device=dev)
+        self.dx = torch.empty(batch, fin, device=dev)
+        self.dw = torch.empty(fout, fin, device=dev)
+        self.qy = torch.empty_like(self.y, dtype=torch.int16)
+        self.qdx = torch.empty_like(self.dx, dtype=torch.int16)
+        self.d = [dfp.make_gemm_desc(batch, fout, fin, False, True, L),
+                  dfp.make_gemm_desc(batch, fin, fout, False, False, L),
+                  dfp.make_gemm_desc(fout, fin, batch, True, False, L)]
+        self.ws = [dfp.alloc_gemm_workspace(d, dev) for d in self.d]
+        self.macs = batch * fin * fout
+
+    def run(self):
+        dfp, q, s, r, sd = self.dfp, self.q, self.s, self.rounding, self.seed
+        dfp.dfp_quantize_tensor(15, r, sd, dfp.ROLE_X, self.fx, q["x"], s["x"])
+        dfp.dfp_quantize_tensor(15, r, sd, dfp.ROLE_W, self.fw, q["w"], s["w"])
+        dfp.dfp_quantize_tensor(15, r, sd, dfp.ROLE_DY, self.fdy, q["dy"], s["dy"])
+        dfp.dfp_gemm(self.d[0], q["x"], s["x"], q["w"], s["w"], self.y, s["y"], self.ws[0])
+        dfp.dfp_downconvert_tensor(15, r, sd, dfp.ROLE_Y, self.y, self.qy, s["y"], amax_ready=True)
+        dfp.dfp_gemm(self.d[1], q["dy"], s["dy"], q["w"], s["w"], self.dx, s["dx"], self.ws[1])
+        dfp.dfp_downconvert_tensor(15, r, sd, dfp.ROLE_DX, self.dx, self.qdx, s["dx"], amax_ready=True)
+        dfp.dfp_gemm(self.d[2], q["dy"], s["dy"], q["x"], s["x"], self.dw, None, self.ws[2])
+
+
+class GemmStep:
+    """One DFP16 GEMM D = A B^T of m x n x k on operands already quantised."""
+
+    def __init__(self, m, n, k, L, dev):
+        import torch
+        from paper_1802_00930_amd import dfp
+        self.dfp, self.torch = dfp, torch
+        g = torch.Generator(device="cpu").manual_seed(7)
+        self.a = torch.randint(-16384, 16385, (m, k), dtype=torch.int16, generator=g).to(dev)
+        self.b = torch.randint(-16384, 16385, (n, k), dtype=torch.int16, generator=g).to(dev)
+        self.sa, self.sb, self.sd = (torch.tensor([0, -14, 0, 0], dtype=torch.int32, device=dev) for _ in range(3))
+        self.out = torch.empty(m, n, device=dev)
+        self.d = dfp.make_gemm_desc(m, n, k, False, True, L)
+        self.ws = dfp.alloc_gemm_workspace(self.d, dev)
+        self.macs = m * n * k
+
+    def run(self):
+        self.dfp.dfp_gemm(self.d, self.a, self.sa, self.b, self.sb, self.out, self.sd, self.ws)
+
+
+def kernel_table(recs, steps):
+    per = {}
+    for name, ms in recs:
+        per.setdefault(name, []).append(ms)
+    return {k: {"launches_per_step": len(v) / steps, "avg_ms": round(float(np.mean(v)), 5)} for k, v in per.items()}
 
 
 def timed(step, steps, warmup, profile=False):
@@ -274,6 +341,30 @@ def main():
                              for k, v in k32.items()}}
         del s32
 
+    # DFP16 GEMM: ResNet-50's FC layer step and one large product (reported beside the headline)
+    gemm = None
+    if not a.no_gemm:
+        fc = FcStep(64, 2048, 1000, a.chunk, rounding, seed, dev)
+        tf, _ = timed(fc, a.steps, a.warmup)
+        _, rf = timed(fc, a.steps, 1, profile=True)
+        big = GemmStep(4096, 4096, 4096, a.chunk, dev)
+        tb, _ = timed(big, max(3, a.steps // 2), 2)
+        _, rb = timed(big, max(3, a.steps // 2), 1, profile=True)
+        kb = kernel_table(rb, max(3, a.steps // 2))
+        gemm_ms = kb["gemm"]["avg_ms"]
+        gemm_tops = 2.0 * big.macs / (gemm_ms * 1e-3) / 1e12
+        gemm = {
+            "fc_2048x1000_b64": {"ms_per_step": round(tf * 1e3, 4),
+                                 "tops": round(3 * 2.0 * fc.macs / tf / 1e12, 3),
+                                 "kernels": kernel_table(rf, a.steps)},
+            "gemm_4096x4096x4096": {"ms_per_call": round(tb * 1e3, 4),
+                                    "tops_call": round(2.0 * big.macs / tb / 1e12, 3),
+                                    "kernel_tops": round(gemm_tops, 3),
+                                    "kernel_frac": round(gemm_tops / PEAK_INT16_BYTESPLIT_TOPS, 4),
+                                    "kernels": kb},
+        }
+        del fc, big
+
     out = {
         "metric": METRIC,
         "value": round(3 * ops_per_dir / sec / 1e12, 4),
@@ -307,6 +398,7 @@ def main():
         "kernels": {k: {kk: round(vv, 5) for kk, vv in v.items()} for k, v in kstats.items()},
         "chunk_sweep": sweep,
         "dfp32_outputs": dfp32,
+        "gemm": gemm,
     }
     if not a.no_cpu:
         out["cpu_baseline"] = cpu_baseline(layer, x, w, dy, a.chunk, a.seg_chunks, rounding, seed, a.cpu_seconds)

@@ -223,6 +223,52 @@ size_t dfp_workspace_bytes(const dfp_desc* d, int32_t direction);
 /* Number of chunks J = ceil(T / L) of a direction; -1 for an invalid descriptor. */
 int64_t dfp_num_chunks(const dfp_desc* d, int32_t direction);
 
+/* ---------------------------------------------------------------- GEMM --
+ * The paper's INT16 kernels serve "convolutions and GEMM" (Sec. 4); its FC
+ * layers stayed FP32 in the experiments.  dfp_gemm computes
+ *   D[i][j] = 2^(Ea+Eb) * fold over chunks c of fl32(P_c[i][j]),
+ *   P_c[i][j] = sum over t in [cL, min(k, (c+1)L)) of opA[i][t] * opB[t][j]
+ * (mod 2^32), the fold adding in chunk order in FP32 with the scale applied
+ * once: the forward convolution's contract (Alg. 2, Sec. 4.3).  Layouts,
+ * all row-major: opA[i][t] = a[i*k + t] (trans_a = 0) or a[t*m + i]
+ * (trans_a = 1); opB[t][j] = b[t*n + j] (trans_b = 0) or b[j*k + t]
+ * (trans_b = 1); D is [m][n].  A fully connected layer y = x W^T with
+ * x [batch][in], W [out][in] is (m, n, k) = (batch, out, in), trans_b = 1;
+ * its backward-data dx = dy W is (batch, in, out), no transposes; its
+ * backward-weights dW = dy^T x is (out, in, batch), trans_a = 1. */
+typedef struct dfp_gemm_desc {
+  int32_t m, n, k;          /* >= 1; m*n, m*k, k*n at most 2^40                */
+  int32_t trans_a, trans_b; /* 0 or 1, as above                                  */
+  int32_t chunk_len;        /* L >= 1                                            */
+  int32_t bits;             /* P of the operands, 15 or 16 (16: VALU path)       */
+  int32_t path;             /* dfp_path                                          */
+} dfp_gemm_desc;
+
+/* a, b: INT16 operands of P = bits (at P = 15 |i| <= 2^14); sa, sb: their
+ * scales (exp read on the device), 16-byte aligned.  out: FP32 [m][n].
+ * sd (nullable, 16-byte aligned): cleared, then receives max |D| as FP32 bits
+ * and OUTPUT_INF, ready for dfp_downconvert_tensor(..., amax_ready = 1).
+ * partials (nullable): INT32 [J][m*n], every chunk partial.  workspace: at
+ * least dfp_gemm_workspace_bytes(d) bytes, 256-byte aligned (the operands'
+ * digit planes).  Errors as for the convolutions. */
+dfp_status dfp_gemm(const dfp_gemm_desc* d, const int16_t* a, const dfp_scale* sa, const int16_t* b,
+                    const dfp_scale* sb, float* out, dfp_scale* sd, void* workspace, size_t ws_bytes,
+                    int32_t* partials, void* stream);
+/* Workspace bytes of dfp_gemm (0 on the VALU path or for an invalid descriptor). */
+size_t dfp_gemm_workspace_bytes(const dfp_gemm_desc* d);
+/* J = ceil(k / L); -1 for an invalid descriptor. */
+int64_t dfp_gemm_num_chunks(const dfp_gemm_desc* d);
+
+/* dfp_quantize / dfp_downconvert for a flat tensor of n elements (GEMM
+ * operands and outputs): the same numerics, bits in {15, 16}, rounding a
+ * dfp_rounding, role (any dfp_role) selecting the stochastic stream.
+ * Alignment, scratch use of dst and errors as for dfp_quantize. */
+dfp_status dfp_quantize_tensor(int64_t n, int32_t bits, int32_t rounding, uint64_t seed, int32_t role,
+                               const float* src, int16_t* dst, dfp_scale* s, void* stream);
+dfp_status dfp_downconvert_tensor(int64_t n, int32_t bits, int32_t rounding, uint64_t seed, int32_t role,
+                                  const float* src, int16_t* dst, dfp_scale* s, int32_t amax_ready,
+                                  void* stream);
+
 /* Output height and width of the forward convolution; DFP_ERR_SHAPE if < 1. */
 dfp_status dfp_output_dims(const dfp_desc* d, int32_t* p, int32_t* q);
 

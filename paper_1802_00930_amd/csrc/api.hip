@@ -131,6 +131,26 @@ dfp_status ws_check(const Geom& g, int32_t dir, int32_t path, int32_t bits, cons
   return DFP_OK;
 }
 
+// GEMM descriptor and flat-tensor checks.
+dfp_status gemm_desc_check(const dfp_gemm_desc* d) {
+  if (!d) return DFP_ERR_NULL;
+  if (d->m < 1 || d->n < 1 || d->k < 1) return DFP_ERR_SHAPE;
+  if ((int64_t)d->m * d->n > ((int64_t)1 << 40) || (int64_t)d->m * d->k > ((int64_t)1 << 40) ||
+      (int64_t)d->k * d->n > ((int64_t)1 << 40))
+    return DFP_ERR_SHAPE;
+  if ((d->trans_a != 0 && d->trans_a != 1) || (d->trans_b != 0 && d->trans_b != 1)) return DFP_ERR_PARAM;
+  if (d->chunk_len < 1 || (d->bits != 15 && d->bits != 16)) return DFP_ERR_PARAM;
+  if (d->path < DFP_PATH_AUTO || d->path > DFP_PATH_VALU) return DFP_ERR_PARAM;
+  return DFP_OK;
+}
+bool gemm_use_mfma(const dfp_gemm_desc* d) {
+  // grid rows of 64-row tiles must fit a launch dimension
+  return d->path != DFP_PATH_VALU && d->bits == 15 && (d->m + 63) / 64 <= 65535;
+}
+bool flat_params_ok(int64_t n, int32_t bits, int32_t rounding, int32_t role) {
+  return n >= 1 && n <= ((int64_t)1 << 40) && (bits == 15 || bits == 16) && rounding >= 0 && rounding <= 3 &&
+         role >= DFP_ROLE_X && role <= DFP_ROLE_DX;
+}
 }  // namespace
 }  // namespace dfp
 
@@ -266,6 +286,61 @@ dfp_status dfp_downconvert_i32(const dfp_desc* d, int32_t role, const int32_t* s
                                 (uint32_t)role, (hipStream_t)stream);
 }
 
+// ------------------------------------------------------------------ GEMM
+size_t dfp_gemm_workspace_bytes(const dfp_gemm_desc* d) {
+  if (gemm_desc_check(d) != DFP_OK || !gemm_use_mfma(d)) return 0;
+  return (size_t)plan_gemm(d->m, d->n, d->k).bytes;
+}
+
+int64_t dfp_gemm_num_chunks(const dfp_gemm_desc* d) {
+  if (gemm_desc_check(d) != DFP_OK) return -1;
+  return ((int64_t)d->k + d->chunk_len - 1) / d->chunk_len;
+}
+
+dfp_status dfp_gemm(const dfp_gemm_desc* d, const int16_t* a, const dfp_scale* sa, const int16_t* b,
+                    const dfp_scale* sb, float* out, dfp_scale* sd, void* workspace, size_t ws_bytes,
+                    int32_t* partials, void* stream) {
+  dfp_status rc = gemm_desc_check(d);
+  if (rc != DFP_OK) return rc;
+  if (!a || !sa || !b || !sb || !out) return DFP_ERR_NULL;
+  if (!aligned(a, 2) || !aligned(b, 2) || !aligned(out, 4) || (sd && !aligned(sd, 16)) ||
+      (partials && !aligned(partials, 4)) || !aligned(sa, 16) || !aligned(sb, 16))
+    return DFP_ERR_ALIGN;
+  hipStream_t st = (hipStream_t)stream;
+  if (gemm_use_mfma(d)) {
+    const size_t need = (size_t)plan_gemm(d->m, d->n, d->k).bytes;
+    if (!workspace || ws_bytes < need || !aligned(workspace, 256)) return DFP_ERR_WORKSPACE;
+    return launch_gemm_mfma(d->m, d->n, d->k, d->trans_a, d->trans_b, d->chunk_len, a, sa, b, sb, out, sd,
+                            partials, workspace, st);
+  }
+  if (sd && (rc = launch_scale_reset(sd, st)) != DFP_OK) return rc;
+  return launch_gemm_valu(d->m, d->n, d->k, d->trans_a, d->trans_b, d->chunk_len, a, sa, b, sb, out, sd,
+                          partials, st);
+}
+
+dfp_status dfp_quantize_tensor(int64_t n, int32_t bits, int32_t rounding, uint64_t seed, int32_t role,
+                               const float* src, int16_t* dst, dfp_scale* s, void* stream) {
+  if (!src || !dst || !s) return DFP_ERR_NULL;
+  if (!flat_params_ok(n, bits, rounding, role)) return DFP_ERR_PARAM;
+  if (!aligned(src, 16) || !aligned(dst, 8) || !aligned(s, 16)) return DFP_ERR_ALIGN;
+  hipStream_t st = (hipStream_t)stream;
+  dfp_status rc;
+  if ((rc = launch_amax(src, n, dst, s, st)) != DFP_OK) return rc;
+  return launch_quant_convert(src, dst, n, s, bits, rounding, seed, (uint32_t)role, st);
+}
+
+dfp_status dfp_downconvert_tensor(int64_t n, int32_t bits, int32_t rounding, uint64_t seed, int32_t role,
+                                  const float* src, int16_t* dst, dfp_scale* s, int32_t amax_ready,
+                                  void* stream) {
+  if (!src || !dst || !s) return DFP_ERR_NULL;
+  if (!flat_params_ok(n, bits, rounding, role) || (amax_ready != 0 && amax_ready != 1)) return DFP_ERR_PARAM;
+  if (!aligned(src, 16) || !aligned(dst, 8) || !aligned(s, 16)) return DFP_ERR_ALIGN;
+  hipStream_t st = (hipStream_t)stream;
+  dfp_status rc;
+  if (!amax_ready && (rc = launch_amax(src, n, dst, s, st)) != DFP_OK) return rc;
+  return launch_quant_convert(src, dst, n, s, bits, rounding, seed, (uint32_t)role, st);
+}
+
 dfp_status dfp_conv_fwd(const dfp_desc* d, const int16_t* x, const dfp_scale* sx, const int16_t* w,
                         const dfp_scale* sw, float* y, dfp_scale* sy, void* workspace, size_t ws_bytes,
                         int32_t* partials, void* stream) {
@@ -322,7 +397,7 @@ const char* dfp_kernel_name(int32_t id) {
   static const char* names[K_NUM_KERNELS] = {
       "scale_reset", "amax", "quant_convert", "conv_fwd_valu", "conv_bwd_data_valu", "conv_bwd_wt_valu",
       "weight_prep", "conv_fwd_mfma", "conv_bwd_data_mfma", "conv_bwd_wt_mfma", "bwd_wt_segment_reduce",
-      "act_prep", "conv_fwd_i32", "conv_bwd_data_i32", "downconvert_i32"};
+      "act_prep", "conv_fwd_i32", "conv_bwd_data_i32", "downconvert_i32", "gemm_prep", "gemm"};
   if (id < 0 || id >= K_NUM_KERNELS) return "unknown";
   return names[id];
 }

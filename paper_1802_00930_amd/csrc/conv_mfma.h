@@ -27,7 +27,13 @@ struct ConvMfmaArgs {
   int32_t ustride_h, ustride_w, rsign, roff_h, roff_w;
 };
 
+// Output rows per workgroup tile of the main kernels (A digits are padded to it).
+constexpr int32_t kMfmaRowTile = 64;
+
 ConvMfmaPlan plan_conv_mfma(const Geom& g, int32_t dir);
+// Picks and launches the main kernel for prepared digit operands (args.L,
+// args.partials and i32 select it); ws_b_bytes is the size of args.xs.
+dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int kid32, bool i32, hipStream_t st);
 // The B prep kernel stages one source row of at least 16 channels in LDS.
 bool conv_mfma_supported(const Geom& g, int32_t dir);
 dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,

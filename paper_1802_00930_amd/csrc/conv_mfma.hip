@@ -47,6 +47,7 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;
 constexpr int kMT = 64;   // output channels per workgroup
+static_assert(kMT == kMfmaRowTile, "row tile shared with the GEMM preps");
 constexpr int kNT = 128;  // output pixels per workgroup
 
 // Byte digits of an INT16 value.
@@ -1446,29 +1447,32 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
     args.roff_h = g.r - 1;
     args.roff_w = g.s - 1;
   }
-  const dim3 grid((unsigned)((args.NP + kNT - 1) / kNT), (unsigned)(p.Mp / kMT));
-  const bool masked = (g.L % 32) != 0;
-  const bool chan16 = (p.Cin % 16) == 0;
-  const int kid = fwd ? K_FWD_MFMA : K_BWDD_MFMA;
+  return launch_mfma_main(args, p.ws_b_bytes, fwd ? K_FWD_MFMA : K_BWDD_MFMA, fwd ? K_FWD_I32 : K_BWDD_I32, i32, st);
+}
+
+dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int kid32, bool i32, hipStream_t st) {
+  const dim3 grid((unsigned)((args.NP + kNT - 1) / kNT), (unsigned)(args.Mp / kMT));
+  const bool masked = (args.L % 32) != 0;
+  const bool chan16 = (args.Cin % 16) == 0;
+  const bool partials = args.partials != nullptr;
   // persistent grid: one workgroup per CU for each 64-row tile of the output channels
   auto persist_grid = [&]() {
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     const int64_t wave_tiles = (args.NP + 31) / 32;
-    const int64_t mtiles = p.Mp / kMT;
+    const int64_t mtiles = args.Mp / kMT;
     int64_t gx = std::max<int64_t>(1, cus / mtiles);
     gx = std::min<int64_t>(gx, (wave_tiles + kWaves3 - 1) / kWaves3);
     return dim3((unsigned)gx, (unsigned)mtiles);
   };
-  const bool persist_ok = chan16 && (p.T % 64) == 0 && p.KB >= 4 && p.KB <= kARes3Max && args.O < (1ll << 31) &&
-                          p.ws_b_bytes < (1ll << 31);
+  const bool small_index = args.O < (1ll << 31) && ws_b_bytes < (1ll << 31);
+  const bool persist_ok = chan16 && (args.T % 64) == 0 && args.KB >= 4 && args.KB <= kARes3Max && small_index;
   if (i32) {
     // DFP-32 output: one chunk over the whole reduction (the caller checked L >= T)
-    args.L = p.KB * 32;
-    const int kid32 = fwd ? K_FWD_I32 : K_BWDD_I32;
+    args.L = args.KB * 32;
     if (persist_ok)
       DFP_LAUNCH(kid32, (k_conv_mfma_persist<false, true>), persist_grid(), dim3(kThreads3), 0, st, args);
-    else if (chan16 && args.O < (1ll << 31) && p.ws_b_bytes < (1ll << 31))
+    else if (chan16 && small_index)
       DFP_LAUNCH(kid32, (k_conv_mfma_q<false, true>), grid, dim3(kThreadsQ), 0, st, args);
     else if (chan16)
       DFP_LAUNCH(kid32, (k_conv_mfma<false, false, true, true>), grid, dim3(kThreads), 0, st, args);
@@ -1477,22 +1481,22 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
     return DFP_OK;
   }
 #define DFP_CONV_MFMA_CASE(MK, PT, CH)                                                      \
-  if (masked == MK && (partials != nullptr) == PT && chan16 == CH) {                       \
+  if (masked == MK && partials == PT && chan16 == CH) {                                    \
     DFP_LAUNCH(kid, (k_conv_mfma<MK, PT, CH>), grid, dim3(kThreads), 0, st, args);          \
     return DFP_OK;                                                                          \
   }
-  if (persist_ok && g.L == 64) {
+  if (persist_ok && args.L == 64) {
     const dim3 grid3 = persist_grid();
     if (partials) DFP_LAUNCH(kid, (k_conv_mfma_persist<true>), grid3, dim3(kThreads3), 0, st, args);
     else DFP_LAUNCH(kid, (k_conv_mfma_persist<false>), grid3, dim3(kThreads3), 0, st, args);
     return DFP_OK;
   }
-  if (chan16 && !masked && args.O < (1ll << 31) && p.ws_b_bytes < (1ll << 31)) {
+  if (chan16 && !masked && small_index) {
     if (partials) DFP_LAUNCH(kid, (k_conv_mfma_q<true>), grid, dim3(kThreadsQ), 0, st, args);
     else DFP_LAUNCH(kid, (k_conv_mfma_q<false>), grid, dim3(kThreadsQ), 0, st, args);
     return DFP_OK;
   }
-  if (chan16 && g.L == 64 && (p.T % 64) == 0 && p.KB >= 4) {
+  if (chan16 && args.L == 64 && (args.T % 64) == 0 && args.KB >= 4) {
     if (partials) DFP_LAUNCH(kid, (k_conv_mfma_skew<true>), grid, dim3(kThreads), 0, st, args);
     else DFP_LAUNCH(kid, (k_conv_mfma_skew<false>), grid, dim3(kThreads), 0, st, args);
     return DFP_OK;

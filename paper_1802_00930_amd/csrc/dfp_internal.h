@@ -25,7 +25,9 @@ enum KernelId : int32_t {
   K_FWD_I32 = 12,
   K_BWDD_I32 = 13,
   K_DC_I32 = 14,
-  K_NUM_KERNELS = 15
+  K_GEMM_PREP = 15,
+  K_GEMM = 16,
+  K_NUM_KERNELS = 17
 };
 
 // Convolution geometry handed to kernels by value.
@@ -73,5 +75,19 @@ dfp_status launch_downconvert_i32(const int32_t* src, int64_t n, const dfp_scale
 dfp_status launch_conv_valu(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa,
                             const int16_t* b, const dfp_scale* sb, float* out, dfp_scale* so,
                             int32_t* partials, hipStream_t st, bool i32 = false);
+
+// gemm.hip: D[m][n] = opA opB with the forward convolution's chunked contract.
+struct GemmPlan {
+  int32_t KB, G16, Mp;                          // 32-blocks and 16-groups of the padded reduction, padded rows
+  int64_t a_bytes, b_bytes, t_bytes, bytes;     // A digits, B digits, B offset table, total workspace
+};
+GemmPlan plan_gemm(int32_t m, int32_t n, int32_t k);
+dfp_status launch_gemm_mfma(int32_t m, int32_t n, int32_t k, int32_t trans_a, int32_t trans_b, int32_t L,
+                            const int16_t* a, const dfp_scale* sa, const int16_t* b, const dfp_scale* sb,
+                            float* d, dfp_scale* so, int32_t* partials, void* ws, hipStream_t st);
+// so (nullable) must be cleared by the caller.
+dfp_status launch_gemm_valu(int32_t m, int32_t n, int32_t k, int32_t trans_a, int32_t trans_b, int32_t L,
+                            const int16_t* a, const dfp_scale* sa, const int16_t* b, const dfp_scale* sb,
+                            float* d, dfp_scale* so, int32_t* partials, hipStream_t st);
 
 }  // namespace dfp

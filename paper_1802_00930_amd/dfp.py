@@ -38,6 +38,12 @@ class Desc(ctypes.Structure):
                  "chunk_len", "seg_chunks", "bits", "rounding", "path")] + [("seed", ctypes.c_uint64)]
 
 
+class GemmDesc(ctypes.Structure):
+    """Mirror of ``dfp_gemm_desc``."""
+    _fields_ = [(name, ctypes.c_int32) for name in
+                ("m", "n", "k", "trans_a", "trans_b", "chunk_len", "bits", "path")]
+
+
 _lib = None
 
 
@@ -50,6 +56,7 @@ def lib():
         L = ctypes.CDLL(LIB_PATH)
         P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
         DP = ctypes.POINTER(Desc)
+        GP = ctypes.POINTER(GemmDesc)
         sigs = {
             "dfp_quantize": ([DP, I32, P, P, P, P], I32),
             "dfp_conv_fwd": ([DP, P, P, P, P, P, P, P, SZ, P, P], I32),
@@ -60,6 +67,11 @@ def lib():
             "dfp_conv_bwd_data_i32": ([DP, P, P, P, P, P, P, P, SZ, P], I32),
             "dfp_downconvert_i32": ([DP, I32, P, P, P, P, I32, P], I32),
             "dfp_workspace_bytes": ([DP, I32], SZ),
+            "dfp_gemm": ([GP, P, P, P, P, P, P, P, SZ, P, P], I32),
+            "dfp_gemm_workspace_bytes": ([GP], SZ),
+            "dfp_gemm_num_chunks": ([GP], I64),
+            "dfp_quantize_tensor": ([I64, I32, I32, ctypes.c_uint64, I32, P, P, P, P], I32),
+            "dfp_downconvert_tensor": ([I64, I32, I32, ctypes.c_uint64, I32, P, P, P, I32, P], I32),
             "dfp_num_chunks": ([DP, I32], I64),
             "dfp_output_dims": ([DP, ctypes.POINTER(I32), ctypes.POINTER(I32)], I32),
             "dfp_status_str": ([I32], ctypes.c_char_p),
@@ -206,6 +218,50 @@ def dfp_downconvert_i32(d: Desc, role: int, src, sin, dst, sout, amax_ready: boo
         _need(t, dt, nm)
     _check("dfp_downconvert_i32", lib().dfp_downconvert_i32(ctypes.byref(d), role, _ptr(src), _ptr(sin), _ptr(dst),
                                                             _ptr(sout), int(bool(amax_ready)), _stream(stream)))
+
+
+def make_gemm_desc(m, n, k, trans_a=False, trans_b=False, chunk_len=64, bits=15, path=PATH_AUTO) -> GemmDesc:
+    return GemmDesc(m, n, k, int(bool(trans_a)), int(bool(trans_b)), chunk_len, bits, path)
+
+
+def gemm_workspace_bytes(d: GemmDesc) -> int:
+    return int(lib().dfp_gemm_workspace_bytes(ctypes.byref(d)))
+
+
+def gemm_num_chunks(d: GemmDesc) -> int:
+    return int(lib().dfp_gemm_num_chunks(ctypes.byref(d)))
+
+
+def alloc_gemm_workspace(d: GemmDesc, device="cuda"):
+    n = gemm_workspace_bytes(d)
+    if n == 0:
+        return None
+    return torch.empty((n + 255) // 256 * 256, dtype=torch.uint8, device=device)
+
+
+def dfp_gemm(d: GemmDesc, a, sa, b, sb, out, sd=None, workspace=None, partials=None, stream=None):
+    for t, dt, nm in ((a, torch.int16, "a"), (b, torch.int16, "b"), (out, torch.float32, "out"),
+                      (sa, torch.int32, "sa"), (sb, torch.int32, "sb"), (sd, torch.int32, "sd"),
+                      (partials, torch.int32, "partials")):
+        _need(t, dt, nm)
+    wp, wn = _ws(workspace)
+    _check("dfp_gemm", lib().dfp_gemm(ctypes.byref(d), _ptr(a), _ptr(sa), _ptr(b), _ptr(sb), _ptr(out), _ptr(sd),
+                                      wp, wn, _ptr(partials), _stream(stream)))
+
+
+def dfp_quantize_tensor(bits, rounding, seed, role, src, dst, scale, stream=None):
+    _need(src, torch.float32, "src"); _need(dst, torch.int16, "dst"); _need(scale, torch.int32, "scale")
+    rnd = ROUNDING[rounding] if isinstance(rounding, str) else int(rounding)
+    _check("dfp_quantize_tensor", lib().dfp_quantize_tensor(src.numel(), bits, rnd, seed, role, _ptr(src),
+                                                            _ptr(dst), _ptr(scale), _stream(stream)))
+
+
+def dfp_downconvert_tensor(bits, rounding, seed, role, src, dst, scale, amax_ready=False, stream=None):
+    _need(src, torch.float32, "src"); _need(dst, torch.int16, "dst"); _need(scale, torch.int32, "scale")
+    rnd = ROUNDING[rounding] if isinstance(rounding, str) else int(rounding)
+    _check("dfp_downconvert_tensor", lib().dfp_downconvert_tensor(src.numel(), bits, rnd, seed, role, _ptr(src),
+                                                                  _ptr(dst), _ptr(scale), int(bool(amax_ready)),
+                                                                  _stream(stream)))
 
 
 def alloc_workspace(d: Desc, direction: int, device="cuda"):

@@ -40,7 +40,8 @@ def test_every_declared_symbol_is_exported(dl):
 def test_binding_exposes_same_names(dl):
     import paper_1802_00930_amd.dfp as b
     for n in ("dfp_quantize", "dfp_conv_fwd", "dfp_conv_bwd_data", "dfp_conv_bwd_weights", "dfp_downconvert",
-              "dfp_conv_fwd_i32", "dfp_conv_bwd_data_i32", "dfp_downconvert_i32"):
+              "dfp_conv_fwd_i32", "dfp_conv_bwd_data_i32", "dfp_downconvert_i32", "dfp_gemm",
+              "dfp_quantize_tensor", "dfp_downconvert_tensor"):
         assert callable(getattr(b, n))
 
 
@@ -180,6 +181,58 @@ def test_downconvert_i32_rejects(dl):
     assert call(src=FAKE + 8) == dl.ERR_ALIGN
     assert call(dst=FAKE + 4096 + 4) == dl.ERR_ALIGN
     assert call(sin=FAKE + 4) == dl.ERR_ALIGN
+
+
+def test_gemm_desc_layout(dl):
+    assert ctypes.sizeof(dl.GemmDesc) == 32
+
+
+def _gemm(dl, d, a=FAKE, b=FAKE + 4096, out=FAKE + 8192, sd=None, ws=None, wsn=0, parts=None):
+    return dl.lib().dfp_gemm(ctypes.byref(d) if d is not None else None, _p(a), _p(FAKE), _p(b), _p(FAKE),
+                             _p(out), _p(sd) if sd else None, _p(ws) if ws else None, wsn,
+                             _p(parts) if parts else None, None)
+
+
+def test_gemm_rejects(dl):
+    ok = dict(m=64, n=1000, k=2048, trans_b=True, chunk_len=64, path=dl.PATH_VALU)
+    assert _gemm(dl, None) == dl.ERR_NULL
+    for field, value, code in (("m", 0, dl.ERR_SHAPE), ("k", -1, dl.ERR_SHAPE), ("trans_a", 2, dl.ERR_PARAM),
+                               ("chunk_len", 0, dl.ERR_PARAM), ("bits", 14, dl.ERR_PARAM),
+                               ("path", 3, dl.ERR_PARAM)):
+        d = dl.make_gemm_desc(**ok)
+        setattr(d, field, value)
+        assert _gemm(dl, d) == code, field
+    big = dl.make_gemm_desc(**dict(ok, m=2 ** 21, n=2 ** 20))
+    assert _gemm(dl, big) == dl.ERR_SHAPE  # m*n > 2^40
+    d = dl.make_gemm_desc(**ok)
+    assert _gemm(dl, d, a=0) == dl.ERR_NULL
+    assert _gemm(dl, d, out=0) == dl.ERR_NULL
+    assert _gemm(dl, d, a=FAKE + 1) == dl.ERR_ALIGN
+    assert _gemm(dl, d, out=FAKE + 8192 + 2) == dl.ERR_ALIGN
+    assert _gemm(dl, d, sd=FAKE + 8) == dl.ERR_ALIGN
+    assert dl.gemm_workspace_bytes(d) == 0  # VALU path needs none
+    mf = dl.make_gemm_desc(**dict(ok, path=dl.PATH_MFMA))
+    need = dl.gemm_workspace_bytes(mf)
+    # A digits 32*2 x 64 rows x 64 B, B digits 1000 columns x 128 groups x 32 B, 64 block offsets
+    assert need == 64 * 64 * 64 + 1000 * 128 * 32 + 512
+    assert _gemm(dl, mf, ws=FAKE, wsn=need - 1) == dl.ERR_WORKSPACE
+    assert _gemm(dl, mf, ws=FAKE + 128, wsn=need) == dl.ERR_WORKSPACE
+    assert dl.gemm_num_chunks(mf) == 32
+    assert dl.gemm_num_chunks(dl.make_gemm_desc(**dict(ok, chunk_len=0))) == -1
+    assert dl.gemm_workspace_bytes(dl.make_gemm_desc(**dict(ok, bits=16, path=dl.PATH_AUTO))) == 0
+
+
+def test_flat_quantize_rejects(dl):
+    q, dc = dl.lib().dfp_quantize_tensor, dl.lib().dfp_downconvert_tensor
+    good = (1000, 15, 0, 0, dl.ROLE_X)
+    assert q(*good, None, _p(FAKE), _p(FAKE), None) == dl.ERR_NULL
+    assert q(0, 15, 0, 0, 0, _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_PARAM
+    assert q(1000, 14, 0, 0, 0, _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_PARAM
+    assert q(1000, 15, 4, 0, 0, _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_PARAM
+    assert q(1000, 15, 0, 0, 5, _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_PARAM
+    assert q(*good, _p(FAKE + 4), _p(FAKE), _p(FAKE), None) == dl.ERR_ALIGN
+    assert dc(*good, _p(FAKE), _p(FAKE), _p(FAKE), 2, None) == dl.ERR_PARAM
+    assert dc(*good, _p(FAKE), _p(FAKE + 2), _p(FAKE), 1, None) == dl.ERR_ALIGN
 
 
 def test_host_queries(dl):
