@@ -83,6 +83,12 @@ def lib():
         L.orc_gemm.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_int, P, P,
                                ctypes.c_int32, ctypes.c_int32, P, P]
         L.orc_gemm.restype = ctypes.c_int64
+        L.orc_quantize_blocked.argtypes = [P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                           ctypes.c_int, ctypes.c_uint64, ctypes.c_uint32, P, P]
+        L.orc_quantize_blocked.restype = ctypes.c_uint32
+        L.orc_gemm_blocked.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P, P, P, P, ctypes.c_int64,
+                                       ctypes.c_int32, P, P]
+        L.orc_gemm_blocked.restype = ctypes.c_int64
         _lib = L
     return _lib
 
@@ -223,4 +229,40 @@ def gemm(a: np.ndarray, b: np.ndarray, e: int, L: int, trans_a: bool = False, tr
     parts = np.empty(((k + L - 1) // L, m * n), dtype=np.int32) if want_partials else None
     ov = lib().orc_gemm(m, n, k, int(trans_a), int(trans_b), _ptr(a), _ptr(b), e, L, _ptr(out),
                         _ptr(parts) if parts is not None else None)
+    return out, parts, int(ov)
+
+
+# --------------------------------------------------------------------------
+# Blocked-DFP (Sec. 3): one exponent per block of B consecutive elements of a
+# row; a GEMM over such operands scales each chunk by its block's exponents
+# before the FP32 fold (Alg. 2).
+# --------------------------------------------------------------------------
+def quantize_blocked(f: np.ndarray, B: int, bits: int = 15, rounding: int = ROUND_NEAREST, seed: int = 0,
+                     role: int = ROLE_X):
+    """f [rows, cols] FP32 -> (int16 [rows, cols], int8 exponents [nb, rows], flags)."""
+    f = np.ascontiguousarray(f, dtype=np.float32)
+    rows, cols = f.shape
+    nb = (cols + B - 1) // B
+    out = np.empty((rows, cols), dtype=np.int16)
+    exps = np.empty((nb, rows), dtype=np.int8)
+    flags = lib().orc_quantize_blocked(_ptr(f), rows, cols, B, bits, rounding, seed, role, _ptr(out), _ptr(exps))
+    return out, exps, int(flags)
+
+
+def gemm_blocked(a: np.ndarray, ea: np.ndarray, b: np.ndarray, eb: np.ndarray, Bk: int, L: int,
+                 want_partials: bool = False):
+    """a [m, k], b [n, k] INT16 (t contiguous), ea [nb, m], eb [nb, n] int8;
+    D [m, n] = fold over chunks of 2^(ea + eb) * fl32(P_c).  Bk % L == 0."""
+    assert Bk % L == 0
+    a = np.ascontiguousarray(a, dtype=np.int16)
+    b = np.ascontiguousarray(b, dtype=np.int16)
+    ea = np.ascontiguousarray(ea, dtype=np.int8)
+    eb = np.ascontiguousarray(eb, dtype=np.int8)
+    m, k = a.shape
+    n = b.shape[0]
+    assert b.shape[1] == k and ea.shape == ((k + Bk - 1) // Bk, m) and eb.shape == ((k + Bk - 1) // Bk, n)
+    out = np.empty((m, n), dtype=np.float32)
+    parts = np.empty(((k + L - 1) // L, m * n), dtype=np.int32) if want_partials else None
+    ov = lib().orc_gemm_blocked(m, n, k, _ptr(a), _ptr(ea), _ptr(b), _ptr(eb), Bk, L, _ptr(out),
+                                _ptr(parts) if parts is not None else None)
     return out, parts, int(ov)

@@ -450,3 +450,92 @@ int64_t orc_gemm(int64_t m, int64_t n, int64_t k, int trans_a, int trans_b, cons
   }
   return overflow;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Blocked-DFP (Sec. 3: several exponents per tensor, each shared by a small  */
+/* block of integers).  A [rows][cols] tensor is split along cols into blocks */
+/* of B consecutive elements (the last one per row possibly shorter); every   */
+/* block is quantised like a tensor of its own (Eq. 1-3, same clamp, zero and */
+/* non-finite rules), the stochastic word of an element still taken from its  */
+/* flat index in the whole tensor.  exps is [nb][rows] (block-major), nb =    */
+/* ceil(cols / B).  Returned flags: NONFINITE, EXP_CLAMPED, SATURATED if any  */
+/* block has them; ZERO_TENSOR only if every block is zero.                   */
+/* ------------------------------------------------------------------------ */
+uint32_t orc_quantize_blocked(const float *src, int64_t rows, int64_t cols, int64_t B, int bits, int rounding,
+                              uint64_t seed, uint32_t role, int16_t *dst, int8_t *exps) {
+  const int64_t nb = (cols + B - 1) / B;
+  const int64_t lim = (bits == 16) ? 32767 : ((int64_t)1 << (bits - 1));
+  uint32_t any = 0;
+  int all_zero = 1;
+#pragma omp parallel for schedule(static) reduction(| : any) reduction(& : all_zero)
+  for (int64_t rb = 0; rb < rows * nb; ++rb) {
+    const int64_t r = rb / nb, b = rb % nb;
+    const int64_t c0 = b * B, c1 = (c0 + B < cols) ? c0 + B : cols;
+    const int64_t base = r * cols;
+    double m = 0.0;
+    int nonfinite = 0;
+    for (int64_t c = c0; c < c1; ++c) {
+      double a = fabs((double)src[base + c]);
+      if (!isfinite(a)) nonfinite = 1;
+      else if (a > m) m = a;
+    }
+    int32_t es = 0;
+    uint32_t f = 0;
+    if (nonfinite) {
+      f = ORC_FLAG_NONFINITE;
+      all_zero = 0; /* a non-finite block is not a zero block */
+    } else {
+      f = shared_exponent(m, bits, &es);
+    }
+    if (nonfinite || (f & ORC_FLAG_ZERO_TENSOR)) {
+      for (int64_t c = c0; c < c1; ++c) dst[base + c] = 0;
+      es = 0;
+    } else {
+      all_zero = 0;
+      for (int64_t c = c0; c < c1; ++c) {
+        const int64_t idx = base + c;
+        double x = ldexp((double)src[idx], -es);
+        uint32_t u = (rounding == ORC_ROUND_STOCHASTIC) ? orc_rng_word(seed, role, (uint64_t)idx) : 0u;
+        int64_t v = round_scaled(x, rounding, u);
+        if (bits == 16) {
+          if (v > lim) { v = lim; f |= ORC_FLAG_SATURATED; }
+          if (v < -lim) { v = -lim; f |= ORC_FLAG_SATURATED; }
+        }
+        dst[idx] = (int16_t)v;
+      }
+    }
+    exps[b * rows + r] = (int8_t)es;
+    any |= f & (ORC_FLAG_NONFINITE | ORC_FLAG_EXP_CLAMPED | ORC_FLAG_SATURATED);
+  }
+  return any | (all_zero ? ORC_FLAG_ZERO_TENSOR : 0u);
+}
+
+/* Blocked-DFP GEMM: D[i][j] = sum over t of a[i][t] * b[j][t] (both stored
+ * with t contiguous), exponents ea [nb][m] and eb [nb][n] per block of Bk
+ * consecutive t.  Chunks of L (Bk a multiple of L) lie inside one block; each
+ * chunk's INT32 partial (mod 2^32) is converted to FP32, scaled by
+ * 2^(ea[blk][i] + eb[blk][j]) and added to the FP32 sum in chunk order (the
+ * per-chunk scaling of Alg. 2).  partials (nullable): [J][m*n]. */
+int64_t orc_gemm_blocked(int64_t m, int64_t n, int64_t k, const int16_t *a, const int8_t *ea, const int16_t *b,
+                         const int8_t *eb, int64_t Bk, int32_t L, float *out, int32_t *partials) {
+  const int64_t J = (k + L - 1) / L;
+  int64_t overflow = 0;
+#pragma omp parallel for schedule(dynamic, 16) reduction(+ : overflow)
+  for (int64_t o = 0; o < m * n; ++o) {
+    const int64_t i = o / n, j = o % n;
+    float total = 0.0f;
+    for (int64_t c = 0; c < J; ++c) {
+      const int64_t t0 = c * (int64_t)L, t1 = (t0 + L < k) ? t0 + L : k;
+      int64_t exact = 0;
+      for (int64_t t = t0; t < t1; ++t) exact += (int64_t)a[i * k + t] * (int64_t)b[j * k + t];
+      const int64_t pc = wrap32(exact);
+      if (pc != exact) ++overflow;
+      if (partials) partials[c * m * n + o] = (int32_t)pc;
+      const int64_t blk = t0 / Bk;
+      const float term = scale_out((float)pc, (int32_t)ea[blk * m + i] + (int32_t)eb[blk * n + j]);
+      total = (c == 0) ? term : total + term;
+    }
+    out[o] = total;
+  }
+  return overflow;
+}
