@@ -269,6 +269,36 @@ dfp_status dfp_downconvert_tensor(int64_t n, int32_t bits, int32_t rounding, uin
                                   const float* src, int16_t* dst, dfp_scale* s, int32_t amax_ready,
                                   void* stream);
 
+/* ----------------------------------------------------------- Blocked-DFP --
+ * Several exponents per tensor, each shared by a small block of integers
+ * (Sec. 3, "Blocked-DFP").  dfp_quantize_blocked splits each row of src
+ * [rows][cols] (FP32, row-major) into blocks of `block` consecutive elements
+ * (the last one of a row possibly shorter) and quantises every block like a
+ * tensor of its own (Eq. 1-3: its own max, exponent clamp at -128, zero and
+ * non-finite rules, P = 16 saturation); the stochastic word of an element is
+ * that of its flat index, as in dfp_quantize.  dst: INT16 [rows][cols].
+ * exps: int8 [nb][rows], nb = ceil(cols / block), block-major.  s: amax_bits
+ * = max |f| of the tensor, exp = 0, flags = NONFINITE / EXP_CLAMPED /
+ * SATURATED if any block has them, ZERO_TENSOR if every block is zero. */
+dfp_status dfp_quantize_blocked(int64_t rows, int64_t cols, int64_t block, int32_t bits, int32_t rounding,
+                                uint64_t seed, int32_t role, const float* src, int16_t* dst, int8_t* exps,
+                                dfp_scale* s, void* stream);
+
+/* Blocked-DFP GEMM: D[i][j] = fold over chunks c, in chunk order in FP32, of
+ * fl32(P_c[i][j]) * 2^(ea[blk][i] + eb[blk][j]), blk = cL / block_k (Alg. 2
+ * scaling each partial; chunks lie inside blocks).  Operands with the
+ * reduction contiguous, as dfp_quantize_blocked writes them: a [m][k], b
+ * [n][k] (the descriptor must say trans_a = 0, trans_b = 1), ea int8 [nb][m],
+ * eb int8 [nb][n], nb = ceil(k / block_k).  block_k must be a multiple of
+ * chunk_len.  out, sd, partials as for dfp_gemm (no final scale: every chunk
+ * carries its own).  workspace: dfp_gemm_blocked_workspace_bytes(d, block_k)
+ * bytes (0 when the call runs on the VALU path: P = 16, chunk_len not a
+ * multiple of 32, or more than 80 blocks). */
+dfp_status dfp_gemm_blocked(const dfp_gemm_desc* d, int32_t block_k, const int16_t* a, const int8_t* ea,
+                            const int16_t* b, const int8_t* eb, float* out, dfp_scale* sd, void* workspace,
+                            size_t ws_bytes, int32_t* partials, void* stream);
+size_t dfp_gemm_blocked_workspace_bytes(const dfp_gemm_desc* d, int32_t block_k);
+
 /* Output height and width of the forward convolution; DFP_ERR_SHAPE if < 1. */
 dfp_status dfp_output_dims(const dfp_desc* d, int32_t* p, int32_t* q);
 

@@ -147,6 +147,13 @@ bool gemm_use_mfma(const dfp_gemm_desc* d) {
   // grid rows of 64-row tiles must fit a launch dimension
   return d->path != DFP_PATH_VALU && d->bits == 15 && (d->m + 63) / 64 <= 65535;
 }
+// Blocked-DFP GEMM on matrix cores: P = 15, chunks of whole 32-blocks, the
+// workgroup's exponent tables small enough for LDS, 32-bit output indices.
+bool gemm_blocked_use_mfma(const dfp_gemm_desc* d, int32_t block_k) {
+  const int64_t nb = ((int64_t)d->k + block_k - 1) / block_k;
+  return gemm_use_mfma(d) && d->chunk_len % 32 == 0 && nb <= kBlockedMaxBlocks &&
+         (int64_t)d->m * d->n < ((int64_t)1 << 31) && plan_gemm(d->m, d->n, d->k).b_bytes < ((int64_t)1 << 31);
+}
 bool flat_params_ok(int64_t n, int32_t bits, int32_t rounding, int32_t role) {
   return n >= 1 && n <= ((int64_t)1 << 40) && (bits == 15 || bits == 16) && rounding >= 0 && rounding <= 3 &&
          role >= DFP_ROLE_X && role <= DFP_ROLE_DX;
@@ -318,6 +325,43 @@ dfp_status dfp_gemm(const dfp_gemm_desc* d, const int16_t* a, const dfp_scale* s
                           partials, st);
 }
 
+dfp_status dfp_quantize_blocked(int64_t rows, int64_t cols, int64_t block, int32_t bits, int32_t rounding,
+                                uint64_t seed, int32_t role, const float* src, int16_t* dst, int8_t* exps,
+                                dfp_scale* s, void* stream) {
+  if (!src || !dst || !exps || !s) return DFP_ERR_NULL;
+  if (rows < 1 || cols < 1 || rows * cols > ((int64_t)1 << 40)) return DFP_ERR_SHAPE;
+  if (block < 1 || !flat_params_ok(rows * cols, bits, rounding, role)) return DFP_ERR_PARAM;
+  if (!aligned(src, 4) || !aligned(dst, 2) || !aligned(s, 16)) return DFP_ERR_ALIGN;
+  return launch_quantize_blocked(src, dst, exps, rows, cols, block, s, bits, rounding, seed, (uint32_t)role,
+                                 (hipStream_t)stream);
+}
+
+size_t dfp_gemm_blocked_workspace_bytes(const dfp_gemm_desc* d, int32_t block_k) {
+  if (gemm_desc_check(d) != DFP_OK || !gemm_blocked_use_mfma(d, block_k)) return 0;
+  return (size_t)plan_gemm(d->m, d->n, d->k).bytes;
+}
+
+dfp_status dfp_gemm_blocked(const dfp_gemm_desc* d, int32_t block_k, const int16_t* a, const int8_t* ea,
+                            const int16_t* b, const int8_t* eb, float* out, dfp_scale* sd, void* workspace,
+                            size_t ws_bytes, int32_t* partials, void* stream) {
+  dfp_status rc = gemm_desc_check(d);
+  if (rc != DFP_OK) return rc;
+  if (!a || !ea || !b || !eb || !out) return DFP_ERR_NULL;
+  if (d->trans_a != 0 || d->trans_b != 1 || block_k < 1 || block_k % d->chunk_len != 0) return DFP_ERR_PARAM;
+  if (!aligned(a, 2) || !aligned(b, 2) || !aligned(out, 4) || (sd && !aligned(sd, 16)) ||
+      (partials && !aligned(partials, 4)))
+    return DFP_ERR_ALIGN;
+  hipStream_t st = (hipStream_t)stream;
+  if (gemm_blocked_use_mfma(d, block_k)) {
+    const size_t need = (size_t)plan_gemm(d->m, d->n, d->k).bytes;
+    if (!workspace || ws_bytes < need || !aligned(workspace, 256)) return DFP_ERR_WORKSPACE;
+    return launch_gemm_mfma(d->m, d->n, d->k, 0, 1, d->chunk_len, a, nullptr, b, nullptr, out, sd, partials,
+                            workspace, st, ea, eb, block_k);
+  }
+  if (sd && (rc = launch_scale_reset(sd, st)) != DFP_OK) return rc;
+  return launch_gemm_blocked_valu(d->m, d->n, d->k, d->chunk_len, block_k, a, ea, b, eb, out, sd, partials, st);
+}
+
 dfp_status dfp_quantize_tensor(int64_t n, int32_t bits, int32_t rounding, uint64_t seed, int32_t role,
                                const float* src, int16_t* dst, dfp_scale* s, void* stream) {
   if (!src || !dst || !s) return DFP_ERR_NULL;
@@ -397,7 +441,7 @@ const char* dfp_kernel_name(int32_t id) {
   static const char* names[K_NUM_KERNELS] = {
       "scale_reset", "amax", "quant_convert", "conv_fwd_valu", "conv_bwd_data_valu", "conv_bwd_wt_valu",
       "weight_prep", "conv_fwd_mfma", "conv_bwd_data_mfma", "conv_bwd_wt_mfma", "bwd_wt_segment_reduce",
-      "act_prep", "conv_fwd_i32", "conv_bwd_data_i32", "downconvert_i32", "gemm_prep", "gemm"};
+      "act_prep", "conv_fwd_i32", "conv_bwd_data_i32", "downconvert_i32", "gemm_prep", "gemm", "quant_blocked", "gemm_blocked"};
   if (id < 0 || id >= K_NUM_KERNELS) return "unknown";
   return names[id];
 }

@@ -25,7 +25,15 @@ struct ConvMfmaArgs {
   int64_t NP, O;
   int32_t M, Mp, Cin, S, T, KB, L, CG, Hp, Wp, Po, Qo;
   int32_t ustride_h, ustride_w, rsign, roff_h, roff_w;
+  // Blocked-DFP (nullable): int8 exponents [nb][M] of the A rows and [nb][NP]
+  // of the B columns, one per block of bk reduction indices (bk a multiple of L)
+  const int8_t* exa;
+  const int8_t* exb;
+  int32_t bk, nb;
 };
+
+// Largest exponent-block count the blocked matrix-core kernel stages in LDS.
+constexpr int32_t kBlockedMaxBlocks = 80;
 
 // Output rows per workgroup tile of the main kernels (A digits are padded to it).
 constexpr int32_t kMfmaRowTile = 64;

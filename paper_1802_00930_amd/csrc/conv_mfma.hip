@@ -245,6 +245,23 @@ __device__ __forceinline__ void flush_tile(const Acc3& acc, float (&sum)[16], in
   }
 }
 
+// Blocked-DFP chunk end: the partial is scaled by 2^(Ea(block) + Eb(block))
+// (per row and column) before it joins the running sum; no final scale.
+template <bool PARTIALS>
+__device__ __forceinline__ void flush_tile_blocked(const Acc3& acc, float (&sum)[16], const int32_t (&ev)[16],
+                                                   int64_t j, int32_t* partials, int64_t O, int64_t obase,
+                                                   int64_t PQ, int32_t mrow0, int32_t M, bool gvalid) {
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const uint32_t p = recombine((uint32_t)acc.hh[v], (uint32_t)acc.xx[v], (uint32_t)acc.ll[v]);
+    sum[v] += ldexpf((float)(int32_t)p, ev[v]);
+    if (PARTIALS) {
+      const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
+      if (gvalid && m < M) partials[j * O + obase + (int64_t)m * PQ] = (int32_t)p;
+    }
+  }
+}
+
 // Single-chunk DFP-32 output: the chunk's wrapped INT32 sum itself, kept as
 // raw bits in the FP32 sum registers until the epilogue stores it.
 __device__ __forceinline__ void keep_tile_i32(const Acc3& acc, float (&sum)[16]) {
@@ -735,9 +752,10 @@ __device__ __forceinline__ void xcd_tile(int32_t& tx, int32_t& ty) {
   tx = t / nby;
 }
 
-template <bool PARTIALS, bool I32 = false>
+template <bool PARTIALS, bool I32 = false, bool BLOCKED = false>
 __global__ __launch_bounds__(kThreadsQ, 4) void k_conv_mfma_q(ConvMfmaArgs a) {
   __shared__ __align__(16) uint8_t smem[kStages * kStageBytes];
+  extern __shared__ __align__(16) int8_t qexp[];  // BLOCKED: exponents [nb][64 rows], then [nb][128 columns]
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
@@ -809,6 +827,47 @@ __global__ __launch_bounds__(kThreadsQ, 4) void k_conv_mfma_q(ConvMfmaArgs a) {
   int32_t blk_in_chunk = 0;
   const int32_t chunk_blocks = a.L / 32;
 
+  // Blocked-DFP: this workgroup's exponents staged in LDS before any DMA; a
+  // lane keeps the exponent sums of its 16 outputs for the current block
+  int32_t ev[16];
+  uint32_t xa = 0, xb = 0;
+  int32_t xblk = 0, chunk_in_xblk = 0;
+  const int32_t chunks_per_xblk = BLOCKED ? a.bk / a.L : 1;
+  if (BLOCKED) {
+    const int32_t nb = a.nb;
+    for (int32_t i = threadIdx.x; i < nb * kMT; i += kThreadsQ) {
+      const int32_t b = i / kMT, row = m0 + i % kMT;
+      qexp[i] = row < a.M ? a.exa[(int64_t)b * a.M + row] : (int8_t)0;
+    }
+    for (int32_t i = threadIdx.x; i < nb * kNT; i += kThreadsQ) {
+      const int32_t b = i / kNT, cc = tx * kNT + i % kNT;
+      qexp[nb * kMT + i] = cc < NP ? a.exb[(int64_t)b * NP + cc] : (int8_t)0;
+    }
+    __syncthreads();
+    const uint32_t qb = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t*)qexp;
+    xa = qb + wm * 32 + 4 * half;
+    xb = qb + nb * kMT + wp * 32 + col;
+  }
+  auto load_ev = [&]() {
+    // rows mrow0 + 8*g + (0..3) are 4 consecutive bytes of the row table
+    uint32_t w0, w1, w2, w3;
+    int32_t eb;
+    const uint32_t ra = xa + (uint32_t)xblk * kMT, rb = xb + (uint32_t)xblk * kNT;
+    asm volatile(
+        "ds_read_b32 %0, %5\n\t"
+        "ds_read_b32 %1, %5 offset:8\n\t"
+        "ds_read_b32 %2, %5 offset:16\n\t"
+        "ds_read_b32 %3, %5 offset:24\n\t"
+        "ds_read_i8 %4, %6\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(w0), "=&v"(w1), "=&v"(w2), "=&v"(w3), "=&v"(eb)
+        : "v"(ra), "v"(rb)
+        : "memory");
+    const uint32_t w[4] = {w0, w1, w2, w3};
+#pragma unroll
+    for (int v = 0; v < 16; ++v) ev[v] = (int32_t)(int8_t)(w[v >> 2] >> (8 * (v & 3))) + eb;
+  };
+
   // One block: wait for its loads (the two newer blocks may stay in flight:
   // two loads each in waves 0-3, one in waves 4-7), barrier, refill the slot
   // freed by the previous block, read and consume.
@@ -830,8 +889,18 @@ __global__ __launch_bounds__(kThreadsQ, 4) void k_conv_mfma_q(ConvMfmaArgs a) {
     read_stage_q<STAGE * kStageBytes>(rb0, rb1, ra0, ra1, bhi, blo, ahi, alo);
     mfma_tile(acc, ahi, alo, bhi, blo, blk_in_chunk == 0);
     if (++blk_in_chunk == chunk_blocks || kb == KB - 1) {
-      if (I32) keep_tile_i32(acc, sum);
-      else flush_tile<PARTIALS>(acc, sum, j, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+      if (I32) {
+        keep_tile_i32(acc, sum);
+      } else if (BLOCKED) {
+        if (chunk_in_xblk == 0) load_ev();
+        flush_tile_blocked<PARTIALS>(acc, sum, ev, j, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+        if (++chunk_in_xblk == chunks_per_xblk) {
+          chunk_in_xblk = 0;
+          ++xblk;
+        }
+      } else {
+        flush_tile<PARTIALS>(acc, sum, j, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+      }
       ++j;
       blk_in_chunk = 0;
     }
@@ -849,8 +918,8 @@ __global__ __launch_bounds__(kThreadsQ, 4) void k_conv_mfma_q(ConvMfmaArgs a) {
   if (kb < KB) step(kb++, std::integral_constant<int, 1>{});
   if (kb < KB) step(kb++, std::integral_constant<int, 2>{});
 
-  // ---- epilogue: scale once, store, max |y|
-  const int32_t e = a.ea->exp + a.eb->exp;
+  // ---- epilogue: scale once (blocked: already scaled per chunk), store, max |y|
+  const int32_t e = BLOCKED ? 0 : a.ea->exp + a.eb->exp;
   uint32_t amax = 0;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -1466,6 +1535,15 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     return dim3((unsigned)gx, (unsigned)mtiles);
   };
   const bool small_index = args.O < (1ll << 31) && ws_b_bytes < (1ll << 31);
+  if (args.exa) {
+    // Blocked-DFP: the shared-ring kernel with per-chunk block scales
+    if (i32 || masked || !chan16 || !small_index || args.nb > kBlockedMaxBlocks || args.bk % args.L != 0)
+      return DFP_ERR_PARAM;
+    const size_t lds = (size_t)args.nb * (kMT + kNT);
+    if (partials) DFP_LAUNCH(kid, (k_conv_mfma_q<true, false, true>), grid, dim3(kThreadsQ), lds, st, args);
+    else DFP_LAUNCH(kid, (k_conv_mfma_q<false, false, true>), grid, dim3(kThreadsQ), lds, st, args);
+    return DFP_OK;
+  }
   const bool persist_ok = chan16 && (args.T % 64) == 0 && args.KB >= 4 && args.KB <= kARes3Max && small_index;
   if (i32) {
     // DFP-32 output: one chunk over the whole reduction (the caller checked L >= T)

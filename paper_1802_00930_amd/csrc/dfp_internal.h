@@ -27,7 +27,9 @@ enum KernelId : int32_t {
   K_DC_I32 = 14,
   K_GEMM_PREP = 15,
   K_GEMM = 16,
-  K_NUM_KERNELS = 17
+  K_QUANT_BLOCKED = 17,
+  K_GEMM_BLOCKED = 18,
+  K_NUM_KERNELS = 19
 };
 
 // Convolution geometry handed to kernels by value.
@@ -70,6 +72,12 @@ dfp_status launch_downconvert_i32(const int32_t* src, int64_t n, const dfp_scale
                                   bool amax_ready, int32_t bits, int32_t rounding, uint64_t seed, uint32_t role,
                                   hipStream_t st);
 
+// Blocked-DFP: blocks of B consecutive elements along each row of src
+// [rows][cols]; exps [nb][rows]; s receives the tensor max and flags.
+dfp_status launch_quantize_blocked(const float* src, int16_t* dst, int8_t* exps, int64_t rows, int64_t cols,
+                                   int64_t B, dfp_scale* s, int32_t bits, int32_t rounding, uint64_t seed,
+                                   uint32_t role, hipStream_t st);
+
 // conv_valu.hip: one lane per output, VALU integer multiply-add.
 // i32: single-chunk DFP-32 output (forward / backward-data), out holds INT32.
 dfp_status launch_conv_valu(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa,
@@ -82,9 +90,16 @@ struct GemmPlan {
   int64_t a_bytes, b_bytes, t_bytes, bytes;     // A digits, B digits, B offset table, total workspace
 };
 GemmPlan plan_gemm(int32_t m, int32_t n, int32_t k);
+// exa / exb (nullable): Blocked-DFP exponent tables [nb][m] and [nb][n] per
+// block of bk reduction indices (then sa / sb are unused).
 dfp_status launch_gemm_mfma(int32_t m, int32_t n, int32_t k, int32_t trans_a, int32_t trans_b, int32_t L,
                             const int16_t* a, const dfp_scale* sa, const int16_t* b, const dfp_scale* sb,
-                            float* d, dfp_scale* so, int32_t* partials, void* ws, hipStream_t st);
+                            float* d, dfp_scale* so, int32_t* partials, void* ws, hipStream_t st,
+                            const int8_t* exa = nullptr, const int8_t* exb = nullptr, int32_t bk = 0);
+// so (nullable) must be cleared by the caller.
+dfp_status launch_gemm_blocked_valu(int32_t m, int32_t n, int32_t k, int32_t L, int32_t bk, const int16_t* a,
+                                    const int8_t* ea, const int16_t* b, const int8_t* eb, float* d, dfp_scale* so,
+                                    int32_t* partials, hipStream_t st);
 // so (nullable) must be cleared by the caller.
 dfp_status launch_gemm_valu(int32_t m, int32_t n, int32_t k, int32_t trans_a, int32_t trans_b, int32_t L,
                             const int16_t* a, const dfp_scale* sa, const int16_t* b, const dfp_scale* sb,

@@ -124,6 +124,54 @@ __global__ __launch_bounds__(kBlock) void k_gemm_valu(const int16_t* __restrict_
   }
 }
 
+// VALU Blocked-DFP GEMM (t contiguous in both operands): every chunk partial is
+// scaled by 2^(ea[blk][i] + eb[blk][j]) before it joins the FP32 sum.
+template <bool PARTIALS>
+__global__ __launch_bounds__(kBlock) void k_gemm_blocked_valu(const int16_t* __restrict__ a,
+                                                              const int8_t* __restrict__ ea,
+                                                              const int16_t* __restrict__ b,
+                                                              const int8_t* __restrict__ eb, int32_t m, int32_t n,
+                                                              int32_t K, int32_t L, int32_t bk,
+                                                              float* __restrict__ d, dfp_scale* so,
+                                                              int32_t* __restrict__ partials) {
+  const int64_t O = (int64_t)m * n;
+  const int64_t o = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  const bool active = o < O;
+  float y = 0.f;
+  if (active) {
+    const int64_t i = o / n, j = o % n;
+    const int16_t* pa = a + i * K;
+    const int16_t* pb = b + j * K;
+    float sum = 0.f;
+    int64_t chunk = 0;
+    for (int32_t t0 = 0; t0 < K; t0 += L, ++chunk) {
+      const int32_t t1 = min(K, t0 + L);
+      uint32_t acc = 0u;
+      for (int32_t t = t0; t < t1; ++t) acc += (uint32_t)((int32_t)pa[t] * (int32_t)pb[t]);
+      if (PARTIALS) partials[chunk * O + o] = (int32_t)acc;
+      const int32_t blk = t0 / bk;
+      const float term = ldexpf((float)(int32_t)acc, (int32_t)ea[(int64_t)blk * m + i] + (int32_t)eb[(int64_t)blk * n + j]);
+      sum = chunk == 0 ? term : sum + term;
+    }
+    y = sum;
+    d[o] = y;
+  }
+  if (so) {
+    __shared__ uint32_t red[kBlock / 64];
+    uint32_t mx = active ? (__float_as_uint(y) & 0x7fffffffu) : 0u;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off, 64));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t bm = red[0];
+      for (int w = 1; w < kBlock / 64; ++w) bm = max(bm, red[w]);
+      if (bm > __atomic_load_n(&so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&so->amax_bits, bm);
+      if (bm == 0x7f800000u) atomicOr(&so->flags, DFP_FLAG_OUTPUT_INF);
+    }
+  }
+}
+
 inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
 
 }  // namespace
@@ -142,7 +190,8 @@ GemmPlan plan_gemm(int32_t m, int32_t n, int32_t k) {
 
 dfp_status launch_gemm_mfma(int32_t m, int32_t n, int32_t k, int32_t trans_a, int32_t trans_b, int32_t L,
                             const int16_t* a, const dfp_scale* sa, const int16_t* b, const dfp_scale* sb,
-                            float* d, dfp_scale* so, int32_t* partials, void* ws, hipStream_t st) {
+                            float* d, dfp_scale* so, int32_t* partials, void* ws, hipStream_t st,
+                            const int8_t* exa, const int8_t* exb, int32_t bk) {
   const GemmPlan p = plan_gemm(m, n, k);
   uint8_t* wsa = reinterpret_cast<uint8_t*>(ws);
   uint8_t* xs = wsa + p.a_bytes;
@@ -185,7 +234,25 @@ dfp_status launch_gemm_mfma(int32_t m, int32_t n, int32_t k, int32_t trans_a, in
   args.NP = n;
   args.O = (int64_t)m * n;
   args.ustride_h = 1; args.ustride_w = 1; args.rsign = 1; args.roff_h = 0; args.roff_w = 0;
-  return launch_mfma_main(args, p.b_bytes, K_GEMM, K_GEMM, false, st);
+  args.exa = exa;
+  args.exb = exb;
+  args.bk = bk;
+  args.nb = exa ? (k + bk - 1) / bk : 0;
+  return launch_mfma_main(args, p.b_bytes, exa ? K_GEMM_BLOCKED : K_GEMM, K_GEMM, false, st);
+}
+
+dfp_status launch_gemm_blocked_valu(int32_t m, int32_t n, int32_t k, int32_t L, int32_t bk, const int16_t* a,
+                                    const int8_t* ea, const int16_t* b, const int8_t* eb, float* d, dfp_scale* so,
+                                    int32_t* partials, hipStream_t st) {
+  const int64_t O = (int64_t)m * n;
+  const dim3 grid((unsigned)((O + kBlock - 1) / kBlock));
+  if (partials)
+    DFP_LAUNCH(K_GEMM_BLOCKED, k_gemm_blocked_valu<true>, grid, dim3(kBlock), 0, st, a, ea, b, eb, m, n, k, L, bk, d,
+               so, partials);
+  else
+    DFP_LAUNCH(K_GEMM_BLOCKED, k_gemm_blocked_valu<false>, grid, dim3(kBlock), 0, st, a, ea, b, eb, m, n, k, L, bk,
+               d, so, partials);
+  return DFP_OK;
 }
 
 dfp_status launch_gemm_valu(int32_t m, int32_t n, int32_t k, int32_t trans_a, int32_t trans_b, int32_t L,

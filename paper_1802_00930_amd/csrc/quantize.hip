@@ -368,6 +368,135 @@ __global__ __launch_bounds__(kBlock) void k_i32_convert(const int32_t* __restric
   if (SAT && saturated) atomicOr(&sout->flags, DFP_FLAG_SATURATED);
 }
 
+// ---------------------------------------------------------------- Blocked-DFP
+// Each block of B consecutive elements of a [rows][cols] row gets its own
+// shared exponent (Eq. 1-2 on the block's max) and is rounded like a tensor of
+// its own (Eq. 3), the stochastic word still that of the element's flat index.
+// One wave per (row, block): a max pass, then the rounding pass.  VEC4: rows
+// and blocks start at multiples of 4 elements, so a lane takes aligned groups
+// of 4 (one Philox block, one 16-byte load).  s->flags starts at ZERO_TENSOR
+// (k_blocked_init); a wave with a non-zero or non-finite block clears it.
+__global__ void k_blocked_init(dfp_scale* s) {
+  if (threadIdx.x == 0) {
+    s->amax_bits = 0u;
+    s->exp = 0;
+    s->flags = DFP_FLAG_ZERO_TENSOR;
+  }
+}
+
+template <int MODE, bool SAT, bool VEC4>
+__global__ __launch_bounds__(kBlock) void k_quant_blocked(const float* __restrict__ src, int16_t* __restrict__ dst,
+                                                          int8_t* __restrict__ exps, int64_t rows, int64_t cols,
+                                                          int64_t B, int64_t nb, dfp_scale* s, int32_t bits,
+                                                          uint32_t key0, uint32_t key1, uint32_t role,
+                                                          int32_t seg_log2) {
+  // a wave serves 64 >> seg_log2 blocks at a time, 2^seg_log2 lanes each, in a
+  // grid-stride loop; the workgroup reports its max and flags once at the end
+  const int lane = threadIdx.x & 63;
+  const int S = 1 << seg_log2;
+  const int sl = lane & (S - 1);
+  const int64_t nblk = rows * nb;
+  const int64_t stride = ((int64_t)gridDim.x * (kBlock / 64)) << (6 - seg_log2);
+  uint32_t wmax = 0u;
+  bool f_nonfinite = false, f_clamped = false, f_sat = false, f_nonzero = false;
+  for (int64_t wave_first = ((int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) << (6 - seg_log2);
+       wave_first < nblk; wave_first += stride) {  // uniform per wave
+    const int64_t blk = wave_first + (lane >> seg_log2);
+    const bool valid = blk < nblk;
+    const int64_t r = valid ? blk / nb : 0, b = valid ? blk % nb : 0;
+    const int64_t c0 = b * B, c1 = valid ? min(c0 + B, cols) : c0;
+    const int64_t base = r * cols;
+    const uint32_t* s32 = reinterpret_cast<const uint32_t*>(src) + base;
+    uint32_t mb = 0u;
+    if (VEC4) {
+      for (int64_t c = c0 + 4 * sl; c < c1; c += 4 * S) {
+        const uint4 v = *reinterpret_cast<const uint4*>(s32 + c);
+        mb = max(mb, max(max(v.x & 0x7fffffffu, v.y & 0x7fffffffu), max(v.z & 0x7fffffffu, v.w & 0x7fffffffu)));
+      }
+    } else {
+      for (int64_t c = c0 + sl; c < c1; c += S) mb = max(mb, s32[c] & 0x7fffffffu);
+    }
+    for (int off = S >> 1; off > 0; off >>= 1) mb = max(mb, (uint32_t)__shfl_xor((int)mb, off, 64));
+    const bool nonfinite = mb >= 0x7f800000u;
+    const bool zero = mb == 0u;
+    int32_t es = 0;
+    bool clamped = false;
+    if (!nonfinite && !zero) {
+      es = floor_log2_bits(mb) - (bits - 2);
+      if (es < -128) {
+        es = -128;
+        clamped = true;
+      }
+    }
+    const bool all_zero = nonfinite || zero;
+    bool saturated = false;
+    auto convert = [&](uint32_t fb, uint32_t u) {
+      int32_t v = all_zero ? 0 : round_one<MODE>(fb, es, u);
+      if (SAT) {
+        const int32_t c = min(max(v, -32767), 32767);
+        saturated |= c != v;
+        v = c;
+      }
+      return v;
+    };
+    if (VEC4) {
+      for (int64_t c = c0 + 4 * sl; c < c1; c += 4 * S) {
+        const uint4 v = *reinterpret_cast<const uint4*>(s32 + c);
+        const uint64_t g = (uint64_t)(base + c) >> 2;
+        uint4 rw = make_uint4(0u, 0u, 0u, 0u);
+        if (MODE == DFP_ROUND_STOCHASTIC)
+          rw = philox4x32_10(make_uint4((uint32_t)g, (uint32_t)(g >> 32), role, 0u), key0, key1);
+        const int32_t i0 = convert(v.x, rw.x), i1 = convert(v.y, rw.y), i2 = convert(v.z, rw.z),
+                      i3 = convert(v.w, rw.w);
+        uint2 packed;
+        packed.x = ((uint32_t)i0 & 0xffffu) | ((uint32_t)i1 << 16);
+        packed.y = ((uint32_t)i2 & 0xffffu) | ((uint32_t)i3 << 16);
+        *reinterpret_cast<uint2*>(dst + base + c) = packed;
+      }
+    } else {
+      for (int64_t c = c0 + sl; c < c1; c += S) {
+        const uint64_t idx = (uint64_t)(base + c);
+        uint32_t u = 0u;
+        if (MODE == DFP_ROUND_STOCHASTIC) {
+          const uint4 rw = philox4x32_10(make_uint4((uint32_t)(idx >> 2), (uint32_t)(idx >> 34), role, 0u), key0,
+                                         key1);
+          const uint32_t w = idx & 3u;
+          u = w == 0 ? rw.x : (w == 1 ? rw.y : (w == 2 ? rw.z : rw.w));
+        }
+        dst[base + c] = (int16_t)convert(s32[c], u);
+      }
+    }
+    if (valid && sl == 0) exps[b * rows + r] = (int8_t)es;
+    wmax = max(wmax, mb);
+    f_nonfinite |= valid && nonfinite;
+    f_clamped |= valid && clamped;
+    f_sat |= saturated;
+    f_nonzero |= valid && !zero;
+  }
+  // workgroup totals, then one guarded set of atomics
+  __shared__ uint32_t red_max[kBlock / 64], red_flags[kBlock / 64];
+  for (int off = 32; off > 0; off >>= 1) wmax = max(wmax, (uint32_t)__shfl_xor((int)wmax, off, 64));
+  const uint32_t wf = (__any(f_nonfinite) ? DFP_FLAG_NONFINITE : 0u) | (__any(f_clamped) ? DFP_FLAG_EXP_CLAMPED : 0u) |
+                      (__any(f_sat) ? DFP_FLAG_SATURATED : 0u) | (__any(f_nonzero) ? 0x80000000u : 0u);
+  if (lane == 0) {
+    red_max[threadIdx.x >> 6] = wmax;
+    red_flags[threadIdx.x >> 6] = wf;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t m = red_max[0], f = red_flags[0];
+    for (int i = 1; i < kBlock / 64; ++i) {
+      m = max(m, red_max[i]);
+      f |= red_flags[i];
+    }
+    if (m > __atomic_load_n(&s->amax_bits, __ATOMIC_RELAXED)) atomicMax(&s->amax_bits, m);
+    const uint32_t fl = f & 0x7fffffffu;
+    if (fl && (__atomic_load_n(&s->flags, __ATOMIC_RELAXED) & fl) != fl) atomicOr(&s->flags, fl);
+    if ((f & 0x80000000u) && (__atomic_load_n(&s->flags, __ATOMIC_RELAXED) & DFP_FLAG_ZERO_TENSOR))
+      atomicAnd(&s->flags, ~DFP_FLAG_ZERO_TENSOR);
+  }
+}
+
 int grid_for(int64_t work_items) {
   int64_t blocks = (work_items + kBlock - 1) / kBlock;
   if (blocks < 1) blocks = 1;
@@ -376,6 +505,55 @@ int grid_for(int64_t work_items) {
 }
 
 }  // namespace
+
+template <int MODE, bool SAT>
+static dfp_status launch_blocked_mode(const float* src, int16_t* dst, int8_t* exps, int64_t rows, int64_t cols,
+                                      int64_t B, dfp_scale* s, int32_t bits, uint32_t k0, uint32_t k1,
+                                      uint32_t role, bool vec4, hipStream_t st) {
+  const int64_t nb = (cols + B - 1) / B;
+  // lanes per block: enough for one pass over the block, a power of two up to 64
+  const int64_t lanes = vec4 ? (B + 3) / 4 : B;
+  int32_t seg_log2 = 0;
+  while (seg_log2 < 6 && ((int64_t)1 << seg_log2) < lanes) ++seg_log2;
+  const int64_t waves = (rows * nb + (64 >> seg_log2) - 1) >> (6 - seg_log2);
+  // at most 1024 workgroups (4 per CU): each reports once, so the scale sees few atomics
+  const dim3 grid((unsigned)std::min<int64_t>(1024, (waves + kBlock / 64 - 1) / (kBlock / 64)));
+  if (vec4)
+    DFP_LAUNCH(K_QUANT_BLOCKED, (k_quant_blocked<MODE, SAT, true>), grid, dim3(kBlock), 0, st, src, dst, exps, rows,
+               cols, B, nb, s, bits, k0, k1, role, seg_log2);
+  else
+    DFP_LAUNCH(K_QUANT_BLOCKED, (k_quant_blocked<MODE, SAT, false>), grid, dim3(kBlock), 0, st, src, dst, exps,
+               rows, cols, B, nb, s, bits, k0, k1, role, seg_log2);
+  return DFP_OK;
+}
+
+template <int MODE>
+static dfp_status launch_blocked_sat(const float* src, int16_t* dst, int8_t* exps, int64_t rows, int64_t cols,
+                                     int64_t B, dfp_scale* s, int32_t bits, uint32_t k0, uint32_t k1, uint32_t role,
+                                     bool vec4, hipStream_t st) {
+  if (bits == 16) return launch_blocked_mode<MODE, true>(src, dst, exps, rows, cols, B, s, bits, k0, k1, role, vec4, st);
+  return launch_blocked_mode<MODE, false>(src, dst, exps, rows, cols, B, s, bits, k0, k1, role, vec4, st);
+}
+
+dfp_status launch_quantize_blocked(const float* src, int16_t* dst, int8_t* exps, int64_t rows, int64_t cols,
+                                   int64_t B, dfp_scale* s, int32_t bits, int32_t rounding, uint64_t seed,
+                                   uint32_t role, hipStream_t st) {
+  DFP_LAUNCH(K_SCALE_RESET, k_blocked_init, dim3(1), dim3(64), 0, st, s);
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  // aligned 4-groups never straddle a block or a row
+  const bool vec4 = (cols % 4) == 0 && (B % 4) == 0 && (reinterpret_cast<uintptr_t>(src) & 15) == 0 &&
+                    (reinterpret_cast<uintptr_t>(dst) & 7) == 0;
+  switch (rounding) {
+    case DFP_ROUND_NEAREST:
+      return launch_blocked_sat<DFP_ROUND_NEAREST>(src, dst, exps, rows, cols, B, s, bits, k0, k1, role, vec4, st);
+    case DFP_ROUND_STOCHASTIC:
+      return launch_blocked_sat<DFP_ROUND_STOCHASTIC>(src, dst, exps, rows, cols, B, s, bits, k0, k1, role, vec4, st);
+    case DFP_ROUND_BIASED:
+      return launch_blocked_sat<DFP_ROUND_BIASED>(src, dst, exps, rows, cols, B, s, bits, k0, k1, role, vec4, st);
+    default:
+      return launch_blocked_sat<DFP_ROUND_DOWN>(src, dst, exps, rows, cols, B, s, bits, k0, k1, role, vec4, st);
+  }
+}
 
 dfp_status launch_scale_reset(dfp_scale* s, hipStream_t st) {
   DFP_LAUNCH(K_SCALE_RESET, k_scale_reset, dim3(1), dim3(64), 0, st, s);

@@ -71,6 +71,9 @@ def lib():
             "dfp_gemm_workspace_bytes": ([GP], SZ),
             "dfp_gemm_num_chunks": ([GP], I64),
             "dfp_quantize_tensor": ([I64, I32, I32, ctypes.c_uint64, I32, P, P, P, P], I32),
+            "dfp_quantize_blocked": ([I64, I64, I64, I32, I32, ctypes.c_uint64, I32, P, P, P, P, P], I32),
+            "dfp_gemm_blocked": ([GP, I32, P, P, P, P, P, P, P, SZ, P, P], I32),
+            "dfp_gemm_blocked_workspace_bytes": ([GP, I32], SZ),
             "dfp_downconvert_tensor": ([I64, I32, I32, ctypes.c_uint64, I32, P, P, P, I32, P], I32),
             "dfp_num_chunks": ([DP, I32], I64),
             "dfp_output_dims": ([DP, ctypes.POINTER(I32), ctypes.POINTER(I32)], I32),
@@ -262,6 +265,36 @@ def dfp_downconvert_tensor(bits, rounding, seed, role, src, dst, scale, amax_rea
     _check("dfp_downconvert_tensor", lib().dfp_downconvert_tensor(src.numel(), bits, rnd, seed, role, _ptr(src),
                                                                   _ptr(dst), _ptr(scale), int(bool(amax_ready)),
                                                                   _stream(stream)))
+
+
+def dfp_quantize_blocked(block, bits, rounding, seed, role, src, dst, exps, scale, stream=None):
+    """src: FP32 [rows, cols]; dst INT16 like src; exps int8 [ceil(cols/block), rows]."""
+    _need(src, torch.float32, "src"); _need(dst, torch.int16, "dst"); _need(exps, torch.int8, "exps")
+    _need(scale, torch.int32, "scale")
+    rows, cols = src.shape
+    rnd = ROUNDING[rounding] if isinstance(rounding, str) else int(rounding)
+    _check("dfp_quantize_blocked", lib().dfp_quantize_blocked(rows, cols, block, bits, rnd, seed, role, _ptr(src),
+                                                              _ptr(dst), _ptr(exps), _ptr(scale), _stream(stream)))
+
+
+def gemm_blocked_workspace_bytes(d: GemmDesc, block_k: int) -> int:
+    return int(lib().dfp_gemm_blocked_workspace_bytes(ctypes.byref(d), block_k))
+
+
+def alloc_gemm_blocked_workspace(d: GemmDesc, block_k: int, device="cuda"):
+    n = gemm_blocked_workspace_bytes(d, block_k)
+    if n == 0:
+        return None
+    return torch.empty((n + 255) // 256 * 256, dtype=torch.uint8, device=device)
+
+
+def dfp_gemm_blocked(d: GemmDesc, block_k, a, ea, b, eb, out, sd=None, workspace=None, partials=None, stream=None):
+    for t, dt, nm in ((a, torch.int16, "a"), (b, torch.int16, "b"), (ea, torch.int8, "ea"), (eb, torch.int8, "eb"),
+                      (out, torch.float32, "out"), (sd, torch.int32, "sd"), (partials, torch.int32, "partials")):
+        _need(t, dt, nm)
+    wp, wn = _ws(workspace)
+    _check("dfp_gemm_blocked", lib().dfp_gemm_blocked(ctypes.byref(d), block_k, _ptr(a), _ptr(ea), _ptr(b), _ptr(eb),
+                                                      _ptr(out), _ptr(sd), wp, wn, _ptr(partials), _stream(stream)))
 
 
 def alloc_workspace(d: Desc, direction: int, device="cuda"):

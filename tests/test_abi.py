@@ -235,6 +235,34 @@ def test_flat_quantize_rejects(dl):
     assert dc(*good, _p(FAKE), _p(FAKE + 2), _p(FAKE), 1, None) == dl.ERR_ALIGN
 
 
+def test_blocked_rejects(dl):
+    lib = dl.lib()
+    d = dl.make_gemm_desc(64, 1000, 2048, False, True, chunk_len=64)
+
+    def g(desc, bk=128, a=FAKE, ea=FAKE + 4096, ws=None, wsn=0):
+        return lib.dfp_gemm_blocked(ctypes.byref(desc), bk, _p(a), _p(ea), _p(FAKE + 8192), _p(FAKE + 12288),
+                                    _p(FAKE + 16384), None, _p(ws) if ws else None, wsn, None, None)
+    assert g(d, bk=96) == dl.ERR_PARAM      # block not a multiple of the chunk
+    assert g(d, bk=0) == dl.ERR_PARAM
+    assert g(dl.make_gemm_desc(64, 1000, 2048, True, True, chunk_len=64)) == dl.ERR_PARAM
+    assert g(dl.make_gemm_desc(64, 1000, 2048, False, False, chunk_len=64)) == dl.ERR_PARAM
+    assert g(d, ea=0) == dl.ERR_NULL
+    assert g(d, a=FAKE + 1) == dl.ERR_ALIGN
+    need = dl.gemm_blocked_workspace_bytes(d, 128)
+    assert need == dl.gemm_workspace_bytes(d) > 0
+    assert g(d, ws=FAKE, wsn=need - 1) == dl.ERR_WORKSPACE
+    # more than 80 exponent blocks, P = 16 or a chunk not a multiple of 32: VALU path, no workspace
+    assert dl.gemm_blocked_workspace_bytes(d, 16 * 1) == 0
+    assert dl.gemm_blocked_workspace_bytes(dl.make_gemm_desc(64, 1000, 2048, False, True, 64, bits=16), 128) == 0
+    assert dl.gemm_blocked_workspace_bytes(dl.make_gemm_desc(64, 1000, 2048, False, True, 16), 128) == 0
+    q = lib.dfp_quantize_blocked
+    assert q(0, 10, 4, 15, 0, 0, 0, _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_SHAPE
+    assert q(3, 10, 0, 15, 0, 0, 0, _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_PARAM
+    assert q(3, 10, 4, 17, 0, 0, 0, _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_PARAM
+    assert q(3, 10, 4, 15, 0, 0, 0, _p(FAKE), _p(FAKE), None, _p(FAKE), None) == dl.ERR_NULL
+    assert q(3, 10, 4, 15, 0, 0, 0, _p(FAKE + 2), _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_ALIGN
+
+
 def test_host_queries(dl):
     d = good_desc(dl, chunk_len=16)
     assert dl.output_dims(d) == (14, 14)
