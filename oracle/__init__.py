@@ -89,6 +89,15 @@ def lib():
         L.orc_gemm_blocked.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P, P, P, P, ctypes.c_int64,
                                        ctypes.c_int32, P, P]
         L.orc_gemm_blocked.restype = ctypes.c_int64
+        I64, I32, F = ctypes.c_int64, ctypes.c_int32, ctypes.c_float
+        L.orc_bn_relu_fwd.argtypes = [P, I32, I64, I64, I64, P, P, P, F, ctypes.c_int, ctypes.c_int, ctypes.c_uint64,
+                                      P, P, P, P, P, P]
+        L.orc_bn_relu_fwd.restype = ctypes.c_uint32
+        L.orc_bn_relu_bwd.argtypes = [P, I32, P, I32, I64, I64, I64, P, P, P, P, P, ctypes.c_int, ctypes.c_int,
+                                      ctypes.c_uint64, P, P, P, P, P, P, P]
+        L.orc_bn_relu_bwd.restype = ctypes.c_uint32
+        L.orc_sgd_quantize.argtypes = [I64, P, P, P, F, F, F, ctypes.c_int, ctypes.c_int, ctypes.c_uint64, P, P]
+        L.orc_sgd_quantize.restype = ctypes.c_uint32
         _lib = L
     return _lib
 
@@ -266,3 +275,68 @@ def gemm_blocked(a: np.ndarray, ea: np.ndarray, b: np.ndarray, eb: np.ndarray, B
     ov = lib().orc_gemm_blocked(m, n, k, _ptr(a), _ptr(ea), _ptr(b), _ptr(eb), Bk, L, _ptr(out),
                                 _ptr(parts) if parts is not None else None)
     return out, parts, int(ov)
+
+
+# --------------------------------------------------------------------------
+# The steps either side of the convolutions in one training step (Sec. 4.1,
+# Fig. 2): batch normalisation on up-converted DFP16 tensors with ReLU and an
+# optional residual add, the quantisers Q_a / Q_e of its outputs, and FP32 SGD
+# on master weights followed by Q_w.  Channel sums are exact integers.
+# --------------------------------------------------------------------------
+def _f32(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.float32)
+
+
+def bn_relu_fwd(y: np.ndarray, ey: int, gamma, beta, res=None, eps: float = 1e-5, bits: int = 15,
+                rounding: int = ROUND_NEAREST, seed: int = 0):
+    """y int16 [N, C, H, W] with exponent ey.  Returns dict: z (FP32), zq, ez,
+    flags, mean, inv_std (FP32 [C]), sums (int64 [C, 2]: S1, S2)."""
+    y = np.ascontiguousarray(y, dtype=np.int16)
+    N, C = y.shape[:2]
+    HW = y[0, 0].size
+    g, b, r = _f32(gamma), _f32(beta), _f32(res)
+    z = np.empty(y.shape, np.float32)
+    zq = np.empty(y.shape, np.int16)
+    ez = np.zeros(1, np.int32)
+    mean = np.empty(C, np.float32)
+    inv = np.empty(C, np.float32)
+    sums = np.empty((C, 2), np.int64)
+    fl = lib().orc_bn_relu_fwd(_ptr(y), ey, N, C, HW, _ptr(g), _ptr(b), _ptr(r) if r is not None else None, eps,
+                               bits, rounding, seed, _ptr(z), _ptr(zq), _ptr(ez), _ptr(mean), _ptr(inv), _ptr(sums))
+    return dict(z=z, zq=zq, ez=int(ez[0]), flags=int(fl), mean=mean, inv_std=inv, sums=sums)
+
+
+def bn_relu_bwd(dz: np.ndarray, edz: int, y: np.ndarray, ey: int, gamma, beta, mean, inv_std, res=None,
+                bits: int = 15, rounding: int = ROUND_NEAREST, seed: int = 0):
+    """Returns dict: dy (FP32), dyq, edy, flags, dgamma, dbeta, dres (FP32 or
+    None), sums (int64 [C, 2]: D, P)."""
+    dz = np.ascontiguousarray(dz, dtype=np.int16)
+    y = np.ascontiguousarray(y, dtype=np.int16)
+    N, C = y.shape[:2]
+    HW = y[0, 0].size
+    g, b, r, m, s = _f32(gamma), _f32(beta), _f32(res), _f32(mean), _f32(inv_std)
+    dy = np.empty(y.shape, np.float32)
+    dyq = np.empty(y.shape, np.int16)
+    edy = np.zeros(1, np.int32)
+    dg = np.empty(C, np.float32)
+    db = np.empty(C, np.float32)
+    dres = np.empty(y.shape, np.float32) if r is not None else None
+    sums = np.empty((C, 2), np.int64)
+    fl = lib().orc_bn_relu_bwd(_ptr(dz), edz, _ptr(y), ey, N, C, HW, _ptr(g), _ptr(b),
+                               _ptr(r) if r is not None else None, _ptr(m), _ptr(s), bits, rounding, seed, _ptr(dy),
+                               _ptr(dyq), _ptr(edy), _ptr(dg), _ptr(db), _ptr(dres) if dres is not None else None,
+                               _ptr(sums))
+    return dict(dy=dy, dyq=dyq, edy=int(edy[0]), flags=int(fl), dgamma=dg, dbeta=db, dres=dres, sums=sums)
+
+
+def sgd_quantize(w, v, dw, lr: float, mu: float, wd: float, bits: int = 15, rounding: int = ROUND_NEAREST,
+                 seed: int = 0):
+    """One FP32 SGD step (returns new copies of w and v) and Q_w of the new w."""
+    w = np.array(w, dtype=np.float32, copy=True).reshape(-1)
+    v = np.array(v, dtype=np.float32, copy=True).reshape(-1)
+    dw = _f32(dw).reshape(-1)
+    wq = np.empty(w.size, np.int16)
+    ew = np.zeros(1, np.int32)
+    fl = lib().orc_sgd_quantize(w.size, _ptr(w), _ptr(v), _ptr(dw), lr, mu, wd, bits, rounding, seed, _ptr(wq),
+                                _ptr(ew))
+    return dict(w=w, v=v, wq=wq, ew=int(ew[0]), flags=int(fl))

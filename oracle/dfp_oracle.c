@@ -65,6 +65,10 @@
 #define ORC_FLAG_EXP_CLAMPED 2u
 #define ORC_FLAG_SATURATED 4u
 #define ORC_FLAG_ZERO_TENSOR 8u
+/* Stochastic-stream roles of the quantisers (the same numbering as the library's) */
+#define ORC_ROLE_X 0u
+#define ORC_ROLE_W 1u
+#define ORC_ROLE_DY 2u
 #define ORC_FLAG_OUTPUT_INF 16u
 
 /* Convolution geometry, mirrored by a ctypes Structure on the Python side. */
@@ -538,4 +542,143 @@ int64_t orc_gemm_blocked(int64_t m, int64_t n, int64_t k, const int16_t *a, cons
     out[o] = total;
   }
   return overflow;
+}
+
+/* ------------------------------------------------------------------------ */
+/* One layer's steps either side of the convolutions (Sec. 4.1, Fig. 2).     */
+/* Batch normalisation reads DFP16 tensors and up-converts them; with the    */
+/* integers I and exponent E of a channel's n = N*H*W elements the sums     */
+/* S1 = sum I, S2 = sum I^2 (and in the backward pass D = sum g, P = sum g*I */
+/* over the ReLU-masked gradient integers g) are exact in 64-bit integers,  */
+/* so the statistics need no FP32 accumulation at all.  Per-channel values  */
+/* are computed in float64 and rounded once to FP32; per-element work is    */
+/* FP32 with the stated operation order (fmaf = fused multiply-add).         */
+/* ------------------------------------------------------------------------ */
+
+/* Per-channel statistics of a DFP16 tensor [N][C][HW]. */
+static void bn_channel_stats(const int16_t *y, int64_t N, int64_t C, int64_t HW, int64_t c, int64_t *s1,
+                             int64_t *s2) {
+  int64_t a = 0, b = 0;
+  for (int64_t n = 0; n < N; ++n)
+    for (int64_t i = 0; i < HW; ++i) {
+      int64_t v = y[(n * C + c) * HW + i];
+      a += v;
+      b += v * v;
+    }
+  *s1 = a;
+  *s2 = b;
+}
+
+/* mean = S1 2^E / n, var = S2 2^2E / n - mean^2 (biased, clamped at 0), both
+ * in float64; mean_f = fl32(mean), inv_std = 1 / sqrt(fl32(var) + eps) in FP32. */
+static void bn_mean_inv_std(int64_t s1, int64_t s2, int32_t e, int64_t cnt, float eps, float *mean_f,
+                            float *inv_std_f) {
+  double mean = ldexp((double)s1, e) / (double)cnt;
+  double var = ldexp((double)s2, 2 * e) / (double)cnt - mean * mean;
+  if (var < 0.0) var = 0.0;
+  *mean_f = (float)mean;
+  float vf = (float)var;
+  *inv_std_f = 1.0f / sqrtf(vf + eps);
+}
+
+/* BN + (residual add) + ReLU forward of one element. */
+static float bn_relu_elem(int16_t yi, int32_t e, float mean_f, float inv_std_f, float g, float b, const float *res,
+                          int64_t idx, float *pre) {
+  float yv = ldexpf((float)yi, e);          /* exact: |yi| < 2^15 */
+  float xh = (yv - mean_f) * inv_std_f;
+  float zp = fmaf(xh, g, b);
+  if (res) zp = zp + res[idx];
+  if (pre) *pre = zp;
+  return zp > 0.0f ? zp : 0.0f;
+}
+
+/* Forward: z = ReLU(gamma * xhat + beta [+ res]) in FP32, then Q_a of z (the
+ * next layer's activation, role X).  Outputs: z (nullable), zq, its exponent
+ * and flags, per-channel mean_f, inv_std_f and the sums [C][2] = S1, S2. */
+uint32_t orc_bn_relu_fwd(const int16_t *y, int32_t ey, int64_t N, int64_t C, int64_t HW, const float *gamma,
+                         const float *beta, const float *res, float eps, int bits, int rounding, uint64_t seed,
+                         float *z, int16_t *zq, int32_t *ez, float *mean_f, float *inv_std_f, int64_t *sums) {
+  const int64_t cnt = N * HW, total = N * C * HW;
+  float *zz = z ? z : (float *)malloc((size_t)total * sizeof(float));
+  for (int64_t c = 0; c < C; ++c) {
+    int64_t s1, s2;
+    bn_channel_stats(y, N, C, HW, c, &s1, &s2);
+    sums[2 * c] = s1;
+    sums[2 * c + 1] = s2;
+    bn_mean_inv_std(s1, s2, ey, cnt, eps, &mean_f[c], &inv_std_f[c]);
+  }
+#pragma omp parallel for schedule(static)
+  for (int64_t idx = 0; idx < total; ++idx) {
+    int64_t c = (idx / HW) % C;
+    zz[idx] = bn_relu_elem(y[idx], ey, mean_f[c], inv_std_f[c], gamma[c], beta[c], res, idx, NULL);
+  }
+  uint32_t flags = orc_quantize(zz, total, bits, rounding, seed, ORC_ROLE_X, zq, ez);
+  if (!z) free(zz);
+  return flags;
+}
+
+/* Backward: dz' = mask * dz (mask: pre-activation > 0, recomputed), dbeta =
+ * sum dz', dgamma = sum dz' * xhat taken exactly as inv_std * 2^Edz *
+ * (P 2^Ey - mean_f D); a = gamma * inv_std, k1 = fl32(a), k2 = fl32(-a dgamma
+ * / n), k3 = fl32(-a dbeta / n) (float64, dgamma and dbeta as FP32);
+ * dy = fmaf(k1, dz', fmaf(k2, xhat, k3)) in FP32, then Q_e of dy (role DY).
+ * dres (nullable) = dz'.  sums [C][2] = D, P. */
+uint32_t orc_bn_relu_bwd(const int16_t *dz, int32_t edz, const int16_t *y, int32_t ey, int64_t N, int64_t C,
+                         int64_t HW, const float *gamma, const float *beta, const float *res, const float *mean_f,
+                         const float *inv_std_f, int bits, int rounding, uint64_t seed, float *dy, int16_t *dyq,
+                         int32_t *edy, float *dgamma, float *dbeta, float *dres, int64_t *sums) {
+  const int64_t cnt = N * HW, total = N * C * HW;
+  float *dd = dy ? dy : (float *)malloc((size_t)total * sizeof(float));
+  float *k = (float *)malloc((size_t)C * 3 * sizeof(float));
+#pragma omp parallel for schedule(static)
+  for (int64_t c = 0; c < C; ++c) {
+    int64_t D = 0, P = 0;
+    for (int64_t n = 0; n < N; ++n)
+      for (int64_t i = 0; i < HW; ++i) {
+        int64_t idx = (n * C + c) * HW + i;
+        float pre;
+        bn_relu_elem(y[idx], ey, mean_f[c], inv_std_f[c], gamma[c], beta[c], res, idx, &pre);
+        int64_t g = pre > 0.0f ? dz[idx] : 0;
+        D += g;
+        P += g * (int64_t)y[idx];
+      }
+    sums[2 * c] = D;
+    sums[2 * c + 1] = P;
+    double db = ldexp((double)D, edz);
+    double dg = (double)inv_std_f[c] * ldexp(ldexp((double)P, ey) - (double)mean_f[c] * (double)D, edz);
+    dbeta[c] = (float)db;
+    dgamma[c] = (float)dg;
+    double a = (double)gamma[c] * (double)inv_std_f[c];
+    k[3 * c] = (float)a;
+    k[3 * c + 1] = (float)(-a * (double)dgamma[c] / (double)cnt);
+    k[3 * c + 2] = (float)(-a * (double)dbeta[c] / (double)cnt);
+  }
+#pragma omp parallel for schedule(static)
+  for (int64_t idx = 0; idx < total; ++idx) {
+    int64_t c = (idx / HW) % C;
+    float pre;
+    float yv = ldexpf((float)y[idx], ey);
+    float xh = (yv - mean_f[c]) * inv_std_f[c];
+    bn_relu_elem(y[idx], ey, mean_f[c], inv_std_f[c], gamma[c], beta[c], res, idx, &pre);
+    float dzv = pre > 0.0f ? ldexpf((float)dz[idx], edz) : 0.0f;
+    dd[idx] = fmaf(k[3 * c], dzv, fmaf(k[3 * c + 1], xh, k[3 * c + 2]));
+    if (dres) dres[idx] = dzv;
+  }
+  uint32_t flags = orc_quantize(dd, total, bits, rounding, seed, ORC_ROLE_DY, dyq, edy);
+  free(k);
+  if (!dy) free(dd);
+  return flags;
+}
+
+/* FP32 SGD with momentum and weight decay on master weights (Fig. 2: the
+ * weight gradient is not quantised): g = fmaf(wd, w, dw), v = fmaf(mu, v, g),
+ * w = fmaf(-lr, v, w); then Q_w of the new weights (role W). */
+uint32_t orc_sgd_quantize(int64_t n, float *w, float *v, const float *dw, float lr, float mu, float wd, int bits,
+                          int rounding, uint64_t seed, int16_t *wq, int32_t *ew) {
+  for (int64_t i = 0; i < n; ++i) {
+    float g = fmaf(wd, w[i], dw[i]);
+    v[i] = fmaf(mu, v[i], g);
+    w[i] = fmaf(-lr, v[i], w[i]);
+  }
+  return orc_quantize(w, n, bits, rounding, seed, ORC_ROLE_W, wq, ew);
 }
