@@ -299,6 +299,81 @@ dfp_status dfp_gemm_blocked(const dfp_gemm_desc* d, int32_t block_k, const int16
                             size_t ws_bytes, int32_t* partials, void* stream);
 size_t dfp_gemm_blocked_workspace_bytes(const dfp_gemm_desc* d, int32_t block_k);
 
+/* ------------------------------------------------ around the convolutions --
+ * The FP32 steps either side of a layer's convolutions in a DFP16 training
+ * step (Sec. 4.1, Fig. 2): batch normalisation reads DFP16 tensors and
+ * up-converts them, works in FP32 and feeds Q_a (forward) or Q_e (backward)
+ * with its outputs; the weight update is FP32 SGD on master weights followed
+ * by Q_w.  Operation orders (every step a single IEEE rounding, no
+ * contraction):
+ *   statistics   S1 = sum i, S2 = sum i^2 over a channel's N*HW integers,
+ *                exact in 64-bit integers; mean = fl64(S1 2^E / cnt),
+ *                var = max(0, fl64(S2 2^2E / cnt) - mean*mean) in float64;
+ *                mean_f = fl32(mean), inv_std = 1 / sqrt(fl32(var) + eps) in
+ *                FP32;
+ *   forward      v = i 2^E, xhat = (v - mean_f) * inv_std,
+ *                pre = fma(xhat, gamma, beta) [+ res], z = pre > 0 ? pre : 0,
+ *                then Q_a of z (role X: the next layer's input);
+ *   backward     g = dz' = (pre > 0 ? dz 2^Edz : 0) with pre recomputed;
+ *                D = sum of the masked dz integers, Pd = sum of masked dz * y
+ *                integers (exact); dbeta = fl32(D 2^Edz), dgamma =
+ *                fl32(inv_std (Pd 2^Ey - mean_f D) 2^Edz); a = gamma inv_std,
+ *                k1 = fl32(a), k2 = fl32(-a dgamma / cnt), k3 = fl32(-a dbeta
+ *                / cnt) in float64; dy = fma(k1, g, fma(k2, xhat, k3)), then
+ *                Q_e of dy (role DY); dres = g.
+ * Tensors are [n][c][hw] (NCHW with hw = H*W), at most 2^31 - 1 elements;
+ * per-channel arrays are FP32 [c]; every pointer is device memory. */
+typedef struct dfp_bn_desc {
+  int32_t n, c, hw; /* >= 1, n*c*hw < 2^31                                     */
+  int32_t bits;     /* P of the quantised output, 15 or 16                      */
+  int32_t rounding; /* dfp_rounding of Q_a / Q_e                                */
+  float eps;        /* finite, >= 0                                             */
+  uint64_t seed;    /* Philox key of stochastic rounding                        */
+} dfp_bn_desc;
+
+/* Batch normalisation + optional residual add + ReLU forward on a DFP16
+ * tensor y (INT16 [n][c][hw], exponent sy->exp), then Q_a of the result.
+ * gamma, beta: FP32 [c].  res (nullable): FP32 [n][c][hw] added before the
+ * ReLU.  z (nullable): receives the FP32 result.  zq: INT16 result of Q_a,
+ * its scale in sz (exp, amax_bits, flags as dfp_quantize).  mean, inv_std:
+ * FP32 [c] (the backward call's inputs).  sums (nullable): int64 [c][2] =
+ * S1, S2.  workspace: dfp_bn_workspace_bytes(d) bytes, 256-byte aligned.
+ * Without res the output max comes from each channel's smallest and largest
+ * integer (z is monotone in i per channel), so the tensor is read twice;
+ * with res a max pass over z runs before the rounding pass and uses zq as
+ * scratch.  zq, z must not alias y or res.  Pointers to FP32 and INT16
+ * tensors 16-byte aligned, scales 16-byte aligned. */
+dfp_status dfp_bn_relu_fwd(const dfp_bn_desc* d, const int16_t* y, const dfp_scale* sy, const float* gamma,
+                           const float* beta, const float* res, float* z, int16_t* zq, dfp_scale* sz,
+                           float* mean, float* inv_std, int64_t* sums, void* workspace, size_t ws_bytes,
+                           void* stream);
+
+/* Backward of dfp_bn_relu_fwd: dz (INT16 [n][c][hw], exponent sdz->exp) is
+ * the gradient at z; y, sy, gamma, beta, res, mean, inv_std as given to and
+ * returned by the forward call.  dyq: INT16 Q_e of the gradient at y, scale
+ * in sdy (a max pass first, with dyq as scratch).  dy (nullable): the FP32
+ * gradient at y.  dgamma, dbeta: FP32 [c].  dres (nullable): the FP32
+ * gradient at res (the masked dz').  sums (nullable): int64 [c][2] = D, Pd.
+ * workspace as for the forward call. */
+dfp_status dfp_bn_relu_bwd(const dfp_bn_desc* d, const int16_t* dz, const dfp_scale* sdz, const int16_t* y,
+                           const dfp_scale* sy, const float* gamma, const float* beta, const float* res,
+                           const float* mean, const float* inv_std, float* dy, int16_t* dyq, dfp_scale* sdy,
+                           float* dgamma, float* dbeta, float* dres, int64_t* sums, void* workspace,
+                           size_t ws_bytes, void* stream);
+
+/* Workspace bytes of dfp_bn_relu_fwd / _bwd; 0 for an invalid descriptor. */
+size_t dfp_bn_workspace_bytes(const dfp_bn_desc* d);
+
+/* One FP32 SGD step with momentum mu and weight decay wd on n master weights,
+ * in place (Fig. 2: the weight gradient is not quantised):
+ *   g = fma(wd, w, dw);  v = fma(mu, v, g);  w = fma(-lr, v, w);
+ * then Q_w of the new w (dfp_quantize numerics, role W): wq INT16 [n] with
+ * scale sw.  w, v, dw: FP32 [n], 16-byte aligned; wq: 8-byte aligned, also
+ * the max pass's scratch. */
+dfp_status dfp_sgd_quantize(int64_t n, float lr, float mu, float wd, int32_t bits, int32_t rounding,
+                            uint64_t seed, float* w, float* v, const float* dw, int16_t* wq, dfp_scale* sw,
+                            void* stream);
+
 /* Output height and width of the forward convolution; DFP_ERR_SHAPE if < 1. */
 dfp_status dfp_output_dims(const dfp_desc* d, int32_t* p, int32_t* q);
 

@@ -158,6 +158,16 @@ bool flat_params_ok(int64_t n, int32_t bits, int32_t rounding, int32_t role) {
   return n >= 1 && n <= ((int64_t)1 << 40) && (bits == 15 || bits == 16) && rounding >= 0 && rounding <= 3 &&
          role >= DFP_ROLE_X && role <= DFP_ROLE_DX;
 }
+
+// Batch-norm descriptor checks: sizes, parameters, then the workspace.
+dfp_status bn_desc_check(const dfp_bn_desc* d) {
+  if (d->n < 1 || d->c < 1 || d->hw < 1) return DFP_ERR_SHAPE;
+  if ((int64_t)d->n * d->c * d->hw >= ((int64_t)1 << 31)) return DFP_ERR_SHAPE;
+  if (d->bits != 15 && d->bits != 16) return DFP_ERR_PARAM;
+  if (d->rounding < 0 || d->rounding > 3) return DFP_ERR_PARAM;
+  if (!(d->eps >= 0.0f) || d->eps == __builtin_inff()) return DFP_ERR_PARAM;
+  return DFP_OK;
+}
 }  // namespace
 }  // namespace dfp
 
@@ -385,6 +395,52 @@ dfp_status dfp_downconvert_tensor(int64_t n, int32_t bits, int32_t rounding, uin
   return launch_quant_convert(src, dst, n, s, bits, rounding, seed, (uint32_t)role, st);
 }
 
+size_t dfp_bn_workspace_bytes(const dfp_bn_desc* d) {
+  if (!d || bn_desc_check(d) != DFP_OK) return 0;
+  return bn_workspace_bytes(*d);
+}
+
+dfp_status dfp_bn_relu_fwd(const dfp_bn_desc* d, const int16_t* y, const dfp_scale* sy, const float* gamma,
+                           const float* beta, const float* res, float* z, int16_t* zq, dfp_scale* sz, float* mean,
+                           float* inv_std, int64_t* sums, void* workspace, size_t ws_bytes, void* stream) {
+  if (!d || !y || !sy || !gamma || !beta || !zq || !sz || !mean || !inv_std) return DFP_ERR_NULL;
+  dfp_status rc;
+  if ((rc = bn_desc_check(d)) != DFP_OK) return rc;
+  if (!aligned(y, 16) || !aligned(zq, 16) || (res && !aligned(res, 16)) || (z && !aligned(z, 16)) ||
+      !aligned(sy, 16) || !aligned(sz, 16) || (sums && !aligned(sums, 8)))
+    return DFP_ERR_ALIGN;
+  if (!workspace || ws_bytes < bn_workspace_bytes(*d) || !aligned(workspace, 256)) return DFP_ERR_WORKSPACE;
+  return launch_bn_relu_fwd(*d, y, sy, gamma, beta, res, z, zq, sz, mean, inv_std, sums, workspace,
+                            (hipStream_t)stream);
+}
+
+dfp_status dfp_bn_relu_bwd(const dfp_bn_desc* d, const int16_t* dz, const dfp_scale* sdz, const int16_t* y,
+                           const dfp_scale* sy, const float* gamma, const float* beta, const float* res,
+                           const float* mean, const float* inv_std, float* dy, int16_t* dyq, dfp_scale* sdy,
+                           float* dgamma, float* dbeta, float* dres, int64_t* sums, void* workspace, size_t ws_bytes,
+                           void* stream) {
+  if (!d || !dz || !sdz || !y || !sy || !gamma || !beta || !mean || !inv_std || !dyq || !sdy || !dgamma || !dbeta)
+    return DFP_ERR_NULL;
+  dfp_status rc;
+  if ((rc = bn_desc_check(d)) != DFP_OK) return rc;
+  if (!aligned(dz, 16) || !aligned(y, 16) || !aligned(dyq, 16) || (res && !aligned(res, 16)) ||
+      (dy && !aligned(dy, 16)) || (dres && !aligned(dres, 16)) || !aligned(sdz, 16) || !aligned(sy, 16) ||
+      !aligned(sdy, 16) || (sums && !aligned(sums, 8)))
+    return DFP_ERR_ALIGN;
+  if (!workspace || ws_bytes < bn_workspace_bytes(*d) || !aligned(workspace, 256)) return DFP_ERR_WORKSPACE;
+  return launch_bn_relu_bwd(*d, dz, sdz, y, sy, gamma, beta, res, mean, inv_std, dy, dyq, sdy, dgamma, dbeta, dres,
+                            sums, workspace, (hipStream_t)stream);
+}
+
+dfp_status dfp_sgd_quantize(int64_t n, float lr, float mu, float wd, int32_t bits, int32_t rounding, uint64_t seed,
+                            float* w, float* v, const float* dw, int16_t* wq, dfp_scale* sw, void* stream) {
+  if (!w || !v || !dw || !wq || !sw) return DFP_ERR_NULL;
+  if (!flat_params_ok(n, bits, rounding, DFP_ROLE_W)) return DFP_ERR_PARAM;
+  if (!aligned(w, 16) || !aligned(v, 16) || !aligned(dw, 16) || !aligned(wq, 8) || !aligned(sw, 16))
+    return DFP_ERR_ALIGN;
+  return launch_sgd_quantize(n, lr, mu, wd, bits, rounding, seed, w, v, dw, wq, sw, (hipStream_t)stream);
+}
+
 dfp_status dfp_conv_fwd(const dfp_desc* d, const int16_t* x, const dfp_scale* sx, const int16_t* w,
                         const dfp_scale* sw, float* y, dfp_scale* sy, void* workspace, size_t ws_bytes,
                         int32_t* partials, void* stream) {
@@ -441,7 +497,8 @@ const char* dfp_kernel_name(int32_t id) {
   static const char* names[K_NUM_KERNELS] = {
       "scale_reset", "amax", "quant_convert", "conv_fwd_valu", "conv_bwd_data_valu", "conv_bwd_wt_valu",
       "weight_prep", "conv_fwd_mfma", "conv_bwd_data_mfma", "conv_bwd_wt_mfma", "bwd_wt_segment_reduce",
-      "act_prep", "conv_fwd_i32", "conv_bwd_data_i32", "downconvert_i32", "gemm_prep", "gemm", "quant_blocked", "gemm_blocked"};
+      "act_prep", "conv_fwd_i32", "conv_bwd_data_i32", "downconvert_i32", "gemm_prep", "gemm", "quant_blocked", "gemm_blocked",
+      "bn_stats", "bn_finalize", "bn_amax", "bn_convert", "sgd"};
   if (id < 0 || id >= K_NUM_KERNELS) return "unknown";
   return names[id];
 }

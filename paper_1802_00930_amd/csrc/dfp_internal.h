@@ -29,7 +29,12 @@ enum KernelId : int32_t {
   K_GEMM = 16,
   K_QUANT_BLOCKED = 17,
   K_GEMM_BLOCKED = 18,
-  K_NUM_KERNELS = 19
+  K_BN_STATS = 19,
+  K_BN_FINAL = 20,
+  K_BN_AMAX = 21,
+  K_BN_CONVERT = 22,
+  K_SGD = 23,
+  K_NUM_KERNELS = 24
 };
 
 // Convolution geometry handed to kernels by value.
@@ -62,6 +67,9 @@ dfp_status launch_scale_reset(dfp_scale* s, hipStream_t st);
 // Writes amax_bits and clears flags; scratch (the destination INT16 buffer of
 // n elements) holds partial maxima until the rounding pass overwrites it.
 dfp_status launch_amax(const float* src, int64_t n, int16_t* scratch, dfp_scale* s, hipStream_t st);
+// Reduces part[0 .. nparts) (per-workgroup maxima of |.| bits) into
+// s->amax_bits and clears s->flags.
+dfp_status launch_amax_final(const uint32_t* part, int32_t nparts, dfp_scale* s, hipStream_t st);
 dfp_status launch_quant_convert(const float* src, int16_t* dst, int64_t n, dfp_scale* s, int32_t bits,
                                 int32_t rounding, uint64_t seed, uint32_t role, hipStream_t st);
 
@@ -104,5 +112,18 @@ dfp_status launch_gemm_blocked_valu(int32_t m, int32_t n, int32_t k, int32_t L, 
 dfp_status launch_gemm_valu(int32_t m, int32_t n, int32_t k, int32_t trans_a, int32_t trans_b, int32_t L,
                             const int16_t* a, const dfp_scale* sa, const int16_t* b, const dfp_scale* sb,
                             float* d, dfp_scale* so, int32_t* partials, hipStream_t st);
+
+// train.hip: the steps either side of the convolutions in a training step.
+dfp_status launch_bn_relu_fwd(const dfp_bn_desc& d, const int16_t* y, const dfp_scale* sy, const float* gamma,
+                              const float* beta, const float* res, float* z, int16_t* zq, dfp_scale* sz, float* mean,
+                              float* inv_std, int64_t* sums, void* ws, hipStream_t st);
+dfp_status launch_bn_relu_bwd(const dfp_bn_desc& d, const int16_t* dz, const dfp_scale* sdz, const int16_t* y,
+                              const dfp_scale* sy, const float* gamma, const float* beta, const float* res,
+                              const float* mean, const float* inv_std, float* dy, int16_t* dyq, dfp_scale* sdy,
+                              float* dgamma, float* dbeta, float* dres, int64_t* sums, void* ws, hipStream_t st);
+size_t bn_workspace_bytes(const dfp_bn_desc& d);
+dfp_status launch_sgd_quantize(int64_t n, float lr, float mu, float wd, int32_t bits, int32_t rounding,
+                               uint64_t seed, float* w, float* v, const float* dw, int16_t* wq, dfp_scale* sw,
+                               hipStream_t st);
 
 }  // namespace dfp

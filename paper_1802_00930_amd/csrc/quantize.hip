@@ -14,6 +14,7 @@
 #include <algorithm>
 
 #include "dfp_internal.h"
+#include "dfp_round.h"
 
 namespace dfp {
 
@@ -105,94 +106,18 @@ __global__ __launch_bounds__(kBlock) void k_amax_final(const uint32_t* __restric
   }
 }
 
-// Philox4x32-10 (Salmon et al., SC'11).
-__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
-#pragma unroll
-  for (int round = 0; round < 10; ++round) {
-    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
-    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
-    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
-    k0 += 0x9E3779B9u;
-    k1 += 0xBB67AE85u;
-  }
-  return c;
-}
-
-// Exponent of the max magnitude from its bit pattern (floor(log2 m), m > 0 finite).
-__device__ __forceinline__ int32_t floor_log2_bits(uint32_t mb) {
-  const uint32_t eb = mb >> 23;
-  if (eb != 0) return (int32_t)eb - 127;
-  return (31 - __clz((int)(mb & 0x7fffffu))) - 149;
-}
-
-// x = f * 2^-es split as X = floor(x * 2^32) = fl * 2^32 + F, in integer
-// arithmetic on the sign / exponent / significand fields.  f = M * 2^(e1 - 150)
-// with M the 24-bit significand, so |x| * 2^32 = M * 2^(32 - sh) with
-// sh = es + 150 - e1.  Every element of the tensor has |x| < 2^(bits-1) <= 2^15,
-// which bounds sh below by 9; shifts past 63 leave nothing but the inexact bit.
-struct Split {
-  int32_t fl;   // floor(x)
-  uint32_t F;   // floor(frac(x) * 2^32)
-};
-__device__ __forceinline__ Split split_scaled(uint32_t fb, int32_t es150) {
-  const uint32_t ax = fb & 0x7fffffffu;
-  const uint32_t eb = ax >> 23;
-  const uint32_t M = (ax & 0x7fffffu) | ((eb != 0u ? 1u : 0u) << 23);
-  const uint32_t sh = min((uint32_t)(es150 - (int32_t)max(eb, 1u)), 63u);
-  const uint64_t A = ((uint64_t)M << 32) >> sh;  // floor(|x| * 2^32)
-  const bool inexact = sh > 32u && (M << (64u - sh)) != 0u;
-  // negative x: floor(-|x| 2^32) = -(A + inexact) = ~A + (1 - inexact)
-  const uint64_t sm = (uint64_t)(int64_t)((int32_t)fb >> 31);
-  const uint64_t X = (A ^ sm) + ((sm != 0u && !inexact) ? 1u : 0u);
-  return {(int32_t)(X >> 32), (uint32_t)X};
-}
-
-// Round f * 2^-es to an integer (Sec. 1 rounding modes).
-//   NEAREST   ties to even: x is exact in FP32 whenever it is a normal number,
-//             and every smaller |x| rounds to 0 however ldexp rounds it.
-//   BIASED    floor(x + 1/2) as floor(x) + (frac(x) >= 1/2); frac is exact for
-//             normal x and the decision is unchanged for smaller |x|.
-//   STOCHASTIC floor(x) + (u < F), u the element's Philox word.
-//   DOWN      floor(x).
-template <int MODE>
-__device__ __forceinline__ int32_t round_one(uint32_t fb, int32_t es, uint32_t u) {
-  if (MODE == DFP_ROUND_NEAREST) {
-    return (int32_t)rintf(ldexpf(__uint_as_float(fb), -es));
-  } else if (MODE == DFP_ROUND_BIASED) {
-    const float x = ldexpf(__uint_as_float(fb), -es);
-    const float fl = floorf(x);
-    return (int32_t)fl + ((x - fl) >= 0.5f ? 1 : 0);
-  } else {
-    const Split sp = split_scaled(fb, es + 150);
-    if (MODE == DFP_ROUND_STOCHASTIC) return sp.fl + (u < sp.F ? 1 : 0);
-    return sp.fl;
-  }
-}
-
 template <int MODE, bool SAT>
 __global__ __launch_bounds__(kBlock) void k_quant_convert(const float* __restrict__ src,
                                                           int16_t* __restrict__ dst, int64_t n,
                                                           dfp_scale* __restrict__ s, int32_t bits,
                                                           uint32_t key0, uint32_t key1, uint32_t role) {
-  const uint32_t mb = s->amax_bits;
-  const bool nonfinite = mb >= 0x7f800000u;
-  const bool zero = mb == 0u;
-  int32_t es = 0;
-  bool clamped = false;
-  if (!nonfinite && !zero) {
-    es = floor_log2_bits(mb) - (bits - 2);
-    if (es < -128) {
-      es = -128;
-      clamped = true;
-    }
-  }
+  const ScaleFromMax sc = scale_from_max(s->amax_bits, bits);
+  const int32_t es = sc.es;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     s->exp = es;
-    const uint32_t f = (nonfinite ? DFP_FLAG_NONFINITE : 0u) | (zero ? DFP_FLAG_ZERO_TENSOR : 0u) |
-                       (clamped ? DFP_FLAG_EXP_CLAMPED : 0u);
-    if (f) atomicOr(&s->flags, f);
+    if (sc.flags) atomicOr(&s->flags, sc.flags);
   }
-  const bool all_zero = nonfinite || zero;
+  const bool all_zero = sc.all_zero;
   const int64_t groups = (n + 3) >> 2;
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   bool saturated = false;
@@ -572,6 +497,11 @@ dfp_status launch_amax(const float* src, int64_t n, int16_t* scratch, dfp_scale*
   uint32_t* part = reinterpret_cast<uint32_t*>(scratch);
   DFP_LAUNCH(K_AMAX, k_amax, dim3((unsigned)parts), dim3(kBlock), 0, st, src, n, part, s);
   DFP_LAUNCH(K_AMAX, k_amax_final, dim3(1), dim3(kBlock), 0, st, part, (int32_t)parts, s);
+  return DFP_OK;
+}
+
+dfp_status launch_amax_final(const uint32_t* part, int32_t nparts, dfp_scale* s, hipStream_t st) {
+  DFP_LAUNCH(K_AMAX, k_amax_final, dim3(1), dim3(kBlock), 0, st, part, nparts, s);
   return DFP_OK;
 }
 

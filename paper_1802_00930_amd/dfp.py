@@ -38,6 +38,12 @@ class Desc(ctypes.Structure):
                  "chunk_len", "seg_chunks", "bits", "rounding", "path")] + [("seed", ctypes.c_uint64)]
 
 
+class BnDesc(ctypes.Structure):
+    """Mirror of ``dfp_bn_desc``."""
+    _fields_ = [(name, ctypes.c_int32) for name in ("n", "c", "hw", "bits", "rounding")] + \
+        [("eps", ctypes.c_float), ("seed", ctypes.c_uint64)]
+
+
 class GemmDesc(ctypes.Structure):
     """Mirror of ``dfp_gemm_desc``."""
     _fields_ = [(name, ctypes.c_int32) for name in
@@ -57,6 +63,8 @@ def lib():
         P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
         DP = ctypes.POINTER(Desc)
         GP = ctypes.POINTER(GemmDesc)
+        BP = ctypes.POINTER(BnDesc)
+        F = ctypes.c_float
         sigs = {
             "dfp_quantize": ([DP, I32, P, P, P, P], I32),
             "dfp_conv_fwd": ([DP, P, P, P, P, P, P, P, SZ, P, P], I32),
@@ -77,6 +85,10 @@ def lib():
             "dfp_downconvert_tensor": ([I64, I32, I32, ctypes.c_uint64, I32, P, P, P, I32, P], I32),
             "dfp_num_chunks": ([DP, I32], I64),
             "dfp_output_dims": ([DP, ctypes.POINTER(I32), ctypes.POINTER(I32)], I32),
+            "dfp_bn_workspace_bytes": ([BP], SZ),
+            "dfp_bn_relu_fwd": ([BP, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+            "dfp_bn_relu_bwd": ([BP, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+            "dfp_sgd_quantize": ([I64, F, F, F, I32, I32, ctypes.c_uint64, P, P, P, P, P, P], I32),
             "dfp_status_str": ([I32], ctypes.c_char_p),
             "dfp_profile_start": ([I32], I32),
             "dfp_profile_stop": ([P, P, I32], I32),
@@ -295,6 +307,58 @@ def dfp_gemm_blocked(d: GemmDesc, block_k, a, ea, b, eb, out, sd=None, workspace
     wp, wn = _ws(workspace)
     _check("dfp_gemm_blocked", lib().dfp_gemm_blocked(ctypes.byref(d), block_k, _ptr(a), _ptr(ea), _ptr(b), _ptr(eb),
                                                       _ptr(out), _ptr(sd), wp, wn, _ptr(partials), _stream(stream)))
+
+
+def make_bn_desc(n, c, hw, bits=15, rounding="nearest", eps=1e-5, seed=0) -> BnDesc:
+    rnd = ROUNDING[rounding] if isinstance(rounding, str) else int(rounding)
+    return BnDesc(n, c, hw, bits, rnd, eps, seed)
+
+
+def bn_workspace_bytes(d: BnDesc) -> int:
+    return int(lib().dfp_bn_workspace_bytes(ctypes.byref(d)))
+
+
+def alloc_bn_workspace(d: BnDesc, device="cuda"):
+    n = bn_workspace_bytes(d)
+    return torch.empty(max(256, (n + 255) // 256 * 256), dtype=torch.uint8, device=device)
+
+
+def dfp_bn_relu_fwd(d: BnDesc, y, sy, gamma, beta, zq, sz, mean, inv_std, res=None, z=None, sums=None,
+                    workspace=None, stream=None):
+    for t, dt, nm in ((y, torch.int16, "y"), (sy, torch.int32, "sy"), (gamma, torch.float32, "gamma"),
+                      (beta, torch.float32, "beta"), (res, torch.float32, "res"), (z, torch.float32, "z"),
+                      (zq, torch.int16, "zq"), (sz, torch.int32, "sz"), (mean, torch.float32, "mean"),
+                      (inv_std, torch.float32, "inv_std"), (sums, torch.int64, "sums")):
+        _need(t, dt, nm)
+    wp, wn = _ws(workspace)
+    _check("dfp_bn_relu_fwd", lib().dfp_bn_relu_fwd(ctypes.byref(d), _ptr(y), _ptr(sy), _ptr(gamma), _ptr(beta),
+                                                    _ptr(res), _ptr(z), _ptr(zq), _ptr(sz), _ptr(mean),
+                                                    _ptr(inv_std), _ptr(sums), wp, wn, _stream(stream)))
+
+
+def dfp_bn_relu_bwd(d: BnDesc, dz, sdz, y, sy, gamma, beta, mean, inv_std, dyq, sdy, dgamma, dbeta, res=None,
+                    dy=None, dres=None, sums=None, workspace=None, stream=None):
+    for t, dt, nm in ((dz, torch.int16, "dz"), (sdz, torch.int32, "sdz"), (y, torch.int16, "y"),
+                      (sy, torch.int32, "sy"), (gamma, torch.float32, "gamma"), (beta, torch.float32, "beta"),
+                      (res, torch.float32, "res"), (mean, torch.float32, "mean"),
+                      (inv_std, torch.float32, "inv_std"), (dy, torch.float32, "dy"), (dyq, torch.int16, "dyq"),
+                      (sdy, torch.int32, "sdy"), (dgamma, torch.float32, "dgamma"),
+                      (dbeta, torch.float32, "dbeta"), (dres, torch.float32, "dres"), (sums, torch.int64, "sums")):
+        _need(t, dt, nm)
+    wp, wn = _ws(workspace)
+    _check("dfp_bn_relu_bwd", lib().dfp_bn_relu_bwd(ctypes.byref(d), _ptr(dz), _ptr(sdz), _ptr(y), _ptr(sy),
+                                                    _ptr(gamma), _ptr(beta), _ptr(res), _ptr(mean), _ptr(inv_std),
+                                                    _ptr(dy), _ptr(dyq), _ptr(sdy), _ptr(dgamma), _ptr(dbeta),
+                                                    _ptr(dres), _ptr(sums), wp, wn, _stream(stream)))
+
+
+def dfp_sgd_quantize(lr, mu, wd, bits, rounding, seed, w, v, dw, wq, sw, stream=None):
+    for t, dt, nm in ((w, torch.float32, "w"), (v, torch.float32, "v"), (dw, torch.float32, "dw"),
+                      (wq, torch.int16, "wq"), (sw, torch.int32, "sw")):
+        _need(t, dt, nm)
+    rnd = ROUNDING[rounding] if isinstance(rounding, str) else int(rounding)
+    _check("dfp_sgd_quantize", lib().dfp_sgd_quantize(w.numel(), lr, mu, wd, bits, rnd, seed, _ptr(w), _ptr(v),
+                                                      _ptr(dw), _ptr(wq), _ptr(sw), _stream(stream)))
 
 
 def alloc_workspace(d: Desc, direction: int, device="cuda"):

@@ -41,7 +41,8 @@ def test_binding_exposes_same_names(dl):
     import paper_1802_00930_amd.dfp as b
     for n in ("dfp_quantize", "dfp_conv_fwd", "dfp_conv_bwd_data", "dfp_conv_bwd_weights", "dfp_downconvert",
               "dfp_conv_fwd_i32", "dfp_conv_bwd_data_i32", "dfp_downconvert_i32", "dfp_gemm",
-              "dfp_quantize_tensor", "dfp_downconvert_tensor"):
+              "dfp_quantize_tensor", "dfp_downconvert_tensor", "dfp_bn_relu_fwd", "dfp_bn_relu_bwd",
+              "dfp_sgd_quantize"):
         assert callable(getattr(b, n))
 
 
@@ -261,6 +262,55 @@ def test_blocked_rejects(dl):
     assert q(3, 10, 4, 17, 0, 0, 0, _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_PARAM
     assert q(3, 10, 4, 15, 0, 0, 0, _p(FAKE), _p(FAKE), None, _p(FAKE), None) == dl.ERR_NULL
     assert q(3, 10, 4, 15, 0, 0, 0, _p(FAKE + 2), _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_ALIGN
+
+
+def test_bn_desc_layout(dl):
+    # five int32, a float, then the uint64 seed at offset 24
+    assert ctypes.sizeof(dl.BnDesc) == 32
+    assert dl.BnDesc.seed.offset == 24
+
+
+def test_bn_rejects(dl):
+    lib = dl.lib()
+    d = dl.make_bn_desc(32, 64, 3136)
+    need = dl.bn_workspace_bytes(d)
+    # 32 image splits x 64 channels x 24 B of partial sums, then 64 x 16 B of coefficients
+    assert need == 32 * 64 * 24 + 1024
+
+    def f(desc, y=FAKE, zq=FAKE + 4096, res=None, z=None, ws=FAKE + 65536, wsn=need, gamma=FAKE):
+        return lib.dfp_bn_relu_fwd(ctypes.byref(desc) if desc is not None else None, _p(y), _p(FAKE), _p(gamma),
+                                   _p(FAKE), _p(res) if res else None, _p(z) if z else None, _p(zq), _p(FAKE),
+                                   _p(FAKE), _p(FAKE), None, _p(ws) if ws else None, wsn, None)
+    assert f(None) == dl.ERR_NULL
+    assert f(d, gamma=0) == dl.ERR_NULL
+    for field, value, code in (("n", 0, dl.ERR_SHAPE), ("hw", -3, dl.ERR_SHAPE), ("bits", 14, dl.ERR_PARAM),
+                               ("rounding", 4, dl.ERR_PARAM), ("eps", -1e-5, dl.ERR_PARAM),
+                               ("eps", float("nan"), dl.ERR_PARAM), ("eps", float("inf"), dl.ERR_PARAM)):
+        bad = dl.make_bn_desc(32, 64, 3136)
+        setattr(bad, field, value)
+        assert f(bad) == code, field
+    assert f(dl.make_bn_desc(2 ** 11, 2 ** 10, 2 ** 10)) == dl.ERR_SHAPE  # 2^31 elements
+    assert dl.bn_workspace_bytes(dl.make_bn_desc(0, 64, 3136)) == 0
+    assert f(d, y=FAKE + 8) == dl.ERR_ALIGN
+    assert f(d, res=FAKE + 4) == dl.ERR_ALIGN
+    assert f(d, z=FAKE + 4) == dl.ERR_ALIGN
+    assert f(d, ws=None) == dl.ERR_WORKSPACE
+    assert f(d, wsn=need - 1) == dl.ERR_WORKSPACE
+    assert f(d, ws=FAKE + 65536 + 128) == dl.ERR_WORKSPACE
+
+    def b(desc, dz=FAKE, dyq=FAKE + 4096, dgamma=FAKE, wsn=need):
+        return lib.dfp_bn_relu_bwd(ctypes.byref(desc), _p(dz), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None,
+                                   _p(FAKE), _p(FAKE), None, _p(dyq), _p(FAKE), _p(dgamma), _p(FAKE), None, None,
+                                   _p(FAKE + 65536), wsn, None)
+    assert b(d, dgamma=0) == dl.ERR_NULL
+    assert b(d, dz=FAKE + 2) == dl.ERR_ALIGN
+    assert b(d, wsn=0) == dl.ERR_WORKSPACE
+    s = lib.dfp_sgd_quantize
+    assert s(1000, 0.1, 0.9, 1e-4, 15, 0, 0, _p(FAKE), _p(FAKE), None, _p(FAKE), _p(FAKE), None) == dl.ERR_NULL
+    assert s(0, 0.1, 0.9, 1e-4, 15, 0, 0, _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_PARAM
+    assert s(1000, 0.1, 0.9, 1e-4, 16, 5, 0, _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE), None) == dl.ERR_PARAM
+    assert s(1000, 0.1, 0.9, 1e-4, 15, 0, 0, _p(FAKE + 4), _p(FAKE), _p(FAKE), _p(FAKE), _p(FAKE),
+             None) == dl.ERR_ALIGN
 
 
 def test_host_queries(dl):
