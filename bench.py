@@ -50,6 +50,7 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dfp32", action="store_true", help="skip the DFP-32-output variant of the step")
     ap.add_argument("--no-gemm", action="store_true", help="skip the GEMM measurements")
+    ap.add_argument("--no-train-ops", action="store_true", help="skip the BN / SGD measurements")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES five times (counter calibration)")
@@ -254,6 +255,50 @@ class BlockedGemmStep(GemmStep):
         self.dfp.dfp_gemm_blocked(self.d, self.bk, self.a, self.ea, self.b, self.eb, self.out, self.sd, self.ws)
 
 
+class TrainOpsStep:
+    """The steps either side of the layer's convolutions: BN + ReLU forward on
+    the DFP16 conv output with Q_a, its backward with Q_e, and FP32 SGD with
+    Q_w on the layer's weights (one call each)."""
+
+    def __init__(self, layer, rounding, seed, dev):
+        import torch
+        from paper_1802_00930_amd import dfp
+        self.dfp, self.torch = dfp, torch
+        n, c, hw = layer.n, layer.k, layer.p * layer.q
+        g = torch.Generator(device="cpu").manual_seed(seed)
+        self.d = dfp.make_bn_desc(n, c, hw, rounding=rounding, seed=seed)
+        self.y = torch.randint(-16384, 16385, (n, c, hw), dtype=torch.int16, generator=g).to(dev)
+        self.dz = torch.randint(-16384, 16385, (n, c, hw), dtype=torch.int16, generator=g).to(dev)
+        self.sy = torch.tensor([0, -12, 0, 0], dtype=torch.int32, device=dev)
+        self.sdz = torch.tensor([0, -24, 0, 0], dtype=torch.int32, device=dev)
+        self.gamma = (torch.rand(c, generator=g) + 0.5).to(dev)
+        self.beta = (torch.rand(c, generator=g) - 0.5).to(dev)
+        self.zq = torch.empty_like(self.y)
+        self.dyq = torch.empty_like(self.y)
+        self.sz, self.sdy, self.swq = (dfp.new_scale(dev) for _ in range(3))
+        self.mean = torch.empty(c, device=dev)
+        self.inv = torch.empty(c, device=dev)
+        self.dg = torch.empty(c, device=dev)
+        self.db = torch.empty(c, device=dev)
+        self.ws = dfp.alloc_bn_workspace(self.d, dev)
+        nw = layer.k * layer.c * layer.r * layer.s
+        self.w = (torch.randn(nw, generator=g) * 0.05).to(dev)
+        self.v = torch.zeros(nw, device=dev)
+        self.dw = (torch.randn(nw, generator=g) * 1e-3).to(dev)
+        self.wq = torch.empty(nw, dtype=torch.int16, device=dev)
+        self.elems, self.nw = n * c * hw, nw
+        self.rounding, self.seed = rounding, seed
+
+    def run(self):
+        dfp = self.dfp
+        dfp.dfp_bn_relu_fwd(self.d, self.y, self.sy, self.gamma, self.beta, self.zq, self.sz, self.mean, self.inv,
+                            workspace=self.ws)
+        dfp.dfp_bn_relu_bwd(self.d, self.dz, self.sdz, self.y, self.sy, self.gamma, self.beta, self.mean, self.inv,
+                            self.dyq, self.sdy, self.dg, self.db, workspace=self.ws)
+        dfp.dfp_sgd_quantize(1e-3, 0.9, 1e-4, 15, self.rounding, self.seed, self.w, self.v, self.dw, self.wq,
+                             self.swq)
+
+
 def kernel_table(recs, steps):
     per = {}
     for name, ms in recs:
@@ -425,6 +470,22 @@ def main():
             "kernel_frac": round(bg_tops / PEAK_INT16_BYTESPLIT_TOPS, 4), "kernels": kbb}
         del fc, big, bfc, bbig
 
+    # BN + ReLU forward / backward on the conv output and SGD + Q_w on the weights
+    train_ops = None
+    if not a.no_train_ops:
+        tr = TrainOpsStep(layer, rounding, seed, dev)
+        ttr, _ = timed(tr, a.steps, a.warmup)
+        _, rtr = timed(tr, a.steps, 1, profile=True)
+        # algorithmic bytes per element: BN forward reads y twice and writes zq (6 B); backward reads y and dz
+        # in each of its three passes and writes dyq (14 B); SGD reads w, v, dw and writes w, v, then the
+        # quantiser reads w and writes wq (26 B)
+        train_ops = {"ms_per_step": round(ttr * 1e3, 4), "bn_elems": tr.elems, "sgd_weights": tr.nw,
+                     "algorithmic_bytes": {"bn_relu_fwd": 6 * tr.elems, "bn_relu_bwd": 14 * tr.elems,
+                                           "sgd_quantize": 26 * tr.nw},
+                     "hbm_gbs_whole_step": round((20 * tr.elems + 26 * tr.nw) / ttr / 1e9, 1),
+                     "kernels": kernel_table(rtr, a.steps)}
+        del tr
+
     out = {
         "metric": METRIC,
         "value": round(3 * ops_per_dir / sec / 1e12, 4),
@@ -459,6 +520,7 @@ def main():
         "chunk_sweep": sweep,
         "dfp32_outputs": dfp32,
         "gemm": gemm,
+        "train_ops": train_ops,
     }
     if not a.no_cpu:
         out["cpu_baseline"] = cpu_baseline(layer, x, w, dy, a.chunk, a.seg_chunks, rounding, seed, a.cpu_seconds)

@@ -98,8 +98,12 @@ __global__ __launch_bounds__(kBlock) void k_bn_stats(const int16_t* __restrict__
                                                      const float* __restrict__ beta, const dfp_scale* __restrict__ sy,
                                                      const dfp_scale* __restrict__ sdz, int32_t N, int32_t C,
                                                      int32_t HW, int32_t S, FastDiv upr_div,
-                                                     int64_t* __restrict__ part) {
+                                                     int64_t* __restrict__ part, dfp_scale* __restrict__ sz) {
   const int32_t s = blockIdx.x, c = blockIdx.y;
+  if (sz && s == 0 && c == 0 && threadIdx.x == 0) {  // the finalize kernel max-reduces into it
+    sz->amax_bits = 0u;
+    sz->flags = 0u;
+  }
   const int32_t n0 = (int32_t)((int64_t)N * s / S), n1 = (int32_t)((int64_t)N * (s + 1) / S);
   constexpr int V = VEC ? 8 : 1;
   const int32_t upr = HW / V;
@@ -172,10 +176,11 @@ __global__ __launch_bounds__(kBlock) void k_bn_stats(const int16_t* __restrict__
 }
 
 // -------------------------------------------------------------- finalize
-// One workgroup; thread t serves channels t, t + 256, ...
+// One wave per channel: the lanes add the channel's S partials (exact
+// integers), lane 0 derives the per-channel values.
 // Forward: mean / inv_std from the exact sums (float64, rounded once), and
-// without a residual the output max from each channel's extreme integers,
-// stored into the output scale (flags cleared) for the rounding pass.
+// without a residual the output max from the channel's extreme integers,
+// max-reduced into the output scale (cleared by the statistics kernel).
 // Backward: dbeta, dgamma and the per-element coefficients k1..k3.
 template <bool BWD>
 __global__ __launch_bounds__(kBlock) void k_bn_finalize(const int64_t* __restrict__ part, int32_t S, int32_t C,
@@ -187,65 +192,61 @@ __global__ __launch_bounds__(kBlock) void k_bn_finalize(const int64_t* __restric
                                                         float* __restrict__ dgamma, float* __restrict__ dbeta,
                                                         float4* __restrict__ kco, dfp_scale* __restrict__ sz,
                                                         bool write_max) {
-  const int32_t ey = sy->exp;
-  const int32_t edz = BWD ? sdz->exp : 0;
-  const double dcnt = (double)cnt;
-  uint32_t m = 0u;
-  for (int32_t c = threadIdx.x; c < C; c += kBlock) {
-    int64_t a = 0, b = 0;
-    int32_t mn = INT_MAX, mx = INT_MIN;
-    for (int32_t s = 0; s < S; ++s) {
-      const int64_t* o = part + ((int64_t)s * C + c) * 3;
-      a += o[0];
-      b += o[1];
-      const uint64_t e = (uint64_t)o[2];
-      mn = min(mn, (int32_t)(uint32_t)e);
-      mx = max(mx, (int32_t)(uint32_t)(e >> 32));
-    }
-    if (sums) {
-      sums[2 * c] = a;
-      sums[2 * c + 1] = b;
-    }
-    if (!BWD) {
-      const double mu = __ddiv_rn(ldexp((double)a, ey), dcnt);
-      double var = __dsub_rn(__ddiv_rn(ldexp((double)b, 2 * ey), dcnt), __dmul_rn(mu, mu));
-      if (var < 0.0) var = 0.0;
-      const float mf = (float)mu;
-      const float t = __fadd_rn((float)var, eps);
-      const float sq = (float)__dsqrt_rn((double)t);  // correctly rounded FP32 square root
-      const float iv = __fdiv_rn(1.0f, sq);
-      mean[c] = mf;
-      inv[c] = iv;
-      if (write_max) {
-        const Chan p{mf, iv, gamma[c], beta[c]};
-        const float zlo = relu(bn_pre(bn_xhat(mn, ey, p), p, nullptr, 0));
-        const float zhi = relu(bn_pre(bn_xhat(mx, ey, p), p, nullptr, 0));
-        m = max(m, max(__float_as_uint(zlo), __float_as_uint(zhi)) & 0x7fffffffu);
-      }
-    } else {
-      const double mf = (double)mean[c], iv = (double)inv[c];
-      const double db = ldexp((double)a, edz);
-      const double dg = __dmul_rn(iv, ldexp(__dsub_rn(ldexp((double)b, ey), __dmul_rn(mf, (double)a)), edz));
-      const float dbf = (float)db, dgf = (float)dg;
-      dbeta[c] = dbf;
-      dgamma[c] = dgf;
-      const double al = __dmul_rn((double)gamma[c], iv);  // exact: two FP32 factors
-      kco[c] = make_float4((float)al, (float)__ddiv_rn(__dmul_rn(-al, (double)dgf), dcnt),
-                           (float)__ddiv_rn(__dmul_rn(-al, (double)dbf), dcnt), 0.0f);
-    }
+  const int lane = threadIdx.x & 63;
+  const int32_t c = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  if (c >= C) return;
+  int64_t a = 0, b = 0;
+  int32_t mn = INT_MAX, mx = INT_MIN;
+  for (int32_t s = lane; s < S; s += 64) {
+    const int64_t* o = part + ((int64_t)s * C + c) * 3;
+    a += o[0];
+    b += o[1];
+    const uint64_t e = (uint64_t)o[2];
+    mn = min(mn, (int32_t)(uint32_t)e);
+    mx = max(mx, (int32_t)(uint32_t)(e >> 32));
   }
-  if (!BWD && write_max) {
-    __shared__ uint32_t red[kBlock / 64];
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      uint32_t r = red[0];
-      for (int i = 1; i < kBlock / 64; ++i) r = max(r, red[i]);
-      sz->amax_bits = r;
-      sz->flags = 0u;
+  for (int off = 32; off > 0; off >>= 1) {
+    a += __shfl_xor(a, off, 64);
+    b += __shfl_xor(b, off, 64);
+    mn = min(mn, __shfl_xor(mn, off, 64));
+    mx = max(mx, __shfl_xor(mx, off, 64));
+  }
+  if (lane != 0) return;
+  const int32_t ey = sy->exp;
+  const double dcnt = (double)cnt;
+  if (sums) {
+    sums[2 * c] = a;
+    sums[2 * c + 1] = b;
+  }
+  if (!BWD) {
+    const double mu = __ddiv_rn(ldexp((double)a, ey), dcnt);
+    double var = __dsub_rn(__ddiv_rn(ldexp((double)b, 2 * ey), dcnt), __dmul_rn(mu, mu));
+    if (var < 0.0) var = 0.0;
+    const float mf = (float)mu;
+    const float t = __fadd_rn((float)var, eps);
+    const float sq = (float)__dsqrt_rn((double)t);  // correctly rounded FP32 square root
+    const float iv = __fdiv_rn(1.0f, sq);
+    mean[c] = mf;
+    inv[c] = iv;
+    if (write_max) {
+      const Chan p{mf, iv, gamma[c], beta[c]};
+      const float zlo = relu(bn_pre(bn_xhat(mn, ey, p), p, nullptr, 0));
+      const float zhi = relu(bn_pre(bn_xhat(mx, ey, p), p, nullptr, 0));
+      const uint32_t m = max(__float_as_uint(zlo), __float_as_uint(zhi)) & 0x7fffffffu;
+      if (m) atomicMax(&sz->amax_bits, m);
     }
+  } else {
+    const int32_t edz = sdz->exp;
+    const double mf = (double)mean[c], iv = (double)inv[c];
+    const double db = ldexp((double)a, edz);
+    const double dg = __dmul_rn(iv, ldexp(__dsub_rn(ldexp((double)b, ey), __dmul_rn(mf, (double)a)), edz));
+    const float dbf = (float)db, dgf = (float)dg;
+    dbeta[c] = dbf;
+    dgamma[c] = dgf;
+    const double al = __dmul_rn((double)gamma[c], iv);  // exact: two FP32 factors
+    kco[c] = make_float4((float)al, (float)__ddiv_rn(__dmul_rn(-al, (double)dgf), dcnt),
+                         (float)__ddiv_rn(__dmul_rn(-al, (double)dbf), dcnt), 0.0f);
   }
 }
 
@@ -495,7 +496,7 @@ int32_t max_parts(int64_t groups, int64_t n) {
 
 dfp_status launch_stats(bool bwd, const dfp_bn_desc& d, const int16_t* y, const int16_t* dz, const float* res,
                         const float* mean, const float* inv, const float* gamma, const float* beta,
-                        const dfp_scale* sy, const dfp_scale* sdz, int64_t* part, hipStream_t st) {
+                        const dfp_scale* sy, const dfp_scale* sdz, int64_t* part, dfp_scale* sz, hipStream_t st) {
   const int32_t S = bn_splits(d);
   const bool vec = (d.hw % 8) == 0 && ((uintptr_t)y & 15) == 0 && (!bwd || ((uintptr_t)dz & 15) == 0);
   const FastDiv upr = make_fastdiv((uint32_t)(vec ? d.hw / 8 : d.hw));
@@ -503,17 +504,17 @@ dfp_status launch_stats(bool bwd, const dfp_bn_desc& d, const int16_t* y, const 
   if (bwd) {
     if (vec)
       DFP_LAUNCH(K_BN_STATS, (k_bn_stats<true, true>), grid, dim3(kBlock), 0, st, y, dz, res, mean, inv, gamma, beta,
-                 sy, sdz, d.n, d.c, d.hw, S, upr, part);
+                 sy, sdz, d.n, d.c, d.hw, S, upr, part, sz);
     else
       DFP_LAUNCH(K_BN_STATS, (k_bn_stats<true, false>), grid, dim3(kBlock), 0, st, y, dz, res, mean, inv, gamma,
-                 beta, sy, sdz, d.n, d.c, d.hw, S, upr, part);
+                 beta, sy, sdz, d.n, d.c, d.hw, S, upr, part, sz);
   } else {
     if (vec)
       DFP_LAUNCH(K_BN_STATS, (k_bn_stats<false, true>), grid, dim3(kBlock), 0, st, y, dz, res, mean, inv, gamma,
-                 beta, sy, sdz, d.n, d.c, d.hw, S, upr, part);
+                 beta, sy, sdz, d.n, d.c, d.hw, S, upr, part, sz);
     else
       DFP_LAUNCH(K_BN_STATS, (k_bn_stats<false, false>), grid, dim3(kBlock), 0, st, y, dz, res, mean, inv, gamma,
-                 beta, sy, sdz, d.n, d.c, d.hw, S, upr, part);
+                 beta, sy, sdz, d.n, d.c, d.hw, S, upr, part, sz);
   }
   return DFP_OK;
 }
@@ -586,10 +587,10 @@ dfp_status launch_bn_relu_fwd(const dfp_bn_desc& d, const int16_t* y, const dfp_
   const BnWs w = bn_ws(d, ws);
   dfp_status rc;
   if ((rc = launch_stats(false, d, y, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, sy, nullptr, w.part,
-                         st)) != DFP_OK)
+                         res ? nullptr : sz, st)) != DFP_OK)
     return rc;
   const int64_t cnt = (int64_t)d.n * d.hw;
-  DFP_LAUNCH(K_BN_FINAL, k_bn_finalize<false>, dim3(1), dim3(kBlock), 0, st, w.part, bn_splits(d), d.c, cnt, sy,
+  DFP_LAUNCH(K_BN_FINAL, k_bn_finalize<false>, dim3((unsigned)((d.c + 3) / 4)), dim3(kBlock), 0, st, w.part, bn_splits(d), d.c, cnt, sy,
              (const dfp_scale*)nullptr, d.eps, gamma, beta, mean, inv_std, sums, (float*)nullptr, (float*)nullptr,
              (float4*)nullptr, sz, res == nullptr);
   const Elems e = make_elems(d, y, nullptr, res, mean, inv_std, gamma, beta, nullptr, sy, nullptr);
@@ -603,9 +604,10 @@ dfp_status launch_bn_relu_bwd(const dfp_bn_desc& d, const int16_t* dz, const dfp
                               float* dgamma, float* dbeta, float* dres, int64_t* sums, void* ws, hipStream_t st) {
   const BnWs w = bn_ws(d, ws);
   dfp_status rc;
-  if ((rc = launch_stats(true, d, y, dz, res, mean, inv_std, gamma, beta, sy, sdz, w.part, st)) != DFP_OK) return rc;
+  if ((rc = launch_stats(true, d, y, dz, res, mean, inv_std, gamma, beta, sy, sdz, w.part, nullptr, st)) != DFP_OK)
+    return rc;
   const int64_t cnt = (int64_t)d.n * d.hw;
-  DFP_LAUNCH(K_BN_FINAL, k_bn_finalize<true>, dim3(1), dim3(kBlock), 0, st, w.part, bn_splits(d), d.c, cnt, sy, sdz,
+  DFP_LAUNCH(K_BN_FINAL, k_bn_finalize<true>, dim3((unsigned)((d.c + 3) / 4)), dim3(kBlock), 0, st, w.part, bn_splits(d), d.c, cnt, sy, sdz,
              d.eps, gamma, beta, const_cast<float*>(mean), const_cast<float*>(inv_std), sums, dgamma, dbeta, w.kco,
              (dfp_scale*)nullptr, false);
   const Elems e = make_elems(d, y, dz, res, mean, inv_std, gamma, beta, w.kco, sy, sdz);
