@@ -30,7 +30,16 @@ struct ConvMfmaArgs {
   const int8_t* exa;
   const int8_t* exb;
   int32_t bk, nb;
+  // 1: xs is in the plane layout [n][Hp][Cin/32][digit][half][Wp][16 B] (the
+  // 16 channels of one half-block and one digit of consecutive columns are
+  // adjacent), written for the four-waves-per-SIMD kernel; 0: [n][Hp][Wp][CG][32 B]
+  int32_t plane;
 };
+
+// The plane layout and its kernel serve 32-channel blocks (Cin a multiple of
+// 32), full chunks of two blocks (T a multiple of 64, L = 64, or one chunk
+// over the whole reduction) and at most 36 blocks of resident filter digits.
+bool conv_w16_eligible(int32_t Cin, int32_t T, int32_t L, bool i32);
 
 // Largest exponent-block count the blocked matrix-core kernel stages in LDS.
 constexpr int32_t kBlockedMaxBlocks = 80;

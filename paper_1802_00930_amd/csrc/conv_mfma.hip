@@ -122,7 +122,11 @@ __global__ __launch_bounds__(256) void k_prep_a(const int16_t* __restrict__ w, u
 // output row is stored contiguously.
 constexpr int kPrepBElems = 16384;  // int16 elements staged per pass (32 KiB)
 
-template <bool VEC>
+// PLANE: write the plane layout [n][u][cb][digit][half][v][16 B] instead
+// (CG even): the hi digits of channel group cg = 2 cb + half of column v at
+// ((cb * 4 + half) * Wp + v) * 16 within the row, the lo digits 2 Wp * 16
+// bytes further.
+template <bool VEC, bool PLANE>
 __global__ __launch_bounds__(256) void k_prep_b(const int16_t* __restrict__ src, uint8_t* __restrict__ xs,
                                                int32_t N, int32_t Cs, int32_t Hs, int32_t Wsrc, int32_t Hp,
                                                int32_t Wp, int32_t CG, int32_t top, int32_t left, int32_t dil_h,
@@ -179,9 +183,16 @@ __global__ __launch_bounds__(256) void k_prep_b(const int16_t* __restrict__ src,
           lo[i >> 2] |= lo_digit(a) << (8 * (i & 3));
         }
       }
-      uint4* d = dst + (v * CG + cg0 + cgl) * 2;
-      d[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-      d[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      if (PLANE) {
+        const int32_t cg = cg0 + cgl;
+        uint4* d = dst + ((cg >> 1) * 4 + (cg & 1)) * Wp + v;
+        d[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+        d[2 * Wp] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      } else {
+        uint4* d = dst + (v * CG + cg0 + cgl) * 2;
+        d[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+        d[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      }
     }
   }
 }
@@ -1422,9 +1433,183 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
   }
 }
 
+// ---------------------------------------------------------------------------
+// Four-waves-per-SIMD persistent variant (chunks of two blocks, L = 64, or one
+// chunk over the whole reduction; reduction channel counts that are multiples
+// of 32; at most kW16MaxKB blocks).  One workgroup of 16 waves per CU and per
+// 64-row tile keeps the tile's filter digits resident in LDS.  The work is a
+// list of units (32-pixel tile, 32-row half), u = 2 * tile + half; workgroup
+// b takes a contiguous range of units (ranges of one XCD adjacent, so its L2
+// holds the input rows the range touches) and wave w of it takes units w,
+// w + 16, ... of the range, so consecutive units run on different SIMDs and
+// every SIMD gets the same number of units to within one.  Each lane loads its
+// B operand (16 channels x hi / lo digits of its pixel) straight into
+// registers, one chunk ahead, from the plane layout of the digit tensor, where
+// the 32 lanes of a channel half read 512 consecutive bytes; the A
+// operand comes from LDS.  With four waves per SIMD one wave's chunk
+// conversion (VALU) runs while the others issue MFMAs, and the reduction loop
+// has no data-dependent branches.
+constexpr int kWaves16 = 16;
+constexpr int kThreads16 = kWaves16 * 64;
+constexpr int32_t kW16MaxKB = 36;
+
+template <bool PARTIALS, bool I32 = false>
+__global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a) {
+  __shared__ __align__(16) uint8_t sA[kW16MaxKB * kStageA];
+  __shared__ uint32_t red[kWaves16];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int half = lane >> 5;
+  const int col = lane & 31;
+  const int32_t m0 = blockIdx.y * kMT;
+  const int32_t KB = a.KB, J = KB / 2, Cin = a.Cin, S = a.S;
+  // the launcher guarantees outputs and the B workspace index below 2^31
+  const int32_t NP = (int32_t)a.NP, Qo = a.Qo, Po = a.Po;
+  const int32_t PQ = Po * Qo;
+
+  // ---- filter digits of this 64-row tile: KB blocks x 256 pieces of 16 B, direct to LDS
+  {
+    const int64_t a_block_bytes = (int64_t)a.Mp * 64;
+    const int32_t insts = (KB * 256) / 64;  // one instruction fills 64 consecutive slots
+    for (int32_t j = wave; j < insts; j += kWaves16) {
+      const int32_t slot0 = j * 64;
+      const int32_t sl = slot0 + lane;
+      const int32_t kb = sl >> 8, sw = sl & 255;
+      const int row = sw >> 2, piece = (sw & 3) ^ ((row >> 2) & 3);
+      const uint8_t* src = a.wsa + kb * a_block_bytes + ((int64_t)(m0 + row) * 2 + (piece >> 1)) * 32 + (piece & 1) * 16;
+      __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(sA + slot0 * 16), 16, 0, 0);
+    }
+  }
+
+  // ---- this workgroup's unit range (XCD x = workgroup id mod 8 gets adjacent ranges)
+  const int32_t units = 2 * ((NP + 31) / 32);
+  const int32_t G = gridDim.x;
+  const int32_t xcd = blockIdx.x & 7, per = G >> 3, rem = G & 7;
+  const int32_t vb = xcd * per + min(xcd, rem) + (blockIdx.x >> 3);
+  const int32_t u0 = (int32_t)((int64_t)units * vb / G), u1 = (int32_t)((int64_t)units * (vb + 1) / G);
+  const int32_t my_units = (u1 - u0 > wave) ? (u1 - u0 - wave + kWaves16 - 1) / kWaves16 : 0;
+  const int32_t nq = my_units * J;  // chunks this wave consumes
+
+  // plane layout: row stride Cin*2*Wp bytes, column stride 16, 32-channel block stride 4*Wp*16,
+  // lo digits 2*Wp*16 bytes after the hi digits, channel half `half` at Wp*16
+  const int32_t cpb = Cin >> 5;  // blocks per filter tap
+  const int32_t plane_bytes = a.Wp * 16;
+  const int32_t tap_row_bytes = a.rsign * cpb * 4 * plane_bytes;
+  const int32_t tap_col_bytes = a.rsign * 16;
+  // byte offset of this lane's operand for the pixel of `tile` (block offsets are added per block)
+  auto pixel_off = [&](int32_t tile) -> int32_t {
+    int32_t gp = tile * 32 + col;
+    if (gp >= NP) gp = 0;
+    const int32_t qo = gp % Qo, po = (gp / Qo) % Po, im = gp / PQ;
+    return ((im * a.Hp + po * a.ustride_h + a.roff_h) * cpb * 4 + half) * plane_bytes +
+           (qo * a.ustride_w + a.roff_w) * 16;
+  };
+  auto unit_of = [&](int32_t i) { return u0 + wave + kWaves16 * i; };
+
+  const int32_t e = a.ea->exp + a.eb->exp;
+  uint32_t amax = 0;
+  wait_vmcnt<0>();  // filter digits landed for this lane
+  __syncthreads();  // ... and for every lane
+
+  if (nq > 0) {
+    // B load stream: chunk ld_c of local unit ld_unit; block position (ld_r, ld_s, ld_cb)
+    int32_t ld_q = 0, ld_unit = 0, ld_c = 0, ld_r = 0, ld_s = 0, ld_cb = 0;
+    int32_t ld_pix = pixel_off(unit_of(0) >> 1);
+    // loads block b (0 or 1) of the stream's next chunk; after block 1 the stream advances
+    // (past its end the last chunk is loaded again: valid addresses, unused data)
+    auto load_block = [&](v4i& hi, v4i& lo, int b) {
+      const int32_t off = ld_r * tap_row_bytes + ld_s * tap_col_bytes + ld_cb * 4 * plane_bytes;
+      const uint8_t* src = a.xs + (uint32_t)(ld_pix + off);
+      hi = *reinterpret_cast<const v4i*>(src);
+      lo = *reinterpret_cast<const v4i*>(src + 2 * plane_bytes);
+      if (++ld_cb == cpb) {
+        ld_cb = 0;
+        if (++ld_s == S) { ld_s = 0; ++ld_r; }
+      }
+      if (b == 1) {
+        if (ld_q + 1 < nq) {
+          ++ld_q;
+          if (++ld_c == J) {
+            ld_c = 0; ld_r = 0; ld_s = 0; ld_cb = 0;
+            ++ld_unit;
+            ld_pix = pixel_off(unit_of(ld_unit) >> 1);
+          }
+        } else {  // step back to the start of the same chunk
+          if (ld_cb >= 2) {
+            ld_cb -= 2;
+          } else {
+            ld_r = 0; ld_s = 0; ld_cb = 0;
+            for (int32_t k = 0; k < 2 * ld_c; ++k)
+              if (++ld_cb == cpb) { ld_cb = 0; if (++ld_s == S) { ld_s = 0; ++ld_r; } }
+          }
+        }
+      }
+    };
+
+    const uint32_t ra_hi = swz(col, 2 * half) * 16, ra_lo = swz(col, 2 * half + 1) * 16;
+    // the stream's first chunk; afterwards each block's registers are refilled
+    // with the block two ahead as soon as its MFMAs have been issued
+    v4i b0h, b0l, b1h, b1l;
+    load_block(b0h, b0l, 0);
+    load_block(b1h, b1l, 1);
+    for (int32_t unit = 0; unit < my_units; ++unit) {
+      const int32_t u = unit_of(unit);
+      const int32_t msub = u & 1;
+      const int32_t g = (u >> 1) * 32 + col;
+      const bool gvalid = g < NP;
+      const int32_t obase = gvalid ? (g / PQ) * a.M * PQ + (g % PQ) : 0;
+      const int32_t mrow0 = m0 + 32 * msub + 4 * half;
+      Acc3 acc;
+      float sum[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sum[v] = 0.f;
+      const uint8_t* ab = sA + msub * 2048;
+      for (int32_t c = 0; c < J; ++c, ab += 2 * kStageA) {
+        const v4i ah0 = *reinterpret_cast<const v4i*>(ab + ra_hi);
+        const v4i al0 = *reinterpret_cast<const v4i*>(ab + ra_lo);
+        if (I32 && c != 0) mfma_tile(acc, ah0, al0, b0h, b0l, false);
+        else mfma_tile(acc, ah0, al0, b0h, b0l, true);
+        load_block(b0h, b0l, 0);
+        const v4i ah1 = *reinterpret_cast<const v4i*>(ab + kStageA + ra_hi);
+        const v4i al1 = *reinterpret_cast<const v4i*>(ab + kStageA + ra_lo);
+        mfma_tile(acc, ah1, al1, b1h, b1l, false);
+        load_block(b1h, b1l, 1);
+        if (!I32) flush_tile<PARTIALS>(acc, sum, c, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+      }
+      if (I32) keep_tile_i32(acc, sum);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
+        if (gvalid && m < a.M) amax = max(amax, store_out<I32>(a.out, (uint32_t)(obase + m * PQ), sum[v], e));
+      }
+    }
+  }
+
+  if (a.so) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
+    if (lane == 0) red[wave] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t b = red[0];
+      for (int i = 1; i < kWaves16; ++i) b = max(b, red[i]);
+      if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
+      if (I32) {
+        if (blockIdx.x == 0 && blockIdx.y == 0) a.so->exp = e;
+      } else if (b == 0x7f800000u) {
+        atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+      }
+    }
+  }
+}
+
 inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
 
 }  // namespace
+
+bool conv_w16_eligible(int32_t Cin, int32_t T, int32_t L, bool i32) {
+  return (Cin % 32) == 0 && (T % 64) == 0 && T / 32 <= kW16MaxKB && (i32 || L == 64);
+}
 
 bool conv_mfma_supported(const Geom& g, int32_t dir) {
   const int32_t wsrc = dir == DFP_FWD ? g.w : g.q;
@@ -1473,6 +1658,8 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   int2* boff = reinterpret_cast<int2*>(xs + p.ws_b_bytes);
   const int32_t rsign = fwd ? 1 : -1;
   const int32_t tap_row_bytes = rsign * p.Wp * p.CG * 32, tap_col_bytes = rsign * p.CG * 32;
+  const bool plane = conv_w16_eligible(p.Cin, p.T, g.L, i32) && (int64_t)g.n * p.Po * p.Qo * p.M < (1ll << 31) &&
+                     p.ws_b_bytes < (1ll << 31);
   {
     const int64_t total = (int64_t)p.KB * p.Mp * 8;
     DFP_LAUNCH(K_WPREP, k_prep_a, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, b, wsa, p.M, p.Mp,
@@ -1483,12 +1670,17 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
     const bool vec = (Wsrc % 8) == 0 && (reinterpret_cast<uintptr_t>(a) & 15) == 0;
     const int32_t cgc = std::max(1, std::min(p.CG, kPrepBElems / (16 * Wsrc)));  // as in the kernel
     const size_t lds = (size_t)cgc * 16 * Wsrc * 2;
-    if (vec)
-      DFP_LAUNCH(K_XPREP, k_prep_b<true>, dim3((unsigned)(g.n * p.Hp)), dim3(256), lds, st, a, xs, g.n, Cs, Hs,
-                 Wsrc, p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w);
-    else
-      DFP_LAUNCH(K_XPREP, k_prep_b<false>, dim3((unsigned)(g.n * p.Hp)), dim3(256), lds, st, a, xs, g.n, Cs, Hs,
-                 Wsrc, p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w);
+#define DFP_PREP_B(V, PL)                                                                                   \
+  DFP_LAUNCH(K_XPREP, (k_prep_b<V, PL>), dim3((unsigned)(g.n * p.Hp)), dim3(256), lds, st, a, xs, g.n, Cs, Hs, \
+             Wsrc, p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w)
+    if (plane) {
+      if (vec) DFP_PREP_B(true, true);
+      else DFP_PREP_B(false, true);
+    } else {
+      if (vec) DFP_PREP_B(true, false);
+      else DFP_PREP_B(false, false);
+    }
+#undef DFP_PREP_B
   }
   ConvMfmaArgs args{};
   args.xs = xs;
@@ -1503,6 +1695,7 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   args.CG = p.CG; args.Hp = p.Hp; args.Wp = p.Wp; args.Po = p.Po; args.Qo = p.Qo;
   args.NP = (int64_t)g.n * p.Po * p.Qo;
   args.O = args.NP * p.M;
+  args.plane = plane ? 1 : 0;
   if (fwd) {
     args.ustride_h = g.sh;
     args.ustride_w = g.sw;
@@ -1545,10 +1738,23 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     return DFP_OK;
   }
   const bool persist_ok = chan16 && (args.T % 64) == 0 && args.KB >= 4 && args.KB <= kARes3Max && small_index;
+  // four waves per SIMD: 32-channel blocks (each block inside one filter tap), full chunks of two blocks
+  const bool w16_ok = args.plane != 0 && small_index;
+  auto w16_grid = [&]() {
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    const int64_t units = 2 * ((args.NP + 31) / 32);
+    const int64_t mtiles = args.Mp / kMT;
+    int64_t gx = std::max<int64_t>(1, cus / mtiles);
+    gx = std::min<int64_t>(gx, (units + kWaves16 - 1) / kWaves16);
+    return dim3((unsigned)gx, (unsigned)mtiles);
+  };
   if (i32) {
     // DFP-32 output: one chunk over the whole reduction (the caller checked L >= T)
     args.L = args.KB * 32;
-    if (persist_ok)
+    if (w16_ok)
+      DFP_LAUNCH(kid32, (k_conv_mfma_w16<false, true>), w16_grid(), dim3(kThreads16), 0, st, args);
+    else if (persist_ok)
       DFP_LAUNCH(kid32, (k_conv_mfma_persist<false, true>), persist_grid(), dim3(kThreads3), 0, st, args);
     else if (chan16 && small_index)
       DFP_LAUNCH(kid32, (k_conv_mfma_q<false, true>), grid, dim3(kThreadsQ), 0, st, args);
@@ -1562,6 +1768,11 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
   if (masked == MK && partials == PT && chan16 == CH) {                                    \
     DFP_LAUNCH(kid, (k_conv_mfma<MK, PT, CH>), grid, dim3(kThreads), 0, st, args);          \
     return DFP_OK;                                                                          \
+  }
+  if (w16_ok && args.L == 64) {
+    if (partials) DFP_LAUNCH(kid, (k_conv_mfma_w16<true>), w16_grid(), dim3(kThreads16), 0, st, args);
+    else DFP_LAUNCH(kid, (k_conv_mfma_w16<false>), w16_grid(), dim3(kThreads16), 0, st, args);
+    return DFP_OK;
   }
   if (persist_ok && args.L == 64) {
     const dim3 grid3 = persist_grid();
