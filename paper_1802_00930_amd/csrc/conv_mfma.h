@@ -34,6 +34,7 @@ struct ConvMfmaArgs {
   // 16 channels of one half-block and one digit of consecutive columns are
   // adjacent), written for the four-waves-per-SIMD kernel; 0: [n][Hp][Wp][CG][32 B]
   int32_t plane;
+  FastDiv div_pq, div_q;  // n / (Po*Qo) and n / Qo for output pixel indices
 };
 
 // The plane layout and its kernel serve 32-channel blocks (Cin a multiple of

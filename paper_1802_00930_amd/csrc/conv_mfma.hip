@@ -230,6 +230,21 @@ __device__ __forceinline__ void mfma_tile(Acc3& acc, const v4i& ahi, const v4i& 
   acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, bhi, acc.xx, 0, 0, 0);
 }
 
+// mfma_tile with the issue order HH, X(hi, lo), LL, X(lo, hi) pinned, so the
+// two dependent cross products of a block are two MFMAs apart and the next
+// block's first cross product follows its HH.
+__device__ __forceinline__ void mfma_tile_ordered(Acc3& acc, const v4i& ahi, const v4i& alo, const v4i& bhi,
+                                                  const v4i& blo, bool fresh) {
+  const v16i z = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+  acc.hh = __builtin_amdgcn_mfma_i32_32x32x32_i8(ahi, bhi, fresh ? z : acc.hh, 0, 0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(ahi, blo, fresh ? z : acc.xx, 0, 0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  acc.ll = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, blo, fresh ? z : acc.ll, 0, 0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  acc.xx = __builtin_amdgcn_mfma_i32_32x32x32_i8(alo, bhi, acc.xx, 0, 0, 0);
+}
+
 // ((a << 8) + b) << 8) + c as two v_lshl_add_u32.  The shift-adds are plain
 // C so the compiler's hazard checks see every read of an MFMA result; the
 // empty asm only stops the re-association into shift, shift, add3.
@@ -1456,16 +1471,16 @@ constexpr int32_t kW16MaxKB = 36;
 template <bool PARTIALS, bool I32 = false>
 __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a) {
   __shared__ __align__(16) uint8_t sA[kW16MaxKB * kStageA];
+  __shared__ __align__(8) int32_t s_boff[kW16MaxKB];
   __shared__ uint32_t red[kWaves16];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int half = lane >> 5;
   const int col = lane & 31;
   const int32_t m0 = blockIdx.y * kMT;
-  const int32_t KB = a.KB, J = KB / 2, Cin = a.Cin, S = a.S;
+  const int32_t KB = a.KB, J = KB / 2, Cin = a.Cin;
   // the launcher guarantees outputs and the B workspace index below 2^31
-  const int32_t NP = (int32_t)a.NP, Qo = a.Qo, Po = a.Po;
-  const int32_t PQ = Po * Qo;
+  const int32_t NP = (int32_t)a.NP, Qo = a.Qo, PQ = a.Po * a.Qo;
 
   // ---- filter digits of this 64-row tile: KB blocks x 256 pieces of 16 B, direct to LDS
   {
@@ -1480,6 +1495,16 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
       __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(sA + slot0 * 16), 16, 0, 0);
     }
   }
+  // plane layout: row stride Cin*2*Wp bytes, column stride 16, 32-channel block stride 4*Wp*16,
+  // lo digits 2*Wp*16 bytes after the hi digits, channel half `half` at Wp*16.
+  // Byte offset of block kb (tap (r, s), channel block cb) from a pixel's operand:
+  const int32_t cpb = Cin >> 5;  // blocks per filter tap
+  const int32_t plane_bytes = a.Wp * 16;
+  if ((int32_t)threadIdx.x < KB) {
+    const int32_t kb = threadIdx.x, tap = kb / cpb, cb = kb - tap * cpb;
+    const int32_t r = tap / a.S, sx = tap - r * a.S;
+    s_boff[kb] = a.rsign * (r * cpb * 4 * plane_bytes + sx * 16) + cb * 4 * plane_bytes;
+  }
 
   // ---- this workgroup's unit range (XCD x = workgroup id mod 8 gets adjacent ranges)
   const int32_t units = 2 * ((NP + 31) / 32);
@@ -1488,76 +1513,56 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   const int32_t vb = xcd * per + min(xcd, rem) + (blockIdx.x >> 3);
   const int32_t u0 = (int32_t)((int64_t)units * vb / G), u1 = (int32_t)((int64_t)units * (vb + 1) / G);
   const int32_t my_units = (u1 - u0 > wave) ? (u1 - u0 - wave + kWaves16 - 1) / kWaves16 : 0;
-  const int32_t nq = my_units * J;  // chunks this wave consumes
-
-  // plane layout: row stride Cin*2*Wp bytes, column stride 16, 32-channel block stride 4*Wp*16,
-  // lo digits 2*Wp*16 bytes after the hi digits, channel half `half` at Wp*16
-  const int32_t cpb = Cin >> 5;  // blocks per filter tap
-  const int32_t plane_bytes = a.Wp * 16;
-  const int32_t tap_row_bytes = a.rsign * cpb * 4 * plane_bytes;
-  const int32_t tap_col_bytes = a.rsign * 16;
-  // byte offset of this lane's operand for the pixel of `tile` (block offsets are added per block)
-  auto pixel_off = [&](int32_t tile) -> int32_t {
-    int32_t gp = tile * 32 + col;
+  auto unit_of = [&](int32_t i) { return u0 + wave + kWaves16 * i; };
+  // byte offset of this lane's operand for the pixel of unit u (block offsets come from s_boff)
+  auto pixel_off = [&](int32_t u) -> int32_t {
+    int32_t gp = (u >> 1) * 32 + col;
     if (gp >= NP) gp = 0;
-    const int32_t qo = gp % Qo, po = (gp / Qo) % Po, im = gp / PQ;
+    const int32_t im = (int32_t)fdiv((uint32_t)gp, a.div_pq), rp = gp - im * PQ;
+    const int32_t po = (int32_t)fdiv((uint32_t)rp, a.div_q), qo = rp - po * Qo;
     return ((im * a.Hp + po * a.ustride_h + a.roff_h) * cpb * 4 + half) * plane_bytes +
            (qo * a.ustride_w + a.roff_w) * 16;
   };
-  auto unit_of = [&](int32_t i) { return u0 + wave + kWaves16 * i; };
+  // the loads of a block stay in stream order (hi, lo, block after block) so
+  // every wait for a block's operands leaves the two newer loads in flight
+  auto load_b = [&](v4i& hi, v4i& lo, int32_t pix, int32_t boff) {
+    const uint32_t off = (uint32_t)(pix + boff);
+    __builtin_amdgcn_sched_barrier(0);
+    hi = *reinterpret_cast<const v4i*>(a.xs + off);
+    lo = *reinterpret_cast<const v4i*>(a.xs + (off + 2 * plane_bytes));
+    __builtin_amdgcn_sched_barrier(0);
+  };
 
   const int32_t e = a.ea->exp + a.eb->exp;
+  const bool full_rows = a.M == a.Mp;  // every row of the 64-row tiles is an output channel
   uint32_t amax = 0;
   wait_vmcnt<0>();  // filter digits landed for this lane
-  __syncthreads();  // ... and for every lane
+  __syncthreads();  // ... and for every lane; the block offsets are written
 
-  if (nq > 0) {
-    // B load stream: chunk ld_c of local unit ld_unit; block position (ld_r, ld_s, ld_cb)
-    int32_t ld_q = 0, ld_unit = 0, ld_c = 0, ld_r = 0, ld_s = 0, ld_cb = 0;
-    int32_t ld_pix = pixel_off(unit_of(0) >> 1);
-    // loads block b (0 or 1) of the stream's next chunk; after block 1 the stream advances
-    // (past its end the last chunk is loaded again: valid addresses, unused data)
-    auto load_block = [&](v4i& hi, v4i& lo, int b) {
-      const int32_t off = ld_r * tap_row_bytes + ld_s * tap_col_bytes + ld_cb * 4 * plane_bytes;
-      const uint8_t* src = a.xs + (uint32_t)(ld_pix + off);
-      hi = *reinterpret_cast<const v4i*>(src);
-      lo = *reinterpret_cast<const v4i*>(src + 2 * plane_bytes);
-      if (++ld_cb == cpb) {
-        ld_cb = 0;
-        if (++ld_s == S) { ld_s = 0; ++ld_r; }
-      }
-      if (b == 1) {
-        if (ld_q + 1 < nq) {
-          ++ld_q;
-          if (++ld_c == J) {
-            ld_c = 0; ld_r = 0; ld_s = 0; ld_cb = 0;
-            ++ld_unit;
-            ld_pix = pixel_off(unit_of(ld_unit) >> 1);
-          }
-        } else {  // step back to the start of the same chunk
-          if (ld_cb >= 2) {
-            ld_cb -= 2;
-          } else {
-            ld_r = 0; ld_s = 0; ld_cb = 0;
-            for (int32_t k = 0; k < 2 * ld_c; ++k)
-              if (++ld_cb == cpb) { ld_cb = 0; if (++ld_s == S) { ld_s = 0; ++ld_r; } }
-          }
-        }
-      }
-    };
-
+  if (my_units > 0) {
     const uint32_t ra_hi = swz(col, 2 * half) * 16, ra_lo = swz(col, 2 * half + 1) * 16;
+    int32_t cur_pix = pixel_off(unit_of(0));
     // the stream's first chunk; afterwards each block's registers are refilled
-    // with the block two ahead as soon as its MFMAs have been issued
+    // with the block two ahead (the next unit's first blocks at a unit's last
+    // chunk, the last unit's first blocks again at the very end) as soon as its
+    // MFMAs have been issued
     v4i b0h, b0l, b1h, b1l;
-    load_block(b0h, b0l, 0);
-    load_block(b1h, b1l, 1);
+    {
+      const int2 bo = *reinterpret_cast<const int2*>(s_boff);
+      load_b(b0h, b0l, cur_pix, bo.x);
+      load_b(b1h, b1l, cur_pix, bo.y);
+    }
     for (int32_t unit = 0; unit < my_units; ++unit) {
       const int32_t u = unit_of(unit);
+      const int32_t next_pix = unit + 1 < my_units ? pixel_off(unit_of(unit + 1)) : cur_pix;
       const int32_t msub = u & 1;
       const int32_t g = (u >> 1) * 32 + col;
       const bool gvalid = g < NP;
-      const int32_t obase = gvalid ? (g / PQ) * a.M * PQ + (g % PQ) : 0;
+      int32_t obase = 0;
+      if (gvalid) {
+        const int32_t im = (int32_t)fdiv((uint32_t)g, a.div_pq);
+        obase = im * a.M * PQ + (g - im * PQ);
+      }
       const int32_t mrow0 = m0 + 32 * msub + 4 * half;
       Acc3 acc;
       float sum[16];
@@ -1565,23 +1570,35 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
       for (int v = 0; v < 16; ++v) sum[v] = 0.f;
       const uint8_t* ab = sA + msub * 2048;
       for (int32_t c = 0; c < J; ++c, ab += 2 * kStageA) {
+        const bool last = c + 1 == J;
+        const int2 bo = *reinterpret_cast<const int2*>(s_boff + (last ? 0 : 2 * c + 2));
+        const int32_t pix = last ? next_pix : cur_pix;
         const v4i ah0 = *reinterpret_cast<const v4i*>(ab + ra_hi);
         const v4i al0 = *reinterpret_cast<const v4i*>(ab + ra_lo);
         if (I32 && c != 0) mfma_tile(acc, ah0, al0, b0h, b0l, false);
         else mfma_tile(acc, ah0, al0, b0h, b0l, true);
-        load_block(b0h, b0l, 0);
+        load_b(b0h, b0l, pix, bo.x);
         const v4i ah1 = *reinterpret_cast<const v4i*>(ab + kStageA + ra_hi);
         const v4i al1 = *reinterpret_cast<const v4i*>(ab + kStageA + ra_lo);
         mfma_tile(acc, ah1, al1, b1h, b1l, false);
-        load_block(b1h, b1l, 1);
+        load_b(b1h, b1l, pix, bo.y);
         if (!I32) flush_tile<PARTIALS>(acc, sum, c, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
       }
       if (I32) keep_tile_i32(acc, sum);
+      if (gvalid) {
+        if (full_rows) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
-        if (gvalid && m < a.M) amax = max(amax, store_out<I32>(a.out, (uint32_t)(obase + m * PQ), sum[v], e));
+          for (int v = 0; v < 16; ++v)
+            amax = max(amax, store_out<I32>(a.out, (uint32_t)(obase + (mrow0 + 8 * (v >> 2) + (v & 3)) * PQ), sum[v], e));
+        } else {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
+            if (m < a.M) amax = max(amax, store_out<I32>(a.out, (uint32_t)(obase + m * PQ), sum[v], e));
+          }
+        }
       }
+      cur_pix = next_pix;
     }
   }
 
@@ -1740,6 +1757,8 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
   const bool persist_ok = chan16 && (args.T % 64) == 0 && args.KB >= 4 && args.KB <= kARes3Max && small_index;
   // four waves per SIMD: 32-channel blocks (each block inside one filter tap), full chunks of two blocks
   const bool w16_ok = args.plane != 0 && small_index;
+  args.div_pq = make_fastdiv((uint32_t)(args.Po * args.Qo));
+  args.div_q = make_fastdiv((uint32_t)args.Qo);
   auto w16_grid = [&]() {
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);

@@ -37,6 +37,21 @@ enum KernelId : int32_t {
   K_NUM_KERNELS = 24
 };
 
+// n / d for 0 <= n < 2^32 by multiply-high (round-up method, l = ceil(log2 d),
+// m = floor(2^32 (2^l - d) / d) + 1, q = (mulhi(m, n) + n) >> l).
+struct FastDiv {
+  uint32_t m, l;
+};
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  const uint64_t m = ((((uint64_t)1 << 32) * (((uint64_t)1 << l) - d)) / d) + 1;
+  return {(uint32_t)m, l};
+}
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) {
+  return (uint32_t)(((uint64_t)__umulhi(n, f.m) + n) >> f.l);
+}
+
 // Convolution geometry handed to kernels by value.
 struct Geom {
   int32_t n, c, h, w;   // activations NCHW

@@ -37,21 +37,6 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kMaxParts = 1024;
 
-// n / d for 0 <= n < 2^32 by multiply-high (round-up method, l = ceil(log2 d),
-// m = floor(2^32 (2^l - d) / d) + 1, q = (mulhi(m, n) + n) >> l).
-struct FastDiv {
-  uint32_t m, l;
-};
-FastDiv make_fastdiv(uint32_t d) {
-  uint32_t l = 0;
-  while ((1ull << l) < d) ++l;
-  const uint64_t m = ((((uint64_t)1 << 32) * (((uint64_t)1 << l) - d)) / d) + 1;
-  return {(uint32_t)m, l};
-}
-__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) {
-  return (uint32_t)(((uint64_t)__umulhi(n, f.m) + n) >> f.l);
-}
-
 struct Chan {
   float mean, inv, gamma, beta;
 };
