@@ -202,8 +202,27 @@ __device__ __forceinline__ void flush_tile(const Acc3& acc, float (&sum)[16], in
   }
 }
 
+// Workgroup -> (column tile, row tile, segment).  Workgroup ids are dealt to
+// the 8 XCDs in turn (id mod 8), each with its own L2.  The (segment, tile)
+// list, segment-major, is cut into 8 contiguous ranges, one per XCD, so the
+// tiles of a segment run on one XCD (except where a range ends) and its dy
+// digits are fetched into that L2 once for all column tiles.  1-D grid of
+// nseg * ntx * nty workgroups.
+struct BwdwTile {
+  int32_t tx, ty, seg;
+};
+__device__ __forceinline__ BwdwTile bwdw_tile(const BwdwArgs& a) {
+  const int32_t per = a.ntx * a.nty;
+  const int32_t W = gridDim.x, b = blockIdx.x, x = b & 7;
+  const int32_t l = x * (W >> 3) + min(x, W & 7) + (b >> 3);
+  const int32_t seg = l / per, t = l - seg * per;
+  return {t % a.ntx, t / a.ntx, seg};
+}
+
 template <bool MASKED, bool PARTIALS>
 __global__ __launch_bounds__(kThreads, 2) void k_bwdw_mfma(BwdwArgs a) {
+  const BwdwTile tl = bwdw_tile(a);
+  if (tl.seg >= a.nseg) return;
   extern __shared__ __align__(16) uint8_t smem[];
   uint16_t* band = reinterpret_cast<uint16_t*>(smem);                        // [nch][rows][Wpad]
   int32_t* toff = reinterpret_cast<int32_t*>(smem + a.band_bytes);           // [kSBT]
@@ -214,7 +233,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_mfma(BwdwArgs a) {
   const int lc = lane & 31;
   const int32_t RS = a.R * a.S;
   const int64_t CRS = (int64_t)a.C * RS;
-  const int64_t col0 = (int64_t)blockIdx.x * kNT;
+  const int64_t col0 = (int64_t)tl.tx * kNT;
   const int64_t col = col0 + wave * 32 + lc;
   const bool cvalid = col < CRS;
   const int64_t colc = cvalid ? col : col0;
@@ -222,10 +241,10 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_mfma(BwdwArgs a) {
   const int32_t c_lo = (int32_t)(col0 / RS);
   const int32_t c_hi = (int32_t)(min(col0 + kNT - 1, CRS - 1) / RS);
   const int32_t nch = c_hi - c_lo + 1;
-  const int32_t m0 = blockIdx.y * kMT;
+  const int32_t m0 = tl.ty * kMT;
 
   // reduction range of this segment
-  const int64_t g = blockIdx.z;
+  const int64_t g = tl.seg;
   const int64_t t_seg0 = g * (int64_t)a.G * a.L;
   const int64_t t_seg1 = min(t_seg0 + (int64_t)a.G * a.L, a.T);
   int64_t j = g * (int64_t)a.G;  // first chunk of the segment
@@ -466,6 +485,8 @@ __device__ __forceinline__ int window8_hi(const v4i& w, uint32_t s) {
 
 template <bool PARTIALS>
 __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band(BwdwArgs a) {
+  const BwdwTile tl = bwdw_tile(a);
+  if (tl.seg >= a.nseg) return;
   // two buffers, each [B band: nch_max channels x rows_max padded rows x 2 planes x Wpad][A: 16 KiB];
   // a B window read past the last row stays inside the A part that follows it
   __shared__ __align__(16) uint8_t smem[kBandLdsBytes];
@@ -476,15 +497,15 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band(BwdwArgs a) {
   const int lc = lane & 31;
   const int32_t RS = a.R * a.S;
   const int32_t CRS = a.C * RS;
-  const int32_t col0 = blockIdx.x * kNT;
+  const int32_t col0 = tl.tx * kNT;
   const int32_t col = col0 + wave * 32 + lc;
   const bool cvalid = col < CRS;
   const int32_t colc = cvalid ? col : col0;
   const int32_t c = colc / RS, rr = (colc % RS) / a.S;
   const uint32_t ss = (uint32_t)(colc % a.S);
   const int32_t c_lo = col0 / RS;
-  const int32_t m0 = blockIdx.y * kMT;
-  const int32_t g = blockIdx.z;
+  const int32_t m0 = tl.ty * kMT;
+  const int32_t g = tl.seg;
   const int32_t seg_len = a.G * a.L;
   const int32_t Ti = (int32_t)a.T;
   const int32_t t_seg0 = g * seg_len;
@@ -640,7 +661,13 @@ __device__ __forceinline__ void interleave_4x16() {
 
 template <bool PARTIALS>
 __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
+  const BwdwTile tl = bwdw_tile(a);
+  if (tl.seg >= a.nseg) return;
   __shared__ __align__(16) uint8_t smem[kBandLdsBytes];
+  // byte offset in a band buffer of each of the band's 16 runs of 8 indices
+  // (padded row of its output position relative to the band's first row,
+  // times the row stride, plus its column), two bands live
+  __shared__ __align__(16) int32_t s_ro[2][kSBT / 8];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
@@ -648,15 +675,15 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
   const int lc = lane & 31;
   const int32_t RS = a.R * a.S;
   const int32_t CRS = a.C * RS;
-  const int32_t col0 = blockIdx.x * kNT;
+  const int32_t col0 = tl.tx * kNT;
   const int32_t col = col0 + wave * 32 + lc;
   const bool cvalid = col < CRS;
   const int32_t colc = cvalid ? col : col0;
   const int32_t c = colc / RS, rr = (colc % RS) / a.S;
   const uint32_t ss = (uint32_t)(colc % a.S);
   const int32_t c_lo = col0 / RS;
-  const int32_t m0 = blockIdx.y * kMT;
-  const int32_t g = blockIdx.z;
+  const int32_t m0 = tl.ty * kMT;
+  const int32_t g = tl.seg;
   const int32_t seg_len = a.G * a.L;
   const int32_t Ti = (int32_t)a.T;
   const int32_t t_seg0 = g * seg_len;
@@ -671,7 +698,6 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
   // to be copied, advanced without divisions; the copy records each band's
   // position and first padded row for the reads that follow (two bands live).
   int32_t cn = t_seg0 / PQ, cp = (t_seg0 % PQ) / a.Q, cq = t_seg0 % a.Q;
-  int32_t pn0 = 0, pp0 = 0, pq0 = 0, pza0 = 0, pn1 = 0, pp1 = 0, pq1 = 0, pza1 = 0;
   const int32_t ppc = a.rows_max * row_b / 16;  // 16-byte pieces per channel
   auto issue_band = [&](int32_t b) {
     const int32_t t_b0 = t_seg0 + b * kSBT;
@@ -699,10 +725,13 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
           __builtin_amdgcn_global_load_lds((const void*)(srcc + k * 16), (lds_ptr_t)(dstc + k0 * 16), 16, 0, 0);
       }
     }
-    if (b & 1) {
-      pn1 = cn; pp1 = cp; pq1 = cq; pza1 = za;
-    } else {
-      pn0 = cn; pp0 = cp; pq0 = cq; pza0 = za;
+    if ((int32_t)threadIdx.x < kSBT / 8) {  // run u starts at output position (cn, cp, cq + 8u)
+      int32_t q = cq + 8 * (int32_t)threadIdx.x, p = cp, n = cn;
+      p += q / a.Q;
+      q %= a.Q;
+      n += p / a.P;
+      p %= a.P;
+      s_ro[b & 1][threadIdx.x] = (n * a.Hpad + p - za) * row_b + q;
     }
     cq += kSBT;
     while (cq >= a.Q) {
@@ -728,30 +757,18 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
     v4i a0h, a0l, a1h, a1l, wl0, wh0, wl1, wh1;
   };
   Raw R0, R1;
-  int32_t rn = 0, rp = 0, rq = 0, za = 0, rkbl = 0;  // read position (uniform)
+  int32_t rkbl = 0, rslot = 0;  // read position (uniform)
   uint32_t rbufA = 0, rbufB = 0;
   auto start_read_band = [&](int32_t bn) {
-    const int slot = bn & 1;
-    rn = slot ? pn1 : pn0;
-    rp = slot ? pp1 : pp0;
-    rq = slot ? pq1 : pq0;
-    za = slot ? pza1 : pza0;
-    rbufB = smem_base + (uint32_t)(slot * a.buf_bytes) + lane_b;
-    rbufA = smem_base + (uint32_t)(slot * a.buf_bytes + b_region);
+    rslot = bn & 1;
+    rbufB = smem_base + (uint32_t)(rslot * a.buf_bytes) + lane_b;
+    rbufA = smem_base + (uint32_t)(rslot * a.buf_bytes + b_region);
     rkbl = 0;
   };
   auto issue_reads = [&](Raw& r) {
-    int32_t ro[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      ro[u] = (rn * a.Hpad + rp - za) * row_b + rq;
-      rq += 8;
-      if (rq == a.Q) {
-        rq = 0;
-        if (++rp == a.P) { rp = 0; ++rn; }
-      }
-    }
-    const uint32_t to0 = (uint32_t)(half ? ro[2] : ro[0]), to1 = (uint32_t)(half ? ro[3] : ro[1]);
+    // runs 4 kbl + 2 half and 4 kbl + 2 half + 1 of the band: this lane's 16 indices
+    const int2 ro = *reinterpret_cast<const int2*>(&s_ro[rslot][4 * rkbl + 2 * half]);
+    const uint32_t to0 = (uint32_t)ro.x, to1 = (uint32_t)ro.y;
     const uint32_t ab = rbufA + (uint32_t)(rkbl * 64 * 64);
     lds_rd128(r.a0h, ab + rd_a0);
     lds_rd128(r.a0l, ab + rd_a1);
@@ -858,6 +875,13 @@ __global__ __launch_bounds__(64) void k_seg_reduce(const float* __restrict__ use
 }
 
 inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
+
+// 1-D grid of bwdw_tile; sets the tile counts in args.
+dim3 bwdw_grid(BwdwArgs& args, const BwdwPlan& p) {
+  args.ntx = (int32_t)((args.O / args.K + kNT - 1) / kNT);
+  args.nty = p.Mp / kMT;
+  return dim3((unsigned)(p.nseg * args.ntx * args.nty));
+}
 
 }  // namespace
 
@@ -972,7 +996,7 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.band_ch_stride = bl.ch_stride;
     args.buf_bytes = bl.buf_bytes;
     args.row_bytes = bl.row_bytes;
-    const dim3 grid((unsigned)((args.O / g.k + kNT - 1) / kNT), (unsigned)(p.Mp / kMT), (unsigned)p.nseg);
+    const dim3 grid = bwdw_grid(args, p);
     if (g.L == 64 && (p.T % 64) == 0) {  // every segment a whole number of two-block chunks
       if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<true>), grid, dim3(kThreads), 0, st, args);
       else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<false>), grid, dim3(kThreads), 0, st, args);
@@ -1017,7 +1041,7 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   args.L = g.L; args.G = g.G; args.nseg = p.nseg;
   args.band_bytes = (int32_t)p.band_bytes;
   args.band_ch_stride = p.band_ch_stride;
-  const dim3 grid((unsigned)((args.O / g.k + kNT - 1) / kNT), (unsigned)(p.Mp / kMT), (unsigned)p.nseg);
+  const dim3 grid = bwdw_grid(args, p);
   const bool masked = (g.L % 32) != 0;
   const size_t smem = (size_t)p.smem_bytes;
   if (masked) {

@@ -1481,6 +1481,8 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   const int32_t KB = a.KB, J = KB / 2, Cin = a.Cin;
   // the launcher guarantees outputs and the B workspace index below 2^31
   const int32_t NP = (int32_t)a.NP, Qo = a.Qo, PQ = a.Po * a.Qo;
+  // output scale exponent, read before any other memory operation is in flight
+  const int32_t e = __builtin_amdgcn_readfirstlane(a.ea->exp + a.eb->exp);
 
   // ---- filter digits of this 64-row tile: KB blocks x 256 pieces of 16 B, direct to LDS
   {
@@ -1500,11 +1502,12 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   // Byte offset of block kb (tap (r, s), channel block cb) from a pixel's operand:
   const int32_t cpb = Cin >> 5;  // blocks per filter tap
   const int32_t plane_bytes = a.Wp * 16;
-  if ((int32_t)threadIdx.x < KB) {
-    const int32_t kb = threadIdx.x, tap = kb / cpb, cb = kb - tap * cpb;
+  auto boff_of = [&](int32_t kb) {
+    const int32_t tap = kb / cpb, cb = kb - tap * cpb;
     const int32_t r = tap / a.S, sx = tap - r * a.S;
-    s_boff[kb] = a.rsign * (r * cpb * 4 * plane_bytes + sx * 16) + cb * 4 * plane_bytes;
-  }
+    return a.rsign * (r * cpb * 4 * plane_bytes + sx * 16) + cb * 4 * plane_bytes;
+  };
+  if ((int32_t)threadIdx.x < KB) s_boff[threadIdx.x] = boff_of(threadIdx.x);
 
   // ---- this workgroup's unit range (XCD x = workgroup id mod 8 gets adjacent ranges)
   const int32_t units = 2 * ((NP + 31) / 32);
@@ -1533,25 +1536,29 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  const int32_t e = a.ea->exp + a.eb->exp;
   const bool full_rows = a.M == a.Mp;  // every row of the 64-row tiles is an output channel
   uint32_t amax = 0;
-  wait_vmcnt<0>();  // filter digits landed for this lane
-  __syncthreads();  // ... and for every lane; the block offsets are written
+  // the stream's first chunk is requested while the filter digits are in
+  // flight; afterwards each block's registers are refilled with the block two
+  // ahead (the next unit's first blocks at a unit's last chunk, the last
+  // unit's first blocks again at the very end) as soon as its MFMAs have been
+  // issued
+  int32_t cur_pix = 0;
+  v4i b0h, b0l, b1h, b1l;
+  if (my_units > 0) {
+    cur_pix = pixel_off(unit_of(0));
+    load_b(b0h, b0l, cur_pix, 0);
+    load_b(b1h, b1l, cur_pix, boff_of(1));
+    wait_vmcnt<4>();  // filter digits landed for this lane (its four B loads may be in flight)
+  } else {
+    wait_vmcnt<0>();
+  }
+  // ... and for every lane, and the block offsets are written: a plain barrier
+  // (__syncthreads would also wait for the B loads in flight)
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
   if (my_units > 0) {
     const uint32_t ra_hi = swz(col, 2 * half) * 16, ra_lo = swz(col, 2 * half + 1) * 16;
-    int32_t cur_pix = pixel_off(unit_of(0));
-    // the stream's first chunk; afterwards each block's registers are refilled
-    // with the block two ahead (the next unit's first blocks at a unit's last
-    // chunk, the last unit's first blocks again at the very end) as soon as its
-    // MFMAs have been issued
-    v4i b0h, b0l, b1h, b1l;
-    {
-      const int2 bo = *reinterpret_cast<const int2*>(s_boff);
-      load_b(b0h, b0l, cur_pix, bo.x);
-      load_b(b1h, b1l, cur_pix, bo.y);
-    }
     for (int32_t unit = 0; unit < my_units; ++unit) {
       const int32_t u = unit_of(unit);
       const int32_t next_pix = unit + 1 < my_units ? pixel_off(unit_of(unit + 1)) : cur_pix;
