@@ -38,7 +38,7 @@ int prof_begin(int32_t id, hipStream_t st) {
   if (!g_prof_on || (int32_t)g_prof.size() >= g_prof_cap) return -1;
   ProfRec rec{id, pooled_event(), pooled_event()};
   if (!rec.start || !rec.stop) return -1;
-  hipEventRecord(rec.start, st);
+  (void)hipEventRecord(rec.start, st);
   g_prof.push_back(rec);
   return (int)g_prof.size() - 1;
 }
@@ -46,7 +46,7 @@ int prof_begin(int32_t id, hipStream_t st) {
 void prof_end(int slot, hipStream_t st) {
   if (slot < 0) return;
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  hipEventRecord(g_prof[slot].stop, st);
+  (void)hipEventRecord(g_prof[slot].stop, st);
 }
 
 // ------------------------------------------------------------- validation

@@ -863,6 +863,13 @@ __global__ __launch_bounds__(64) void k_seg_reduce(const float* __restrict__ use
   if (o >= O) return;
   float s = 0.f;
   int32_t g = 0;
+  for (; g + 32 <= nseg; g += 32) {  // 32 loads in flight per lane
+    float v[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) v[i] = useg[(int64_t)(g + i) * O + o];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) s += v[i];
+  }
   for (; g + 8 <= nseg; g += 8) {
     float v[8];
 #pragma unroll
