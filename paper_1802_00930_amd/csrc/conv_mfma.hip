@@ -122,11 +122,7 @@ __global__ __launch_bounds__(256) void k_prep_a(const int16_t* __restrict__ w, u
 // output row is stored contiguously.
 constexpr int kPrepBElems = 16384;  // int16 elements staged per pass (32 KiB)
 
-// PLANE: write the plane layout [n][u][cb][digit][half][v][16 B] instead
-// (CG even): the hi digits of channel group cg = 2 cb + half of column v at
-// ((cb * 4 + half) * Wp + v) * 16 within the row, the lo digits 2 Wp * 16
-// bytes further.
-template <bool VEC, bool PLANE>
+template <bool VEC>
 __global__ __launch_bounds__(256) void k_prep_b(const int16_t* __restrict__ src, uint8_t* __restrict__ xs,
                                                int32_t N, int32_t Cs, int32_t Hs, int32_t Wsrc, int32_t Hp,
                                                int32_t Wp, int32_t CG, int32_t top, int32_t left, int32_t dil_h,
@@ -183,17 +179,92 @@ __global__ __launch_bounds__(256) void k_prep_b(const int16_t* __restrict__ src,
           lo[i >> 2] |= lo_digit(a) << (8 * (i & 3));
         }
       }
-      if (PLANE) {
-        const int32_t cg = cg0 + cgl;
-        uint4* d = dst + ((cg >> 1) * 4 + (cg & 1)) * Wp + v;
-        d[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-        d[2 * Wp] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-      } else {
-        uint4* d = dst + (v * CG + cg0 + cgl) * 2;
-        d[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-        d[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      uint4* d = dst + (v * CG + cg0 + cgl) * 2;
+      d[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+      d[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+    }
+  }
+}
+
+// Plane layout Xs[n][u][cb][digit][half][v][16 B] (CG even): the hi digits of
+// channel group cg = 2 cb + half at column v sit at ((cb * 4 + half) * Wp + v)
+// * 16 within row u, the lo digits 2 * Wp * 16 bytes further; sources and
+// zero rows / columns as for k_prep_b.  Workgroup (row block, cg, n) stages
+// the group's 16 channels for up to kPlaneRows output rows in LDS as channel
+// pairs, [row][pair][w] of 32-bit (even | odd << 16) words: for one channel the
+// source rows of a block are adjacent (unit dilation), so the global reads are
+// long runs along w, the LDS writes and reads are consecutive words across
+// lanes (no bank conflicts), and the digits of each output row are written as
+// two contiguous runs of Wp * 16 bytes.
+constexpr int kPlaneRows = 8;
+constexpr int kPlaneElems = 16384;  // int16 elements staged (32 KiB)
+
+template <bool VEC>
+__global__ __launch_bounds__(256) void k_prep_plane(const int16_t* __restrict__ src, uint8_t* __restrict__ xs,
+                                                   int32_t Cs, int32_t Hs, int32_t Wsrc, int32_t Hp, int32_t Wp,
+                                                   int32_t CG, int32_t top, int32_t left, int32_t dil_h,
+                                                   int32_t dil_w, int32_t rb) {
+  extern __shared__ __align__(16) uint32_t tile2[];  // [rb][8][Wsrc] channel pairs
+  const int32_t u0 = blockIdx.x * rb, cg = blockIdx.y, n = blockIdx.z;
+  const int32_t nr = min(rb, Hp - u0);
+  const int64_t plane = (int64_t)Hs * Wsrc;
+  const int16_t* sbase = src + ((int64_t)n * Cs + cg * 16) * plane;
+  // source row of output row u0 + r, or -1 for a zero row
+  auto src_row = [&](int32_t r) {
+    const int32_t zu = u0 + r - top;
+    return (zu >= 0 && (zu % dil_h) == 0 && zu / dil_h < Hs) ? zu / dil_h : -1;
+  };
+  if (VEC) {  // 8 consecutive columns of one (row, channel pair) per thread
+    const int32_t W8 = Wsrc >> 3;
+    for (int32_t j = threadIdx.x; j < nr * 8 * W8; j += 256) {
+      const int32_t w8 = j % W8, rest = j / W8, pr = rest & 7, r = rest >> 3;
+      const int32_t h = src_row(r);
+      const int32_t c0 = cg * 16 + 2 * pr;
+      uint4 e = make_uint4(0u, 0u, 0u, 0u), o = make_uint4(0u, 0u, 0u, 0u);
+      if (h >= 0 && c0 < Cs) e = *reinterpret_cast<const uint4*>(sbase + 2 * pr * plane + (int64_t)h * Wsrc + w8 * 8);
+      if (h >= 0 && c0 + 1 < Cs)
+        o = *reinterpret_cast<const uint4*>(sbase + (2 * pr + 1) * plane + (int64_t)h * Wsrc + w8 * 8);
+      uint4* t = reinterpret_cast<uint4*>(tile2 + ((int64_t)r * 8 + pr) * Wsrc + w8 * 8);
+      t[0] = make_uint4(__builtin_amdgcn_perm(o.x, e.x, 0x05040100u), __builtin_amdgcn_perm(o.x, e.x, 0x07060302u),
+                        __builtin_amdgcn_perm(o.y, e.y, 0x05040100u), __builtin_amdgcn_perm(o.y, e.y, 0x07060302u));
+      t[1] = make_uint4(__builtin_amdgcn_perm(o.z, e.z, 0x05040100u), __builtin_amdgcn_perm(o.z, e.z, 0x07060302u),
+                        __builtin_amdgcn_perm(o.w, e.w, 0x05040100u), __builtin_amdgcn_perm(o.w, e.w, 0x07060302u));
+    }
+  } else {
+    for (int32_t j = threadIdx.x; j < nr * 8 * Wsrc; j += 256) {
+      const int32_t w = j % Wsrc, rest = j / Wsrc, pr = rest & 7, r = rest >> 3;
+      const int32_t h = src_row(r);
+      const int32_t c0 = cg * 16 + 2 * pr;
+      const uint32_t ev = (h >= 0 && c0 < Cs) ? (uint16_t)sbase[2 * pr * plane + (int64_t)h * Wsrc + w] : 0u;
+      const uint32_t ov = (h >= 0 && c0 + 1 < Cs) ? (uint16_t)sbase[(2 * pr + 1) * plane + (int64_t)h * Wsrc + w] : 0u;
+      tile2[((int64_t)r * 8 + pr) * Wsrc + w] = ev | (ov << 16);
+    }
+  }
+  __syncthreads();
+  const int64_t row_bytes = (int64_t)CG * 32 * Wp;
+  const int32_t off_hi = ((cg >> 1) * 4 + (cg & 1)) * Wp;  // in 16-byte units within the row
+  for (int32_t j = threadIdx.x; j < nr * Wp; j += 256) {
+    const int32_t v = j % Wp, r = j / Wp;
+    const int32_t zv = v - left;
+    const bool in = src_row(r) >= 0 && zv >= 0 && (zv % dil_w) == 0 && zv / dil_w < Wsrc;
+    uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+    if (in) {
+      const uint32_t* tp = tile2 + (int64_t)r * 8 * Wsrc + zv / dil_w;
+#pragma unroll
+      for (int pr = 0; pr < 8; ++pr) {
+        const uint32_t wv = tp[pr * Wsrc];
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+          const int i = 2 * pr + h2;
+          const int32_t a = (int32_t)(int16_t)(wv >> (16 * h2));
+          hi[i >> 2] |= hi_digit(a) << (8 * (i & 3));
+          lo[i >> 2] |= lo_digit(a) << (8 * (i & 3));
+        }
       }
     }
+    uint4* d = reinterpret_cast<uint4*>(xs + ((int64_t)n * Hp + u0 + r) * row_bytes) + off_hi + v;
+    d[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+    d[2 * Wp] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
   }
 }
 
@@ -1694,17 +1765,23 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
     const bool vec = (Wsrc % 8) == 0 && (reinterpret_cast<uintptr_t>(a) & 15) == 0;
     const int32_t cgc = std::max(1, std::min(p.CG, kPrepBElems / (16 * Wsrc)));  // as in the kernel
     const size_t lds = (size_t)cgc * 16 * Wsrc * 2;
-#define DFP_PREP_B(V, PL)                                                                                   \
-  DFP_LAUNCH(K_XPREP, (k_prep_b<V, PL>), dim3((unsigned)(g.n * p.Hp)), dim3(256), lds, st, a, xs, g.n, Cs, Hs, \
-             Wsrc, p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w)
     if (plane) {
-      if (vec) DFP_PREP_B(true, true);
-      else DFP_PREP_B(false, true);
+      const int32_t rb = std::max(1, std::min(kPlaneRows, kPlaneElems / (16 * Wsrc)));
+      const dim3 grid((unsigned)((p.Hp + rb - 1) / rb), (unsigned)p.CG, (unsigned)g.n);
+      const size_t plds = (size_t)rb * Wsrc * 16 * 2;
+      if (vec)
+        DFP_LAUNCH(K_XPREP, k_prep_plane<true>, grid, dim3(256), plds, st, a, xs, Cs, Hs, Wsrc, p.Hp, p.Wp, p.CG,
+                   p.top, p.left, p.dil_h, p.dil_w, rb);
+      else
+        DFP_LAUNCH(K_XPREP, k_prep_plane<false>, grid, dim3(256), plds, st, a, xs, Cs, Hs, Wsrc, p.Hp, p.Wp, p.CG,
+                   p.top, p.left, p.dil_h, p.dil_w, rb);
+    } else if (vec) {
+      DFP_LAUNCH(K_XPREP, k_prep_b<true>, dim3((unsigned)(g.n * p.Hp)), dim3(256), lds, st, a, xs, g.n, Cs, Hs, Wsrc,
+                 p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w);
     } else {
-      if (vec) DFP_PREP_B(true, false);
-      else DFP_PREP_B(false, false);
+      DFP_LAUNCH(K_XPREP, k_prep_b<false>, dim3((unsigned)(g.n * p.Hp)), dim3(256), lds, st, a, xs, g.n, Cs, Hs, Wsrc,
+                 p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w);
     }
-#undef DFP_PREP_B
   }
   ConvMfmaArgs args{};
   args.xs = xs;
