@@ -98,6 +98,28 @@ def test_bwd_wt_band_shapes(shape, L, G):
     run_all(shape, L, G=G)
 
 
+# 32-channel blocks with reductions a multiple of 64 at L = 64: the
+# four-waves-per-SIMD kernel over the plane layout takes the forward (and the
+# backward-data where K is a multiple of 32), across one-chunk reductions
+# (T = 64), several 64-row tiles with a ragged last one, the largest resident
+# filter (36 blocks; its backward-data, 54 blocks, goes to another kernel),
+# strides, and fewer output pixels than one wave's unit.
+W16_SHAPES = [
+    (2, 64, 7, 7, 64, 1, 1, 1, 0),
+    (1, 64, 13, 13, 200, 3, 3, 1, 1),
+    (2, 128, 5, 5, 192, 3, 3, 1, 1),
+    (2, 64, 14, 14, 64, 3, 3, 2, 1),
+    (2, 64, 14, 14, 128, 1, 1, 2, 0),
+    (1, 64, 2, 3, 64, 3, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", W16_SHAPES)
+@pytest.mark.parametrize("partials", [True, False])
+def test_w16_shapes(shape, partials):
+    run_all(shape, 64, path=dfp.PATH_MFMA, partials=partials)
+
+
 @pytest.mark.parametrize("G", [1, 2, 3, 50])
 def test_bwd_wt_segments(G):
     run_all((4, 16, 12, 12, 8, 3, 3, 1, 1), 16, G=G)
