@@ -28,6 +28,8 @@ struct BwdwArgs {
   int32_t K, Mp, C, R, S, P, Q, sh, sw, Hpad, Wpad, NH, L, G, nseg, band_bytes, band_ch_stride;
   int32_t rows_max, nch_max, buf_bytes, row_bytes;  // band kernel: rows / channels per band, buffer and row bytes
   int32_t ntx, nty;  // column tiles and row tiles per segment (the grid is 1-D, see bwdw_grid)
+  uint32_t ad_bytes, xb_bytes;  // sizes of the two digit tensors (band kernels: buffer bounds)
+  FastDiv div_q, div_p;         // division by Q and by P (band-table positions)
 };
 
 BwdwPlan plan_bwdw_mfma(const Geom& g);

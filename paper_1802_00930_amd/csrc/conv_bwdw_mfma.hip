@@ -416,6 +416,11 @@ constexpr int kBandLdsBytes = 76 * 1024;             // two buffers; two workgro
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
+// Raw buffer resource over [p, p + bytes) (offsets past the end read zeros).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint8_t*)p;
 }
@@ -699,6 +704,15 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
   // position and first padded row for the reads that follow (two bands live).
   int32_t cn = t_seg0 / PQ, cp = (t_seg0 % PQ) / a.Q, cq = t_seg0 % a.Q;
   const int32_t ppc = a.rows_max * row_b / 16;  // 16-byte pieces per channel
+  // Every copy below is a buffer load of a per-lane offset fixed for the whole
+  // kernel plus a uniform offset, so the address arithmetic stays scalar.
+  // A slot j*256 + tid holds piece (tid & 3) ^ ((tid >> 4) & 3) of row tid >> 2
+  // of block kb0 + j.
+  const __amdgpu_buffer_rsrc_t rs_a = make_rsrc(a.ad, a.ad_bytes);
+  const __amdgpu_buffer_rsrc_t rs_b = make_rsrc(a.xb, a.xb_bytes);
+  const uint32_t a_lane = (uint32_t)((m0 + (threadIdx.x >> 2)) * 64 + (((threadIdx.x & 3) ^ ((threadIdx.x >> 4) & 3)) * 16));
+  const uint32_t a_block = (uint32_t)a.Mp * 64;
+  const uint32_t b_lane = (uint32_t)lane * 16;
   auto issue_band = [&](int32_t b) {
     const int32_t t_b0 = t_seg0 + b * kSBT;
     uint8_t* dstB = smem + (b & 1) * a.buf_bytes;
@@ -706,23 +720,21 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
     const int32_t kb0 = t_b0 / 32;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int32_t slot = j * 256 + threadIdx.x;
-      const int32_t row = slot >> 2;
-      const int32_t piece = (slot & 3) ^ ((row >> 2) & 3);
-      const int32_t kb = min(kb0 + (row >> 6), last_kb);
-      const uint8_t* src = a.ad + ((int64_t)kb * a.Mp + m0 + (row & 63)) * 64 + piece * 16;
-      __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(dstA + (j * 256 + wave_u * 64) * 16), 16, 0, 0);
+      const int32_t kb = min(kb0 + j, last_kb);  // blocks past the segment reload a valid one (unused)
+      const uint32_t so = __builtin_amdgcn_readfirstlane((uint32_t)kb * a_block);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_a, (lds_ptr_t)(dstA + (j * 256 + wave_u * 64) * 16), 16, a_lane, so,
+                                               0, 0);
     }
     // B: rows [za, za + rows_max) of each channel (wave w copies channels w, w + 4, ...)
-    const int32_t za = min(cn * a.Hpad + cp, a.NH - a.rows_max);
+    const int32_t za = __builtin_amdgcn_readfirstlane(min(cn * a.Hpad + cp, a.NH - a.rows_max));
     for (int32_t cc = wave_u; cc < a.nch_max; cc += kThreads / 64) {
       const int32_t ch = min(c_lo + cc, a.C - 1);
-      const uint8_t* srcc = a.xb + ((int64_t)ch * a.NH + za) * row_b;
+      const uint32_t soc = (uint32_t)((ch * a.NH + za) * row_b);
       uint8_t* dstc = dstB + cc * a.band_ch_stride;
       for (int32_t k0 = 0; k0 < ppc; k0 += 64) {
-        const int32_t k = k0 + lane;
-        if (k < ppc)
-          __builtin_amdgcn_global_load_lds((const void*)(srcc + k * 16), (lds_ptr_t)(dstc + k0 * 16), 16, 0, 0);
+        if (lane < ppc - k0)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_b, (lds_ptr_t)(dstc + k0 * 16), 16, b_lane,
+                                                   __builtin_amdgcn_readfirstlane(soc + (uint32_t)k0 * 16), 0, 0);
       }
     }
     if ((int32_t)threadIdx.x < kSBT / 8) {  // run u starts at output position (cn, cp, cq + 8u)
@@ -738,6 +750,9 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
       cq -= a.Q;
       if (++cp == a.P) { cp = 0; ++cn; }
     }
+    cn = __builtin_amdgcn_readfirstlane(cn);
+    cp = __builtin_amdgcn_readfirstlane(cp);
+    cq = __builtin_amdgcn_readfirstlane(cq);
   };
 
   Acc3 acc0, acc1;
@@ -856,6 +871,228 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
   }
 }
 
+// Eight-wave variant of the band kernel for two-block chunks: the same bands
+// and workgroup tile (128 columns x 64 rows), but each wave owns one 32 x 32
+// output tile (row tile wave / 4, column group wave % 4), so every wave needs
+// at most 128 VGPRs and two workgroups give four waves per SIMD to hide the
+// LDS and matrix-core latencies of the per-block chain.  Per chunk the eight
+// MFMAs are issued, then the reads of the next chunk, then the conversion.
+// The operand reads are ordinary LDS loads (the compiler places their waits
+// and knows which registers are still being filled); the band copies are
+// issued from inline assembly and waited for before each band's barrier.
+// One 16-byte direct-to-LDS buffer load (lane i writes lds + 16 i) issued from
+// inline assembly: the compiler then neither tracks it nor makes its own LDS
+// reads wait for it (it cannot tell which buffer a copy targets); the caller
+// waits with s_waitcnt vmcnt before a barrier.  M0 carries the LDS address;
+// the kernels that use this helper issue no other instruction that reads M0.
+__device__ __forceinline__ void dma16(const v4i& rsrc, uint32_t lds, uint32_t voff, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(rsrc), "s"(soff)
+               : "memory", "m0");
+}
+// Raw buffer resource words (uniform) over [p, p + bytes).
+__device__ __forceinline__ v4i rsrc_words(const void* p, uint32_t bytes) {
+  const uint64_t b = (uint64_t)(uintptr_t)p;
+  return v4i{__builtin_amdgcn_readfirstlane((int)(uint32_t)b), __builtin_amdgcn_readfirstlane((int)(uint32_t)(b >> 32)),
+             __builtin_amdgcn_readfirstlane((int)bytes), 0x00020000};
+}
+
+// Lane id (0..63) computed afresh at each use: the asm is volatile, so the
+// compiler recomputes it rather than keeping it (or values derived from it)
+// in a register across a loop.
+__device__ __forceinline__ int32_t fresh_lane() {
+  int32_t l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
+constexpr int kThreadsW8 = 512;
+constexpr int kBandBufBytes = kBandLdsBytes / 2;
+
+template <bool PARTIALS>
+__global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_band_w8(BwdwArgs a) {
+  const BwdwTile tl = bwdw_tile(a);
+  if (tl.seg >= a.nseg) return;
+  // output scale exponent, read before any copy is in flight (the compiler
+  // would otherwise wait for a load still pending, and with it the copies)
+  const int32_t e = __builtin_amdgcn_readfirstlane(a.ea->exp + a.eb->exp);
+  __shared__ __align__(16) uint8_t sb0[kBandBufBytes];
+  __shared__ __align__(16) uint8_t sb1[kBandBufBytes];
+  // byte offset in a band buffer of each of the band's 16 runs of 8 indices
+  __shared__ __align__(16) int32_t ro0[kSBT / 8];
+  __shared__ __align__(16) int32_t ro1[kSBT / 8];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int rt = wave >> 2;  // row tile
+  const int half = lane >> 5;
+  const int lc = lane & 31;
+  const int32_t RS = a.R * a.S;
+  const int32_t CRS = a.C * RS;
+  const int32_t col0 = tl.tx * kNT;
+  const int32_t col = col0 + (wave & 3) * 32 + lc;
+  const bool cvalid = col < CRS;
+  const int32_t colc = cvalid ? col : col0;
+  const int32_t c = colc / RS, rr = (colc % RS) / a.S;
+  const uint32_t ss = (uint32_t)(colc % a.S);
+  const int32_t c_lo = col0 / RS;
+  const int32_t m0 = tl.ty * kMT;
+  const int32_t g = tl.seg;
+  const int32_t seg_len = a.G * a.L;
+  const int32_t Ti = (int32_t)a.T;
+  const int32_t t_seg0 = g * seg_len;
+  const int32_t t_seg1 = min(t_seg0 + seg_len, Ti);
+  const int32_t nbands = (t_seg1 - t_seg0 + kSBT - 1) / kSBT;
+  const int32_t NB = (t_seg1 - t_seg0) / 32;  // blocks of the segment (whole chunks)
+  const int32_t row_b = a.row_bytes;
+  const int32_t b_region = a.buf_bytes - kBandABytes;
+  const int32_t last_kb = t_seg1 / 32 - 1;
+
+  // band cursor (n, p, q) of the next band to copy, advanced without divisions
+  int32_t cn = t_seg0 / (a.P * a.Q), cp = (t_seg0 % (a.P * a.Q)) / a.Q, cq = t_seg0 % a.Q;
+  const int32_t ppc = a.rows_max * row_b / 16;  // 16-byte pieces per channel
+  // Copies are buffer loads of a per-lane offset fixed for the kernel plus a
+  // uniform offset.  A slot j*512 + tid holds piece (tid & 3) ^ ((tid >> 4) & 3)
+  // of row (tid >> 2) & 63 of band block 2j + (tid >> 8).
+  const v4i rs_a = rsrc_words(a.ad, a.ad_bytes);
+  const v4i rs_b = rsrc_words(a.xb, a.xb_bytes);
+  const uint32_t a_block = (uint32_t)a.Mp * 64;
+  auto issue_band = [&](int32_t b, uint8_t* buf, int32_t* ro) __attribute__((always_inline)) {
+    const int32_t t_b0 = t_seg0 + b * kSBT;
+    uint8_t* dstA = buf + b_region;
+    const int32_t kb0 = t_b0 / 32;
+    // lane values recomputed here rather than held in registers across the band
+    const int32_t ln = fresh_lane();
+    const int32_t tid = wave * 64 + ln;
+    const uint32_t a_lane = (uint32_t)((m0 + ((tid >> 2) & 63)) * 64 + (((tid & 3) ^ ((tid >> 4) & 3)) * 16));
+    const uint32_t b_lane = (uint32_t)ln * 16;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int32_t kb = min(kb0 + 2 * j + (wave >> 2), last_kb);  // blocks past the segment reload a valid one
+      const uint32_t so = __builtin_amdgcn_readfirstlane((uint32_t)kb * a_block);
+      dma16(rs_a, lds_addr(dstA + (j * 512 + wave * 64) * 16), a_lane, so);
+    }
+    const int32_t za = __builtin_amdgcn_readfirstlane(min(cn * a.Hpad + cp, a.NH - a.rows_max));
+    for (int32_t cc = wave; cc < a.nch_max; cc += kThreadsW8 / 64) {
+      const int32_t ch = min(c_lo + cc, a.C - 1);
+      const uint32_t soc = (uint32_t)((ch * a.NH + za) * row_b);
+      uint8_t* dstc = buf + cc * a.band_ch_stride;
+      for (int32_t k0 = 0; k0 < ppc; k0 += 64) {
+        if (ln < ppc - k0)
+          dma16(rs_b, lds_addr(dstc + k0 * 16), b_lane, __builtin_amdgcn_readfirstlane(soc + (uint32_t)k0 * 16));
+      }
+    }
+    if (tid < kSBT / 8) {  // run u starts at output position (cn, cp, cq + 8u)
+      int32_t q = cq + 8 * tid, p = cp, n = cn;
+      const int32_t dq = (int32_t)fdiv((uint32_t)q, a.div_q);
+      p += dq;
+      q -= dq * a.Q;
+      const int32_t dp = (int32_t)fdiv((uint32_t)p, a.div_p);
+      n += dp;
+      p -= dp * a.P;
+      ro[tid] = (n * a.Hpad + p - za) * row_b + q;
+    }
+    cq += kSBT;
+    while (cq >= a.Q) {
+      cq -= a.Q;
+      if (++cp == a.P) { cp = 0; ++cn; }
+    }
+    cn = __builtin_amdgcn_readfirstlane(cn);
+    cp = __builtin_amdgcn_readfirstlane(cp);
+    cq = __builtin_amdgcn_readfirstlane(cq);
+  };
+
+  Acc3 acc;
+  float sum[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) sum[v] = 0.f;
+  const int32_t j0 = g * a.G;  // first chunk of the segment
+  const uint32_t lane_b = (uint32_t)((c - c_lo) * a.band_ch_stride + rr * row_b);
+  const uint32_t rd_a0 = (uint32_t)(swz(lc, 2 * half) * 16 + rt * 2048);
+  const uint32_t rd_a1 = (uint32_t)(swz(lc, 2 * half + 1) * 16 + rt * 2048);
+  const int32_t mrow = m0 + 32 * rt + 4 * half;
+
+  // Operand reads are inline-assembly LDS reads with explicit waits (wait_raw)
+  // placed one block after the issue.  Between a read and its wait the
+  // compiler takes the destination registers as already written: the kernel
+  // relies on it neither copying nor spilling them there (the forward-only
+  // variant built here uses no scratch; the partials variant runs another
+  // kernel).
+  struct Raw {
+    v4i ah, al, wl0, wh0, wl1, wh1;
+  };
+  Raw R0, R1;
+  auto read_block = [&](Raw& r, const uint8_t* buf, const int32_t* ro, int32_t k) __attribute__((always_inline)) {
+    const int2 o = *reinterpret_cast<const int2*>(ro + 4 * k + 2 * half);
+    const uint32_t ab = lds_addr(buf + b_region + k * 4096);
+    const uint32_t rb = lds_addr(buf) + lane_b;
+    lds_rd128(r.ah, ab + rd_a0);
+    lds_rd128(r.al, ab + rd_a1);
+    lds_rd2x64(r.wl0, rb + (uint32_t)o.x);
+    lds_rd2x64(r.wh0, rb + (uint32_t)o.x + a.Wpad);
+    lds_rd2x64(r.wl1, rb + (uint32_t)o.y);
+    lds_rd2x64(r.wh1, rb + (uint32_t)o.y + a.Wpad);
+  };
+  auto wait_raw = [&](Raw& r) __attribute__((always_inline)) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(r.wl0), "+v"(r.wh0), "+v"(r.wl1), "+v"(r.wh1), "+v"(r.ah), "+v"(r.al)
+                 :
+                 : "memory");
+  };
+  auto operand_b = [&](const v4i& w0, const v4i& w1) __attribute__((always_inline)) {
+    return v4i{window8_lo(w0, ss), window8_hi(w0, ss), window8_lo(w1, ss), window8_hi(w1, ss)};
+  };
+  // One band (two chunks, or one at the end of a segment of an odd number of
+  // chunk pairs) from cur.  Block k + 1 is read while block k is multiplied;
+  // the first read of the next band comes from nxt after the band barrier,
+  // and the band after next is then copied into cur.
+  auto do_band = [&](int32_t b, uint8_t* cur, int32_t* rcur, const uint8_t* nxt, const int32_t* rnxt)
+                     __attribute__((always_inline)) {
+    const int32_t nch = min(2, (NB - 4 * b) >> 1);
+    for (int32_t ch = 0; ch < nch; ++ch) {
+      wait_raw(R0);
+      read_block(R1, cur, rcur, 2 * ch + 1);
+      mfma_tile(acc, R0.ah, R0.al, operand_b(R0.wh0, R0.wh1), operand_b(R0.wl0, R0.wl1), true);
+      wait_raw(R1);
+      if (ch + 1 < nch) {
+        read_block(R0, cur, rcur, 2 * ch + 2);
+      } else if (b + 1 < nbands) {
+        // every wave has read band b and band b + 1 has landed; band b + 2 may
+        // then overwrite band b
+        wait_vmcnt<0>();
+        __syncthreads();
+        if (b + 2 < nbands) issue_band(b + 2, cur, rcur);
+        read_block(R0, nxt, rnxt, 0);
+      }
+      mfma_tile(acc, R1.ah, R1.al, operand_b(R1.wh0, R1.wh1), operand_b(R1.wl0, R1.wl1), false);
+      flush_tile<PARTIALS>(acc, sum, j0 + 2 * b + ch, a.partials, a.O, colc, CRS, mrow, a.K, cvalid);
+    }
+  };
+
+  issue_band(0, sb0, ro0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  if (nbands > 1) issue_band(1, sb1, ro1);
+  read_block(R0, sb0, ro0, 0);
+  for (int32_t b = 0; b < nbands; b += 2) {
+    do_band(b, sb0, ro0, sb1, ro1);
+    if (b + 1 < nbands) do_band(b + 1, sb1, ro1, sb0, ro0);
+  }
+
+  const int32_t ln = fresh_lane();
+  const int32_t ocol = col0 + (wave & 3) * 32 + (ln & 31);
+  const int32_t orow = m0 + 32 * rt + 4 * (ln >> 5);
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int32_t m = orow + 8 * (v >> 2) + (v & 3);
+    if (ocol < CRS && m < a.K) {
+      const int32_t o = m * CRS + ocol;
+      if (a.nseg == 1) a.out[o] = ldexpf(sum[v], e);
+      else a.useg[(int64_t)g * a.O + o] = sum[v];
+    }
+  }
+}
+
 // dW = 2^e * (((U_0 + U_1) + U_2) + ...), segment order.
 __global__ __launch_bounds__(64) void k_seg_reduce(const float* __restrict__ useg, float* __restrict__ out, int64_t O,
                                                   int32_t nseg, const dfp_scale* ea, const dfp_scale* eb) {
@@ -968,7 +1205,9 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
                g.p * g.q, (int32_t)p.T, (int32_t)p.KBT);
   }
   const BandLayout bl = band_layout(g, p);
-  if (bl.buf_bytes > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) {
+  // the band kernels address both digit tensors with 32-bit buffer offsets
+  if (bl.buf_bytes > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 && p.ad_bytes < (1ll << 31) &&
+      p.xp_bytes < (1ll << 31)) {
     uint8_t* xb = reinterpret_cast<uint8_t*>(xp);  // same workspace region as the pair layout
     const int64_t per_c = (int64_t)g.n * p.Hpad * (p.Wpad / 8);
     const dim3 grid_xb((unsigned)((per_c + 255) / 256), (unsigned)g.c);
@@ -1003,10 +1242,17 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.band_ch_stride = bl.ch_stride;
     args.buf_bytes = bl.buf_bytes;
     args.row_bytes = bl.row_bytes;
+    args.ad_bytes = (uint32_t)p.ad_bytes;
+    args.div_q = make_fastdiv((uint32_t)g.q);
+    args.div_p = make_fastdiv((uint32_t)g.p);
+    args.xb_bytes = (uint32_t)p.xp_bytes;
     const dim3 grid = bwdw_grid(args, p);
     if (g.L == 64 && (p.T % 64) == 0) {  // every segment a whole number of two-block chunks
+      // the partials variant of the eight-wave kernel would spill registers
+      // its inline-assembly reads are still filling: partials use the
+      // two-tile kernel (same chunks, same order of additions)
       if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<true>), grid, dim3(kThreads), 0, st, args);
-      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<false>), grid, dim3(kThreads), 0, st, args);
+      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false>), grid, dim3(kThreadsW8), 0, st, args);
     } else {
       if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<true>), grid, dim3(kThreads), 0, st, args);
       else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<false>), grid, dim3(kThreads), 0, st, args);

@@ -98,6 +98,15 @@ def test_bwd_wt_band_shapes(shape, L, G):
     run_all(shape, L, G=G)
 
 
+# Without partials, L = 64 runs the eight-wave band kernel (with partials the
+# two-tile one): segments of one chunk, of an odd number of chunks (a last band
+# of one chunk), several bands, one segment per layer.
+@pytest.mark.parametrize("shape", BAND_SHAPES + [(2, 64, 56, 56, 64, 3, 3, 1, 1)])
+@pytest.mark.parametrize("G", [0, 1, 3, 5, 10 ** 6])
+def test_bwd_wt_band_no_partials(shape, G):
+    run_all(shape, 64, G=G, partials=False)
+
+
 # 32-channel blocks with reductions a multiple of 64 at L = 64: the
 # four-waves-per-SIMD kernel over the plane layout takes the forward (and the
 # backward-data where K is a multiple of 32), across one-chunk reductions
