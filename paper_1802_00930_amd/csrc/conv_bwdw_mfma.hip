@@ -41,10 +41,15 @@ __device__ __forceinline__ uint32_t lo_digit(int32_t a) { return (uint32_t)a & 0
 // contiguous; each thread reads 16 consecutive reduction indices of one plane,
 // as two 16-byte loads when they lie in one image and are aligned.  Every
 // index fits 32 bits (dy has fewer than 2^31 elements).
-__global__ __launch_bounds__(256) void k_prep_dy(const int16_t* __restrict__ dy, uint8_t* __restrict__ ad, int32_t K,
-                                                int32_t Mp, int32_t PQ, int32_t T, int32_t KBT) {
-  const int32_t idx = blockIdx.x * 256 + threadIdx.x;
-  if (idx >= KBT * Mp * 2) return;
+struct DyPrep {
+  const int16_t* dy;
+  uint8_t* ad;
+  int32_t K, Mp, PQ, T, KBT;
+};
+__device__ __forceinline__ void prep_dy_item(const DyPrep& q, int32_t idx) {
+  const int16_t* __restrict__ dy = q.dy;
+  const int32_t K = q.K, Mp = q.Mp, PQ = q.PQ, T = q.T;
+  if (idx >= q.KBT * Mp * 2) return;
   const int32_t half = idx & 1;
   const int32_t m = (idx >> 1) % Mp;
   const int32_t kb = (idx >> 1) / Mp;
@@ -76,10 +81,11 @@ __global__ __launch_bounds__(256) void k_prep_dy(const int16_t* __restrict__ dy,
       }
     }
   }
-  uint4* dst = reinterpret_cast<uint4*>(ad + (int64_t)idx * 32);
+  uint4* dst = reinterpret_cast<uint4*>(q.ad + (int64_t)idx * 32);
   dst[0] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
   dst[1] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
 }
+__global__ __launch_bounds__(256) void k_prep_dy(DyPrep q) { prep_dy_item(q, blockIdx.x * 256 + threadIdx.x); }
 
 // XP[c][n*Hpad + u][v] = (lo | hi << 8) of x[n][c][u - ph][v - pw], zero outside.
 // Grid (rows of channel c, c): one thread per 8 consecutive pairs of a row
@@ -433,8 +439,12 @@ __device__ __forceinline__ int swz(int row, int piece) { return row * 4 + (piece
 template <int PW>
 __global__ __launch_bounds__(256) void k_prep_xb(const int16_t* __restrict__ x, uint8_t* __restrict__ xb, int32_t N,
                                                 int32_t C, int32_t H, int32_t W, int32_t Hpad, int32_t Wpad,
-                                                int32_t ph, int32_t row_bytes) {
+                                                int32_t ph, int32_t row_bytes, DyPrep q) {
   const int32_t c = blockIdx.y;
+  if (c >= C) {  // rows of workgroups past the channels prepare the dy digits
+    prep_dy_item(q, ((c - C) * gridDim.x + blockIdx.x) * 256 + threadIdx.x);
+    return;
+  }
   const int32_t i = blockIdx.x * 256 + threadIdx.x;  // (n * Hpad + u) * W8 + v8
   const int32_t W8 = Wpad >> 3;
   if (i >= N * Hpad * W8) return;
@@ -1199,30 +1209,33 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   uint8_t* ad = base;
   uint16_t* xp = reinterpret_cast<uint16_t*>(base + p.ad_bytes);
   float* useg = reinterpret_cast<float*>(base + p.ad_bytes + p.xp_bytes);
-  {
-    const int64_t total = p.KBT * p.Mp * 2;
-    DFP_LAUNCH(K_WPREP, k_prep_dy, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, dy, ad, g.k, p.Mp,
-               g.p * g.q, (int32_t)p.T, (int32_t)p.KBT);
-  }
+  const DyPrep dq{dy, ad, g.k, p.Mp, g.p * g.q, (int32_t)p.T, (int32_t)p.KBT};
+  const int64_t dy_blocks = (p.KBT * p.Mp * 2 + 255) / 256;
   const BandLayout bl = band_layout(g, p);
   // the band kernels address both digit tensors with 32-bit buffer offsets
   if (bl.buf_bytes > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 && p.ad_bytes < (1ll << 31) &&
       p.xp_bytes < (1ll << 31)) {
     uint8_t* xb = reinterpret_cast<uint8_t*>(xp);  // same workspace region as the pair layout
+    // one launch prepares both operands: rows of workgroups 0 .. C-1 the x
+    // planes, the rows after them the dy digits
     const int64_t per_c = (int64_t)g.n * p.Hpad * (p.Wpad / 8);
-    const dim3 grid_xb((unsigned)((per_c + 255) / 256), (unsigned)g.c);
+    const int64_t gx = (per_c + 255) / 256;
+    const int64_t gy_dy = (dy_blocks + gx - 1) / gx;
+    const bool merged = g.c + gy_dy <= 65535;  // grid y limit; else dy gets its own launch
+    if (!merged) DFP_LAUNCH(K_WPREP, k_prep_dy, dim3((unsigned)dy_blocks), dim3(256), 0, st, dq);
+    const dim3 grid_xb((unsigned)gx, (unsigned)(g.c + (merged ? gy_dy : 0)));
     if (g.pw == 0)
       DFP_LAUNCH(K_XPREP, k_prep_xb<0>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
-                 bl.row_bytes);
+                 bl.row_bytes, dq);
     else if (g.pw == 1)
       DFP_LAUNCH(K_XPREP, k_prep_xb<1>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
-                 bl.row_bytes);
+                 bl.row_bytes, dq);
     else if (g.pw == 2)
       DFP_LAUNCH(K_XPREP, k_prep_xb<2>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
-                 bl.row_bytes);
+                 bl.row_bytes, dq);
     else
       DFP_LAUNCH(K_XPREP, k_prep_xb<3>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
-                 bl.row_bytes);
+                 bl.row_bytes, dq);
     BwdwArgs args{};
     args.ad = ad;
     args.xb = xb;
@@ -1263,6 +1276,7 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     }
     return DFP_OK;
   }
+  DFP_LAUNCH(K_WPREP, k_prep_dy, dim3((unsigned)dy_blocks), dim3(256), 0, st, dq);
   {
     const int64_t per_c = (int64_t)g.n * p.Hpad * (p.Wpad / 8);
     const dim3 grid_xp((unsigned)((per_c + 255) / 256), (unsigned)g.c);

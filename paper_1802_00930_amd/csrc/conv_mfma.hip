@@ -60,57 +60,65 @@ __device__ __forceinline__ uint32_t lo_digit(int32_t a) { return (uint32_t)a & 0
 // one (kb, m, half) piece: the hi and lo words it packs land 16 bytes apart.
 // The same launch clears the output scale and writes the per-block B offset
 // table of the main kernels.
-__global__ __launch_bounds__(256) void k_prep_a(const int16_t* __restrict__ w, uint8_t* __restrict__ ws,
-                                               int32_t M, int32_t Mp, int32_t Cin, int32_t R, int32_t S,
-                                               int32_t T, int32_t KB, int32_t transposed, int32_t Cw,
-                                               dfp_scale* so, int2* boff, int32_t tap_row_bytes,
-                                               int32_t tap_col_bytes) {
-  const int32_t idx = blockIdx.x * 256 + threadIdx.x;  // ((kb, m, half), quarter)
-  if (so && idx == 0) {  // the output scale starts empty; the conv epilogue raises its max
-    so->amax_bits = 0u;
-    so->flags = 0u;
+struct PrepAArgs {
+  const int16_t* w;
+  uint8_t* ws;
+  int32_t M, Mp, Cin, R, S, T, KB, transposed, Cw;
+  dfp_scale* so;
+  int2* boff;
+  int32_t tap_row_bytes, tap_col_bytes;
+};
+
+// Work item idx of the filter-digit preparation: ((kb, m, half), quarter), plus
+// the block offset table (idx < KB) and the output-scale reset (idx 0).
+__device__ __forceinline__ void prep_a_item(const PrepAArgs& a, int32_t idx) {
+  if (a.so && idx == 0) {  // the output scale starts empty; the conv epilogue raises its max
+    a.so->amax_bits = 0u;
+    a.so->flags = 0u;
   }
-  if (idx < KB) {
+  if (idx < a.KB) {
     // block idx covers t0 .. t0+31; each 16-index half is one channel group of one tap
     // (Cin is a multiple of 16 wherever the table is read); indices past T read offset 0
     int32_t o[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int32_t t = idx * 32 + 16 * h;
-      const int32_t tap = t / Cin, ci = t % Cin;
-      o[h] = t < T ? (tap / S) * tap_row_bytes + (tap % S) * tap_col_bytes + (ci >> 4) * 32 : 0;
+      const int32_t tap = t / a.Cin, ci = t % a.Cin;
+      o[h] = t < a.T ? (tap / a.S) * a.tap_row_bytes + (tap % a.S) * a.tap_col_bytes + (ci >> 4) * 32 : 0;
     }
-    boff[idx] = make_int2(o[0], o[1]);
+    a.boff[idx] = make_int2(o[0], o[1]);
   }
-  const int32_t total = KB * Mp * 8;
+  const int32_t total = a.KB * a.Mp * 8;
   if (idx >= total) return;
   const int32_t quarter = idx & 3;
   const int32_t piece = idx >> 2;  // (kb * Mp + m) * 2 + half
   const int32_t half = piece & 1;
-  const int32_t m = (piece >> 1) % Mp;
-  const int32_t kb = (piece >> 1) / Mp;
+  const int32_t m = (piece >> 1) % a.Mp;
+  const int32_t kb = (piece >> 1) / a.Mp;
   uint32_t hi = 0u, lo = 0u;
-  if (m < M) {
+  if (m < a.M) {
     const int32_t t0 = kb * 32 + half * 16 + quarter * 4;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int32_t t = t0 + i;
       int32_t v = 0;
-      if (t < T) {
-        const int32_t ci = t % Cin, tap = t / Cin;
-        const int32_t r = tap / S, s = tap % S;
+      if (t < a.T) {
+        const int32_t ci = t % a.Cin, tap = t / a.Cin;
+        const int32_t r = tap / a.S, s = tap % a.S;
         // forward: w[m][ci][r][s]; backward-data: w[ci][m][r][s] (Cw = C)
-        const int32_t off = transposed ? ((ci * Cw + m) * R + r) * S + s : ((m * Cw + ci) * R + r) * S + s;
-        v = w[off];
+        const int32_t off = a.transposed ? ((ci * a.Cw + m) * a.R + r) * a.S + s : ((m * a.Cw + ci) * a.R + r) * a.S + s;
+        v = a.w[off];
       }
       hi |= hi_digit(v) << (8 * i);
       lo |= lo_digit(v) << (8 * i);
     }
   }
-  uint32_t* dst = reinterpret_cast<uint32_t*>(ws + (int64_t)piece * 32) + quarter;
+  uint32_t* dst = reinterpret_cast<uint32_t*>(a.ws + (int64_t)piece * 32) + quarter;
   dst[0] = hi;
   dst[4] = lo;
 }
+
+__global__ __launch_bounds__(256) void k_prep_a(PrepAArgs a) { prep_a_item(a, blockIdx.x * 256 + threadIdx.x); }
 
 // ---------------------------------------------------------------- B prep
 // Xs[n][u][v][cg][32 B] = digits of src[n][cg*16 + i][(u-top)/dil_h][(v-left)/dil_w]
@@ -203,8 +211,15 @@ template <bool VEC>
 __global__ __launch_bounds__(256) void k_prep_plane(const int16_t* __restrict__ src, uint8_t* __restrict__ xs,
                                                    int32_t Cs, int32_t Hs, int32_t Wsrc, int32_t Hp, int32_t Wp,
                                                    int32_t CG, int32_t top, int32_t left, int32_t dil_h,
-                                                   int32_t dil_w, int32_t rb) {
+                                                   int32_t dil_w, int32_t rb, PrepAArgs pa, int32_t with_a) {
   extern __shared__ __align__(16) uint32_t tile2[];  // [rb][8][Wsrc] channel pairs
+  if (with_a && blockIdx.z == gridDim.z - 1) {  // one extra slice of workgroups prepares the filter digits
+    const int32_t nthr = gridDim.x * gridDim.y * 256;
+    const int32_t total = max(pa.KB * pa.Mp * 8, pa.KB);
+    for (int32_t idx = (blockIdx.y * gridDim.x + blockIdx.x) * 256 + threadIdx.x; idx < total; idx += nthr)
+      prep_a_item(pa, idx);
+    return;
+  }
   const int32_t u0 = blockIdx.x * rb, cg = blockIdx.y, n = blockIdx.z;
   const int32_t nr = min(rb, Hp - u0);
   const int64_t plane = (int64_t)Hs * Wsrc;
@@ -1755,26 +1770,31 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   const int32_t tap_row_bytes = rsign * p.Wp * p.CG * 32, tap_col_bytes = rsign * p.CG * 32;
   const bool plane = conv_w16_eligible(p.Cin, p.T, g.L, i32) && (int64_t)g.n * p.Po * p.Qo * p.M < (1ll << 31) &&
                      p.ws_b_bytes < (1ll << 31);
-  {
-    const int64_t total = (int64_t)p.KB * p.Mp * 8;
-    DFP_LAUNCH(K_WPREP, k_prep_a, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, b, wsa, p.M, p.Mp,
-               p.Cin, g.r, g.s, p.T, p.KB, fwd ? 0 : 1, g.c, so, boff, tap_row_bytes, tap_col_bytes);
-  }
+  const PrepAArgs pa{b, wsa, p.M, p.Mp, p.Cin, g.r, g.s, p.T, p.KB, fwd ? 0 : 1, g.c, so, boff,
+                     tap_row_bytes, tap_col_bytes};
+  const int64_t a_total = (int64_t)p.KB * p.Mp * 8;
+  // the plane-layout preparation takes the filter digits in an extra slice of
+  // its grid when that slice needs at most 8 items per thread
+  const int32_t rb_plane = std::max(1, std::min(kPlaneRows, kPlaneElems / (16 * (fwd ? g.w : g.q))));
+  const int64_t slice_threads = (int64_t)((p.Hp + rb_plane - 1) / rb_plane) * p.CG * 256;
+  const bool merge_a = plane && a_total <= 8 * slice_threads;
+  if (!merge_a) DFP_LAUNCH(K_WPREP, k_prep_a, dim3((unsigned)((a_total + 255) / 256)), dim3(256), 0, st, pa);
   {
     const int32_t Cs = fwd ? g.c : g.k, Hs = fwd ? g.h : g.p, Wsrc = fwd ? g.w : g.q;
     const bool vec = (Wsrc % 8) == 0 && (reinterpret_cast<uintptr_t>(a) & 15) == 0;
     const int32_t cgc = std::max(1, std::min(p.CG, kPrepBElems / (16 * Wsrc)));  // as in the kernel
     const size_t lds = (size_t)cgc * 16 * Wsrc * 2;
     if (plane) {
-      const int32_t rb = std::max(1, std::min(kPlaneRows, kPlaneElems / (16 * Wsrc)));
-      const dim3 grid((unsigned)((p.Hp + rb - 1) / rb), (unsigned)p.CG, (unsigned)g.n);
+      const int32_t rb = rb_plane;
+      const dim3 grid((unsigned)((p.Hp + rb - 1) / rb), (unsigned)p.CG, (unsigned)(g.n + (merge_a ? 1 : 0)));
       const size_t plds = (size_t)rb * Wsrc * 16 * 2;
+      const int32_t wa = merge_a ? 1 : 0;
       if (vec)
         DFP_LAUNCH(K_XPREP, k_prep_plane<true>, grid, dim3(256), plds, st, a, xs, Cs, Hs, Wsrc, p.Hp, p.Wp, p.CG,
-                   p.top, p.left, p.dil_h, p.dil_w, rb);
+                   p.top, p.left, p.dil_h, p.dil_w, rb, pa, wa);
       else
         DFP_LAUNCH(K_XPREP, k_prep_plane<false>, grid, dim3(256), plds, st, a, xs, Cs, Hs, Wsrc, p.Hp, p.Wp, p.CG,
-                   p.top, p.left, p.dil_h, p.dil_w, rb);
+                   p.top, p.left, p.dil_h, p.dil_w, rb, pa, wa);
     } else if (vec) {
       DFP_LAUNCH(K_XPREP, k_prep_b<true>, dim3((unsigned)(g.n * p.Hp)), dim3(256), lds, st, a, xs, g.n, Cs, Hs, Wsrc,
                  p.Hp, p.Wp, p.CG, p.top, p.left, p.dil_h, p.dil_w);

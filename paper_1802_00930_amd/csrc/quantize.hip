@@ -48,16 +48,17 @@ __global__ void k_scale_reset(dfp_scale* s) {
   }
 }
 
-// Max of |src| bit patterns in two stages with no atomics.  Stage 1:
-// workgroup b reduces the 16 KiB chunks b, b + grid, ... (each lane keeps four
-// independent 16-byte loads in flight) and stores its max in part[b].  part
-// is the destination INT16 buffer, which the rounding pass overwrites only
-// after stage 2 has read it.  Stage 2: one workgroup reduces the partial
-// maxima into the scale and clears its flags.  A tensor of at most one chunk
-// goes straight to the scale in stage 1.
+// Max of |src| bit patterns in two stages with no atomics.  Stage 1: the
+// 16-byte vectors are cut into one contiguous, equal range per workgroup
+// (up to kAmaxMaxParts workgroups, about eight per CU, so every range is read
+// in one pass with four loads per lane in flight); workgroup b stores its max
+// in part[b].  part is the destination INT16 buffer, which the rounding pass
+// overwrites only after stage 2 has read it.  Stage 2: one workgroup reduces
+// the partial maxima into the scale and clears its flags.  A tensor small
+// enough for one workgroup goes straight to the scale in stage 1.
 constexpr int kAmaxUnroll = 4;
-constexpr int kAmaxChunk = kBlock * kAmaxUnroll;  // 16-byte vectors per chunk
-constexpr int kAmaxMaxParts = 1024;
+constexpr int kAmaxChunk = kBlock * kAmaxUnroll;  // 16-byte vectors per chunk (INT32 max pass)
+constexpr int kAmaxMaxParts = 2048;
 
 __device__ __forceinline__ uint32_t abs_max4(uint4 v) {
   return max(max(v.x & 0x7fffffffu, v.y & 0x7fffffffu), max(v.z & 0x7fffffffu, v.w & 0x7fffffffu));
@@ -67,18 +68,17 @@ __global__ __launch_bounds__(kBlock) void k_amax(const float* __restrict__ src, 
                                                  uint32_t* __restrict__ part, dfp_scale* __restrict__ s) {
   const uint4* src4 = reinterpret_cast<const uint4*>(src);
   const int64_t n4 = n >> 2;
+  const int64_t lo = n4 * blockIdx.x / gridDim.x, hi = n4 * (blockIdx.x + 1) / gridDim.x;
   uint32_t m[kAmaxUnroll] = {0u, 0u, 0u, 0u};
-  for (int64_t base = (int64_t)blockIdx.x * kAmaxChunk; base < n4; base += (int64_t)gridDim.x * kAmaxChunk) {
-    if (base + kAmaxChunk <= n4) {
-      uint4 v[kAmaxUnroll];
+  int64_t i = lo + threadIdx.x;
+  for (; i + (kAmaxUnroll - 1) * kBlock < hi; i += kAmaxUnroll * kBlock) {
+    uint4 v[kAmaxUnroll];
 #pragma unroll
-      for (int k = 0; k < kAmaxUnroll; ++k) v[k] = src4[base + threadIdx.x + k * kBlock];
+    for (int k = 0; k < kAmaxUnroll; ++k) v[k] = src4[i + k * kBlock];
 #pragma unroll
-      for (int k = 0; k < kAmaxUnroll; ++k) m[k] = max(m[k], abs_max4(v[k]));
-    } else {
-      for (int64_t i = base + threadIdx.x; i < n4; i += kBlock) m[0] = max(m[0], abs_max4(src4[i]));
-    }
+    for (int k = 0; k < kAmaxUnroll; ++k) m[k] = max(m[k], abs_max4(v[k]));
   }
+  for (; i < hi; i += kBlock) m[0] = max(m[0], abs_max4(src4[i]));
   uint32_t mm = max(max(m[0], m[1]), max(m[2], m[3]));
   if (blockIdx.x == 0) {
     const uint32_t* s1 = reinterpret_cast<const uint32_t*>(src);
@@ -106,6 +106,33 @@ __global__ __launch_bounds__(kBlock) void k_amax_final(const uint32_t* __restric
   }
 }
 
+// One group of four consecutive elements: four roundings with the group's
+// Philox block, packed as four INT16.
+template <int MODE, bool SAT>
+__device__ __forceinline__ uint2 quant_group(const uint4 v, int64_t g, int32_t es, bool all_zero, uint32_t key0,
+                                             uint32_t key1, uint32_t role, bool& saturated) {
+  const uint32_t fb[4] = {v.x, v.y, v.z, v.w};
+  uint32_t u[4] = {0u, 0u, 0u, 0u};
+  if (MODE == DFP_ROUND_STOCHASTIC) {
+    const uint4 r = philox4x32_10(make_uint4((uint32_t)g, (uint32_t)((uint64_t)g >> 32), role, 0u), key0, key1);
+    u[0] = r.x; u[1] = r.y; u[2] = r.z; u[3] = r.w;
+  }
+  int32_t iv[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    int32_t q = round_one<MODE>(fb[i], es, u[i]);
+    q = all_zero ? 0 : q;
+    if (SAT) {  // P = 16: |x| < 2^15 rounds to at most 2^15
+      const int32_t c = min(max(q, -32767), 32767);
+      saturated |= c != q;
+      q = c;
+    }
+    iv[i] = q;
+  }
+  return make_uint2(((uint32_t)iv[0] & 0xffffu) | ((uint32_t)iv[1] << 16),
+                    ((uint32_t)iv[2] & 0xffffu) | ((uint32_t)iv[3] << 16));
+}
+
 template <int MODE, bool SAT>
 __global__ __launch_bounds__(kBlock) void k_quant_convert(const float* __restrict__ src,
                                                           int16_t* __restrict__ dst, int64_t n,
@@ -118,48 +145,30 @@ __global__ __launch_bounds__(kBlock) void k_quant_convert(const float* __restric
     if (sc.flags) atomicOr(&s->flags, sc.flags);
   }
   const bool all_zero = sc.all_zero;
-  const int64_t groups = (n + 3) >> 2;
+  const int64_t full = n >> 2;  // whole groups of four
   const int64_t stride = (int64_t)gridDim.x * kBlock;
+  const uint4* src4 = reinterpret_cast<const uint4*>(src);
+  uint2* dst4 = reinterpret_cast<uint2*>(dst);
   bool saturated = false;
-  for (int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x; g < groups; g += stride) {
-    const int64_t base = g << 2;
-    uint32_t fb[4];
-    const bool full = base + 4 <= n;
-    if (full) {
-      const uint4 v = reinterpret_cast<const uint4*>(src)[g];
-      fb[0] = v.x; fb[1] = v.y; fb[2] = v.z; fb[3] = v.w;
-    } else {
-      const uint32_t* s1 = reinterpret_cast<const uint32_t*>(src);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) fb[i] = (base + i < n) ? s1[base + i] : 0u;
-    }
-    uint32_t u[4] = {0u, 0u, 0u, 0u};
-    if (MODE == DFP_ROUND_STOCHASTIC) {
-      const uint4 r = philox4x32_10(make_uint4((uint32_t)g, (uint32_t)((uint64_t)g >> 32), role, 0u), key0, key1);
-      u[0] = r.x; u[1] = r.y; u[2] = r.z; u[3] = r.w;
-    }
-    int32_t iv[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int32_t v = round_one<MODE>(fb[i], es, u[i]);
-      v = all_zero ? 0 : v;
-      if (SAT) {  // P = 16: |x| < 2^15 rounds to at most 2^15
-        const int32_t c = min(max(v, -32767), 32767);
-        saturated |= c != v;
-        v = c;
-      }
-      iv[i] = v;
-    }
-    if (full) {
-      uint2 packed;
-      packed.x = ((uint32_t)iv[0] & 0xffffu) | ((uint32_t)iv[1] << 16);
-      packed.y = ((uint32_t)iv[2] & 0xffffu) | ((uint32_t)iv[3] << 16);
-      reinterpret_cast<uint2*>(dst)[g] = packed;
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (base + i < n) dst[base + i] = (int16_t)iv[i];
-    }
+  int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  // two groups per iteration: both loads in flight before either is rounded
+  for (; g + stride < full; g += 2 * stride) {
+    const uint4 v0 = src4[g], v1 = src4[g + stride];
+    dst4[g] = quant_group<MODE, SAT>(v0, g, es, all_zero, key0, key1, role, saturated);
+    dst4[g + stride] = quant_group<MODE, SAT>(v1, g + stride, es, all_zero, key0, key1, role, saturated);
+  }
+  if (g < full) dst4[g] = quant_group<MODE, SAT>(src4[g], g, es, all_zero, key0, key1, role, saturated);
+  if ((n & 3) && blockIdx.x == 0 && threadIdx.x == 0) {  // the last, partial group
+    const uint32_t* s1 = reinterpret_cast<const uint32_t*>(src);
+    const int64_t base = full << 2;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    v.x = s1[base];
+    if (base + 1 < n) v.y = s1[base + 1];
+    if (base + 2 < n) v.z = s1[base + 2];
+    const uint2 packed = quant_group<MODE, SAT>(v, full, es, all_zero, key0, key1, role, saturated);
+    dst[base] = (int16_t)(packed.x & 0xffffu);
+    if (base + 1 < n) dst[base + 1] = (int16_t)(packed.x >> 16);
+    if (base + 2 < n) dst[base + 2] = (int16_t)(packed.y & 0xffffu);
   }
   if (SAT && saturated) atomicOr(&s->flags, DFP_FLAG_SATURATED);
 }
@@ -486,9 +495,9 @@ dfp_status launch_scale_reset(dfp_scale* s, hipStream_t st) {
 }
 
 dfp_status launch_amax(const float* src, int64_t n, int16_t* scratch, dfp_scale* s, hipStream_t st) {
-  // one workgroup per 16 KiB chunk up to kAmaxMaxParts (grid-stride beyond); the
+  // about 16 KiB or more per workgroup, at most kAmaxMaxParts workgroups; the
   // partial maxima need 4 bytes each of the 2n-byte destination
-  int64_t parts = (n / 4 + kAmaxChunk - 1) / kAmaxChunk;
+  int64_t parts = (n / 4 + kBlock * kAmaxUnroll - 1) / (kBlock * kAmaxUnroll);
   parts = std::min<int64_t>(std::min<int64_t>(parts, kAmaxMaxParts), n / 2);
   if (parts <= 1) {
     DFP_LAUNCH(K_AMAX, k_amax, dim3(1), dim3(kBlock), 0, st, src, n, (uint32_t*)nullptr, s);
@@ -508,7 +517,12 @@ dfp_status launch_amax_final(const uint32_t* part, int32_t nparts, dfp_scale* s,
 template <int MODE>
 static dfp_status launch_qc_mode(const float* src, int16_t* dst, int64_t n, dfp_scale* s, int32_t bits,
                                  uint32_t k0, uint32_t k1, uint32_t role, hipStream_t st) {
-  const dim3 grid(grid_for((n + 3) / 4));
+  // Without the Philox stream the pass is bound by memory: at most eight
+  // workgroups per CU, so a thread rounds several groups and shares its set-up
+  // (scale, exponent) among them.  Stochastic rounding is bound by its VALU
+  // work and runs faster with one group per thread (more waves to interleave).
+  const int64_t blocks = grid_for((n + 3) / 4);
+  const dim3 grid((unsigned)(MODE == DFP_ROUND_STOCHASTIC ? blocks : std::min<int64_t>(blocks, 2048)));
   if (bits == 16)
     DFP_LAUNCH(K_QUANT, (k_quant_convert<MODE, true>), grid, dim3(kBlock), 0, st, src, dst, n, s, bits, k0, k1, role);
   else
