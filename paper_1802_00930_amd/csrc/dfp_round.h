@@ -56,24 +56,22 @@ __device__ __forceinline__ ScaleFromMax scale_from_max(uint32_t mb, int32_t bits
 }
 
 // x = f * 2^-es split as X = floor(x * 2^32) = fl * 2^32 + F, in integer
-// arithmetic on the sign / exponent / significand fields.  f = M * 2^(e1 - 150)
-// with M the 24-bit significand, so |x| * 2^32 = M * 2^(32 - sh) with
-// sh = es + 150 - e1.  Every element of the tensor has |x| < 2^(bits-1) <= 2^15,
-// which bounds sh below by 9; shifts past 63 leave nothing but the inexact bit.
+// arithmetic on the sign / exponent / significand fields.  f = S * 2^(e1 - 150)
+// with S the signed 24-bit significand, so x * 2^32 = S * 2^(32 - sh) with
+// sh = es + 150 - e1, and X = (S * 2^32) >> sh with an arithmetic shift (the
+// floor, for either sign).  Every element of the tensor has |x| < 2^(bits-1)
+// <= 2^15, which bounds sh below by 9 (|X| < 2^47); shifts are clamped at 63,
+// which leaves 0 or -1 (a value below 2^-31 in magnitude).
 struct Split {
   int32_t fl;   // floor(x)
   uint32_t F;   // floor(frac(x) * 2^32)
 };
 __device__ __forceinline__ Split split_scaled(uint32_t fb, int32_t es150) {
-  const uint32_t ax = fb & 0x7fffffffu;
-  const uint32_t eb = ax >> 23;
-  const uint32_t M = (ax & 0x7fffffu) | ((eb != 0u ? 1u : 0u) << 23);
+  const uint32_t eb = (fb >> 23) & 0xffu;
+  const int32_t M = (int32_t)((fb & 0x7fffffu) | ((eb != 0u ? 1u : 0u) << 23));
+  const int32_t S = (int32_t)fb < 0 ? -M : M;
   const uint32_t sh = min((uint32_t)(es150 - (int32_t)max(eb, 1u)), 63u);
-  const uint64_t A = ((uint64_t)M << 32) >> sh;  // floor(|x| * 2^32)
-  const bool inexact = sh > 32u && (M << (64u - sh)) != 0u;
-  // negative x: floor(-|x| 2^32) = -(A + inexact) = ~A + (1 - inexact)
-  const uint64_t sm = (uint64_t)(int64_t)((int32_t)fb >> 31);
-  const uint64_t X = (A ^ sm) + ((sm != 0u && !inexact) ? 1u : 0u);
+  const int64_t X = (int64_t)((uint64_t)(uint32_t)S << 32) >> sh;
   return {(int32_t)(X >> 32), (uint32_t)X};
 }
 
