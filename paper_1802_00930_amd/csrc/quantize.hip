@@ -64,21 +64,23 @@ __device__ __forceinline__ uint32_t abs_max4(uint4 v) {
   return max(max(v.x & 0x7fffffffu, v.y & 0x7fffffffu), max(v.z & 0x7fffffffu, v.w & 0x7fffffffu));
 }
 
-__global__ __launch_bounds__(kBlock) void k_amax(const float* __restrict__ src, int64_t n,
+// Range of workgroup b: per vectors each, the first rem workgroups one more.
+__global__ __launch_bounds__(kBlock) void k_amax(const float* __restrict__ src, int64_t n, int64_t per, int32_t rem,
                                                  uint32_t* __restrict__ part, dfp_scale* __restrict__ s) {
   const uint4* src4 = reinterpret_cast<const uint4*>(src);
   const int64_t n4 = n >> 2;
-  const int64_t lo = n4 * blockIdx.x / gridDim.x, hi = n4 * (blockIdx.x + 1) / gridDim.x;
+  const int32_t b = blockIdx.x;
+  const int64_t lo = per * b + min(b, rem), hi = lo + per + (b < rem ? 1 : 0);
   uint32_t m[kAmaxUnroll] = {0u, 0u, 0u, 0u};
-  int64_t i = lo + threadIdx.x;
-  for (; i + (kAmaxUnroll - 1) * kBlock < hi; i += kAmaxUnroll * kBlock) {
+  // all four loads of a step are issued before any is reduced; a load past
+  // the range re-reads the range's last vector (the max is unchanged)
+  for (int64_t base = lo + threadIdx.x; base < hi; base += kAmaxUnroll * kBlock) {
     uint4 v[kAmaxUnroll];
 #pragma unroll
-    for (int k = 0; k < kAmaxUnroll; ++k) v[k] = src4[i + k * kBlock];
+    for (int k = 0; k < kAmaxUnroll; ++k) v[k] = src4[min(base + k * kBlock, hi - 1)];
 #pragma unroll
     for (int k = 0; k < kAmaxUnroll; ++k) m[k] = max(m[k], abs_max4(v[k]));
   }
-  for (; i < hi; i += kBlock) m[0] = max(m[0], abs_max4(src4[i]));
   uint32_t mm = max(max(m[0], m[1]), max(m[2], m[3]));
   if (blockIdx.x == 0) {
     const uint32_t* s1 = reinterpret_cast<const uint32_t*>(src);
@@ -500,11 +502,12 @@ dfp_status launch_amax(const float* src, int64_t n, int16_t* scratch, dfp_scale*
   int64_t parts = (n / 4 + kBlock * kAmaxUnroll - 1) / (kBlock * kAmaxUnroll);
   parts = std::min<int64_t>(std::min<int64_t>(parts, kAmaxMaxParts), n / 2);
   if (parts <= 1) {
-    DFP_LAUNCH(K_AMAX, k_amax, dim3(1), dim3(kBlock), 0, st, src, n, (uint32_t*)nullptr, s);
+    DFP_LAUNCH(K_AMAX, k_amax, dim3(1), dim3(kBlock), 0, st, src, n, n / 4, 0, (uint32_t*)nullptr, s);
     return DFP_OK;
   }
   uint32_t* part = reinterpret_cast<uint32_t*>(scratch);
-  DFP_LAUNCH(K_AMAX, k_amax, dim3((unsigned)parts), dim3(kBlock), 0, st, src, n, part, s);
+  DFP_LAUNCH(K_AMAX, k_amax, dim3((unsigned)parts), dim3(kBlock), 0, st, src, n, (n / 4) / parts,
+             (int32_t)((n / 4) % parts), part, s);
   DFP_LAUNCH(K_AMAX, k_amax_final, dim3(1), dim3(kBlock), 0, st, part, (int32_t)parts, s);
   return DFP_OK;
 }
