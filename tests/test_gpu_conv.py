@@ -114,6 +114,9 @@ def test_bwd_wt_band_no_partials(shape, G):
 # filter (36 blocks; its backward-data, 54 blocks, goes to another kernel),
 # strides, and fewer output pixels than one wave's unit.
 W16_SHAPES = [
+    (2, 64, 12, 12, 64, 3, 3, 1, 1),
+    (2, 64, 16, 16, 128, 3, 3, 2, 1),  # strided: backward-data reads a dilated plane
+    (2, 64, 20, 12, 64, 1, 1, 1, 0),   # no padding columns
     (2, 64, 7, 7, 64, 1, 1, 1, 0),
     (1, 64, 13, 13, 200, 3, 3, 1, 1),
     (2, 128, 5, 5, 192, 3, 3, 1, 1),
