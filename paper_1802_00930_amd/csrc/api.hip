@@ -219,9 +219,7 @@ dfp_status dfp_quantize(const dfp_desc* d, int32_t role, const float* src, int16
   if (!aligned(src, 16) || !aligned(dst, 8) || !aligned(s, 16)) return DFP_ERR_ALIGN;
   const int64_t n = role_numel(g, role);
   hipStream_t st = (hipStream_t)stream;
-  dfp_status rc;
-  if ((rc = launch_amax(src, n, dst, s, st)) != DFP_OK) return rc;
-  return launch_quant_convert(src, dst, n, s, d->bits, d->rounding, d->seed, (uint32_t)role, st);
+  return launch_quantize(src, dst, n, s, d->bits, d->rounding, d->seed, (uint32_t)role, st);
 }
 
 dfp_status dfp_downconvert(const dfp_desc* d, int32_t role, const float* src, int16_t* dst, dfp_scale* s,
@@ -378,9 +376,7 @@ dfp_status dfp_quantize_tensor(int64_t n, int32_t bits, int32_t rounding, uint64
   if (!flat_params_ok(n, bits, rounding, role)) return DFP_ERR_PARAM;
   if (!aligned(src, 16) || !aligned(dst, 8) || !aligned(s, 16)) return DFP_ERR_ALIGN;
   hipStream_t st = (hipStream_t)stream;
-  dfp_status rc;
-  if ((rc = launch_amax(src, n, dst, s, st)) != DFP_OK) return rc;
-  return launch_quant_convert(src, dst, n, s, bits, rounding, seed, (uint32_t)role, st);
+  return launch_quantize(src, dst, n, s, bits, rounding, seed, (uint32_t)role, st);
 }
 
 dfp_status dfp_downconvert_tensor(int64_t n, int32_t bits, int32_t rounding, uint64_t seed, int32_t role,

@@ -85,6 +85,9 @@ dfp_status launch_amax(const float* src, int64_t n, int16_t* scratch, dfp_scale*
 // Reduces part[0 .. nparts) (per-workgroup maxima of |.| bits) into
 // s->amax_bits and clears s->flags.
 dfp_status launch_amax_final(const uint32_t* part, int32_t nparts, dfp_scale* s, hipStream_t st);
+// Max pass + rounding pass, or one launch for a small P = 15 tensor.
+dfp_status launch_quantize(const float* src, int16_t* dst, int64_t n, dfp_scale* s, int32_t bits, int32_t rounding,
+                           uint64_t seed, uint32_t role, hipStream_t st);
 dfp_status launch_quant_convert(const float* src, int16_t* dst, int64_t n, dfp_scale* s, int32_t bits,
                                 int32_t rounding, uint64_t seed, uint32_t role, hipStream_t st);
 

@@ -47,7 +47,7 @@ def check(f, bits, rounding, seed=0, role=0):
         assert sc["amax_bits"] == int((f.view(np.uint32) & 0x7fffffff).max())
 
 
-@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 7, 8, 63, 1000, 4097, (1 << 20) + 3])
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 7, 8, 63, 1000, 4097, 65535, 65536, 65537, (1 << 20) + 3])
 @pytest.mark.parametrize("rounding", [0, 1, 2, 3])
 def test_sizes_and_modes(n, rounding):
     rng = np.random.default_rng(n * 7 + rounding)
