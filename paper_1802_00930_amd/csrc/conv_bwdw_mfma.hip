@@ -430,6 +430,15 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint3
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint8_t*)p;
 }
+// Lane id (0..63) computed afresh at each use: the asm is volatile, so the
+// compiler recomputes it rather than keeping it (or values derived from it)
+// in a register across a loop.
+__device__ __forceinline__ int32_t fresh_lane() {
+  int32_t l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 __device__ __forceinline__ int swz(int row, int piece) { return row * 4 + (piece ^ ((row >> 2) & 3)); }
 
 // XB[c][n*Hpad + u][d][Wpad]: d = 0 lo digits, d = 1 hi digits of
@@ -720,14 +729,17 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
   // of block kb0 + j.
   const __amdgpu_buffer_rsrc_t rs_a = make_rsrc(a.ad, a.ad_bytes);
   const __amdgpu_buffer_rsrc_t rs_b = make_rsrc(a.xb, a.xb_bytes);
-  const uint32_t a_lane = (uint32_t)((m0 + (threadIdx.x >> 2)) * 64 + (((threadIdx.x & 3) ^ ((threadIdx.x >> 4) & 3)) * 16));
   const uint32_t a_block = (uint32_t)a.Mp * 64;
-  const uint32_t b_lane = (uint32_t)lane * 16;
   auto issue_band = [&](int32_t b) {
     const int32_t t_b0 = t_seg0 + b * kSBT;
     uint8_t* dstB = smem + (b & 1) * a.buf_bytes;
     uint8_t* dstA = dstB + b_region;
     const int32_t kb0 = t_b0 / 32;
+    // lane values recomputed here rather than held in registers across the band
+    const int32_t ln = fresh_lane();
+    const int32_t tid = wave_u * 64 + ln;
+    const uint32_t a_lane = (uint32_t)((m0 + (tid >> 2)) * 64 + (((tid & 3) ^ ((tid >> 4) & 3)) * 16));
+    const uint32_t b_lane = (uint32_t)ln * 16;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int32_t kb = min(kb0 + j, last_kb);  // blocks past the segment reload a valid one (unused)
@@ -742,7 +754,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
       const uint32_t soc = (uint32_t)((ch * a.NH + za) * row_b);
       uint8_t* dstc = dstB + cc * a.band_ch_stride;
       for (int32_t k0 = 0; k0 < ppc; k0 += 64) {
-        if (lane < ppc - k0)
+        if (ln < ppc - k0)
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_b, (lds_ptr_t)(dstc + k0 * 16), 16, b_lane,
                                                    __builtin_amdgcn_readfirstlane(soc + (uint32_t)k0 * 16), 0, 0);
       }
@@ -908,14 +920,6 @@ __device__ __forceinline__ v4i rsrc_words(const void* p, uint32_t bytes) {
              __builtin_amdgcn_readfirstlane((int)bytes), 0x00020000};
 }
 
-// Lane id (0..63) computed afresh at each use: the asm is volatile, so the
-// compiler recomputes it rather than keeping it (or values derived from it)
-// in a register across a loop.
-__device__ __forceinline__ int32_t fresh_lane() {
-  int32_t l;
-  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
-  return l;
-}
 
 constexpr int kThreadsW8 = 512;
 constexpr int kBandBufBytes = kBandLdsBytes / 2;
@@ -1139,6 +1143,21 @@ dim3 bwdw_grid(BwdwArgs& args, const BwdwPlan& p) {
 
 }  // namespace
 
+// The band kernels read LDS with inline assembly and wait for the reads
+// explicitly (see no_scratch): a band kernel is used only if its build has no
+// scratch, else the general kernel (ordinary LDS reads) runs.
+struct BandKernelsSafe {
+  bool w8, skew_t, skew_f, band_t, band_f;
+};
+static const BandKernelsSafe& band_kernels_safe() {
+  static const BandKernelsSafe safe{no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false>)),
+                                    no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<true>)),
+                                    no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<false>)),
+                                    no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<true>)),
+                                    no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<false>))};
+  return safe;
+}
+
 BwdwPlan plan_bwdw_mfma(const Geom& g) {
   BwdwPlan p{};
   p.T = (int64_t)g.n * g.p * g.q;
@@ -1213,7 +1232,11 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   const int64_t dy_blocks = (p.KBT * p.Mp * 2 + 255) / 256;
   const BandLayout bl = band_layout(g, p);
   // the band kernels address both digit tensors with 32-bit buffer offsets
-  if (bl.buf_bytes > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 && p.ad_bytes < (1ll << 31) &&
+  const BandKernelsSafe& safe = band_kernels_safe();
+  const bool l64 = g.L == 64 && (p.T % 64) == 0;  // every segment a whole number of two-block chunks
+  const bool band_ok = l64 ? (partials ? safe.skew_t : (safe.w8 || safe.skew_f))
+                           : (partials ? safe.band_t : safe.band_f);
+  if (band_ok && bl.buf_bytes > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 && p.ad_bytes < (1ll << 31) &&
       p.xp_bytes < (1ll << 31)) {
     uint8_t* xb = reinterpret_cast<uint8_t*>(xp);  // same workspace region as the pair layout
     // one launch prepares both operands: rows of workgroups 0 .. C-1 the x
@@ -1260,12 +1283,12 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.div_p = make_fastdiv((uint32_t)g.p);
     args.xb_bytes = (uint32_t)p.xp_bytes;
     const dim3 grid = bwdw_grid(args, p);
-    if (g.L == 64 && (p.T % 64) == 0) {  // every segment a whole number of two-block chunks
-      // the partials variant of the eight-wave kernel would spill registers
-      // its inline-assembly reads are still filling: partials use the
-      // two-tile kernel (same chunks, same order of additions)
+    if (l64) {
+      // the partials variant of the eight-wave kernel would spill: partials
+      // use the two-tile kernel (same chunks, same order of additions)
       if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<true>), grid, dim3(kThreads), 0, st, args);
-      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false>), grid, dim3(kThreadsW8), 0, st, args);
+      else if (safe.w8) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false>), grid, dim3(kThreadsW8), 0, st, args);
+      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<false>), grid, dim3(kThreads), 0, st, args);
     } else {
       if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<true>), grid, dim3(kThreads), 0, st, args);
       else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<false>), grid, dim3(kThreads), 0, st, args);

@@ -1929,7 +1929,7 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     args.L = args.KB * 32;
     if (w16_ok)
       DFP_LAUNCH(kid32, (k_conv_mfma_w16<false, true>), w16_grid(), dim3(kThreads16), 0, st, args);
-    else if (persist_ok)
+    else if (persist_ok && no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_persist<false, true>)))
       DFP_LAUNCH(kid32, (k_conv_mfma_persist<false, true>), persist_grid(), dim3(kThreads3), 0, st, args);
     else if (chan16 && small_index)
       DFP_LAUNCH(kid32, (k_conv_mfma_q<false, true>), grid, dim3(kThreadsQ), 0, st, args);
@@ -1949,7 +1949,14 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     else DFP_LAUNCH(kid, (k_conv_mfma_w16<false>), w16_grid(), dim3(kThreads16), 0, st, args);
     return DFP_OK;
   }
-  if (persist_ok && args.L == 64) {
+  // the persistent and skewed kernels wait for their inline-assembly LDS reads
+  // in a later statement: a build of them with scratch is not used (see
+  // no_scratch); the shared-ring and LDS kernels wait inside the same asm
+  static const bool persist_safe[2] = {no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_persist<false>)),
+                                       no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_persist<true>))};
+  static const bool skew_safe[2] = {no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_skew<false>)),
+                                    no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_skew<true>))};
+  if (persist_ok && args.L == 64 && persist_safe[partials ? 1 : 0]) {
     const dim3 grid3 = persist_grid();
     if (partials) DFP_LAUNCH(kid, (k_conv_mfma_persist<true>), grid3, dim3(kThreads3), 0, st, args);
     else DFP_LAUNCH(kid, (k_conv_mfma_persist<false>), grid3, dim3(kThreads3), 0, st, args);
@@ -1960,7 +1967,7 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     else DFP_LAUNCH(kid, (k_conv_mfma_q<false>), grid, dim3(kThreadsQ), 0, st, args);
     return DFP_OK;
   }
-  if (chan16 && args.L == 64 && (args.T % 64) == 0 && args.KB >= 4) {
+  if (chan16 && args.L == 64 && (args.T % 64) == 0 && args.KB >= 4 && skew_safe[partials ? 1 : 0]) {
     if (partials) DFP_LAUNCH(kid, (k_conv_mfma_skew<true>), grid, dim3(kThreads), 0, st, args);
     else DFP_LAUNCH(kid, (k_conv_mfma_skew<false>), grid, dim3(kThreads), 0, st, args);
     return DFP_OK;

@@ -52,6 +52,15 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) {
   return (uint32_t)(((uint64_t)__umulhi(n, f.m) + n) >> f.l);
 }
 
+// True if the kernel's build uses no scratch (private segment).  Kernels that
+// read LDS with inline assembly and wait for the reads in a later statement
+// rely on the compiler neither copying nor spilling a register such a read is
+// still filling between the two; a build with scratch is not used.
+inline bool no_scratch(const void* kernel) {
+  hipFuncAttributes attr{};
+  return hipFuncGetAttributes(&attr, kernel) == hipSuccess && attr.localSizeBytes == 0;
+}
+
 // Convolution geometry handed to kernels by value.
 struct Geom {
   int32_t n, c, h, w;   // activations NCHW
