@@ -1670,6 +1670,10 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   };
 
   const bool full_rows = a.M == a.Mp;  // every row of the 64-row tiles is an output channel
+  // FP32 output addressed by 32-bit byte offsets (fewer than 2^30 outputs)
+  const bool out_buf = a.O < (1ll << 30);
+  const __amdgpu_buffer_rsrc_t rs_out =
+      __builtin_amdgcn_make_buffer_rsrc(a.out, (short)0, out_buf ? (int)(a.O * 4) : 0, 0x00020000);
   uint32_t amax = 0;
   // the stream's first chunk is requested while the filter digits are in
   // flight; afterwards each block's registers are refilled with the block two
@@ -1726,7 +1730,20 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
       }
       if (I32) keep_tile_i32(acc, sum);
       if (gvalid) {
-        if (full_rows) {
+        if (!I32 && full_rows && out_buf) {
+          // buffer stores at a per-lane offset plus a uniform one per output row,
+          // max |y| on floats (y is never NaN), two values per v_max3
+          const uint32_t lane_off = (uint32_t)(obase + mrow0 * PQ) * 4u;
+          float fmx = 0.f;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float y = ldexpf(sum[v], e);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(y), rs_out, lane_off,
+                                                  (uint32_t)((8 * (v >> 2) + (v & 3)) * PQ) * 4u, 0);
+            fmx = fmaxf(fmx, fabsf(y));
+          }
+          amax = max(amax, __float_as_uint(fmx));
+        } else if (full_rows) {
 #pragma unroll
           for (int v = 0; v < 16; ++v)
             amax = max(amax, store_out<I32>(a.out, (uint32_t)(obase + (mrow0 + 8 * (v >> 2) + (v & 3)) * PQ), sum[v], e));
