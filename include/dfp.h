@@ -103,10 +103,15 @@ typedef enum dfp_role {
 
 typedef enum dfp_direction { DFP_FWD = 0, DFP_BWD_DATA = 1, DFP_BWD_WT = 2 } dfp_direction;
 
-/* Integer-product path (the measured choice is the default). */
+/* Integer-product path (the measured choice is the default).  AUTO and MFMA
+ * both build exact INT16 products from int8 MFMA on byte digits and give the
+ * same results; AUTO also weighs the work size when it picks the kernel (a
+ * filter of more than 36 blocks of 32 reduction indices takes the
+ * four-waves-per-SIMD kernel in phases only when the layer has enough output
+ * pixels), MFMA takes that kernel whenever its operand layout fits. */
 typedef enum dfp_path {
-  DFP_PATH_AUTO = 0, /* byte-split int8 MFMA                                   */
-  DFP_PATH_MFMA = 1, /* exact INT16 products from int8 MFMA on byte digits      */
+  DFP_PATH_AUTO = 0, /* byte-split int8 MFMA, kernel by shape and work size     */
+  DFP_PATH_MFMA = 1, /* byte-split int8 MFMA, four-waves-per-SIMD kernel first  */
   DFP_PATH_VALU = 2  /* one lane per output, VALU integer multiply-add          */
 } dfp_path;
 

@@ -249,7 +249,7 @@ static dfp_status conv_common(int32_t dir, const dfp_desc* d, const int16_t* a, 
   if (use_mfma(g, d->path, d->bits, dir)) {
     if (dir == DFP_BWD_WT) return launch_bwdw_mfma(g, a, sa, b, sb, out, partials, ws, st);
     // the filter prep kernel clears so before the main kernel raises it
-    return launch_conv_mfma(dir, g, a, sa, b, sb, out, so, partials, ws, st);
+    return launch_conv_mfma(dir, g, a, sa, b, sb, out, so, partials, ws, st, false, d->path == DFP_PATH_MFMA);
   }
   if (so && (rc = launch_scale_reset(so, st)) != DFP_OK) return rc;
   return launch_conv_valu(dir, g, a, sa, b, sb, out, so, partials, st);

@@ -35,11 +35,15 @@ struct ConvMfmaArgs {
   // adjacent), written for the four-waves-per-SIMD kernel; 0: [n][Hp][Wp][CG][32 B]
   int32_t plane;
   FastDiv div_pq, div_q;  // n / (Po*Qo) and n / Qo for output pixel indices
+  // four-waves-per-SIMD kernel: filter blocks kb0 .. kb0 + kbn - 1 in this launch;
+  // phase_flags bit 0: first phase (sums start at 0), bit 1: last (scale, store, max)
+  int32_t kb0, kbn, phase_flags;
 };
 
 // The plane layout and its kernel serve 32-channel blocks (Cin a multiple of
-// 32), full chunks of two blocks (T a multiple of 64, L = 64, or one chunk
-// over the whole reduction) and at most 36 blocks of resident filter digits.
+// 32) and full chunks of two blocks (T a multiple of 64): at L = 64 any number
+// of blocks, in phases of at most 36 resident blocks; one chunk over the whole
+// reduction (INT32 outputs) at most 36 blocks.
 bool conv_w16_eligible(int32_t Cin, int32_t T, int32_t L, bool i32);
 
 // Largest exponent-block count the blocked matrix-core kernel stages in LDS.
@@ -56,6 +60,7 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
 bool conv_mfma_supported(const Geom& g, int32_t dir);
 dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,
                             const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, void* ws,
-                            hipStream_t st, bool i32 = false);
+                            hipStream_t st, bool i32 = false,
+                            bool prefer_w16 = false);
 
 }  // namespace dfp

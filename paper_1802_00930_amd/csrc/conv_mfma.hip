@@ -1601,7 +1601,7 @@ constexpr int kWaves16 = 16;
 constexpr int kThreads16 = kWaves16 * 64;
 constexpr int32_t kW16MaxKB = 36;
 
-template <bool PARTIALS, bool I32 = false>
+template <bool PARTIALS, bool I32 = false, bool PHASED = false>
 __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a) {
   __shared__ __align__(16) uint8_t sA[kW16MaxKB * kStageA];
   __shared__ __align__(8) int32_t s_boff[kW16MaxKB];
@@ -1611,7 +1611,9 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   const int half = lane >> 5;
   const int col = lane & 31;
   const int32_t m0 = blockIdx.y * kMT;
-  const int32_t KB = a.KB, J = KB / 2, Cin = a.Cin;
+  // this launch's phase: filter blocks kb0 .. kb0 + KB - 1 (whole chunks)
+  const int32_t kb0 = PHASED ? a.kb0 : 0, KB = PHASED ? a.kbn : a.KB, J = KB / 2, Cin = a.Cin;
+  const bool first_phase = !PHASED || (a.phase_flags & 1) != 0, last_phase = !PHASED || (a.phase_flags & 2) != 0;
   // the launcher guarantees outputs and the B workspace index below 2^31
   const int32_t NP = (int32_t)a.NP, Qo = a.Qo, PQ = a.Po * a.Qo;
   // output scale exponent, read before any other memory operation is in flight
@@ -1626,7 +1628,8 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
       const int32_t sl = slot0 + lane;
       const int32_t kb = sl >> 8, sw = sl & 255;
       const int row = sw >> 2, piece = (sw & 3) ^ ((row >> 2) & 3);
-      const uint8_t* src = a.wsa + kb * a_block_bytes + ((int64_t)(m0 + row) * 2 + (piece >> 1)) * 32 + (piece & 1) * 16;
+      const uint8_t* src =
+          a.wsa + (kb0 + kb) * a_block_bytes + ((int64_t)(m0 + row) * 2 + (piece >> 1)) * 32 + (piece & 1) * 16;
       __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(sA + slot0 * 16), 16, 0, 0);
     }
   }
@@ -1640,7 +1643,7 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
     const int32_t r = tap / a.S, sx = tap - r * a.S;
     return a.rsign * (r * cpb * 4 * plane_bytes + sx * 16) + cb * 4 * plane_bytes;
   };
-  if ((int32_t)threadIdx.x < KB) s_boff[threadIdx.x] = boff_of(threadIdx.x);
+  if ((int32_t)threadIdx.x < KB) s_boff[threadIdx.x] = boff_of(kb0 + (int32_t)threadIdx.x);
 
   // ---- this workgroup's unit range (XCD x = workgroup id mod 8 gets adjacent ranges)
   const int32_t units = 2 * ((NP + 31) / 32);
@@ -1684,8 +1687,8 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   v4i b0h, b0l, b1h, b1l;
   if (my_units > 0) {
     cur_pix = pixel_off(unit_of(0));
-    load_b(b0h, b0l, cur_pix, 0);
-    load_b(b1h, b1l, cur_pix, boff_of(1));
+    load_b(b0h, b0l, cur_pix, boff_of(kb0));
+    load_b(b1h, b1l, cur_pix, boff_of(kb0 + 1));
     wait_vmcnt<4>();  // filter digits landed for this lane (its four B loads may be in flight)
   } else {
     wait_vmcnt<0>();
@@ -1712,6 +1715,21 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
       float sum[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) sum[v] = 0.f;
+      if (PHASED && !first_phase && gvalid) {  // the chunk sums so far, left in the output by the previous phase
+        if (full_rows && out_buf) {
+          const uint32_t lane_off = (uint32_t)(obase + mrow0 * PQ) * 4u;
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            sum[v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                rs_out, lane_off, (uint32_t)((8 * (v >> 2) + (v & 3)) * PQ) * 4u, 0));
+        } else {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
+            if (m < a.M) sum[v] = a.out[(uint32_t)(obase + m * PQ)];
+          }
+        }
+      }
       const uint8_t* ab = sA + msub * 2048;
       for (int32_t c = 0; c < J; ++c, ab += 2 * kStageA) {
         const bool last = c + 1 == J;
@@ -1726,10 +1744,24 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
         const v4i al1 = *reinterpret_cast<const v4i*>(ab + kStageA + ra_lo);
         mfma_tile(acc, ah1, al1, b1h, b1l, false);
         load_b(b1h, b1l, pix, bo.y);
-        if (!I32) flush_tile<PARTIALS>(acc, sum, c, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+        if (!I32) flush_tile<PARTIALS>(acc, sum, kb0 / 2 + c, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
       }
       if (I32) keep_tile_i32(acc, sum);
-      if (gvalid) {
+      if (PHASED && gvalid && !last_phase) {  // unscaled sums for the next phase
+        if (full_rows && out_buf) {
+          const uint32_t lane_off = (uint32_t)(obase + mrow0 * PQ) * 4u;
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(sum[v]), rs_out, lane_off,
+                                                  (uint32_t)((8 * (v >> 2) + (v & 3)) * PQ) * 4u, 0);
+        } else {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
+            if (m < a.M) a.out[(uint32_t)(obase + m * PQ)] = sum[v];
+          }
+        }
+      } else if (gvalid) {
         if (!I32 && full_rows && out_buf) {
           // buffer stores at a per-lane offset plus a uniform one per output row,
           // max |y| on floats (y is never NaN), two values per v_max3
@@ -1759,7 +1791,7 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
     }
   }
 
-  if (a.so) {
+  if (a.so && last_phase) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
     if (lane == 0) red[wave] = amax;
@@ -1782,7 +1814,9 @@ inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
 }  // namespace
 
 bool conv_w16_eligible(int32_t Cin, int32_t T, int32_t L, bool i32) {
-  return (Cin % 32) == 0 && (T % 64) == 0 && T / 32 <= kW16MaxKB && (i32 || L == 64);
+  // FP32 outputs at L = 64 take any number of blocks in phases of at most
+  // kW16MaxKB; single-chunk INT32 outputs one phase
+  return (Cin % 32) == 0 && (T % 64) == 0 && (i32 ? T / 32 <= kW16MaxKB : L == 64);
 }
 
 bool conv_mfma_supported(const Geom& g, int32_t dir) {
@@ -1823,7 +1857,7 @@ ConvMfmaPlan plan_conv_mfma(const Geom& g, int32_t dir) {
 
 dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,
                             const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, void* ws,
-                            hipStream_t st, bool i32) {
+                            hipStream_t st, bool i32, bool prefer_w16) {
   // fwd: a = x (B source), b = w.  bwd-data: a = dy (B source), b = w.
   const ConvMfmaPlan p = plan_conv_mfma(g, dir);
   const bool fwd = dir == DFP_FWD;
@@ -1832,8 +1866,17 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   int2* boff = reinterpret_cast<int2*>(xs + p.ws_b_bytes);
   const int32_t rsign = fwd ? 1 : -1;
   const int32_t tap_row_bytes = rsign * p.Wp * p.CG * 32, tap_col_bytes = rsign * p.CG * 32;
-  const bool plane = conv_w16_eligible(p.Cin, p.T, g.L, i32) && (int64_t)g.n * p.Po * p.Qo * p.M < (1ll << 31) &&
-                     p.ws_b_bytes < (1ll << 31);
+  bool plane = conv_w16_eligible(p.Cin, p.T, g.L, i32) && (int64_t)g.n * p.Po * p.Qo * p.M < (1ll << 31) &&
+               p.ws_b_bytes < (1ll << 31);
+  if (plane && p.KB > kW16MaxKB && !prefer_w16) {
+    // phases pay the kernel's fixed cost once each: taken only when every wave
+    // of a workgroup has a unit of work in each phase
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    const int64_t units = 2 * (((int64_t)g.n * p.Po * p.Qo + 31) / 32);
+    const int64_t gx = std::max<int64_t>(1, cus / (p.Mp / kMT));
+    plane = units >= gx * kWaves16;
+  }
   const PrepAArgs pa{b, wsa, p.M, p.Mp, p.Cin, g.r, g.s, p.T, p.KB, fwd ? 0 : 1, g.c, so, boff,
                      tap_row_bytes, tap_col_bytes};
   const int64_t a_total = (int64_t)p.KB * p.Mp * 8;
@@ -1941,6 +1984,9 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     gx = std::min<int64_t>(gx, (units + kWaves16 - 1) / kWaves16);
     return dim3((unsigned)gx, (unsigned)mtiles);
   };
+  args.kb0 = 0;
+  args.kbn = args.KB;
+  args.phase_flags = 3;
   if (i32) {
     // DFP-32 output: one chunk over the whole reduction (the caller checked L >= T)
     args.L = args.KB * 32;
@@ -1962,8 +2008,22 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     return DFP_OK;                                                                          \
   }
   if (w16_ok && args.L == 64) {
-    if (partials) DFP_LAUNCH(kid, (k_conv_mfma_w16<true>), w16_grid(), dim3(kThreads16), 0, st, args);
-    else DFP_LAUNCH(kid, (k_conv_mfma_w16<false>), w16_grid(), dim3(kThreads16), 0, st, args);
+    // phases of whole chunks, at most kW16MaxKB blocks each, as equal as possible;
+    // each launch continues the chunk sums the previous one left in the output
+    const int32_t chunks = args.KB / 2;
+    const int32_t nph = (args.KB + kW16MaxKB - 1) / kW16MaxKB;
+    const dim3 grid16 = w16_grid();
+    for (int32_t ph = 0; ph < nph; ++ph) {
+      const int32_t c0 = chunks * ph / nph, c1 = chunks * (ph + 1) / nph;
+      args.kb0 = 2 * c0;
+      args.kbn = 2 * (c1 - c0);
+      args.phase_flags = (ph == 0 ? 1 : 0) | (ph == nph - 1 ? 2 : 0);
+      if (nph == 1 && partials) DFP_LAUNCH(kid, (k_conv_mfma_w16<true>), grid16, dim3(kThreads16), 0, st, args);
+      else if (nph == 1) DFP_LAUNCH(kid, (k_conv_mfma_w16<false>), grid16, dim3(kThreads16), 0, st, args);
+      else if (partials)
+        DFP_LAUNCH(kid, (k_conv_mfma_w16<true, false, true>), grid16, dim3(kThreads16), 0, st, args);
+      else DFP_LAUNCH(kid, (k_conv_mfma_w16<false, false, true>), grid16, dim3(kThreads16), 0, st, args);
+    }
     return DFP_OK;
   }
   // the persistent and skewed kernels wait for their inline-assembly LDS reads

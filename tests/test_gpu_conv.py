@@ -111,12 +111,16 @@ def test_bwd_wt_band_no_partials(shape, G):
 # four-waves-per-SIMD kernel over the plane layout takes the forward (and the
 # backward-data where K is a multiple of 32), across one-chunk reductions
 # (T = 64), several 64-row tiles with a ragged last one, the largest resident
-# filter (36 blocks; its backward-data, 54 blocks, goes to another kernel),
-# strides, and fewer output pixels than one wave's unit.
+# filter (36 blocks), larger filters in phases of at most 36 blocks (the
+# chunk sums carried in the output between launches), strides, and fewer
+# output pixels than one wave's unit.
 W16_SHAPES = [
     (2, 64, 12, 12, 64, 3, 3, 1, 1),
     (2, 64, 16, 16, 128, 3, 3, 2, 1),  # strided: backward-data reads a dilated plane
     (2, 64, 20, 12, 64, 1, 1, 1, 0),   # no padding columns
+    (1, 256, 6, 6, 64, 3, 3, 1, 1),    # 72 filter blocks: two phases of 18 chunks
+    (1, 512, 4, 5, 96, 3, 3, 1, 1),    # 144 blocks: four phases
+    (2, 96, 6, 6, 416, 3, 3, 2, 1),    # 27 chunks: phases of 13 and 14; 416 rows, ragged tile
     (2, 64, 7, 7, 64, 1, 1, 1, 0),
     (1, 64, 13, 13, 200, 3, 3, 1, 1),
     (2, 128, 5, 5, 192, 3, 3, 1, 1),
