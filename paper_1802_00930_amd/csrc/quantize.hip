@@ -99,8 +99,16 @@ __global__ __launch_bounds__(kBlock) void k_amax(const float* __restrict__ src, 
 
 __global__ __launch_bounds__(kBlock) void k_amax_final(const uint32_t* __restrict__ part, int32_t nparts,
                                                        dfp_scale* __restrict__ s) {
+  // eight loads per lane in flight; an index past the end re-reads the last
+  // partial (the max is unchanged)
   uint32_t m = 0u;
-  for (int32_t i = threadIdx.x; i < nparts; i += kBlock) m = max(m, part[i]);
+  for (int32_t base = threadIdx.x; base < nparts; base += 8 * kBlock) {
+    uint32_t v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = part[min(base + k * kBlock, nparts - 1)];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) m = max(m, v[k]);
+  }
   m = block_max(m);
   if (threadIdx.x == 0) {
     s->amax_bits = m;
