@@ -89,6 +89,7 @@ BAND_SHAPES = [
     (2, 8, 12, 24, 16, 1, 1, 1, 0),
     (4, 32, 7, 8, 20, 3, 3, 1, 1),
     (2, 64, 24, 16, 64, 3, 3, 1, 1),
+    (2, 16, 10, 8, 80, 3, 3, 1, 1),  # dy digits: two 64-channel tiles, 160 indices (a partial 128-index tile)
 ]
 
 
