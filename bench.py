@@ -377,8 +377,8 @@ def main():
         copy_probe(a.copy_probe)
         return
     if a.gpus != 1:
-        print("bench.py: this build runs on one GPU only (the path is per-GPU); --gpus %d is not supported"
-              % a.gpus, file=sys.stderr)
+        print("bench.py: the DFP convolution path measures one GPU (its kernels work on one GPU's share); "
+              "--gpus %d is not supported" % a.gpus, file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_1802_00930_amd.workloads import WORKLOADS, layer_inputs
