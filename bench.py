@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--no-dfp32", action="store_true", help="skip the DFP-32-output variant of the step")
     ap.add_argument("--no-gemm", action="store_true", help="skip the GEMM measurements")
     ap.add_argument("--no-train-ops", action="store_true", help="skip the BN / SGD measurements")
+    ap.add_argument("--no-layers", action="store_true",
+                    help="skip the per-layer sweep (ResNet-50 conv4_x 1x1 pair, VGG-16 conv1_2 / conv3_3, all 53 "
+                         "ResNet-50 convolutions)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES five times (counter calibration)")
@@ -371,6 +374,49 @@ def cpu_baseline(layer, x, w, dy, L, G, rounding, seed, budget_s):
     }
 
 
+LAYER_WORKLOADS = ("resnet50_conv4x_1x1", "vgg16_conv1_2_conv3_3", "resnet50_all_convs")
+DIRECTIONS = (("fwd", "conv_fwd_"), ("bwd_data", "conv_bwd_data_"), ("bwd_wt", "conv_bwd_wt_"))
+
+
+def layer_sweep(a, dev):
+    """The whole step on every layer of the other benchmark workloads, each at
+    its own size, rounding and seed (inputs from the same host recipe as the
+    headline): step time, and per direction the convolution kernels' time per
+    step (all launches of the direction, e.g. phases) with TOPS and the
+    fraction of the peak of the product path that ran."""
+    from paper_1802_00930_amd.workloads import WORKLOADS, layer_inputs
+    res = {}
+    for name in LAYER_WORKLOADS:
+        wl = WORKLOADS[name]
+        rows, total_s, total_ops = [], 0.0, 0.0
+        for i in range(len(wl.layers)):
+            layer, x, w, dy = layer_inputs(wl, i)
+            ops = 2.0 * layer.macs
+            for rounding in wl.roundings:
+                st = Step(layer, x, w, dy, a.chunk, rounding, wl.seed, a.path, dev, a.seg_chunks)
+                sec, _ = timed(st, 3, 1)
+                _, recs = timed(st, 3, 0, profile=True)
+                row = {"layer": layer.name, "shape": "N%d C%d %dx%d K%d %dx%d s%d p%d" % (
+                    layer.n, layer.c, layer.h, layer.w, layer.k, layer.r, layer.s, layer.stride, layer.pad),
+                    "rounding": rounding, "step_ms": round(sec * 1e3, 4), "step_tops": round(3 * ops / sec / 1e12, 2)}
+                for dname, prefix in DIRECTIONS:
+                    ks = [(n_, ms) for n_, ms in recs if n_.startswith(prefix)]
+                    dsec = sum(ms for _, ms in ks) / 3 * 1e-3
+                    mfma = all(n_.endswith(("_mfma", "_i32")) for n_, _ in ks)
+                    tops = ops / dsec / 1e12 if dsec > 0 else 0.0
+                    row[dname] = {"us": round(dsec * 1e6, 2), "tops": round(tops, 1),
+                                  "frac": round(tops / (PEAK_INT16_BYTESPLIT_TOPS if mfma else PEAK_VALU_DOT2_TOPS), 4),
+                                  "path": "mfma" if mfma else "valu"}
+                rows.append(row)
+                total_s += sec
+                total_ops += 3 * ops
+                del st
+            del x, w, dy
+        res[name] = {"layers": rows, "sum_step_ms": round(total_s * 1e3, 3),
+                     "tops_over_steps": round(total_ops / total_s / 1e12, 2)}
+    return res
+
+
 def main():
     a = parse()
     if a.copy_probe:
@@ -521,6 +567,7 @@ def main():
         "dfp32_outputs": dfp32,
         "gemm": gemm,
         "train_ops": train_ops,
+        "layers": None if a.no_layers else layer_sweep(a, dev),
     }
     if not a.no_cpu:
         out["cpu_baseline"] = cpu_baseline(layer, x, w, dy, a.chunk, a.seg_chunks, rounding, seed, a.cpu_seconds)

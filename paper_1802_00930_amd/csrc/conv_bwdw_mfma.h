@@ -13,6 +13,7 @@ struct BwdwPlan {
   int32_t nch_max, rows_max, band_ch_stride;
   int64_t band_bytes, smem_bytes;       // LDS band (all channels of a column tile) + offset table
   int64_t ad_bytes, xp_bytes, u_bytes, bytes;
+  int64_t sub_bytes;                    // strided 1x1: the subsampled input, at the end of the workspace
 };
 
 struct BwdwArgs {

@@ -1158,7 +1158,41 @@ static const BandKernelsSafe& band_kernels_safe() {
   return safe;
 }
 
+// A 1x1 convolution without padding and with stride (sh, sw) reads input
+// pixel (p*sh, q*sw) for output pixel (p, q), so its weight gradient is the
+// unit-stride one over the subsampled input x[:, :, ::sh, ::sw] (N x C x P x
+// Q), with the same reduction index t = (n*P + p)*Q + q and hence the same
+// chunks and segments.  The subsampled input is gathered into the workspace
+// and the unit-stride kernels run on it (their input band then spans P*Q
+// pixels per image instead of H*W).
+static bool strided_1x1(const Geom& g) {
+  return g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0 && (g.sh > 1 || g.sw > 1);
+}
+static Geom subsampled(const Geom& g) {
+  Geom u = g;
+  u.h = g.p;
+  u.w = g.q;
+  u.sh = u.sw = 1;
+  return u;
+}
+
+__global__ __launch_bounds__(256) void k_subsample(const int16_t* __restrict__ x, int16_t* __restrict__ xs,
+                                                   int64_t total, int32_t H, int32_t W, int32_t P, int32_t Q,
+                                                   int32_t sh, int32_t sw) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t nc = i / ((int64_t)P * Q);
+    const int32_t pq = (int32_t)(i - nc * P * Q), pp = pq / Q, qq = pq - pp * Q;
+    xs[i] = x[(nc * H + (int64_t)pp * sh) * W + (int64_t)qq * sw];
+  }
+}
+
 BwdwPlan plan_bwdw_mfma(const Geom& g) {
+  if (strided_1x1(g)) {
+    BwdwPlan p = plan_bwdw_mfma(subsampled(g));
+    p.sub_bytes = align256((int64_t)g.n * g.c * g.p * g.q * 2);
+    p.bytes += p.sub_bytes;
+    return p;
+  }
   BwdwPlan p{};
   p.T = (int64_t)g.n * g.p * g.q;
   p.KBT = (p.T + 31) / 32;
@@ -1223,6 +1257,16 @@ bool bwdw_mfma_supported(const Geom& g) {
 
 dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx, const int16_t* dy,
                             const dfp_scale* sdy, float* dw, int32_t* partials, void* ws, hipStream_t st) {
+  if (strided_1x1(g)) {
+    const BwdwPlan p = plan_bwdw_mfma(g);
+    int16_t* xs = reinterpret_cast<int16_t*>(reinterpret_cast<uint8_t*>(ws) + (p.bytes - p.sub_bytes));
+    const int64_t total = (int64_t)g.n * g.c * g.p * g.q;
+    const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+    DFP_LAUNCH(K_XPREP, k_subsample, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(256), 0, st, x, xs, total,
+               g.h, g.w, g.p, g.q, g.sh, g.sw);
+    // the subsampled plan's workspace ends where xs begins
+    return launch_bwdw_mfma(subsampled(g), xs, sx, dy, sdy, dw, partials, ws, st);
+  }
   const BwdwPlan p = plan_bwdw_mfma(g);
   uint8_t* base = reinterpret_cast<uint8_t*>(ws);
   uint8_t* ad = base;

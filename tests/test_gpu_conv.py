@@ -99,6 +99,21 @@ def test_bwd_wt_band_shapes(shape, L, G):
     run_all(shape, L, G=G)
 
 
+# Strided 1x1 layers without padding (ResNet-50's downsampling projections):
+# the weight gradient runs on the subsampled input with unit stride, so the
+# MFMA path takes layers whose strided input band would not fit in LDS (the
+# first shape), at odd sizes and stride 3 too; bit-exact against the oracle's
+# strided sum.
+@pytest.mark.parametrize("shape", [(2, 256, 16, 16, 64, 1, 1, 2, 0), (1, 40, 15, 13, 24, 1, 1, 3, 0),
+                                   (2, 130, 14, 14, 96, 1, 1, 2, 0)])
+@pytest.mark.parametrize("L,G", [(64, 0), (32, 3), (64, 1)])
+def test_bwd_wt_strided_1x1(shape, L, G):
+    n, c, h, w, k, r, s, st, pd = shape
+    d = dfp.make_desc(n, c, h, w, k, r, s, st, pd, chunk_len=L, seg_chunks=G)
+    assert dfp.workspace_bytes(d, dfp.BWD_WT) > 0  # the MFMA path (the VALU path needs no workspace)
+    run_all(shape, L, G=G)
+
+
 # Without partials, L = 64 runs the eight-wave band kernel (with partials the
 # two-tile one): segments of one chunk, of an odd number of chunks (a last band
 # of one chunk), several bands, one segment per layer.
