@@ -92,9 +92,10 @@ def copy_probe(nbytes):
 class Step:
     """Device buffers and the ABI calls of one step."""
 
-    def __init__(self, layer, x, w, dy, L, rounding, seed, path, dev, G=0):
+    def __init__(self, layer, x, w, dy, L, rounding, seed, path, dev, G=0, bwd_data=True):
         import torch
         from paper_1802_00930_amd import dfp
+        self.bwd_data = bwd_data  # False: the network's first layer, whose input gradient training never uses
         self.dfp = dfp
         self.torch = torch
         self.layer = layer
@@ -119,8 +120,9 @@ class Step:
         dfp.dfp_quantize(d, dfp.ROLE_DY, self.fdy, self.qdy, self.sdy)
         dfp.dfp_conv_fwd(d, self.qx, self.sx, self.qw, self.sw, self.y, self.sy, self.ws[0])
         dfp.dfp_downconvert(d, dfp.ROLE_Y, self.y, self.qy, self.sy, amax_ready=True)
-        dfp.dfp_conv_bwd_data(d, self.qdy, self.sdy, self.qw, self.sw, self.dx, self.sdx, self.ws[1])
-        dfp.dfp_downconvert(d, dfp.ROLE_DX, self.dx, self.qdx, self.sdx, amax_ready=True)
+        if self.bwd_data:
+            dfp.dfp_conv_bwd_data(d, self.qdy, self.sdy, self.qw, self.sw, self.dx, self.sdx, self.ws[1])
+            dfp.dfp_downconvert(d, dfp.ROLE_DX, self.dx, self.qdx, self.sdx, amax_ready=True)
         dfp.dfp_conv_bwd_weights(d, self.qx, self.sx, self.qdy, self.sdy, self.dw, self.ws[2])
 
 
@@ -383,7 +385,10 @@ def layer_sweep(a, dev):
     its own size, rounding and seed (inputs from the same host recipe as the
     headline): step time, and per direction the convolution kernels' time per
     step (all launches of the direction, e.g. phases) with TOPS and the
-    fraction of the peak of the product path that ran."""
+    fraction of the peak of the product path that ran.  The network's first
+    layer (3 input channels) is summed without its backward-data and DC(dx),
+    which training does not use; its row still times them, in a second run of
+    the full step."""
     from paper_1802_00930_amd.workloads import WORKLOADS, layer_inputs
     res = {}
     for name in LAYER_WORKLOADS:
@@ -392,10 +397,16 @@ def layer_sweep(a, dev):
         for i in range(len(wl.layers)):
             layer, x, w, dy = layer_inputs(wl, i)
             ops = 2.0 * layer.macs
+            stem = name == "resnet50_all_convs" and layer.c == 3
             for rounding in wl.roundings:
                 st = Step(layer, x, w, dy, a.chunk, rounding, wl.seed, a.path, dev, a.seg_chunks)
                 sec, _ = timed(st, 3, 1)
                 _, recs = timed(st, 3, 0, profile=True)
+                full_sec = None
+                if stem:  # the step training runs: no input gradient
+                    full_sec = sec
+                    st.bwd_data = False
+                    sec, _ = timed(st, 3, 1)
                 row = {"layer": layer.name, "shape": "N%d C%d %dx%d K%d %dx%d s%d p%d" % (
                     layer.n, layer.c, layer.h, layer.w, layer.k, layer.r, layer.s, layer.stride, layer.pad),
                     "rounding": rounding, "step_ms": round(sec * 1e3, 4), "step_tops": round(3 * ops / sec / 1e12, 2)}
@@ -407,9 +418,14 @@ def layer_sweep(a, dev):
                     row[dname] = {"us": round(dsec * 1e6, 2), "tops": round(tops, 1),
                                   "frac": round(tops / (PEAK_INT16_BYTESPLIT_TOPS if mfma else PEAK_VALU_DOT2_TOPS), 4),
                                   "path": "mfma" if mfma else "valu"}
+                if stem:
+                    row["step_ms"] = round(sec * 1e3, 4)
+                    row["step_tops"] = round(2 * ops / sec / 1e12, 2)
+                    row["step_ms_with_bwd_data"] = round(full_sec * 1e3, 4)
+                    row["bwd_data_not_in_sum"] = True
                 rows.append(row)
                 total_s += sec
-                total_ops += 3 * ops
+                total_ops += (2 if stem else 3) * ops
                 del st
             del x, w, dy
         res[name] = {"layers": rows, "sum_step_ms": round(total_s * 1e3, 3),
