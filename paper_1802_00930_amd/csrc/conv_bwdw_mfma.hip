@@ -402,6 +402,66 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_mfma(BwdwArgs a) {
   }
 }
 
+// Unit-stride 1x1 layers without padding: x[n][c][p][q] is a C x T matrix of
+// the same form as dy (K x T, t = (n*P + p)*Q + q), so both operands are
+// prepared by prep_dy_item as digit blocks [KBT][rows][2][16 hi | 16 lo].  In
+// that layout a lane's MFMA operand (row lane % 32, indices 16 * (lane / 32)
+// .. + 15 of a 32-index block) is one 32-byte piece, and the 64 lanes of a
+// wave read 2 KiB of contiguous digits per operand and block, straight into
+// registers (the four waves of a workgroup share each row and column piece
+// through L1).  Workgroup: a 64 x 64 tile (2 x 2 wave tiles of 32 x 32) of
+// one segment; the operands of block kb + 1 are loaded while block kb is
+// multiplied.  Chunks are whole blocks (L a multiple of 32) and digits past T
+// are zero, so no masking is needed.  Chunk sums and segment output as in the
+// kernels above.
+constexpr int k1x1Threads = 256;
+__global__ __launch_bounds__(k1x1Threads, 4) void k_bwdw_1x1(BwdwArgs a, const uint8_t* __restrict__ bd,
+                                                            int32_t Cp) {
+  const BwdwTile tl = bwdw_tile(a);
+  if (tl.seg >= a.nseg) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, lc = lane & 31;
+  const int32_t m0 = tl.ty * 64 + (wave >> 1) * 32;  // the wave's 32 rows (k)
+  const int32_t c0 = tl.tx * 64 + (wave & 1) * 32;   // and 32 columns (c)
+  const int64_t t_seg0 = (int64_t)tl.seg * a.G * a.L;
+  const int64_t t_seg1 = min(t_seg0 + (int64_t)a.G * a.L, a.T);
+  const int64_t kb_begin = t_seg0 / 32, kb_end = (t_seg1 + 31) / 32;
+  const int32_t chunk_blocks = a.L / 32;
+  const int64_t astep = (int64_t)a.Mp * 64, bstep = (int64_t)Cp * 64;
+  const uint4* ap = reinterpret_cast<const uint4*>(a.ad + kb_begin * astep + ((int64_t)(m0 + lc) * 2 + half) * 32);
+  const uint4* bp = reinterpret_cast<const uint4*>(bd + kb_begin * bstep + ((int64_t)(c0 + lc) * 2 + half) * 32);
+  Acc3 acc;
+  float sum[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) sum[v] = 0.f;
+  uint4 ah = ap[0], al = ap[1], bh = bp[0], bl = bp[1];
+  int32_t blk = 0;
+  for (int64_t kb = kb_begin; kb < kb_end; ++kb) {
+    const v4i ahi = {(int)ah.x, (int)ah.y, (int)ah.z, (int)ah.w}, alo = {(int)al.x, (int)al.y, (int)al.z, (int)al.w};
+    const v4i bhi = {(int)bh.x, (int)bh.y, (int)bh.z, (int)bh.w}, blo = {(int)bl.x, (int)bl.y, (int)bl.z, (int)bl.w};
+    if (kb + 1 < kb_end) {
+      ap += astep / 16;
+      bp += bstep / 16;
+      ah = ap[0]; al = ap[1]; bh = bp[0]; bl = bp[1];
+    }
+    mfma_tile(acc, ahi, alo, bhi, blo, blk == 0);
+    if (++blk == chunk_blocks || kb == kb_end - 1) {
+      flush_tile<false>(acc, sum, 0, nullptr, a.O, 0, a.C, 0, a.K, false);
+      blk = 0;
+    }
+  }
+  const int32_t c = c0 + lc;
+  const int32_t e = a.ea->exp + a.eb->exp;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int32_t m = m0 + 8 * (v >> 2) + 4 * half + (v & 3);
+    if (c < a.C && m < a.K) {
+      const int64_t o = (int64_t)m * a.C + c;
+      if (a.nseg == 1) a.out[o] = ldexpf(sum[v], e);
+      else a.useg[(int64_t)tl.seg * a.O + o] = sum[v];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Band kernel: unit strides, output rows of a multiple of 8, filter width at
 // most 4, chunks of whole 32-index blocks.  Reduction indices then come in
@@ -1168,6 +1228,10 @@ static const BandKernelsSafe& band_kernels_safe() {
 static bool strided_1x1(const Geom& g) {
   return g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0 && (g.sh > 1 || g.sw > 1);
 }
+// Unit-stride 1x1 layers without padding (x is then a C x T matrix like dy).
+static bool unit_1x1(const Geom& g) {
+  return g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0 && g.sh == 1 && g.sw == 1;
+}
 static Geom subsampled(const Geom& g) {
   Geom u = g;
   u.h = g.p;
@@ -1223,6 +1287,7 @@ BwdwPlan plan_bwdw_mfma(const Geom& g) {
   p.ad_bytes = align256(p.KBT * p.Mp * 64);
   // pair layout [C][N*Hpad][Wpad] u16, or the band kernel's byte planes with 16 spare bytes per row
   p.xp_bytes = align256((int64_t)g.c * g.n * p.Hpad * (2 * p.Wpad + 16));
+  if (unit_1x1(g)) p.xp_bytes = std::max<int64_t>(p.xp_bytes, align256(p.KBT * ((g.c + 63) / 64 * 64) * 64));
   p.u_bytes = p.nseg > 1 ? align256((int64_t)p.nseg * g.k * g.c * RS * 4) : 0;
   p.bytes = p.ad_bytes + p.xp_bytes + p.u_bytes;
   return p;
@@ -1274,6 +1339,33 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   float* useg = reinterpret_cast<float*>(base + p.ad_bytes + p.xp_bytes);
   const DyPrep dq{dy, ad, g.k, p.Mp, g.p * g.q, (int32_t)p.T, (int32_t)p.KBT};
   const int64_t dy_blocks = (p.KBT * p.Mp * 2 + 255) / 256;
+  // unit-stride 1x1 without partials: both operands as digit blocks (the
+  // digit preparation indexes elements with 32 bits)
+  if (unit_1x1(g) && !partials && (g.L % 32) == 0 && (int64_t)g.n * std::max(g.c, g.k) * g.p * g.q < (1ll << 31)) {
+    const int32_t Cp = (g.c + 63) / 64 * 64;
+    uint8_t* bd = reinterpret_cast<uint8_t*>(xp);
+    const DyPrep dqx{x, bd, g.c, Cp, g.p * g.q, (int32_t)p.T, (int32_t)p.KBT};
+    DFP_LAUNCH(K_WPREP, k_prep_dy, dim3((unsigned)dy_blocks), dim3(256), 0, st, dq);
+    DFP_LAUNCH(K_XPREP, k_prep_dy, dim3((unsigned)((p.KBT * Cp * 2 + 255) / 256)), dim3(256), 0, st, dqx);
+    BwdwArgs args{};
+    args.ad = ad;
+    args.ea = sx;
+    args.eb = sdy;
+    args.out = dw;
+    args.useg = useg;
+    args.T = p.T;
+    args.O = (int64_t)g.k * g.c;
+    args.K = g.k; args.Mp = p.Mp; args.C = g.c; args.R = 1; args.S = 1;
+    args.L = g.L; args.G = g.G; args.nseg = p.nseg;
+    args.ntx = Cp / 64;
+    args.nty = p.Mp / 64;
+    DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_1x1, dim3((unsigned)(p.nseg * args.ntx * args.nty)), dim3(k1x1Threads), 0, st,
+               args, bd, Cp);
+    if (p.nseg > 1)
+      DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 63) / 64)), dim3(64), 0, st, useg, dw,
+                 args.O, p.nseg, sx, sdy);
+    return DFP_OK;
+  }
   const BandLayout bl = band_layout(g, p);
   // the band kernels address both digit tensors with 32-bit buffer offsets
   const BandKernelsSafe& safe = band_kernels_safe();

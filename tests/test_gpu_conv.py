@@ -114,6 +114,17 @@ def test_bwd_wt_strided_1x1(shape, L, G):
     run_all(shape, L, G=G)
 
 
+# Unit-stride 1x1 layers without padding, without partials: both operands as
+# digit blocks (channel counts that are not multiples of 64, reductions that
+# end mid-chunk, one to many segments; the strided shape takes the same
+# kernel on its subsampled input).  0 ulp against the oracle.
+@pytest.mark.parametrize("shape", [(2, 96, 7, 7, 130, 1, 1, 1, 0), (1, 64, 14, 14, 64, 1, 1, 1, 0),
+                                   (3, 40, 5, 9, 24, 1, 1, 1, 0), (2, 256, 16, 16, 64, 1, 1, 2, 0)])
+@pytest.mark.parametrize("L,G", [(64, 0), (32, 3), (128, 1), (64, 10 ** 6)])
+def test_bwd_wt_1x1_digit_blocks(shape, L, G):
+    run_all(shape, L, G=G, partials=False)
+
+
 # Without partials, L = 64 runs the eight-wave band kernel (with partials the
 # two-tile one): segments of one chunk, of an odd number of chunks (a last band
 # of one chunk), several bands, one segment per layer.
