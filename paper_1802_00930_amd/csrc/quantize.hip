@@ -48,36 +48,36 @@ __global__ void k_scale_reset(dfp_scale* s) {
   }
 }
 
-// Max of |src| bit patterns in two stages with no atomics.  Stage 1: the
-// 16-byte vectors are cut into one contiguous, equal range per workgroup
-// (up to kAmaxMaxParts workgroups, about eight per CU, so every range is read
-// in one pass with four loads per lane in flight); workgroup b stores its max
-// in part[b].  part is the destination INT16 buffer, which the rounding pass
+// Max of |src| bit patterns in two stages with no atomics.  Stage 1: up to
+// kAmaxMaxParts workgroups (about eight per CU) read the 16-byte vectors in
+// grid-stride steps of 1024 vectors per workgroup, four loads per lane in
+// flight; workgroup b stores its max in part[b].  part is the destination INT16 buffer, which the rounding pass
 // overwrites only after stage 2 has read it.  Stage 2: one workgroup reduces
 // the partial maxima into the scale and clears its flags.  A tensor small
 // enough for one workgroup goes straight to the scale in stage 1.
 constexpr int kAmaxUnroll = 4;
-constexpr int kAmaxChunk = kBlock * kAmaxUnroll;  // 16-byte vectors per chunk (INT32 max pass)
+constexpr int kAmaxChunk = kBlock * kAmaxUnroll;  // 16-byte vectors per workgroup and step
 constexpr int kAmaxMaxParts = 2048;
 
 __device__ __forceinline__ uint32_t abs_max4(uint4 v) {
   return max(max(v.x & 0x7fffffffu, v.y & 0x7fffffffu), max(v.z & 0x7fffffffu, v.w & 0x7fffffffu));
 }
 
-// Range of workgroup b: per vectors each, the first rem workgroups one more.
-__global__ __launch_bounds__(kBlock) void k_amax(const float* __restrict__ src, int64_t n, int64_t per, int32_t rem,
+// Workgroup b reads vectors b * 1024 + i .. in steps of the whole grid (1024
+// vectors per workgroup and step, four loads per lane in flight), so at any
+// moment the grid streams one contiguous region.
+__global__ __launch_bounds__(kBlock) void k_amax(const float* __restrict__ src, int64_t n,
                                                  uint32_t* __restrict__ part, dfp_scale* __restrict__ s) {
   const uint4* src4 = reinterpret_cast<const uint4*>(src);
   const int64_t n4 = n >> 2;
-  const int32_t b = blockIdx.x;
-  const int64_t lo = per * b + min(b, rem), hi = lo + per + (b < rem ? 1 : 0);
   uint32_t m[kAmaxUnroll] = {0u, 0u, 0u, 0u};
   // all four loads of a step are issued before any is reduced; a load past
-  // the range re-reads the range's last vector (the max is unchanged)
-  for (int64_t base = lo + threadIdx.x; base < hi; base += kAmaxUnroll * kBlock) {
+  // the end re-reads the last vector (the max is unchanged)
+  for (int64_t base = (int64_t)blockIdx.x * kAmaxChunk + threadIdx.x; base < n4;
+       base += (int64_t)gridDim.x * kAmaxChunk) {
     uint4 v[kAmaxUnroll];
 #pragma unroll
-    for (int k = 0; k < kAmaxUnroll; ++k) v[k] = src4[min(base + k * kBlock, hi - 1)];
+    for (int k = 0; k < kAmaxUnroll; ++k) v[k] = src4[min(base + k * kBlock, n4 - 1)];
 #pragma unroll
     for (int k = 0; k < kAmaxUnroll; ++k) m[k] = max(m[k], abs_max4(v[k]));
   }
@@ -575,12 +575,11 @@ dfp_status launch_amax(const float* src, int64_t n, int16_t* scratch, dfp_scale*
   int64_t parts = (n / 4 + kBlock * kAmaxUnroll - 1) / (kBlock * kAmaxUnroll);
   parts = std::min<int64_t>(std::min<int64_t>(parts, kAmaxMaxParts), n / 2);
   if (parts <= 1) {
-    DFP_LAUNCH(K_AMAX, k_amax, dim3(1), dim3(kBlock), 0, st, src, n, n / 4, 0, (uint32_t*)nullptr, s);
+    DFP_LAUNCH(K_AMAX, k_amax, dim3(1), dim3(kBlock), 0, st, src, n, (uint32_t*)nullptr, s);
     return DFP_OK;
   }
   uint32_t* part = reinterpret_cast<uint32_t*>(scratch);
-  DFP_LAUNCH(K_AMAX, k_amax, dim3((unsigned)parts), dim3(kBlock), 0, st, src, n, (n / 4) / parts,
-             (int32_t)((n / 4) % parts), part, s);
+  DFP_LAUNCH(K_AMAX, k_amax, dim3((unsigned)parts), dim3(kBlock), 0, st, src, n, part, s);
   DFP_LAUNCH(K_AMAX, k_amax_final, dim3(1), dim3(kBlock), 0, st, part, (int32_t)parts, s);
   return DFP_OK;
 }
