@@ -118,8 +118,11 @@ def test_bwd_wt_strided_1x1(shape, L, G):
 # digit blocks (channel counts that are not multiples of 64, reductions that
 # end mid-chunk, one to many segments; the strided shape takes the same
 # kernel on its subsampled input).  0 ulp against the oracle.
+# P*Q a multiple of 16 (the last four shapes) reads the INT16 tensors directly.
 @pytest.mark.parametrize("shape", [(2, 96, 7, 7, 130, 1, 1, 1, 0), (1, 64, 14, 14, 64, 1, 1, 1, 0),
-                                   (3, 40, 5, 9, 24, 1, 1, 1, 0), (2, 256, 16, 16, 64, 1, 1, 2, 0)])
+                                   (3, 40, 5, 9, 24, 1, 1, 1, 0), (2, 256, 16, 16, 64, 1, 1, 2, 0),
+                                   (2, 96, 8, 8, 130, 1, 1, 1, 0), (3, 40, 4, 12, 24, 1, 1, 1, 0),
+                                   (1, 64, 16, 16, 64, 1, 1, 1, 0)])
 @pytest.mark.parametrize("L,G", [(64, 0), (32, 3), (128, 1), (64, 10 ** 6)])
 def test_bwd_wt_1x1_digit_blocks(shape, L, G):
     run_all(shape, L, G=G, partials=False)
