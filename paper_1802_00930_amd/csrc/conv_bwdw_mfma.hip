@@ -1300,6 +1300,7 @@ static Geom subsampled(const Geom& g) {
   return u;
 }
 
+namespace {
 __global__ __launch_bounds__(256) void k_subsample(const int16_t* __restrict__ x, int16_t* __restrict__ xs,
                                                    int64_t total, int32_t H, int32_t W, int32_t P, int32_t Q,
                                                    int32_t sh, int32_t sw) {
@@ -1309,6 +1310,7 @@ __global__ __launch_bounds__(256) void k_subsample(const int16_t* __restrict__ x
     xs[i] = x[(nc * H + (int64_t)pp * sh) * W + (int64_t)qq * sw];
   }
 }
+}  // namespace
 
 BwdwPlan plan_bwdw_mfma(const Geom& g) {
   if (strided_1x1(g)) {
