@@ -1,5 +1,6 @@
 // C ABI of libdfp: host-side validation and dispatch.  Every argument check
 // runs before the first HIP call, so an invalid call enqueues nothing.
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -120,7 +121,9 @@ bool use_mfma(const Geom& g, int32_t path, int32_t bits, int32_t dir) {
 
 size_t workspace_bytes(const Geom& g, int32_t dir, int32_t path, int32_t bits) {
   if (!use_mfma(g, path, bits, dir)) return 0;
-  if (dir == DFP_FWD || dir == DFP_BWD_DATA) return (size_t)plan_conv_mfma(g, dir).bytes;
+  if (dir == DFP_BWD_DATA)  // room for either route (partials take the general one)
+    return (size_t)std::max<int64_t>(plan_conv_mfma(g, dir).bytes, conv_bwd_data_sub_bytes(g));
+  if (dir == DFP_FWD) return (size_t)plan_conv_mfma(g, dir).bytes;
   return (size_t)plan_bwdw_mfma(g).bytes;
 }
 
@@ -248,6 +251,8 @@ static dfp_status conv_common(int32_t dir, const dfp_desc* d, const int16_t* a, 
   hipStream_t st = (hipStream_t)stream;
   if (use_mfma(g, d->path, d->bits, dir)) {
     if (dir == DFP_BWD_WT) return launch_bwdw_mfma(g, a, sa, b, sb, out, partials, ws, st);
+    if (dir == DFP_BWD_DATA && !partials && conv_bwd_data_sub_bytes(g) > 0)
+      return launch_conv_bwd_data_sub(g, a, sa, b, sb, out, so, ws, st, d->path == DFP_PATH_MFMA);
     // the filter prep kernel clears so before the main kernel raises it
     return launch_conv_mfma(dir, g, a, sa, b, sb, out, so, partials, ws, st, false, d->path == DFP_PATH_MFMA);
   }

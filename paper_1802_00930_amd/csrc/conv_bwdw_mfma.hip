@@ -1301,14 +1301,16 @@ static Geom subsampled(const Geom& g) {
 }
 
 namespace {
+// Thread (x, y): in-plane position pq of every subsampled plane (n, c) =
+// y, y + gridDim.y, ...; its source offset in the plane is computed once.
 __global__ __launch_bounds__(256) void k_subsample(const int16_t* __restrict__ x, int16_t* __restrict__ xs,
-                                                   int64_t total, int32_t H, int32_t W, int32_t P, int32_t Q,
+                                                   int64_t planes, int32_t H, int32_t W, int32_t P, int32_t Q,
                                                    int32_t sh, int32_t sw) {
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
-    const int64_t nc = i / ((int64_t)P * Q);
-    const int32_t pq = (int32_t)(i - nc * P * Q), pp = pq / Q, qq = pq - pp * Q;
-    xs[i] = x[(nc * H + (int64_t)pp * sh) * W + (int64_t)qq * sw];
-  }
+  const int32_t pq = blockIdx.x * 256 + threadIdx.x;
+  if (pq >= P * Q) return;
+  const int32_t pp = pq / Q, qq = pq - pp * Q;
+  const int32_t off = pp * sh * W + qq * sw;
+  for (int64_t nc = blockIdx.y; nc < planes; nc += gridDim.y) xs[nc * P * Q + pq] = x[nc * H * W + off];
 }
 }  // namespace
 
@@ -1387,10 +1389,11 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   if (strided_1x1(g)) {
     const BwdwPlan p = plan_bwdw_mfma(g);
     int16_t* xs = reinterpret_cast<int16_t*>(reinterpret_cast<uint8_t*>(ws) + (p.bytes - p.sub_bytes));
-    const int64_t total = (int64_t)g.n * g.c * g.p * g.q;
-    const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
-    DFP_LAUNCH(K_XPREP, k_subsample, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(256), 0, st, x, xs, total,
-               g.h, g.w, g.p, g.q, g.sh, g.sw);
+    const int64_t planes = (int64_t)g.n * g.c;
+    const int32_t gx = (g.p * g.q + 255) / 256;
+    const int64_t gy = std::max<int64_t>(1, std::min<int64_t>(planes, std::max(1, 16384 / gx)));
+    DFP_LAUNCH(K_XPREP, k_subsample, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, st, x, xs, planes, g.h, g.w,
+               g.p, g.q, g.sh, g.sw);
     // the subsampled plan's workspace ends where xs begins
     return launch_bwdw_mfma(subsampled(g), xs, sx, dy, sdy, dw, partials, ws, st);
   }

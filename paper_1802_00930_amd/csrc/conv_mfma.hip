@@ -2064,4 +2064,58 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
   return DFP_ERR_PARAM;
 }
 
+// Backward-data of a 1x1 convolution without padding and with stride
+// (sh, sw): dx[n][c][h][w] has the single term set k = 0 .. K-1 of
+// dy[n][k][h/sh][w/sw] w[k][c] where sh divides h and sw divides w, and no term
+// elsewhere (0).  The sampled pixels are the unit-stride backward-data over
+// the P x Q grid, with the same reduction index k and hence the same chunks,
+// so that runs into the end of the workspace and k_scatter_strided spreads it
+// over dx; the zeros leave the epilogue's max unchanged.  (The general route
+// runs the reduction over a zero-dilated dy, three quarters of it zeros at
+// stride 2.)
+namespace {
+// Thread (x, y): in-plane position hw of every dx plane (n, c) = y, y +
+// gridDim.y, ...; the position's row / column split is done once.
+__global__ __launch_bounds__(256) void k_scatter_strided(const float* __restrict__ sub, float* __restrict__ dx,
+                                                         int64_t planes, int32_t H, int32_t W, int32_t P, int32_t Q,
+                                                         int32_t sh, int32_t sw) {
+  const int32_t hw = blockIdx.x * 256 + threadIdx.x;
+  if (hw >= H * W) return;
+  const int32_t h = hw / W, w = hw - h * W, p = h / sh, q = w / sw;
+  const bool hit = h == p * sh && w == q * sw && p < P && q < Q;
+  const int32_t pq = hit ? p * Q + q : 0;
+  for (int64_t nc = blockIdx.y; nc < planes; nc += gridDim.y)
+    dx[nc * H * W + hw] = hit ? sub[nc * P * Q + pq] : 0.f;
+}
+Geom unit_grid(const Geom& g) {
+  Geom u = g;
+  u.h = g.p;
+  u.w = g.q;
+  u.sh = u.sw = 1;
+  return u;
+}
+}  // namespace
+
+int64_t conv_bwd_data_sub_bytes(const Geom& g) {
+  if (g.r != 1 || g.s != 1 || g.ph != 0 || g.pw != 0 || (g.sh == 1 && g.sw == 1)) return 0;
+  const Geom u = unit_grid(g);
+  if (!conv_mfma_supported(u, DFP_BWD_DATA)) return 0;
+  return plan_conv_mfma(u, DFP_BWD_DATA).bytes + align256((int64_t)g.n * g.c * g.p * g.q * 4);
+}
+
+dfp_status launch_conv_bwd_data_sub(const Geom& g, const int16_t* dy, const dfp_scale* sdy, const int16_t* w,
+                                    const dfp_scale* sw, float* dx, dfp_scale* so, void* ws, hipStream_t st,
+                                    bool prefer_w16) {
+  const Geom u = unit_grid(g);
+  float* sub = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(ws) + plan_conv_mfma(u, DFP_BWD_DATA).bytes);
+  dfp_status rc = launch_conv_mfma(DFP_BWD_DATA, u, dy, sdy, w, sw, sub, so, nullptr, ws, st, false, prefer_w16);
+  if (rc != DFP_OK) return rc;
+  const int64_t planes = (int64_t)g.n * g.c;
+  const int32_t gx = (g.h * g.w + 255) / 256;
+  const int64_t gy = std::max<int64_t>(1, std::min<int64_t>(planes, std::max(1, 16384 / gx)));
+  DFP_LAUNCH(K_XPREP, k_scatter_strided, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, st, sub, dx, planes, g.h,
+             g.w, g.p, g.q, g.sh, g.sw);
+  return DFP_OK;
+}
+
 }  // namespace dfp

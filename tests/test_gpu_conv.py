@@ -107,11 +107,14 @@ def test_bwd_wt_band_shapes(shape, L, G):
 @pytest.mark.parametrize("shape", [(2, 256, 16, 16, 64, 1, 1, 2, 0), (1, 40, 15, 13, 24, 1, 1, 3, 0),
                                    (2, 130, 14, 14, 96, 1, 1, 2, 0)])
 @pytest.mark.parametrize("L,G", [(64, 0), (32, 3), (64, 1)])
-def test_bwd_wt_strided_1x1(shape, L, G):
+@pytest.mark.parametrize("partials", [True, False])
+def test_bwd_wt_strided_1x1(shape, L, G, partials):
+    # without partials, backward-data also runs over the P x Q grid and is
+    # scattered into dx (zeros at the pixels no output reads)
     n, c, h, w, k, r, s, st, pd = shape
     d = dfp.make_desc(n, c, h, w, k, r, s, st, pd, chunk_len=L, seg_chunks=G)
     assert dfp.workspace_bytes(d, dfp.BWD_WT) > 0  # the MFMA path (the VALU path needs no workspace)
-    run_all(shape, L, G=G)
+    run_all(shape, L, G=G, partials=partials)
 
 
 # Unit-stride 1x1 layers without padding, without partials: both operands as
