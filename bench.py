@@ -55,6 +55,8 @@ def parse():
                     help="skip the per-layer sweep (ResNet-50 conv4_x 1x1 pair, VGG-16 conv1_2 / conv3_3, all 53 "
                          "ResNet-50 convolutions)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--detail-out", default="", metavar="PATH",
+                    help="also write every detail block and the headline line to this file")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES five times (counter calibration)")
     return ap.parse_args()
@@ -330,10 +332,33 @@ def timed(step, steps, warmup, profile=False):
     return (t1 - t0) / steps, recs
 
 
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _omp():
+    """libgomp as loaded by the oracle (its thread count is set per call site)."""
+    import ctypes
+    lib = ctypes.CDLL("libgomp.so.1")
+    lib.omp_get_max_threads.restype = ctypes.c_int
+    lib.omp_set_num_threads.argtypes = [ctypes.c_int]
+    return lib
+
+
 def cpu_baseline(layer, x, w, dy, L, G, rounding, seed, budget_s):
     """The CPU oracle on a bounded sample of the same layer: every quantisation
-    in full, then the three convolutions at sampled output elements."""
+    in full, then the three convolutions at sampled output elements, once on
+    all host threads and once on one thread (a third of the budget)."""
     import oracle
+    oracle.lib()
+    omp = _omp()
+    threads = int(omp.omp_get_max_threads())
     rnd = oracle.ROUNDING[rounding]
     t0 = time.perf_counter()
     ox, ex, _ = oracle.quantize(x, 15, rnd, seed, oracle.ROLE_X)
@@ -346,33 +371,41 @@ def cpu_baseline(layer, x, w, dy, L, G, rounding, seed, budget_s):
     O = {0: layer.n * layer.k * layer.p * layer.q, 1: layer.n * layer.c * layer.h * layer.w,
          2: layer.k * layer.c * layer.r * layer.s}
     args = {0: (ox, ow, ex + ew), 1: (ody, ow, edy + ew), 2: (ox, ody, ex + edy)}
-    # calibrate on a small sample, then size each direction to ~budget/3 seconds
-    macs = 0
-    secs = 0.0
-    samples = {}
-    for dirn in (0, 1, 2):
-        m = max(16, 2_000_000 // T[dirn])
-        idx = rng.choice(O[dirn], size=min(m, O[dirn]), replace=False)
-        t0 = time.perf_counter()
-        oracle.conv_at(g, dirn, args[dirn][0], args[dirn][1], args[dirn][2], L, idx, G)
-        dt = time.perf_counter() - t0
-        per = dt / idx.size
-        m2 = int(min(O[dirn], max(idx.size, (budget_s / 3.0) / max(per, 1e-9))))
-        idx = rng.choice(O[dirn], size=m2, replace=False)
-        t0 = time.perf_counter()
-        oracle.conv_at(g, dirn, args[dirn][0], args[dirn][1], args[dirn][2], L, idx, G)
-        secs += time.perf_counter() - t0
-        macs += idx.size * T[dirn]
-        samples[dirn] = int(idx.size)
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+    def run(budget):
+        # calibrate on a small sample, then size each direction to ~budget/3 seconds
+        macs, secs, samples = 0, 0.0, {}
+        for dirn in (0, 1, 2):
+            m = max(16, 2_000_000 // T[dirn])
+            idx = rng.choice(O[dirn], size=min(m, O[dirn]), replace=False)
+            t0 = time.perf_counter()
+            oracle.conv_at(g, dirn, args[dirn][0], args[dirn][1], args[dirn][2], L, idx, G)
+            per = (time.perf_counter() - t0) / idx.size
+            m2 = int(min(O[dirn], max(idx.size, (budget / 3.0) / max(per, 1e-9))))
+            idx = rng.choice(O[dirn], size=m2, replace=False)
+            t0 = time.perf_counter()
+            oracle.conv_at(g, dirn, args[dirn][0], args[dirn][1], args[dirn][2], L, idx, G)
+            secs += time.perf_counter() - t0
+            macs += idx.size * T[dirn]
+            samples[dirn] = int(idx.size)
+        return 2.0 * macs / secs / 1e12, macs, secs, samples
+
+    all_v, macs, secs, samples = run(budget_s)
+    omp.omp_set_num_threads(1)
+    try:
+        one_v, _, one_secs, _ = run(budget_s / 3.0)
+    finally:
+        omp.omp_set_num_threads(threads)
     return {
-        "value": round(2.0 * macs / secs / 1e12, 6),
+        "value": round(all_v, 6),
         "unit": "TOPS",
-        "cores": cores,
+        "cores": threads,
         "kind": "oracle",
-        "sample": "oracle conv at %d fwd / %d bwd-data / %d bwd-wt sampled outputs (%.3g MAC, %.1f s) of the same "
-                  "layer and chunk length; quantisation of x, w, dy in full took %.2f s (not in value)"
-                  % (samples[0], samples[1], samples[2], macs, secs, tq),
+        "cpu": _cpu_model(),
+        "single_thread_value": round(one_v, 7),
+        "sample": "oracle conv at %d fwd / %d bwd-data / %d bwd-wt sampled outputs (%.3g MAC, %.1f s on %d "
+                  "threads; single thread %.1f s) of the same layer and chunk length; full quantisation of x, w, "
+                  "dy %.2f s, not in value" % (samples[0], samples[1], samples[2], macs, secs, threads, one_secs, tq),
     }
 
 
@@ -433,6 +466,33 @@ def layer_sweep(a, dev):
     return res
 
 
+def cold_timed(step, steps, flush_bytes=512 << 20):
+    """Median seconds of one step whose inputs were pushed out of the caches
+    first: a write of flush_bytes (twice the 256 MB Infinity Cache) runs
+    before every timed step, outside its HIP-event bracket."""
+    torch = step.torch
+    junk = torch.empty(flush_bytes // 4, dtype=torch.float32, device="cuda:0")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for s, e in ev:
+        junk.fill_(1.0)
+        s.record()
+        step.run()
+        e.record()
+    torch.cuda.synchronize()
+    del junk
+    return float(np.median([s.elapsed_time(e) for s, e in ev])) * 1e-3
+
+
+def emit_detail(name, payload, sink):
+    """One detail block as its own JSON line (printed before the headline
+    line, which stays last and short) and, with --detail-out, in a file."""
+    line = json.dumps({"detail": name, **payload})
+    print(line, flush=True)
+    if sink is not None:
+        sink.write(line + "\n")
+        sink.flush()
+
+
 def main():
     a = parse()
     if a.copy_probe:
@@ -447,6 +507,7 @@ def main():
     from paper_1802_00930_amd import dfp
     dfp.lib()  # fail loudly if the HIP library is missing
     dev = torch.device("cuda:0")
+    sink = open(a.detail_out, "w") if a.detail_out else None
     wl = WORKLOADS[WORKLOAD]
     layer, x, w, dy = layer_inputs(wl, 0)
     rounding, seed = wl.roundings[0], wl.seed
@@ -454,6 +515,7 @@ def main():
 
     step = Step(layer, x, w, dy, a.chunk, rounding, seed, a.path, dev, a.seg_chunks)
     sec, _ = timed(step, a.steps, a.warmup)              # the headline: no per-launch events
+    cold_sec = cold_timed(step, max(5, a.steps // 2))    # the same step after a 512 MB cache flush
     _, recs = timed(step, a.steps, 1, profile=True)      # per-kernel durations (HIP events)
     per_kernel = {}
     for name, ms in recs:
@@ -470,70 +532,65 @@ def main():
     per_dir = {}
     for k, v in conv_kernels.items():
         per_dir[k] = {"avg_ms": round(v["avg_ms"], 5),
-                      "tops": round(ops_per_dir / (v["avg_ms"] * 1e-3) / 1e12, 3)}
+                      "tops": round(ops_per_dir / (v["avg_ms"] * 1e-3) / 1e12, 3),
+                      "frac": round(ops_per_dir / (v["avg_ms"] * 1e-3) / 1e12 / peak, 4)}
+    emit_detail("headline_kernels", {
+        "workload": WORKLOAD, "per_direction": per_dir,
+        "kernels": {k: {kk: round(vv, 5) for kk, vv in v.items()} for k, v in kstats.items()},
+        "traffic_detail": traffic, "cold_ms_per_step": round(cold_sec * 1e3, 4)}, sink)
 
-    sweep = {}
     if not a.no_sweep:
+        sweep = {}
         for L in (8, 16, 32, 64):
             s2 = Step(layer, x, w, dy, L, rounding, seed, a.path, dev, max(1, a.seg_chunks * a.chunk // L))
             t2, _ = timed(s2, max(3, a.steps // 2), 2)
             sweep[str(L)] = {"ms_per_step": round(t2 * 1e3, 4), "tops": round(3 * ops_per_dir / t2 / 1e12, 3)}
             del s2
+        emit_detail("chunk_sweep", {"workload": WORKLOAD, "by_chunk_len": sweep}, sink)
 
     # the DFP-32-output variant of the same step (reported beside the headline)
-    dfp32 = None
     if not a.no_dfp32:
         s32 = StepDfp32(layer, x, w, dy, a.chunk, rounding, seed, a.path, dev, a.seg_chunks)
         t32, _ = timed(s32, a.steps, a.warmup)
         _, recs32 = timed(s32, a.steps, 1, profile=True)
-        k32 = {}
-        for name, ms in recs32:
-            k32.setdefault(name, []).append(ms)
-        dfp32 = {"ms_per_step": round(t32 * 1e3, 4), "tops": round(3 * ops_per_dir / t32 / 1e12, 3),
-                 "chunk_len_fwd_bwd_data": s32.d32.chunk_len,
-                 "kernels": {k: {"launches_per_step": len(v) / a.steps, "avg_ms": round(float(np.mean(v)), 5)}
-                             for k, v in k32.items()}}
+        emit_detail("dfp32_outputs", {
+            "ms_per_step": round(t32 * 1e3, 4), "tops": round(3 * ops_per_dir / t32 / 1e12, 3),
+            "chunk_len_fwd_bwd_data": s32.d32.chunk_len, "kernels": kernel_table(recs32, a.steps)}, sink)
         del s32
 
     # DFP16 GEMM: ResNet-50's FC layer step and one large product (reported beside the headline)
-    gemm = None
     if not a.no_gemm:
         fc = FcStep(64, 2048, 1000, a.chunk, rounding, seed, dev)
         tf, _ = timed(fc, a.steps, a.warmup)
         _, rf = timed(fc, a.steps, 1, profile=True)
         big = GemmStep(4096, 4096, 4096, a.chunk, dev)
-        tb, _ = timed(big, max(3, a.steps // 2), 2)
-        _, rb = timed(big, max(3, a.steps // 2), 1, profile=True)
-        kb = kernel_table(rb, max(3, a.steps // 2))
-        gemm_ms = kb["gemm"]["avg_ms"]
-        gemm_tops = 2.0 * big.macs / (gemm_ms * 1e-3) / 1e12
-        gemm = {
-            "fc_2048x1000_b64": {"ms_per_step": round(tf * 1e3, 4),
-                                 "tops": round(3 * 2.0 * fc.macs / tf / 1e12, 3),
-                                 "kernels": kernel_table(rf, a.steps)},
-            "gemm_4096x4096x4096": {"ms_per_call": round(tb * 1e3, 4),
-                                    "tops_call": round(2.0 * big.macs / tb / 1e12, 3),
-                                    "kernel_tops": round(gemm_tops, 3),
-                                    "kernel_frac": round(gemm_tops / PEAK_INT16_BYTESPLIT_TOPS, 4),
-                                    "kernels": kb},
-        }
-        # Blocked-DFP: the FC forward at 128-feature blocks and the 4096^3 product at 128-index blocks
+        nb = max(3, a.steps // 2)
+        tb, _ = timed(big, nb, 2)
+        _, rb = timed(big, nb, 1, profile=True)
+        kb = kernel_table(rb, nb)
+        gemm_tops = 2.0 * big.macs / (kb["gemm"]["avg_ms"] * 1e-3) / 1e12
         bfc = BlockedFcStep(64, 2048, 1000, a.chunk, 128, rounding, seed, dev)
         tbf, _ = timed(bfc, a.steps, a.warmup)
         _, rbf = timed(bfc, a.steps, 1, profile=True)
         bbig = BlockedGemmStep(4096, 4096, 4096, a.chunk, 128, dev)
-        tbb, _ = timed(bbig, max(3, a.steps // 2), 2)
-        _, rbb = timed(bbig, max(3, a.steps // 2), 1, profile=True)
-        kbb = kernel_table(rbb, max(3, a.steps // 2))
+        tbb, _ = timed(bbig, nb, 2)
+        _, rbb = timed(bbig, nb, 1, profile=True)
+        kbb = kernel_table(rbb, nb)
         bg_tops = 2.0 * bbig.macs / (kbb["gemm_blocked"]["avg_ms"] * 1e-3) / 1e12
-        gemm["blocked_fc_forward_bk128"] = {"ms_per_step": round(tbf * 1e3, 4), "kernels": kernel_table(rbf, a.steps)}
-        gemm["blocked_gemm_4096x4096x4096_bk128"] = {
-            "ms_per_call": round(tbb * 1e3, 4), "kernel_tops": round(bg_tops, 3),
-            "kernel_frac": round(bg_tops / PEAK_INT16_BYTESPLIT_TOPS, 4), "kernels": kbb}
+        emit_detail("gemm", {
+            "fc_2048x1000_b64": {"ms_per_step": round(tf * 1e3, 4), "tops": round(3 * 2.0 * fc.macs / tf / 1e12, 3),
+                                 "kernels": kernel_table(rf, a.steps)},
+            "gemm_4096x4096x4096": {"ms_per_call": round(tb * 1e3, 4),
+                                    "tops_call": round(2.0 * big.macs / tb / 1e12, 3),
+                                    "kernel_tops": round(gemm_tops, 3),
+                                    "kernel_frac": round(gemm_tops / PEAK_INT16_BYTESPLIT_TOPS, 4), "kernels": kb},
+            "blocked_fc_forward_bk128": {"ms_per_step": round(tbf * 1e3, 4), "kernels": kernel_table(rbf, a.steps)},
+            "blocked_gemm_4096x4096x4096_bk128": {
+                "ms_per_call": round(tbb * 1e3, 4), "kernel_tops": round(bg_tops, 3),
+                "kernel_frac": round(bg_tops / PEAK_INT16_BYTESPLIT_TOPS, 4), "kernels": kbb}}, sink)
         del fc, big, bfc, bbig
 
     # BN + ReLU forward / backward on the conv output and SGD + Q_w on the weights
-    train_ops = None
     if not a.no_train_ops:
         tr = TrainOpsStep(layer, rounding, seed, dev)
         ttr, _ = timed(tr, a.steps, a.warmup)
@@ -541,12 +598,21 @@ def main():
         # algorithmic bytes per element: BN forward reads y twice and writes zq (6 B); backward reads y and dz
         # in each of its three passes and writes dyq (14 B); SGD reads w, v, dw and writes w, v, then the
         # quantiser reads w and writes wq (26 B)
-        train_ops = {"ms_per_step": round(ttr * 1e3, 4), "bn_elems": tr.elems, "sgd_weights": tr.nw,
-                     "algorithmic_bytes": {"bn_relu_fwd": 6 * tr.elems, "bn_relu_bwd": 14 * tr.elems,
-                                           "sgd_quantize": 26 * tr.nw},
-                     "hbm_gbs_whole_step": round((20 * tr.elems + 26 * tr.nw) / ttr / 1e9, 1),
-                     "kernels": kernel_table(rtr, a.steps)}
+        emit_detail("train_ops", {
+            "ms_per_step": round(ttr * 1e3, 4), "bn_elems": tr.elems, "sgd_weights": tr.nw,
+            "algorithmic_bytes": {"bn_relu_fwd": 6 * tr.elems, "bn_relu_bwd": 14 * tr.elems,
+                                  "sgd_quantize": 26 * tr.nw},
+            "hbm_gbs_whole_step": round((20 * tr.elems + 26 * tr.nw) / ttr / 1e9, 1),
+            "kernels": kernel_table(rtr, a.steps)}, sink)
         del tr
+
+    layer_sums = None
+    if not a.no_layers:
+        lay = layer_sweep(a, dev)
+        layer_sums = {}
+        for name, res in lay.items():
+            emit_detail("layers", {"workload": name, **res}, sink)
+            layer_sums[name] = {"sum_step_ms": res["sum_step_ms"], "tops": res["tops_over_steps"]}
 
     out = {
         "metric": METRIC,
@@ -556,38 +622,35 @@ def main():
         "steps": a.steps,
         "warmup": a.warmup,
         "ms_per_step": round(sec * 1e3, 4),
+        "cold_ms_per_step": round(cold_sec * 1e3, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int16",
         "data": "synthetic",
         "config": {
-            "workload": "%s: N=%d C=%d K=%d %dx%d 3x3 s1 p1, DFP15, chunk_len=%d, %s rounding seed %d; step = "
-                        "Q(x)+Q(w)+Q(dy)+fwd+DC(y)+bwd-data+DC(dx)+bwd-wt"
-                        % (WORKLOAD, layer.n, layer.c, layer.k, layer.h, layer.w, a.chunk, rounding, seed),
-            "chunk_len": a.chunk, "seg_chunks": a.seg_chunks, "bits": 15, "rounding": rounding, "path": a.path,
-        },
+            "workload": "ResNet-50 conv2_x 3x3 layer N=%d C=K=%d %dx%d s1 p1, DFP15, L=%d, G=%d, %s rounding seed %d; "
+                        "step = Q(x)+Q(w)+Q(dy)+fwd+DC(y)+bwd-data+DC(dx)+bwd-wt"
+                        % (layer.n, layer.c, layer.h, layer.w, a.chunk, a.seg_chunks, rounding, seed),
+            "chunk_len": a.chunk, "seg_chunks": a.seg_chunks},
         "roofline": {
             "bound": "mfma" if mfma else "alu",
             "kernel": dominant,
             "achieved": round(achieved, 3),
             "peak": peak,
-            "unit": "TOP/s (INT16-equivalent ops)" if mfma else "TOP/s (INT16 ops)",
+            "unit": "TOP/s",
             "frac": round(achieved / peak, 4),
             "traffic": (traffic or {}).get("bytes"),
-            "traffic_detail": traffic,
         },
-        "per_direction": per_dir,
-        "kernels": {k: {kk: round(vv, 5) for kk, vv in v.items()} for k, v in kstats.items()},
-        "chunk_sweep": sweep,
-        "dfp32_outputs": dfp32,
-        "gemm": gemm,
-        "train_ops": train_ops,
-        "layers": None if a.no_layers else layer_sweep(a, dev),
     }
+    if layer_sums is not None:
+        out["layer_sums"] = layer_sums
     if not a.no_cpu:
         out["cpu_baseline"] = cpu_baseline(layer, x, w, dy, a.chunk, a.seg_chunks, rounding, seed, a.cpu_seconds)
-    print(json.dumps(out), flush=True)
+    if sink is not None:
+        sink.write(json.dumps(out) + "\n")
+        sink.close()
+    print(json.dumps(out, separators=(",", ":")), flush=True)
 
 
 if __name__ == "__main__":

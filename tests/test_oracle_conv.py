@@ -270,6 +270,46 @@ def test_bwd_wt_segments(orc):
         assert np.all(np.abs(c.reshape(-1) - exact) <= bound)
 
 
+def _segment_fold_float32(parts, G, e):
+    """Sec. 4.3 reading C8 replayed in numpy float32 from the chunk partials:
+    each segment of G consecutive chunks summed in chunk order (the last
+    segment possibly shorter), then the segment sums in segment order, then
+    one rounding of the sum times 2^e."""
+    F = parts.astype(np.float32)
+    J = F.shape[0]
+    seg_sums = []
+    for g0 in range(0, J, G):
+        u = F[g0].copy()
+        for j in range(g0 + 1, min(J, g0 + G)):
+            u = (u + F[j]).astype(np.float32)
+        seg_sums.append(u)
+    s = seg_sums[0].copy()
+    for u in seg_sums[1:]:
+        s = (s + u).astype(np.float32)
+    return np.ldexp(s.astype(np.float64), e).astype(np.float32)
+
+
+@pytest.mark.parametrize("G", [2, 3, 16, 17])
+def test_bwd_wt_segment_fold_float32_replay(orc, G):
+    """The oracle's two-level backward-weights sum equals an independent
+    float32 replay of its own partials bit for bit, for segment sizes whose
+    last segment is only partly filled (J = 65 chunks: 1, 2, 1 and 14 chunks
+    in the last segment) and with large-magnitude operands so that the
+    float32 additions round."""
+    g = orc.geom(4, 3, 9, 9, 4, 3, 3, 1, 1)
+    rng = np.random.default_rng(161)
+    x, _, dy = _rand_pair(rng, g, 2 ** 14)
+    L, e = 5, -23
+    J = orc.num_chunks(g, orc.BWD_WT, L)
+    assert J == 65 and J % G != 0
+    y, parts, _ = orc.conv(g, orc.BWD_WT, x, dy, e, L, G, want_partials=True)
+    ref = _segment_fold_float32(parts, G, e)
+    assert np.array_equal(y.reshape(-1).view(np.uint32), ref.view(np.uint32))
+    # the replay is sensitive to the segment boundaries: a neighbouring G differs somewhere
+    other = _segment_fold_float32(parts, G + 1, e)
+    assert not np.array_equal(other.view(np.uint32), ref.view(np.uint32))
+
+
 # ---------------------------------------------------- linearity mod 2^32 --
 def test_partials_linear_mod_2_32(orc):
     g = orc.geom(1, 16, 5, 5, 3, 3, 3, 1, 1)
