@@ -57,6 +57,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--detail-out", default="", metavar="PATH",
                     help="also write every detail block and the headline line to this file")
+    ap.add_argument("--peaks", action="store_true",
+                    help="only measure the unit ceilings (int8 MFMA, v_dot2_i32_i16, the byte-split chunk loop with "
+                         "register operands, HBM read and copy) with libpeaks.so")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES five times (counter calibration)")
     return ap.parse_args()
@@ -89,6 +92,48 @@ def copy_probe(nbytes):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes": nbytes, "launches": 5}), flush=True)
+
+
+def measure_peaks():
+    """Measured ceilings next to the published ones: each kernel runs twice
+    and the second launch is timed (HIP events)."""
+    import ctypes
+    import torch
+    path = os.path.join(ROOT, "paper_1802_00930_amd", "libpeaks.so")
+    if not os.path.exists(path):
+        raise ImportError("libpeaks.so is not built; run __graft_entry__.build()")
+    torch.cuda.init()
+    lib = ctypes.CDLL(path)
+    for fn, args in (("peaks_mfma_i8", [ctypes.c_int] * 3), ("peaks_dot2_i16", [ctypes.c_int] * 2),
+                     ("peaks_chunk_loop", [ctypes.c_int] * 2), ("peaks_hbm_read", [ctypes.c_int64, ctypes.c_int]),
+                     ("peaks_hbm_copy", [ctypes.c_int64, ctypes.c_int])):
+        getattr(lib, fn).argtypes = args
+        getattr(lib, fn).restype = ctypes.c_float
+    res = {}
+    blocks, iters = 1024, 20000  # 4 waves per SIMD on 256 CUs
+    for shape, name in ((0, "mfma_i32_32x32x32_i8"), (1, "mfma_i32_16x16x64_i8")):
+        ms = lib.peaks_mfma_i8(shape, blocks, iters)
+        ops = blocks * 4 * iters * 4 * 32768 * 2.0
+        res[name] = {"ms": round(ms, 4), "int8_tops": round(ops / ms / 1e9, 1),
+                     "frac_of_published": round(ops / ms / 1e9 / PEAK_INT8_MFMA_TOPS, 4)}
+    dblocks, diters = 2048, 20000
+    ms = lib.peaks_dot2_i16(dblocks, diters)
+    ops = dblocks * 256 * 8 * diters * 2 * 2.0
+    res["dot2_i32_i16"] = {"ms": round(ms, 4), "int16_tops": round(ops / ms / 1e9, 1),
+                           "frac_of_assumed_full_rate": round(ops / ms / 1e9 / PEAK_VALU_DOT2_TOPS, 4)}
+    citers = 5000
+    ms = lib.peaks_chunk_loop(blocks, citers)
+    ops = blocks * 4 * citers * 32 * 32 * 64 * 2.0
+    res["bytesplit_chunk_loop_l64"] = {"ms": round(ms, 4), "int16_eq_tops": round(ops / ms / 1e9, 1),
+                                       "frac_of_bytesplit_peak": round(ops / ms / 1e9 / PEAK_INT16_BYTESPLIT_TOPS, 4)}
+    nbytes = 1 << 30
+    ms = lib.peaks_hbm_read(nbytes, 2048)
+    res["hbm_read_1GiB"] = {"ms": round(ms, 4), "gbs": round(nbytes / ms / 1e6, 1),
+                            "frac_of_published": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4)}
+    ms = lib.peaks_hbm_copy(nbytes // 2, 2048)
+    res["hbm_copy_512MiB"] = {"ms": round(ms, 4), "gbs_read_plus_write": round(nbytes / ms / 1e6, 1),
+                              "frac_of_published": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4)}
+    print(json.dumps({"peaks": res}), flush=True)
 
 
 class Step:
@@ -497,6 +542,9 @@ def main():
     a = parse()
     if a.copy_probe:
         copy_probe(a.copy_probe)
+        return
+    if a.peaks:
+        measure_peaks()
         return
     if a.gpus != 1:
         print("bench.py: the DFP convolution path measures one GPU (its kernels work on one GPU's share); "

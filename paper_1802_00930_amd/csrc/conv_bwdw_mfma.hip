@@ -1017,11 +1017,13 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_band_skew(BwdwArgs a) {
 // and workgroup tile (128 columns x 64 rows), but each wave owns one 32 x 32
 // output tile (row tile wave / 4, column group wave % 4), so every wave needs
 // at most 128 VGPRs and two workgroups give four waves per SIMD to hide the
-// LDS and matrix-core latencies of the per-block chain.  Per chunk the eight
-// MFMAs are issued, then the reads of the next chunk, then the conversion.
-// The operand reads are ordinary LDS loads (the compiler places their waits
-// and knows which registers are still being filled); the band copies are
-// issued from inline assembly and waited for before each band's barrier.
+// LDS and matrix-core latencies of the per-block chain.  The operands of
+// block k + 1 are read while block k is multiplied, then the chunk is
+// converted.  Both the operand reads (ds_read_b128 / ds_read2_b64) and the
+// band copies are issued from inline assembly and waited for explicitly: the
+// reads one block later, the copies before each band's barrier.  The build
+// checks in the generated assembly that no instruction touches a read's
+// registers before its wait (asm_check.py).
 // One 16-byte direct-to-LDS buffer load (lane i writes lds + 16 i) issued from
 // inline assembly: the compiler then neither tracks it nor makes its own LDS
 // reads wait for it (it cannot tell which buffer a copy targets); the caller
@@ -1148,10 +1150,10 @@ __global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_band_w8(BwdwArgs a) {
 
   // Operand reads are inline-assembly LDS reads with explicit waits (wait_raw)
   // placed one block after the issue.  Between a read and its wait the
-  // compiler takes the destination registers as already written: the kernel
-  // relies on it neither copying nor spilling them there (the forward-only
-  // variant built here uses no scratch; the partials variant runs another
-  // kernel).
+  // compiler takes the destination registers as already written, so it must
+  // neither copy nor spill them there: the build checks the generated
+  // assembly for exactly that (asm_check.py) and the launcher also requires a
+  // build without scratch.
   struct Raw {
     v4i ah, al, wl0, wh0, wl1, wh1;
   };
@@ -1266,15 +1268,34 @@ dim3 bwdw_grid(BwdwArgs& args, const BwdwPlan& p) {
 // The band kernels read LDS with inline assembly and wait for the reads
 // explicitly (see no_scratch): a band kernel is used only if its build has no
 // scratch, else the general kernel (ordinary LDS reads) runs.
+// The build also checks the assembly of these kernels (asm_check.py: no
+// instruction names a register of an LDS read before the wait that completes
+// it) and defines DFP_ASM_UNSAFE_* = 1 for a kernel that fails.
+#ifndef DFP_ASM_UNSAFE_BAND_W8
+#define DFP_ASM_UNSAFE_BAND_W8 0
+#endif
+#ifndef DFP_ASM_UNSAFE_BAND_SKEW
+#define DFP_ASM_UNSAFE_BAND_SKEW 0
+#endif
+#ifndef DFP_ASM_UNSAFE_BAND_SKEW_PARTIALS
+#define DFP_ASM_UNSAFE_BAND_SKEW_PARTIALS 0
+#endif
+#ifndef DFP_ASM_UNSAFE_BAND
+#define DFP_ASM_UNSAFE_BAND 0
+#endif
+#ifndef DFP_ASM_UNSAFE_BAND_PARTIALS
+#define DFP_ASM_UNSAFE_BAND_PARTIALS 0
+#endif
 struct BandKernelsSafe {
   bool w8, skew_t, skew_f, band_t, band_f;
 };
 static const BandKernelsSafe& band_kernels_safe() {
-  static const BandKernelsSafe safe{no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false>)),
-                                    no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<true>)),
-                                    no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<false>)),
-                                    no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<true>)),
-                                    no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<false>))};
+  static const BandKernelsSafe safe{
+      !DFP_ASM_UNSAFE_BAND_W8 && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false>)),
+      !DFP_ASM_UNSAFE_BAND_SKEW_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<true>)),
+      !DFP_ASM_UNSAFE_BAND_SKEW && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<false>)),
+      !DFP_ASM_UNSAFE_BAND_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<true>)),
+      !DFP_ASM_UNSAFE_BAND && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<false>))};
   return safe;
 }
 
@@ -1286,7 +1307,9 @@ static const BandKernelsSafe& band_kernels_safe() {
 // and the unit-stride kernels run on it (their input band then spans P*Q
 // pixels per image instead of H*W).
 static bool strided_1x1(const Geom& g) {
-  return g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0 && (g.sh > 1 || g.sw > 1);
+  // (k_subsample indexes a plane and sizes its grid with 32 bits)
+  return g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0 && (g.sh > 1 || g.sw > 1) &&
+         (int64_t)g.h * g.w < (1ll << 31) - 256;
 }
 // Unit-stride 1x1 layers without padding (x is then a C x T matrix like dy).
 static bool unit_1x1(const Geom& g) {

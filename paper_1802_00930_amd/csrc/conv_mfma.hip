@@ -38,6 +38,25 @@
 #include "dfp_internal.h"
 #include "conv_mfma.h"
 
+// Set to 1 by the build for a kernel whose assembly fails the split-read
+// check of asm_check.py (an instruction names a register of an inline-asm LDS
+// read before the wait that completes it); such a kernel is not launched.
+#ifndef DFP_ASM_UNSAFE_PERSIST
+#define DFP_ASM_UNSAFE_PERSIST 0
+#endif
+#ifndef DFP_ASM_UNSAFE_PERSIST_PARTIALS
+#define DFP_ASM_UNSAFE_PERSIST_PARTIALS 0
+#endif
+#ifndef DFP_ASM_UNSAFE_PERSIST_I32
+#define DFP_ASM_UNSAFE_PERSIST_I32 0
+#endif
+#ifndef DFP_ASM_UNSAFE_SKEW
+#define DFP_ASM_UNSAFE_SKEW 0
+#endif
+#ifndef DFP_ASM_UNSAFE_SKEW_PARTIALS
+#define DFP_ASM_UNSAFE_SKEW_PARTIALS 0
+#endif
+
 namespace dfp {
 
 namespace {
@@ -1992,7 +2011,8 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     args.L = args.KB * 32;
     if (w16_ok)
       DFP_LAUNCH(kid32, (k_conv_mfma_w16<false, true>), w16_grid(), dim3(kThreads16), 0, st, args);
-    else if (persist_ok && no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_persist<false, true>)))
+    else if (persist_ok && !DFP_ASM_UNSAFE_PERSIST_I32 &&
+             no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_persist<false, true>)))
       DFP_LAUNCH(kid32, (k_conv_mfma_persist<false, true>), persist_grid(), dim3(kThreads3), 0, st, args);
     else if (chan16 && small_index)
       DFP_LAUNCH(kid32, (k_conv_mfma_q<false, true>), grid, dim3(kThreadsQ), 0, st, args);
@@ -2029,10 +2049,13 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
   // the persistent and skewed kernels wait for their inline-assembly LDS reads
   // in a later statement: a build of them with scratch is not used (see
   // no_scratch); the shared-ring and LDS kernels wait inside the same asm
-  static const bool persist_safe[2] = {no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_persist<false>)),
-                                       no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_persist<true>))};
-  static const bool skew_safe[2] = {no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_skew<false>)),
-                                    no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_skew<true>))};
+  // (the build's assembly check can also take them out of use, DFP_ASM_UNSAFE_*)
+  static const bool persist_safe[2] = {
+      !DFP_ASM_UNSAFE_PERSIST && no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_persist<false>)),
+      !DFP_ASM_UNSAFE_PERSIST_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_persist<true>))};
+  static const bool skew_safe[2] = {
+      !DFP_ASM_UNSAFE_SKEW && no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_skew<false>)),
+      !DFP_ASM_UNSAFE_SKEW_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_conv_mfma_skew<true>))};
   if (persist_ok && args.L == 64 && persist_safe[partials ? 1 : 0]) {
     const dim3 grid3 = persist_grid();
     if (partials) DFP_LAUNCH(kid, (k_conv_mfma_persist<true>), grid3, dim3(kThreads3), 0, st, args);
@@ -2098,6 +2121,8 @@ Geom unit_grid(const Geom& g) {
 
 int64_t conv_bwd_data_sub_bytes(const Geom& g) {
   if (g.r != 1 || g.s != 1 || g.ph != 0 || g.pw != 0 || (g.sh == 1 && g.sw == 1)) return 0;
+  // k_scatter_strided indexes a plane (and sizes its grid) with 32 bits
+  if ((int64_t)g.h * g.w >= (1ll << 31) - 256) return 0;
   const Geom u = unit_grid(g);
   if (!conv_mfma_supported(u, DFP_BWD_DATA)) return 0;
   return plan_conv_mfma(u, DFP_BWD_DATA).bytes + align256((int64_t)g.n * g.c * g.p * g.q * 4);

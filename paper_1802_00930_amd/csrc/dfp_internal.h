@@ -54,8 +54,10 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) {
 
 // True if the kernel's build uses no scratch (private segment).  Kernels that
 // read LDS with inline assembly and wait for the reads in a later statement
-// rely on the compiler neither copying nor spilling a register such a read is
-// still filling between the two; a build with scratch is not used.
+// need the compiler neither to copy nor to spill a register such a read is
+// still filling between the two.  The build verifies that on the generated
+// assembly (asm_check.py, which takes a failing kernel out of use); a kernel
+// whose build has scratch is not launched either.
 inline bool no_scratch(const void* kernel) {
   hipFuncAttributes attr{};
   return hipFuncGetAttributes(&attr, kernel) == hipSuccess && attr.localSizeBytes == 0;
