@@ -80,7 +80,9 @@ typedef enum dfp_status {
   DFP_ERR_PARAM = 3,     /* bits, rounding, role, chunk_len, seg_chunks or path */
   DFP_ERR_ALIGN = 4,     /* FP32 src not 16-byte aligned or INT16 dst not 8-byte */
   DFP_ERR_WORKSPACE = 5, /* workspace NULL or smaller than dfp_workspace_bytes() */
-  DFP_ERR_HIP = 6        /* a HIP launch or runtime call failed                 */
+  DFP_ERR_HIP = 6,       /* a HIP launch or runtime call failed                 */
+  DFP_ERR_SCRATCH_LIMIT = 7 /* dfp_conv_bwd_weights_noalloc: the layer needs more
+                               than DFP_NOALLOC_SCRATCH_BYTES of scratch        */
 } dfp_status;
 
 typedef enum dfp_rounding {
@@ -180,6 +182,26 @@ dfp_status dfp_conv_bwd_data(const dfp_desc* d, const int16_t* dy, const dfp_sca
 dfp_status dfp_conv_bwd_weights(const dfp_desc* d, const int16_t* x, const dfp_scale* sx,
                                 const int16_t* dy, const dfp_scale* sdy, float* dw, void* workspace,
                                 size_t ws_bytes, int32_t* partials, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * backward-weights convolution of dfp_conv_bwd_weights, with the same
+ * operands, numerics and argument errors, no partials, and no workspace
+ * argument.  Its scratch (digit planes of x and dy, the per-segment FP32
+ * sums) lives in a static device array of DFP_NOALLOC_SCRATCH_BYTES bytes
+ * inside the library: every GPU the call runs on holds one such array from
+ * the library's first use on it until the process ends.  A layer whose
+ * workspace, dfp_workspace_bytes(d, DFP_BWD_WT), exceeds that size returns
+ * DFP_ERR_SCRATCH_LIMIT before any HIP call.  stream (NULL = the default
+ * stream) must belong to the current device, else DFP_ERR_PARAM.  Nothing in
+ * the scratch needs to start at zero; the array keeps the last call's
+ * contents.  Calls in flight at the same time on one GPU share the array and
+ * race: order them (one stream, or events).  The call allocates nothing: no
+ * hipMalloc, hipFree or allocating library routine (with the optional
+ * launch profiler below switched on, it records HIP events). */
+#define DFP_NOALLOC_SCRATCH_BYTES (64u << 20)
+dfp_status dfp_conv_bwd_weights_noalloc(const dfp_desc* d, const int16_t* x, const dfp_scale* sx,
+                                        const int16_t* dy, const dfp_scale* sdy, float* dw, void* stream);
 
 /* Down-convert an FP32 convolution output to DFP (Sec. 1: scale from the max
  * of the current output; Sec. 4.1: Q_a after FP, Q_e after BP).  role is

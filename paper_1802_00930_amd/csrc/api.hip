@@ -50,6 +50,30 @@ void prof_end(int slot, hipStream_t st) {
   (void)hipEventRecord(g_prof[slot].stop, st);
 }
 
+// ---------------------------------------------------- no-allocation scratch
+// The scratch of dfp_conv_bwd_weights_noalloc.  In host code `scratch` only
+// names the symbol; its device address on a GPU comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+static __device__ __align__(256) uint8_t scratch[DFP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev` (the current device), or null.
+void* scratch_on_device(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+}  // namespace
+
 // ------------------------------------------------------------- validation
 namespace {
 
@@ -187,6 +211,7 @@ const char* dfp_status_str(int32_t status) {
     case DFP_ERR_ALIGN: return "misaligned pointer";
     case DFP_ERR_WORKSPACE: return "workspace missing or too small";
     case DFP_ERR_HIP: return "HIP error";
+    case DFP_ERR_SCRATCH_LIMIT: return "layer needs more than the no-allocation scratch (64 MiB)";
     default: return "unknown status";
   }
 }
@@ -458,6 +483,28 @@ dfp_status dfp_conv_bwd_weights(const dfp_desc* d, const int16_t* x, const dfp_s
                                 const dfp_scale* sdy, float* dw, void* workspace, size_t ws_bytes,
                                 int32_t* partials, void* stream) {
   return conv_common(DFP_BWD_WT, d, x, sx, dy, sdy, dw, nullptr, workspace, ws_bytes, partials, stream);
+}
+
+dfp_status dfp_conv_bwd_weights_noalloc(const dfp_desc* d, const int16_t* x, const dfp_scale* sx,
+                                        const int16_t* dy, const dfp_scale* sdy, float* dw, void* stream) {
+  Geom g;
+  dfp_status rc = conv_checks(d, &g, x, sx, dy, sdy, dw);
+  if (rc != DFP_OK) return rc;
+  const size_t need = workspace_bytes(g, DFP_BWD_WT, d->path, d->bits);
+  if (need > (size_t)DFP_NOALLOC_SCRATCH_BYTES) return DFP_ERR_SCRATCH_LIMIT;
+  hipStream_t st = (hipStream_t)stream;
+  if (!use_mfma(g, d->path, d->bits, DFP_BWD_WT)) return launch_conv_valu(DFP_BWD_WT, g, x, sx, dy, sdy, dw, nullptr,
+                                                                            nullptr, st);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return DFP_ERR_HIP;
+  if (st) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(st, &sdev) != hipSuccess) return DFP_ERR_HIP;
+    if ((int)sdev != dev) return DFP_ERR_PARAM;
+  }
+  void* ws = scratch_on_device(dev);
+  if (!ws) return DFP_ERR_HIP;
+  return launch_bwdw_mfma(g, x, sx, dy, sdy, dw, nullptr, ws, st);
 }
 
 dfp_status dfp_profile_start(int32_t capacity) {

@@ -16,7 +16,8 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libdfp.so")
 
-OK, ERR_NULL, ERR_SHAPE, ERR_PARAM, ERR_ALIGN, ERR_WORKSPACE, ERR_HIP = range(7)
+OK, ERR_NULL, ERR_SHAPE, ERR_PARAM, ERR_ALIGN, ERR_WORKSPACE, ERR_HIP, ERR_SCRATCH_LIMIT = range(8)
+NOALLOC_SCRATCH_BYTES = 64 << 20
 ROUND_NEAREST, ROUND_STOCHASTIC, ROUND_BIASED, ROUND_DOWN = range(4)
 ROUNDING = {"nearest": 0, "stochastic": 1, "biased": 2, "down": 3}
 ROLE_X, ROLE_W, ROLE_DY, ROLE_Y, ROLE_DX = range(5)
@@ -70,6 +71,7 @@ def lib():
             "dfp_conv_fwd": ([DP, P, P, P, P, P, P, P, SZ, P, P], I32),
             "dfp_conv_bwd_data": ([DP, P, P, P, P, P, P, P, SZ, P, P], I32),
             "dfp_conv_bwd_weights": ([DP, P, P, P, P, P, P, SZ, P, P], I32),
+            "dfp_conv_bwd_weights_noalloc": ([DP, P, P, P, P, P, P], I32),
             "dfp_downconvert": ([DP, I32, P, P, P, I32, P], I32),
             "dfp_conv_fwd_i32": ([DP, P, P, P, P, P, P, P, SZ, P], I32),
             "dfp_conv_bwd_data_i32": ([DP, P, P, P, P, P, P, P, SZ, P], I32),
@@ -206,6 +208,15 @@ def dfp_conv_bwd_weights(d: Desc, x, sx, dy, sdy, dw, workspace=None, partials=N
     _check("dfp_conv_bwd_weights", lib().dfp_conv_bwd_weights(ctypes.byref(d), _ptr(x), _ptr(sx), _ptr(dy),
                                                               _ptr(sdy), _ptr(dw), wp, wn, _ptr(partials),
                                                               _stream(stream)))
+
+
+def dfp_conv_bwd_weights_noalloc(d: Desc, x, sx, dy, sdy, dw, stream=None):
+    for t, dt, nm in ((x, torch.int16, "x"), (dy, torch.int16, "dy"), (dw, torch.float32, "dw"),
+                      (sx, torch.int32, "sx"), (sdy, torch.int32, "sdy")):
+        _need(t, dt, nm)
+    _check("dfp_conv_bwd_weights_noalloc",
+           lib().dfp_conv_bwd_weights_noalloc(ctypes.byref(d), _ptr(x), _ptr(sx), _ptr(dy), _ptr(sdy), _ptr(dw),
+                                              _stream(stream)))
 
 
 def dfp_conv_fwd_i32(d: Desc, x, sx, w, sw, y, sy, workspace=None, stream=None):

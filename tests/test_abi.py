@@ -336,3 +336,18 @@ def test_oracle_not_reachable_from_product():
                 text = open(os.path.join(dirpath, fn)).read()
                 assert "import oracle" not in text and "from oracle" not in text, fn
                 assert "liboracle" not in text and "dfp_oracle" not in text, fn
+
+
+def test_noalloc_scratch_limit_and_nulls_on_host(dl):
+    """dfp_conv_bwd_weights_noalloc rejects, before any HIP call, null
+    operands and a layer whose workspace exceeds the static scratch."""
+    lib = dl.lib()
+    big = dl.make_desc(32, 64, 224, 224, 64, 3, 3, 1, 1, chunk_len=64, seg_chunks=16)
+    assert dl.workspace_bytes(big, dl.BWD_WT) > dl.NOALLOC_SCRATCH_BYTES
+    args = [_p(FAKE)] * 5
+    assert lib.dfp_conv_bwd_weights_noalloc(ctypes.byref(big), *args, None) == dl.ERR_SCRATCH_LIMIT
+    small = good_desc(dl)
+    assert lib.dfp_conv_bwd_weights_noalloc(ctypes.byref(small), None, *args[1:], None) == dl.ERR_NULL
+    bad = good_desc(dl, bits=14)
+    assert lib.dfp_conv_bwd_weights_noalloc(ctypes.byref(bad), *args, None) == dl.ERR_PARAM
+    assert "64 MiB" in dl.status_str(dl.ERR_SCRATCH_LIMIT)
