@@ -36,6 +36,7 @@ def _hipcc():
 SPLIT_READ_KERNELS = {
     "conv_bwdw_mfma.hip": {
         "k_bwdw_band_w8ILb0E": "DFP_ASM_UNSAFE_BAND_W8",
+        "k_bwdw_band_w8ILb1E": "DFP_ASM_UNSAFE_BAND_W8_PARTIALS",
         "k_bwdw_band_skewILb0E": "DFP_ASM_UNSAFE_BAND_SKEW",
         "k_bwdw_band_skewILb1E": "DFP_ASM_UNSAFE_BAND_SKEW_PARTIALS",
         "k_bwdw_bandILb0E": "DFP_ASM_UNSAFE_BAND",

@@ -1047,7 +1047,7 @@ constexpr int kThreadsW8 = 512;
 constexpr int kBandBufBytes = kBandLdsBytes / 2;
 
 template <bool PARTIALS>
-__global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_band_w8(BwdwArgs a) {
+__global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(BwdwArgs a) {
   const BwdwTile tl = bwdw_tile(a);
   if (tl.seg >= a.nseg) return;
   // output scale exponent, read before any copy is in flight (the compiler
@@ -1274,6 +1274,9 @@ dim3 bwdw_grid(BwdwArgs& args, const BwdwPlan& p) {
 #ifndef DFP_ASM_UNSAFE_BAND_W8
 #define DFP_ASM_UNSAFE_BAND_W8 0
 #endif
+#ifndef DFP_ASM_UNSAFE_BAND_W8_PARTIALS
+#define DFP_ASM_UNSAFE_BAND_W8_PARTIALS 0
+#endif
 #ifndef DFP_ASM_UNSAFE_BAND_SKEW
 #define DFP_ASM_UNSAFE_BAND_SKEW 0
 #endif
@@ -1287,11 +1290,12 @@ dim3 bwdw_grid(BwdwArgs& args, const BwdwPlan& p) {
 #define DFP_ASM_UNSAFE_BAND_PARTIALS 0
 #endif
 struct BandKernelsSafe {
-  bool w8, skew_t, skew_f, band_t, band_f;
+  bool w8, w8_t, skew_t, skew_f, band_t, band_f;
 };
 static const BandKernelsSafe& band_kernels_safe() {
   static const BandKernelsSafe safe{
       !DFP_ASM_UNSAFE_BAND_W8 && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false>)),
+      !DFP_ASM_UNSAFE_BAND_W8_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<true>)),
       !DFP_ASM_UNSAFE_BAND_SKEW_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<true>)),
       !DFP_ASM_UNSAFE_BAND_SKEW && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<false>)),
       !DFP_ASM_UNSAFE_BAND_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<true>)),
@@ -1515,9 +1519,11 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.xb_bytes = (uint32_t)p.xp_bytes;
     const dim3 grid = bwdw_grid(args, p);
     if (l64) {
-      // the partials variant of the eight-wave kernel would spill: partials
-      // use the two-tile kernel (same chunks, same order of additions)
-      if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<true>), grid, dim3(kThreads), 0, st, args);
+      // partials: the eight-wave kernel built for two waves per SIMD (its
+      // partial stores need more than 128 VGPRs), else the two-tile kernel
+      // (same chunks, same order of additions)
+      if (partials && safe.w8_t) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<true>), grid, dim3(kThreadsW8), 0, st, args);
+      else if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<true>), grid, dim3(kThreads), 0, st, args);
       else if (safe.w8) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false>), grid, dim3(kThreadsW8), 0, st, args);
       else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<false>), grid, dim3(kThreads), 0, st, args);
     } else {

@@ -1,146 +1,184 @@
-"""GPU parity at the full sizes of the benchmark workloads, in the launch
-configuration the benchmark times (default path, chunk lengths of the
-workload, default backward-weights segments unless stated).
+"""GPU parity at the full sizes of every benchmark workload, in the launch
+configuration the benchmark times (bench.Step: default path, the workload's
+chunk length and rounding, backward-weights segments of G = 16 * 64 / L
+chunks).
 
-Every quantisation is compared in full (INT16 bit-exact, exponents and flags
-equal).  Convolution outputs are compared in full where the oracle finishes
-in seconds (the ResNet-50 conv2_x 3x3 layer at L = 64, the configuration of
-the headline number) and otherwise at sampled output elements, each computed
-one by one by the oracle, together with their INT32 chunk partials.  The
-down-convert is checked in full against the oracle's quantiser applied to the
-GPU's FP32 output, and the convolution epilogue's max |y| against the output
-itself.
+Every tensor of the chain is compared in full against the CPU oracle's own
+chain: Q(x), Q(w), Q(dy) (INT16, exponent, flags), the three FP32
+convolution outputs, the epilogue's max |y| / |dx|, and the down-converted
+INT16 outputs with their exponents and flags.  The oracle side is stored as
+SHA-256 digests (whole tensor and per 1 MiB tile) in
+tests/golden/oracle_digests.json, written by make_oracle_digests.py, which
+calls only the oracle and the seeded input generators; a mismatch names the
+tiles that differ.  FP32 outputs must then be bit-identical (0 ulp, inside
+the 1e-6 relative bound), INT16 tensors, exponents and flags equal.
+
+INT32 chunk partials are compared on sampled 32 x 32 output tiles (a 32-row,
+32-position block of the output) plus the first and last tile, evaluated one
+by one by the oracle, from a second call that records them.
 """
+import hashlib
+import json
+import os
 import zlib
 
 import numpy as np
 import pytest
 import torch
 
+import bench
 import oracle
-from gpu_helpers import DEV, GpuLayer, assert_fp32_close, note, oracle_geom, ulp_diff
+from gpu_helpers import DEV, note, oracle_geom
 from paper_1802_00930_amd import dfp
 from paper_1802_00930_amd.workloads import WORKLOADS, layer_inputs
 
 pytestmark = pytest.mark.gpu
 
-DIRS = (dfp.FWD, dfp.BWD_DATA, dfp.BWD_WT)
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "oracle_digests.json")
+DB = json.load(open(GOLDEN)) if os.path.exists(GOLDEN) else {"cases": {}, "tile_bytes": 1 << 20}
+TILE = DB["tile_bytes"]
 
 
-def _quantize_both(gl, f, role, bits, rounding, seed):
-    q, sc = gl.quantize(f, role)
-    oq, oe, oflags = oracle.quantize(f, bits, oracle.ROUNDING[rounding], seed, role)
+def _digest(a: np.ndarray):
+    b = np.ascontiguousarray(a).reshape(-1).view(np.uint8)
+    tiles = [hashlib.sha256(b[i:i + TILE].tobytes()).hexdigest()[:16] for i in range(0, b.size, TILE)]
+    return hashlib.sha256(b.tobytes()).hexdigest(), tiles
+
+
+def _check(name, got: np.ndarray, ref: dict, problems: list):
+    sha, tiles = _digest(got)
+    if sha != ref["sha256"]:
+        bad = [i for i, (g, r) in enumerate(zip(tiles, ref["tiles"])) if g != r]
+        problems.append("%s: %d of %d 1 MiB tiles differ, first %s" % (name, len(bad), len(ref["tiles"]), bad[:8]))
+
+
+def _tiles(rng, rows, cols, count):
+    """Flat output indices of `count` sampled 32 x 32 tiles plus the first and
+    the last tile of an output viewed as [rows][cols] (each tile: 32
+    consecutive rows x 32 consecutive columns, clipped at the edges)."""
+    nr, nc = (rows + 31) // 32, (cols + 31) // 32
+    picks = {(0, 0), (nr - 1, nc - 1)}
+    while len(picks) < min(count + 2, nr * nc):
+        picks.add((int(rng.integers(0, nr)), int(rng.integers(0, nc))))
+    idx = []
+    for tr, tc in sorted(picks):
+        r = np.arange(tr * 32, min(rows, tr * 32 + 32))
+        c = np.arange(tc * 32, min(cols, tc * 32 + 32))
+        idx.append((r[:, None] * cols + c[None, :]).reshape(-1))
+    return np.unique(np.concatenate(idx)).astype(np.int64)
+
+
+def _partial_tiles(step, direction, a, sa, b, sb, oa, ob, e, L, G, ntiles, seed):
+    """Chunk partials of sampled output tiles, GPU (partials call) vs oracle."""
+    layer = step.layer
+    d = step.d
+    g = oracle.geom(layer.n, layer.c, layer.h, layer.w, layer.k, layer.r, layer.s, layer.stride, layer.pad)
+    rng = np.random.default_rng(seed)
+    if direction == dfp.FWD:  # y [N][K][PQ]: rows (n, k), columns pixels
+        rows, cols = layer.n * layer.k, layer.p * layer.q
+        out_shape = (layer.n, layer.k, layer.p, layer.q)
+    elif direction == dfp.BWD_DATA:  # dx [N][C][HW]
+        rows, cols = layer.n * layer.c, layer.h * layer.w
+        out_shape = (layer.n, layer.c, layer.h, layer.w)
+    else:  # dw [K][CRS]
+        rows, cols = layer.k, layer.c * layer.r * layer.s
+        out_shape = (layer.k, layer.c, layer.r, layer.s)
+    idx = _tiles(rng, rows, cols, ntiles)
+    J = dfp.num_chunks(d, direction)
+    O = int(np.prod(out_shape))
+    out = torch.empty(out_shape, dtype=torch.float32, device=DEV)
+    parts = torch.full((J, O), 0x5A5A5A5A, dtype=torch.int32, device=DEV)
+    ws = dfp.alloc_workspace(d, direction, DEV)
+    if direction == dfp.FWD:
+        dfp.dfp_conv_fwd(d, a, sa, b, sb, out, None, ws, parts)
+    elif direction == dfp.BWD_DATA:
+        dfp.dfp_conv_bwd_data(d, a, sa, b, sb, out, None, ws, parts)
+    else:
+        dfp.dfp_conv_bwd_weights(d, a, sa, b, sb, out, ws, parts)
+    gp = parts[:, torch.from_numpy(idx).to(DEV)].cpu().numpy().T
+    del parts, out, ws
+    _, rp, _ = oracle.conv_at(g, direction, oa, ob, e, L, idx, G, want_partials=True)
+    bad = np.nonzero((gp != rp).any(axis=1))[0]
+    assert bad.size == 0, "dir %d: partials differ at %d of %d sampled outputs, first flat index %d" % (
+        direction, bad.size, idx.size, idx[bad[0]])
+
+
+# partial-tile budget per workload (tiles per direction; backward-weights
+# outputs each reduce over N*P*Q products, so fewer of them)
+PARTIAL_TILES = {"layer16x32": (64, 64, 64), "resnet50_conv2x_3x3": (64, 64, 8), "resnet50_conv4x_1x1": (64, 64, 4),
+                 "vgg16_conv1_2_conv3_3": (64, 64, 2), "resnet50_all_convs": (16, 16, 1)}
+
+
+@pytest.mark.parametrize("key", sorted(DB["cases"]))
+def test_full_chain_against_oracle_digests(key):
+    case = DB["cases"][key]
+    wname, index, rounding, _ = key.split("/")
+    wl = WORKLOADS[wname]
+    layer, x, w, dy = layer_inputs(wl, int(index))
+    L, G, seed = case["L"], case["G"], case["seed"]
+    assert list(case["shape"]) == [layer.n, layer.c, layer.h, layer.w, layer.k, layer.r, layer.s, layer.stride,
+                                   layer.pad] and case["bits"] == 15
+    note("full chain %s (L=%d, G=%d)" % (key, L, G))
+    step = bench.Step(layer, x, w, dy, L, rounding, seed, dfp.PATH_AUTO, DEV, G)
+    assert step.d.seg_chunks == G
+    step.run()
     torch.cuda.synchronize()
-    got = q.cpu().numpy()
-    bad = np.count_nonzero(got != oq)
-    assert bad == 0, "quantise role %d: %d elements differ" % (role, bad)
-    s = dfp.read_scale(sc)
-    assert s["exp"] == oe and s["flags"] == oflags, (role, s, oe, oflags)
-    return q, sc, oq, oe
+    problems = []
+    for name, q, sc in (("x", step.qx, step.sx), ("w", step.qw, step.sw), ("dy", step.qdy, step.sdy)):
+        s = dfp.read_scale(sc)
+        ref = case["q"][name]
+        if (s["exp"], s["flags"]) != (ref["exp"], ref["flags"]):
+            problems.append("Q(%s): exp/flags %s vs oracle %s" % (name, (s["exp"], s["flags"]), (ref["exp"], ref["flags"])))
+        _check("Q(%s)" % name, q.cpu().numpy(), ref, problems)
+    for name, t in (("y", step.y), ("dx", step.dx), ("dw", step.dw)):
+        _check(name, t.cpu().numpy(), case["out"][name], problems)
+    for name, sc, q in (("y", step.sy, step.qy), ("dx", step.sdx, step.qdx)):
+        s = dfp.read_scale(sc)
+        ref = case["dc"][name]
+        if s["amax_bits"] != case["out"][name]["amax_bits"]:
+            problems.append("max|%s| bits %#x vs oracle %#x" % (name, s["amax_bits"], case["out"][name]["amax_bits"]))
+        if (s["exp"], s["flags"]) != (ref["exp"], ref["flags"]):
+            problems.append("DC(%s): exp/flags %s vs oracle %s" % (name, (s["exp"], s["flags"]), (ref["exp"], ref["flags"])))
+        _check("DC(%s)" % name, q.cpu().numpy(), ref, problems)
+    assert not problems, "%s:\n  %s" % (key, "\n  ".join(problems))
+
+    # INT32 chunk partials on sampled output tiles (operands are the oracle's, equal to the GPU's by now)
+    rnd = oracle.ROUNDING[rounding]
+    ox, ex, _ = oracle.quantize(x, 15, rnd, seed, oracle.ROLE_X)
+    ow, ew, _ = oracle.quantize(w, 15, rnd, seed, oracle.ROLE_W)
+    ody, edy, _ = oracle.quantize(dy, 15, rnd, seed, oracle.ROLE_DY)
+    nt = PARTIAL_TILES[wname]
+    s0 = zlib.crc32(key.encode())
+    for direction, a, sa, b, sb, oa, ob, e in (
+            (dfp.FWD, step.qx, step.sx, step.qw, step.sw, ox, ow, ex + ew),
+            (dfp.BWD_DATA, step.qdy, step.sdy, step.qw, step.sw, ody, ow, edy + ew),
+            (dfp.BWD_WT, step.qx, step.sx, step.qdy, step.sdy, ox, ody, ex + edy)):
+        note("  partials dir %d" % direction)
+        _partial_tiles(step, direction, a, sa, b, sb, oa, ob, e, L, G, nt[direction], s0 + direction)
+    del step
+    torch.cuda.empty_cache()
 
 
-def check_layer(layer, x, w, dy, L, rounding, seed, nsample=0, G=0, dirs=DIRS, partial_samples=64):
-    """Quantise, run the three convolutions and both down-converts of one layer
-    on the GPU; compare with the oracle.  nsample = 0: every output element."""
-    gl = GpuLayer(layer.n, layer.c, layer.h, layer.w, layer.k, layer.r, layer.s, layer.stride, layer.pad, L=L,
-                  rounding=rounding, seed=seed, G=G)
-    g = oracle_geom(gl)
-    Gd = G if G > 0 else oracle.default_seg_chunks(L)
-    note("layer %s N=%d L=%d %s: quantise" % (layer.name, layer.n, L, rounding))
-    qx, sx, ox, ex = _quantize_both(gl, x, dfp.ROLE_X, 15, rounding, seed)
-    qw, sw, ow, ew = _quantize_both(gl, w, dfp.ROLE_W, 15, rounding, seed)
-    qdy, sdy, ody, edy = _quantize_both(gl, dy, dfp.ROLE_DY, 15, rounding, seed)
-    rng = np.random.default_rng(zlib.crc32(("%s/%d/%s" % (layer.name, L, rounding)).encode()))
-    operands = {dfp.FWD: (qx, sx, qw, sw, ox, ow, ex + ew),
-                dfp.BWD_DATA: (qdy, sdy, qw, sw, ody, ow, edy + ew),
-                dfp.BWD_WT: (qx, sx, qdy, sdy, ox, ody, ex + edy)}
-    for direction in dirs:
-        a, sa, b, sb, oa, ob, e = operands[direction]
-        note("layer %s dir %d: conv" % (layer.name, direction))
-        out, so, _ = gl.conv(direction, a, sa, b, sb)
-        torch.cuda.synchronize()
-        got = out.cpu().numpy().reshape(-1)
-        if nsample == 0:
-            ref, _, _ = oracle.conv(g, direction, oa, ob, e, L, Gd)
-            ref = ref.reshape(-1)
-            idx = None
-        else:
-            # backward-weights outputs each reduce over N*P*Q products: bound the oracle's work
-            ns = nsample if direction != dfp.BWD_WT else max(64, min(nsample, int(2e8 // (g.n * gl.p * gl.q))))
-            idx = np.unique(np.concatenate([rng.integers(0, got.size, ns), [0, got.size - 1]]))
-            ref, _, _ = oracle.conv_at(g, direction, oa, ob, e, L, idx, Gd)
-            got = got[idx]
-        assert_fp32_close(got, ref, "%s dir %d" % (layer.name, direction))
-        assert ulp_diff(got, ref) == 0
-        # INT32 chunk partials at a few outputs, from a second call that records them
-        if partial_samples:
-            pidx = rng.integers(0, out.numel(), partial_samples)
-            J = dfp.num_chunks(gl.d, direction)
-            if J * out.numel() * 4 <= (4 << 30):
-                _, _, parts = gl.conv(direction, a, sa, b, sb, want_scale=False, want_partials=True)
-                gp = parts[:, torch.from_numpy(pidx).to(DEV)].cpu().numpy().T
-                del parts
-                _, rp, _ = oracle.conv_at(g, direction, oa, ob, e, L, pidx, Gd, want_partials=True)
-                assert np.array_equal(gp, rp), "%s dir %d partials differ" % (layer.name, direction)
-        if direction != dfp.BWD_WT:
-            # epilogue max |y| and the down-convert of this output (role Y or DX)
-            y = out.cpu().numpy()
-            s = dfp.read_scale(so)
-            assert s["amax_bits"] == int((y.view(np.uint32) & 0x7fffffff).max())
-            role = dfp.ROLE_Y if direction == dfp.FWD else dfp.ROLE_DX
-            qo, sq = gl.downconvert(out, role, so)
-            oq, oe, oflags = oracle.quantize(y, 15, oracle.ROUNDING[rounding], seed, role)
-            torch.cuda.synchronize()
-            assert np.count_nonzero(qo.cpu().numpy() != oq) == 0, "%s down-convert differs" % layer.name
-            assert dfp.read_scale(sq)["exp"] == oe
-        del out
-
-
-def test_resnet50_conv2x_3x3_full_l64():
-    """N=32, 64->64 at 56x56, stochastic seed 1, L = 64: every output of all
-    three convolutions (the benchmark's workload and launch configuration)."""
-    wl = WORKLOADS["resnet50_conv2x_3x3"]
-    layer, x, w, dy = layer_inputs(wl, 0)
-    check_layer(layer, x, w, dy, 64, "stochastic", wl.seed, nsample=0, G=16)
-
-
-@pytest.mark.parametrize("L", [8, 16, 32])
-def test_resnet50_conv2x_3x3_chunk_sweep(L):
-    wl = WORKLOADS["resnet50_conv2x_3x3"]
-    layer, x, w, dy = layer_inputs(wl, 0)
-    check_layer(layer, x, w, dy, L, "stochastic", wl.seed, nsample=20000, G=max(1, 16 * 64 // L))
-
-
-@pytest.mark.parametrize("rounding", ["nearest", "biased"])
-def test_resnet50_conv4x_1x1_pair(rounding):
-    wl = WORKLOADS["resnet50_conv4x_1x1"]
-    for i in range(len(wl.layers)):
-        layer, x, w, dy = layer_inputs(wl, i)
-        check_layer(layer, x, w, dy, 64, rounding, wl.seed, nsample=20000)
-
-
-def test_vgg16_conv1_2_conv3_3():
-    wl = WORKLOADS["vgg16_conv1_2_conv3_3"]
-    for i in range(len(wl.layers)):
-        layer, x, w, dy = layer_inputs(wl, i)
-        check_layer(layer, x, w, dy, 64, "stochastic", wl.seed, nsample=4000, partial_samples=16)
-
-
-def test_resnet50_all_53_layers():
-    """Every ResNet-50 convolution (7x7 stem, strided 1x1 and projection
-    shortcuts, 3x3 bottlenecks) at N=64, nearest, L = 64, sampled outputs."""
-    wl = WORKLOADS["resnet50_all_convs"]
-    assert len(wl.layers) == 53
-    for i in range(len(wl.layers)):
-        layer, x, w, dy = layer_inputs(wl, i)
-        check_layer(layer, x, w, dy, 64, "nearest", wl.seed, nsample=1500, partial_samples=8)
-        torch.cuda.empty_cache()
+def test_digest_file_covers_every_benchmark_workload():
+    """Every layer, rounding and chunk length of the benchmark workloads has
+    its oracle digests."""
+    need = []
+    for name, lens in (("layer16x32", (16,)), ("resnet50_conv2x_3x3", (64, 32, 16, 8)), ("resnet50_conv4x_1x1", (64,)),
+                       ("vgg16_conv1_2_conv3_3", (64,)), ("resnet50_all_convs", (64,))):
+        wl = WORKLOADS[name]
+        for L in lens:
+            for r in wl.roundings:
+                for i in range(len(wl.layers)):
+                    need.append("%s/%d/%s/L%d" % (name, i, r, L))
+    missing = [k for k in need if k not in DB["cases"]]
+    assert not missing, "%d cases without oracle digests, e.g. %s" % (len(missing), missing[:3])
 
 
 def test_resnet50_conv2x_3x3_dfp32_full():
-    """The same layer through the single-chunk DFP-32 outputs (forward and
+    """The benchmark layer through the single-chunk DFP-32 outputs (forward and
     backward-data at L = C*R*S = K*R*S = 576) and the integer down-convert
     with the epilogue's max, every element against the oracle."""
+    from gpu_helpers import GpuLayer
     wl = WORKLOADS["resnet50_conv2x_3x3"]
     layer, x, w, dy = layer_inputs(wl, 0)
     L = layer.c * layer.r * layer.s
@@ -148,9 +186,15 @@ def test_resnet50_conv2x_3x3_dfp32_full():
                   rounding="stochastic", seed=wl.seed)
     g = oracle_geom(gl)
     rnd = oracle.ROUNDING["stochastic"]
-    qx, sx, ox, ex = _quantize_both(gl, x, dfp.ROLE_X, 15, "stochastic", wl.seed)
-    qw, sw, ow, ew = _quantize_both(gl, w, dfp.ROLE_W, 15, "stochastic", wl.seed)
-    qdy, sdy, ody, edy = _quantize_both(gl, dy, dfp.ROLE_DY, 15, "stochastic", wl.seed)
+    qx, sx = gl.quantize(x, dfp.ROLE_X)
+    qw, sw = gl.quantize(w, dfp.ROLE_W)
+    qdy, sdy = gl.quantize(dy, dfp.ROLE_DY)
+    ox, ex, _ = oracle.quantize(x, 15, rnd, wl.seed, oracle.ROLE_X)
+    ow, ew, _ = oracle.quantize(w, 15, rnd, wl.seed, oracle.ROLE_W)
+    ody, edy, _ = oracle.quantize(dy, 15, rnd, wl.seed, oracle.ROLE_DY)
+    torch.cuda.synchronize()
+    assert np.array_equal(qx.cpu().numpy(), ox) and np.array_equal(qdy.cpu().numpy(), ody)
+    assert np.array_equal(qw.cpu().numpy(), ow)
     for direction, a, sa, oa, ea, role, shape in ((dfp.FWD, qx, sx, ox, ex, dfp.ROLE_Y, gl.shape_y),
                                                   (dfp.BWD_DATA, qdy, sdy, ody, edy, dfp.ROLE_DX, gl.shape_x)):
         note("dfp32 layer %s dir %d" % (layer.name, direction))
