@@ -19,6 +19,8 @@
 // that band.  A lane owning column (c, r, s) then gathers its 16 operand pairs
 // as band[c][offset(t) + r*Wpad + s], which covers padding, strides and image
 // boundaries with no branches.
+#include <type_traits>
+
 #include "conv_bwdw_mfma.h"
 
 namespace dfp {
@@ -1046,18 +1048,35 @@ __device__ __forceinline__ v4i rsrc_words(const void* p, uint32_t bytes) {
 constexpr int kThreadsW8 = 512;
 constexpr int kBandBufBytes = kBandLdsBytes / 2;
 
-template <bool PARTIALS>
+template <int N>
+using IC = std::integral_constant<int, N>;
+
+// LDS reads at a lane address plus an immediate byte offset.
+template <int OFF>
+__device__ __forceinline__ void lds_rd128_at(v4i& d, uint32_t addr) {
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(d) : "v"(addr), "n"(OFF) : "memory");
+}
+template <int OFF8>
+__device__ __forceinline__ void lds_rd2x64_at(v4i& d, uint32_t addr) {
+  asm volatile("ds_read2_b64 %0, %1 offset0:%2 offset1:%3" : "=v"(d) : "v"(addr), "n"(OFF8), "n"(OFF8 + 1) : "memory");
+}
+
+// Eight-wave band kernel.  Each band buffer holds the band's dy digits first
+// (kBandABytes) and then its input rows; the run-offset tables hold offsets
+// from the start of the first buffer, so that every operand read is one lane
+// register plus an immediate (WPAD: the padded row width when it is one of
+// the instantiated values, which puts a run's hi-digit window at an immediate
+// distance from its lo-digit window; 0 = any width).
+template <bool PARTIALS, int WPAD>
 __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(BwdwArgs a) {
   const BwdwTile tl = bwdw_tile(a);
   if (tl.seg >= a.nseg) return;
   // output scale exponent, read before any copy is in flight (the compiler
   // would otherwise wait for a load still pending, and with it the copies)
   const int32_t e = __builtin_amdgcn_readfirstlane(a.ea->exp + a.eb->exp);
-  __shared__ __align__(16) uint8_t sb0[kBandBufBytes];
-  __shared__ __align__(16) uint8_t sb1[kBandBufBytes];
-  // byte offset in a band buffer of each of the band's 16 runs of 8 indices
-  __shared__ __align__(16) int32_t ro0[kSBT / 8];
-  __shared__ __align__(16) int32_t ro1[kSBT / 8];
+  __shared__ __align__(16) uint8_t sb[2][kBandBufBytes];
+  // byte offset from sb[0] of each of a band's 16 runs of 8 indices, per buffer
+  __shared__ __align__(16) int32_t ro[2][kSBT / 8];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int rt = wave >> 2;  // row tile
@@ -1081,11 +1100,8 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
   const int32_t nbands = (t_seg1 - t_seg0 + kSBT - 1) / kSBT;
   const int32_t NB = (t_seg1 - t_seg0) / 32;  // blocks of the segment (whole chunks)
   const int32_t row_b = a.row_bytes;
-  const int32_t b_region = a.buf_bytes - kBandABytes;
   const int32_t last_kb = t_seg1 / 32 - 1;
 
-  // band cursor (n, p, q) of the next band to copy, advanced without divisions
-  int32_t cn = t_seg0 / (a.P * a.Q), cp = (t_seg0 % (a.P * a.Q)) / a.Q, cq = t_seg0 % a.Q;
   const int32_t ppc = a.rows_max * row_b / 16;  // 16-byte pieces per channel
   // Copies are buffer loads of a per-lane offset fixed for the kernel plus a
   // uniform offset.  A slot j*512 + tid holds piece (tid & 3) ^ ((tid >> 4) & 3)
@@ -1093,9 +1109,14 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
   const v4i rs_a = rsrc_words(a.ad, a.ad_bytes);
   const v4i rs_b = rsrc_words(a.xb, a.xb_bytes);
   const uint32_t a_block = (uint32_t)a.Mp * 64;
-  auto issue_band = [&](int32_t b, uint8_t* buf, int32_t* ro) __attribute__((always_inline)) {
+  auto issue_band = [&](int32_t b, int buf_i) __attribute__((always_inline)) {
     const int32_t t_b0 = t_seg0 + b * kSBT;
-    uint8_t* dstA = buf + b_region;
+    // output position (cn, cp, cq) of the band's first index (uniform: scalar arithmetic)
+    const int32_t tq = (int32_t)fdiv((uint32_t)t_b0, a.div_q);
+    const int32_t cq = __builtin_amdgcn_readfirstlane(t_b0 - tq * a.Q);
+    const int32_t cn = __builtin_amdgcn_readfirstlane((int32_t)fdiv((uint32_t)tq, a.div_p));
+    const int32_t cp = __builtin_amdgcn_readfirstlane(tq - cn * a.P);
+    uint8_t* dstA = sb[buf_i];
     const int32_t kb0 = t_b0 / 32;
     // lane values recomputed here rather than held in registers across the band
     const int32_t ln = fresh_lane();
@@ -1112,7 +1133,7 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
     for (int32_t cc = wave; cc < a.nch_max; cc += kThreadsW8 / 64) {
       const int32_t ch = min(c_lo + cc, a.C - 1);
       const uint32_t soc = (uint32_t)((ch * a.NH + za) * row_b);
-      uint8_t* dstc = buf + cc * a.band_ch_stride;
+      uint8_t* dstc = sb[buf_i] + kBandABytes + cc * a.band_ch_stride;
       for (int32_t k0 = 0; k0 < ppc; k0 += 64) {
         if (ln < ppc - k0)
           dma16(rs_b, lds_addr(dstc + k0 * 16), b_lane, __builtin_amdgcn_readfirstlane(soc + (uint32_t)k0 * 16));
@@ -1126,16 +1147,8 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
       const int32_t dp = (int32_t)fdiv((uint32_t)p, a.div_p);
       n += dp;
       p -= dp * a.P;
-      ro[tid] = (n * a.Hpad + p - za) * row_b + q;
+      ro[buf_i][tid] = buf_i * kBandBufBytes + kBandABytes + (n * a.Hpad + p - za) * row_b + q;
     }
-    cq += kSBT;
-    while (cq >= a.Q) {
-      cq -= a.Q;
-      if (++cp == a.P) { cp = 0; ++cn; }
-    }
-    cn = __builtin_amdgcn_readfirstlane(cn);
-    cp = __builtin_amdgcn_readfirstlane(cp);
-    cq = __builtin_amdgcn_readfirstlane(cq);
   };
 
   Acc3 acc;
@@ -1143,9 +1156,11 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
 #pragma unroll
   for (int v = 0; v < 16; ++v) sum[v] = 0.f;
   const int32_t j0 = g * a.G;  // first chunk of the segment
-  const uint32_t lane_b = (uint32_t)((c - c_lo) * a.band_ch_stride + rr * row_b);
-  const uint32_t rd_a0 = (uint32_t)(swz(lc, 2 * half) * 16 + rt * 2048);
-  const uint32_t rd_a1 = (uint32_t)(swz(lc, 2 * half + 1) * 16 + rt * 2048);
+  // lane parts of the operand addresses, with the base of buffer 0 folded in
+  const uint32_t base0 = lds_addr(&sb[0][0]);
+  const uint32_t lane_b = base0 + (uint32_t)((c - c_lo) * a.band_ch_stride + rr * row_b);
+  const uint32_t rd_a0 = base0 + (uint32_t)(swz(lc, 2 * half) * 16 + rt * 2048);
+  const uint32_t rd_a1 = base0 + (uint32_t)(swz(lc, 2 * half + 1) * 16 + rt * 2048);
   const int32_t mrow = m0 + 32 * rt + 4 * half;
 
   // Operand reads are inline-assembly LDS reads with explicit waits (wait_raw)
@@ -1158,16 +1173,22 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
     v4i ah, al, wl0, wh0, wl1, wh1;
   };
   Raw R0, R1;
-  auto read_block = [&](Raw& r, const uint8_t* buf, const int32_t* ro, int32_t k) __attribute__((always_inline)) {
-    const int2 o = *reinterpret_cast<const int2*>(ro + 4 * k + 2 * half);
-    const uint32_t ab = lds_addr(buf + b_region + k * 4096);
-    const uint32_t rb = lds_addr(buf) + lane_b;
-    lds_rd128(r.ah, ab + rd_a0);
-    lds_rd128(r.al, ab + rd_a1);
-    lds_rd2x64(r.wl0, rb + (uint32_t)o.x);
-    lds_rd2x64(r.wh0, rb + (uint32_t)o.x + a.Wpad);
-    lds_rd2x64(r.wl1, rb + (uint32_t)o.y);
-    lds_rd2x64(r.wh1, rb + (uint32_t)o.y + a.Wpad);
+  // block K (0..3) of the band in buffer BUF (both compile-time)
+  auto read_block = [&](Raw& r, auto bufc, auto kc) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value, K = decltype(kc)::value;
+    const int2 o = *reinterpret_cast<const int2*>(&ro[BUF][4 * K + 2 * half]);
+    lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.ah, rd_a0);
+    lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.al, rd_a1);
+    const uint32_t w0 = lane_b + (uint32_t)o.x, w1 = lane_b + (uint32_t)o.y;
+    lds_rd2x64_at<0>(r.wl0, w0);
+    lds_rd2x64_at<0>(r.wl1, w1);
+    if constexpr (WPAD > 0) {
+      lds_rd2x64_at<WPAD / 8>(r.wh0, w0);
+      lds_rd2x64_at<WPAD / 8>(r.wh1, w1);
+    } else {
+      lds_rd2x64_at<0>(r.wh0, w0 + a.Wpad);
+      lds_rd2x64_at<0>(r.wh1, w1 + a.Wpad);
+    }
   };
   auto wait_raw = [&](Raw& r) __attribute__((always_inline)) {
     asm volatile("s_waitcnt lgkmcnt(0)"
@@ -1178,41 +1199,44 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
   auto operand_b = [&](const v4i& w0, const v4i& w1) __attribute__((always_inline)) {
     return v4i{window8_lo(w0, ss), window8_hi(w0, ss), window8_lo(w1, ss), window8_hi(w1, ss)};
   };
-  // One band (two chunks, or one at the end of a segment of an odd number of
-  // chunk pairs) from cur.  Block k + 1 is read while block k is multiplied;
-  // the first read of the next band comes from nxt after the band barrier,
-  // and the band after next is then copied into cur.
-  auto do_band = [&](int32_t b, uint8_t* cur, int32_t* rcur, const uint8_t* nxt, const int32_t* rnxt)
-                     __attribute__((always_inline)) {
-    const int32_t nch = min(2, (NB - 4 * b) >> 1);
-    for (int32_t ch = 0; ch < nch; ++ch) {
-      wait_raw(R0);
-      read_block(R1, cur, rcur, 2 * ch + 1);
-      mfma_tile(acc, R0.ah, R0.al, operand_b(R0.wh0, R0.wh1), operand_b(R0.wl0, R0.wl1), true);
-      wait_raw(R1);
-      if (ch + 1 < nch) {
-        read_block(R0, cur, rcur, 2 * ch + 2);
-      } else if (b + 1 < nbands) {
-        // every wave has read band b and band b + 1 has landed; band b + 2 may
-        // then overwrite band b
-        wait_vmcnt<0>();
-        __syncthreads();
-        if (b + 2 < nbands) issue_band(b + 2, cur, rcur);
-        read_block(R0, nxt, rnxt, 0);
-      }
-      mfma_tile(acc, R1.ah, R1.al, operand_b(R1.wh0, R1.wh1), operand_b(R1.wl0, R1.wl1), false);
-      flush_tile<PARTIALS>(acc, sum, j0 + 2 * b + ch, a.partials, a.O, colc, CRS, mrow, a.K, cvalid);
+  // Chunk CH (0 or 1) of band b in buffer CUR: block 2 CH + 1 is read while
+  // block 2 CH is multiplied; after the band's last chunk the first block of
+  // the next band comes from the other buffer after the band barrier, and the
+  // band after next is then copied into this one.
+  auto do_chunk = [&](auto curc, auto chc, int32_t b, int32_t nch) __attribute__((always_inline)) {
+    constexpr int CUR = decltype(curc)::value, CH = decltype(chc)::value;
+    wait_raw(R0);
+    read_block(R1, IC<CUR>{}, IC<2 * CH + 1>{});
+    mfma_tile(acc, R0.ah, R0.al, operand_b(R0.wh0, R0.wh1), operand_b(R0.wl0, R0.wl1), true);
+    wait_raw(R1);
+    if (CH + 1 < nch) {
+      read_block(R0, IC<CUR>{}, IC<(2 * CH + 2) & 3>{});
+    } else if (b + 1 < nbands) {
+      // every wave has read band b and band b + 1 has landed; band b + 2 may
+      // then overwrite band b
+      wait_vmcnt<0>();
+      __syncthreads();
+      if (b + 2 < nbands) issue_band(b + 2, CUR);
+      read_block(R0, IC<1 - CUR>{}, IC<0>{});
     }
+    mfma_tile(acc, R1.ah, R1.al, operand_b(R1.wh0, R1.wh1), operand_b(R1.wl0, R1.wl1), false);
+    flush_tile<PARTIALS>(acc, sum, j0 + 2 * b + CH, a.partials, a.O, colc, CRS, mrow, a.K, cvalid);
+  };
+  // One band: two chunks, or one at the end of a segment of an odd number of chunk pairs.
+  auto do_band = [&](auto curc, int32_t b) __attribute__((always_inline)) {
+    const int32_t nch = min(2, (NB - 4 * b) >> 1);
+    do_chunk(curc, IC<0>{}, b, nch);
+    if (nch > 1) do_chunk(curc, IC<1>{}, b, nch);
   };
 
-  issue_band(0, sb0, ro0);
+  issue_band(0, 0);
   wait_vmcnt<0>();
   __syncthreads();
-  if (nbands > 1) issue_band(1, sb1, ro1);
-  read_block(R0, sb0, ro0, 0);
+  if (nbands > 1) issue_band(1, 1);
+  read_block(R0, IC<0>{}, IC<0>{});
   for (int32_t b = 0; b < nbands; b += 2) {
-    do_band(b, sb0, ro0, sb1, ro1);
-    if (b + 1 < nbands) do_band(b + 1, sb1, ro1, sb0, ro0);
+    do_band(IC<0>{}, b);
+    if (b + 1 < nbands) do_band(IC<1>{}, b + 1);
   }
 
   const int32_t ln = fresh_lane();
@@ -1294,8 +1318,11 @@ struct BandKernelsSafe {
 };
 static const BandKernelsSafe& band_kernels_safe() {
   static const BandKernelsSafe safe{
-      !DFP_ASM_UNSAFE_BAND_W8 && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false>)),
-      !DFP_ASM_UNSAFE_BAND_W8_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<true>)),
+      !DFP_ASM_UNSAFE_BAND_W8 && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 0>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 32>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 64>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 232>)),
+      !DFP_ASM_UNSAFE_BAND_W8_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<true, 0>)),
       !DFP_ASM_UNSAFE_BAND_SKEW_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<true>)),
       !DFP_ASM_UNSAFE_BAND_SKEW && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<false>)),
       !DFP_ASM_UNSAFE_BAND_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<true>)),
@@ -1522,9 +1549,16 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
       // partials: the eight-wave kernel built for two waves per SIMD (its
       // partial stores need more than 128 VGPRs), else the two-tile kernel
       // (same chunks, same order of additions)
-      if (partials && safe.w8_t) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<true>), grid, dim3(kThreadsW8), 0, st, args);
+      if (partials && safe.w8_t) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<true, 0>), grid, dim3(kThreadsW8), 0, st, args);
       else if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<true>), grid, dim3(kThreads), 0, st, args);
-      else if (safe.w8) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false>), grid, dim3(kThreadsW8), 0, st, args);
+      // padded row widths of ResNet-50 56 x 56 and 28 x 28 and VGG-16 224 x 224 layers as immediates
+      else if (safe.w8 && p.Wpad == 64)
+        DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 64>), grid, dim3(kThreadsW8), 0, st, args);
+      else if (safe.w8 && p.Wpad == 32)
+        DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 32>), grid, dim3(kThreadsW8), 0, st, args);
+      else if (safe.w8 && p.Wpad == 232)
+        DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 232>), grid, dim3(kThreadsW8), 0, st, args);
+      else if (safe.w8) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 0>), grid, dim3(kThreadsW8), 0, st, args);
       else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<false>), grid, dim3(kThreads), 0, st, args);
     } else {
       if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<true>), grid, dim3(kThreads), 0, st, args);
