@@ -310,12 +310,19 @@ __global__ __launch_bounds__(256) void k_prep_plane(const int16_t* __restrict__ 
 // (lanes of a wave take consecutive columns, so each of the 16 channel loads
 // of a wave reads one contiguous run of the source row, and each of its two
 // 16-byte stores one contiguous run of the plane).  An extra row of
-// workgroups (with_a) prepares the filter digits.
+// workgroups (with_a) prepares the filter digits.  Workgroup ids are mapped
+// to rows so that each XCD (id mod 8) takes one contiguous range of rows of
+// whole images: a 128-byte line of the source holds parts of two rows, and
+// with neighbouring rows on different XCDs every such line was fetched into
+// two L2s.
 __global__ __launch_bounds__(256) void k_prep_plane_direct(const int16_t* __restrict__ src, uint8_t* __restrict__ xs,
                                                           int32_t Cs, int32_t Hs, int32_t Wsrc, int32_t Hp, int32_t Wp,
                                                           int32_t CG, int32_t top, int32_t left, int32_t dil_h,
                                                           int32_t dil_w, PrepAArgs pa, int32_t with_a) {
-  const int32_t u = blockIdx.x, n = blockIdx.y;
+  const int32_t nwg = gridDim.x * gridDim.y, id = blockIdx.y * gridDim.x + blockIdx.x;
+  const int32_t xcd = id & 7, per = nwg >> 3, rem = nwg & 7;
+  const int32_t l = xcd * per + min(xcd, rem) + (id >> 3);
+  const int32_t n = l / (int32_t)gridDim.x, u = l - n * (int32_t)gridDim.x;
   if (with_a && n == (int32_t)gridDim.y - 1) {
     const int32_t nthr = gridDim.x * 256;
     const int32_t total = max(pa.KB * pa.Mp * 8, pa.KB);
