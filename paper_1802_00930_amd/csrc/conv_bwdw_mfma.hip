@@ -28,6 +28,7 @@ namespace dfp {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;
@@ -565,9 +566,11 @@ __device__ __forceinline__ int swz(int row, int piece) { return row * 4 + (piece
 
 // XB[c][n*Hpad + u][d][Wpad]: d = 0 lo digits, d = 1 hi digits of
 // x[n][c][u - ph][v - pw], zero outside; rows are row_bytes = 2*Wpad + 16 apart
-// (the 16 spare bytes shift successive rows across LDS banks).  Rows of a multiple of 8 elements,
-// 16-byte aligned, column pad PW below 4 (same windowing as k_prep_xp_vec).
-template <int PW>
+// (the 16 spare bytes shift successive rows across LDS banks).  Column pad PW
+// below 4 (same windowing as k_prep_xp_vec).  VEC = 8: rows of a multiple of 8
+// elements, read in 16-byte pieces; VEC = 4: rows of a multiple of 4 elements,
+// read in 8-byte pieces.  x 16-byte aligned.
+template <int PW, int VEC = 8>
 __global__ __launch_bounds__(256) void k_prep_xb(const int16_t* __restrict__ x, uint8_t* __restrict__ xb, int32_t N,
                                                 int32_t C, int32_t H, int32_t W, int32_t Hpad, int32_t Wpad,
                                                 int32_t ph, int32_t row_bytes, DyPrep q) {
@@ -586,13 +589,29 @@ __global__ __launch_bounds__(256) void k_prep_xb(const int16_t* __restrict__ x, 
   if (ih >= 0 && ih < H) {
     const int16_t* row = x + ((int64_t)(n * C + c) * H + ih) * W;
     uint32_t g[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};  // elements v0-8 .. v0+7
-    if (PW > 0 && v0 >= 8 && v0 - 8 < W) {
-      const uint4 q = *reinterpret_cast<const uint4*>(row + v0 - 8);
-      g[0] = q.x; g[1] = q.y; g[2] = q.z; g[3] = q.w;
-    }
-    if (v0 < W) {
-      const uint4 q = *reinterpret_cast<const uint4*>(row + v0);
-      g[4] = q.x; g[5] = q.y; g[6] = q.z; g[7] = q.w;
+    if (VEC == 8) {
+      if (PW > 0 && v0 >= 8 && v0 - 8 < W) {
+        const uint4 q = *reinterpret_cast<const uint4*>(row + v0 - 8);
+        g[0] = q.x; g[1] = q.y; g[2] = q.z; g[3] = q.w;
+      }
+      if (v0 < W) {
+        const uint4 q = *reinterpret_cast<const uint4*>(row + v0);
+        g[4] = q.x; g[5] = q.y; g[6] = q.z; g[7] = q.w;
+      }
+    } else {
+      // elements v0-4 .. v0+7 in pieces of four, each wholly inside or outside the row
+      if (PW > 0 && v0 >= 4 && v0 - 4 < W) {
+        const uint2 q = *reinterpret_cast<const uint2*>(row + v0 - 4);
+        g[2] = q.x; g[3] = q.y;
+      }
+      if (v0 < W) {
+        const uint2 q = *reinterpret_cast<const uint2*>(row + v0);
+        g[4] = q.x; g[5] = q.y;
+      }
+      if (v0 + 4 < W) {
+        const uint2 q = *reinterpret_cast<const uint2*>(row + v0 + 4);
+        g[6] = q.x; g[7] = q.y;
+      }
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -1060,23 +1079,46 @@ template <int OFF8>
 __device__ __forceinline__ void lds_rd2x64_at(v4i& d, uint32_t addr) {
   asm volatile("ds_read2_b64 %0, %1 offset0:%2 offset1:%3" : "=v"(d) : "v"(addr), "n"(OFF8), "n"(OFF8 + 1) : "memory");
 }
+template <int OFF4>
+__device__ __forceinline__ void lds_rd2x32_at(v2i& d, uint32_t addr) {
+  asm volatile("ds_read2_b32 %0, %1 offset0:%2 offset1:%3" : "=v"(d) : "v"(addr), "n"(OFF4), "n"(OFF4 + 1) : "memory");
+}
+
+// Operand registers of one block: A digits (hi, lo) and the B windows of the
+// lane's runs, lo and hi digits.  Runs of 8 indices: two 16-byte windows per
+// digit; runs of 4: four 8-byte windows per digit.
+template <int RUN>
+struct BandRaw;
+template <>
+struct BandRaw<8> {
+  v4i ah, al, wl0, wh0, wl1, wh1;
+};
+template <>
+struct BandRaw<4> {
+  v4i ah, al;
+  v2i wl0, wl1, wl2, wl3, wh0, wh1, wh2, wh3;
+};
 
 // Eight-wave band kernel.  Each band buffer holds the band's dy digits first
 // (kBandABytes) and then its input rows; the run-offset tables hold offsets
 // from the start of the first buffer, so that every operand read is one lane
 // register plus an immediate (WPAD: the padded row width when it is one of
 // the instantiated values, which puts a run's hi-digit window at an immediate
-// distance from its lo-digit window; 0 = any width).
-template <bool PARTIALS, int WPAD>
+// distance from its lo-digit window; 0 = any width).  RUN: reduction indices
+// per run, consecutive output columns of one output row (8 when the output
+// width is a multiple of 8, else 4 for widths that are multiples of 4, such
+// as 28); a lane's 16 indices of a block are 16 / RUN runs.
+template <bool PARTIALS, int WPAD, int RUN = 8>
 __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(BwdwArgs a) {
+  static_assert(RUN == 8 || RUN == 4, "runs of 8 or 4 indices");
   const BwdwTile tl = bwdw_tile(a);
   if (tl.seg >= a.nseg) return;
   // output scale exponent, read before any copy is in flight (the compiler
   // would otherwise wait for a load still pending, and with it the copies)
   const int32_t e = __builtin_amdgcn_readfirstlane(a.ea->exp + a.eb->exp);
   __shared__ __align__(16) uint8_t sb[2][kBandBufBytes];
-  // byte offset from sb[0] of each of a band's 16 runs of 8 indices, per buffer
-  __shared__ __align__(16) int32_t ro[2][kSBT / 8];
+  // byte offset from sb[0] of each of a band's kSBT / RUN runs, per buffer
+  __shared__ __align__(16) int32_t ro[2][kSBT / RUN];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int rt = wave >> 2;  // row tile
@@ -1139,8 +1181,8 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
           dma16(rs_b, lds_addr(dstc + k0 * 16), b_lane, __builtin_amdgcn_readfirstlane(soc + (uint32_t)k0 * 16));
       }
     }
-    if (tid < kSBT / 8) {  // run u starts at output position (cn, cp, cq + 8u)
-      int32_t q = cq + 8 * tid, p = cp, n = cn;
+    if (tid < kSBT / RUN) {  // run u starts at output position (cn, cp, cq + RUN u)
+      int32_t q = cq + RUN * tid, p = cp, n = cn;
       const int32_t dq = (int32_t)fdiv((uint32_t)q, a.div_q);
       p += dq;
       q -= dq * a.Q;
@@ -1169,35 +1211,77 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
   // neither copy nor spill them there: the build checks the generated
   // assembly for exactly that (asm_check.py) and the launcher also requires a
   // build without scratch.
-  struct Raw {
-    v4i ah, al, wl0, wh0, wl1, wh1;
-  };
+  using Raw = BandRaw<RUN>;
   Raw R0, R1;
   // block K (0..3) of the band in buffer BUF (both compile-time)
   auto read_block = [&](Raw& r, auto bufc, auto kc) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value, K = decltype(kc)::value;
-    const int2 o = *reinterpret_cast<const int2*>(&ro[BUF][4 * K + 2 * half]);
-    lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.ah, rd_a0);
-    lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.al, rd_a1);
-    const uint32_t w0 = lane_b + (uint32_t)o.x, w1 = lane_b + (uint32_t)o.y;
-    lds_rd2x64_at<0>(r.wl0, w0);
-    lds_rd2x64_at<0>(r.wl1, w1);
-    if constexpr (WPAD > 0) {
-      lds_rd2x64_at<WPAD / 8>(r.wh0, w0);
-      lds_rd2x64_at<WPAD / 8>(r.wh1, w1);
+    if constexpr (RUN == 8) {
+      const int2 o = *reinterpret_cast<const int2*>(&ro[BUF][4 * K + 2 * half]);
+      lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.ah, rd_a0);
+      lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.al, rd_a1);
+      const uint32_t w0 = lane_b + (uint32_t)o.x, w1 = lane_b + (uint32_t)o.y;
+      lds_rd2x64_at<0>(r.wl0, w0);
+      lds_rd2x64_at<0>(r.wl1, w1);
+      if constexpr (WPAD > 0) {
+        lds_rd2x64_at<WPAD / 8>(r.wh0, w0);
+        lds_rd2x64_at<WPAD / 8>(r.wh1, w1);
+      } else {
+        lds_rd2x64_at<0>(r.wh0, w0 + a.Wpad);
+        lds_rd2x64_at<0>(r.wh1, w1 + a.Wpad);
+      }
     } else {
-      lds_rd2x64_at<0>(r.wh0, w0 + a.Wpad);
-      lds_rd2x64_at<0>(r.wh1, w1 + a.Wpad);
+      const v4i o = *reinterpret_cast<const v4i*>(&ro[BUF][8 * K + 4 * half]);
+      lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.ah, rd_a0);
+      lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.al, rd_a1);
+      const uint32_t w0 = lane_b + (uint32_t)o.x, w1 = lane_b + (uint32_t)o.y;
+      const uint32_t w2 = lane_b + (uint32_t)o.z, w3 = lane_b + (uint32_t)o.w;
+      lds_rd2x32_at<0>(r.wl0, w0);
+      lds_rd2x32_at<0>(r.wl1, w1);
+      lds_rd2x32_at<0>(r.wl2, w2);
+      lds_rd2x32_at<0>(r.wl3, w3);
+      if constexpr (WPAD > 0) {
+        lds_rd2x32_at<WPAD / 4>(r.wh0, w0);
+        lds_rd2x32_at<WPAD / 4>(r.wh1, w1);
+        lds_rd2x32_at<WPAD / 4>(r.wh2, w2);
+        lds_rd2x32_at<WPAD / 4>(r.wh3, w3);
+      } else {
+        lds_rd2x32_at<0>(r.wh0, w0 + a.Wpad);
+        lds_rd2x32_at<0>(r.wh1, w1 + a.Wpad);
+        lds_rd2x32_at<0>(r.wh2, w2 + a.Wpad);
+        lds_rd2x32_at<0>(r.wh3, w3 + a.Wpad);
+      }
     }
   };
   auto wait_raw = [&](Raw& r) __attribute__((always_inline)) {
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(r.wl0), "+v"(r.wh0), "+v"(r.wl1), "+v"(r.wh1), "+v"(r.ah), "+v"(r.al)
-                 :
-                 : "memory");
+    if constexpr (RUN == 8) {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(r.wl0), "+v"(r.wh0), "+v"(r.wl1), "+v"(r.wh1), "+v"(r.ah), "+v"(r.al)
+                   :
+                   : "memory");
+    } else {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(r.wl0), "+v"(r.wl1), "+v"(r.wl2), "+v"(r.wl3), "+v"(r.wh0), "+v"(r.wh1), "+v"(r.wh2),
+                     "+v"(r.wh3), "+v"(r.ah), "+v"(r.al)
+                   :
+                   : "memory");
+    }
   };
-  auto operand_b = [&](const v4i& w0, const v4i& w1) __attribute__((always_inline)) {
-    return v4i{window8_lo(w0, ss), window8_hi(w0, ss), window8_lo(w1, ss), window8_hi(w1, ss)};
+  // bytes ss .. ss + 3 of an 8-byte window (ss in 0..3)
+  auto win4 = [&](const v2i& w) __attribute__((always_inline)) {
+    return (int)__builtin_amdgcn_alignbyte((uint32_t)w.y, (uint32_t)w.x, ss);
+  };
+  auto operand_hi = [&](const Raw& r) __attribute__((always_inline)) {
+    if constexpr (RUN == 8)
+      return v4i{window8_lo(r.wh0, ss), window8_hi(r.wh0, ss), window8_lo(r.wh1, ss), window8_hi(r.wh1, ss)};
+    else
+      return v4i{win4(r.wh0), win4(r.wh1), win4(r.wh2), win4(r.wh3)};
+  };
+  auto operand_lo = [&](const Raw& r) __attribute__((always_inline)) {
+    if constexpr (RUN == 8)
+      return v4i{window8_lo(r.wl0, ss), window8_hi(r.wl0, ss), window8_lo(r.wl1, ss), window8_hi(r.wl1, ss)};
+    else
+      return v4i{win4(r.wl0), win4(r.wl1), win4(r.wl2), win4(r.wl3)};
   };
   // Chunk CH (0 or 1) of band b in buffer CUR: block 2 CH + 1 is read while
   // block 2 CH is multiplied; after the band's last chunk the first block of
@@ -1207,7 +1291,7 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
     constexpr int CUR = decltype(curc)::value, CH = decltype(chc)::value;
     wait_raw(R0);
     read_block(R1, IC<CUR>{}, IC<2 * CH + 1>{});
-    mfma_tile(acc, R0.ah, R0.al, operand_b(R0.wh0, R0.wh1), operand_b(R0.wl0, R0.wl1), true);
+    mfma_tile(acc, R0.ah, R0.al, operand_hi(R0), operand_lo(R0), true);
     wait_raw(R1);
     if (CH + 1 < nch) {
       read_block(R0, IC<CUR>{}, IC<(2 * CH + 2) & 3>{});
@@ -1219,7 +1303,7 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
       if (b + 2 < nbands) issue_band(b + 2, CUR);
       read_block(R0, IC<1 - CUR>{}, IC<0>{});
     }
-    mfma_tile(acc, R1.ah, R1.al, operand_b(R1.wh0, R1.wh1), operand_b(R1.wl0, R1.wl1), false);
+    mfma_tile(acc, R1.ah, R1.al, operand_hi(R1), operand_lo(R1), false);
     flush_tile<PARTIALS>(acc, sum, j0 + 2 * b + CH, a.partials, a.O, colc, CRS, mrow, a.K, cvalid);
   };
   // One band: two chunks, or one at the end of a segment of an odd number of chunk pairs.
@@ -1314,7 +1398,7 @@ dim3 bwdw_grid(BwdwArgs& args, const BwdwPlan& p) {
 #define DFP_ASM_UNSAFE_BAND_PARTIALS 0
 #endif
 struct BandKernelsSafe {
-  bool w8, w8_t, skew_t, skew_f, band_t, band_f;
+  bool w8, w8_t, skew_t, skew_f, band_t, band_f, w8_r4;
 };
 static const BandKernelsSafe& band_kernels_safe() {
   static const BandKernelsSafe safe{
@@ -1326,7 +1410,9 @@ static const BandKernelsSafe& band_kernels_safe() {
       !DFP_ASM_UNSAFE_BAND_SKEW_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<true>)),
       !DFP_ASM_UNSAFE_BAND_SKEW && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<false>)),
       !DFP_ASM_UNSAFE_BAND_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<true>)),
-      !DFP_ASM_UNSAFE_BAND && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<false>))};
+      !DFP_ASM_UNSAFE_BAND && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<false>)),
+      !DFP_ASM_UNSAFE_BAND_W8 && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 0, 4>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 32, 4>))};
   return safe;
 }
 
@@ -1411,15 +1497,19 @@ BwdwPlan plan_bwdw_mfma(const Geom& g) {
   return p;
 }
 
-// Band kernel geometry: row stride, channel stride (bytes) and bytes per
-// buffer; buf_bytes = 0 when the layer does not meet the kernel's conditions.
+// Band kernel geometry: row stride, channel stride (bytes), bytes per buffer
+// and run length (reduction indices per run: 8 when output and input widths
+// are multiples of 8, 4 when they are multiples of 4, which only the
+// eight-wave kernel reads); buf_bytes = 0 when the layer does not meet the
+// kernels' conditions.
 struct BandLayout {
-  int32_t row_bytes, ch_stride, buf_bytes;
+  int32_t row_bytes, ch_stride, buf_bytes, run;
 };
 static BandLayout band_layout(const Geom& g, const BwdwPlan& p) {
-  BandLayout bl{0, 0, 0};
-  if (g.sh != 1 || g.sw != 1 || (g.q % 8) != 0 || g.s > 4 || g.pw >= 4 || (g.w % 8) != 0 || (g.L % 32) != 0 ||
-      (p.T % 32) != 0 || p.T >= (1ll << 31))
+  BandLayout bl{0, 0, 0, 0};
+  const int32_t run = (g.q % 8) == 0 && (g.w % 8) == 0 ? 8 : (g.q % 4) == 0 && (g.w % 4) == 0 ? 4 : 0;
+  if (run == 0 || g.sh != 1 || g.sw != 1 || g.s > 4 || g.pw >= 4 || (g.L % 32) != 0 || (p.T % 32) != 0 ||
+      p.T >= (1ll << 31))
     return bl;
   bl.row_bytes = 2 * p.Wpad + 16;
   // channel stride congruent to 64 mod 256: with the odd row stride above, the
@@ -1430,6 +1520,7 @@ static BandLayout band_layout(const Geom& g, const BwdwPlan& p) {
   if (2 * buf > kBandLdsBytes) return bl;
   bl.ch_stride = (int32_t)chs;
   bl.buf_bytes = (int32_t)buf;
+  bl.run = run;
   return bl;
 }
 
@@ -1496,8 +1587,10 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   // the band kernels address both digit tensors with 32-bit buffer offsets
   const BandKernelsSafe& safe = band_kernels_safe();
   const bool l64 = g.L == 64 && (p.T % 64) == 0;  // every segment a whole number of two-block chunks
-  const bool band_ok = l64 ? (partials ? safe.skew_t : (safe.w8 || safe.skew_f))
-                           : (partials ? safe.band_t : safe.band_f);
+  // runs of 4: the eight-wave kernel only (L = 64, no partials)
+  const bool band_ok = bl.run == 8 ? (l64 ? (partials ? safe.skew_t : (safe.w8 || safe.skew_f))
+                                          : (partials ? safe.band_t : safe.band_f))
+                                   : (l64 && !partials && safe.w8_r4);
   if (band_ok && bl.buf_bytes > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 && p.ad_bytes < (1ll << 31) &&
       p.xp_bytes < (1ll << 31)) {
     uint8_t* xb = reinterpret_cast<uint8_t*>(xp);  // same workspace region as the pair layout
@@ -1509,18 +1602,21 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     const bool merged = g.c + gy_dy <= 65535;  // grid y limit; else dy gets its own launch
     if (!merged) DFP_LAUNCH(K_WPREP, k_prep_dy, dim3((unsigned)dy_blocks), dim3(256), 0, st, dq);
     const dim3 grid_xb((unsigned)gx, (unsigned)(g.c + (merged ? gy_dy : 0)));
-    if (g.pw == 0)
-      DFP_LAUNCH(K_XPREP, k_prep_xb<0>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
-                 bl.row_bytes, dq);
-    else if (g.pw == 1)
-      DFP_LAUNCH(K_XPREP, k_prep_xb<1>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
-                 bl.row_bytes, dq);
-    else if (g.pw == 2)
-      DFP_LAUNCH(K_XPREP, k_prep_xb<2>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
-                 bl.row_bytes, dq);
-    else
-      DFP_LAUNCH(K_XPREP, k_prep_xb<3>, grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, g.ph,
-                 bl.row_bytes, dq);
+#define DFP_PREP_XB(PW, VEC)                                                                                  \
+  DFP_LAUNCH(K_XPREP, (k_prep_xb<PW, VEC>), grid_xb, dim3(256), 0, st, x, xb, g.n, g.c, g.h, g.w, p.Hpad, p.Wpad, \
+             g.ph, bl.row_bytes, dq)
+    if (bl.run == 8) {
+      if (g.pw == 0) DFP_PREP_XB(0, 8);
+      else if (g.pw == 1) DFP_PREP_XB(1, 8);
+      else if (g.pw == 2) DFP_PREP_XB(2, 8);
+      else DFP_PREP_XB(3, 8);
+    } else {
+      if (g.pw == 0) DFP_PREP_XB(0, 4);
+      else if (g.pw == 1) DFP_PREP_XB(1, 4);
+      else if (g.pw == 2) DFP_PREP_XB(2, 4);
+      else DFP_PREP_XB(3, 4);
+    }
+#undef DFP_PREP_XB
     BwdwArgs args{};
     args.ad = ad;
     args.xb = xb;
@@ -1545,7 +1641,10 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.div_p = make_fastdiv((uint32_t)g.p);
     args.xb_bytes = (uint32_t)p.xp_bytes;
     const dim3 grid = bwdw_grid(args, p);
-    if (l64) {
+    if (bl.run == 4) {
+      if (p.Wpad == 32) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 32, 4>), grid, dim3(kThreadsW8), 0, st, args);
+      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 0, 4>), grid, dim3(kThreadsW8), 0, st, args);
+    } else if (l64) {
       // partials: the eight-wave kernel built for two waves per SIMD (its
       // partial stores need more than 128 VGPRs), else the two-tile kernel
       // (same chunks, same order of additions)

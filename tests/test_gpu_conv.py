@@ -140,6 +140,27 @@ def test_bwd_wt_band_no_partials(shape, G):
     run_all(shape, 64, G=G, partials=False)
 
 
+# Output widths that are multiples of 4 but not of 8 (ResNet-50's 28 x 28
+# layers): without partials at L = 64 the eight-wave band kernel reads runs of
+# 4 indices (8-byte windows); Q = 4 (one run per row), two 64-row dy tiles,
+# segments of one chunk to the whole reduction.
+RUN4_SHAPES = [
+    (4, 16, 12, 12, 32, 3, 3, 1, 1),
+    (4, 24, 20, 20, 40, 3, 3, 1, 1),
+    (4, 64, 28, 28, 64, 3, 3, 1, 1),
+    (4, 32, 12, 4, 20, 3, 3, 1, 1),
+    (8, 16, 10, 12, 80, 3, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", RUN4_SHAPES)
+@pytest.mark.parametrize("G", [0, 1, 3, 10 ** 6])
+def test_bwd_wt_band_runs_of_4(shape, G):
+    n, c, h, w, k, r, s, st, pd = shape
+    assert (w % 8) == 4 and (n * h * w) % 64 == 0
+    run_all(shape, 64, G=G, partials=False)
+
+
 # 32-channel blocks with reductions a multiple of 64 at L = 64: the
 # four-waves-per-SIMD kernel over the plane layout takes the forward (and the
 # backward-data where K is a multiple of 32), across one-chunk reductions
