@@ -1835,9 +1835,226 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   }
 }
 
+// Variant of the four-waves-per-SIMD kernel with 16 x 16 output tiles
+// (v_mfma_i32_16x16x64_i8: one instruction covers a whole chunk of 64
+// reduction indices), for layers whose 32 x 32 tiles are too few to give
+// every wave of the chip work (ResNet-50's 14 x 14 and 7 x 7 layers: 3136
+// and 1568 tiles of 32 x 32 for 4096 waves; 12544 and 6272 tiles of
+// 16 x 16).  Same plane-layout operands and unit ranges as the 32 x 32
+// kernel, but a workgroup keeps a 32-row filter slice in LDS, so a phase
+// holds up to 72 blocks (a ResNet-50 14 x 14 3 x 3 layer in one phase, a
+// 7 x 7 one in two); a unit is (16-pixel tile, 16-row subtile),
+// u = 2 * tile + sub.  Lane l multiplies pixel l % 16 of the tile (B) and row
+// l % 16 of the subtile (A) over the chunk's indices 16 (l / 16) .. + 15,
+// that is channel half (l / 16) % 2 of block 2 c + l / 32; it accumulates
+// rows 4 (l / 16) .. + 3 of the tile at pixel l % 16.  The B registers of
+// chunk c + 2 are loaded as soon as chunk c's MFMAs have issued (two
+// register sets, chunks taken in pairs: every phase has an even number of
+// chunks).  FP32 outputs only (no partials, no single-chunk INT32 mode).
+constexpr int32_t kS16Rows = 32;                   // filter rows per workgroup
+constexpr int32_t kS16Block = kS16Rows * 64;        // LDS bytes of one filter block
+constexpr int32_t kS16MaxKB = kW16MaxKB * kStageA / kS16Block;  // 72
+
+template <bool PHASED>
+__global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_s16(ConvMfmaArgs a) {
+  __shared__ __align__(16) uint8_t sA[kS16MaxKB * kS16Block];
+  __shared__ __align__(8) int32_t s_boff[kS16MaxKB];
+  __shared__ uint32_t red[kWaves16];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15;  // pixel of the tile, row of the subtile
+  const int kg = lane >> 4;   // index group of the chunk
+  const int32_t m0 = blockIdx.y * kS16Rows;
+  const int32_t kb0 = PHASED ? a.kb0 : 0, KB = PHASED ? a.kbn : a.KB, J = KB / 2, Cin = a.Cin;
+  const bool first_phase = !PHASED || (a.phase_flags & 1) != 0, last_phase = !PHASED || (a.phase_flags & 2) != 0;
+  const int32_t NP = (int32_t)a.NP, Qo = a.Qo, PQ = a.Po * a.Qo;
+  const int32_t e = __builtin_amdgcn_readfirstlane(a.ea->exp + a.eb->exp);
+
+  // ---- filter digits of this 32-row slice: KB blocks x 128 pieces of 16 B, direct to LDS
+  {
+    const int64_t a_block_bytes = (int64_t)a.Mp * 64;
+    const int32_t insts = (KB * kS16Block / 16) / 64;  // one instruction fills 64 consecutive slots
+    for (int32_t j = wave; j < insts; j += kWaves16) {
+      const int32_t slot0 = j * 64;
+      const int32_t sl = slot0 + lane;
+      const int32_t kb = sl / (kS16Block / 16), sw = sl % (kS16Block / 16);
+      const int row = sw >> 2, piece = (sw & 3) ^ ((row >> 2) & 3);
+      const uint8_t* src =
+          a.wsa + (kb0 + kb) * a_block_bytes + ((int64_t)(m0 + row) * 2 + (piece >> 1)) * 32 + (piece & 1) * 16;
+      __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(sA + slot0 * 16), 16, 0, 0);
+    }
+  }
+  const int32_t cpb = Cin >> 5;
+  const int32_t plane_bytes = a.Wp * 16;
+  auto boff_of = [&](int32_t kb) {
+    const int32_t tap = kb / cpb, cb = kb - tap * cpb;
+    const int32_t r = tap / a.S, sx = tap - r * a.S;
+    return a.rsign * (r * cpb * 4 * plane_bytes + sx * 16) + cb * 4 * plane_bytes;
+  };
+  if ((int32_t)threadIdx.x < KB) s_boff[threadIdx.x] = boff_of(kb0 + (int32_t)threadIdx.x);
+
+  // ---- this workgroup's unit range (XCD x = workgroup id mod 8 gets adjacent ranges)
+  const int32_t units = 2 * ((NP + 15) / 16);
+  const int32_t G = gridDim.x;
+  const int32_t xcd = blockIdx.x & 7, per = G >> 3, rem = G & 7;
+  const int32_t vb = xcd * per + min(xcd, rem) + (blockIdx.x >> 3);
+  const int32_t u0 = (int32_t)((int64_t)units * vb / G), u1 = (int32_t)((int64_t)units * (vb + 1) / G);
+  const int32_t my_units = (u1 - u0 > wave) ? (u1 - u0 - wave + kWaves16 - 1) / kWaves16 : 0;
+  auto unit_of = [&](int32_t i) { return u0 + wave + kWaves16 * i; };
+  // byte offset of this lane's operand (pixel of unit u, channel half kg % 2)
+  auto pixel_off = [&](int32_t u) -> int32_t {
+    int32_t gp = (u >> 1) * 16 + col;
+    if (gp >= NP) gp = 0;
+    const int32_t im = (int32_t)fdiv((uint32_t)gp, a.div_pq), rp = gp - im * PQ;
+    const int32_t po = (int32_t)fdiv((uint32_t)rp, a.div_q), qo = rp - po * Qo;
+    return ((im * a.Hp + po * a.ustride_h + a.roff_h) * cpb * 4 + (kg & 1)) * plane_bytes +
+           (qo * a.ustride_w + a.roff_w) * 16;
+  };
+  // this lane's block offset for chunk c (block 2 c + kg / 2 of the phase)
+  auto boff_chunk = [&](int32_t c) {
+    const int2 bo = *reinterpret_cast<const int2*>(s_boff + 2 * c);
+    return (kg & 2) ? bo.y : bo.x;
+  };
+  auto load_b = [&](v4i& hi, v4i& lo, int32_t pix, int32_t boff) {
+    const uint32_t off = (uint32_t)(pix + boff);
+    __builtin_amdgcn_sched_barrier(0);
+    hi = *reinterpret_cast<const v4i*>(a.xs + off);
+    lo = *reinterpret_cast<const v4i*>(a.xs + (off + 2 * plane_bytes));
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  const bool full_rows = a.M == a.Mp;
+  const bool out_buf = a.O < (1ll << 30);
+  const __amdgpu_buffer_rsrc_t rs_out =
+      __builtin_amdgcn_make_buffer_rsrc(a.out, (short)0, out_buf ? (int)(a.O * 4) : 0, 0x00020000);
+  uint32_t amax = 0;
+  int32_t cur_pix = 0;
+  v4i b0h, b0l, b1h, b1l;
+  // B of the first unit's chunks 0 and 1 while the filter digits are in flight
+  if (my_units > 0) {
+    cur_pix = pixel_off(unit_of(0));
+    const int32_t kq = kg >> 1;
+    load_b(b0h, b0l, cur_pix, boff_of(kb0 + kq));
+    load_b(b1h, b1l, cur_pix, boff_of(kb0 + 2 + kq));
+    wait_vmcnt<4>();
+  } else {
+    wait_vmcnt<0>();
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+  if (my_units > 0) {
+    // A: row col of the subtile, channel half kg % 2 of block kg / 2 (hi, lo pieces)
+    const uint32_t ra_hi = swz(col, 2 * (kg & 1)) * 16 + (kg >> 1) * kS16Block;
+    const uint32_t ra_lo = swz(col, 2 * (kg & 1) + 1) * 16 + (kg >> 1) * kS16Block;
+    for (int32_t unit = 0; unit < my_units; ++unit) {
+      const int32_t u = unit_of(unit);
+      const int32_t next_pix = unit + 1 < my_units ? pixel_off(unit_of(unit + 1)) : cur_pix;
+      const int32_t sub = u & 1;
+      const int32_t g = (u >> 1) * 16 + col;
+      const bool gvalid = g < NP;
+      int32_t obase = 0;
+      if (gvalid) {
+        const int32_t im = (int32_t)fdiv((uint32_t)g, a.div_pq);
+        obase = im * a.M * PQ + (g - im * PQ);
+      }
+      const int32_t mrow0 = m0 + 16 * sub + 4 * kg;
+      v4i hh, xx, ll;
+      float sum[4] = {0.f, 0.f, 0.f, 0.f};
+      if (PHASED && !first_phase && gvalid) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int32_t m = mrow0 + v;
+          if (m < a.M) sum[v] = a.out[(uint32_t)(obase + m * PQ)];
+        }
+      }
+      const uint8_t* ab = sA + sub * 1024;
+      auto chunk = [&](int32_t c, v4i& bh, v4i& bl) __attribute__((always_inline)) {
+        const v4i ah = *reinterpret_cast<const v4i*>(ab + c * 2 * kS16Block + ra_hi);
+        const v4i al = *reinterpret_cast<const v4i*>(ab + c * 2 * kS16Block + ra_lo);
+        const v4i z = {0, 0, 0, 0};
+        hh = __builtin_amdgcn_mfma_i32_16x16x64_i8(ah, bh, z, 0, 0, 0);
+        ll = __builtin_amdgcn_mfma_i32_16x16x64_i8(al, bl, z, 0, 0, 0);
+        xx = __builtin_amdgcn_mfma_i32_16x16x64_i8(ah, bl, z, 0, 0, 0);
+        xx = __builtin_amdgcn_mfma_i32_16x16x64_i8(al, bh, xx, 0, 0, 0);
+        // chunk c + 2 of this unit, or chunk c + 2 - J of the next one
+        const int32_t nc = c + 2 < J ? c + 2 : c + 2 - J;
+        load_b(bh, bl, c + 2 < J ? cur_pix : next_pix, boff_chunk(nc));
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const uint32_t p = recombine((uint32_t)hh[v], (uint32_t)xx[v], (uint32_t)ll[v]);
+          sum[v] += (float)(int32_t)p;
+        }
+      };
+      for (int32_t c = 0; c < J; c += 2) {
+        chunk(c, b0h, b0l);
+        chunk(c + 1, b1h, b1l);
+      }
+      if (PHASED && gvalid && !last_phase) {  // unscaled sums for the next phase
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int32_t m = mrow0 + v;
+          if (m < a.M) a.out[(uint32_t)(obase + m * PQ)] = sum[v];
+        }
+      } else if (gvalid) {
+        if (full_rows && out_buf) {
+          const uint32_t lane_off = (uint32_t)(obase + mrow0 * PQ) * 4u;
+          float fmx = 0.f;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const float y = ldexpf(sum[v], e);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(y), rs_out, lane_off, (uint32_t)(v * PQ) * 4u, 0);
+            fmx = fmaxf(fmx, fabsf(y));
+          }
+          amax = max(amax, __float_as_uint(fmx));
+        } else {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int32_t m = mrow0 + v;
+            if (m < a.M) amax = max(amax, store_out<false>(a.out, (uint32_t)(obase + m * PQ), sum[v], e));
+          }
+        }
+      }
+      cur_pix = next_pix;
+    }
+  }
+
+  if (a.so && last_phase) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
+    if (lane == 0) red[wave] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t b = red[0];
+      for (int i = 1; i < kWaves16; ++i) b = max(b, red[i]);
+      if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
+      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+    }
+  }
+}
+
 inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
 
 }  // namespace
+
+// The 16 x 16-tile kernel serves FP32 outputs at L = 64 without partials
+// when the 32 x 32 tiles are fewer than the chip's wave slots (16 per CU) and
+// every phase (whole chunks, at most kS16MaxKB blocks, as equal as possible)
+// has an even number of chunks.
+static bool use_s16(int64_t NP, int32_t Mp, int32_t KB, bool partials, int cus) {
+  if (partials || 2 * ((NP + 31) / 32) * (Mp / kMT) >= (int64_t)cus * kWaves16) return false;
+  const int32_t chunks = KB / 2, nph = (KB + kS16MaxKB - 1) / kS16MaxKB;
+  for (int32_t ph = 0; ph < nph; ++ph) {
+    const int32_t n = chunks * (ph + 1) / nph - chunks * ph / nph;
+    if (n < 2 || n % 2 != 0) return false;
+  }
+  return true;
+}
+
+static int device_cus() {
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  return cus;
+}
 
 bool conv_w16_eligible(int32_t Cin, int32_t T, int32_t L, bool i32) {
   // FP32 outputs at L = 64 take any number of blocks in phases of at most
@@ -1896,12 +2113,17 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
                p.ws_b_bytes < (1ll << 31);
   if (plane && p.KB > kW16MaxKB && !prefer_w16) {
     // phases pay the kernel's fixed cost once each: taken only when every wave
-    // of a workgroup has a unit of work in each phase
-    int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    const int64_t units = 2 * (((int64_t)g.n * p.Po * p.Qo + 31) / 32);
-    const int64_t gx = std::max<int64_t>(1, cus / (p.Mp / kMT));
-    plane = units >= gx * kWaves16;
+    // of a workgroup has a unit of work in each phase (units of the 16 x 16
+    // kernel where that one runs)
+    const int cus = device_cus();
+    const int64_t NP = (int64_t)g.n * p.Po * p.Qo;
+    if (use_s16(NP, p.Mp, p.KB, partials != nullptr, cus)) {
+      const int64_t gx = std::max<int64_t>(1, cus / (p.Mp / kS16Rows));
+      plane = 2 * ((NP + 15) / 16) >= gx * kWaves16 || p.KB <= kS16MaxKB;
+    } else {
+      const int64_t gx = std::max<int64_t>(1, cus / (p.Mp / kMT));
+      plane = 2 * ((NP + 31) / 32) >= gx * kWaves16;
+    }
   }
   const PrepAArgs pa{b, wsa, p.M, p.Mp, p.Cin, g.r, g.s, p.T, p.KB, fwd ? 0 : 1, g.c, so, boff,
                      tap_row_bytes, tap_col_bytes};
@@ -2039,6 +2261,24 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     // each launch continues the chunk sums the previous one left in the output
     const int32_t chunks = args.KB / 2;
     const int32_t nph = (args.KB + kW16MaxKB - 1) / kW16MaxKB;
+    const int cus = device_cus();
+    const int64_t mtiles = args.Mp / kMT;
+    if (use_s16(args.NP, args.Mp, args.KB, partials, cus)) {
+      const int64_t units16 = 2 * ((args.NP + 15) / 16), stiles = args.Mp / kS16Rows;
+      const int32_t nph16 = (args.KB + kS16MaxKB - 1) / kS16MaxKB;
+      int64_t gx = std::max<int64_t>(1, cus / stiles);
+      gx = std::min<int64_t>(gx, (units16 + kWaves16 - 1) / kWaves16);
+      const dim3 grid_s((unsigned)gx, (unsigned)stiles);
+      for (int32_t ph = 0; ph < nph16; ++ph) {
+        const int32_t c0 = chunks * ph / nph16, c1 = chunks * (ph + 1) / nph16;
+        args.kb0 = 2 * c0;
+        args.kbn = 2 * (c1 - c0);
+        args.phase_flags = (ph == 0 ? 1 : 0) | (ph == nph16 - 1 ? 2 : 0);
+        if (nph16 == 1) DFP_LAUNCH(kid, (k_conv_mfma_s16<false>), grid_s, dim3(kThreads16), 0, st, args);
+        else DFP_LAUNCH(kid, (k_conv_mfma_s16<true>), grid_s, dim3(kThreads16), 0, st, args);
+      }
+      return DFP_OK;
+    }
     const dim3 grid16 = w16_grid();
     for (int32_t ph = 0; ph < nph; ++ph) {
       const int32_t c0 = chunks * ph / nph, c1 = chunks * (ph + 1) / nph;

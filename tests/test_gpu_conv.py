@@ -190,6 +190,27 @@ def test_w16_shapes(shape, partials):
     run_all(shape, 64, path=dfp.PATH_MFMA, partials=partials)
 
 
+# Fewer 32 x 32 output tiles than the chip's wave slots, every phase an even
+# number of chunks, no partials: the 16 x 16-tile kernel (ResNet-50's 14 x 14
+# and 7 x 7 layers): one to three phases of up to 72 blocks, ragged pixel
+# tiles, output channels not a multiple of 64, stride 2 (backward-data of that
+# shape reads a dilated plane), 1 x 1 with two and four chunks.
+S16_SHAPES = [
+    (2, 256, 14, 14, 64, 3, 3, 1, 1),
+    (1, 768, 5, 5, 64, 3, 3, 1, 1),
+    (1, 512, 7, 7, 96, 3, 3, 1, 1),
+    (2, 128, 5, 5, 192, 3, 3, 1, 1),
+    (2, 128, 10, 10, 64, 3, 3, 2, 1),
+    (2, 128, 8, 8, 256, 1, 1, 1, 0),
+    (4, 256, 7, 7, 512, 3, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", S16_SHAPES)
+def test_s16_shapes(shape):
+    run_all(shape, 64, path=dfp.PATH_MFMA, partials=False)
+
+
 @pytest.mark.parametrize("G", [1, 2, 3, 50])
 def test_bwd_wt_segments(G):
     run_all((4, 16, 12, 12, 8, 3, 3, 1, 1), 16, G=G)
