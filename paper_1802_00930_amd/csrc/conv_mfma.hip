@@ -2032,6 +2032,216 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_s16(ConvMfmaArgs a)
   }
 }
 
+// Forward kernel for inputs with few channels (fewer than 16, such as an
+// image's three colour channels), at L = 64 with FP32 outputs.  The forward
+// reduction order is t = (r S + s) C + c, and for one filter row r the S C
+// values (s, c) of an output pixel are contiguous in a channel-last row of the
+// input (byte (q sw + s) C + c of input row p sh + r), so the 16 consecutive
+// indices a lane multiplies are at most two contiguous byte runs, one at the
+// end of filter row r0 and one at the start of row r0 + 1 (S C >= 16).  The
+// input digits are prepared as XC[n][hp][d][row_b] (k_prep_cl); a lane loads
+// 16 bytes at each run's start (byte-aligned buffer loads) and keeps the
+// first n0 bytes of the first and the rest of the second (v_bfi with byte
+// masks).  The offsets and masks of each (block, lane half) are a table in
+// LDS.  Indices past T meet zero filter digits.  Filter digits are resident in
+// LDS (at most kW16MaxKB blocks); the units, output epilogue and max are
+// those of the four-waves-per-SIMD kernel; chunks are two blocks, the last one
+// of an odd block count is a single block.
+struct ClArgs {
+  int32_t row_b;  // bytes of one digit row (at least Wp C + 16, a multiple of 16)
+  int32_t SC;     // S C
+  uint32_t xc_bytes;
+};
+
+template <bool PARTIALS>
+__global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_cl(ConvMfmaArgs a, ClArgs cl) {
+  __shared__ __align__(16) uint8_t sA[kW16MaxKB * kStageA];
+  // per (block, lane half): byte offsets of the two runs, then the four dword masks of the first
+  __shared__ __align__(16) int4 s_tab[2 * kW16MaxKB][2];
+  __shared__ uint32_t red[kWaves16];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int half = lane >> 5;
+  const int col = lane & 31;
+  const int32_t m0 = blockIdx.y * kMT;
+  const int32_t KB = a.KB, Cin = a.Cin;
+  const int32_t NP = (int32_t)a.NP, Qo = a.Qo, PQ = a.Po * a.Qo;
+  const int32_t e = __builtin_amdgcn_readfirstlane(a.ea->exp + a.eb->exp);
+  const int32_t rstride = 2 * cl.row_b;  // one input row: hi and lo digit rows
+
+  {
+    const int64_t a_block_bytes = (int64_t)a.Mp * 64;
+    const int32_t insts = (KB * 256) / 64;
+    for (int32_t j = wave; j < insts; j += kWaves16) {
+      const int32_t slot0 = j * 64;
+      const int32_t sl = slot0 + lane;
+      const int32_t kb = sl >> 8, sw = sl & 255;
+      const int row = sw >> 2, piece = (sw & 3) ^ ((row >> 2) & 3);
+      const uint8_t* src = a.wsa + kb * a_block_bytes + ((int64_t)(m0 + row) * 2 + (piece >> 1)) * 32 + (piece & 1) * 16;
+      __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(sA + slot0 * 16), 16, 0, 0);
+    }
+  }
+  if ((int32_t)threadIdx.x < 2 * KB) {
+    const int32_t t0 = 16 * (int32_t)threadIdx.x;  // (block b, half h) = (i / 2, i % 2)
+    const int32_t r0 = t0 / cl.SC, j0 = t0 - r0 * cl.SC, n0 = cl.SC - j0;
+    int4 m;
+    int* mp = reinterpret_cast<int*>(&m);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int32_t nb = min(max(n0 - 4 * k, 0), 4);
+      mp[k] = nb >= 4 ? -1 : (int)((1u << (8 * nb)) - 1u);
+    }
+    s_tab[threadIdx.x][0] = make_int4(r0 * rstride + j0, (r0 + 1) * rstride - n0, 0, 0);
+    s_tab[threadIdx.x][1] = m;
+  }
+
+  const int32_t units = 2 * ((NP + 31) / 32);
+  const int32_t G = gridDim.x;
+  const int32_t xcd = blockIdx.x & 7, per = G >> 3, rem = G & 7;
+  const int32_t vb = xcd * per + min(xcd, rem) + (blockIdx.x >> 3);
+  const int32_t u0 = (int32_t)((int64_t)units * vb / G), u1 = (int32_t)((int64_t)units * (vb + 1) / G);
+  const int32_t my_units = (u1 - u0 > wave) ? (u1 - u0 - wave + kWaves16 - 1) / kWaves16 : 0;
+  auto unit_of = [&](int32_t i) { return u0 + wave + kWaves16 * i; };
+  // byte offset in XC of this lane's pixel of unit u at filter row 0, channel 0
+  auto pixel_off = [&](int32_t u) -> int32_t {
+    int32_t gp = (u >> 1) * 32 + col;
+    if (gp >= NP) gp = 0;
+    const int32_t im = (int32_t)fdiv((uint32_t)gp, a.div_pq), rp = gp - im * PQ;
+    const int32_t po = (int32_t)fdiv((uint32_t)rp, a.div_q), qo = rp - po * Qo;
+    return (im * a.Hp + po * a.ustride_h) * rstride + qo * a.ustride_w * Cin;
+  };
+  const __amdgpu_buffer_rsrc_t rs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.xs), (short)0,
+                                                                        (int)cl.xc_bytes, 0x00020000);
+  struct Raw {
+    v4i ha, hb, la, lb;
+  };
+  auto load_raw = [&](Raw& r, int32_t pix, int32_t kb) {
+    const int4 o = s_tab[2 * kb + half][0];
+    const uint32_t oa = (uint32_t)(pix + o.x), ob = (uint32_t)(pix + o.y);
+    r.ha = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rs_x, oa, 0, 0));
+    r.hb = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rs_x, ob, 0, 0));
+    r.la = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rs_x, oa + cl.row_b, 0, 0));
+    r.lb = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rs_x, ob + cl.row_b, 0, 0));
+  };
+  auto merge = [&](const v4i& x, const v4i& y, const int4& m) {
+    return v4i{(x[0] & m.x) | (y[0] & ~m.x), (x[1] & m.y) | (y[1] & ~m.y), (x[2] & m.z) | (y[2] & ~m.z),
+               (x[3] & m.w) | (y[3] & ~m.w)};
+  };
+
+  const bool full_rows = a.M == a.Mp;
+  const bool out_buf = a.O < (1ll << 30);
+  const __amdgpu_buffer_rsrc_t rs_out =
+      __builtin_amdgcn_make_buffer_rsrc(a.out, (short)0, out_buf ? (int)(a.O * 4) : 0, 0x00020000);
+  uint32_t amax = 0;
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  if (my_units > 0) {
+    const uint32_t ra_hi = swz(col, 2 * half) * 16, ra_lo = swz(col, 2 * half + 1) * 16;
+    int32_t cur_pix = pixel_off(unit_of(0));
+    Raw nx;
+    load_raw(nx, cur_pix, 0);
+    for (int32_t unit = 0; unit < my_units; ++unit) {
+      const int32_t u = unit_of(unit);
+      const int32_t msub = u & 1;
+      const int32_t g = (u >> 1) * 32 + col;
+      const bool gvalid = g < NP;
+      int32_t obase = 0;
+      if (gvalid) {
+        const int32_t im = (int32_t)fdiv((uint32_t)g, a.div_pq);
+        obase = im * a.M * PQ + (g - im * PQ);
+      }
+      const int32_t mrow0 = m0 + 32 * msub + 4 * half;
+      Acc3 acc;
+      float sum[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sum[v] = 0.f;
+      const uint8_t* ab = sA + msub * 2048;
+      for (int32_t kb = 0; kb < KB; ++kb) {
+        const int4 m = s_tab[2 * kb + half][1];
+        const v4i bh = merge(nx.ha, nx.hb, m), bl = merge(nx.la, nx.lb, m);
+        // the next block of this unit, or the first block of the next unit
+        if (kb + 1 < KB) {
+          load_raw(nx, cur_pix, kb + 1);
+        } else {
+          if (unit + 1 < my_units) cur_pix = pixel_off(unit_of(unit + 1));
+          load_raw(nx, cur_pix, 0);
+        }
+        const v4i ah = *reinterpret_cast<const v4i*>(ab + kb * kStageA + ra_hi);
+        const v4i al = *reinterpret_cast<const v4i*>(ab + kb * kStageA + ra_lo);
+        mfma_tile(acc, ah, al, bh, bl, (kb & 1) == 0);
+        if ((kb & 1) == 1 || kb + 1 == KB)
+          flush_tile<PARTIALS>(acc, sum, kb >> 1, a.partials, a.O, obase, PQ, mrow0, a.M, gvalid);
+      }
+      if (gvalid) {
+        if (full_rows && out_buf) {
+          const uint32_t lane_off = (uint32_t)(obase + mrow0 * PQ) * 4u;
+          float fmx = 0.f;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float y = ldexpf(sum[v], e);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(y), rs_out, lane_off,
+                                                  (uint32_t)((8 * (v >> 2) + (v & 3)) * PQ) * 4u, 0);
+            fmx = fmaxf(fmx, fabsf(y));
+          }
+          amax = max(amax, __float_as_uint(fmx));
+        } else {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int32_t m = mrow0 + 8 * (v >> 2) + (v & 3);
+            if (m < a.M) amax = max(amax, store_out<false>(a.out, (uint32_t)(obase + m * PQ), sum[v], e));
+          }
+        }
+      }
+    }
+  }
+
+  if (a.so) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, off, 64));
+    if (lane == 0) red[wave] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t b = red[0];
+      for (int i = 1; i < kWaves16; ++i) b = max(b, red[i]);
+      if (b > __atomic_load_n(&a.so->amax_bits, __ATOMIC_RELAXED)) atomicMax(&a.so->amax_bits, b);
+      if (b == 0x7f800000u) atomicOr(&a.so->flags, DFP_FLAG_OUTPUT_INF);
+    }
+  }
+}
+
+// XC[n][hp][d][row_b] for k_conv_mfma_cl: byte wp C + c of digit row d (0 hi,
+// 1 lo) holds that digit of x[n][c][hp - ph][wp - pw] (zero outside the
+// image); thread (n, hp, group of four columns).  Bytes past Wp C stay unset
+// (they only ever meet zero filter digits or a mask).
+__global__ __launch_bounds__(256) void k_prep_cl(const int16_t* __restrict__ x, uint8_t* __restrict__ xc, int32_t N,
+                                                int32_t C, int32_t H, int32_t W, int32_t Hp, int32_t Wp, int32_t ph,
+                                                int32_t pw, int32_t row_b) {
+  const int32_t W4 = (Wp + 3) / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)N * Hp * W4) return;
+  const int32_t w4 = (int32_t)(i % W4);
+  const int64_t r = i / W4;  // n * Hp + hp
+  const int32_t hp = (int32_t)(r % Hp), n = (int32_t)(r / Hp);
+  const int32_t h = hp - ph;
+  uint8_t* hi = xc + r * 2 * row_b + 4 * w4 * C;
+  uint8_t* lo = hi + row_b;
+  for (int32_t k = 0; k < 4 * C; k += 4) {  // four bytes: (column, channel) = divmod(4 w4 C + k + b, C)
+    uint32_t dh = 0u, dl = 0u;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int32_t idx = k + b, wq = 4 * w4 + idx / C, c = idx - (idx / C) * C;
+      const int32_t w = wq - pw;
+      int32_t v = 0;
+      if (wq < Wp && h >= 0 && h < H && w >= 0 && w < W) v = x[(((int64_t)n * C + c) * H + h) * W + w];
+      dh |= hi_digit(v) << (8 * b);
+      dl |= lo_digit(v) << (8 * b);
+    }
+    *reinterpret_cast<uint32_t*>(hi + k) = dh;
+    *reinterpret_cast<uint32_t*>(lo + k) = dl;
+  }
+}
+
 inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
 
 }  // namespace
@@ -2135,6 +2345,40 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
       kPlaneDirect ? (int64_t)p.Hp * 256 : (int64_t)((p.Hp + rb_plane - 1) / rb_plane) * p.CG * 256;
   const bool merge_a = plane && a_total <= 8 * slice_threads;
   if (!merge_a) DFP_LAUNCH(K_WPREP, k_prep_a, dim3((unsigned)((a_total + 255) / 256)), dim3(256), 0, st, pa);
+  // few input channels (forward, L = 64, FP32 outputs): channel-last digit rows
+  const int32_t cl_row_b = (p.Wp * p.Cin + 31) / 16 * 16;
+  const int64_t cl_bytes = ((int64_t)g.n * p.Hp + 2) * 2 * cl_row_b;
+  if (fwd && !i32 && g.L == 64 && p.Cin < 16 && g.s * p.Cin >= 16 && p.KB <= kW16MaxKB &&
+      cl_bytes <= p.ws_b_bytes && cl_bytes < (1ll << 31) && (int64_t)g.n * p.Po * p.Qo * p.M < (1ll << 30)) {
+    const int64_t items = (int64_t)g.n * p.Hp * ((p.Wp + 3) / 4);
+    DFP_LAUNCH(K_XPREP, k_prep_cl, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, a, xs, g.n, p.Cin, g.h,
+               g.w, p.Hp, p.Wp, g.ph, g.pw, cl_row_b);
+    ConvMfmaArgs args{};
+    args.xs = xs;
+    args.wsa = wsa;
+    args.ea = sa;
+    args.eb = sb;
+    args.out = out;
+    args.so = so;
+    args.partials = partials;
+    args.M = p.M; args.Mp = p.Mp; args.Cin = p.Cin; args.S = g.s; args.T = p.T; args.KB = p.KB; args.L = g.L;
+    args.Hp = p.Hp; args.Wp = p.Wp; args.Po = p.Po; args.Qo = p.Qo;
+    args.NP = (int64_t)g.n * p.Po * p.Qo;
+    args.O = args.NP * p.M;
+    args.ustride_h = g.sh;
+    args.ustride_w = g.sw;
+    args.div_pq = make_fastdiv((uint32_t)(p.Po * p.Qo));
+    args.div_q = make_fastdiv((uint32_t)p.Qo);
+    const ClArgs cla{cl_row_b, g.s * p.Cin, (uint32_t)cl_bytes};
+    const int cus = device_cus();
+    const int64_t units = 2 * ((args.NP + 31) / 32), mtiles = p.Mp / kMT;
+    int64_t gx = std::max<int64_t>(1, cus / mtiles);
+    gx = std::min<int64_t>(gx, (units + kWaves16 - 1) / kWaves16);
+    const dim3 grid((unsigned)gx, (unsigned)mtiles);
+    if (partials) DFP_LAUNCH(K_FWD_MFMA, (k_conv_mfma_cl<true>), grid, dim3(kThreads16), 0, st, args, cla);
+    else DFP_LAUNCH(K_FWD_MFMA, (k_conv_mfma_cl<false>), grid, dim3(kThreads16), 0, st, args, cla);
+    return DFP_OK;
+  }
   {
     const int32_t Cs = fwd ? g.c : g.k, Hs = fwd ? g.h : g.p, Wsrc = fwd ? g.w : g.q;
     const bool vec = (Wsrc % 8) == 0 && (reinterpret_cast<uintptr_t>(a) & 15) == 0;
