@@ -525,6 +525,131 @@ __global__ __launch_bounds__(k1x1Threads, 4) void k_bwdw_1x1(BwdwArgs a, const u
   }
 }
 
+// 16-byte piece `piece` of row `row` in a 64-byte-per-row operand block,
+// swizzled so that the pieces a wave reads fall on distinct LDS banks.
+__device__ __forceinline__ int swz(int row, int piece) { return row * 4 + (piece ^ ((row >> 2) & 3)); }
+
+// Unit-stride 1x1 weight gradient from the INT16 tensors through LDS (the
+// default when P*Q is a multiple of 4).  Per band of 64 indices (two 32-index
+// blocks) the workgroup loads the 64-row slices of dy and x it multiplies with
+// coalesced loads, PIECE consecutive elements per lane (16 or 8 bytes, 128
+// contiguous bytes per row and band), splits every element into its byte
+// digits once, and writes them in the MFMA operand layout: per block and row,
+// four 16-byte pieces (hi digits of indices 0-15, 16-31, then lo), swizzled
+// across LDS banks as in the forward kernels.  Each of the four waves then
+// reads its 32 x 32 tile's operands from LDS.  The loads of band b + 1 are in
+// flight while band b is multiplied (two LDS buffers, one barrier per band).
+// A piece lies in one image (P*Q a multiple of PIECE); rows past K or C and
+// indices past T are zeros.  Chunks, segments and output as in k_bwdw_1x1.
+template <int PIECE>
+__global__ __launch_bounds__(k1x1Threads, 4) void k_bwdw_1x1s(BwdwArgs a, Raw1x1 raw) {
+  constexpr int kLoads = 64 * 64 / PIECE / k1x1Threads;  // pieces per thread and operand per band
+  constexpr int kPerRow = 64 / PIECE;                     // pieces per row and band
+  __shared__ __align__(16) uint8_t sbuf[2][2][2 * 4096];  // [buffer][operand][block][64 rows x 64 B]
+  const BwdwTile tl = bwdw_tile(a);
+  if (tl.seg >= a.nseg) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, lc = lane & 31;
+  const int32_t rA0 = tl.ty * 64, rB0 = tl.tx * 64;  // the workgroup's dy rows (k) and x rows (c)
+  const int64_t t_seg0 = (int64_t)tl.seg * a.G * a.L;
+  const int64_t t_seg1 = min(t_seg0 + (int64_t)a.G * a.L, a.T);
+  const int64_t kb_begin = t_seg0 / 32, kb_end = (t_seg1 + 31) / 32;
+  const int32_t chunk_blocks = a.L / 32;
+  const int32_t PQ = raw.PQ;
+  typedef uint32_t vraw __attribute__((ext_vector_type(PIECE / 2)));
+  vraw ra[kLoads], rb[kLoads];
+  // piece i = j * 256 + thread of the band starting at block kb: row i / kPerRow,
+  // indices PIECE (i % kPerRow) .. of the band; i % kPerRow is the same for
+  // every j (256 is a multiple of kPerRow), so a thread's pieces share one
+  // index range and one image (element offsets below 2^31: checked by the launcher)
+  const int32_t pj = (int32_t)threadIdx.x % kPerRow, row0 = (int32_t)threadIdx.x / kPerRow;
+  auto load_band = [&](int64_t kb) {
+    const int32_t t = (int32_t)(kb * 32) + PIECE * pj;
+    const bool tin = t < (int32_t)a.T;
+    const int32_t n = (int32_t)fdiv((uint32_t)(tin ? t : 0), a.div_q), pq = t - n * PQ;
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int32_t row = j * (k1x1Threads / kPerRow) + row0;
+      ra[j] = vraw{};
+      rb[j] = vraw{};
+      if (tin && rA0 + row < a.K)
+        ra[j] = *reinterpret_cast<const vraw*>(raw.dy + (uint32_t)((n * a.K + rA0 + row) * PQ + pq));
+      if (tin && rB0 + row < a.C)
+        rb[j] = *reinterpret_cast<const vraw*>(raw.x + (uint32_t)((n * a.C + rB0 + row) * PQ + pq));
+    }
+  };
+  // digits of the staged pieces into buffer buf
+  auto write_band = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int32_t row = j * (k1x1Threads / kPerRow) + row0;
+      const int32_t e = PIECE * pj;                       // index within the band
+      const int32_t blk = e >> 5, h16 = (e >> 4) & 1, sub = e & 15;
+      const int32_t off_hi = blk * 4096 + swz(row, h16) * 16 + sub;
+      const int32_t off_lo = blk * 4096 + swz(row, 2 + h16) * 16 + sub;
+#pragma unroll
+      for (int op = 0; op < 2; ++op) {
+        const vraw w = op == 0 ? ra[j] : rb[j];
+        uint32_t hi[PIECE / 4], lo[PIECE / 4];
+#pragma unroll
+        for (int d = 0; d < PIECE / 4; ++d) {
+          const uint32_t w0 = w[2 * d], w1 = w[2 * d + 1];
+          const uint32_t h0 = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, w0) + (u16x2){128, 128});
+          const uint32_t h1 = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, w1) + (u16x2){128, 128});
+          lo[d] = __builtin_amdgcn_perm(w1, w0, 0x06040200u);
+          hi[d] = __builtin_amdgcn_perm(h1, h0, 0x07050301u);
+        }
+        uint8_t* base = &sbuf[buf][op][0];
+        if (PIECE == 8) {
+          *reinterpret_cast<uint2*>(base + off_hi) = make_uint2(hi[0], hi[1]);
+          *reinterpret_cast<uint2*>(base + off_lo) = make_uint2(lo[0], lo[1]);
+        } else {
+          *reinterpret_cast<uint32_t*>(base + off_hi) = hi[0];
+          *reinterpret_cast<uint32_t*>(base + off_lo) = lo[0];
+        }
+      }
+    }
+  };
+
+  Acc3 acc;
+  float sum[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) sum[v] = 0.f;
+  const int32_t ra_row = (wave >> 1) * 32 + lc, rb_row = (wave & 1) * 32 + lc;
+  const uint32_t oa_hi = swz(ra_row, half) * 16, oa_lo = swz(ra_row, 2 + half) * 16;
+  const uint32_t ob_hi = swz(rb_row, half) * 16, ob_lo = swz(rb_row, 2 + half) * 16;
+  int32_t blk_in_chunk = 0;
+  load_band(kb_begin);
+  int buf = 0;
+  for (int64_t kb = kb_begin; kb < kb_end; kb += 2, buf ^= 1) {
+    write_band(buf);
+    __syncthreads();
+    if (kb + 2 < kb_end) load_band(kb + 2);
+    const int32_t nblk = (int32_t)min((int64_t)2, kb_end - kb);
+    for (int32_t b = 0; b < nblk; ++b) {
+      const uint8_t* pa = &sbuf[buf][0][b * 4096];
+      const uint8_t* pb = &sbuf[buf][1][b * 4096];
+      const v4i ahi = *reinterpret_cast<const v4i*>(pa + oa_hi), alo = *reinterpret_cast<const v4i*>(pa + oa_lo);
+      const v4i bhi = *reinterpret_cast<const v4i*>(pb + ob_hi), blo = *reinterpret_cast<const v4i*>(pb + ob_lo);
+      mfma_tile(acc, ahi, alo, bhi, blo, blk_in_chunk == 0);
+      if (++blk_in_chunk == chunk_blocks || kb + b == kb_end - 1) {
+        flush_tile<false>(acc, sum, 0, nullptr, a.O, 0, a.C, 0, a.K, false);
+        blk_in_chunk = 0;
+      }
+    }
+  }
+  const int32_t m0 = rA0 + (wave >> 1) * 32, c = rB0 + (wave & 1) * 32 + lc;
+  const int32_t e = a.ea->exp + a.eb->exp;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int32_t m = m0 + 8 * (v >> 2) + 4 * half + (v & 3);
+    if (c < a.C && m < a.K) {
+      const int64_t o = (int64_t)m * a.C + c;
+      if (a.nseg == 1) a.out[o] = ldexpf(sum[v], e);
+      else a.useg[(int64_t)tl.seg * a.O + o] = sum[v];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Band kernel: unit strides, output rows of a multiple of 8, filter width at
 // most 4, chunks of whole 32-index blocks.  Reduction indices then come in
@@ -562,7 +687,6 @@ __device__ __forceinline__ int32_t fresh_lane() {
   return l;
 }
 
-__device__ __forceinline__ int swz(int row, int piece) { return row * 4 + (piece ^ ((row >> 2) & 3)); }
 
 // XB[c][n*Hpad + u][d][Wpad]: d = 0 lo digits, d = 1 hi digits of
 // x[n][c][u - ph][v - pw], zero outside; rows are row_bytes = 2*Wpad + 16 apart
@@ -1555,7 +1679,8 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     const int32_t Cp = (g.c + 63) / 64 * 64;
     uint8_t* bd = reinterpret_cast<uint8_t*>(xp);
     const int32_t PQ = g.p * g.q;
-    const bool direct = PQ % 16 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
+    // P*Q a multiple of 4: the INT16 tensors are read directly (staged through LDS)
+    const bool direct = PQ % 4 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
                         (reinterpret_cast<uintptr_t>(dy) & 15) == 0;
     if (!direct) {
       const DyPrep dqx{x, bd, g.c, Cp, PQ, (int32_t)p.T, (int32_t)p.KBT};
@@ -1576,7 +1701,9 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.ntx = Cp / 64;
     args.nty = p.Mp / 64;
     const dim3 grid1((unsigned)(p.nseg * args.ntx * args.nty));
-    if (direct) DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_1x1<true>, grid1, dim3(k1x1Threads), 0, st, args, bd, Cp, raw);
+    args.div_q = make_fastdiv((uint32_t)PQ);  // the direct kernels: image of an index
+    if (direct && PQ % 8 == 0) DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_1x1s<8>, grid1, dim3(k1x1Threads), 0, st, args, raw);
+    else if (direct) DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_1x1s<4>, grid1, dim3(k1x1Threads), 0, st, args, raw);
     else DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_1x1<false>, grid1, dim3(k1x1Threads), 0, st, args, bd, Cp, raw);
     if (p.nseg > 1)
       DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 63) / 64)), dim3(64), 0, st, useg, dw,
