@@ -211,6 +211,29 @@ def test_s16_shapes(shape):
     run_all(shape, 64, path=dfp.PATH_MFMA, partials=False)
 
 
+# Forward with fewer than 16 input channels and S*C >= 16 (the 7x7 stem's
+# C = 3): channel-last digit rows, a lane's 16 indices as at most two byte runs
+# merged with byte masks.  S*C = 16 exactly, wide and narrow filters, C = 1,
+# strides 1 and 2, output channels not a multiple of 64 (two row tiles),
+# reductions ending mid-block (odd block counts: a last chunk of one block).
+CL_SHAPES = [
+    (2, 3, 20, 20, 64, 7, 7, 2, 3),
+    (2, 4, 10, 10, 32, 4, 4, 1, 1),
+    (1, 2, 12, 12, 40, 3, 9, 1, 4),
+    (3, 1, 30, 30, 16, 5, 16, 1, 2),
+    (2, 3, 17, 17, 96, 7, 7, 2, 3),
+    (1, 5, 9, 11, 70, 2, 4, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", CL_SHAPES)
+@pytest.mark.parametrize("partials", [True, False])
+def test_few_channel_forward(shape, partials):
+    n, c, h, w, k, r, s, st, pd = shape
+    assert c < 16 and s * c >= 16
+    run_all(shape, 64, partials=partials)
+
+
 @pytest.mark.parametrize("G", [1, 2, 3, 50])
 def test_bwd_wt_segments(G):
     run_all((4, 16, 12, 12, 8, 3, 3, 1, 1), 16, G=G)
