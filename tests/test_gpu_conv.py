@@ -226,6 +226,24 @@ CL_SHAPES = [
 ]
 
 
+# Unit-stride 1x1 layers with many pixels (N*P*Q >= 32768) and short
+# reductions (at most 8 blocks): forward and backward-data read the NCHW
+# activations through LDS (no plane preparation).  Output channels not a
+# multiple of 64, reductions ending mid-block and an odd block count (the
+# last band one block), chunk lengths spanning bands.
+STAGED_1X1_SHAPES = [
+    (8, 64, 64, 64, 96, 1, 1, 1, 0),
+    (4, 200, 96, 96, 40, 1, 1, 1, 0),
+]
+
+
+@pytest.mark.parametrize("shape", STAGED_1X1_SHAPES)
+@pytest.mark.parametrize("L", [64, 32, 96])
+@pytest.mark.parametrize("partials", [True, False])
+def test_1x1_staged(shape, L, partials):
+    run_all(shape, L, partials=partials)
+
+
 @pytest.mark.parametrize("shape", CL_SHAPES)
 @pytest.mark.parametrize("partials", [True, False])
 def test_few_channel_forward(shape, partials):
