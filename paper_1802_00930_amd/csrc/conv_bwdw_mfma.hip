@@ -1190,6 +1190,10 @@ __device__ __forceinline__ v4i rsrc_words(const void* p, uint32_t bytes) {
 
 constexpr int kThreadsW8 = 512;
 constexpr int kBandBufBytes = kBandLdsBytes / 2;
+// Buffers of the one-workgroup-per-CU build of the eight-wave kernel (wide
+// input rows): the second buffer's operand reads still take 16-bit immediate
+// offsets (kBandBufBigBytes + 3 * 4096 + 15 < 65536).
+constexpr int kBandBufBigBytes = 51 * 1024;
 
 template <int N>
 using IC = std::integral_constant<int, N>;
@@ -1231,16 +1235,19 @@ struct BandRaw<4> {
 // distance from its lo-digit window; 0 = any width).  RUN: reduction indices
 // per run, consecutive output columns of one output row (8 when the output
 // width is a multiple of 8, else 4 for widths that are multiples of 4, such
-// as 28); a lane's 16 indices of a block are 16 / RUN runs.
-template <bool PARTIALS, int WPAD, int RUN = 8>
+// as 28); a lane's 16 indices of a block are 16 / RUN runs.  BUFB: bytes per
+// band buffer (kBandBufBytes, two workgroups per CU, or kBandBufBigBytes for
+// layers whose band needs more, one workgroup per CU: VGG-16's 224-wide rows).
+template <bool PARTIALS, int WPAD, int RUN = 8, int BUFB = kBandBufBytes>
 __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(BwdwArgs a) {
   static_assert(RUN == 8 || RUN == 4, "runs of 8 or 4 indices");
+  static_assert(BUFB + 3 * 4096 + 15 < 65536, "LDS read offsets are 16-bit immediates");
   const BwdwTile tl = bwdw_tile(a);
   if (tl.seg >= a.nseg) return;
   // output scale exponent, read before any copy is in flight (the compiler
   // would otherwise wait for a load still pending, and with it the copies)
   const int32_t e = __builtin_amdgcn_readfirstlane(a.ea->exp + a.eb->exp);
-  __shared__ __align__(16) uint8_t sb[2][kBandBufBytes];
+  __shared__ __align__(16) uint8_t sb[2][BUFB];
   // byte offset from sb[0] of each of a band's kSBT / RUN runs, per buffer
   __shared__ __align__(16) int32_t ro[2][kSBT / RUN];
   const int lane = threadIdx.x & 63;
@@ -1313,7 +1320,7 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
       const int32_t dp = (int32_t)fdiv((uint32_t)p, a.div_p);
       n += dp;
       p -= dp * a.P;
-      ro[buf_i][tid] = buf_i * kBandBufBytes + kBandABytes + (n * a.Hpad + p - za) * row_b + q;
+      ro[buf_i][tid] = buf_i * BUFB + kBandABytes + (n * a.Hpad + p - za) * row_b + q;
     }
   };
 
@@ -1342,8 +1349,8 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
     constexpr int BUF = decltype(bufc)::value, K = decltype(kc)::value;
     if constexpr (RUN == 8) {
       const int2 o = *reinterpret_cast<const int2*>(&ro[BUF][4 * K + 2 * half]);
-      lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.ah, rd_a0);
-      lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.al, rd_a1);
+      lds_rd128_at<BUF * BUFB + K * 4096>(r.ah, rd_a0);
+      lds_rd128_at<BUF * BUFB + K * 4096>(r.al, rd_a1);
       const uint32_t w0 = lane_b + (uint32_t)o.x, w1 = lane_b + (uint32_t)o.y;
       lds_rd2x64_at<0>(r.wl0, w0);
       lds_rd2x64_at<0>(r.wl1, w1);
@@ -1356,8 +1363,8 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
       }
     } else {
       const v4i o = *reinterpret_cast<const v4i*>(&ro[BUF][8 * K + 4 * half]);
-      lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.ah, rd_a0);
-      lds_rd128_at<BUF * kBandBufBytes + K * 4096>(r.al, rd_a1);
+      lds_rd128_at<BUF * BUFB + K * 4096>(r.ah, rd_a0);
+      lds_rd128_at<BUF * BUFB + K * 4096>(r.al, rd_a1);
       const uint32_t w0 = lane_b + (uint32_t)o.x, w1 = lane_b + (uint32_t)o.y;
       const uint32_t w2 = lane_b + (uint32_t)o.z, w3 = lane_b + (uint32_t)o.w;
       lds_rd2x32_at<0>(r.wl0, w0);
@@ -1522,7 +1529,7 @@ dim3 bwdw_grid(BwdwArgs& args, const BwdwPlan& p) {
 #define DFP_ASM_UNSAFE_BAND_PARTIALS 0
 #endif
 struct BandKernelsSafe {
-  bool w8, w8_t, skew_t, skew_f, band_t, band_f, w8_r4;
+  bool w8, w8_t, skew_t, skew_f, band_t, band_f, w8_r4, w8_big;
 };
 static const BandKernelsSafe& band_kernels_safe() {
   static const BandKernelsSafe safe{
@@ -1536,7 +1543,10 @@ static const BandKernelsSafe& band_kernels_safe() {
       !DFP_ASM_UNSAFE_BAND_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<true>)),
       !DFP_ASM_UNSAFE_BAND && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<false>)),
       !DFP_ASM_UNSAFE_BAND_W8 && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 0, 4>)) &&
-          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 32, 4>))};
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 32, 4>)),
+      !DFP_ASM_UNSAFE_BAND_W8 &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 0, 8, kBandBufBigBytes>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 232, 8, kBandBufBigBytes>))};
   return safe;
 }
 
@@ -1628,9 +1638,10 @@ BwdwPlan plan_bwdw_mfma(const Geom& g) {
 // kernels' conditions.
 struct BandLayout {
   int32_t row_bytes, ch_stride, buf_bytes, run;
+  bool big;  // buffers beyond two workgroups' share of LDS: the eight-wave kernel's one-workgroup build only
 };
 static BandLayout band_layout(const Geom& g, const BwdwPlan& p) {
-  BandLayout bl{0, 0, 0, 0};
+  BandLayout bl{0, 0, 0, 0, false};
   const int32_t run = (g.q % 8) == 0 && (g.w % 8) == 0 ? 8 : (g.q % 4) == 0 && (g.w % 4) == 0 ? 4 : 0;
   if (run == 0 || g.sh != 1 || g.sw != 1 || g.s > 4 || g.pw >= 4 || (g.L % 32) != 0 || (p.T % 32) != 0 ||
       p.T >= (1ll << 31))
@@ -1641,7 +1652,8 @@ static BandLayout band_layout(const Geom& g, const BwdwPlan& p) {
   int64_t chs = (int64_t)p.rows_max * bl.row_bytes;
   chs += (64 - chs % 256 + 256) % 256;
   const int64_t buf = kBandABytes + p.nch_max * chs;
-  if (2 * buf > kBandLdsBytes) return bl;
+  if (buf > kBandBufBigBytes) return bl;
+  bl.big = 2 * buf > kBandLdsBytes;
   bl.ch_stride = (int32_t)chs;
   bl.buf_bytes = (int32_t)buf;
   bl.run = run;
@@ -1714,10 +1726,11 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   // the band kernels address both digit tensors with 32-bit buffer offsets
   const BandKernelsSafe& safe = band_kernels_safe();
   const bool l64 = g.L == 64 && (p.T % 64) == 0;  // every segment a whole number of two-block chunks
-  // runs of 4: the eight-wave kernel only (L = 64, no partials)
-  const bool band_ok = bl.run == 8 ? (l64 ? (partials ? safe.skew_t : (safe.w8 || safe.skew_f))
-                                          : (partials ? safe.band_t : safe.band_f))
-                                   : (l64 && !partials && safe.w8_r4);
+  // runs of 4 and big buffers: the eight-wave kernel only (L = 64, no partials)
+  const bool band_ok = bl.big ? (bl.run == 8 && l64 && !partials && safe.w8_big)
+                       : bl.run == 8 ? (l64 ? (partials ? safe.skew_t : (safe.w8 || safe.skew_f))
+                                            : (partials ? safe.band_t : safe.band_f))
+                                     : (l64 && !partials && safe.w8_r4);
   if (band_ok && bl.buf_bytes > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 && p.ad_bytes < (1ll << 31) &&
       p.xp_bytes < (1ll << 31)) {
     uint8_t* xb = reinterpret_cast<uint8_t*>(xp);  // same workspace region as the pair layout
@@ -1768,7 +1781,11 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.div_p = make_fastdiv((uint32_t)g.p);
     args.xb_bytes = (uint32_t)p.xp_bytes;
     const dim3 grid = bwdw_grid(args, p);
-    if (bl.run == 4) {
+    if (bl.big) {
+      if (p.Wpad == 232)
+        DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 232, 8, kBandBufBigBytes>), grid, dim3(kThreadsW8), 0, st, args);
+      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 0, 8, kBandBufBigBytes>), grid, dim3(kThreadsW8), 0, st, args);
+    } else if (bl.run == 4) {
       if (p.Wpad == 32) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 32, 4>), grid, dim3(kThreadsW8), 0, st, args);
       else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 0, 4>), grid, dim3(kThreadsW8), 0, st, args);
     } else if (l64) {

@@ -140,6 +140,15 @@ def test_bwd_wt_band_no_partials(shape, G):
     run_all(shape, 64, G=G, partials=False)
 
 
+# Rows too wide for two workgroups' band buffers per CU (VGG-16's 224 x 224
+# layers): the eight-wave kernel's one-workgroup-per-CU build, with the padded
+# width 232 as an immediate and with a generic width (168).
+@pytest.mark.parametrize("shape", [(1, 16, 4, 224, 32, 3, 3, 1, 1), (2, 24, 3, 160, 40, 3, 3, 1, 1)])
+@pytest.mark.parametrize("G", [0, 1, 3, 10 ** 6])
+def test_bwd_wt_band_wide_rows(shape, G):
+    run_all(shape, 64, G=G, partials=False)
+
+
 # Output widths that are multiples of 4 but not of 8 (ResNet-50's 28 x 28
 # layers): without partials at L = 64 the eight-wave band kernel reads runs of
 # 4 indices (8-byte windows); Q = 4 (one run per row), two 64-row dy tiles,
