@@ -31,6 +31,8 @@ struct BwdwArgs {
   int32_t ntx, nty;  // column tiles and row tiles per segment (the grid is 1-D, see bwdw_grid)
   uint32_t ad_bytes, xb_bytes;  // sizes of the two digit tensors (band kernels: buffer bounds)
   FastDiv div_q, div_p;         // division by Q and by P (band-table positions)
+  int32_t flat_plane;           // flat-band kernel: bytes per digit plane of the t-ordered input
+  uint32_t flat_tab;            // flat-band kernel: byte offset of the selector table after the planes
 };
 
 BwdwPlan plan_bwdw_mfma(const Geom& g);

@@ -1468,6 +1468,270 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
   }
 }
 
+// ---------------------------------------------------------------------------
+// Flat-band kernel: 3x3 filters, unit stride and one pixel of padding, on
+// images narrower than 16 (ResNet-50's 14 x 14 and 7 x 7 layers), whose output
+// rows are too short for runs of 4 or 8.  There H = P and W = Q, so the input
+// pixel that column (c, r, s) pairs with reduction index t = (n*P + p)*Q + q,
+// x[n][c][p + r - 1][q + s - 1], sits at index t + delta(r, s) of channel c's
+// pixels laid out in t order (delta = (r - 1)*W + s - 1), unless p + r - 1 or
+// q + s - 1 falls outside the image, where the product must vanish (the index
+// t + delta then lands on a neighbouring row or image).  A lane therefore
+// reads its 16 indices of a block as one window at a fixed distance from the
+// band start, and zeroes the bytes of invalid pairs: v_perm_b32 does both per
+// dword, with selector byte a + k for byte k of a valid index (a = the
+// window's byte misalignment, fixed per (r, s)) and 12 (the constant 0)
+// otherwise.  The selectors depend only on t and (r, s): the preparation pass
+// writes them for every group of 64 indices, TAB[t / 64][r*3 + s][4 pieces of
+// 16 indices][4 dwords], and each band copies its two groups beside the
+// operands.  The input is prepared as byte planes in t order,
+// XF[c][d][16 + t] (d = 0 lo digits, 1 hi digits; 16 zero bytes before t = 0
+// and zeros past T); a band of 128 indices copies bytes t_b0 .. t_b0 + 175 of
+// each plane (from 16 indices before the band to 32 after it).  The dy
+// digits, the workgroup tiles, the band double buffer and the chunk / segment
+// order are those of the eight-wave kernel above.
+constexpr int kFlatHalo = 16;                                   // plane bytes before t = 0
+constexpr int kFlatRS = 9;                                      // 3 x 3 filters
+constexpr int kFlatPlane = kFlatHalo + kSBT + 32;               // band bytes per digit plane
+constexpr int kFlatChStride = 2 * kFlatPlane;                   // both planes of a channel
+constexpr int kFlatNch = (kNT - 1) / kFlatRS + 2;               // channels a column tile touches (16)
+constexpr int kFlatXBytes = kFlatNch * kFlatChStride;           // 5632
+constexpr int kFlatTabBytes = 2 * kFlatRS * 64;                 // selectors of the band's two groups
+constexpr int kFlatBufBytes = kBandABytes + kFlatXBytes + kFlatTabBytes;
+static_assert(kFlatChStride % 16 == 0 && kFlatBufBytes % 16 == 0, "16-byte copy pieces");
+static_assert(kFlatNch * kFlatChStride / 16 <= 6 * 64 && kFlatTabBytes / 16 <= 2 * 64,
+              "six waves copy the planes, two the selectors");
+
+// The preparation pass: workgroups [0, nbx) write XF, [nbx, nbx + nbt) the
+// selector table, the rest the dy digits.
+struct FlatPrep {
+  const int16_t* x;
+  uint8_t* xf;
+  int32_t C, P, Q, PQ, T, plane, ngroups;
+  uint32_t tab;
+};
+__global__ __launch_bounds__(256) void k_prep_flat(FlatPrep f, DyPrep q, int32_t nbx, int32_t nbt) {
+  const int32_t b = blockIdx.x;
+  if (b >= nbx + nbt) {
+    prep_dy_item(q, (b - nbx - nbt) * 256 + threadIdx.x);
+    return;
+  }
+  if (b >= nbx) {  // one thread per selector dword (group, r*3 + s, piece, dword)
+    const int32_t i = (b - nbx) * 256 + threadIdx.x;
+    if (i >= f.ngroups * kFlatRS * 16) return;
+    const int32_t gi = i / (kFlatRS * 16), rem = i - gi * (kFlatRS * 16);
+    const int32_t rsv = rem >> 4, r = rsv / 3, s = rsv - 3 * r;
+    const uint32_t a = (uint32_t)(kFlatHalo + (r - 1) * f.Q + (s - 1)) & 3u;
+    const int32_t t0 = gi * 64 + (rem & 15) * 4;
+    uint32_t sel = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int32_t t = t0 + k;
+      bool valid = false;
+      if (t < f.T) {
+        const int32_t n = t / f.PQ, pq = t - n * f.PQ;
+        const int32_t p = pq / f.Q, qq = pq - p * f.Q;
+        valid = (uint32_t)(p + r - 1) < (uint32_t)f.P && (uint32_t)(qq + s - 1) < (uint32_t)f.Q;
+      }
+      sel |= (valid ? a + (uint32_t)k : 12u) << (8 * k);
+    }
+    reinterpret_cast<uint32_t*>(f.xf + f.tab)[i] = sel;
+    return;
+  }
+  // one thread per 4 bytes of channel c's two planes
+  const int32_t per = f.plane >> 2;
+  const int32_t i = b * 256 + threadIdx.x;
+  if (i >= f.C * per) return;
+  const int32_t c = i / per, u = (i - c * per) * 4;
+  uint32_t lo = 0, hi = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int32_t t = u + k - kFlatHalo;
+    if (t >= 0 && t < f.T) {
+      const int32_t n = t / f.PQ, pq = t - n * f.PQ;
+      const int32_t v = f.x[((int64_t)n * f.C + c) * f.PQ + pq];
+      lo |= lo_digit(v) << (8 * k);
+      hi |= hi_digit(v) << (8 * k);
+    }
+  }
+  uint8_t* row = f.xf + (int64_t)c * 2 * f.plane + u;
+  *reinterpret_cast<uint32_t*>(row) = lo;
+  *reinterpret_cast<uint32_t*>(row + f.plane) = hi;
+}
+
+// Two dwords at independent immediate dword offsets.
+template <int O0, int O1>
+__device__ __forceinline__ void lds_rd2x32_o(v2i& d, uint32_t addr) {
+  asm volatile("ds_read2_b32 %0, %1 offset0:%2 offset1:%3" : "=v"(d) : "v"(addr), "n"(O0), "n"(O1) : "memory");
+}
+
+struct FlatRaw {
+  v4i ah, al;
+  v2i l01, l23, h01, h23, x4;  // lo / hi window dwords 0..3, and dword 4 of both
+  v4i sel;
+};
+
+__global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_flat(BwdwArgs a) {
+  static_assert(kFlatBufBytes + 3 * 4096 + 15 < 65536, "LDS read offsets are 16-bit immediates");
+  const BwdwTile tl = bwdw_tile(a);
+  if (tl.seg >= a.nseg) return;
+  const int32_t e = __builtin_amdgcn_readfirstlane(a.ea->exp + a.eb->exp);
+  __shared__ __align__(16) uint8_t sb[2][kFlatBufBytes];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int rt = wave >> 2;  // row tile
+  const int half = lane >> 5;
+  const int lc = lane & 31;
+  const int32_t CRS = a.C * kFlatRS;
+  const int32_t col0 = tl.tx * kNT;
+  const int32_t col = col0 + (wave & 3) * 32 + lc;
+  const bool cvalid = col < CRS;
+  const int32_t colc = cvalid ? col : col0;
+  const int32_t c = colc / kFlatRS, rs = colc - c * kFlatRS;
+  const int32_t r = rs / 3, s = rs - 3 * r;
+  const int32_t c_lo = col0 / kFlatRS;
+  const int32_t m0 = tl.ty * kMT;
+  const int32_t g = tl.seg;
+  const int32_t seg_len = a.G * a.L;
+  const int32_t Ti = (int32_t)a.T;
+  const int32_t t_seg0 = g * seg_len;
+  const int32_t t_seg1 = min(t_seg0 + seg_len, Ti);
+  const int32_t nbands = (t_seg1 - t_seg0 + kSBT - 1) / kSBT;
+  const int32_t NB = (t_seg1 - t_seg0) / 32;  // blocks of the segment (whole chunks)
+  const int32_t last_kb = t_seg1 / 32 - 1;
+
+  const v4i rs_a = rsrc_words(a.ad, a.ad_bytes);
+  const v4i rs_b = rsrc_words(a.xb, a.xb_bytes);
+  const uint32_t a_block = (uint32_t)a.Mp * 64;
+  auto issue_band = [&](int32_t b, int buf_i) __attribute__((always_inline)) {
+    const int32_t t_b0 = t_seg0 + b * kSBT;
+    uint8_t* dst = sb[buf_i];
+    const int32_t kb0 = t_b0 / 32;
+    const int32_t ln = fresh_lane();
+    const int32_t tid = wave * 64 + ln;
+    const uint32_t a_lane = (uint32_t)((m0 + ((tid >> 2) & 63)) * 64 + (((tid & 3) ^ ((tid >> 4) & 3)) * 16));
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int32_t kb = min(kb0 + 2 * j + (wave >> 2), last_kb);  // blocks past the segment reload a valid one
+      const uint32_t so = __builtin_amdgcn_readfirstlane((uint32_t)kb * a_block);
+      dma16(rs_a, lds_addr(dst + (j * 512 + wave * 64) * 16), a_lane, so);
+    }
+    if (wave < 6) {
+      // plane piece i: channel i / 22, plane (i % 22) / 11, 16-byte piece (i % 22) % 11
+      const int32_t i = tid;
+      if (i < kFlatXBytes / 16) {
+        const int32_t cc = i / (kFlatChStride / 16), pi = i - cc * (kFlatChStride / 16);
+        const int32_t d = pi >= kFlatPlane / 16 ? 1 : 0;
+        const int32_t k = pi - d * (kFlatPlane / 16);
+        const int32_t ch = min(c_lo + cc, a.C - 1);
+        const uint32_t voff = (uint32_t)(ch * 2 + d) * (uint32_t)a.flat_plane + (uint32_t)k * 16;
+        dma16(rs_b, lds_addr(dst + kBandABytes + wave * 1024), voff, __builtin_amdgcn_readfirstlane((uint32_t)t_b0));
+      }
+    } else {
+      const int32_t i = tid - 6 * 64;
+      if (i < kFlatTabBytes / 16)
+        dma16(rs_b, lds_addr(dst + kBandABytes + kFlatXBytes + (wave - 6) * 1024), a.flat_tab + (uint32_t)i * 16,
+              __builtin_amdgcn_readfirstlane((uint32_t)(t_b0 / 64) * (kFlatRS * 64)));
+    }
+  };
+
+  Acc3 acc;
+  float sum[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) sum[v] = 0.f;
+  const int32_t j0 = g * a.G;  // first chunk of the segment
+  const uint32_t base0 = lds_addr(&sb[0][0]);
+  const uint32_t rd_a0 = base0 + (uint32_t)(swz(lc, 2 * half) * 16 + rt * 2048);
+  const uint32_t rd_a1 = base0 + (uint32_t)(swz(lc, 2 * half + 1) * 16 + rt * 2048);
+  // window start: byte kFlatHalo + delta of the lane's 16 indices, rounded down to a dword
+  const uint32_t wofs = (uint32_t)(kFlatHalo + (r - 1) * a.Q + (s - 1)) & ~3u;
+  const uint32_t xw0 = base0 + (uint32_t)(kBandABytes + (c - c_lo) * kFlatChStride + half * 16) + wofs;
+  const uint32_t xw1 = xw0 + kFlatBufBytes;
+  const uint32_t selw = base0 + (uint32_t)(kBandABytes + kFlatXBytes + rs * 64 + half * 16);
+  const int32_t mrow = m0 + 32 * rt + 4 * half;
+
+  // Operand reads are inline-assembly LDS reads with explicit waits one block
+  // after the issue (checked in the generated assembly by asm_check.py, and
+  // the launcher requires a build without scratch).
+  FlatRaw R0, R1;
+  auto read_block = [&](FlatRaw& q, auto bufc, auto kc) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value, K = decltype(kc)::value;
+    lds_rd128_at<BUF * kFlatBufBytes + K * 4096>(q.ah, rd_a0);
+    lds_rd128_at<BUF * kFlatBufBytes + K * 4096>(q.al, rd_a1);
+    const uint32_t xw = BUF ? xw1 : xw0;
+    constexpr int D = K * 8, H = kFlatPlane / 4;  // dword offsets of the block and of the hi plane
+    lds_rd2x32_o<D, D + 1>(q.l01, xw);
+    lds_rd2x32_o<D + 2, D + 3>(q.l23, xw);
+    lds_rd2x32_o<H + D, H + D + 1>(q.h01, xw);
+    lds_rd2x32_o<H + D + 2, H + D + 3>(q.h23, xw);
+    lds_rd2x32_o<D + 4, H + D + 4>(q.x4, xw);
+    lds_rd128_at<BUF * kFlatBufBytes + (K >> 1) * (kFlatRS * 64) + (K & 1) * 32>(q.sel, selw);
+  };
+  auto wait_raw = [&](FlatRaw& q) __attribute__((always_inline)) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(q.ah), "+v"(q.al), "+v"(q.l01), "+v"(q.l23), "+v"(q.h01), "+v"(q.h23), "+v"(q.x4),
+                   "+v"(q.sel)
+                 :
+                 : "memory");
+  };
+  auto pm = [](int hi, int lo, int sel) __attribute__((always_inline)) {
+    return (int)__builtin_amdgcn_perm((uint32_t)hi, (uint32_t)lo, (uint32_t)sel);
+  };
+  auto operand_lo = [&](const FlatRaw& q) __attribute__((always_inline)) {
+    return v4i{pm(q.l01.y, q.l01.x, q.sel.x), pm(q.l23.x, q.l01.y, q.sel.y), pm(q.l23.y, q.l23.x, q.sel.z),
+               pm(q.x4.x, q.l23.y, q.sel.w)};
+  };
+  auto operand_hi = [&](const FlatRaw& q) __attribute__((always_inline)) {
+    return v4i{pm(q.h01.y, q.h01.x, q.sel.x), pm(q.h23.x, q.h01.y, q.sel.y), pm(q.h23.y, q.h23.x, q.sel.z),
+               pm(q.x4.y, q.h23.y, q.sel.w)};
+  };
+  auto do_chunk = [&](auto curc, auto chc, int32_t b, int32_t nch) __attribute__((always_inline)) {
+    constexpr int CUR = decltype(curc)::value, CH = decltype(chc)::value;
+    wait_raw(R0);
+    read_block(R1, IC<CUR>{}, IC<2 * CH + 1>{});
+    mfma_tile(acc, R0.ah, R0.al, operand_hi(R0), operand_lo(R0), true);
+    wait_raw(R1);
+    if (CH + 1 < nch) {
+      read_block(R0, IC<CUR>{}, IC<(2 * CH + 2) & 3>{});
+    } else if (b + 1 < nbands) {
+      wait_vmcnt<0>();
+      __syncthreads();
+      if (b + 2 < nbands) issue_band(b + 2, CUR);
+      read_block(R0, IC<1 - CUR>{}, IC<0>{});
+    }
+    mfma_tile(acc, R1.ah, R1.al, operand_hi(R1), operand_lo(R1), false);
+    flush_tile<false>(acc, sum, j0 + 2 * b + CH, nullptr, a.O, colc, CRS, mrow, a.K, cvalid);
+  };
+  auto do_band = [&](auto curc, int32_t b) __attribute__((always_inline)) {
+    const int32_t nch = min(2, (NB - 4 * b) >> 1);
+    do_chunk(curc, IC<0>{}, b, nch);
+    if (nch > 1) do_chunk(curc, IC<1>{}, b, nch);
+  };
+
+  issue_band(0, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  if (nbands > 1) issue_band(1, 1);
+  read_block(R0, IC<0>{}, IC<0>{});
+  for (int32_t b = 0; b < nbands; b += 2) {
+    do_band(IC<0>{}, b);
+    if (b + 1 < nbands) do_band(IC<1>{}, b + 1);
+  }
+
+  const int32_t ln = fresh_lane();
+  const int32_t ocol = col0 + (wave & 3) * 32 + (ln & 31);
+  const int32_t orow = m0 + 32 * rt + 4 * (ln >> 5);
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int32_t m = orow + 8 * (v >> 2) + (v & 3);
+    if (ocol < CRS && m < a.K) {
+      const int32_t o = m * CRS + ocol;
+      if (a.nseg == 1) a.out[o] = ldexpf(sum[v], e);
+      else a.useg[(int64_t)g * a.O + o] = sum[v];
+    }
+  }
+}
+
 // dW = 2^e * (((U_0 + U_1) + U_2) + ...), segment order.
 __global__ __launch_bounds__(64) void k_seg_reduce(const float* __restrict__ useg, float* __restrict__ out, int64_t O,
                                                   int32_t nseg, const dfp_scale* ea, const dfp_scale* eb) {
@@ -1525,11 +1789,14 @@ dim3 bwdw_grid(BwdwArgs& args, const BwdwPlan& p) {
 #ifndef DFP_ASM_UNSAFE_BAND
 #define DFP_ASM_UNSAFE_BAND 0
 #endif
+#ifndef DFP_ASM_UNSAFE_BAND_FLAT
+#define DFP_ASM_UNSAFE_BAND_FLAT 0
+#endif
 #ifndef DFP_ASM_UNSAFE_BAND_PARTIALS
 #define DFP_ASM_UNSAFE_BAND_PARTIALS 0
 #endif
 struct BandKernelsSafe {
-  bool w8, w8_t, skew_t, skew_f, band_t, band_f, w8_r4, w8_big;
+  bool w8, w8_t, skew_t, skew_f, band_t, band_f, w8_r4, w8_big, flat;
 };
 static const BandKernelsSafe& band_kernels_safe() {
   static const BandKernelsSafe safe{
@@ -1546,7 +1813,8 @@ static const BandKernelsSafe& band_kernels_safe() {
           no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 32, 4>)),
       !DFP_ASM_UNSAFE_BAND_W8 &&
           no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 0, 8, kBandBufBigBytes>)) &&
-          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 232, 8, kBandBufBigBytes>))};
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 232, 8, kBandBufBigBytes>)),
+      !DFP_ASM_UNSAFE_BAND_FLAT && no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat))};
   return safe;
 }
 
@@ -1588,6 +1856,30 @@ __global__ __launch_bounds__(256) void k_subsample(const int16_t* __restrict__ x
 }
 }  // namespace
 
+// Layers the flat-band kernel takes: 3x3 filters with unit stride and one
+// pixel of padding (so H = P and W = Q) on images narrower than 16, chunks of
+// 64 indices and whole chunks only.  Its workspace (in the x-operand region):
+// the planes XF[C][2][plane] and, from byte tab on, the selector table of
+// T / 64 + 2 groups (a band reads the group after its last one).
+struct FlatLayout {
+  int32_t plane, ngroups;
+  int64_t tab, bytes;
+};
+static bool flat_geom(const Geom& g) {
+  const int64_t T = (int64_t)g.n * g.p * g.q;
+  return g.r == 3 && g.s == 3 && g.ph == 1 && g.pw == 1 && g.sh == 1 && g.sw == 1 && g.h == g.p && g.w == g.q &&
+         g.q <= 15 && g.L == 64 && T % 64 == 0 && T + 256 < (1ll << 31);
+}
+static FlatLayout flat_layout(const Geom& g) {
+  const int64_t T = (int64_t)g.n * g.p * g.q;
+  FlatLayout f{};
+  f.plane = (int32_t)((T + 112 + 15) / 16 * 16);  // a band reads plane bytes up to t_b0 + 175 <= T + 111
+  f.ngroups = (int32_t)(T / 64 + 2);
+  f.tab = align256((int64_t)g.c * 2 * f.plane);
+  f.bytes = f.tab + (int64_t)f.ngroups * kFlatRS * 64;
+  return f;
+}
+
 BwdwPlan plan_bwdw_mfma(const Geom& g) {
   if (strided_1x1(g)) {
     BwdwPlan p = plan_bwdw_mfma(subsampled(g));
@@ -1626,6 +1918,7 @@ BwdwPlan plan_bwdw_mfma(const Geom& g) {
   // pair layout [C][N*Hpad][Wpad] u16, or the band kernel's byte planes with 16 spare bytes per row
   p.xp_bytes = align256((int64_t)g.c * g.n * p.Hpad * (2 * p.Wpad + 16));
   if (unit_1x1(g)) p.xp_bytes = std::max<int64_t>(p.xp_bytes, align256(p.KBT * ((g.c + 63) / 64 * 64) * 64));
+  if (flat_geom(g)) p.xp_bytes = std::max<int64_t>(p.xp_bytes, align256(flat_layout(g).bytes));
   p.u_bytes = p.nseg > 1 ? align256((int64_t)p.nseg * g.k * g.c * RS * 4) : 0;
   p.bytes = p.ad_bytes + p.xp_bytes + p.u_bytes;
   return p;
@@ -1725,6 +2018,39 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   const BandLayout bl = band_layout(g, p);
   // the band kernels address both digit tensors with 32-bit buffer offsets
   const BandKernelsSafe& safe = band_kernels_safe();
+  if (bl.buf_bytes == 0 && flat_geom(g) && !partials && safe.flat && p.ad_bytes < (1ll << 31) &&
+      flat_layout(g).bytes < (1ll << 31)) {
+    // rows too short for runs: the flat-band kernel, after one preparation
+    // launch for the t-ordered planes, the selector table and the dy digits
+    const FlatLayout fl = flat_layout(g);
+    uint8_t* xf = reinterpret_cast<uint8_t*>(xp);
+    const FlatPrep f{x, xf, g.c, g.p, g.q, g.p * g.q, (int32_t)p.T, fl.plane, fl.ngroups, (uint32_t)fl.tab};
+    const int32_t nbx = (int32_t)(((int64_t)g.c * (fl.plane / 4) + 255) / 256);
+    const int32_t nbt = (fl.ngroups * kFlatRS * 16 + 255) / 256;
+    DFP_LAUNCH(K_XPREP, k_prep_flat, dim3((unsigned)(nbx + nbt + dy_blocks)), dim3(256), 0, st, f, dq, nbx, nbt);
+    BwdwArgs args{};
+    args.ad = ad;
+    args.xb = xf;
+    args.ea = sx;
+    args.eb = sdy;
+    args.out = dw;
+    args.useg = useg;
+    args.T = p.T;
+    args.O = (int64_t)g.k * g.c * 9;
+    args.K = g.k; args.Mp = p.Mp; args.C = g.c; args.R = 3; args.S = 3;
+    args.P = g.p; args.Q = g.q; args.sh = 1; args.sw = 1;
+    args.L = g.L; args.G = g.G; args.nseg = p.nseg;
+    args.ad_bytes = (uint32_t)p.ad_bytes;
+    args.xb_bytes = (uint32_t)fl.bytes;
+    args.flat_plane = fl.plane;
+    args.flat_tab = (uint32_t)fl.tab;
+    const dim3 grid = bwdw_grid(args, p);
+    DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat, grid, dim3(kThreadsW8), 0, st, args);
+    if (p.nseg > 1)
+      DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 63) / 64)), dim3(64), 0, st, useg, dw,
+                 args.O, p.nseg, sx, sdy);
+    return DFP_OK;
+  }
   const bool l64 = g.L == 64 && (p.T % 64) == 0;  // every segment a whole number of two-block chunks
   // runs of 4 and big buffers: the eight-wave kernel only (L = 64, no partials)
   const bool band_ok = bl.big ? (bl.run == 8 && l64 && !partials && safe.w8_big)

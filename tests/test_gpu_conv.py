@@ -170,6 +170,32 @@ def test_bwd_wt_band_runs_of_4(shape, G):
     run_all(shape, 64, G=G, partials=False)
 
 
+# 3x3 layers with unit stride and one pixel of padding on images narrower
+# than 16 whose output width is not a multiple of 4 (ResNet-50's 14 x 14 and
+# 7 x 7 layers): without partials at L = 64 the flat-band kernel takes the
+# backward-weights (windows over t-ordered input planes, selector-masked at
+# image edges).  Ragged column tiles (C*9 not a multiple of 128), fewer than
+# 16 channels, ragged dy row tiles, one-column images, width 15 (the widest
+# shift), odd widths, and segments of one chunk to the whole reduction.
+FLAT_SHAPES = [
+    (64, 16, 7, 7, 64, 3, 3, 1, 1),
+    (16, 32, 14, 14, 40, 3, 3, 1, 1),
+    (64, 8, 7, 7, 16, 3, 3, 1, 1),
+    (32, 16, 6, 6, 32, 3, 3, 1, 1),
+    (64, 24, 5, 15, 24, 3, 3, 1, 1),
+    (64, 16, 8, 1, 32, 3, 3, 1, 1),
+    (64, 16, 13, 13, 72, 3, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", FLAT_SHAPES)
+@pytest.mark.parametrize("G", [0, 1, 3, 10 ** 6])
+def test_bwd_wt_flat_band(shape, G):
+    n, c, h, w, k, r, s, st, pd = shape
+    assert (w % 4) != 0 and w < 16 and (n * h * w) % 64 == 0
+    run_all(shape, 64, G=G, partials=False)
+
+
 # 32-channel blocks with reductions a multiple of 64 at L = 64: the
 # four-waves-per-SIMD kernel over the plane layout takes the forward (and the
 # backward-data where K is a multiple of 32), across one-chunk reductions
