@@ -41,7 +41,7 @@ SPLIT_READ_KERNELS = {
         "k_bwdw_band_skewILb1E": "DFP_ASM_UNSAFE_BAND_SKEW_PARTIALS",
         "k_bwdw_bandILb0E": "DFP_ASM_UNSAFE_BAND",
         "k_bwdw_bandILb1E": "DFP_ASM_UNSAFE_BAND_PARTIALS",
-        "k_bwdw_flatE": "DFP_ASM_UNSAFE_BAND_FLAT",
+        "k_bwdw_flatILi": "DFP_ASM_UNSAFE_BAND_FLAT",
     },
     "conv_mfma.hip": {
         "k_conv_mfma_persistILb0ELb0E": "DFP_ASM_UNSAFE_PERSIST",

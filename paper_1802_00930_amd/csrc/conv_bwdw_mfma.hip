@@ -1230,15 +1230,15 @@ struct BandRaw<4> {
 // Eight-wave band kernel.  Each band buffer holds the band's dy digits first
 // (kBandABytes) and then its input rows; the run-offset tables hold offsets
 // from the start of the first buffer, so that every operand read is one lane
-// register plus an immediate (WPAD: the padded row width when it is one of
-// the instantiated values, which puts a run's hi-digit window at an immediate
-// distance from its lo-digit window; 0 = any width).  RUN: reduction indices
+// register plus an immediate, and a run's hi-digit window lies Wpad bytes
+// after its lo-digit window.  The flat-band kernel below takes the 3x3
+// same-padding layers; this one the other shapes with runs.  RUN: reduction indices
 // per run, consecutive output columns of one output row (8 when the output
 // width is a multiple of 8, else 4 for widths that are multiples of 4, such
 // as 28); a lane's 16 indices of a block are 16 / RUN runs.  BUFB: bytes per
 // band buffer (kBandBufBytes, two workgroups per CU, or kBandBufBigBytes for
-// layers whose band needs more, one workgroup per CU: VGG-16's 224-wide rows).
-template <bool PARTIALS, int WPAD, int RUN = 8, int BUFB = kBandBufBytes>
+// layers whose band needs more, one workgroup per CU: rows of about 200 and more).
+template <bool PARTIALS, int RUN = 8, int BUFB = kBandBufBytes>
 __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(BwdwArgs a) {
   static_assert(RUN == 8 || RUN == 4, "runs of 8 or 4 indices");
   static_assert(BUFB + 3 * 4096 + 15 < 65536, "LDS read offsets are 16-bit immediates");
@@ -1354,13 +1354,8 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
       const uint32_t w0 = lane_b + (uint32_t)o.x, w1 = lane_b + (uint32_t)o.y;
       lds_rd2x64_at<0>(r.wl0, w0);
       lds_rd2x64_at<0>(r.wl1, w1);
-      if constexpr (WPAD > 0) {
-        lds_rd2x64_at<WPAD / 8>(r.wh0, w0);
-        lds_rd2x64_at<WPAD / 8>(r.wh1, w1);
-      } else {
-        lds_rd2x64_at<0>(r.wh0, w0 + a.Wpad);
-        lds_rd2x64_at<0>(r.wh1, w1 + a.Wpad);
-      }
+      lds_rd2x64_at<0>(r.wh0, w0 + a.Wpad);
+      lds_rd2x64_at<0>(r.wh1, w1 + a.Wpad);
     } else {
       const v4i o = *reinterpret_cast<const v4i*>(&ro[BUF][8 * K + 4 * half]);
       lds_rd128_at<BUF * BUFB + K * 4096>(r.ah, rd_a0);
@@ -1371,17 +1366,10 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
       lds_rd2x32_at<0>(r.wl1, w1);
       lds_rd2x32_at<0>(r.wl2, w2);
       lds_rd2x32_at<0>(r.wl3, w3);
-      if constexpr (WPAD > 0) {
-        lds_rd2x32_at<WPAD / 4>(r.wh0, w0);
-        lds_rd2x32_at<WPAD / 4>(r.wh1, w1);
-        lds_rd2x32_at<WPAD / 4>(r.wh2, w2);
-        lds_rd2x32_at<WPAD / 4>(r.wh3, w3);
-      } else {
-        lds_rd2x32_at<0>(r.wh0, w0 + a.Wpad);
-        lds_rd2x32_at<0>(r.wh1, w1 + a.Wpad);
-        lds_rd2x32_at<0>(r.wh2, w2 + a.Wpad);
-        lds_rd2x32_at<0>(r.wh3, w3 + a.Wpad);
-      }
+      lds_rd2x32_at<0>(r.wh0, w0 + a.Wpad);
+      lds_rd2x32_at<0>(r.wh1, w1 + a.Wpad);
+      lds_rd2x32_at<0>(r.wh2, w2 + a.Wpad);
+      lds_rd2x32_at<0>(r.wh3, w3 + a.Wpad);
     }
   };
   auto wait_raw = [&](Raw& r) __attribute__((always_inline)) {
@@ -1469,46 +1457,49 @@ __global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_band_w8(B
 }
 
 // ---------------------------------------------------------------------------
-// Flat-band kernel: 3x3 filters, unit stride and one pixel of padding, on
-// images narrower than 16 (ResNet-50's 14 x 14 and 7 x 7 layers), whose output
-// rows are too short for runs of 4 or 8.  There H = P and W = Q, so the input
-// pixel that column (c, r, s) pairs with reduction index t = (n*P + p)*Q + q,
-// x[n][c][p + r - 1][q + s - 1], sits at index t + delta(r, s) of channel c's
-// pixels laid out in t order (delta = (r - 1)*W + s - 1), unless p + r - 1 or
-// q + s - 1 falls outside the image, where the product must vanish (the index
-// t + delta then lands on a neighbouring row or image).  A lane therefore
-// reads its 16 indices of a block as one window at a fixed distance from the
-// band start, and zeroes the bytes of invalid pairs: v_perm_b32 does both per
-// dword, with selector byte a + k for byte k of a valid index (a = the
+// Flat-band kernel: 3x3 filters with unit stride and one pixel of padding.
+// There H = P and W = Q, so the input pixel that column (c, r, s) pairs with
+// reduction index t = (n*P + p)*Q + q, x[n][c][p + r - 1][q + s - 1], sits
+// at index t + delta(r, s) of channel c's pixels laid out in t order
+// (delta = (r - 1)*W + s - 1), unless p + r - 1 or q + s - 1 falls outside
+// the image, where the product must vanish (the index t + delta then lands on
+// a neighbouring row or image).  A lane therefore reads its 16 indices of a
+// block as one window at a fixed distance from the band start, whatever the
+// image width, and zeroes the bytes of invalid pairs: v_perm_b32 does both
+// per dword, with selector byte a + k for byte k of a valid index (a = the
 // window's byte misalignment, fixed per (r, s)) and 12 (the constant 0)
-// otherwise.  The selectors depend only on t and (r, s): the preparation pass
-// writes them for every group of 64 indices, TAB[t / 64][r*3 + s][4 pieces of
-// 16 indices][4 dwords], and each band copies its two groups beside the
-// operands.  The input is prepared as byte planes in t order,
-// XF[c][d][16 + t] (d = 0 lo digits, 1 hi digits; 16 zero bytes before t = 0
-// and zeros past T); a band of 128 indices copies bytes t_b0 .. t_b0 + 175 of
-// each plane (from 16 indices before the band to 32 after it).  The dy
-// digits, the workgroup tiles, the band double buffer and the chunk / segment
-// order are those of the eight-wave kernel above.
-constexpr int kFlatHalo = 16;                                   // plane bytes before t = 0
-constexpr int kFlatRS = 9;                                      // 3 x 3 filters
-constexpr int kFlatPlane = kFlatHalo + kSBT + 32;               // band bytes per digit plane
-constexpr int kFlatChStride = 2 * kFlatPlane;                   // both planes of a channel
-constexpr int kFlatNch = (kNT - 1) / kFlatRS + 2;               // channels a column tile touches (16)
-constexpr int kFlatXBytes = kFlatNch * kFlatChStride;           // 5632
-constexpr int kFlatTabBytes = 2 * kFlatRS * 64;                 // selectors of the band's two groups
-constexpr int kFlatBufBytes = kBandABytes + kFlatXBytes + kFlatTabBytes;
-static_assert(kFlatChStride % 16 == 0 && kFlatBufBytes % 16 == 0, "16-byte copy pieces");
-static_assert(kFlatNch * kFlatChStride / 16 <= 6 * 64 && kFlatTabBytes / 16 <= 2 * 64,
-              "six waves copy the planes, two the selectors");
+// otherwise.  The selectors depend only on t and (r, s): the preparation
+// pass writes them for every group of 64 indices, TAB[t / 64][r*3 + s][4
+// pieces of 16 indices][4 dwords], and each band copies its two groups beside
+// the operands.  The input is prepared as byte planes in t order,
+// XF[c][d][HALO + t] (d = 0 lo digits, 1 hi digits; HALO >= W + 1 zero bytes
+// before t = 0 and zeros past T); a band of 128 indices copies plane bytes
+// t_b0 .. t_b0 + kPlane - 1 (from HALO indices before the band to HALO + 16
+// after it).  The dy digits, the workgroup tiles, the band double buffer and
+// the chunk / segment order are those of the eight-wave kernel above.
+constexpr int kFlatRS = 9;                            // 3 x 3 filters
+constexpr int kFlatNch = (kNT - 1) / kFlatRS + 2;     // channels a column tile touches (16)
+constexpr int kFlatTabBytes = 2 * kFlatRS * 64;       // selectors of the band's two groups
+template <int HALO>
+struct FlatGeo {
+  static_assert(HALO % 16 == 0, "16-byte copy pieces");
+  static constexpr int kPlane = 2 * HALO + kSBT + 16;  // band bytes per digit plane
+  static constexpr int kChStride = 2 * kPlane;         // both planes of a channel
+  static constexpr int kXBytes = kFlatNch * kChStride;
+  static constexpr int kBuf = kBandABytes + kXBytes + kFlatTabBytes;
+  static constexpr int kPieces = (kXBytes + kFlatTabBytes) / 16;  // copied per band besides dy
+  static_assert(kBuf + 3 * 4096 + 15 < 65536, "LDS read offsets are 16-bit immediates");
+  static_assert(kPlane / 4 + 3 * 8 + 4 < 256, "ds_read2_b32 dword offsets are 8-bit");
+};
 
 // The preparation pass: workgroups [0, nbx) write XF, [nbx, nbx + nbt) the
 // selector table, the rest the dy digits.
 struct FlatPrep {
   const int16_t* x;
   uint8_t* xf;
-  int32_t C, P, Q, PQ, T, plane, ngroups;
+  int32_t C, P, Q, PQ, T, plane, halo, ngroups;
   uint32_t tab;
+  bool vec8;  // P*Q a multiple of 8 and x 16-byte aligned: 8 plane bytes per thread
 };
 __global__ __launch_bounds__(256) void k_prep_flat(FlatPrep f, DyPrep q, int32_t nbx, int32_t nbt) {
   const int32_t b = blockIdx.x;
@@ -1521,7 +1512,8 @@ __global__ __launch_bounds__(256) void k_prep_flat(FlatPrep f, DyPrep q, int32_t
     if (i >= f.ngroups * kFlatRS * 16) return;
     const int32_t gi = i / (kFlatRS * 16), rem = i - gi * (kFlatRS * 16);
     const int32_t rsv = rem >> 4, r = rsv / 3, s = rsv - 3 * r;
-    const uint32_t a = (uint32_t)(kFlatHalo + (r - 1) * f.Q + (s - 1)) & 3u;
+    // the window's misalignment: HALO is a multiple of 4, so delta mod 4
+    const uint32_t a = (uint32_t)(16 + (r - 1) * f.Q + (s - 1)) & 3u;
     const int32_t t0 = gi * 64 + (rem & 15) * 4;
     uint32_t sel = 0;
 #pragma unroll
@@ -1538,6 +1530,32 @@ __global__ __launch_bounds__(256) void k_prep_flat(FlatPrep f, DyPrep q, int32_t
     reinterpret_cast<uint32_t*>(f.xf + f.tab)[i] = sel;
     return;
   }
+  if (f.vec8) {
+    // one thread per 8 bytes of channel c's two planes: P*Q a multiple of 8
+    // and x 16-byte aligned, so the 8 indices from a multiple of 8 lie in one
+    // image and are one 16-byte load
+    const int32_t per = f.plane >> 3;
+    const int32_t i = b * 256 + threadIdx.x;
+    if (i >= f.C * per) return;
+    const int32_t c = i / per, u = (i - c * per) * 8;
+    const int32_t t = u - f.halo;
+    uint32_t lo[2] = {0u, 0u}, hi[2] = {0u, 0u};
+    if (t >= 0 && t < f.T) {
+      const int32_t n = t / f.PQ, pq = t - n * f.PQ;
+      const uint4 v = *reinterpret_cast<const uint4*>(f.x + ((int64_t)n * f.C + c) * f.PQ + pq);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int32_t a = (int32_t)(int16_t)(w[k >> 1] >> (16 * (k & 1)));
+        lo[k >> 2] |= lo_digit(a) << (8 * (k & 3));
+        hi[k >> 2] |= hi_digit(a) << (8 * (k & 3));
+      }
+    }
+    uint8_t* row = f.xf + (int64_t)c * 2 * f.plane + u;
+    *reinterpret_cast<uint2*>(row) = make_uint2(lo[0], lo[1]);
+    *reinterpret_cast<uint2*>(row + f.plane) = make_uint2(hi[0], hi[1]);
+    return;
+  }
   // one thread per 4 bytes of channel c's two planes
   const int32_t per = f.plane >> 2;
   const int32_t i = b * 256 + threadIdx.x;
@@ -1546,7 +1564,7 @@ __global__ __launch_bounds__(256) void k_prep_flat(FlatPrep f, DyPrep q, int32_t
   uint32_t lo = 0, hi = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const int32_t t = u + k - kFlatHalo;
+    const int32_t t = u + k - f.halo;
     if (t >= 0 && t < f.T) {
       const int32_t n = t / f.PQ, pq = t - n * f.PQ;
       const int32_t v = f.x[((int64_t)n * f.C + c) * f.PQ + pq];
@@ -1571,12 +1589,13 @@ struct FlatRaw {
   v4i sel;
 };
 
+template <int HALO>
 __global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_flat(BwdwArgs a) {
-  static_assert(kFlatBufBytes + 3 * 4096 + 15 < 65536, "LDS read offsets are 16-bit immediates");
+  using F = FlatGeo<HALO>;
   const BwdwTile tl = bwdw_tile(a);
   if (tl.seg >= a.nseg) return;
   const int32_t e = __builtin_amdgcn_readfirstlane(a.ea->exp + a.eb->exp);
-  __shared__ __align__(16) uint8_t sb[2][kFlatBufBytes];
+  __shared__ __align__(16) uint8_t sb[2][F::kBuf];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int rt = wave >> 2;  // row tile
@@ -1616,22 +1635,24 @@ __global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_flat(BwdwArgs a) {
       const uint32_t so = __builtin_amdgcn_readfirstlane((uint32_t)kb * a_block);
       dma16(rs_a, lds_addr(dst + (j * 512 + wave * 64) * 16), a_lane, so);
     }
-    if (wave < 6) {
-      // plane piece i: channel i / 22, plane (i % 22) / 11, 16-byte piece (i % 22) % 11
-      const int32_t i = tid;
-      if (i < kFlatXBytes / 16) {
-        const int32_t cc = i / (kFlatChStride / 16), pi = i - cc * (kFlatChStride / 16);
-        const int32_t d = pi >= kFlatPlane / 16 ? 1 : 0;
-        const int32_t k = pi - d * (kFlatPlane / 16);
-        const int32_t ch = min(c_lo + cc, a.C - 1);
-        const uint32_t voff = (uint32_t)(ch * 2 + d) * (uint32_t)a.flat_plane + (uint32_t)k * 16;
-        dma16(rs_b, lds_addr(dst + kBandABytes + wave * 1024), voff, __builtin_amdgcn_readfirstlane((uint32_t)t_b0));
+    // piece i < kXBytes / 16: channel i / (kChStride / 16), its plane and
+    // 16-byte piece; the pieces after them: the band's selector groups
+#pragma unroll
+    for (int32_t jj = 0; jj * 512 < F::kPieces; ++jj) {
+      const int32_t i = jj * 512 + tid;
+      if (i < F::kPieces) {
+        uint32_t voff;
+        if (i < F::kXBytes / 16) {
+          const int32_t cc = i / (F::kChStride / 16), pi = i - cc * (F::kChStride / 16);
+          const int32_t d = pi >= F::kPlane / 16 ? 1 : 0;
+          const int32_t k = pi - d * (F::kPlane / 16);
+          const int32_t ch = min(c_lo + cc, a.C - 1);
+          voff = (uint32_t)(ch * 2 + d) * (uint32_t)a.flat_plane + (uint32_t)(k * 16 + t_b0);
+        } else {
+          voff = a.flat_tab + (uint32_t)(t_b0 / 64) * (kFlatRS * 64) + (uint32_t)(i - F::kXBytes / 16) * 16;
+        }
+        dma16(rs_b, lds_addr(dst + kBandABytes + (jj * 512 + wave * 64) * 16), voff, 0u);
       }
-    } else {
-      const int32_t i = tid - 6 * 64;
-      if (i < kFlatTabBytes / 16)
-        dma16(rs_b, lds_addr(dst + kBandABytes + kFlatXBytes + (wave - 6) * 1024), a.flat_tab + (uint32_t)i * 16,
-              __builtin_amdgcn_readfirstlane((uint32_t)(t_b0 / 64) * (kFlatRS * 64)));
     }
   };
 
@@ -1643,11 +1664,11 @@ __global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_flat(BwdwArgs a) {
   const uint32_t base0 = lds_addr(&sb[0][0]);
   const uint32_t rd_a0 = base0 + (uint32_t)(swz(lc, 2 * half) * 16 + rt * 2048);
   const uint32_t rd_a1 = base0 + (uint32_t)(swz(lc, 2 * half + 1) * 16 + rt * 2048);
-  // window start: byte kFlatHalo + delta of the lane's 16 indices, rounded down to a dword
-  const uint32_t wofs = (uint32_t)(kFlatHalo + (r - 1) * a.Q + (s - 1)) & ~3u;
-  const uint32_t xw0 = base0 + (uint32_t)(kBandABytes + (c - c_lo) * kFlatChStride + half * 16) + wofs;
-  const uint32_t xw1 = xw0 + kFlatBufBytes;
-  const uint32_t selw = base0 + (uint32_t)(kBandABytes + kFlatXBytes + rs * 64 + half * 16);
+  // window start: byte HALO + delta of the lane's 16 indices, rounded down to a dword
+  const uint32_t wofs = (uint32_t)(HALO + (r - 1) * a.Q + (s - 1)) & ~3u;
+  const uint32_t xw0 = base0 + (uint32_t)(kBandABytes + (c - c_lo) * F::kChStride + half * 16) + wofs;
+  const uint32_t xw1 = xw0 + F::kBuf;
+  const uint32_t selw = base0 + (uint32_t)(kBandABytes + F::kXBytes + rs * 64 + half * 16);
   const int32_t mrow = m0 + 32 * rt + 4 * half;
 
   // Operand reads are inline-assembly LDS reads with explicit waits one block
@@ -1656,16 +1677,16 @@ __global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_flat(BwdwArgs a) {
   FlatRaw R0, R1;
   auto read_block = [&](FlatRaw& q, auto bufc, auto kc) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value, K = decltype(kc)::value;
-    lds_rd128_at<BUF * kFlatBufBytes + K * 4096>(q.ah, rd_a0);
-    lds_rd128_at<BUF * kFlatBufBytes + K * 4096>(q.al, rd_a1);
+    lds_rd128_at<BUF * F::kBuf + K * 4096>(q.ah, rd_a0);
+    lds_rd128_at<BUF * F::kBuf + K * 4096>(q.al, rd_a1);
     const uint32_t xw = BUF ? xw1 : xw0;
-    constexpr int D = K * 8, H = kFlatPlane / 4;  // dword offsets of the block and of the hi plane
+    constexpr int D = K * 8, H = F::kPlane / 4;  // dword offsets of the block and of the hi plane
     lds_rd2x32_o<D, D + 1>(q.l01, xw);
     lds_rd2x32_o<D + 2, D + 3>(q.l23, xw);
     lds_rd2x32_o<H + D, H + D + 1>(q.h01, xw);
     lds_rd2x32_o<H + D + 2, H + D + 3>(q.h23, xw);
     lds_rd2x32_o<D + 4, H + D + 4>(q.x4, xw);
-    lds_rd128_at<BUF * kFlatBufBytes + (K >> 1) * (kFlatRS * 64) + (K & 1) * 32>(q.sel, selw);
+    lds_rd128_at<BUF * F::kBuf + (K >> 1) * (kFlatRS * 64) + (K & 1) * 32>(q.sel, selw);
   };
   auto wait_raw = [&](FlatRaw& q) __attribute__((always_inline)) {
     asm volatile("s_waitcnt lgkmcnt(0)"
@@ -1800,21 +1821,20 @@ struct BandKernelsSafe {
 };
 static const BandKernelsSafe& band_kernels_safe() {
   static const BandKernelsSafe safe{
-      !DFP_ASM_UNSAFE_BAND_W8 && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 0>)) &&
-          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 32>)) &&
-          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 64>)) &&
-          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 232>)),
-      !DFP_ASM_UNSAFE_BAND_W8_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<true, 0>)),
+      !DFP_ASM_UNSAFE_BAND_W8 && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false>)),
+      !DFP_ASM_UNSAFE_BAND_W8_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<true>)),
       !DFP_ASM_UNSAFE_BAND_SKEW_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<true>)),
       !DFP_ASM_UNSAFE_BAND_SKEW && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_skew<false>)),
       !DFP_ASM_UNSAFE_BAND_PARTIALS && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<true>)),
       !DFP_ASM_UNSAFE_BAND && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band<false>)),
-      !DFP_ASM_UNSAFE_BAND_W8 && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 0, 4>)) &&
-          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 32, 4>)),
+      !DFP_ASM_UNSAFE_BAND_W8 && no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 4>)),
       !DFP_ASM_UNSAFE_BAND_W8 &&
-          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 0, 8, kBandBufBigBytes>)) &&
-          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 232, 8, kBandBufBigBytes>)),
-      !DFP_ASM_UNSAFE_BAND_FLAT && no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat))};
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_band_w8<false, 8, kBandBufBigBytes>)),
+      !DFP_ASM_UNSAFE_BAND_FLAT && no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<16>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<32>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<64>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<128>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<240>))};
   return safe;
 }
 
@@ -1857,23 +1877,31 @@ __global__ __launch_bounds__(256) void k_subsample(const int16_t* __restrict__ x
 }  // namespace
 
 // Layers the flat-band kernel takes: 3x3 filters with unit stride and one
-// pixel of padding (so H = P and W = Q) on images narrower than 16, chunks of
-// 64 indices and whole chunks only.  Its workspace (in the x-operand region):
-// the planes XF[C][2][plane] and, from byte tab on, the selector table of
+// pixel of padding (so H = P and W = Q) on images up to 239 wide, chunks of 64
+// indices and whole chunks only.  Its workspace (in the x-operand region): the
+// planes XF[C][2][plane] with halo bytes before t = 0 (the smallest built
+// halo of at least W + 1) and, from byte tab on, the selector table of
 // T / 64 + 2 groups (a band reads the group after its last one).
 struct FlatLayout {
-  int32_t plane, ngroups;
+  int32_t halo, plane, ngroups;
   int64_t tab, bytes;
 };
+static int32_t flat_halo(int32_t w) {
+  for (int32_t h : {16, 32, 64, 128, 240})
+    if (w + 1 <= h) return h;
+  return 0;
+}
 static bool flat_geom(const Geom& g) {
   const int64_t T = (int64_t)g.n * g.p * g.q;
   return g.r == 3 && g.s == 3 && g.ph == 1 && g.pw == 1 && g.sh == 1 && g.sw == 1 && g.h == g.p && g.w == g.q &&
-         g.q <= 15 && g.L == 64 && T % 64 == 0 && T + 256 < (1ll << 31);
+         flat_halo(g.q) > 0 && g.L == 64 && T % 64 == 0 && T + 1024 < (1ll << 31);
 }
 static FlatLayout flat_layout(const Geom& g) {
   const int64_t T = (int64_t)g.n * g.p * g.q;
   FlatLayout f{};
-  f.plane = (int32_t)((T + 112 + 15) / 16 * 16);  // a band reads plane bytes up to t_b0 + 175 <= T + 111
+  f.halo = flat_halo(g.q);
+  // a band starts at t_b0 <= T - 64 and reads plane bytes t_b0 .. t_b0 + 2 halo + 143
+  f.plane = (int32_t)((T - 64 + 2 * f.halo + kSBT + 16 + 15) / 16 * 16);
   f.ngroups = (int32_t)(T / 64 + 2);
   f.tab = align256((int64_t)g.c * 2 * f.plane);
   f.bytes = f.tab + (int64_t)f.ngroups * kFlatRS * 64;
@@ -2018,14 +2046,18 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   const BandLayout bl = band_layout(g, p);
   // the band kernels address both digit tensors with 32-bit buffer offsets
   const BandKernelsSafe& safe = band_kernels_safe();
-  if (bl.buf_bytes == 0 && flat_geom(g) && !partials && safe.flat && p.ad_bytes < (1ll << 31) &&
+  if (flat_geom(g) && !partials && safe.flat && p.ad_bytes < (1ll << 31) &&
       flat_layout(g).bytes < (1ll << 31)) {
-    // rows too short for runs: the flat-band kernel, after one preparation
-    // launch for the t-ordered planes, the selector table and the dy digits
+    // 3x3 same-padding layers: the flat-band kernel (also where the band
+    // kernels' runs apply: it takes no per-band run table and reads every
+    // operand at an immediate offset), after one preparation launch for the
+    // t-ordered planes, the selector table and the dy digits
     const FlatLayout fl = flat_layout(g);
     uint8_t* xf = reinterpret_cast<uint8_t*>(xp);
-    const FlatPrep f{x, xf, g.c, g.p, g.q, g.p * g.q, (int32_t)p.T, fl.plane, fl.ngroups, (uint32_t)fl.tab};
-    const int32_t nbx = (int32_t)(((int64_t)g.c * (fl.plane / 4) + 255) / 256);
+    const bool vec8 = (g.p * g.q) % 8 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0;
+    const FlatPrep f{x, xf, g.c, g.p, g.q, g.p * g.q, (int32_t)p.T, fl.plane, fl.halo, fl.ngroups, (uint32_t)fl.tab,
+                     vec8};
+    const int32_t nbx = (int32_t)(((int64_t)g.c * (fl.plane / (vec8 ? 8 : 4)) + 255) / 256);
     const int32_t nbt = (fl.ngroups * kFlatRS * 16 + 255) / 256;
     DFP_LAUNCH(K_XPREP, k_prep_flat, dim3((unsigned)(nbx + nbt + dy_blocks)), dim3(256), 0, st, f, dq, nbx, nbt);
     BwdwArgs args{};
@@ -2045,7 +2077,13 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.flat_plane = fl.plane;
     args.flat_tab = (uint32_t)fl.tab;
     const dim3 grid = bwdw_grid(args, p);
-    DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat, grid, dim3(kThreadsW8), 0, st, args);
+    switch (fl.halo) {
+      case 16: DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat<16>, grid, dim3(kThreadsW8), 0, st, args); break;
+      case 32: DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat<32>, grid, dim3(kThreadsW8), 0, st, args); break;
+      case 64: DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat<64>, grid, dim3(kThreadsW8), 0, st, args); break;
+      case 128: DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat<128>, grid, dim3(kThreadsW8), 0, st, args); break;
+      default: DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat<240>, grid, dim3(kThreadsW8), 0, st, args); break;
+    }
     if (p.nseg > 1)
       DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 63) / 64)), dim3(64), 0, st, useg, dw,
                  args.O, p.nseg, sx, sdy);
@@ -2108,26 +2146,16 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.xb_bytes = (uint32_t)p.xp_bytes;
     const dim3 grid = bwdw_grid(args, p);
     if (bl.big) {
-      if (p.Wpad == 232)
-        DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 232, 8, kBandBufBigBytes>), grid, dim3(kThreadsW8), 0, st, args);
-      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 0, 8, kBandBufBigBytes>), grid, dim3(kThreadsW8), 0, st, args);
+      DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 8, kBandBufBigBytes>), grid, dim3(kThreadsW8), 0, st, args);
     } else if (bl.run == 4) {
-      if (p.Wpad == 32) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 32, 4>), grid, dim3(kThreadsW8), 0, st, args);
-      else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 0, 4>), grid, dim3(kThreadsW8), 0, st, args);
+      DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 4>), grid, dim3(kThreadsW8), 0, st, args);
     } else if (l64) {
       // partials: the eight-wave kernel built for two waves per SIMD (its
       // partial stores need more than 128 VGPRs), else the two-tile kernel
       // (same chunks, same order of additions)
-      if (partials && safe.w8_t) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<true, 0>), grid, dim3(kThreadsW8), 0, st, args);
+      if (partials && safe.w8_t) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<true>), grid, dim3(kThreadsW8), 0, st, args);
       else if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<true>), grid, dim3(kThreads), 0, st, args);
-      // padded row widths of ResNet-50 56 x 56 and 28 x 28 and VGG-16 224 x 224 layers as immediates
-      else if (safe.w8 && p.Wpad == 64)
-        DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 64>), grid, dim3(kThreadsW8), 0, st, args);
-      else if (safe.w8 && p.Wpad == 32)
-        DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 32>), grid, dim3(kThreadsW8), 0, st, args);
-      else if (safe.w8 && p.Wpad == 232)
-        DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 232>), grid, dim3(kThreadsW8), 0, st, args);
-      else if (safe.w8) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false, 0>), grid, dim3(kThreadsW8), 0, st, args);
+      else if (safe.w8) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_w8<false>), grid, dim3(kThreadsW8), 0, st, args);
       else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band_skew<false>), grid, dim3(kThreads), 0, st, args);
     } else {
       if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_band<true>), grid, dim3(kThreads), 0, st, args);

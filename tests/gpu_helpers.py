@@ -49,9 +49,9 @@ class GpuLayer:
     """The DFP path of one conv layer on the GPU, all calls through libdfp."""
 
     def __init__(self, n, c, h, w, k, r, s, stride=1, pad=0, L=64, bits=15, rounding="nearest", seed=0,
-                 path=dfp.PATH_AUTO, G=0):
+                 path=dfp.PATH_AUTO, G=0, pad_w=None):
         self.d = dfp.make_desc(n, c, h, w, k, r, s, stride, pad, chunk_len=L, seg_chunks=G, bits=bits,
-                               rounding=rounding, path=path, seed=seed)
+                               rounding=rounding, path=path, seed=seed, pad_w=pad_w)
         self.p, self.q = dfp.output_dims(self.d)
         self.shape_x = (n, c, h, w)
         self.shape_w = (k, c, r, s)

@@ -28,9 +28,11 @@ SHAPES = [
 ]
 
 
-def run_all(shape, L, path=dfp.PATH_AUTO, rounding="nearest", seed=0, G=0, scale=1.0, partials=True, bits=15):
+def run_all(shape, L, path=dfp.PATH_AUTO, rounding="nearest", seed=0, G=0, scale=1.0, partials=True, bits=15,
+            pad_w=None):
     n, c, h, w, k, r, s, st, pd = shape
-    gl = GpuLayer(n, c, h, w, k, r, s, st, pd, L=L, bits=bits, rounding=rounding, seed=seed, path=path, G=G)
+    gl = GpuLayer(n, c, h, w, k, r, s, st, pd, L=L, bits=bits, rounding=rounding, seed=seed, path=path, G=G,
+                  pad_w=pad_w)
     rng = np.random.default_rng(abs(hash((shape, L, seed))) % 2 ** 32)
     x = (rng.standard_normal(gl.shape_x) * scale).astype(np.float32)
     wt = (rng.standard_normal(gl.shape_w) * scale).astype(np.float32)
@@ -131,28 +133,43 @@ def test_bwd_wt_1x1_digit_blocks(shape, L, G):
     run_all(shape, L, G=G, partials=False)
 
 
-# Without partials, L = 64 runs the eight-wave band kernel (with partials the
-# two-tile one): segments of one chunk, of an odd number of chunks (a last band
-# of one chunk), several bands, one segment per layer.
+# Without partials, L = 64 runs the flat-band kernel on the 3x3 shapes here
+# (with partials the eight-wave band kernel): segments of one chunk, of an odd
+# number of chunks (a last band of one chunk), several bands, one segment per
+# layer.
 @pytest.mark.parametrize("shape", BAND_SHAPES + [(2, 64, 56, 56, 64, 3, 3, 1, 1)])
 @pytest.mark.parametrize("G", [0, 1, 3, 5, 10 ** 6])
 def test_bwd_wt_band_no_partials(shape, G):
     run_all(shape, 64, G=G, partials=False)
 
 
-# Rows too wide for two workgroups' band buffers per CU (VGG-16's 224 x 224
-# layers): the eight-wave kernel's one-workgroup-per-CU build, with the padded
-# width 232 as an immediate and with a generic width (168).
-@pytest.mark.parametrize("shape", [(1, 16, 4, 224, 32, 3, 3, 1, 1), (2, 24, 3, 160, 40, 3, 3, 1, 1)])
+# Wide rows: the flat-band kernel's widest planes (VGG-16's 224-wide rows,
+# halo 240) and width 160 (halo 240 too); width 240 runs the eight-wave band
+# kernel's one-workgroup-per-CU build (buffers beyond two workgroups' share of
+# LDS), 256 and 320 the general kernel (a band of 16 channels no longer fits).
+@pytest.mark.parametrize("shape", [(1, 16, 4, 224, 32, 3, 3, 1, 1), (2, 24, 3, 160, 40, 3, 3, 1, 1),
+                                   (1, 16, 4, 240, 32, 3, 3, 1, 1), (1, 16, 4, 256, 32, 3, 3, 1, 1),
+                                   (1, 8, 2, 320, 24, 3, 3, 1, 1)])
 @pytest.mark.parametrize("G", [0, 1, 3, 10 ** 6])
 def test_bwd_wt_band_wide_rows(shape, G):
     run_all(shape, 64, G=G, partials=False)
 
 
+# Shapes with runs that are not 3x3 same-padding layers, without partials at
+# L = 64: the eight-wave band kernel with runs of 8 (output width 16) and of 4
+# (widths 28 and 12), 1x3 filters with column padding only and a 3x1 filter
+# without padding.
+@pytest.mark.parametrize("shape,pad_w", [((2, 16, 8, 16, 32, 1, 3, 1, 0), 1), ((8, 24, 6, 28, 40, 1, 3, 1, 0), 1),
+                                         ((4, 16, 10, 8, 48, 3, 1, 1, 0), 0), ((4, 32, 8, 12, 20, 1, 3, 1, 0), 1)])
+@pytest.mark.parametrize("G", [0, 1, 3, 10 ** 6])
+def test_bwd_wt_band_not_flat(shape, pad_w, G):
+    run_all(shape, 64, G=G, partials=False, pad_w=pad_w)
+
+
 # Output widths that are multiples of 4 but not of 8 (ResNet-50's 28 x 28
-# layers): without partials at L = 64 the eight-wave band kernel reads runs of
-# 4 indices (8-byte windows); Q = 4 (one run per row), two 64-row dy tiles,
-# segments of one chunk to the whole reduction.
+# layers): 3x3 same-padding layers, so without partials at L = 64 the
+# flat-band kernel; Q = 4, two 64-row dy tiles, segments of one chunk to the
+# whole reduction.
 RUN4_SHAPES = [
     (4, 16, 12, 12, 32, 3, 3, 1, 1),
     (4, 24, 20, 20, 40, 3, 3, 1, 1),
