@@ -1485,9 +1485,13 @@ struct FlatGeo {
   static_assert(HALO % 16 == 0, "16-byte copy pieces");
   static constexpr int kPlane = 2 * HALO + kSBT + 16;  // band bytes per digit plane
   static constexpr int kChStride = 2 * kPlane;         // both planes of a channel
-  static constexpr int kXBytes = kFlatNch * kChStride;
+  // the planes' copy in wave instructions of 64 pieces (1 KiB); the last one
+  // partly fills padding, so that the selector groups start on an instruction
+  static constexpr int kXInstr = (kFlatNch * kChStride / 16 + 63) / 64;
+  static constexpr int kXBytes = kXInstr * 1024;
+  static constexpr int kInstr = kXInstr + 2;  // + the selector groups (64 + 8 pieces)
+  static constexpr int kPerWave = (kInstr + 7) / 8;
   static constexpr int kBuf = kBandABytes + kXBytes + kFlatTabBytes;
-  static constexpr int kPieces = (kXBytes + kFlatTabBytes) / 16;  // copied per band besides dy
   static_assert(kBuf + 3 * 4096 + 15 < 65536, "LDS read offsets are 16-bit immediates");
   static_assert(kPlane / 4 + 3 * 8 + 4 < 256, "ds_read2_b32 dword offsets are 8-bit");
 };
@@ -1622,37 +1626,52 @@ __global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_flat(BwdwArgs a) {
   const v4i rs_a = rsrc_words(a.ad, a.ad_bytes);
   const v4i rs_b = rsrc_words(a.xb, a.xb_bytes);
   const uint32_t a_block = (uint32_t)a.Mp * 64;
+  // Per-lane source offsets of the band copies, the same for every band (the
+  // band start goes into the uniform offset).  A slot j*512 + tid of the dy
+  // region holds piece (tid & 3) ^ ((tid >> 4) & 3) of row (tid >> 2) & 63 of
+  // band block 2j + (tid >> 8).  Wave w issues the plane / selector copy
+  // instructions w, w + 8, ...: instruction q < kXInstr copies plane pieces
+  // 64q .. 64q + 63 (piece i: channel i / (kChStride / 16), its plane and
+  // 16-byte piece; pieces past the 16 channels reload piece 0 into padding),
+  // the next two the 72 selector pieces of the band's two groups.
+  const uint32_t a_lane =
+      (uint32_t)((m0 + ((threadIdx.x >> 2) & 63)) * 64 + (((threadIdx.x & 3) ^ ((threadIdx.x >> 4) & 3)) * 16));
+  uint32_t vo[F::kPerWave];
+#pragma unroll
+  for (int u = 0; u < F::kPerWave; ++u) {
+    const int32_t q = u * 8 + wave;
+    if (q < F::kXInstr) {
+      int32_t i = q * 64 + lane;
+      if (i >= kFlatNch * F::kChStride / 16) i = 0;
+      const int32_t cc = i / (F::kChStride / 16), pi = i - cc * (F::kChStride / 16);
+      const int32_t d = pi >= F::kPlane / 16 ? 1 : 0;
+      const int32_t k = pi - d * (F::kPlane / 16);
+      const int32_t ch = min(c_lo + cc, a.C - 1);
+      vo[u] = (uint32_t)(ch * 2 + d) * (uint32_t)a.flat_plane + (uint32_t)(k * 16);
+    } else {
+      vo[u] = a.flat_tab + (uint32_t)((q - F::kXInstr) * 64 + lane) * 16;
+    }
+  }
   auto issue_band = [&](int32_t b, int buf_i) __attribute__((always_inline)) {
     const int32_t t_b0 = t_seg0 + b * kSBT;
     uint8_t* dst = sb[buf_i];
     const int32_t kb0 = t_b0 / 32;
-    const int32_t ln = fresh_lane();
-    const int32_t tid = wave * 64 + ln;
-    const uint32_t a_lane = (uint32_t)((m0 + ((tid >> 2) & 63)) * 64 + (((tid & 3) ^ ((tid >> 4) & 3)) * 16));
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int32_t kb = min(kb0 + 2 * j + (wave >> 2), last_kb);  // blocks past the segment reload a valid one
       const uint32_t so = __builtin_amdgcn_readfirstlane((uint32_t)kb * a_block);
       dma16(rs_a, lds_addr(dst + (j * 512 + wave * 64) * 16), a_lane, so);
     }
-    // piece i < kXBytes / 16: channel i / (kChStride / 16), its plane and
-    // 16-byte piece; the pieces after them: the band's selector groups
+    // a band's planes start t_b0 bytes into each plane, its selector groups
+    // (t_b0 / 64) * 576 = 9 * t_b0 bytes into the table
+    const uint32_t so_x = __builtin_amdgcn_readfirstlane((uint32_t)t_b0);
 #pragma unroll
-    for (int32_t jj = 0; jj * 512 < F::kPieces; ++jj) {
-      const int32_t i = jj * 512 + tid;
-      if (i < F::kPieces) {
-        uint32_t voff;
-        if (i < F::kXBytes / 16) {
-          const int32_t cc = i / (F::kChStride / 16), pi = i - cc * (F::kChStride / 16);
-          const int32_t d = pi >= F::kPlane / 16 ? 1 : 0;
-          const int32_t k = pi - d * (F::kPlane / 16);
-          const int32_t ch = min(c_lo + cc, a.C - 1);
-          voff = (uint32_t)(ch * 2 + d) * (uint32_t)a.flat_plane + (uint32_t)(k * 16 + t_b0);
-        } else {
-          voff = a.flat_tab + (uint32_t)(t_b0 / 64) * (kFlatRS * 64) + (uint32_t)(i - F::kXBytes / 16) * 16;
-        }
-        dma16(rs_b, lds_addr(dst + kBandABytes + (jj * 512 + wave * 64) * 16), voff, 0u);
-      }
+    for (int u = 0; u < F::kPerWave; ++u) {
+      const int32_t q = u * 8 + wave;
+      if (q < F::kXInstr)
+        dma16(rs_b, lds_addr(dst + kBandABytes + q * 1024), vo[u], so_x);
+      else if (q < F::kInstr && (q == F::kXInstr || lane < kFlatTabBytes / 16 - 64))
+        dma16(rs_b, lds_addr(dst + kBandABytes + q * 1024), vo[u], so_x * (uint32_t)kFlatRS);
     }
   };
 
@@ -1739,16 +1758,30 @@ __global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_flat(BwdwArgs a) {
     if (b + 1 < nbands) do_band(IC<1>{}, b + 1);
   }
 
+  // Stores: a 64-bit base per workgroup, the lane's column and half in the
+  // vector offset and each value's row in the uniform one (whole 64-row
+  // tiles); the ragged last tile checks its rows.
   const int32_t ln = fresh_lane();
   const int32_t ocol = col0 + (wave & 3) * 32 + (ln & 31);
   const int32_t orow = m0 + 32 * rt + 4 * (ln >> 5);
+  if (ocol < CRS) {
+    float* dst = a.nseg == 1 ? a.out : a.useg + (int64_t)g * a.O;
+    if (m0 + kMT <= a.K) {
+      const __amdgpu_buffer_rsrc_t rs_o = make_rsrc(dst, (uint32_t)a.O * 4u);
+      const uint32_t lane_off = (uint32_t)(4 * (ln >> 5) * CRS + ocol) * 4u;
+      const uint32_t row0 = (uint32_t)(m0 + 32 * rt);
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int32_t m = orow + 8 * (v >> 2) + (v & 3);
-    if (ocol < CRS && m < a.K) {
-      const int32_t o = m * CRS + ocol;
-      if (a.nseg == 1) a.out[o] = ldexpf(sum[v], e);
-      else a.useg[(int64_t)g * a.O + o] = sum[v];
+      for (int v = 0; v < 16; ++v) {
+        const float y = a.nseg == 1 ? ldexpf(sum[v], e) : sum[v];
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(y), rs_o, lane_off,
+                                              (row0 + (uint32_t)(8 * (v >> 2) + (v & 3))) * (uint32_t)CRS * 4u, 0);
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int32_t m = orow + 8 * (v >> 2) + (v & 3);
+        if (m < a.K) dst[m * CRS + ocol] = a.nseg == 1 ? ldexpf(sum[v], e) : sum[v];
+      }
     }
   }
 }
@@ -2047,7 +2080,7 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   // the band kernels address both digit tensors with 32-bit buffer offsets
   const BandKernelsSafe& safe = band_kernels_safe();
   if (flat_geom(g) && !partials && safe.flat && p.ad_bytes < (1ll << 31) &&
-      flat_layout(g).bytes < (1ll << 31)) {
+      flat_layout(g).bytes < (1ll << 31) && (int64_t)g.k * g.c * 9 * 4 < (1ll << 32)) {
     // 3x3 same-padding layers: the flat-band kernel (also where the band
     // kernels' runs apply: it takes no per-band run table and reads every
     // operand at an immediate offset), after one preparation launch for the
