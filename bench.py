@@ -66,20 +66,29 @@ def parse():
 
 
 def measured_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE /
-    WRITE_SIZE passes (calibrated on a plain copy), or None when they were taken
-    on another kernel or on a source that has changed since."""
+    """HBM bytes per launch of `kernel` (one of the three convolution
+    directions) from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE passes
+    (calibrated on a plain copy), or None when none was taken on that kernel
+    or its source has changed since."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "traffic_conv2x_3x3.json")
     try:
-        rec = json.load(open(path))
-        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+        recs = json.load(open(path))["records"]
     except (OSError, ValueError, KeyError):
         return None
-    if rec.get("kernel") != kernel or hashlib.sha256(src).hexdigest() != rec.get("source_sha256"):
-        return None
-    return {"bytes": int(rec["fetch_bytes"] + rec["write_bytes"]), "fetch_bytes": int(rec["fetch_bytes"]),
-            "write_bytes": int(rec["write_bytes"]), "source": rec.get("summary")}
+    for rec in recs:
+        if rec.get("kernel") != kernel:
+            continue
+        try:
+            src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+        except (OSError, KeyError):
+            return None
+        if hashlib.sha256(src).hexdigest() != rec.get("source_sha256"):
+            return None
+        return {"bytes": int(rec["fetch_bytes"] + rec["write_bytes"]), "fetch_bytes": int(rec["fetch_bytes"]),
+                "write_bytes": int(rec["write_bytes"]), "device_kernel": rec.get("device_kernel"),
+                "source": rec.get("summary")}
+    return None
 
 
 def copy_probe(nbytes):
