@@ -357,6 +357,65 @@ __global__ __launch_bounds__(256) void k_prep_plane_direct(const int16_t* __rest
   }
 }
 
+// The same plane layout from pairs of source columns (no dilation, an even
+// source width, the source 4-byte aligned): a thread loads columns 2i, 2i + 1
+// of its 16 channels as one dword each (a wave's load covers 256 contiguous
+// bytes of a source row instead of 128) and writes output pixels 2i + left
+// and 2i + 1 + left; the remaining threads of a row write its padding columns.
+__global__ __launch_bounds__(256) void k_prep_plane_pair(const int16_t* __restrict__ src, uint8_t* __restrict__ xs,
+                                                        int32_t Cs, int32_t Hs, int32_t Wsrc, int32_t Hp, int32_t Wp,
+                                                        int32_t CG, int32_t top, int32_t left, PrepAArgs pa,
+                                                        int32_t with_a) {
+  const int32_t nwg = gridDim.x * gridDim.y, id = blockIdx.y * gridDim.x + blockIdx.x;
+  const int32_t xcd = id & 7, per_x = nwg >> 3, rem = nwg & 7;
+  const int32_t l = xcd * per_x + min(xcd, rem) + (id >> 3);
+  const int32_t n = l / (int32_t)gridDim.x, u = l - n * (int32_t)gridDim.x;
+  if (with_a && n == (int32_t)gridDim.y - 1) {
+    const int32_t nthr = gridDim.x * 256;
+    const int32_t total = max(pa.KB * pa.Mp * 8, pa.KB);
+    for (int32_t idx = u * 256 + threadIdx.x; idx < total; idx += nthr) prep_a_item(pa, idx);
+    return;
+  }
+  const int32_t h = u - top;
+  const bool row_in = h >= 0 && h < Hs;
+  const int64_t plane = (int64_t)Hs * Wsrc;
+  uint8_t* rowp = xs + ((int64_t)n * Hp + u) * ((int64_t)CG * 32 * Wp);
+  const int32_t npair = Wsrc >> 1, per = npair + (Wp - Wsrc);
+  for (int32_t j = threadIdx.x; j < CG * per; j += 256) {
+    const int32_t cg = j / per, i = j - cg * per;
+    uint4* d = reinterpret_cast<uint4*>(rowp) + ((cg >> 1) * 4 + (cg & 1)) * Wp;
+    if (i < npair) {
+      uint32_t hi0[4] = {0u, 0u, 0u, 0u}, lo0[4] = {0u, 0u, 0u, 0u}, hi1[4] = {0u, 0u, 0u, 0u},
+               lo1[4] = {0u, 0u, 0u, 0u};
+      if (row_in) {
+        const uint32_t* sp = reinterpret_cast<const uint32_t*>(src + ((int64_t)n * Cs + cg * 16) * plane +
+                                                               (int64_t)h * Wsrc + 2 * i);
+        uint32_t wv[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) wv[k] = (cg * 16 + k < Cs) ? sp[k * (plane >> 1)] : 0u;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int32_t a0 = (int32_t)(int16_t)(wv[k] & 0xffffu), a1 = (int32_t)(int16_t)(wv[k] >> 16);
+          hi0[k >> 2] |= hi_digit(a0) << (8 * (k & 3));
+          lo0[k >> 2] |= lo_digit(a0) << (8 * (k & 3));
+          hi1[k >> 2] |= hi_digit(a1) << (8 * (k & 3));
+          lo1[k >> 2] |= lo_digit(a1) << (8 * (k & 3));
+        }
+      }
+      const int32_t v = 2 * i + left;
+      d[v] = make_uint4(hi0[0], hi0[1], hi0[2], hi0[3]);
+      d[v + 1] = make_uint4(hi1[0], hi1[1], hi1[2], hi1[3]);
+      d[2 * Wp + v] = make_uint4(lo0[0], lo0[1], lo0[2], lo0[3]);
+      d[2 * Wp + v + 1] = make_uint4(lo1[0], lo1[1], lo1[2], lo1[3]);
+    } else {  // padding columns: [0, left) and [left + Wsrc, Wp)
+      const int32_t z = i - npair;
+      const int32_t v = z < left ? z : Wsrc + z;
+      d[v] = make_uint4(0u, 0u, 0u, 0u);
+      d[2 * Wp + v] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+}
+
 // Byte mask keeping bytes [lo, hi) of a 16-byte operand (0 <= lo <= hi <= 16).
 __device__ __forceinline__ v4i byte_mask16(int32_t lo, int32_t hi) {
   const uint32_t bits = ((hi >= 16 ? 0xffffu : ((1u << hi) - 1u)) & ~((1u << lo) - 1u)) & 0xffffu;
@@ -2564,8 +2623,12 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
       const dim3 grid((unsigned)((p.Hp + rb - 1) / rb), (unsigned)p.CG, (unsigned)(g.n + (merge_a ? 1 : 0)));
       const size_t plds = (size_t)rb * Wsrc * 16 * 2;
       const int32_t wa = merge_a ? 1 : 0;
-      if (kPlaneDirect) {
-        const dim3 gridd((unsigned)p.Hp, (unsigned)(g.n + (merge_a ? 1 : 0)));
+      const dim3 gridd((unsigned)p.Hp, (unsigned)(g.n + (merge_a ? 1 : 0)));
+      if (kPlaneDirect && p.dil_h == 1 && p.dil_w == 1 && (Wsrc % 2) == 0 &&
+          (reinterpret_cast<uintptr_t>(a) & 3) == 0 && p.left >= 0 && p.left + Wsrc <= p.Wp) {
+        DFP_LAUNCH(K_XPREP, k_prep_plane_pair, gridd, dim3(256), 0, st, a, xs, Cs, Hs, Wsrc, p.Hp, p.Wp, p.CG,
+                   p.top, p.left, pa, wa);
+      } else if (kPlaneDirect) {
         DFP_LAUNCH(K_XPREP, k_prep_plane_direct, gridd, dim3(256), 0, st, a, xs, Cs, Hs, Wsrc, p.Hp, p.Wp, p.CG,
                    p.top, p.left, p.dil_h, p.dil_w, pa, wa);
       } else if (vec)
