@@ -105,8 +105,8 @@ def _partial_tiles(step, direction, a, sa, b, sb, oa, ob, e, L, G, ntiles, seed)
 
 # partial-tile budget per workload (tiles per direction; backward-weights
 # outputs each reduce over N*P*Q products, so fewer of them)
-PARTIAL_TILES = {"layer16x32": (64, 64, 64), "resnet50_conv2x_3x3": (64, 64, 8), "resnet50_conv4x_1x1": (64, 64, 4),
-                 "vgg16_conv1_2_conv3_3": (64, 64, 2), "resnet50_all_convs": (16, 16, 1)}
+PARTIAL_TILES = {"layer16x32": (64, 64, 64), "resnet50_conv2x_3x3": (64, 64, 64), "resnet50_conv4x_1x1": (64, 64, 64),
+                 "vgg16_conv1_2_conv3_3": (64, 64, 4), "resnet50_all_convs": (16, 16, 4)}
 
 
 @pytest.mark.parametrize("key", sorted(DB["cases"]))
