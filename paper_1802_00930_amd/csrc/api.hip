@@ -146,7 +146,8 @@ bool use_mfma(const Geom& g, int32_t path, int32_t bits, int32_t dir) {
 size_t workspace_bytes(const Geom& g, int32_t dir, int32_t path, int32_t bits) {
   if (!use_mfma(g, path, bits, dir)) return 0;
   if (dir == DFP_BWD_DATA)  // room for either route (partials take the general one)
-    return (size_t)std::max<int64_t>(plan_conv_mfma(g, dir).bytes, conv_bwd_data_sub_bytes(g));
+    return (size_t)std::max(std::max<int64_t>(plan_conv_mfma(g, dir).bytes, conv_bwd_data_sub_bytes(g)),
+                            conv_bwd_data_phase_bytes(g));
   if (dir == DFP_FWD) return (size_t)plan_conv_mfma(g, dir).bytes;
   return (size_t)plan_bwdw_mfma(g).bytes;
 }
@@ -278,6 +279,8 @@ static dfp_status conv_common(int32_t dir, const dfp_desc* d, const int16_t* a, 
     if (dir == DFP_BWD_WT) return launch_bwdw_mfma(g, a, sa, b, sb, out, partials, ws, st);
     if (dir == DFP_BWD_DATA && !partials && conv_bwd_data_sub_bytes(g) > 0)
       return launch_conv_bwd_data_sub(g, a, sa, b, sb, out, so, ws, st, d->path == DFP_PATH_MFMA);
+    if (dir == DFP_BWD_DATA && !partials && conv_bwd_data_phase_bytes(g) > 0)
+      return launch_conv_bwd_data_phases(g, a, sa, b, sb, out, so, ws, st, d->path == DFP_PATH_MFMA);
     // the filter prep kernel clears so before the main kernel raises it
     return launch_conv_mfma(dir, g, a, sa, b, sb, out, so, partials, ws, st, false, d->path == DFP_PATH_MFMA);
   }

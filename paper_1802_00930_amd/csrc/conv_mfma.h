@@ -61,10 +61,17 @@ bool conv_mfma_supported(const Geom& g, int32_t dir);
 dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,
                             const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, void* ws,
                             hipStream_t st, bool i32 = false,
-                            bool prefer_w16 = false);
+                            bool prefer_w16 = false, bool so_reset = true);
 // Strided 1x1 backward-data without padding through the unit-stride grid:
 // workspace bytes it needs (0 if the layer does not qualify), and the launch.
 int64_t conv_bwd_data_sub_bytes(const Geom& g);
+// Strided backward-data split by output phase into unit-stride problems over
+// the undilated dy (K a multiple of the chunk length): workspace bytes (0 if
+// the layer does not qualify), and the launch.
+int64_t conv_bwd_data_phase_bytes(const Geom& g);
+dfp_status launch_conv_bwd_data_phases(const Geom& g, const int16_t* dy, const dfp_scale* sdy, const int16_t* w,
+                                       const dfp_scale* sw, float* dx, dfp_scale* so, void* ws, hipStream_t st,
+                                       bool prefer_w16);
 dfp_status launch_conv_bwd_data_sub(const Geom& g, const int16_t* dy, const dfp_scale* sdy, const int16_t* w,
                                     const dfp_scale* sw, float* dx, dfp_scale* so, void* ws, hipStream_t st,
                                     bool prefer_w16);

@@ -2515,7 +2515,7 @@ ConvMfmaPlan plan_conv_mfma(const Geom& g, int32_t dir) {
 
 dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const dfp_scale* sa, const int16_t* b,
                             const dfp_scale* sb, float* out, dfp_scale* so, int32_t* partials, void* ws,
-                            hipStream_t st, bool i32, bool prefer_w16) {
+                            hipStream_t st, bool i32, bool prefer_w16, bool so_reset) {
   // fwd: a = x (B source), b = w.  bwd-data: a = dy (B source), b = w.
   const ConvMfmaPlan p = plan_conv_mfma(g, dir);
   const bool fwd = dir == DFP_FWD;
@@ -2540,7 +2540,9 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
       plane = 2 * ((NP + 31) / 32) >= gx * kWaves16;
     }
   }
-  const PrepAArgs pa{b, wsa, p.M, p.Mp, p.Cin, g.r, g.s, p.T, p.KB, fwd ? 0 : 1, g.c, so, boff,
+  // the filter preparation clears so (unless a previous launch of the same
+  // output has already raised it) before the main kernel raises it
+  const PrepAArgs pa{b, wsa, p.M, p.Mp, p.Cin, g.r, g.s, p.T, p.KB, fwd ? 0 : 1, g.c, so_reset ? so : nullptr, boff,
                      tap_row_bytes, tap_col_bytes};
   // unit-stride 1x1 without padding (forward, or backward-data as the 1x1 of dy
   // with the transposed filter): the activations are read in NCHW through LDS.
@@ -2869,6 +2871,133 @@ dfp_status launch_conv_bwd_data_sub(const Geom& g, const int16_t* dy, const dfp_
   const int64_t gy = std::max<int64_t>(1, std::min<int64_t>(planes, std::max(1, 16384 / gx)));
   DFP_LAUNCH(K_XPREP, k_scatter_strided, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, st, sub, dx, planes, g.h,
              g.w, g.p, g.q, g.sh, g.sw);
+  return DFP_OK;
+}
+
+
+namespace {
+
+// Strided backward-data split by output phase.  A pixel (h, w) of dx with
+// h = alpha + sh*i and w = beta + sw*j receives only the filter taps
+// r = r0 + sh*m, s = s0 + sw*m' with r0 = (alpha + ph) mod sh (s0 likewise),
+// from dy[n][k][i + a0 - m][j + b0 - m'] with a0 = (alpha + ph - r0) / sh
+// (b0 likewise): a unit-stride backward-data over the undilated dy with the
+// sub-filter of those taps (in their canonical order) and padding (a0, b0),
+// whose output is the phase's Ha x Wb grid of pixels.  When K is a multiple
+// of L every chunk of the reduction t = (r*S + s)*K + k lies inside one tap,
+// so the chunks of the other taps, whose products all vanish at these pixels,
+// have partial 0, and leaving them out of the FP32 sum (+0.0 added to a sum
+// that is never -0.0) changes nothing: each phase is bit-identical to the
+// strided sum.  The phases run one after another into the end of the
+// workspace, and each is spread over its pixels of dx.
+struct Phase {
+  Geom g;  // the unit-stride sub-problem (g.h, g.w: the phase grid; g.p, g.q: dy)
+  int32_t alpha, beta, r0, s0;
+  bool empty;  // no tap reaches these pixels (or no pixel has this phase): zeros
+};
+Phase phase_of(const Geom& g, int32_t idx) {
+  Phase f{};
+  f.alpha = idx / g.sw;
+  f.beta = idx - f.alpha * g.sw;
+  f.r0 = (f.alpha + g.ph) % g.sh;
+  f.s0 = (f.beta + g.pw) % g.sw;
+  const int32_t Mr = f.r0 < g.r ? (g.r - f.r0 + g.sh - 1) / g.sh : 0;
+  const int32_t Ms = f.s0 < g.s ? (g.s - f.s0 + g.sw - 1) / g.sw : 0;
+  const int32_t Ha = f.alpha < g.h ? (g.h - f.alpha + g.sh - 1) / g.sh : 0;
+  const int32_t Wb = f.beta < g.w ? (g.w - f.beta + g.sw - 1) / g.sw : 0;
+  f.g = g;
+  f.g.h = Ha;
+  f.g.w = Wb;
+  f.g.r = Mr;
+  f.g.s = Ms;
+  f.g.sh = f.g.sw = 1;
+  f.g.ph = (f.alpha + g.ph - f.r0) / g.sh;
+  f.g.pw = (f.beta + g.pw - f.s0) / g.sw;
+  f.empty = Mr == 0 || Ms == 0 || Ha == 0 || Wb == 0;
+  return f;
+}
+
+// wsub[kc][m][m'] = w[kc][r0 + sh*m][s0 + sw*m'] (kc = k*C + c)
+__global__ __launch_bounds__(256) void k_gather_taps(const int16_t* __restrict__ w, int16_t* __restrict__ wsub,
+                                                    int64_t KC, int32_t R, int32_t S, int32_t r0, int32_t sh,
+                                                    int32_t Mr, int32_t s0, int32_t sw, int32_t Ms) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= KC * Mr * Ms) return;
+  const int64_t kc = i / (Mr * Ms);
+  const int32_t t = (int32_t)(i - kc * (Mr * Ms)), m = t / Ms, mm = t - m * Ms;
+  wsub[i] = w[(kc * R + r0 + sh * m) * S + s0 + sw * mm];
+}
+
+// dx[nc][alpha + sh*i][beta + sw*j] = sub[nc][i][j] (0 where sub is null)
+__global__ __launch_bounds__(256) void k_scatter_phase(const float* __restrict__ sub, float* __restrict__ dx,
+                                                      int64_t planes, int32_t H, int32_t W, int32_t Ha, int32_t Wb,
+                                                      int32_t alpha, int32_t beta, int32_t sh, int32_t sw) {
+  const int32_t ij = blockIdx.x * 256 + threadIdx.x;
+  if (ij >= Ha * Wb) return;
+  const int32_t i = ij / Wb, j = ij - i * Wb;
+  const int64_t o = (int64_t)(alpha + sh * i) * W + beta + sw * j;
+  for (int64_t nc = blockIdx.y; nc < planes; nc += gridDim.y)
+    dx[nc * H * W + o] = sub ? sub[nc * Ha * Wb + ij] : 0.f;
+}
+
+}  // namespace
+
+int64_t conv_bwd_data_phase_bytes(const Geom& g) {
+  if ((g.sh == 1 && g.sw == 1) || g.L < 1 || g.k % g.L != 0 || conv_bwd_data_sub_bytes(g) > 0) return 0;
+  // k_scatter_phase indexes a plane (and sizes its grid) with 32 bits
+  if ((int64_t)g.h * g.w >= (1ll << 31) - 256) return 0;
+  int64_t conv = 0, wsub = 0, out = 0;
+  for (int32_t idx = 0; idx < g.sh * g.sw; ++idx) {
+    const Phase f = phase_of(g, idx);
+    if (f.empty) continue;
+    // every phase on the plane-layout kernels, whose preparation takes any
+    // padding; a 1x1 phase without padding must cover dy exactly (the 1x1
+    // route reads its input with the output's pixel count)
+    if (!conv_mfma_supported(f.g, DFP_BWD_DATA) ||
+        !conv_w16_eligible(g.k, g.k * f.g.r * f.g.s, g.L, false) ||
+        (f.g.r == 1 && f.g.s == 1 && f.g.ph == 0 && f.g.pw == 0 && (f.g.h != g.p || f.g.w != g.q)))
+      return 0;
+    conv = std::max(conv, plan_conv_mfma(f.g, DFP_BWD_DATA).bytes);
+    wsub = std::max(wsub, align256((int64_t)g.k * g.c * f.g.r * f.g.s * 2));
+    out = std::max(out, align256((int64_t)g.n * g.c * f.g.h * f.g.w * 4));
+  }
+  return conv > 0 ? conv + wsub + out : 0;
+}
+
+dfp_status launch_conv_bwd_data_phases(const Geom& g, const int16_t* dy, const dfp_scale* sdy, const int16_t* w,
+                                       const dfp_scale* sw, float* dx, dfp_scale* so, void* ws, hipStream_t st,
+                                       bool prefer_w16) {
+  int64_t conv = 0, wsub_b = 0;
+  for (int32_t idx = 0; idx < g.sh * g.sw; ++idx) {
+    const Phase f = phase_of(g, idx);
+    if (f.empty) continue;
+    conv = std::max(conv, plan_conv_mfma(f.g, DFP_BWD_DATA).bytes);
+    wsub_b = std::max(wsub_b, align256((int64_t)g.k * g.c * f.g.r * f.g.s * 2));
+  }
+  int16_t* wsub = reinterpret_cast<int16_t*>(reinterpret_cast<uint8_t*>(ws) + conv);
+  float* sub = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(ws) + conv + wsub_b);
+  const int64_t planes = (int64_t)g.n * g.c;
+  bool first = true;
+  for (int32_t idx = 0; idx < g.sh * g.sw; ++idx) {
+    const Phase f = phase_of(g, idx);
+    const int32_t Ha = f.alpha < g.h ? (g.h - f.alpha + g.sh - 1) / g.sh : 0;
+    const int32_t Wb = f.beta < g.w ? (g.w - f.beta + g.sw - 1) / g.sw : 0;
+    if (Ha == 0 || Wb == 0) continue;
+    if (!f.empty) {
+      const int64_t n_sub = (int64_t)g.k * g.c * f.g.r * f.g.s;
+      DFP_LAUNCH(K_WPREP, k_gather_taps, dim3((unsigned)((n_sub + 255) / 256)), dim3(256), 0, st, w, wsub,
+                 (int64_t)g.k * g.c, g.r, g.s, f.r0, g.sh, f.g.r, f.s0, g.sw, f.g.s);
+      const dfp_status rc = launch_conv_mfma(DFP_BWD_DATA, f.g, dy, sdy, wsub, sw, sub, so, nullptr, ws, st, false,
+                                             prefer_w16, first);
+      if (rc != DFP_OK) return rc;
+      first = false;
+    }
+    const int32_t gx = (Ha * Wb + 255) / 256;
+    const int64_t gy = std::max<int64_t>(1, std::min<int64_t>(planes, std::max(1, 16384 / gx)));
+    DFP_LAUNCH(K_XPREP, k_scatter_phase, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, st,
+               f.empty ? nullptr : sub, dx, planes, g.h, g.w, Ha, Wb, f.alpha, f.beta, g.sh, g.sw);
+  }
+  if (first && so) return launch_scale_reset(so, st);  // no tap reached any pixel: dx is zero
   return DFP_OK;
 }
 

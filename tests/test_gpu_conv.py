@@ -213,6 +213,29 @@ def test_bwd_wt_flat_band(shape, G):
     run_all(shape, 64, G=G, partials=False)
 
 
+# Strided backward-data without partials at L = 64 with K a multiple of 64:
+# split by output phase into unit-stride problems over the undilated dy (the
+# stem's 7x7 stride 2 on C = 3, odd sizes, 3x3 / 5x5 / 4x4 / 2x2 filters,
+# stride 3, phases whose only tap is a 1x1 without padding, and a 1x3
+# filter whose odd-row phases receive no tap at all).
+PHASE_SHAPES = [
+    (2, 3, 16, 16, 64, 7, 7, 2, 3),
+    (2, 5, 15, 13, 64, 7, 7, 2, 3),
+    (2, 16, 14, 14, 64, 3, 3, 2, 1),
+    (2, 16, 13, 11, 128, 3, 3, 2, 1),
+    (2, 8, 9, 9, 64, 5, 5, 2, 2),
+    (2, 4, 10, 10, 64, 3, 3, 3, 1),
+    (1, 3, 20, 20, 64, 4, 4, 2, 1),
+    (2, 6, 12, 12, 64, 2, 2, 2, 0),
+    (2, 8, 12, 12, 64, 1, 3, 2, 0),
+]
+
+
+@pytest.mark.parametrize("shape", PHASE_SHAPES)
+def test_bwd_data_phases(shape):
+    run_all(shape, 64, partials=False)
+
+
 # 32-channel blocks with reductions a multiple of 64 at L = 64: the
 # four-waves-per-SIMD kernel over the plane layout takes the forward (and the
 # backward-data where K is a multiple of 32), across one-chunk reductions
