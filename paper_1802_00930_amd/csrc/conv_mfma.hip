@@ -1732,7 +1732,10 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   if ((int32_t)threadIdx.x < KB) s_boff[threadIdx.x] = boff_of(kb0 + (int32_t)threadIdx.x);
 
   // ---- this workgroup's unit range (XCD x = workgroup id mod 8 gets adjacent ranges)
-  const int32_t units = 2 * ((NP + 31) / 32);
+  // units (32-pixel tile, 32-row half); a tile whose second half lies past
+  // the output rows (M - m0 <= 32) has only its first half as a unit
+  const int32_t hsh = a.M - m0 > 32 ? 1 : 0;
+  const int32_t units = ((NP + 31) / 32) << hsh;
   const int32_t G = gridDim.x;
   const int32_t xcd = blockIdx.x & 7, per = G >> 3, rem = G & 7;
   const int32_t vb = xcd * per + min(xcd, rem) + (blockIdx.x >> 3);
@@ -1741,7 +1744,7 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   auto unit_of = [&](int32_t i) { return u0 + wave + kWaves16 * i; };
   // byte offset of this lane's operand for the pixel of unit u (block offsets come from s_boff)
   auto pixel_off = [&](int32_t u) -> int32_t {
-    int32_t gp = (u >> 1) * 32 + col;
+    int32_t gp = (u >> hsh) * 32 + col;
     if (gp >= NP) gp = 0;
     const int32_t im = (int32_t)fdiv((uint32_t)gp, a.div_pq), rp = gp - im * PQ;
     const int32_t po = (int32_t)fdiv((uint32_t)rp, a.div_q), qo = rp - po * Qo;
@@ -1788,8 +1791,8 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
     for (int32_t unit = 0; unit < my_units; ++unit) {
       const int32_t u = unit_of(unit);
       const int32_t next_pix = unit + 1 < my_units ? pixel_off(unit_of(unit + 1)) : cur_pix;
-      const int32_t msub = u & 1;
-      const int32_t g = (u >> 1) * 32 + col;
+      const int32_t msub = u & hsh;
+      const int32_t g = (u >> hsh) * 32 + col;
       const bool gvalid = g < NP;
       int32_t obase = 0;
       if (gvalid) {
@@ -1954,7 +1957,10 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_s16(ConvMfmaArgs a)
   if ((int32_t)threadIdx.x < KB) s_boff[threadIdx.x] = boff_of(kb0 + (int32_t)threadIdx.x);
 
   // ---- this workgroup's unit range (XCD x = workgroup id mod 8 gets adjacent ranges)
-  const int32_t units = 2 * ((NP + 15) / 16);
+  // units (16-pixel tile, 16-row subtile); only the first subtile where the
+  // second lies past the output rows (M - m0 <= 16)
+  const int32_t hsh = a.M - m0 > 16 ? 1 : 0;
+  const int32_t units = ((NP + 15) / 16) << hsh;
   const int32_t G = gridDim.x;
   const int32_t xcd = blockIdx.x & 7, per = G >> 3, rem = G & 7;
   const int32_t vb = xcd * per + min(xcd, rem) + (blockIdx.x >> 3);
@@ -1963,7 +1969,7 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_s16(ConvMfmaArgs a)
   auto unit_of = [&](int32_t i) { return u0 + wave + kWaves16 * i; };
   // byte offset of this lane's operand (pixel of unit u, channel half kg % 2)
   auto pixel_off = [&](int32_t u) -> int32_t {
-    int32_t gp = (u >> 1) * 16 + col;
+    int32_t gp = (u >> hsh) * 16 + col;
     if (gp >= NP) gp = 0;
     const int32_t im = (int32_t)fdiv((uint32_t)gp, a.div_pq), rp = gp - im * PQ;
     const int32_t po = (int32_t)fdiv((uint32_t)rp, a.div_q), qo = rp - po * Qo;
@@ -2009,8 +2015,8 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_s16(ConvMfmaArgs a)
     for (int32_t unit = 0; unit < my_units; ++unit) {
       const int32_t u = unit_of(unit);
       const int32_t next_pix = unit + 1 < my_units ? pixel_off(unit_of(unit + 1)) : cur_pix;
-      const int32_t sub = u & 1;
-      const int32_t g = (u >> 1) * 16 + col;
+      const int32_t sub = u & hsh;
+      const int32_t g = (u >> hsh) * 16 + col;
       const bool gvalid = g < NP;
       int32_t obase = 0;
       if (gvalid) {
