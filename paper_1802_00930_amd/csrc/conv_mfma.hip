@@ -2458,11 +2458,12 @@ inline int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
 }  // namespace
 
 // The 16 x 16-tile kernel serves FP32 outputs at L = 64 without partials
-// when the 32 x 32 tiles are fewer than the chip's wave slots (16 per CU) and
-// every phase (whole chunks, at most kS16MaxKB blocks, as equal as possible)
-// has an even number of chunks.
-static bool use_s16(int64_t NP, int32_t Mp, int32_t KB, bool partials, int cus) {
-  if (partials || 2 * ((NP + 31) / 32) * (Mp / kMT) >= (int64_t)cus * kWaves16) return false;
+// when the 32 x 32 tiles are fewer than the chip's wave slots (16 per CU), or
+// the output has at most 16 rows (a 16-row subtile then wastes half as many
+// rows as a 32-row half), and every phase (whole chunks, at most kS16MaxKB
+// blocks, as equal as possible) has an even number of chunks.
+static bool use_s16(int64_t NP, int32_t M, int32_t Mp, int32_t KB, bool partials, int cus) {
+  if (partials || (M > 16 && 2 * ((NP + 31) / 32) * (Mp / kMT) >= (int64_t)cus * kWaves16)) return false;
   const int32_t chunks = KB / 2, nph = (KB + kS16MaxKB - 1) / kS16MaxKB;
   for (int32_t ph = 0; ph < nph; ++ph) {
     const int32_t n = chunks * (ph + 1) / nph - chunks * ph / nph;
@@ -2538,8 +2539,8 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
     // kernel where that one runs)
     const int cus = device_cus();
     const int64_t NP = (int64_t)g.n * p.Po * p.Qo;
-    if (use_s16(NP, p.Mp, p.KB, partials != nullptr, cus)) {
-      const int64_t gx = std::max<int64_t>(1, cus / (p.Mp / kS16Rows));
+    if (use_s16(NP, p.M, p.Mp, p.KB, partials != nullptr, cus)) {
+      const int64_t gx = std::max<int64_t>(1, cus / ((p.M + kS16Rows - 1) / kS16Rows));
       plane = 2 * ((NP + 15) / 16) >= gx * kWaves16 || p.KB <= kS16MaxKB;
     } else {
       const int64_t gx = std::max<int64_t>(1, cus / (p.Mp / kMT));
@@ -2753,8 +2754,9 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     const int32_t nph = (args.KB + kW16MaxKB - 1) / kW16MaxKB;
     const int cus = device_cus();
     const int64_t mtiles = args.Mp / kMT;
-    if (use_s16(args.NP, args.Mp, args.KB, partials, cus)) {
-      const int64_t units16 = 2 * ((args.NP + 15) / 16), stiles = args.Mp / kS16Rows;
+    if (use_s16(args.NP, args.M, args.Mp, args.KB, partials, cus)) {
+      // 32-row filter slices up to the last output row
+      const int64_t units16 = 2 * ((args.NP + 15) / 16), stiles = (args.M + kS16Rows - 1) / kS16Rows;
       const int32_t nph16 = (args.KB + kS16MaxKB - 1) / kS16MaxKB;
       int64_t gx = std::max<int64_t>(1, cus / stiles);
       gx = std::min<int64_t>(gx, (units16 + kWaves16 - 1) / kWaves16);
