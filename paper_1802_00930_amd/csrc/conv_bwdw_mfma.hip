@@ -1593,8 +1593,11 @@ struct FlatRaw {
   v4i sel;
 };
 
-template <int HALO>
-__global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_flat(BwdwArgs a) {
+// PARTIALS (test and verification runs): the same kernel also stores every
+// chunk partial, built for two waves per SIMD (the partial stores need more
+// than 128 VGPRs).
+template <int HALO, bool PARTIALS = false>
+__global__ __launch_bounds__(kThreadsW8, PARTIALS ? 2 : 4) void k_bwdw_flat(BwdwArgs a) {
   using F = FlatGeo<HALO>;
   const BwdwTile tl = bwdw_tile(a);
   if (tl.seg >= a.nseg) return;
@@ -1740,7 +1743,7 @@ __global__ __launch_bounds__(kThreadsW8, 4) void k_bwdw_flat(BwdwArgs a) {
       read_block(R0, IC<1 - CUR>{}, IC<0>{});
     }
     mfma_tile(acc, R1.ah, R1.al, operand_hi(R1), operand_lo(R1), false);
-    flush_tile<false>(acc, sum, j0 + 2 * b + CH, nullptr, a.O, colc, CRS, mrow, a.K, cvalid);
+    flush_tile<PARTIALS>(acc, sum, j0 + 2 * b + CH, a.partials, a.O, colc, CRS, mrow, a.K, cvalid);
   };
   auto do_band = [&](auto curc, int32_t b) __attribute__((always_inline)) {
     const int32_t nch = min(2, (NB - 4 * b) >> 1);
@@ -1850,7 +1853,7 @@ dim3 bwdw_grid(BwdwArgs& args, const BwdwPlan& p) {
 #define DFP_ASM_UNSAFE_BAND_PARTIALS 0
 #endif
 struct BandKernelsSafe {
-  bool w8, w8_t, skew_t, skew_f, band_t, band_f, w8_r4, w8_big, flat;
+  bool w8, w8_t, skew_t, skew_f, band_t, band_f, w8_r4, w8_big, flat, flat_t;
 };
 static const BandKernelsSafe& band_kernels_safe() {
   static const BandKernelsSafe safe{
@@ -1867,7 +1870,12 @@ static const BandKernelsSafe& band_kernels_safe() {
           no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<32>)) &&
           no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<64>)) &&
           no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<128>)) &&
-          no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<240>))};
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<240>)),
+      !DFP_ASM_UNSAFE_BAND_FLAT && no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<16, true>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<32, true>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<64, true>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<128, true>)) &&
+          no_scratch(reinterpret_cast<const void*>(&k_bwdw_flat<240, true>))};
   return safe;
 }
 
@@ -2079,7 +2087,7 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
   const BandLayout bl = band_layout(g, p);
   // the band kernels address both digit tensors with 32-bit buffer offsets
   const BandKernelsSafe& safe = band_kernels_safe();
-  if (flat_geom(g) && !partials && safe.flat && p.ad_bytes < (1ll << 31) &&
+  if (flat_geom(g) && (partials ? safe.flat_t : safe.flat) && p.ad_bytes < (1ll << 31) &&
       flat_layout(g).bytes < (1ll << 31) && (int64_t)g.k * g.c * 9 * 4 < (1ll << 32)) {
     // 3x3 same-padding layers: the flat-band kernel (also where the band
     // kernels' runs apply: it takes no per-band run table and reads every
@@ -2100,6 +2108,7 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.eb = sdy;
     args.out = dw;
     args.useg = useg;
+    args.partials = partials;
     args.T = p.T;
     args.O = (int64_t)g.k * g.c * 9;
     args.K = g.k; args.Mp = p.Mp; args.C = g.c; args.R = 3; args.S = 3;
@@ -2110,13 +2119,19 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.flat_plane = fl.plane;
     args.flat_tab = (uint32_t)fl.tab;
     const dim3 grid = bwdw_grid(args, p);
+#define DFP_FLAT(H)                                                                                  \
+  do {                                                                                               \
+    if (partials) DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_flat<H, true>), grid, dim3(kThreadsW8), 0, st, args); \
+    else DFP_LAUNCH(K_BWDW_MFMA, (k_bwdw_flat<H, false>), grid, dim3(kThreadsW8), 0, st, args);         \
+  } while (0)
     switch (fl.halo) {
-      case 16: DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat<16>, grid, dim3(kThreadsW8), 0, st, args); break;
-      case 32: DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat<32>, grid, dim3(kThreadsW8), 0, st, args); break;
-      case 64: DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat<64>, grid, dim3(kThreadsW8), 0, st, args); break;
-      case 128: DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat<128>, grid, dim3(kThreadsW8), 0, st, args); break;
-      default: DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_flat<240>, grid, dim3(kThreadsW8), 0, st, args); break;
+      case 16: DFP_FLAT(16); break;
+      case 32: DFP_FLAT(32); break;
+      case 64: DFP_FLAT(64); break;
+      case 128: DFP_FLAT(128); break;
+      default: DFP_FLAT(240); break;
     }
+#undef DFP_FLAT
     if (p.nseg > 1)
       DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 63) / 64)), dim3(64), 0, st, useg, dw,
                  args.O, p.nseg, sx, sdy);

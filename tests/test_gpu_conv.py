@@ -189,7 +189,8 @@ def test_bwd_wt_band_runs_of_4(shape, G):
 
 # 3x3 layers with unit stride and one pixel of padding on images narrower
 # than 16 whose output width is not a multiple of 4 (ResNet-50's 14 x 14 and
-# 7 x 7 layers): without partials at L = 64 the flat-band kernel takes the
+# 7 x 7 layers): at L = 64 the flat-band kernel (with partials its
+# two-waves-per-SIMD build, which also stores every chunk partial) takes the
 # backward-weights (windows over t-ordered input planes, selector-masked at
 # image edges).  Ragged column tiles (C*9 not a multiple of 128), fewer than
 # 16 channels, ragged dy row tiles, one-column images, width 15 (the widest
@@ -207,10 +208,11 @@ FLAT_SHAPES = [
 
 @pytest.mark.parametrize("shape", FLAT_SHAPES)
 @pytest.mark.parametrize("G", [0, 1, 3, 10 ** 6])
-def test_bwd_wt_flat_band(shape, G):
+@pytest.mark.parametrize("partials", [False, True])
+def test_bwd_wt_flat_band(shape, G, partials):
     n, c, h, w, k, r, s, st, pd = shape
     assert (w % 4) != 0 and w < 16 and (n * h * w) % 64 == 0
-    run_all(shape, 64, G=G, partials=False)
+    run_all(shape, 64, G=G, partials=partials)
 
 
 # Strided backward-data without partials at L = 64 with K a multiple of 64:
