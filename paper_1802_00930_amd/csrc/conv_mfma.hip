@@ -1692,6 +1692,7 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   __shared__ __align__(16) uint8_t sA[kW16MaxKB * kStageA];
   __shared__ __align__(8) int32_t s_boff[kW16MaxKB];
   __shared__ uint32_t red[kWaves16];
+  __shared__ int32_t s_next;  // the first unit of the range no wave has taken yet
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int half = lane >> 5;
@@ -1742,6 +1743,7 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
   const int32_t u0 = (int32_t)((int64_t)units * vb / G), u1 = (int32_t)((int64_t)units * (vb + 1) / G);
   const int32_t my_units = (u1 - u0 > wave) ? (u1 - u0 - wave + kWaves16 - 1) / kWaves16 : 0;
   auto unit_of = [&](int32_t i) { return u0 + wave + kWaves16 * i; };
+  if (threadIdx.x == 0) s_next = u0 + kWaves16;
   // byte offset of this lane's operand for the pixel of unit u (block offsets come from s_boff)
   auto pixel_off = [&](int32_t u) -> int32_t {
     int32_t gp = (u >> hsh) * 32 + col;
@@ -1788,9 +1790,13 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
 
   if (my_units > 0) {
     const uint32_t ra_hi = swz(col, 2 * half) * 16, ra_lo = swz(col, 2 * half + 1) * 16;
-    for (int32_t unit = 0; unit < my_units; ++unit) {
-      const int32_t u = unit_of(unit);
-      const int32_t next_pix = unit + 1 < my_units ? pixel_off(unit_of(unit + 1)) : cur_pix;
+    // wave w starts with unit w of the range and then takes the next free
+    // one (a wave that runs faster takes more units)
+    for (int32_t u = unit_of(0); u < u1;) {
+      int32_t nu = 0;
+      if (lane == 0) nu = atomicAdd(&s_next, 1);
+      nu = __builtin_amdgcn_readfirstlane(nu);
+      const int32_t next_pix = nu < u1 ? pixel_off(nu) : cur_pix;
       const int32_t msub = u & hsh;
       const int32_t g = (u >> hsh) * 32 + col;
       const bool gvalid = g < NP;
@@ -1877,6 +1883,7 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
         }
       }
       cur_pix = next_pix;
+      u = nu;
     }
   }
 
