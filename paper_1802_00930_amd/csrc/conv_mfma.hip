@@ -1674,9 +1674,10 @@ __global__ __launch_bounds__(kThreads3, 1) void k_conv_mfma_persist(ConvMfmaArgs
 // 64-row tile keeps the tile's filter digits resident in LDS.  The work is a
 // list of units (32-pixel tile, 32-row half), u = 2 * tile + half; workgroup
 // b takes a contiguous range of units (ranges of one XCD adjacent, so its L2
-// holds the input rows the range touches) and wave w of it takes units w,
-// w + 16, ... of the range, so consecutive units run on different SIMDs and
-// every SIMD gets the same number of units to within one.  Each lane loads its
+// holds the input rows the range touches); wave w of it starts with unit w
+// of the range and then takes the next unit no wave has taken (a counter in
+// LDS), so a wave that the issue arbitration favours takes more units and
+// the SIMDs finish close together.  Each lane loads its
 // B operand (16 channels x hi / lo digits of its pixel) straight into
 // registers, one chunk ahead, from the plane layout of the digit tensor, where
 // the 32 lanes of a channel half read 512 consecutive bytes; the A
