@@ -540,7 +540,15 @@ __device__ __forceinline__ int swz(int row, int piece) { return row * 4 + (piece
 // reads its 32 x 32 tile's operands from LDS.  The loads of band b + 1 are in
 // flight while band b is multiplied (two LDS buffers, one barrier per band).
 // A piece lies in one image (P*Q a multiple of PIECE); rows past K or C and
-// indices past T are zeros.  Chunks, segments and output as in k_bwdw_1x1.
+// indices past T are zeros.  The loads are buffer loads: per band one offset
+// per lane and operand (one division), the row step of the thread's pieces in
+// the scalar offset, and rows past K or C or indices past T at an offset past
+// the end of the tensor, which reads zeros (both tensors below 2 GiB: checked
+// by the launcher).  Chunks, segments and output as in k_bwdw_1x1.
+// Raw buffer resource over [p, p + bytes) (offsets past the end read zeros).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
 template <int PIECE>
 __global__ __launch_bounds__(k1x1Threads, 4) void k_bwdw_1x1s(BwdwArgs a, Raw1x1 raw) {
   constexpr int kLoads = 64 * 64 / PIECE / k1x1Threads;  // pieces per thread and operand per band
@@ -560,21 +568,34 @@ __global__ __launch_bounds__(k1x1Threads, 4) void k_bwdw_1x1s(BwdwArgs a, Raw1x1
   // piece i = j * 256 + thread of the band starting at block kb: row i / kPerRow,
   // indices PIECE (i % kPerRow) .. of the band; i % kPerRow is the same for
   // every j (256 is a multiple of kPerRow), so a thread's pieces share one
-  // index range and one image (element offsets below 2^31: checked by the launcher)
+  // index range and one image, and piece j lies j * (256 / kPerRow) rows after
+  // piece 0
   const int32_t pj = (int32_t)threadIdx.x % kPerRow, row0 = (int32_t)threadIdx.x / kPerRow;
+  const __amdgpu_buffer_rsrc_t rs_dy = make_rsrc(raw.dy, (uint32_t)(a.T * a.K * 2));
+  const __amdgpu_buffer_rsrc_t rs_x = make_rsrc(raw.x, (uint32_t)(a.T * a.C * 2));
+  const int32_t KPQ = a.K * PQ, CPQ = a.C * PQ;
+  const int32_t rowA = (rA0 + row0) * PQ, rowB = (rB0 + row0) * PQ;
+  const uint32_t jstep = (uint32_t)(k1x1Threads / kPerRow) * (uint32_t)PQ * 2u;
+  constexpr uint32_t kOut = 0x80000000u;  // past the end of either tensor
   auto load_band = [&](int64_t kb) {
     const int32_t t = (int32_t)(kb * 32) + PIECE * pj;
     const bool tin = t < (int32_t)a.T;
     const int32_t n = (int32_t)fdiv((uint32_t)(tin ? t : 0), a.div_q), pq = t - n * PQ;
+    const uint32_t oa0 = tin ? (uint32_t)(n * KPQ + rowA + pq) * 2u : kOut;
+    const uint32_t ob0 = tin ? (uint32_t)(n * CPQ + rowB + pq) * 2u : kOut;
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
       const int32_t row = j * (k1x1Threads / kPerRow) + row0;
-      ra[j] = vraw{};
-      rb[j] = vraw{};
-      if (tin && rA0 + row < a.K)
-        ra[j] = *reinterpret_cast<const vraw*>(raw.dy + (uint32_t)((n * a.K + rA0 + row) * PQ + pq));
-      if (tin && rB0 + row < a.C)
-        rb[j] = *reinterpret_cast<const vraw*>(raw.x + (uint32_t)((n * a.C + rB0 + row) * PQ + pq));
+      const uint32_t oa = rA0 + row < a.K ? oa0 : kOut;
+      const uint32_t ob = rB0 + row < a.C ? ob0 : kOut;
+      const uint32_t so = __builtin_amdgcn_readfirstlane((uint32_t)j * jstep);
+      if constexpr (PIECE == 8) {
+        ra[j] = __builtin_bit_cast(vraw, __builtin_amdgcn_raw_buffer_load_b128(rs_dy, oa, so, 0));
+        rb[j] = __builtin_bit_cast(vraw, __builtin_amdgcn_raw_buffer_load_b128(rs_x, ob, so, 0));
+      } else {
+        ra[j] = __builtin_bit_cast(vraw, __builtin_amdgcn_raw_buffer_load_b64(rs_dy, oa, so, 0));
+        rb[j] = __builtin_bit_cast(vraw, __builtin_amdgcn_raw_buffer_load_b64(rs_x, ob, so, 0));
+      }
     }
   };
   // digits of the staged pieces into buffer buf
@@ -670,10 +691,6 @@ constexpr int kBandLdsBytes = 76 * 1024;             // two buffers; two workgro
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-// Raw buffer resource over [p, p + bytes) (offsets past the end read zeros).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
-}
 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint8_t*)p;
@@ -2053,9 +2070,11 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     const int32_t Cp = (g.c + 63) / 64 * 64;
     uint8_t* bd = reinterpret_cast<uint8_t*>(xp);
     const int32_t PQ = g.p * g.q;
-    // P*Q a multiple of 4: the INT16 tensors are read directly (staged through LDS)
+    // P*Q a multiple of 4: the INT16 tensors are read directly (staged through
+    // LDS, buffer loads over tensors below 2 GiB)
     const bool direct = PQ % 4 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
-                        (reinterpret_cast<uintptr_t>(dy) & 15) == 0;
+                        (reinterpret_cast<uintptr_t>(dy) & 15) == 0 &&
+                        p.T * std::max(g.c, g.k) * 2 < (1ll << 31);
     if (!direct) {
       const DyPrep dqx{x, bd, g.c, Cp, PQ, (int32_t)p.T, (int32_t)p.KBT};
       DFP_LAUNCH(K_WPREP, k_prep_dy, dim3((unsigned)dy_blocks), dim3(256), 0, st, dq);
