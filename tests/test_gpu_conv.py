@@ -269,9 +269,10 @@ def test_w16_shapes(shape, partials):
 
 # Fewer 32 x 32 output tiles than the chip's wave slots, every phase an even
 # number of chunks, no partials: the 16 x 16-tile kernel (ResNet-50's 14 x 14
-# and 7 x 7 layers): one to three phases of up to 72 blocks, ragged pixel
-# tiles, output channels not a multiple of 64, stride 2 (backward-data of that
-# shape reads a dilated plane), 1 x 1 with two and four chunks.
+# and 7 x 7 layers): one to six phases of up to 72 blocks (reductions of 144,
+# 216 and 432 blocks), ragged pixel tiles, output channels not a multiple of
+# 64 (nor of 16), stride 2 (backward-data of that shape reads a dilated
+# plane), 1 x 1 with two and four chunks.
 S16_SHAPES = [
     (2, 256, 14, 14, 64, 3, 3, 1, 1),
     (1, 768, 5, 5, 64, 3, 3, 1, 1),
@@ -280,6 +281,8 @@ S16_SHAPES = [
     (2, 128, 10, 10, 64, 3, 3, 2, 1),
     (2, 128, 8, 8, 256, 1, 1, 1, 0),
     (4, 256, 7, 7, 512, 3, 3, 1, 1),
+    (1, 512, 6, 6, 40, 3, 3, 1, 1),
+    (1, 1536, 3, 3, 48, 3, 3, 1, 1),
 ]
 
 
