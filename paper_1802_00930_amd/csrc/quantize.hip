@@ -184,16 +184,17 @@ __global__ __launch_bounds__(kBlock) void k_quant_convert(const float* __restric
 }
 
 // Whole quantisation of a small tensor in one launch (P = 15, so no workgroup
-// raises a saturation flag): every workgroup reduces the max of the whole
-// tensor (it is at most kSmallQuantElems elements, read from L2 by all but the
-// first), derives the scale, and rounds its own contiguous share of the
-// groups of four with the same per-group Philox counters as k_quant_convert.
-// Workgroup 0 writes the scale.
+// raises a saturation flag).  Group g (elements 4g .. 4g + 3) is group
+// g mod 1024 of slice g / 1024; workgroup b rounds slice b, one group per
+// thread.  Every workgroup loads the whole tensor (at most kSmallQuantElems
+// elements, 16 slices; read from L2 by all but the first), thread i slice k's
+// group i into register k, and its own group once more, all loads in flight
+// at once; it reduces the max, derives the scale and rounds its group, with
+// the same per-group Philox counters as k_quant_convert.  Workgroup 0 writes
+// the scale.
 constexpr int64_t kSmallQuantElems = 65536;
-constexpr int kSmallQuantBlocks = 16;
-
 constexpr int kSmallThreads = 1024;
-constexpr int kSmallUnroll = 8;
+constexpr int kSmallSlices = (int)(kSmallQuantElems / 4 / kSmallThreads);  // 16
 
 template <int MODE>
 __global__ __launch_bounds__(kSmallThreads) void k_quant_small(const float* __restrict__ src,
@@ -202,49 +203,59 @@ __global__ __launch_bounds__(kSmallThreads) void k_quant_small(const float* __re
                                                                uint32_t key0, uint32_t key1, uint32_t role) {
   __shared__ uint32_t red[kSmallThreads / 64];
   const uint4* src4 = reinterpret_cast<const uint4*>(src);
-  const int32_t n4 = (int32_t)(n >> 2);
-  uint32_t mm = 0u;
-  // up to kSmallUnroll loads per lane in flight per step (a 64 Ki-element tensor is two steps)
-  for (int32_t base = threadIdx.x; base < n4; base += kSmallUnroll * kSmallThreads) {
-    uint4 v[kSmallUnroll];
-#pragma unroll
-    for (int k = 0; k < kSmallUnroll; ++k) v[k] = src4[min(base + k * kSmallThreads, n4 - 1)];
-#pragma unroll
-    for (int k = 0; k < kSmallUnroll; ++k) mm = max(mm, abs_max4(v[k]));
-  }
   const uint32_t* s1 = reinterpret_cast<const uint32_t*>(src);
-  for (int32_t t = 4 * n4 + threadIdx.x; t < (int32_t)n; t += kSmallThreads) mm = max(mm, s1[t] & 0x7fffffffu);
+  const int32_t n4 = (int32_t)(n >> 2);
+  const int32_t groups = (int32_t)((n + 3) >> 2);
+  const int32_t nsl = (groups + kSmallThreads - 1) / kSmallThreads;  // slices, one per workgroup
+  const int32_t tid = (int32_t)threadIdx.x;
+  const int32_t g = (int32_t)blockIdx.x * kSmallThreads + tid;  // the group this thread rounds
+  // its own group, requested with the others (a second request for one of
+  // them, in flight at the same time); every load is issued (an index past the
+  // whole groups re-reads the last one: the max is unchanged), so that none
+  // waits for another
+  uint4 w4 = make_uint4(0u, 0u, 0u, 0u);
+  uint4 v[kSmallSlices];
+#pragma unroll
+  for (int k = 0; k < kSmallSlices; ++k) v[k] = make_uint4(0u, 0u, 0u, 0u);
+  if (n4 > 0) {
+    w4 = src4[min(g, n4 - 1)];
+#pragma unroll
+    for (int k = 0; k < kSmallSlices; ++k) v[k] = src4[min(k * kSmallThreads + tid, n4 - 1)];
+  }
+  // the partial last group (n not a multiple of 4), from single elements
+  uint4 vp = make_uint4(0u, 0u, 0u, 0u);
+  if (n4 < groups && (n4 & (kSmallThreads - 1)) == tid) {
+    const int64_t base = (int64_t)n4 << 2;
+    vp.x = s1[base];
+    if (base + 1 < n) vp.y = s1[base + 1];
+    if (base + 2 < n) vp.z = s1[base + 2];
+  }
+  uint32_t mm = abs_max4(vp);
+#pragma unroll
+  for (int k = 0; k < kSmallSlices; ++k) mm = max(mm, abs_max4(v[k]));
   mm = wave_max(mm);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mm;
+  if ((tid & 63) == 0) red[tid >> 6] = mm;
   __syncthreads();
   mm = red[0];
 #pragma unroll
   for (int i = 1; i < kSmallThreads / 64; ++i) mm = max(mm, red[i]);
   const ScaleFromMax sc = scale_from_max(mm, bits);
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+  if (blockIdx.x == 0 && tid == 0) {
     s->amax_bits = mm;
     s->exp = sc.es;
     s->flags = sc.flags;
   }
-  const int32_t groups = (int32_t)((n + 3) >> 2);
-  const int32_t lo = groups * (int32_t)blockIdx.x / (int32_t)gridDim.x;
-  const int32_t hi = groups * ((int32_t)blockIdx.x + 1) / (int32_t)gridDim.x;
-  uint2* dst4 = reinterpret_cast<uint2*>(dst);
+  if (g >= groups) return;
+  const uint4 w = g < n4 ? w4 : vp;  // g == n4: the partial group
   bool saturated = false;
-  for (int32_t g = lo + threadIdx.x; g < hi; g += kSmallThreads) {
-    if (g < n4) {
-      dst4[g] = quant_group<MODE, false>(src4[g], g, sc.es, sc.all_zero, key0, key1, role, saturated);
-    } else {  // the last, partial group
-      const int64_t base = (int64_t)g << 2;
-      uint4 v = make_uint4(0u, 0u, 0u, 0u);
-      v.x = s1[base];
-      if (base + 1 < n) v.y = s1[base + 1];
-      if (base + 2 < n) v.z = s1[base + 2];
-      const uint2 packed = quant_group<MODE, false>(v, g, sc.es, sc.all_zero, key0, key1, role, saturated);
-      dst[base] = (int16_t)(packed.x & 0xffffu);
-      if (base + 1 < n) dst[base + 1] = (int16_t)(packed.x >> 16);
-      if (base + 2 < n) dst[base + 2] = (int16_t)(packed.y & 0xffffu);
-    }
+  const uint2 packed = quant_group<MODE, false>(w, g, sc.es, sc.all_zero, key0, key1, role, saturated);
+  if (g < n4) {
+    reinterpret_cast<uint2*>(dst)[g] = packed;
+  } else {  // the last, partial group
+    const int64_t base = (int64_t)g << 2;
+    dst[base] = (int16_t)(packed.x & 0xffffu);
+    if (base + 1 < n) dst[base + 1] = (int16_t)(packed.x >> 16);
+    if (base + 2 < n) dst[base + 2] = (int16_t)(packed.y & 0xffffu);
   }
 }
 
@@ -608,8 +619,7 @@ static dfp_status launch_qc_mode(const float* src, int16_t* dst, int64_t n, dfp_
 template <int MODE>
 static dfp_status launch_small_mode(const float* src, int16_t* dst, int64_t n, dfp_scale* s, int32_t bits,
                                     uint32_t k0, uint32_t k1, uint32_t role, hipStream_t st) {
-  const int64_t blocks =
-      std::min<int64_t>(kSmallQuantBlocks, std::max<int64_t>(1, (n + 4 * kSmallThreads - 1) / (4 * kSmallThreads)));
+  const int64_t blocks = std::max<int64_t>(1, ((n + 3) / 4 + kSmallThreads - 1) / kSmallThreads);  // slices
   DFP_LAUNCH(K_QUANT, k_quant_small<MODE>, dim3((unsigned)blocks), dim3(kSmallThreads), 0, st, src, dst, n, s, bits,
              k0, k1, role);
   return DFP_OK;
