@@ -1914,14 +1914,19 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_w16(ConvMfmaArgs a)
 // 16 x 16).  Same plane-layout operands and unit ranges as the 32 x 32
 // kernel, but a workgroup keeps a 32-row filter slice in LDS, so a phase
 // holds up to 72 blocks (a ResNet-50 14 x 14 3 x 3 layer in one phase, a
-// 7 x 7 one in two); a unit is (16-pixel tile, 16-row subtile),
-// u = 2 * tile + sub.  Lane l multiplies pixel l % 16 of the tile (B) and row
-// l % 16 of the subtile (A) over the chunk's indices 16 (l / 16) .. + 15,
-// that is channel half (l / 16) % 2 of block 2 c + l / 32; it accumulates
-// rows 4 (l / 16) .. + 3 of the tile at pixel l % 16.  The B registers of
-// chunk c + 2 are loaded as soon as chunk c's MFMAs have issued (two
-// register sets, chunks taken in pairs: every phase has an even number of
-// chunks).  FP32 outputs only (no partials, no single-chunk INT32 mode).
+// 7 x 7 one in two); a unit is a 16-pixel tile, whose B operand a wave loads
+// once per chunk and multiplies with both 16-row subtiles of the slice (only
+// the first where the second lies past the output rows).  Lane l multiplies
+// pixel l % 16 of the tile (B) and row l % 16 of each subtile (A) over the
+// chunk's indices 16 (l / 16) .. + 15, that is channel half (l / 16) % 2 of
+// block 2 c + l / 32; it accumulates rows 4 (l / 16) .. + 3 of each subtile
+// at pixel l % 16.  The B registers of chunk c + 2 are loaded as soon as
+// chunk c's MFMAs have issued (two register sets, chunks taken in pairs:
+// every phase has an even number of chunks).  FP32 outputs only (no
+// partials, no single-chunk INT32 mode).  Against units of one subtile each
+// (twice as many, each loading B): ResNet-50 res4 3 x 3 forward 47.8 ->
+// 43.4 us, backward-data 50.6 -> 43.3 us; res5 65 -> 57 us with one
+// workgroup per CU although some waves then get no tile.
 constexpr int32_t kS16Rows = 32;                   // filter rows per workgroup
 constexpr int32_t kS16Block = kS16Rows * 64;        // LDS bytes of one filter block
 constexpr int32_t kS16MaxKB = kW16MaxKB * kStageA / kS16Block;  // 72
@@ -1965,10 +1970,10 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_s16(ConvMfmaArgs a)
   if ((int32_t)threadIdx.x < KB) s_boff[threadIdx.x] = boff_of(kb0 + (int32_t)threadIdx.x);
 
   // ---- this workgroup's unit range (XCD x = workgroup id mod 8 gets adjacent ranges)
-  // units (16-pixel tile, 16-row subtile); only the first subtile where the
-  // second lies past the output rows (M - m0 <= 16)
-  const int32_t hsh = a.M - m0 > 16 ? 1 : 0;
-  const int32_t units = ((NP + 15) / 16) << hsh;
+  // units: 16-pixel tiles; both 16-row subtiles of the slice, or only the
+  // first where the second lies past the output rows (M - m0 <= 16)
+  const bool two_sub = a.M - m0 > 16;
+  const int32_t units = (NP + 15) / 16;
   const int32_t G = gridDim.x;
   const int32_t xcd = blockIdx.x & 7, per = G >> 3, rem = G & 7;
   const int32_t vb = xcd * per + min(xcd, rem) + (blockIdx.x >> 3);
@@ -1977,7 +1982,7 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_s16(ConvMfmaArgs a)
   auto unit_of = [&](int32_t i) { return u0 + wave + kWaves16 * i; };
   // byte offset of this lane's operand (pixel of unit u, channel half kg % 2)
   auto pixel_off = [&](int32_t u) -> int32_t {
-    int32_t gp = (u >> hsh) * 16 + col;
+    int32_t gp = u * 16 + col;
     if (gp >= NP) gp = 0;
     const int32_t im = (int32_t)fdiv((uint32_t)gp, a.div_pq), rp = gp - im * PQ;
     const int32_t po = (int32_t)fdiv((uint32_t)rp, a.div_q), qo = rp - po * Qo;
@@ -2016,80 +2021,105 @@ __global__ __launch_bounds__(kThreads16, 1) void k_conv_mfma_s16(ConvMfmaArgs a)
   }
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
-  if (my_units > 0) {
+  // The units of NSUB subtiles (rows m0 + 16 sub + 4 (l / 16) .. + 3 at
+  // pixel l % 16 of the tile): the tile's B operand is loaded once per chunk
+  // and multiplied with each subtile's filter rows.
+  auto run_units = [&](auto nsub_c) __attribute__((always_inline)) {
+    constexpr int NSUB = decltype(nsub_c)::value;
     // A: row col of the subtile, channel half kg % 2 of block kg / 2 (hi, lo pieces)
     const uint32_t ra_hi = swz(col, 2 * (kg & 1)) * 16 + (kg >> 1) * kS16Block;
     const uint32_t ra_lo = swz(col, 2 * (kg & 1) + 1) * 16 + (kg >> 1) * kS16Block;
     for (int32_t unit = 0; unit < my_units; ++unit) {
       const int32_t u = unit_of(unit);
       const int32_t next_pix = unit + 1 < my_units ? pixel_off(unit_of(unit + 1)) : cur_pix;
-      const int32_t sub = u & hsh;
-      const int32_t g = (u >> hsh) * 16 + col;
+      const int32_t g = u * 16 + col;
       const bool gvalid = g < NP;
       int32_t obase = 0;
       if (gvalid) {
         const int32_t im = (int32_t)fdiv((uint32_t)g, a.div_pq);
         obase = im * a.M * PQ + (g - im * PQ);
       }
-      const int32_t mrow0 = m0 + 16 * sub + 4 * kg;
-      v4i hh, xx, ll;
-      float sum[4] = {0.f, 0.f, 0.f, 0.f};
+      const int32_t mrow0 = m0 + 4 * kg;  // row of value v of subtile sub: mrow0 + 16 sub + v
+      v4i hh[NSUB], xx[NSUB], ll[NSUB];
+      float sum[NSUB][4];
+#pragma unroll
+      for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sum[sb][v] = 0.f;
       if (PHASED && !first_phase && gvalid) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int32_t m = mrow0 + v;
-          if (m < a.M) sum[v] = a.out[(uint32_t)(obase + m * PQ)];
-        }
+        for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int32_t m = mrow0 + 16 * sb + v;
+            if (m < a.M) sum[sb][v] = a.out[(uint32_t)(obase + m * PQ)];
+          }
       }
-      const uint8_t* ab = sA + sub * 1024;
       auto chunk = [&](int32_t c, v4i& bh, v4i& bl) __attribute__((always_inline)) {
-        const v4i ah = *reinterpret_cast<const v4i*>(ab + c * 2 * kS16Block + ra_hi);
-        const v4i al = *reinterpret_cast<const v4i*>(ab + c * 2 * kS16Block + ra_lo);
+        const uint8_t* ab = sA + c * 2 * kS16Block;
         const v4i z = {0, 0, 0, 0};
-        hh = __builtin_amdgcn_mfma_i32_16x16x64_i8(ah, bh, z, 0, 0, 0);
-        ll = __builtin_amdgcn_mfma_i32_16x16x64_i8(al, bl, z, 0, 0, 0);
-        xx = __builtin_amdgcn_mfma_i32_16x16x64_i8(ah, bl, z, 0, 0, 0);
-        xx = __builtin_amdgcn_mfma_i32_16x16x64_i8(al, bh, xx, 0, 0, 0);
+        v4i ah[NSUB], al[NSUB];
+#pragma unroll
+        for (int sb = 0; sb < NSUB; ++sb) {
+          ah[sb] = *reinterpret_cast<const v4i*>(ab + sb * 1024 + ra_hi);
+          al[sb] = *reinterpret_cast<const v4i*>(ab + sb * 1024 + ra_lo);
+        }
+#pragma unroll
+        for (int sb = 0; sb < NSUB; ++sb) {
+          hh[sb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ah[sb], bh, z, 0, 0, 0);
+          ll[sb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(al[sb], bl, z, 0, 0, 0);
+          xx[sb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ah[sb], bl, z, 0, 0, 0);
+        }
+#pragma unroll
+        for (int sb = 0; sb < NSUB; ++sb) xx[sb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(al[sb], bh, xx[sb], 0, 0, 0);
         // chunk c + 2 of this unit, or chunk c + 2 - J of the next one
         const int32_t nc = c + 2 < J ? c + 2 : c + 2 - J;
         load_b(bh, bl, c + 2 < J ? cur_pix : next_pix, boff_chunk(nc));
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const uint32_t p = recombine((uint32_t)hh[v], (uint32_t)xx[v], (uint32_t)ll[v]);
-          sum[v] += (float)(int32_t)p;
-        }
+        for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const uint32_t p = recombine((uint32_t)hh[sb][v], (uint32_t)xx[sb][v], (uint32_t)ll[sb][v]);
+            sum[sb][v] += (float)(int32_t)p;
+          }
       };
       for (int32_t c = 0; c < J; c += 2) {
         chunk(c, b0h, b0l);
         chunk(c + 1, b1h, b1l);
       }
-      if (PHASED && gvalid && !last_phase) {  // unscaled sums for the next phase
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int32_t m = mrow0 + v;
-          if (m < a.M) a.out[(uint32_t)(obase + m * PQ)] = sum[v];
-        }
-      } else if (gvalid) {
-        if (full_rows && out_buf) {
-          const uint32_t lane_off = (uint32_t)(obase + mrow0 * PQ) * 4u;
-          float fmx = 0.f;
+      for (int sb = 0; sb < NSUB; ++sb) {
+        const int32_t mr = mrow0 + 16 * sb;
+        if (PHASED && gvalid && !last_phase) {  // unscaled sums for the next phase
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            const float y = ldexpf(sum[v], e);
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(y), rs_out, lane_off, (uint32_t)(v * PQ) * 4u, 0);
-            fmx = fmaxf(fmx, fabsf(y));
+            if (mr + v < a.M) a.out[(uint32_t)(obase + (mr + v) * PQ)] = sum[sb][v];
           }
-          amax = max(amax, __float_as_uint(fmx));
-        } else {
+        } else if (gvalid) {
+          if (full_rows && out_buf) {
+            const uint32_t lane_off = (uint32_t)(obase + mr * PQ) * 4u;
+            float fmx = 0.f;
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int32_t m = mrow0 + v;
-            if (m < a.M) amax = max(amax, store_out<false>(a.out, (uint32_t)(obase + m * PQ), sum[v], e));
+            for (int v = 0; v < 4; ++v) {
+              const float y = ldexpf(sum[sb][v], e);
+              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(y), rs_out, lane_off, (uint32_t)(v * PQ) * 4u, 0);
+              fmx = fmaxf(fmx, fabsf(y));
+            }
+            amax = max(amax, __float_as_uint(fmx));
+          } else {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              if (mr + v < a.M) amax = max(amax, store_out<false>(a.out, (uint32_t)(obase + (mr + v) * PQ), sum[sb][v], e));
+            }
           }
         }
       }
       cur_pix = next_pix;
     }
+  };
+  if (my_units > 0) {
+    if (two_sub) run_units(std::integral_constant<int, 2>{});
+    else run_units(std::integral_constant<int, 1>{});
   }
 
   if (a.so && last_phase) {
@@ -2542,9 +2572,9 @@ dfp_status launch_conv_mfma(int32_t dir, const Geom& g, const int16_t* a, const 
   bool plane = conv_w16_eligible(p.Cin, p.T, g.L, i32) && (int64_t)g.n * p.Po * p.Qo * p.M < (1ll << 31) &&
                p.ws_b_bytes < (1ll << 31);
   if (plane && p.KB > kW16MaxKB && !prefer_w16) {
-    // phases pay the kernel's fixed cost once each: taken only when every wave
-    // of a workgroup has a unit of work in each phase (units of the 16 x 16
-    // kernel where that one runs)
+    // phases pay the kernel's fixed cost once each: taken only when there are
+    // at least as many 16 x 16 (32 x 32) output tiles per workgroup as it has
+    // waves, in each phase
     const int cus = device_cus();
     const int64_t NP = (int64_t)g.n * p.Po * p.Qo;
     if (use_s16(NP, p.M, p.Mp, p.KB, partials != nullptr, cus)) {
@@ -2764,10 +2794,10 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     const int64_t mtiles = args.Mp / kMT;
     if (use_s16(args.NP, args.M, args.Mp, args.KB, partials, cus)) {
       // 32-row filter slices up to the last output row
-      const int64_t units16 = 2 * ((args.NP + 15) / 16), stiles = (args.M + kS16Rows - 1) / kS16Rows;
+      // (one workgroup per CU, even where some waves get no 16-pixel tile)
+      const int64_t stiles = (args.M + kS16Rows - 1) / kS16Rows;
       const int32_t nph16 = (args.KB + kS16MaxKB - 1) / kS16MaxKB;
-      int64_t gx = std::max<int64_t>(1, cus / stiles);
-      gx = std::min<int64_t>(gx, (units16 + kWaves16 - 1) / kWaves16);
+      const int64_t gx = std::max<int64_t>(1, cus / stiles);
       const dim3 grid_s((unsigned)gx, (unsigned)stiles);
       for (int32_t ph = 0; ph < nph16; ++ph) {
         const int32_t c0 = chunks * ph / nph16, c1 = chunks * (ph + 1) / nph16;
