@@ -2794,10 +2794,11 @@ dfp_status launch_mfma_main(ConvMfmaArgs& args, int64_t ws_b_bytes, int kid, int
     const int64_t mtiles = args.Mp / kMT;
     if (use_s16(args.NP, args.M, args.Mp, args.KB, partials, cus)) {
       // 32-row filter slices up to the last output row
-      // (one workgroup per CU, even where some waves get no 16-pixel tile)
+      // (one workgroup per CU, even where some waves get no 16-pixel tile, but
+      // at least 8 tiles per workgroup: every workgroup copies its filter slice)
       const int64_t stiles = (args.M + kS16Rows - 1) / kS16Rows;
       const int32_t nph16 = (args.KB + kS16MaxKB - 1) / kS16MaxKB;
-      const int64_t gx = std::max<int64_t>(1, cus / stiles);
+      const int64_t gx = std::max<int64_t>(1, std::min<int64_t>(cus / stiles, (args.NP + 16 * 8 - 1) / (16 * 8)));
       const dim3 grid_s((unsigned)gx, (unsigned)stiles);
       for (int32_t ph = 0; ph < nph16; ++ph) {
         const int32_t c0 = chunks * ph / nph16, c1 = chunks * (ph + 1) / nph16;
