@@ -417,48 +417,15 @@ __global__ __launch_bounds__(kThreads, 2) void k_bwdw_mfma(BwdwArgs a) {
 // multiplied.  Chunks are whole blocks (L a multiple of 32) and digits past T
 // are zero, so no masking is needed.  Chunk sums and segment output as in the
 // kernels above.
-//
-// DIRECT (P*Q a multiple of 16): the 16 indices of a lane's piece lie in one
-// image, so the lane reads them as 32 contiguous bytes of the INT16 tensor
-// itself (dy[n][k][.] or x[n][c][.]) and splits the digits in registers; no
-// preparation pass.
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ void split_digits(const uint4& w0, const uint4& w1, v4i& hi, v4i& lo) {
-  const uint32_t w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-  uint32_t h[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {  // a + 128 in each 16-bit half: the hi digit is its high byte
-    const u16x2 v = __builtin_bit_cast(u16x2, w[i]) + (u16x2){128, 128};
-    h[i] = __builtin_bit_cast(uint32_t, v);
-  }
-#pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    lo[d] = (int)__builtin_amdgcn_perm(w[2 * d + 1], w[2 * d], 0x06040200u);
-    hi[d] = (int)__builtin_amdgcn_perm(h[2 * d + 1], h[2 * d], 0x07050301u);
-  }
-}
 struct Raw1x1 {
   const int16_t* dy;  // [N][K][PQ]
   const int16_t* x;   // [N][C][PQ]
   int32_t PQ;
 };
-// The lane's 16-index piece of row `row` (of `rows`) starting at t0, or zeros.
-__device__ __forceinline__ void load_raw_piece(const int16_t* base, int32_t rows, int32_t row, int64_t t0, int64_t T,
-                                               int32_t PQ, uint4& w0, uint4& w1) {
-  w0 = make_uint4(0u, 0u, 0u, 0u);
-  w1 = w0;
-  if (row < rows && t0 < T) {
-    const int64_t n = t0 / PQ, pq = t0 - n * PQ;
-    const uint4* p = reinterpret_cast<const uint4*>(base + (n * rows + row) * PQ + pq);
-    w0 = p[0];
-    w1 = p[1];
-  }
-}
 
 constexpr int k1x1Threads = 256;
-template <bool DIRECT>
-__global__ __launch_bounds__(k1x1Threads, 4) void k_bwdw_1x1(BwdwArgs a, const uint8_t* __restrict__ bd,
-                                                            int32_t Cp, Raw1x1 raw) {
+__global__ __launch_bounds__(k1x1Threads, 4) void k_bwdw_1x1(BwdwArgs a, const uint8_t* __restrict__ bd, int32_t Cp) {
   const BwdwTile tl = bwdw_tile(a);
   if (tl.seg >= a.nseg) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, lc = lane & 31;
@@ -469,42 +436,23 @@ __global__ __launch_bounds__(k1x1Threads, 4) void k_bwdw_1x1(BwdwArgs a, const u
   const int64_t kb_begin = t_seg0 / 32, kb_end = (t_seg1 + 31) / 32;
   const int32_t chunk_blocks = a.L / 32;
   const int64_t astep = (int64_t)a.Mp * 64, bstep = (int64_t)Cp * 64;
-  const uint4* ap = nullptr;
-  const uint4* bp = nullptr;
-  uint4 ah, al, bh, bl;  // digit pieces, or the raw INT16 pieces when DIRECT
-  if (DIRECT) {
-    load_raw_piece(raw.dy, a.K, m0 + lc, kb_begin * 32 + 16 * half, a.T, raw.PQ, ah, al);
-    load_raw_piece(raw.x, a.C, c0 + lc, kb_begin * 32 + 16 * half, a.T, raw.PQ, bh, bl);
-  } else {
-    ap = reinterpret_cast<const uint4*>(a.ad + kb_begin * astep + ((int64_t)(m0 + lc) * 2 + half) * 32);
-    bp = reinterpret_cast<const uint4*>(bd + kb_begin * bstep + ((int64_t)(c0 + lc) * 2 + half) * 32);
-    ah = ap[0]; al = ap[1]; bh = bp[0]; bl = bp[1];
-  }
+  const uint4* ap = reinterpret_cast<const uint4*>(a.ad + kb_begin * astep + ((int64_t)(m0 + lc) * 2 + half) * 32);
+  const uint4* bp = reinterpret_cast<const uint4*>(bd + kb_begin * bstep + ((int64_t)(c0 + lc) * 2 + half) * 32);
+  uint4 ah = ap[0], al = ap[1], bh = bp[0], bl = bp[1];  // digit pieces of the block
   Acc3 acc;
   float sum[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) sum[v] = 0.f;
   int32_t blk = 0;
   for (int64_t kb = kb_begin; kb < kb_end; ++kb) {
-    v4i ahi, alo, bhi, blo;
-    if (DIRECT) {
-      split_digits(ah, al, ahi, alo);
-      split_digits(bh, bl, bhi, blo);
-    } else {
-      ahi = (v4i){(int)ah.x, (int)ah.y, (int)ah.z, (int)ah.w};
-      alo = (v4i){(int)al.x, (int)al.y, (int)al.z, (int)al.w};
-      bhi = (v4i){(int)bh.x, (int)bh.y, (int)bh.z, (int)bh.w};
-      blo = (v4i){(int)bl.x, (int)bl.y, (int)bl.z, (int)bl.w};
-    }
+    const v4i ahi = (v4i){(int)ah.x, (int)ah.y, (int)ah.z, (int)ah.w};
+    const v4i alo = (v4i){(int)al.x, (int)al.y, (int)al.z, (int)al.w};
+    const v4i bhi = (v4i){(int)bh.x, (int)bh.y, (int)bh.z, (int)bh.w};
+    const v4i blo = (v4i){(int)bl.x, (int)bl.y, (int)bl.z, (int)bl.w};
     if (kb + 1 < kb_end) {
-      if (DIRECT) {
-        load_raw_piece(raw.dy, a.K, m0 + lc, (kb + 1) * 32 + 16 * half, a.T, raw.PQ, ah, al);
-        load_raw_piece(raw.x, a.C, c0 + lc, (kb + 1) * 32 + 16 * half, a.T, raw.PQ, bh, bl);
-      } else {
-        ap += astep / 16;
-        bp += bstep / 16;
-        ah = ap[0]; al = ap[1]; bh = bp[0]; bl = bp[1];
-      }
+      ap += astep / 16;
+      bp += bstep / 16;
+      ah = ap[0]; al = ap[1]; bh = bp[0]; bl = bp[1];
     }
     mfma_tile(acc, ahi, alo, bhi, blo, blk == 0);
     if (++blk == chunk_blocks || kb == kb_end - 1) {
@@ -2097,7 +2045,7 @@ dfp_status launch_bwdw_mfma(const Geom& g, const int16_t* x, const dfp_scale* sx
     args.div_q = make_fastdiv((uint32_t)PQ);  // the direct kernels: image of an index
     if (direct && PQ % 8 == 0) DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_1x1s<8>, grid1, dim3(k1x1Threads), 0, st, args, raw);
     else if (direct) DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_1x1s<4>, grid1, dim3(k1x1Threads), 0, st, args, raw);
-    else DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_1x1<false>, grid1, dim3(k1x1Threads), 0, st, args, bd, Cp, raw);
+    else DFP_LAUNCH(K_BWDW_MFMA, k_bwdw_1x1, grid1, dim3(k1x1Threads), 0, st, args, bd, Cp);
     if (p.nseg > 1)
       DFP_LAUNCH(K_BWDW_REDUCE, k_seg_reduce, dim3((unsigned)((args.O + 63) / 64)), dim3(64), 0, st, useg, dw,
                  args.O, p.nseg, sx, sdy);
